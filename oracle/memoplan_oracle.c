@@ -1,0 +1,282 @@
+/*
+ * memoplan_oracle.c -- plain, slow, single-threaded CPU oracle of static
+ * memory planning (greedy_by_size of Section 2.3, the planner chosen in
+ * Section 3.2 of Levental, "Memory Planning for Deep Neural Networks").
+ *
+ * TEST INFRASTRUCTURE ONLY: used by the tests, the smoke check and the CPU
+ * baseline of the benchmark, never by the product path.  No code is shared
+ * with the GPU library.
+ *
+ * Readings of the thesis fixed here (the text leaves them open):
+ *  - a lifetime is the closed op interval [first, last]; two tensors conflict
+ *    when they share at least one op;
+ *  - a tensor occupies the half-open byte range [offset, offset + size)
+ *    (Eq. 2.1: offset_i + mem_i <= offset_j is non-overlap);
+ *  - greedy_by_size sorts by size descending, ties by first op ascending, then
+ *    by id ascending;
+ *  - "fit" for the main policy is the lowest gap that fits (LOWEST_FIT); the
+ *    tightest-gap reading of "best fit" is offered as BEST_FIT;
+ *  - offsets are never rounded; the peak is max(offset + size) (total_mem of
+ *    Eq. 2.1), 0 for an empty trace.
+ */
+#include "memoplan_oracle.h"
+
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------- */
+/* Input checks (problem statement of Section 2.3: known sizes and lifetimes) */
+
+/* has_ops == 0 skips the upper bound (plan validation takes no op count). */
+static int32_t check_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                           int64_t n, int32_t num_ops, int has_ops) {
+    if (n < 0 || num_ops < 0) return MPO_EINVAL;
+    if (n > 0 && (!size || !first || !last)) return MPO_EINVAL;
+    if (n > INT32_MAX) return MPO_EINVAL;
+    int32_t status = MPO_OK;
+    uint64_t total = 0; /* saturates at UINT64_MAX */
+    for (int64_t i = 0; i < n; ++i) {
+        if (size[i] <= 0 || first[i] < 0 || first[i] > last[i] || (has_ops && last[i] >= num_ops))
+            status = MPO_EINVAL;
+        if (size[i] > 0) {
+            uint64_t s = (uint64_t)size[i];
+            total = (total > UINT64_MAX - s) ? UINT64_MAX : total + s;
+        }
+    }
+    if (total > (uint64_t)INT64_MAX) status = MPO_EOVERFLOW;
+    return status;
+}
+
+int32_t mpo_check_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                        int64_t n, int32_t num_ops) {
+    return check_trace(size, first, last, n, num_ops, 1);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Rank order: "sorting all intermediate allocations by size" (Section 2.3). */
+
+typedef struct {
+    int64_t size;
+    int32_t first;
+    int32_t id;
+} rank_key;
+
+static int cmp_rank(const void* pa, const void* pb) {
+    const rank_key* a = (const rank_key*)pa;
+    const rank_key* b = (const rank_key*)pb;
+    if (a->size != b->size) return a->size > b->size ? -1 : 1; /* larger first */
+    if (a->first != b->first) return a->first < b->first ? -1 : 1;
+    if (a->id != b->id) return a->id < b->id ? -1 : 1;
+    return 0;
+}
+
+int32_t mpo_rank_order(const int64_t* size, const int32_t* first, int64_t n, int32_t* order_out) {
+    if (n < 0 || n > INT32_MAX) return MPO_EINVAL;
+    if (n == 0) return MPO_OK;
+    if (!size || !first || !order_out) return MPO_EINVAL;
+    rank_key* keys = (rank_key*)malloc((size_t)n * sizeof(rank_key));
+    if (!keys) return MPO_EINVAL;
+    for (int64_t i = 0; i < n; ++i) {
+        keys[i].size = size[i];
+        keys[i].first = first[i];
+        keys[i].id = (int32_t)i;
+    }
+    qsort(keys, (size_t)n, sizeof(rank_key), cmp_rank);
+    for (int64_t k = 0; k < n; ++k) order_out[k] = keys[k].id;
+    free(keys);
+    return MPO_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Gap search over the byte ranges of the conflicting, already placed tensors.
+ * A free gap is a maximal interval of [0, inf) not covered by any range. */
+
+typedef struct {
+    int64_t start;
+    int64_t end;
+} range;
+
+static int cmp_range(const void* pa, const void* pb) {
+    const range* a = (const range*)pa;
+    const range* b = (const range*)pb;
+    if (a->start != b->start) return a->start < b->start ? -1 : 1;
+    if (a->end != b->end) return a->end < b->end ? -1 : 1;
+    return 0;
+}
+
+/* Lowest offset x >= 0 with [x, x + s) disjoint from every range. */
+static int64_t lowest_fit(range* r, int64_t k, int64_t s) {
+    qsort(r, (size_t)k, sizeof(range), cmp_range);
+    int64_t covered_to = 0; /* every byte below covered_to that follows the last gap is taken */
+    for (int64_t i = 0; i < k; ++i) {
+        if (r[i].start - covered_to >= s) return covered_to;
+        if (r[i].end > covered_to) covered_to = r[i].end;
+    }
+    return covered_to;
+}
+
+/* Smallest finite free gap that holds s bytes (lowest start among equals);
+ * the unbounded gap above every range only when no finite gap fits. */
+static int64_t best_fit(range* r, int64_t k, int64_t s) {
+    qsort(r, (size_t)k, sizeof(range), cmp_range);
+    int64_t covered_to = 0;
+    int64_t best_start = -1, best_len = 0;
+    for (int64_t i = 0; i < k; ++i) {
+        int64_t gap = r[i].start - covered_to;
+        if (gap >= s && (best_start < 0 || gap < best_len)) {
+            best_start = covered_to;
+            best_len = gap;
+        }
+        if (r[i].end > covered_to) covered_to = r[i].end;
+    }
+    return best_start >= 0 ? best_start : covered_to;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Conflict index: time buckets of width w over the ops; every placed tensor is
+ * listed in each bucket its lifetime touches.  Two intersecting lifetimes both
+ * contain the op max(first_p, first_t), so a conflicting pair is accepted only
+ * in the bucket holding that op, which makes each pair appear exactly once. */
+
+typedef struct {
+    int32_t* ids;
+    int64_t len;
+    int64_t cap;
+} id_list;
+
+static int push_id(id_list* l, int32_t id) {
+    if (l->len == l->cap) {
+        int64_t cap = l->cap ? 2 * l->cap : 16;
+        int32_t* p = (int32_t*)realloc(l->ids, (size_t)cap * sizeof(int32_t));
+        if (!p) return 0;
+        l->ids = p;
+        l->cap = cap;
+    }
+    l->ids[l->len++] = id;
+    return 1;
+}
+
+int32_t mpo_plan_trace_w(const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n, int32_t num_ops, int32_t policy, int32_t bucket_width,
+                         int64_t* offset_out, int64_t* peak_out) {
+    if (policy != MPO_LOWEST_FIT && policy != MPO_BEST_FIT) return MPO_EINVAL;
+    if (bucket_width < 1 || !peak_out) return MPO_EINVAL;
+    if (n > 0 && !offset_out) return MPO_EINVAL;
+    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
+    if (st != MPO_OK) return st;
+    *peak_out = 0;
+    if (n == 0) return MPO_OK;
+
+    int32_t* order = (int32_t*)malloc((size_t)n * sizeof(int32_t));
+    int64_t nb = ((int64_t)num_ops + bucket_width - 1) / bucket_width;
+    id_list* bucket = (id_list*)calloc((size_t)nb, sizeof(id_list));
+    range* conf = (range*)malloc((size_t)n * sizeof(range));
+    if (!order || !bucket || !conf) {
+        free(order); free(bucket); free(conf);
+        return MPO_EINVAL;
+    }
+    mpo_rank_order(size, first, n, order);
+
+    int32_t status = MPO_OK;
+    int64_t peak = 0;
+    for (int64_t k = 0; k < n && status == MPO_OK; ++k) {
+        int32_t t = order[k];
+        int64_t b_lo = first[t] / bucket_width, b_hi = last[t] / bucket_width;
+        /* C_t: already placed tensors whose lifetimes intersect t's. */
+        int64_t nc = 0;
+        for (int64_t b = b_lo; b <= b_hi; ++b) {
+            for (int64_t e = 0; e < bucket[b].len; ++e) {
+                int32_t p = bucket[b].ids[e];
+                if (first[p] > last[t] || first[t] > last[p]) continue;
+                int32_t meet = first[p] > first[t] ? first[p] : first[t];
+                if (meet / bucket_width != b) continue;
+                conf[nc].start = offset_out[p];
+                conf[nc].end = offset_out[p] + size[p];
+                ++nc;
+            }
+        }
+        int64_t off = (policy == MPO_LOWEST_FIT) ? lowest_fit(conf, nc, size[t])
+                                                 : best_fit(conf, nc, size[t]);
+        offset_out[t] = off;
+        if (off + size[t] > peak) peak = off + size[t];
+        for (int64_t b = b_lo; b <= b_hi; ++b)
+            if (!push_id(&bucket[b], t)) status = MPO_EINVAL;
+    }
+    *peak_out = peak;
+
+    for (int64_t b = 0; b < nb; ++b) free(bucket[b].ids);
+    free(bucket);
+    free(conf);
+    free(order);
+    return status;
+}
+
+int32_t mpo_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                       int64_t n, int32_t num_ops, int32_t policy,
+                       int64_t* offset_out, int64_t* peak_out) {
+    /* Bucket width: about one mean lifetime (only speed depends on it). */
+    int64_t w = 1;
+    if (n > 0 && size && first && last) {
+        int64_t span = 0;
+        for (int64_t i = 0; i < n; ++i)
+            if (last[i] >= first[i]) span += (int64_t)last[i] - first[i] + 1;
+        w = span / n;
+        if (w < 1) w = 1;
+        if (w > num_ops && num_ops > 0) w = num_ops;
+        if (w > INT32_MAX) w = INT32_MAX;
+    }
+    return mpo_plan_trace_w(size, first, last, n, num_ops, policy, (int32_t)w, offset_out,
+                            peak_out);
+}
+
+/* ------------------------------------------------------------------------- */
+/* Live bytes per op: the sum, over tensors alive at op t, of their sizes. */
+
+int32_t mpo_live_bytes_profile(const int64_t* size, const int32_t* first, const int32_t* last,
+                               int64_t n, int32_t num_ops, int64_t* live_out,
+                               int64_t* max_live_out) {
+    if (!max_live_out) return MPO_EINVAL;
+    if (num_ops > 0 && !live_out) return MPO_EINVAL;
+    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
+    if (st != MPO_OK) return st;
+    for (int32_t t = 0; t < num_ops; ++t) live_out[t] = 0;
+    for (int64_t i = 0; i < n; ++i)
+        for (int32_t t = first[i]; t <= last[i]; ++t) live_out[t] += size[i];
+    int64_t best = 0;
+    for (int32_t t = 0; t < num_ops; ++t)
+        if (live_out[t] > best) best = live_out[t];
+    *max_live_out = best;
+    return MPO_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Plan validation: the pairwise ordering constraints of Eq. 2.1 say that two
+ * tensors with intersecting lifetimes must not overlap in memory. */
+
+int32_t mpo_validate_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                          const int64_t* offset, int64_t n, int64_t* pairs_out,
+                          int64_t capacity, int64_t* n_conflicts_out) {
+    if (!n_conflicts_out || capacity < 0) return MPO_EINVAL;
+    if (capacity > 0 && !pairs_out) return MPO_EINVAL;
+    if (n > 0 && !offset) return MPO_EINVAL;
+    int32_t st = check_trace(size, first, last, n, 0, 0);
+    if (st != MPO_OK) return st;
+    for (int64_t i = 0; i < n; ++i)
+        if (offset[i] < 0 || offset[i] > INT64_MAX - size[i]) return MPO_EINVAL;
+    int64_t count = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        for (int64_t j = i + 1; j < n; ++j) {
+            int lifetimes_meet = first[i] <= last[j] && first[j] <= last[i];
+            int bytes_meet = offset[i] < offset[j] + size[j] && offset[j] < offset[i] + size[i];
+            if (lifetimes_meet && bytes_meet) {
+                if (count < capacity) {
+                    pairs_out[2 * count] = i;
+                    pairs_out[2 * count + 1] = j;
+                }
+                ++count;
+            }
+        }
+    }
+    *n_conflicts_out = count;
+    return count > capacity ? MPO_ENOSPC : MPO_OK;
+}

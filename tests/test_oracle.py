@@ -1,0 +1,307 @@
+"""Pins of the CPU oracle against what the thesis and the mathematics fix.
+
+Nothing here compares the oracle with itself: every check uses a hand-worked
+example, a closed form, a textbook special case, a brute-force optimum or an
+independent definitional computation (tests/defs.py).
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+import oracle
+from defs import (best_fit_candidates, brute_force_opt, conflict, greedy_definitional,
+                  intersecting_pairs_band, live_profile_bruteforce, lowest_fit_candidates,
+                  rank_order)
+from paper_2203_00448_amd import tracegen as tg
+
+LOWEST, BEST = oracle.LOWEST_FIT, oracle.BEST_FIT
+
+
+def _num_ops(ex):
+    return max(ex["last"]) + 1
+
+
+# ---------------------------------------------------------------- hand examples
+
+def test_hand_examples_offsets(hand_examples):
+    for ex in hand_examples:
+        off, peak = oracle.plan_trace(ex["size"], ex["first"], ex["last"], _num_ops(ex), LOWEST)
+        assert off.tolist() == ex["lowest_fit"], ex["name"]
+        assert peak == ex["peak"], ex["name"]
+        offb, peakb = oracle.plan_trace(ex["size"], ex["first"], ex["last"], _num_ops(ex), BEST)
+        assert offb.tolist() == ex["best_fit"], ex["name"]
+        assert peakb == ex["peak_best"], ex["name"]
+
+
+def test_hand_examples_live_and_opt(hand_examples):
+    for ex in hand_examples:
+        _, lb = oracle.live_bytes_profile(ex["size"], ex["first"], ex["last"], _num_ops(ex))
+        assert lb == ex["lb"], ex["name"]
+        assert brute_force_opt(ex["size"], ex["first"], ex["last"], stack=False) == ex["opt"]
+        assert brute_force_opt(ex["size"], ex["first"], ex["last"], stack=True) == ex["opt"]
+
+
+def test_hand_examples_validate_clean(hand_examples):
+    for ex in hand_examples:
+        pairs, cnt = oracle.validate_plan(ex["size"], ex["first"], ex["last"], ex["lowest_fit"])
+        assert cnt == 0 and pairs.shape == (0, 2)
+
+
+# ---------------------------------------------------------------- ordering
+
+def test_rank_order_matches_python_sort():
+    rng = np.random.default_rng(11)
+    for _ in range(20):
+        n = int(rng.integers(1, 300))
+        size = 64 * rng.integers(1, 5, n)  # few sizes -> many ties
+        first = rng.integers(0, 7, n)
+        assert oracle.rank_order(size, first).tolist() == rank_order(size, first)
+
+
+# ---------------------------------------------------------------- special cases
+
+def test_full_overlap_prefix_sums():
+    rng = np.random.default_rng(12)
+    for _ in range(10):
+        n = int(rng.integers(1, 60))
+        size = 64 * rng.integers(1, 20, n)
+        first = np.zeros(n, np.int64)
+        last = np.full(n, 5)
+        off, peak = oracle.plan_trace(size, first, last, 6)
+        order = rank_order(size, first)
+        expect = np.zeros(n, np.int64)
+        expect[order] = np.concatenate([[0], np.cumsum(size[order])[:-1]])
+        assert off.tolist() == expect.tolist()
+        assert peak == int(size.sum())
+
+
+def test_disjoint_all_zero():
+    rng = np.random.default_rng(13)
+    n = 50
+    size = 64 * rng.integers(1, 100, n)
+    first = np.arange(n) * 2
+    last = first + 1
+    off, peak = oracle.plan_trace(size, first, last, 2 * n)
+    assert (off == 0).all() and peak == int(size.max())
+
+
+def test_equal_sizes_interval_colouring_optimal():
+    # First-fit colouring of an interval graph in left-endpoint order uses
+    # exactly clique-number colours, so the peak is size * max live count.
+    rng = np.random.default_rng(14)
+    for _ in range(20):
+        t = tg.random_trace(rng, int(rng.integers(1, 200)), 40, max_len=8, sizes=[192])
+        off, peak = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+        count = np.zeros(t.num_ops + 1, np.int64)
+        np.add.at(count, t.first, 1)
+        np.add.at(count, t.last.astype(np.int64) + 1, -1)
+        assert peak == 192 * int(np.cumsum(count).max())
+        assert (off % 192 == 0).all()
+
+
+# ---------------------------------------------------------------- definitional cross-checks
+
+@pytest.mark.parametrize("policy", [LOWEST, BEST])
+def test_definitional_random(policy):
+    rng = np.random.default_rng(15 + policy)
+    for trial in range(150):
+        n = int(rng.integers(0, 40))
+        T = int(rng.integers(1, 12))
+        alphabet = [64, 128, 192, 448] if trial % 2 else None
+        t = tg.random_trace(rng, n, T, sizes=alphabet)
+        off, peak = oracle.plan_trace(t.size, t.first, t.last, T, policy)
+        ref, ref_peak = greedy_definitional(t.size, t.first, t.last, policy)
+        assert off.tolist() == ref and peak == ref_peak
+
+
+@pytest.mark.parametrize("width", [1, 2, 3, 7, 1000])
+def test_bucket_width_does_not_matter(width):
+    rng = np.random.default_rng(16)
+    t = tg.random_trace(rng, 300, 50, max_len=12, sizes=[64, 128, 320, 4096])
+    ref, ref_peak = oracle.plan_trace(t.size, t.first, t.last, t.num_ops, LOWEST, bucket_width=1000)
+    off, peak = oracle.plan_trace(t.size, t.first, t.last, t.num_ops, LOWEST, bucket_width=width)
+    assert off.tolist() == ref.tolist() and peak == ref_peak
+    assert oracle.validate_plan(t.size, t.first, t.last, off)[1] == 0
+
+
+def test_lowest_gap_is_minimal_bruteforce():
+    # I8: no byte offset below the chosen one is feasible against the
+    # earlier-ranked conflicting tensors (scan of every integer offset).
+    rng = np.random.default_rng(17)
+    for _ in range(40):
+        t = tg.random_trace(rng, int(rng.integers(1, 14)), 6, unit=1,
+                            sizes=[1, 2, 3, 5])
+        off, _ = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+        order = rank_order(t.size, t.first)
+        for k, i in enumerate(order):
+            placed = [(int(off[p]), int(t.size[p])) for p in order[:k]
+                      if conflict(t.first, t.last, p, i)]
+            for x in range(int(off[i]) + 1):
+                ok = all(x + t.size[i] <= o or o + z <= x for o, z in placed)
+                assert ok == (x == off[i])
+
+
+def test_best_fit_gap_definition_small():
+    # tightest gap, lowest start among equal gaps, top gap only as fallback
+    assert best_fit_candidates(64, [(128, 64), (256, 64)]) == 192      # gaps [0,128) [192,256)
+    assert best_fit_candidates(64, [(64, 64), (192, 64)]) == 0         # equal gaps: lowest start
+    assert best_fit_candidates(64, [(128, 64), (256, 64), (384, 64)]) == 192
+    assert best_fit_candidates(200, [(100, 50)]) == 150                # only the top gap fits
+    assert lowest_fit_candidates(64, [(128, 64), (256, 64)]) == 0
+    assert lowest_fit_candidates(64, [(0, 64), (64, 64)]) == 128
+
+
+# ---------------------------------------------------------------- invariants
+
+def _invariants(t, off, peak):
+    size = t.size.astype(np.int64)
+    _, lb = oracle.live_bytes_profile(t.size, t.first, t.last, t.num_ops)
+    assert oracle.validate_plan(t.size, t.first, t.last, off)[1] == 0          # I1
+    assert peak >= lb                                                          # I2
+    acc = int(np.bitwise_or.reduce(size))
+    unit = acc & -acc                                                          # 2^ctz(OR sizes)
+    assert (off % unit == 0).all()                                             # I4
+    assert peak <= int(size.sum())                                             # I6
+    order = rank_order(t.size, t.first)
+    rank = np.empty(t.n, np.int64)
+    rank[order] = np.arange(t.n)
+    for i in range(t.n):                                                       # I5
+        if off[i] == 0:
+            continue
+        ends = {int(off[p] + size[p]) for p in range(t.n)
+                if rank[p] < rank[i] and conflict(t.first, t.last, p, i)}
+        assert int(off[i]) in ends
+
+
+def test_invariants_chain256():
+    t = tg.chain256()
+    off, peak = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+    _invariants(t, off, peak)
+
+
+def test_invariants_random():
+    rng = np.random.default_rng(18)
+    for _ in range(30):
+        t = tg.random_trace(rng, int(rng.integers(1, 120)), 30, max_len=10)
+        off, peak = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+        _invariants(t, off, peak)
+
+
+def test_relabelling_permutes_offsets():
+    # I7: with distinct (size, first) keys the ids carry no information.
+    rng = np.random.default_rng(19)
+    n = 80
+    size = 64 * rng.permutation(np.arange(1, n + 1))
+    first = rng.integers(0, 20, n)
+    last = first + rng.integers(0, 6, n)
+    off, peak = oracle.plan_trace(size, first, last, 26)
+    perm = rng.permutation(n)
+    off2, peak2 = oracle.plan_trace(size[perm], first[perm], last[perm], 26)
+    assert peak2 == peak and off2.tolist() == off[perm].tolist()
+
+
+def test_greedy_at_least_opt_tiny():
+    rng = np.random.default_rng(20)
+    for _ in range(25):
+        t = tg.random_trace(rng, int(rng.integers(1, 7)), 5, sizes=[64, 128, 192, 256])
+        _, peak = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+        opt = brute_force_opt(t.size, t.first, t.last, stack=False)
+        assert opt == brute_force_opt(t.size, t.first, t.last, stack=True)
+        _, lb = oracle.live_bytes_profile(t.size, t.first, t.last, t.num_ops)
+        assert lb <= opt <= peak
+
+
+# ---------------------------------------------------------------- liveness
+
+def test_live_profile_bruteforce():
+    rng = np.random.default_rng(21)
+    for _ in range(20):
+        T = int(rng.integers(1, 30))
+        t = tg.random_trace(rng, int(rng.integers(0, 60)), T)
+        live, mx = oracle.live_bytes_profile(t.size, t.first, t.last, T)
+        ref = live_profile_bruteforce(t.size, t.first, t.last, T)
+        assert live.tolist() == ref.tolist() and mx == int(ref.max())
+
+
+def test_live_profile_empty_ops():
+    live, mx = oracle.live_bytes_profile([], [], [], 0)
+    assert live.shape == (0,) and mx == 0
+    live, mx = oracle.live_bytes_profile([], [], [], 5)
+    assert live.tolist() == [0] * 5 and mx == 0
+
+
+# ---------------------------------------------------------------- validation
+
+def test_validate_all_zero_offsets_reports_every_intersecting_pair():
+    rng = np.random.default_rng(22)
+    for _ in range(10):
+        t = tg.random_trace(rng, int(rng.integers(0, 120)), 25, max_len=6)
+        pairs, cnt = oracle.validate_plan(t.size, t.first, t.last, np.zeros(t.n, np.int64))
+        expect = sorted(intersecting_pairs_band(t.first, t.last))
+        assert cnt == len(expect)
+        assert [tuple(p) for p in pairs.tolist()] == expect
+
+
+def test_validate_corrupted_plan_properties():
+    rng = np.random.default_rng(23)
+    t = tg.random_trace(rng, 400, 40, max_len=5, sorted_first=True)
+    off, _ = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+    bad, chosen = tg.corrupt_offsets(t.first, t.last, off, seed=7, k=10)
+    pairs, cnt = oracle.validate_plan(t.size, t.first, t.last, bad)
+    chosen_set = set(chosen.tolist())
+    assert cnt > 0
+    for i, j in pairs.tolist():
+        assert i < j and (i in chosen_set or j in chosen_set)
+        assert conflict(t.first, t.last, i, j)
+        assert not (bad[i] + t.size[i] <= bad[j] or bad[j] + t.size[j] <= bad[i])
+    # every perturbed tensor now sits exactly on a live neighbour
+    assert chosen_set <= {v for p in pairs.tolist() for v in p}
+    assert [tuple(p) for p in pairs.tolist()] == sorted(map(tuple, pairs.tolist()))
+
+
+def test_validate_capacity():
+    size, first, last = [64, 64, 64], [0, 0, 0], [1, 1, 1]
+    pairs, cnt = oracle.validate_plan(size, first, last, [0, 0, 0])
+    assert cnt == 3 and pairs.tolist() == [[0, 1], [0, 2], [1, 2]]
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.validate_plan(size, first, last, [0, 0, 0], capacity=2)
+    assert e.value.status == oracle.ENOSPC
+    # touching byte ranges are not a conflict
+    assert oracle.validate_plan(size, first, last, [0, 64, 128])[1] == 0
+
+
+# ---------------------------------------------------------------- input errors
+
+def test_invalid_traces():
+    ok = ([64], [0], [0])
+    assert oracle.check_trace(*ok, 1) == oracle.OK
+    assert oracle.check_trace([0], [0], [0], 1) == oracle.EINVAL        # size <= 0
+    assert oracle.check_trace([-64], [0], [0], 1) == oracle.EINVAL
+    assert oracle.check_trace([64], [-1], [0], 1) == oracle.EINVAL      # first < 0
+    assert oracle.check_trace([64], [2], [1], 3) == oracle.EINVAL       # first > last
+    assert oracle.check_trace([64], [0], [1], 1) == oracle.EINVAL       # last >= num_ops
+    big = 2 ** 62
+    assert oracle.check_trace([big, big - 1], [0, 0], [0, 0], 1) == oracle.OK  # INT64_MAX
+    assert oracle.check_trace([big, big], [0, 0], [0, 0], 1) == oracle.EOVERFLOW
+    # most negative code wins when both kinds are present
+    assert oracle.check_trace([big, big, big, 0], [0, 0, 0, 0], [0, 0, 0, 0], 1) == oracle.EOVERFLOW
+    with pytest.raises(oracle.OracleError):
+        oracle.plan_trace([64], [0], [3], 2)
+
+
+def test_empty_trace():
+    off, peak = oracle.plan_trace([], [], [], 0)
+    assert off.shape == (0,) and peak == 0
+
+
+# ---------------------------------------------------------------- generator self-checks
+
+def test_generator_statistics_small():
+    t = tg.chain256()
+    assert int(t.size.min()) >= 1024 and int(t.size.max()) <= 4 << 20
+    _, lb = oracle.live_bytes_profile(t.size, t.first, t.last, t.num_ops)
+    assert lb == 6_039_488
+    b = tg.resnext_trace(0)
+    assert b.n == 2000 and (b.size % 64 == 0).all()
+    assert int(b.size.min()) >= 4096 and int(b.size.max()) <= 1 << 26
