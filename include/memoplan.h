@@ -1,0 +1,97 @@
+/*
+ * memoplan.h -- C ABI of the MI355X (gfx950) static memory planner.
+ *
+ * What it computes (Levental, "Memory Planning for Deep Neural Networks"):
+ * given the byte size and the lifetime [first, last] (closed interval of op
+ * indices) of every intermediate tensor of a recorded trace, assign each
+ * tensor a byte offset in one arena so that no two tensors whose lifetimes
+ * intersect overlap in memory (the offline dynamic-storage-allocation problem
+ * of Section 2.3; the non-overlap constraint is the ordering constraint of
+ * Eq. 2.1).  Offsets come from greedy_by_size (Section 2.3, the default
+ * planner of Section 3.2): tensors are taken by size descending, ties by first
+ * op ascending, then by id ascending; each is put at the lowest offset at
+ * which it does not overlap any already placed tensor whose lifetime meets
+ * its own.  The arena size (total_mem of Eq. 2.1, the slab of Section 3.3)
+ * is max(offset + size), 0 for an empty trace.
+ *
+ * Conventions shared by every entry point
+ *  - All array arguments are DEVICE pointers owned by the caller; the library
+ *    never allocates device memory, never frees, never synchronises.  Work is
+ *    enqueued on `stream` (a hipStream_t passed as void*; NULL = null stream).
+ *  - Tensor id = array index (in a batch: index within its trace).  Sizes are
+ *    int64 bytes, lifetimes int32 op indices, offsets int64 bytes.
+ *  - Return value (host, synchronous): MP_OK when the work was enqueued;
+ *    MP_EINVAL for bad host arguments (NULL pointer where data is needed,
+ *    negative counts, unknown policy, workspace too small), in which case
+ *    nothing is launched; MP_EDEVICE when a launch fails.
+ *  - Data-dependent errors are found on the device and stored into the
+ *    caller's device int32 `*status_out` (reset to MP_OK by the call itself;
+ *    the most negative code wins): MP_EINVAL for size <= 0, first < 0,
+ *    first > last or last >= num_ops; MP_EOVERFLOW when the sizes of a trace
+ *    sum past INT64_MAX; MP_ENOSPC when a documented capacity is exceeded.
+ *    Outputs are unspecified when *status_out != MP_OK.
+ *  - Calls that share a status word or outputs on different streams race.
+ */
+#ifndef MEMOPLAN_H
+#define MEMOPLAN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MP_OK 0
+#define MP_EINVAL (-1)
+#define MP_ENOSPC (-2)
+#define MP_EOVERFLOW (-3)
+#define MP_EDEVICE (-4)
+
+/* Fit policy.  LOWEST_FIT: lowest gap that fits.  BEST_FIT: tightest finite
+ * gap that fits (lowest start among equals), the space above every conflicting
+ * tensor only when no finite gap fits -- the "best fit criterion" wording of
+ * Section 2.3. */
+#define MP_LOWEST_FIT 0
+#define MP_BEST_FIT 1
+
+/* Longest trace (tensors) the batched planner accepts. */
+#define MP_BATCH_MAX_TRACE_LEN 4096
+
+/* Human-readable name of a status code (static storage). */
+const char* mp_status_string(int32_t status);
+
+/* Greedy-by-size plans for many independent traces in one launch (one
+ * workgroup per trace, the trace held in LDS).
+ *   begin[n_traces + 1] int64: trace b owns tensors [begin[b], begin[b+1]) of
+ *                        the concatenated arrays; 0 <= begin[b] <= begin[b+1]
+ *                        <= n_tensors (checked on device, MP_EINVAL).
+ *   num_ops[n_traces]  int32: op count of each trace (lifetimes < num_ops[b]).
+ *   size, first, last  [n_tensors] (int64, int32, int32).
+ *   max_trace_len      host bound on begin[b+1] - begin[b], 0..4096; a longer
+ *                      trace sets MP_EINVAL.
+ *   policy             MP_LOWEST_FIT (MP_BEST_FIT returns MP_EINVAL for now).
+ *   offset_out[n_tensors] int64, peak_out[n_traces] int64 (arena bytes),
+ *   lb_out[n_traces]   int64 or NULL: max over ops of the live bytes, a lower
+ *                      bound on any valid arena size.
+ *   workspace          unused (may be NULL, 0 bytes).
+ * Capacity limits (MP_ENOSPC on device): per trace, sum of sizes divided by
+ * 2^ctz(OR of sizes) must be < 2^32, and the number of (earlier-ranked,
+ * lifetime-intersecting) tensor pairs must fit the LDS pair list reported by
+ * mp_batch_pair_capacity(max_trace_len).  Use mp_plan_trace beyond them. */
+int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                      const int64_t* size, const int32_t* first, const int32_t* last,
+                      int64_t n_tensors, int64_t max_trace_len, int32_t policy,
+                      int64_t* offset_out, int64_t* peak_out, int64_t* lb_out,
+                      void* workspace, size_t workspace_bytes, int32_t* status_out,
+                      void* stream);
+
+/* Pair-list capacity per trace of mp_plan_batch for a given max_trace_len
+ * (host query, no device work); -1 when max_trace_len is out of range. */
+int64_t mp_batch_pair_capacity(int64_t max_trace_len);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

@@ -1,0 +1,49 @@
+// C ABI entry points: host-side argument checks, then launches on the
+// caller's stream.  No allocation, no synchronisation.
+#include "internal.hpp"
+
+using namespace mp;
+
+namespace {
+
+int32_t launched(hipError_t e) { return e == hipSuccess ? MP_OK : MP_EDEVICE; }
+
+}  // namespace
+
+extern "C" const char* mp_status_string(int32_t status) {
+    switch (status) {
+        case MP_OK: return "ok";
+        case MP_EINVAL: return "invalid argument or trace";
+        case MP_ENOSPC: return "capacity exceeded";
+        case MP_EOVERFLOW: return "sum of sizes exceeds INT64_MAX";
+        case MP_EDEVICE: return "device launch or execution failure";
+        default: return "unknown status";
+    }
+}
+
+extern "C" int64_t mp_batch_pair_capacity(int64_t max_trace_len) {
+    const BatchShape s = batch_shape(max_trace_len);
+    return s.ok ? (int64_t)s.cap_pairs : -1;
+}
+
+extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                                 const int64_t* size, const int32_t* first, const int32_t* last,
+                                 int64_t n_tensors, int64_t max_trace_len, int32_t policy,
+                                 int64_t* offset_out, int64_t* peak_out, int64_t* lb_out,
+                                 void* workspace, size_t workspace_bytes, int32_t* status_out,
+                                 void* stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || !status_out) return MP_EINVAL;
+    if (policy != MP_LOWEST_FIT) return MP_EINVAL;
+    if (!batch_shape(max_trace_len).ok) return MP_EINVAL;
+    if (!begin) return MP_EINVAL;
+    if (n_traces > 0 && (!num_ops || !peak_out)) return MP_EINVAL;
+    if (n_tensors > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = launch_reset_status(status_out, st);
+    if (e != hipSuccess || n_traces == 0) return launched(e);
+    BatchArgs a{begin,      n_traces, num_ops,  size,   first,     last,
+                n_tensors,  max_trace_len, offset_out, peak_out, lb_out, status_out};
+    return launched(launch_plan_batch(a, st));
+}

@@ -1,0 +1,71 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function the public header declares, and rejects bad host arguments
+before touching the device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "memoplan.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mp_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2203_00448_amd import binding
+    return binding.load_library()
+
+
+def test_header_declares_entry_points():
+    names = declared_functions()
+    for required in ("mp_plan_batch", "mp_status_string"):
+        assert required in names
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code in (0, -1, -2, -3, -4):
+        assert lib.mp_status_string(code)
+    assert lib.mp_status_string(0) == b"ok"
+
+
+def test_plan_batch_host_checks(lib):
+    from paper_2203_00448_amd import binding as b
+    dummy = ctypes.c_void_p(16)  # never dereferenced: every call below fails a host check
+    st = dummy
+    # negative counts
+    assert lib.mp_plan_batch(dummy, -1, dummy, dummy, dummy, dummy, 0, 10, 0, dummy, dummy, None,
+                             None, 0, st, None) == b.MP_EINVAL
+    assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, -5, 10, 0, dummy, dummy, None,
+                             None, 0, st, None) == b.MP_EINVAL
+    # unknown policy
+    assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 10, 7, dummy, dummy, None,
+                             None, 0, st, None) == b.MP_EINVAL
+    # max_trace_len out of range
+    assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 5000, 0, dummy, dummy, None,
+                             None, 0, st, None) == b.MP_EINVAL
+    # missing status word / arrays
+    assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
+                             None, 0, None, None) == b.MP_EINVAL
+    assert lib.mp_plan_batch(dummy, 1, dummy, None, dummy, dummy, 4, 10, 0, dummy, dummy, None,
+                             None, 0, st, None) == b.MP_EINVAL
+    assert lib.mp_plan_batch(None, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
+                             None, 0, st, None) == b.MP_EINVAL
+
+
+def test_pair_capacity(lib):
+    assert lib.mp_batch_pair_capacity(-1) == -1
+    assert lib.mp_batch_pair_capacity(4097) == -1
+    assert lib.mp_batch_pair_capacity(2000) >= 12000   # the 2000-tensor traces need ~11K
+    assert lib.mp_batch_pair_capacity(4096) > 0

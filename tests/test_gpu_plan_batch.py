@@ -1,0 +1,147 @@
+"""Parity of the batched HIP planner (mp_plan_batch) with the CPU oracle.
+
+Integer work: offsets, peaks and lower bounds must match bit for bit."""
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import batch_to_device, dev, host, need_gpu, torch
+from paper_2203_00448_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle_batch(batch):
+    off, peak = oracle.plan_batch(batch.begin, batch.num_ops, batch.size, batch.first, batch.last)
+    lb = np.array([oracle.live_bytes_profile(*[a for a in (batch.trace(b).size, batch.trace(b).first,
+                                                            batch.trace(b).last)],
+                                             batch.trace(b).num_ops)[1]
+                   for b in range(batch.n_traces)], dtype=np.int64)
+    return off, peak, lb
+
+
+def _gpu_batch(binding, batch, **kw):
+    args = batch_to_device(batch)
+    off, peak, lb = binding.plan_batch(*args, **kw)
+    return host(off), host(peak), host(lb)
+
+
+def _check(binding, batch, **kw):
+    off, peak, lb = _gpu_batch(binding, batch, **kw)
+    eo, ep, el = _oracle_batch(batch)
+    bad = np.nonzero(off != eo)[0]
+    assert bad.size == 0, f"{bad.size} offsets differ, first at {bad[:5]}"
+    assert (peak == ep).all()
+    assert (lb == el).all()
+    return off, peak, lb
+
+
+def test_chain256_single_trace_batch():
+    binding = need_gpu()
+    print("case chain256 as a batch of one", flush=True)
+    _check(binding, tg.concat([tg.chain256()]))
+
+
+def test_resnext_batch_full():
+    binding = need_gpu()
+    print("case resnext batch 1024 x 2000", flush=True)
+    batch = tg.resnext_batch()
+    off, peak, lb = _check(binding, batch, max_trace_len=2000)
+    assert (peak >= lb).all()
+
+
+def test_random_ragged_batches():
+    binding = need_gpu()
+    rng = np.random.default_rng(100)
+    traces = []
+    for k in range(300):
+        n = int(rng.choice([0, 1, 2, 3, 17, 64, 255, 256, 257, 700, 1500]))
+        if n <= 64:   # dense: up to n^2/2 pairs
+            T, span = int(rng.integers(1, 20)), int(rng.integers(1, 20))
+        else:         # about one birth per op, short lifetimes
+            T, span = n * int(rng.integers(1, 3)) + 1, int(rng.integers(1, 12))
+        alphabet = [64, 128, 192, 448, 1024] if k % 3 == 0 else None
+        traces.append(tg.random_trace(rng, n, T, max_len=span, sizes=alphabet,
+                                      sorted_first=(k % 2 == 0)))
+    print("case 300 random ragged traces (sorted and unsorted first)", flush=True)
+    _check(binding, tg.concat(traces), max_trace_len=1500)
+
+
+def test_adversarial_shapes():
+    binding = need_gpu()
+    rng = np.random.default_rng(101)
+    n = 200
+    full = tg.Trace(64 * rng.integers(1, 50, n), np.zeros(n, np.int32), np.full(n, 9, np.int32), 10)
+    equal = tg.random_trace(rng, 600, 300, max_len=10, sizes=[320])
+    disjoint = tg.Trace(64 * rng.integers(1, 50, n), np.arange(n, dtype=np.int32),
+                        np.arange(n, dtype=np.int32), n)
+    span = tg.random_trace(rng, 500, 100, max_len=5, sorted_first=True)
+    span.first[250], span.last[250] = 0, 99
+    odd = tg.random_trace(rng, 300, 50, max_len=10, sizes=[1, 3, 7, 100, 1001])
+    print("case adversarial shapes", flush=True)
+    _check(binding, tg.concat([full, equal, disjoint, span, odd]), max_trace_len=1000)
+
+
+def test_max_trace_len_4096():
+    binding = need_gpu()
+    rng = np.random.default_rng(102)
+    t = tg.random_trace(rng, 4096, 4096, max_len=4, sorted_first=True)
+    print("case 4096-tensor trace", flush=True)
+    _check(binding, tg.concat([t, tg.resnext_trace(5)]), max_trace_len=4096)
+
+
+def test_deterministic_repeats():
+    binding = need_gpu()
+    batch = tg.concat(tg.resnext_trace(b) for b in range(64))
+    args = batch_to_device(batch)
+    print("case 10 repeats of 64 resnext traces", flush=True)
+    ref = [host(x) for x in binding.plan_batch(*args, max_trace_len=2000)]
+    for _ in range(10):
+        got = [host(x) for x in binding.plan_batch(*args, max_trace_len=2000)]
+        for a, b in zip(ref, got):
+            assert np.array_equal(a, b)
+
+
+def _status(binding, batch, **kw):
+    args = batch_to_device(batch)
+    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    binding.plan_batch(*args, check=False, status=status, **kw)
+    return int(status.item())
+
+
+def test_device_status_codes():
+    binding = need_gpu()
+    good = tg.chain256()
+    print("case device status codes", flush=True)
+    assert _status(binding, tg.concat([good])) == binding.MP_OK
+    bad = tg.Trace(good.size.copy(), good.first.copy(), good.last.copy(), good.num_ops)
+    bad.size[7] = 0
+    assert _status(binding, tg.concat([good, bad])) == binding.MP_EINVAL
+    bad = tg.Trace(good.size.copy(), good.first.copy(), good.last.copy(), good.num_ops)
+    bad.first[3] = bad.last[3] + 1
+    assert _status(binding, tg.concat([bad])) == binding.MP_EINVAL
+    bad = tg.Trace(good.size.copy(), good.first.copy(), good.last.copy(), 200)
+    assert _status(binding, tg.concat([bad])) == binding.MP_EINVAL  # last >= num_ops
+    big = tg.Trace(np.array([2 ** 62, 2 ** 62], np.int64), np.zeros(2, np.int32),
+                   np.zeros(2, np.int32), 1)
+    assert _status(binding, tg.concat([good, big])) == binding.MP_EOVERFLOW
+    # offsets kept in 32-bit units of the common alignment: 2^32 units do not fit
+    wide = tg.Trace(np.array([2 ** 31 + 1, 2 ** 31 + 1], np.int64), np.zeros(2, np.int32),
+                    np.zeros(2, np.int32), 1)
+    assert _status(binding, tg.concat([wide])) == binding.MP_ENOSPC
+    # more tensors than the declared maximum trace length
+    assert _status(binding, tg.concat([good]), max_trace_len=100) == binding.MP_EINVAL
+    # too many predecessor pairs for the LDS list
+    n = 2000
+    dense = tg.Trace(np.full(n, 64, np.int64), np.zeros(n, np.int32), np.zeros(n, np.int32), 1)
+    assert _status(binding, tg.concat([dense])) == binding.MP_ENOSPC
+
+
+def test_empty_batch_and_empty_traces():
+    binding = need_gpu()
+    batch = tg.concat([tg.Trace(np.zeros(0, np.int64), np.zeros(0, np.int32), np.zeros(0, np.int32), 0)] * 3)
+    off, peak, lb = _gpu_batch(binding, batch, max_trace_len=0)
+    assert off.shape == (0,) and peak.tolist() == [0, 0, 0] and lb.tolist() == [0, 0, 0]
+    batch = tg.concat([])
+    off, peak, lb = _gpu_batch(binding, batch, max_trace_len=0)
+    assert off.shape == (0,) and peak.shape == (0,)
