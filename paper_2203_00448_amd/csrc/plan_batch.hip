@@ -4,69 +4,186 @@
 // (size desc, first asc, id asc) and each is placed at the lowest offset that
 // avoids the byte ranges of the already placed tensors whose lifetimes meet
 // its own.  Only lifetime-intersecting pairs interact, so the sequential
-// greedy is the same as evaluating each tensor once all of its
-// "predecessors" -- intersecting tensors of lower rank -- are placed.  This
-// kernel builds the predecessor lists in LDS and lets every lane place its
-// tensors as soon as their predecessors are final (a dataflow schedule whose
-// length is the depth of the predecessor DAG, not the tensor count).
+// greedy equals evaluating each tensor once all of its "predecessors" --
+// intersecting tensors of lower rank -- are placed.  The kernel builds the
+// predecessor lists in LDS and places tensors in a dataflow schedule whose
+// length is the depth of the predecessor DAG, not the tensor count.
 //
 // Positions q: the trace's tensors ordered by (first, id).  For q < q' the
 // pair intersects iff first[q'] <= last[q], so tensor q meets exactly the
 // positions (q, reach[q]) ahead of it, reach[q] = upper_bound(first, last[q]).
 // For such a pair q ranks before q' iff size[q] >= size[q'] (equal sizes are
-// ordered by first then id, which is position order) -- the rank comparison
-// needs no global sort.
+// ordered by first then id, which is position order).
+//
+// Phases (one workgroup of 512 threads):
+//   ingest + checks -> position order -> reach, band prefix, live-bytes deltas
+//   -> pair count (balanced over pairs) -> list starts -> list fill ->
+//   placement (dataflow: a tensor is fitted once its predecessors are placed)
+//   -> outputs.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
 namespace mp {
 
+#ifdef MP_PHASE_TIMING
+// Debug builds only: clock stamps of workgroup phases (thread 0), per trace.
+constexpr int kPhaseSlots = 8;
+__device__ long long g_phase_clock[4096 * kPhaseSlots];
+__device__ unsigned int g_dbg[4096 * 8];
+#define MP_DBG_MAX(slot, v) \
+    do { if (blockIdx.x < 4096) atomicMax(&g_dbg[blockIdx.x * 8 + (slot)], (unsigned)(v)); } while (0)
+#define MP_DBG_ADD(slot, v) \
+    do { if (blockIdx.x < 4096) atomicAdd(&g_dbg[blockIdx.x * 8 + (slot)], (unsigned)(v)); } while (0)
+#define MP_STAMP(slot)                                                              \
+    do {                                                                            \
+        if (threadIdx.x == 0 && blockIdx.x < 4096)                                  \
+            g_phase_clock[blockIdx.x * kPhaseSlots + (slot)] = clock64();           \
+    } while (0)
+#else
+#define MP_STAMP(slot) \
+    do {               \
+    } while (0)
+#define MP_DBG_MAX(slot, v) do { } while (0)
+#define MP_DBG_ADD(slot, v) do { } while (0)
+#endif
+#ifdef MP_PHASE_TIMING
+#define MP_DBG_DECL uint32_t dbg_iters = 0, dbg_chunks = 0, dbg_blocks = 0
+#define MP_DBG_ITER ++dbg_iters
+#define MP_DBG_CHUNK ++dbg_chunks
+#define MP_DBG_BLOCK ++dbg_blocks
+#define MP_DBG_FLUSH                  \
+    do {                              \
+        MP_DBG_MAX(0, dbg_iters);     \
+        MP_DBG_ADD(1, dbg_iters);     \
+        MP_DBG_ADD(2, dbg_chunks);    \
+        MP_DBG_ADD(4, dbg_blocks);    \
+    } while (0)
+#else
+#define MP_DBG_DECL do { } while (0)
+#define MP_DBG_ITER do { } while (0)
+#define MP_DBG_CHUNK do { } while (0)
+#define MP_DBG_BLOCK do { } while (0)
+#define MP_DBG_FLUSH do { } while (0)
+#endif
+
 namespace {
 
+constexpr int kBatchBlock = 512;
 constexpr uint32_t kIdleLimit = 1u << 22;  // idle polls without workgroup progress
+constexpr int kChunk = 8;                  // predecessors gathered per round trip
+constexpr uint32_t kMaxBackoff = 8;        // idle rounds sleep up to 8 x 128 cycles
+constexpr int kCoopSlots = 4;              // whole-wave fits take up to 4 x 64 predecessors
+constexpr uint32_t kCoopMax = 64u * kCoopSlots;
 
-// Lowest x >= 0 with [x, x+s) clear of every predecessor's [off, off+size).
-// Each move jumps past a range that overlaps the candidate window; no offset
-// skipped over can fit.  Circular scan: stop after a full lap without moves.
-__device__ __forceinline__ uint32_t fit_lowest(const uint16_t* preds, uint32_t pb, uint32_t pe,
-                                               const uint32_t* off, const uint32_t* sz,
-                                               uint32_t s) {
-    const uint32_t k = pe - pb;
-    uint32_t x = 0;
-    uint32_t c = pb, clean = 0;
-    while (clean < k) {
-        const uint32_t p = preds[c];
-        const uint32_t o = lds_poll(off + p);
-        const uint32_t e = o + sz[p];
-        if (o < x + s && x < e) {
-            x = e;
-            clean = 1;
-        } else {
-            ++clean;
-        }
-        if (++c == pe) c = pb;
+__device__ __forceinline__ uint64_t lds_poll64(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+__device__ __forceinline__ void lds_publish64(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+// A tensor's LDS word: offset (units) in the high half, size (units) in the
+// low half; the offset half is kUnplaced until the tensor is placed.
+__device__ __forceinline__ uint32_t word_off(uint64_t w) { return (uint32_t)(w >> 32); }
+__device__ __forceinline__ uint32_t word_end(uint64_t w) {
+    return (uint32_t)(w >> 32) + (uint32_t)w;
+}
+
+// Gather up to kChunk predecessor ranges [o, e) starting at list index c.
+// Slots past `end` read the tensor's own word (`self`) and get an empty
+// range that never blocks; the loads are issued unconditionally so that
+// they overlap.  Returns the slot of the first predecessor not placed yet,
+// or kChunk if all are placed.
+__device__ __forceinline__ int gather(const uint16_t* preds, uint32_t c, uint32_t end,
+                                      uint32_t self, const uint64_t* ofsz,
+                                      uint32_t (&o)[kChunk], uint32_t (&e)[kChunk]) {
+    uint32_t idx[kChunk];
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        const uint32_t v = preds[c + j];  // in bounds: the list area is padded
+        idx[j] = (c + j < end) ? v : self;
     }
-    return x;
+    uint64_t w[kChunk];
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) w[j] = lds_poll64(ofsz + idx[j]);
+    int blocked = kChunk;
+#pragma unroll
+    for (int j = kChunk - 1; j >= 0; --j) {
+        const bool live = c + j < end;
+        o[j] = live ? word_off(w[j]) : kUnplaced;
+        e[j] = live ? word_end(w[j]) : 0u;
+        if (live && o[j] == kUnplaced) blocked = j;
+    }
+    return blocked;
+}
+
+// Move x past every range in the chunk that overlaps [x, x + s); any offset
+// jumped over overlaps that range, so none of them can fit.  Returns true if
+// x moved.
+__device__ __forceinline__ bool bump(uint32_t& x, uint32_t s, const uint32_t (&o)[kChunk],
+                                     const uint32_t (&e)[kChunk]) {
+    bool moved = false;
+#pragma unroll
+    for (int j = 0; j < kChunk; ++j) {
+        if (o[j] < x + s && x < e[j]) {
+            x = e[j];
+            moved = true;
+        }
+    }
+    return moved;
+}
+
+// Maximum over the 64 lanes, returned to every lane: DPP row shifts build
+// row-wise prefix maxima, row broadcasts carry them across rows, lane 63
+// ends up with the total.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
 template <int BLOCK>
 __device__ void bitonic_sort_u64(uint64_t* keys, int m) {
     for (int k = 2; k <= m; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = threadIdx.x; i < m; i += BLOCK) {
-                const int ixj = i ^ j;
-                if (ixj > i) {
-                    const uint64_t a = keys[i], b = keys[ixj];
-                    const bool up = (i & k) == 0;
-                    if ((a > b) == up) {
-                        keys[i] = b;
-                        keys[ixj] = a;
-                    }
+            for (int i = threadIdx.x; i < (m >> 1); i += BLOCK) {
+                // i-th compare-exchange pair of this stage
+                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+                const int hi = lo | j;
+                const uint64_t a = keys[lo], b = keys[hi];
+                const bool up = (lo & k) == 0;
+                if ((a > b) == up) {
+                    keys[lo] = b;
+                    keys[hi] = a;
                 }
             }
             __syncthreads();
         }
     }
+}
+
+// Exclusive scan of a[0..n) in place (contiguous chunk per thread); a[n] =
+// total.  Returns the total.  Barriers inside.
+template <int BLOCK>
+__device__ uint32_t scan_exclusive_inplace(uint32_t* a, int n, uint32_t* scratch) {
+    const int chunk = (n + BLOCK - 1) / BLOCK;
+    const int a0 = min(n, (int)threadIdx.x * chunk), a1 = min(n, a0 + chunk);
+    uint32_t s = 0;
+    for (int i = a0; i < a1; ++i) s += a[i];
+    uint32_t total;
+    uint32_t run = block_exclusive_sum<BLOCK>(s, &total, scratch);
+    for (int i = a0; i < a1; ++i) {
+        const uint32_t v = a[i];
+        a[i] = run;
+        run += v;
+    }
+    if (threadIdx.x == 0) a[n] = total;
+    __syncthreads();
+    return total;
 }
 
 template <int BLOCK, int ITEMS>
@@ -80,19 +197,28 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     __shared__ uint64_t red[BLOCK / kWave];
     __shared__ uint32_t progress_count;
 
+    // LDS layout (N = cap_n tensor slots, P = cap_pairs list slots):
+    //   R0 [8N]     first[N]                     -> placement words ofsz[N]
+    //   R1 [4N]     size / unit
+    //   R2 [4N+4]   band lengths -> band starts (prefix)
+    //   R3 [4N+4]   live-bytes deltas -> predecessor counts -> fill cursors
+    //   R4 [4N+4]   predecessor list starts
+    //   R5 [2P]     predecessor lists (positions, u16)
+    //   R4+R5 hold the u64 sort keys of an unsorted trace before the lists.
     const size_t N = (size_t)cap_n;
-    uint32_t* sz = reinterpret_cast<uint32_t*>(smem);                  // [N] size / unit
-    int32_t* fst = reinterpret_cast<int32_t*>(smem + 4 * N);           // [N] first
-    uint32_t* off = reinterpret_cast<uint32_t*>(smem + 4 * N);         // [N] offset / unit (reuses fst)
-    int32_t* lst = reinterpret_cast<int32_t*>(smem + 8 * N);           // [N] last
-    uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + 12 * N);        // [N] pair counts, then cursors
-    uint32_t* pbeg = reinterpret_cast<uint32_t*>(smem + 16 * N);       // [N+1] list starts
-    uint32_t* diff = reinterpret_cast<uint32_t*>(smem + 20 * N + 4);   // [N+1] live-bytes deltas
-    uint16_t* preds = reinterpret_cast<uint16_t*>(smem + 24 * N + 8);  // [cap_pairs]
-    uint64_t* keys = reinterpret_cast<uint64_t*>(smem);                // unsorted traces only
+    int32_t* fst = reinterpret_cast<int32_t*>(smem);
+    uint64_t* ofsz = reinterpret_cast<uint64_t*>(smem);
+    uint32_t* sz = reinterpret_cast<uint32_t*>(smem + 8 * N);
+    uint32_t* bstart = reinterpret_cast<uint32_t*>(smem + 12 * N);
+    uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + 16 * N + 4);
+    uint32_t* pbeg = reinterpret_cast<uint32_t*>(smem + 20 * N + 8);
+    uint16_t* preds = reinterpret_cast<uint16_t*>(smem + 24 * N + 12);
+    uint64_t* keys = reinterpret_cast<uint64_t*>(smem + ((20 * N + 8 + 7) & ~(size_t)7));
+    uint32_t* scratch = reinterpret_cast<uint32_t*>(red);
 
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
+    MP_STAMP(0);
     const int64_t lo = begin[b], hi = begin[b + 1];
     const int32_t n_ops = num_ops[b];
     if (lo < 0 || hi < lo || hi > n_tensors || n_ops < 0 || hi - lo > cap_n) {
@@ -133,7 +259,7 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         const int i = tid + k * BLOCK;
         if (i > 0 && i < n && fst[i] < fst[i - 1]) flags |= 2u;
     }
-    flags = block_reduce<BLOCK>(flags, OpOr<uint32_t>(), reinterpret_cast<uint32_t*>(red));
+    flags = block_reduce<BLOCK>(flags, OpOr<uint32_t>(), scratch);
     const uint64_t or_all = block_reduce<BLOCK>(orv, OpOr<uint64_t>(), red);
     const uint64_t total = block_reduce<BLOCK>(sum, OpSatAdd(), red);
     {
@@ -144,6 +270,7 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
             return;
         }
     }
+    MP_STAMP(1);
     if (n == 0) {
         if (tid == 0) {
             peak_out[b] = 0;
@@ -158,9 +285,9 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     }
 
     // ---- position order (first, id); recorded traces are normally sorted already
+    int m = 1;
+    while (m < n) m <<= 1;
     if (flags & 2u) {
-        int m = 1;
-        while (m < n) m <<= 1;
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int i = tid + k * BLOCK;
@@ -185,157 +312,329 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
             }
         }
     }
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        if (q < n) {
-            sz[q] = (uint32_t)((uint64_t)s_r[k] >> sh);
-            fst[q] = f_r[k];
-            lst[q] = l_r[k];
-            cnt[q] = 0;
-            diff[q] = 0;
-        }
-    }
-    if (tid == 0) {
-        diff[n] = 0;
-        progress_count = 0;
-    }
-    __syncthreads();
-
-    // ---- intersecting pairs: count predecessors, live-bytes deltas
     uint32_t su_r[ITEMS];
-    int32_t reach_r[ITEMS];
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
         su_r[k] = 0;
-        reach_r[k] = 0;
         if (q < n) {
-            const uint32_t su = sz[q];
-            const int32_t l = lst[q];
-            int a = q + 1, z = n;  // every position <= q starts no later than l
+            su_r[k] = (uint32_t)((uint64_t)s_r[k] >> sh);
+            sz[q] = su_r[k];
+            fst[q] = f_r[k];
+            cnt[q] = 0;
+        }
+    }
+    if (tid == 0) {
+        cnt[n] = 0;
+        progress_count = 0;
+    }
+    __syncthreads();
+    MP_STAMP(2);
+
+    // ---- reach (galloping search), band lengths, live-bytes deltas
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+        const int q = tid + k * BLOCK;
+        if (q < n) {
+            const int32_t l = l_r[k];
+            int known = q, step = 1, probe = q + 1;  // first[known] <= l
+            while (probe < n && fst[probe] <= l) {
+                known = probe;
+                step <<= 1;
+                probe = q + step;
+            }
+            int a = known + 1, z = probe < n ? probe : n;
             while (a < z) {
                 const int mid = (a + z) >> 1;
                 if (fst[mid] <= l) a = mid + 1;
                 else z = mid;
             }
-            su_r[k] = su;
-            reach_r[k] = a;
-            atomicAdd(&diff[q], su);
-            atomicAdd(&diff[a], 0u - su);
-            uint32_t mine = 0;
-            for (int j = q + 1; j < a; ++j) {
-                if (su >= sz[j]) atomicAdd(&cnt[j], 1u);
-                else ++mine;
-            }
-            if (mine) atomicAdd(&cnt[q], mine);
+            bstart[q] = (uint32_t)(a - q - 1);
+            atomicAdd(&cnt[q], su_r[k]);
+            atomicAdd(&cnt[a], 0u - su_r[k]);
         }
     }
     __syncthreads();
 
-    // ---- scans: list starts (exclusive sum of counts) and max live bytes
+    // ---- prefix sums: band starts, max live bytes
+    const uint32_t n_band = scan_exclusive_inplace<BLOCK>(bstart, n, scratch);
     uint32_t live_max;
-    uint32_t n_pairs;
     {
         const int chunk = (n + BLOCK - 1) / BLOCK;
         const int a0 = min(n, tid * chunk), a1 = min(n, a0 + chunk);
-        uint32_t cs = 0, ds = 0;
-        for (int i = a0; i < a1; ++i) {
-            cs += cnt[i];
-            ds += diff[i];
-        }
+        uint32_t ds = 0;
+        for (int i = a0; i < a1; ++i) ds += cnt[i];
         uint32_t dtot;
-        uint32_t cpre = block_exclusive_sum<BLOCK>(cs, &n_pairs, reinterpret_cast<uint32_t*>(red));
-        uint32_t dpre = block_exclusive_sum<BLOCK>(ds, &dtot, reinterpret_cast<uint32_t*>(red));
+        uint32_t run = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
         uint32_t lm = 0;
         for (int i = a0; i < a1; ++i) {
-            const uint32_t c = cnt[i];
-            pbeg[i] = cpre;
-            cpre += c;
-            dpre += diff[i];
-            lm = lm > dpre ? lm : dpre;
+            run += cnt[i];
+            lm = lm > run ? lm : run;
         }
-        if (tid == 0) pbeg[n] = n_pairs;
-        live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), reinterpret_cast<uint32_t*>(red));
+        live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), scratch);
     }
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+        const int q = tid + k * BLOCK;
+        if (q < n) cnt[q] = 0;
+    }
+    __syncthreads();
+    MP_STAMP(3);
+
+    // ---- predecessor counts, balanced over the pairs: pair index p -> (q, j)
+    const uint32_t per = (n_band + BLOCK - 1) / BLOCK;
+    const uint32_t p_lo = min(n_band, (uint32_t)tid * per), p_hi = min(n_band, p_lo + per);
+    int q_lo = 0;  // last position whose band starts at or before p_lo
+    if (p_lo < p_hi) {
+        int a = 0, z = n;
+        while (a < z) {
+            const int mid = (a + z + 1) >> 1;
+            if (bstart[mid] <= p_lo) a = mid;
+            else z = mid - 1;
+        }
+        q_lo = a;
+    }
+    if (p_lo < p_hi) {
+        int q = q_lo;
+        uint32_t nxt = bstart[q + 1];
+        uint32_t sq = sz[q];
+        for (uint32_t p = p_lo; p < p_hi; ++p) {
+            while (nxt <= p) {
+                ++q;
+                nxt = bstart[q + 1];
+                sq = sz[q];
+            }
+            const int j = q + 1 + (int)(p - bstart[q]);
+            const int succ = (sq >= sz[j]) ? j : q;
+            atomicAdd(&cnt[succ], 1u);
+        }
+    }
+    __syncthreads();
+    const uint32_t n_pairs = scan_exclusive_inplace<BLOCK>(cnt, n, scratch);
     if (n_pairs > (uint32_t)cap_pairs) {
         if (tid == 0) raise_status(status, MP_ENOSPC);
         return;
     }
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        if (q < n) {
-            cnt[q] = pbeg[q];
-            off[q] = kUnplaced;
-        }
-    }
+    for (int i = tid; i <= n; i += BLOCK) pbeg[i] = cnt[i];
     __syncthreads();
+    MP_STAMP(4);
 
     // ---- predecessor lists
+    if (p_lo < p_hi) {
+        int q = q_lo;
+        uint32_t nxt = bstart[q + 1];
+        uint32_t sq = sz[q];
+        for (uint32_t p = p_lo; p < p_hi; ++p) {
+            while (nxt <= p) {
+                ++q;
+                nxt = bstart[q + 1];
+                sq = sz[q];
+            }
+            const int j = q + 1 + (int)(p - bstart[q]);
+            if (sq >= sz[j]) preds[atomicAdd(&cnt[j], 1u)] = (uint16_t)q;
+            else preds[atomicAdd(&cnt[q], 1u)] = (uint16_t)j;
+        }
+    }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
-        if (q < n) {
-            const uint32_t su = su_r[k];
-            const int a = reach_r[k];
-            for (int j = q + 1; j < a; ++j) {
-                if (su >= sz[j]) preds[atomicAdd(&cnt[j], 1u)] = (uint16_t)q;
-                else preds[atomicAdd(&cnt[q], 1u)] = (uint16_t)j;
-            }
-        }
+        if (q < n) ofsz[q] = ((uint64_t)kUnplaced << 32) | su_r[k];
     }
     __syncthreads();
+    MP_STAMP(5);
 
-    // ---- placement: each tensor as soon as all its predecessors are placed
+    // ---- placement: dataflow over the predecessor DAG.  Each lane owns the
+    // positions tid + k * BLOCK and works on one of them per round.  A round
+    // gathers the current tensor's predecessor words kChunk at a time (the
+    // loads of a chunk overlap): when one is not placed yet the tensor is
+    // parked on it and, in later rounds, only that word is polled; when all
+    // are placed the lowest fitting gap is found and published.  The polls of
+    // parked tensors are issued at the start of a round and consumed at the
+    // start of the next one, so they overlap the round's gathers.
     {
-        uint32_t cur_r[ITEMS];
-        uint32_t todo = 0;
+        uint32_t todo = 0, waitp[ITEMS], cursor[ITEMS], lpb[ITEMS], lpe[ITEMS];
+        uint64_t polled[ITEMS];
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
-            cur_r[k] = 0;
+            waitp[k] = kUnplaced;
+            cursor[k] = lpb[k] = lpe[k] = 0;
+            polled[k] = 0;
             if (q < n) {
                 todo |= 1u << k;
-                cur_r[k] = pbeg[q];
+                lpb[k] = cursor[k] = pbeg[q];
+                lpe[k] = pbeg[q + 1];
             }
         }
-        uint32_t seen = 0, idle = 0;
+        uint32_t seen = 0, idle = 0, backoff = 0;
         bool stuck = false;
-        while (todo) {
-            bool progress = false;
+        MP_DBG_DECL;
+        // The loop runs until every lane of the wave is done, so that all 64
+        // lanes take part in the whole-wave fits.
+        while (__ballot(todo != 0)) {
+            MP_DBG_ITER;
+            // consume last round's polls, issue this round's
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k)
+                if (word_off(polled[k]) != kUnplaced) waitp[k] = kUnplaced;
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k)
+                polled[k] = lds_poll64(ofsz + (waitp[k] != kUnplaced ? waitp[k] : 0u));
+            int cur = -1;
+#pragma unroll
+            for (int k = ITEMS - 1; k >= 0; --k)
+                if ((todo >> k & 1u) && waitp[k] == kUnplaced) cur = k;
+            bool progressed = false;
+            uint32_t c = 0, pb = 0, pe = 0;
 #pragma unroll
             for (int k = 0; k < ITEMS; ++k) {
-                if (todo & (1u << k)) {
-                    const int q = tid + k * BLOCK;
-                    const uint32_t pe = pbeg[q + 1];
-                    uint32_t c = cur_r[k];
-                    while (c < pe && lds_poll(off + preds[c]) != kUnplaced) ++c;
-                    cur_r[k] = c;
-                    if (c == pe) {
-                        lds_publish(off + q, fit_lowest(preds, pbeg[q], pe, off, sz, su_r[k]));
-                        todo &= ~(1u << k);
-                        progress = true;
+                if (k == cur) {
+                    c = cursor[k];
+                    pb = lpb[k];
+                    pe = lpe[k];
+                }
+            }
+            const uint32_t q = cur >= 0 ? tid + cur * BLOCK : 0u;
+            const uint32_t s = (uint32_t)ofsz[q];
+            const bool coop_item = cur >= 0 && pe - pb > (uint32_t)kChunk && pe - pb <= kCoopMax;
+            if (cur >= 0 && !coop_item) {
+                uint32_t o[kChunk], e[kChunk];
+                uint32_t blocker = kUnplaced;
+                int blocked = kChunk;
+                do {  // scan: advance over placed predecessors
+                    blocked = gather(preds, c, pe, q, ofsz, o, e);
+                    if (blocked < kChunk) {
+                        blocker = preds[c + blocked];
+                        if (pe - pb > (uint32_t)kChunk) c += blocked;  // short lists restart at pb
+                        break;
+                    }
+                    c += kChunk;
+                } while (c < pe);
+                if (blocker == kUnplaced) {
+                    uint32_t x = 0;
+                    if (pe - pb <= (uint32_t)kChunk) {
+                        while (bump(x, s, o, e)) {
+                        }
+                    } else {  // circular sweep over the chunks until a lap is clean
+                        const uint32_t nch = (pe - pb + kChunk - 1) / kChunk;
+                        uint32_t cc = pb, clean = 0;
+                        while (clean < nch) {
+                            gather(preds, cc, pe, q, ofsz, o, e);
+                            bool moved = false;
+                            while (bump(x, s, o, e)) moved = true;
+                            clean = moved ? 1u : clean + 1u;
+                            cc += kChunk;
+                            if (cc >= pe) cc = pb;
+                            MP_DBG_CHUNK;
+                        }
+                    }
+                    lds_publish64(ofsz + q, ((uint64_t)x << 32) | s);
+                    todo &= ~(1u << cur);
+                    progressed = true;
+                } else {
+                    MP_DBG_BLOCK;
+#pragma unroll
+                    for (int k = 0; k < ITEMS; ++k) {
+                        if (k == cur) {
+                            waitp[k] = blocker;
+                            cursor[k] = c;
+                            polled[k] = (uint64_t)kUnplaced << 32;  // the poll in flight is stale
+                        }
                     }
                 }
             }
-            if (progress) {
-                atomicAdd(&progress_count, 1u);
+            // whole-wave fits of long predecessor lists, one tensor at a time
+            uint64_t coop = __ballot(coop_item);
+            while (coop) {
+                const int L = __ffsll((long long)coop) - 1;
+                coop &= coop - 1;
+                const uint32_t uq = (uint32_t)__builtin_amdgcn_readlane((int)q, L);
+                const uint32_t upb = (uint32_t)__builtin_amdgcn_readlane((int)pb, L);
+                const uint32_t upe = (uint32_t)__builtin_amdgcn_readlane((int)pe, L);
+                const uint32_t us = (uint32_t)__builtin_amdgcn_readlane((int)s, L);
+                const uint32_t lane = tid & (kWave - 1);
+                uint32_t co[kCoopSlots], ce[kCoopSlots];
+                uint64_t w[kCoopSlots];
+#pragma unroll
+                for (int r = 0; r < kCoopSlots; ++r) {
+                    const uint32_t pos = upb + r * kWave + lane;
+                    const uint32_t v = preds[pos < upe ? pos : upb];
+                    w[r] = lds_poll64(ofsz + (pos < upe ? v : uq));
+                }
+                uint32_t blocker = kUnplaced;
+#pragma unroll
+                for (int r = kCoopSlots - 1; r >= 0; --r) {
+                    const uint32_t pos = upb + r * kWave + lane;
+                    const bool live = pos < upe;
+                    co[r] = live ? word_off(w[r]) : kUnplaced;
+                    ce[r] = live ? word_end(w[r]) : 0u;
+                    const uint64_t unplaced = __ballot(live && co[r] == kUnplaced);
+                    if (unplaced) blocker = upb + r * kWave + (__ffsll((long long)unplaced) - 1);
+                }
+                if (blocker != kUnplaced) {  // park the owner's tensor on that predecessor
+                    const uint32_t bq = preds[blocker];
+                    if ((int)lane == L) {
+#pragma unroll
+                        for (int k = 0; k < ITEMS; ++k) {
+                            if (k == cur) {
+                                waitp[k] = bq;
+                                polled[k] = (uint64_t)kUnplaced << 32;
+                            }
+                        }
+                    }
+                    MP_DBG_BLOCK;
+                } else {
+                    // move x to the highest end among the ranges overlapping
+                    // [x, x + s) until none overlaps
+                    uint32_t x = 0;
+                    while (true) {
+                        bool ov = false;
+                        uint32_t mx = 0;
+#pragma unroll
+                        for (int r = 0; r < kCoopSlots; ++r) {
+                            if (co[r] < x + us && x < ce[r]) {
+                                ov = true;
+                                mx = max(mx, ce[r]);
+                            }
+                        }
+                        if (!__ballot(ov)) break;
+                        x = wave_max_u32(mx);
+                        MP_DBG_CHUNK;
+                    }
+                    if ((int)lane == L) {
+                        lds_publish64(ofsz + uq, ((uint64_t)x << 32) | us);
+                        todo &= ~(1u << cur);
+                        progressed = true;
+                    }
+                }
+            }
+            const uint64_t any = __ballot(progressed);
+            if (any) {
+                if ((tid & (kWave - 1)) == __ffsll((long long)any) - 1)
+                    atomicAdd(&progress_count, 1u);
+                backoff = 0;
             } else {
                 const uint32_t now = lds_poll(&progress_count);
                 if (now != seen) {
                     seen = now;
                     idle = 0;
-                } else if (++idle > kIdleLimit) {
+                } else {
+                    ++idle;
+                }
+                if (__ballot(idle > kIdleLimit)) {
                     stuck = true;  // cannot happen for a valid predecessor DAG
                     break;
                 }
-                __builtin_amdgcn_s_sleep(1);
+                // an idle wave backs off so that busy waves get the SIMD
+                backoff = backoff < kMaxBackoff ? backoff + 1 : kMaxBackoff;
+                for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(2);
             }
         }
         if (stuck) raise_status(status, MP_EDEVICE);
+        MP_DBG_FLUSH;
     }
     __syncthreads();
+    MP_STAMP(6);
 
     // ---- outputs
     uint32_t pk = 0;
@@ -343,22 +642,21 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
         if (q < n) {
-            const uint32_t o = off[q];
-            offset_out[lo + id_r[k]] = (int64_t)((uint64_t)o << sh);
-            const uint32_t e = o + su_r[k];
+            const uint64_t w = ofsz[q];
+            offset_out[lo + id_r[k]] = (int64_t)((uint64_t)word_off(w) << sh);
+            const uint32_t e = word_end(w);
             pk = pk > e ? pk : e;
         }
     }
-    pk = block_reduce<BLOCK>(pk, OpMax<uint32_t>(), reinterpret_cast<uint32_t*>(red));
+    pk = block_reduce<BLOCK>(pk, OpMax<uint32_t>(), scratch);
     if (tid == 0) {
         peak_out[b] = (int64_t)((uint64_t)pk << sh);
         if (lb_out) lb_out[b] = (int64_t)((uint64_t)live_max << sh);
     }
+    MP_STAMP(7);
 }
 
 __global__ void reset_status_kernel(int32_t* status) { *status = MP_OK; }
-
-constexpr int kBatchBlock = 256;
 
 template <int ITEMS>
 hipError_t launch_items(const BatchArgs& a, int cap_n, int cap_pairs, size_t lds, hipStream_t st) {
@@ -374,25 +672,48 @@ hipError_t launch_items(const BatchArgs& a, int cap_n, int cap_pairs, size_t lds
 
 }  // namespace
 
+#ifdef MP_PHASE_TIMING
+extern "C" int32_t mp_debug_counters(unsigned* host_out, int64_t n, int reset) {
+    if (n > 4096 * 8) n = 4096 * 8;
+    if (reset) {
+        static unsigned zeros[4096 * 8];
+        return hipMemcpyToSymbol(HIP_SYMBOL(g_dbg), zeros, sizeof(zeros)) == hipSuccess ? MP_OK : MP_EDEVICE;
+    }
+    return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_dbg), n * sizeof(unsigned), 0,
+                               hipMemcpyDeviceToHost) == hipSuccess ? MP_OK : MP_EDEVICE;
+}
+extern "C" int32_t mp_debug_phase_clock(long long* host_out, int64_t n) {
+    if (n > 4096 * kPhaseSlots) n = 4096 * kPhaseSlots;
+    return hipMemcpyFromSymbol(host_out, HIP_SYMBOL(g_phase_clock), n * sizeof(long long), 0,
+                               hipMemcpyDeviceToHost) == hipSuccess
+               ? MP_OK
+               : MP_EDEVICE;
+}
+#endif
+
 hipError_t launch_reset_status(int32_t* status, hipStream_t st) {
     hipLaunchKernelGGL(reset_status_kernel, dim3(1), dim3(1), 0, st, status);
     return hipGetLastError();
 }
 
-// LDS bytes per workgroup: 24 per tensor slot + 8 + 2 per pair slot.  Traces
-// up to 2000 tensors get a budget that lets two workgroups share a CU's
-// 160 KiB of LDS.
+// LDS bytes per workgroup: 24 per tensor slot + 16 + 2 per pair slot.  Traces
+// up to about 2000 tensors get a budget that lets two workgroups share a CU's
+// 160 KiB of LDS.  The sort keys (8 bytes per power-of-two slot) must fit in
+// the last two regions.
 BatchShape batch_shape(int64_t max_trace_len) {
     BatchShape s{};
     if (max_trace_len < 0 || max_trace_len > MP_BATCH_MAX_TRACE_LEN) return s;
     const int64_t cap_n = max_trace_len < 1 ? 1 : max_trace_len;
-    const int64_t fixed = 24 * cap_n + 8;
+    const int64_t fixed = 24 * cap_n + 16;
     const int64_t budget = (fixed <= 48 * 1024) ? 78 * 1024 : 156 * 1024;
-    int64_t pairs = (budget - fixed) / 2;
+    int64_t pairs = (budget - fixed - 16) / 2;
     pairs &= ~(int64_t)7;
+    int64_t m = 1;
+    while (m < cap_n) m <<= 1;
+    if (4 * cap_n + 2 * pairs < 8 * m) return s;  // keys would not fit (never for <= 4096)
     s.cap_n = (int32_t)cap_n;
     s.cap_pairs = (int32_t)pairs;
-    s.lds_bytes = (size_t)(fixed + 2 * pairs);
+    s.lds_bytes = (size_t)(fixed + 2 * pairs + 16);  // list reads run up to 8 slots past the end
     int items = 1;
     while (items * kBatchBlock < cap_n) items <<= 1;
     s.items = items;
@@ -408,7 +729,6 @@ hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st) {
         case 2: return launch_items<2>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
         case 4: return launch_items<4>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
         case 8: return launch_items<8>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
-        case 16: return launch_items<16>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
         default: return hipErrorInvalidValue;
     }
 }

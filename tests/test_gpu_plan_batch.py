@@ -104,7 +104,7 @@ def test_deterministic_repeats():
 
 def _status(binding, batch, **kw):
     args = batch_to_device(batch)
-    status = torch.zeros(1, dtype=torch.int32, device="cuda")
+    status = binding.new_status()
     binding.plan_batch(*args, check=False, status=status, **kw)
     return int(status.item())
 
