@@ -96,6 +96,65 @@ int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num
  * (host query, no device work); -1 when max_trace_len is out of range. */
 int64_t mp_batch_pair_capacity(int64_t max_trace_len);
 
+/* Greedy-by-size plan of one trace of any length, using the whole device
+ * (one cooperative persistent launch places the tensors).
+ *   size, first, last [n] (int64, int32, int32), 0 <= n < 2^30.
+ *   offset_out[n] int64, peak_out: one device int64 (arena bytes).
+ *   policy: MP_LOWEST_FIT.
+ *   workspace: mp_workspace_size(MP_OP_PLAN_TRACE, n, num_ops, 0) bytes; its
+ *              contents need no initialisation.
+ * Capacity limits (MP_ENOSPC on device): the sum of the sizes divided by
+ * 2^ctz(OR of sizes) must be < 2^32, and a tensor may have at most 131072
+ * earlier-ranked lifetime-intersecting tensors.  Tensors need not be sorted
+ * by first. */
+int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
+                      int32_t num_ops, int32_t policy, int64_t* offset_out, int64_t* peak_out,
+                      void* workspace, size_t workspace_bytes, int32_t* status_out,
+                      void* stream);
+
+/* Workspace sizes (host query).  op: MP_OP_LIVE_BYTES (uses num_ops),
+ * MP_OP_VALIDATE (uses n_tensors and capacity), MP_OP_PLAN_TRACE (uses
+ * n_tensors and num_ops).  Returns 0 for an unknown op or negative sizes. */
+#define MP_OP_LIVE_BYTES 1
+#define MP_OP_VALIDATE 2
+#define MP_OP_PLAN_TRACE 3
+size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops, int64_t capacity);
+
+/* Per-op live bytes of one trace (the quantity whose maximum lower-bounds
+ * total_mem of Eq. 2.1: every tensor alive at an op needs its own bytes).
+ *   live_out[num_ops] int64: live_out[t] = sum of size[i] over first[i] <= t <= last[i].
+ *   max_live_out: one device int64, max over t (0 when num_ops == 0).
+ *   workspace: mp_workspace_size(MP_OP_LIVE_BYTES, n, num_ops, 0) bytes. */
+int32_t mp_live_bytes_profile(const int64_t* size, const int32_t* first, const int32_t* last,
+                              int64_t n, int32_t num_ops, int64_t* live_out,
+                              int64_t* max_live_out, void* workspace, size_t workspace_bytes,
+                              int32_t* status_out, void* stream);
+
+/* Plan validation against the pairwise constraints of Eq. 2.1: every pair
+ * i < j whose lifetimes intersect and whose byte ranges [offset, offset +
+ * size) overlap.
+ *   pairs_out[2 * capacity] int64: (i, j) pairs in lexicographic order; only
+ *                      the first `capacity` are written.
+ *   n_conflicts_out:   one device int64, always the exact number of pairs;
+ *                      MP_ENOSPC on the status word when it exceeds capacity.
+ *   workspace:         mp_workspace_size(MP_OP_VALIDATE, n, 0, capacity) bytes.
+ * Data errors (MP_EINVAL): size <= 0, first < 0, first > last, offset < 0,
+ * offset + size > INT64_MAX.  Tensors need not be sorted by first. */
+int32_t mp_validate_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                         const int64_t* offset, int64_t n, int64_t* pairs_out, int64_t capacity,
+                         int64_t* n_conflicts_out, void* workspace, size_t workspace_bytes,
+                         int32_t* status_out, void* stream);
+
+/* mp_validate_plan over a batch of independent traces (trace b = tensors
+ * [begin[b], begin[b+1]) with begin[0] == 0 and begin[n_traces] == n_tensors,
+ * checked on device).  Pairs use indices into the concatenated arrays; no
+ * pair crosses traces.  Workspace as for mp_validate_plan with n_tensors. */
+int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t* size,
+                          const int32_t* first, const int32_t* last, const int64_t* offset,
+                          int64_t n_tensors, int64_t* pairs_out, int64_t capacity,
+                          int64_t* n_conflicts_out, void* workspace, size_t workspace_bytes,
+                          int32_t* status_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

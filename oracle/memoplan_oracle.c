@@ -259,10 +259,13 @@ int32_t mpo_validate_plan(const int64_t* size, const int32_t* first, const int32
     if (!n_conflicts_out || capacity < 0) return MPO_EINVAL;
     if (capacity > 0 && !pairs_out) return MPO_EINVAL;
     if (n > 0 && !offset) return MPO_EINVAL;
-    int32_t st = check_trace(size, first, last, n, 0, 0);
-    if (st != MPO_OK) return st;
+    if (n < 0 || n > INT32_MAX || (n > 0 && (!size || !first || !last))) return MPO_EINVAL;
+    /* Each tensor's lifetime and byte range must be well formed; the sum of
+     * the sizes plays no part in checking a given plan. */
     for (int64_t i = 0; i < n; ++i)
-        if (offset[i] < 0 || offset[i] > INT64_MAX - size[i]) return MPO_EINVAL;
+        if (size[i] <= 0 || first[i] < 0 || first[i] > last[i] || offset[i] < 0 ||
+            offset[i] > INT64_MAX - size[i])
+            return MPO_EINVAL;
     int64_t count = 0;
     for (int64_t i = 0; i < n; ++i) {
         for (int64_t j = i + 1; j < n; ++j) {

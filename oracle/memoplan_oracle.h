@@ -62,6 +62,8 @@ int32_t mpo_live_bytes_profile(const int64_t* size, const int32_t* first, const 
 
 /* Every pair i < j whose lifetimes intersect and whose byte ranges
  * [offset, offset + size) overlap (the pairwise constraints of Eq. 2.1).
+ * Input errors (-1): size <= 0, first < 0, first > last, offset < 0,
+ * offset + size > INT64_MAX; the sum of the sizes is not checked here.
  * pairs_out[2k], pairs_out[2k+1] = (i, j) in lexicographic order; at most
  * `capacity` pairs are written; *n_conflicts_out is always the exact count and
  * the status is -2 when it exceeds capacity. */

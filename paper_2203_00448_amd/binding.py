@@ -15,6 +15,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
+OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE = 1, 2, 3
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
 
@@ -44,6 +45,16 @@ def load_library(path: str = LIB_PATH):
     L.mp_batch_pair_capacity.restype = i64
     L.mp_plan_batch.argtypes = [p, i64, p, p, p, p, i64, i64, i32, p, p, p, p, sz, p, p]
     L.mp_plan_batch.restype = i32
+    L.mp_workspace_size.argtypes = [i32, i64, i64, i64]
+    L.mp_workspace_size.restype = sz
+    L.mp_live_bytes_profile.argtypes = [p, p, p, i64, i32, p, p, p, sz, p, p]
+    L.mp_live_bytes_profile.restype = i32
+    L.mp_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p, p, sz, p, p]
+    L.mp_validate_plan.restype = i32
+    L.mp_validate_batch.argtypes = [p, i64, p, p, p, p, i64, p, i64, p, p, sz, p, p]
+    L.mp_validate_batch.restype = i32
+    L.mp_plan_trace.argtypes = [p, p, p, i64, i32, i32, p, p, p, sz, p, p]
+    L.mp_plan_trace.restype = i32
     _lib = L
     return L
 
@@ -132,3 +143,120 @@ def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None =
                          None, 0, _p(status), _stream(stream))
     _finish(rc, status, "plan_batch", check)
     return offset, peak, lb
+
+
+def workspace_size(op: int, n_tensors: int = 0, num_ops: int = 0, capacity: int = 0) -> int:
+    return int(load_library().mp_workspace_size(int(op), int(n_tensors), int(num_ops),
+                                                 int(capacity)))
+
+
+def _workspace(op, dev, n_tensors=0, num_ops=0, capacity=0, workspace=None):
+    need = workspace_size(op, n_tensors, num_ops, capacity)
+    if workspace is not None:
+        if workspace.numel() * workspace.element_size() < need:
+            raise ValueError(f"workspace needs {need} bytes")
+        return workspace, need
+    return torch.empty(max(need, 1), dtype=torch.uint8, device=dev), need
+
+
+def live_bytes_profile(size, first, last, num_ops: int, *, check: bool = True, out=None,
+                       status=None, workspace=None, stream=None):
+    """Per-op live bytes of one trace (mp_live_bytes_profile).
+    Returns (live int64[num_ops], max_live int64[1]) on the GPU."""
+    L = load_library()
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    n = size.numel()
+    dev = size.device
+    if out is None:
+        live = torch.empty(int(num_ops), dtype=torch.int64, device=dev)
+        mx = torch.empty(1, dtype=torch.int64, device=dev)
+    else:
+        live, mx = out
+    ws, need = _workspace(OP_LIVE_BYTES, dev, n, num_ops, 0, workspace)
+    if status is None:
+        status = new_status(dev, stream)
+    rc = L.mp_live_bytes_profile(_p(size), _p(first), _p(last), n, int(num_ops), _p(live), _p(mx),
+                                 _p(ws), need, _p(status), _stream(stream))
+    _finish(rc, status, "live_bytes_profile", check)
+    return live, mx
+
+
+def _validate(begin, size, first, last, offset, capacity, check, status, workspace, stream,
+              out=None):
+    L = load_library()
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    offset = _dev(offset, torch.int64, "offset")
+    n = size.numel()
+    dev = size.device
+    if capacity is None:
+        capacity = 1 << 20
+    if out is None:
+        pairs = torch.empty((int(capacity), 2), dtype=torch.int64, device=dev)
+        count = torch.empty(1, dtype=torch.int64, device=dev)
+    else:
+        pairs, count = out
+    ws, need = _workspace(OP_VALIDATE, dev, n, 0, capacity, workspace)
+    if status is None:
+        status = new_status(dev, stream)
+    if begin is None:
+        rc = L.mp_validate_plan(_p(size), _p(first), _p(last), _p(offset), n, _p(pairs),
+                                int(capacity), _p(count), _p(ws), need, _p(status),
+                                _stream(stream))
+    else:
+        begin = _dev(begin, torch.int64, "begin")
+        rc = L.mp_validate_batch(_p(begin), begin.numel() - 1, _p(size), _p(first), _p(last),
+                                 _p(offset), n, _p(pairs), int(capacity), _p(count), _p(ws), need,
+                                 _p(status), _stream(stream))
+    if rc != MP_OK:
+        raise PlanError(rc, "validate")
+    if check:
+        st = int(status.item())
+        if st not in (MP_OK, MP_ENOSPC):
+            raise PlanError(st, "validate")
+        k = int(count.item())
+        return pairs[: min(k, int(capacity))], k, st
+    return pairs, count, status
+
+
+def validate_plan(size, first, last, offset, *, capacity: int | None = None, check: bool = True,
+                  status=None, workspace=None, stream=None, out=None):
+    """All lifetime-intersecting pairs whose byte ranges overlap (mp_validate_plan).
+    With check=True returns (pairs[k, 2] lexicographic, exact count k, status);
+    status is MP_ENOSPC when k exceeds capacity (only capacity pairs returned)."""
+    return _validate(None, size, first, last, offset, capacity, check, status, workspace, stream,
+                     out)
+
+
+def validate_batch(begin, size, first, last, offset, *, capacity: int | None = None,
+                   check: bool = True, status=None, workspace=None, stream=None, out=None):
+    """mp_validate_batch: like validate_plan over the traces begin[b]..begin[b+1]."""
+    return _validate(begin, size, first, last, offset, capacity, check, status, workspace, stream,
+                     out)
+
+
+def plan_trace(size, first, last, num_ops: int, *, policy: int = LOWEST_FIT, check: bool = True,
+               out=None, status=None, workspace=None, stream=None):
+    """Greedy-by-size plan of one trace on the whole device (mp_plan_trace).
+    Returns (offset int64[n], peak int64[1]) on the GPU."""
+    L = load_library()
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    n = size.numel()
+    dev = size.device
+    if out is None:
+        offset = torch.empty(n, dtype=torch.int64, device=dev)
+        peak = torch.empty(1, dtype=torch.int64, device=dev)
+    else:
+        offset, peak = out
+    ws, need = _workspace(OP_PLAN_TRACE, dev, n, num_ops, 0, workspace)
+    if status is None:
+        status = new_status(dev, stream)
+    rc = L.mp_plan_trace(_p(size), _p(first), _p(last), n, int(num_ops), int(policy), _p(offset),
+                         _p(peak), _p(ws), need, _p(status), _stream(stream))
+    _finish(rc, status, "plan_trace", check)
+    return offset, peak

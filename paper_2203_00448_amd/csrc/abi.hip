@@ -51,3 +51,83 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
                 n_tensors,  max_trace_len, offset_out, peak_out, lb_out, status_out};
     return launched(launch_plan_batch(a, st));
 }
+
+extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops,
+                                    int64_t capacity) {
+    if (n_tensors < 0 || num_ops < 0 || capacity < 0) return 0;
+    switch (op) {
+        case MP_OP_LIVE_BYTES:
+            return num_ops > INT32_MAX ? 0 : live_workspace_bytes((int32_t)num_ops);
+        case MP_OP_VALIDATE:
+            return validate_workspace_bytes(n_tensors, capacity);
+        case MP_OP_PLAN_TRACE:
+            return n_tensors >= (int64_t)1 << 30 ? 0 : plan_trace_workspace_bytes(n_tensors);
+        default:
+            return 0;
+    }
+}
+
+extern "C" int32_t mp_live_bytes_profile(const int64_t* size, const int32_t* first,
+                                         const int32_t* last, int64_t n, int32_t num_ops,
+                                         int64_t* live_out, int64_t* max_live_out, void* workspace,
+                                         size_t workspace_bytes, int32_t* status_out,
+                                         void* stream) {
+    if (n < 0 || num_ops < 0 || !status_out || !max_live_out || !workspace) return MP_EINVAL;
+    if (n > 0 && (!size || !first || !last)) return MP_EINVAL;
+    if (num_ops > 0 && !live_out) return MP_EINVAL;
+    if (workspace_bytes < live_workspace_bytes(num_ops)) return MP_EINVAL;
+    return launched(launch_live_profile(size, first, last, n, num_ops, live_out, max_live_out,
+                                        workspace, status_out, static_cast<hipStream_t>(stream)));
+}
+
+namespace {
+
+int32_t validate_common(const int64_t* begin, int64_t n_seg, const int64_t* size,
+                        const int32_t* first, const int32_t* last, const int64_t* offset,
+                        int64_t n, int64_t* pairs_out, int64_t capacity, int64_t* n_conflicts_out,
+                        void* workspace, size_t workspace_bytes, int32_t* status_out,
+                        void* stream) {
+    if (n < 0 || n > INT32_MAX - 1 || capacity < 0 || !status_out || !n_conflicts_out ||
+        !workspace)
+        return MP_EINVAL;
+    if (n > 0 && (!size || !first || !last || !offset)) return MP_EINVAL;
+    if (capacity > 0 && !pairs_out) return MP_EINVAL;
+    if (workspace_bytes < validate_workspace_bytes(n, capacity)) return MP_EINVAL;
+    return launched(launch_validate(begin, n_seg, size, first, last, offset, n, pairs_out,
+                                    capacity, n_conflicts_out, workspace, status_out,
+                                    static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" int32_t mp_validate_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                                    const int64_t* offset, int64_t n, int64_t* pairs_out,
+                                    int64_t capacity, int64_t* n_conflicts_out, void* workspace,
+                                    size_t workspace_bytes, int32_t* status_out, void* stream) {
+    return validate_common(nullptr, 1, size, first, last, offset, n, pairs_out, capacity,
+                           n_conflicts_out, workspace, workspace_bytes, status_out, stream);
+}
+
+extern "C" int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t* size,
+                                     const int32_t* first, const int32_t* last,
+                                     const int64_t* offset, int64_t n_tensors, int64_t* pairs_out,
+                                     int64_t capacity, int64_t* n_conflicts_out, void* workspace,
+                                     size_t workspace_bytes, int32_t* status_out, void* stream) {
+    if (!begin || n_traces < 1 || n_traces > INT32_MAX) return MP_EINVAL;
+    return validate_common(begin, n_traces, size, first, last, offset, n_tensors, pairs_out,
+                           capacity, n_conflicts_out, workspace, workspace_bytes, status_out,
+                           stream);
+}
+
+extern "C" int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                                 int64_t n, int32_t num_ops, int32_t policy, int64_t* offset_out,
+                                 int64_t* peak_out, void* workspace, size_t workspace_bytes,
+                                 int32_t* status_out, void* stream) {
+    if (n < 0 || n >= (int64_t)1 << 30 || num_ops < 0 || !status_out || !peak_out || !workspace)
+        return MP_EINVAL;
+    if (policy != MP_LOWEST_FIT) return MP_EINVAL;
+    if (n > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
+    if (workspace_bytes < plan_trace_workspace_bytes(n)) return MP_EINVAL;
+    return launched(launch_plan_trace(size, first, last, n, num_ops, offset_out, peak_out,
+                                      workspace, status_out, static_cast<hipStream_t>(stream)));
+}

@@ -37,3 +37,40 @@ hipError_t launch_reset_status(int32_t* status, hipStream_t st);
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st);
 
 }  // namespace mp
+
+namespace mp {
+
+// device-wide prefix sums (scan.hip)
+size_t scan_workspace_bytes(int64_t n);
+hipError_t device_scan_i64(int64_t* data, int64_t n, bool inclusive, int64_t* partial,
+                           unsigned long long* max_out, hipStream_t st,
+                           const uint32_t* skip = nullptr);
+
+// stable LSD radix sort of (u64 key, u32 value) pairs (radix.hip)
+size_t radix_workspace_bytes(int64_t n);
+hipError_t radix_sort_pairs(uint64_t* k0, uint32_t* v0, uint64_t* k1, uint32_t* v1, int64_t n,
+                            int begin_bit, int end_bit, void* ws, bool* in_alt, hipStream_t st,
+                            const uint32_t* skip = nullptr);
+
+// liveness profile (live.hip)
+size_t live_workspace_bytes(int32_t num_ops);
+hipError_t launch_live_profile(const int64_t* size, const int32_t* first, const int32_t* last,
+                               int64_t n, int32_t num_ops, int64_t* live_out, int64_t* max_out,
+                               void* ws, int32_t* status, hipStream_t st);
+
+
+// plan validation (validate.hip); begin == nullptr means one trace of n tensors
+size_t validate_workspace_bytes(int64_t n, int64_t capacity);
+hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* size,
+                           const int32_t* first, const int32_t* last, const int64_t* off,
+                           int64_t n, int64_t* pairs, int64_t cap, int64_t* n_out, void* ws,
+                           int32_t* status, hipStream_t st);
+
+
+// single-trace planner (plan_trace.hip)
+size_t plan_trace_workspace_bytes(int64_t n);
+hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                             int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out,
+                             void* ws, int32_t* status, hipStream_t st);
+
+}  // namespace mp

@@ -1,0 +1,644 @@
+// Greedy-by-size planner for one large trace, using the whole device.
+//
+// Same method as the batched planner (Section 2.3 greedy_by_size, the
+// planner of Section 3.2): tensors ranked by (size desc, first asc, id asc),
+// each put at the lowest offset clear of the already placed tensors whose
+// lifetimes meet its own.  For a single trace of up to millions of tensors
+// the work is spread over the device:
+//
+//   ingest     checks, common power-of-two unit of the sizes, sortedness
+//   positions  order by (first, id) -- a radix sort when not already sorted
+//   reach      reach[q] = first position after q born after q dies; the pair
+//              (q, j), q < j, intersects iff j < reach[q]
+//   long list  positions whose band (q, reach[q]) is longer than a threshold
+//              chosen from a histogram of band lengths, so that the other
+//              tensors meeting t from behind lie in a short window before t
+//   rank       stable radix sort by size descending over positions
+//   place      persistent kernel: workgroups take ranks from a counter.  For
+//              tensor t the workgroup walks t's candidates (forward band,
+//              backward window, long list), keeps those ranked before t,
+//              sorts the already placed ones by offset (LDS bitonic sort,
+//              prefix maxima of the ends), waits for the rest, and finds the
+//              lowest fitting gap.  A tensor only waits on lower ranks, which
+//              were taken earlier by running workgroups, so the schedule
+//              cannot deadlock.
+//   output     offsets (scaled back to bytes) and the peak.
+#include "internal.hpp"
+#include "mp_device.hpp"
+
+namespace mp {
+
+namespace {
+
+constexpr int kTBlock = 512;
+constexpr int kRunCap = 16384;    // ranges sorted at once in LDS
+constexpr int kDynCap = 1024;     // predecessors still unplaced when t is examined
+constexpr int64_t kScratchRuns = 8;  // global scratch per workgroup: 8 sorted runs
+constexpr uint32_t kUnplacedT = 0xFFFFFFFFu;
+constexpr int kLongMax = 4096;    // the long list is kept at most this long when possible
+
+struct TFlags {
+    uint32_t unsorted, sorted, abort, pad0;
+    uint64_t or_all, sum;
+    uint32_t shift, lthr, n_long, ticket;
+    uint32_t hist[64];      // band lengths by bit width
+    uint64_t peak;
+    int64_t long_prefix_tiles;
+};
+
+struct TView {  // position-ordered arrays
+    const int32_t* first;
+    const int32_t* last;
+    const uint32_t* id;  // null when the input was sorted
+};
+
+// ---------------------------------------------------------------- ingest
+
+__global__ void t_init_kernel(TFlags* fl) {
+    const int i = threadIdx.x;
+    if (i < 64) fl->hist[i] = 0;
+    if (i == 0) {
+        fl->unsorted = 0;
+        fl->sorted = 1;
+        fl->abort = 0;
+        fl->or_all = 0;
+        fl->sum = 0;
+        fl->shift = 0;
+        fl->lthr = 0;
+        fl->n_long = 0;
+        fl->ticket = 0;
+        fl->peak = 0;
+    }
+}
+
+__global__ __launch_bounds__(256) void t_ingest_kernel(const int64_t* __restrict__ size,
+                                                       const int32_t* __restrict__ first,
+                                                       const int32_t* __restrict__ last,
+                                                       int64_t n, int32_t num_ops, TFlags* fl,
+                                                       int32_t* __restrict__ status) {
+    __shared__ uint64_t red[256 / kWave];
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    uint32_t bad = 0, unsorted = 0;
+    uint64_t orv = 0, acc = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const int64_t s = size[i];
+        const int32_t f = first[i], l = last[i];
+        if (s <= 0 || f < 0 || f > l || l >= num_ops) bad = 1;
+        if (s > 0) {
+            orv |= (uint64_t)s;
+            acc = sat_add(acc, (uint64_t)s);
+        }
+        if (i + 1 < n && first[i + 1] < f) unsorted = 1;
+    }
+    bad = block_reduce<256>(bad, OpOr<uint32_t>(), reinterpret_cast<uint32_t*>(red));
+    unsorted = block_reduce<256>(unsorted, OpOr<uint32_t>(), reinterpret_cast<uint32_t*>(red));
+    orv = block_reduce<256>(orv, OpOr<uint64_t>(), red);
+    acc = block_reduce<256>(acc, OpSatAdd(), red);
+    if (threadIdx.x == 0) {
+        if (bad) {
+            raise_status(status, MP_EINVAL);
+            atomicOr(&fl->abort, 1u);
+        }
+        if (unsorted) {
+            atomicOr(&fl->unsorted, 1u);
+            atomicAnd(&fl->sorted, 0u);
+        }
+        atomicOr(reinterpret_cast<unsigned long long*>(&fl->or_all), (unsigned long long)orv);
+        const uint64_t old = atomicAdd(reinterpret_cast<unsigned long long*>(&fl->sum),
+                                       (unsigned long long)acc);
+        if (acc > (uint64_t)INT64_MAX || old > (uint64_t)INT64_MAX - acc) {
+            raise_status(status, MP_EOVERFLOW);
+            atomicOr(&fl->abort, 1u);
+        }
+    }
+}
+
+// unit shift; offsets are kept as 32-bit counts of the unit
+__global__ void t_unit_kernel(TFlags* fl, int32_t* status) {
+    if (fl->abort) return;
+    const uint64_t o = fl->or_all;
+    const uint32_t sh = o ? (uint32_t)__builtin_ctzll(o) : 0u;
+    fl->shift = sh;
+    if ((fl->sum >> sh) > 0xFFFFFFFEull) {
+        raise_status(status, MP_ENOSPC);
+        fl->abort = 1;
+    }
+}
+
+__global__ void t_keys_first_kernel(const int32_t* __restrict__ first, int64_t n,
+                                    uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                    const TFlags* fl) {
+    if (!fl->unsorted || fl->abort) return;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        keys[i] = (uint64_t)(uint32_t)first[i];
+        vals[i] = (uint32_t)i;
+    }
+}
+
+// positions: size in units, first/last in (first, id) order, ids
+__global__ void t_positions_kernel(const uint32_t* __restrict__ perm,
+                                   const int64_t* __restrict__ size,
+                                   const int32_t* __restrict__ first,
+                                   const int32_t* __restrict__ last, int64_t n,
+                                   uint32_t* __restrict__ su, int32_t* __restrict__ pf,
+                                   int32_t* __restrict__ pl, uint32_t* __restrict__ pid,
+                                   uint32_t* __restrict__ off, const TFlags* fl) {
+    if (fl->abort) return;
+    const bool uns = fl->unsorted != 0;
+    const uint32_t sh = fl->shift;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        const uint32_t i = uns ? perm[q] : (uint32_t)q;
+        su[q] = (uint32_t)((uint64_t)size[i] >> sh);
+        if (uns) {
+            pf[q] = first[i];
+            pl[q] = last[i];
+        }
+        pid[q] = i;
+        off[q] = kUnplacedT;
+    }
+}
+
+__device__ __forceinline__ TView view(const TFlags* fl, const int32_t* first, const int32_t* last,
+                                      const int32_t* pf, const int32_t* pl, const uint32_t* pid) {
+    if (fl->unsorted) return TView{pf, pl, pid};
+    return TView{first, last, nullptr};
+}
+
+__device__ __forceinline__ int32_t gallop_reach(const int32_t* f, int32_t q, int32_t n,
+                                                int32_t l) {
+    int64_t known = q, step = 1, probe = (int64_t)q + 1;
+    while (probe < n && f[probe] <= l) {
+        known = probe;
+        step <<= 1;
+        probe = ((int64_t)q + step < n) ? (int64_t)q + step : (int64_t)n;
+    }
+    int64_t a = known + 1, z = probe < n ? probe : (int64_t)n;
+    while (a < z) {
+        const int64_t mid = a + ((z - a) >> 1);
+        if (f[mid] <= l) a = mid + 1;
+        else z = mid;
+    }
+    return (int32_t)a;
+}
+
+__global__ void t_reach_kernel(const int32_t* first, const int32_t* last, const int32_t* pf,
+                               const int32_t* pl, const uint32_t* pid, int64_t n,
+                               int32_t* __restrict__ reach, TFlags* fl) {
+    if (fl->abort) return;
+    const TView v = view(fl, first, last, pf, pl, pid);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        const int32_t r = gallop_reach(v.first, (int32_t)q, (int32_t)n, v.last[q]);
+        reach[q] = r;
+        const uint32_t band = (uint32_t)(r - q - 1);
+        atomicAdd(&fl->hist[band ? 32 - __builtin_clz(band) : 0], 1u);
+    }
+}
+
+// threshold: smallest 2^b with at most kLongMax bands longer than it
+__global__ void t_threshold_kernel(TFlags* fl) {
+    if (fl->abort) return;
+    uint32_t above = 0;
+    int b = 33;
+    // bands of bit width w lie in [2^(w-1), 2^w); count from the top down
+    for (int w = 32; w >= 0; --w) {
+        if (above + fl->hist[w] > (uint32_t)kLongMax) break;
+        above += fl->hist[w];
+        b = w;
+    }
+    // bands with bit width >= b are long: band >= 2^(b-1)
+    fl->lthr = (b >= 33) ? 0xFFFFFFFFu : (b <= 1 ? 0u : (1u << (b - 1)) - 1u);
+}
+
+__global__ void t_long_flags_kernel(const int32_t* __restrict__ reach, int64_t n,
+                                    int64_t* __restrict__ flag, const TFlags* fl) {
+    if (fl->abort) return;
+    const uint32_t lthr = fl->lthr;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride)
+        flag[q] = ((uint32_t)(reach[q] - q - 1) > lthr) ? 1 : 0;
+}
+
+__global__ void t_long_list_kernel(const int32_t* __restrict__ reach,
+                                   const int64_t* __restrict__ pos, int64_t n,
+                                   int32_t* __restrict__ long_list, TFlags* fl) {
+    if (fl->abort) return;
+    const uint32_t lthr = fl->lthr;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        if ((uint32_t)(reach[q] - q - 1) > lthr) long_list[pos[q]] = (int32_t)q;
+        if (q == n - 1) fl->n_long = (uint32_t)(pos[q] + (((uint32_t)(reach[q] - q - 1) > lthr) ? 1 : 0));
+    }
+}
+
+__global__ void t_rank_keys_kernel(const uint32_t* __restrict__ su, int64_t n,
+                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                                   const TFlags* fl) {
+    if (fl->abort) return;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        keys[q] = (uint64_t)(0xFFFFFFFFu - su[q]);  // size descending; ties keep position order
+        vals[q] = (uint32_t)q;
+    }
+}
+
+// ---------------------------------------------------------------- placement
+
+// Offsets are published once and carry no other data, so device-coherent
+// relaxed accesses suffice (no acquire/release cache maintenance per load).
+__device__ __forceinline__ uint32_t agent_load(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void agent_store(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int BLOCK>
+__device__ void bitonic_sort_keys(uint64_t* keys, int m) {
+    for (int k = 2; k <= m; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = threadIdx.x; i < (m >> 1); i += BLOCK) {
+                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+                const int hi = lo | j;
+                const uint64_t a = keys[lo], b = keys[hi];
+                const bool up = (lo & k) == 0;
+                if ((a > b) == up) {
+                    keys[lo] = b;
+                    keys[hi] = a;
+                }
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// A run: byte ranges as keys (start << 32 | end) sorted ascending; after
+// sorting, the low half of key i is replaced by the maximum end of keys
+// 0..i.  The start of key i and the prefix maximum below it are all the
+// fit needs.
+__device__ __forceinline__ uint32_t run_start(uint64_t k) { return (uint32_t)(k >> 32); }
+__device__ __forceinline__ uint32_t run_pmax(uint64_t k) { return (uint32_t)k; }
+
+// Sort keys[0..m0) in LDS (padded to a power of two) and turn the low halves
+// into prefix maxima of the ends.  Contiguous chunk per thread for the scan.
+template <int BLOCK>
+__device__ void make_run(uint64_t* keys, int m0, uint32_t* scratch) {
+    int m = 1;
+    while (m < m0) m <<= 1;
+    for (int i = m0 + threadIdx.x; i < m; i += BLOCK) keys[i] = ~0ull;
+    __syncthreads();
+    bitonic_sort_keys<BLOCK>(keys, m);
+    const int chunk = (m0 + BLOCK - 1) / BLOCK;
+    const int a0 = min(m0, (int)threadIdx.x * chunk), a1 = min(m0, a0 + chunk);
+    uint32_t local = 0;
+    for (int i = a0; i < a1; ++i) local = max(local, (uint32_t)keys[i]);
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    uint32_t inc = local;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint32_t y = __shfl_up(inc, o, kWave);
+        if (lane >= o) inc = max(inc, y);
+    }
+    if (lane == kWave - 1) scratch[wid] = inc;
+    __syncthreads();
+    uint32_t run = 0;
+    for (int w = 0; w < wid; ++w) run = max(run, scratch[w]);
+    const uint32_t prev_lane = __shfl_up(inc, 1, kWave);
+    if (lane > 0) run = max(run, prev_lane);
+    for (int i = a0; i < a1; ++i) {
+        run = max(run, (uint32_t)keys[i]);
+        keys[i] = (keys[i] & 0xFFFFFFFF00000000ull) | run;
+    }
+    __syncthreads();
+}
+
+// Is [c, c + s) clear of every range of the run?  The ranges starting below
+// c + s are a prefix of the run; their highest end must not exceed c.
+__device__ __forceinline__ bool run_clear(const uint64_t* keys, int m, uint32_t c, uint32_t s) {
+    int a = 0, z = m;  // first key with start >= c + s
+    const uint32_t lim = c + s;
+    while (a < z) {
+        const int mid = (a + z) >> 1;
+        if (run_start(keys[mid]) < lim) a = mid + 1;
+        else z = mid;
+    }
+    return a == 0 || run_pmax(keys[a - 1]) <= c;
+}
+
+// Lowest offset clear of every run.  It is 0 or the end of some range; an
+// end that is clear of its own run is the prefix maximum just below a gap of
+// at least s in that run (or the run's top), so those gap starts, checked
+// against the other runs, are the only candidates.
+struct RunRef {
+    const uint64_t* keys;
+    int m;
+};
+
+template <int BLOCK, int MAXR>
+__device__ uint32_t fit_runs(const RunRef (&runs)[MAXR], int nr, uint32_t s, uint32_t* scratch) {
+    uint32_t best = 0xFFFFFFFFu;
+    for (int r = 0; r < nr; ++r) {
+        const uint64_t* k = runs[r].keys;
+        const int m = runs[r].m;
+        for (int i = threadIdx.x; i <= m; i += BLOCK) {
+            const uint32_t c = (i == 0) ? 0u : run_pmax(k[i - 1]);
+            if (c >= best) continue;
+            if (i < m && run_start(k[i]) < c + s) continue;  // no room in this run
+            bool ok = true;
+            for (int r2 = 0; r2 < nr && ok; ++r2)
+                if (r2 != r) ok = run_clear(runs[r2].keys, runs[r2].m, c, s);
+            if (ok) best = c;
+        }
+    }
+    return block_reduce<BLOCK>(best, OpMin<uint32_t>(), scratch);
+}
+
+struct PlaceArgs {
+    const uint32_t* su;
+    const int32_t* reach;
+    const uint32_t* order;
+    const int32_t* long_list;
+    uint32_t* off;
+    uint64_t* run_keys;  // per workgroup: kScratchRuns * kRunCap
+    int64_t n;
+    TFlags* fl;
+    int32_t* status;
+};
+
+// Visit the positions ranked before t whose lifetimes meet t's: the forward
+// band, the backward window of short bands and the long list.
+template <int BLOCK, typename F>
+__device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, uint32_t st,
+                                              uint32_t lthr, uint32_t n_long, F&& fn) {
+    const int32_t rt = a.reach[qt];
+    // forward band: meets t; ranked before t iff strictly larger
+    for (int32_t j = qt + 1 + threadIdx.x; j < rt; j += BLOCK)
+        if (a.su[j] > st) fn(j);
+    // backward window of short bands: ranked before t iff at least as large
+    const int64_t lo = (int64_t)qt - (int64_t)lthr - 1;
+    for (int64_t p = (lo > 0 ? lo : 0) + threadIdx.x; p < qt; p += BLOCK) {
+        const int32_t r = a.reach[p];
+        if ((uint32_t)(r - p - 1) <= lthr && r > qt && a.su[p] >= st) fn((int32_t)p);
+    }
+    // long bands that started before t
+    for (uint32_t k = threadIdx.x; k < n_long; k += BLOCK) {
+        const int32_t p = a.long_list[k];
+        if (p >= qt) continue;
+        if (a.reach[p] > qt && a.su[p] >= st) fn(p);
+    }
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
+    __shared__ uint64_t skeys[kRunCap];  // placed predecessors (one run)
+    __shared__ uint64_t dkeys[kDynCap];  // predecessors placed after t was examined
+    __shared__ uint32_t dpos[kDynCap];
+    __shared__ uint32_t scratch[BLOCK / kWave];
+    __shared__ uint32_t s_rank, s_nstat, s_ndyn;
+    if (a.fl->abort) return;
+    const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
+    uint64_t* gkeys = a.run_keys + (int64_t)blockIdx.x * kScratchRuns * kRunCap;
+    const int64_t stat_cap = kScratchRuns * (int64_t)kRunCap;
+    while (true) {
+        if (threadIdx.x == 0) {
+            s_rank = atomicAdd(&a.fl->ticket, 1u);
+            s_nstat = 0;
+            s_ndyn = 0;
+        }
+        __syncthreads();
+        const uint32_t r = s_rank;
+        if (r >= (uint32_t)a.n) break;
+        const int32_t qt = (int32_t)a.order[r];
+        const uint32_t st = a.su[qt];
+        // 1. collect: placed predecessors as keys, unplaced ones by position
+        //    (beyond kDynCap of those, wait for them right here)
+        for_each_pred<BLOCK>(a, qt, st, lthr, n_long, [&](int32_t p) {
+            uint32_t o = agent_load(a.off + p);
+            if (o == kUnplacedT) {
+                const uint32_t d = atomicAdd(&s_ndyn, 1u);
+                if (d < (uint32_t)kDynCap) {
+                    dpos[d] = (uint32_t)p;
+                    return;
+                }
+                while ((o = agent_load(a.off + p)) == kUnplacedT) __builtin_amdgcn_s_sleep(2);
+            }
+            const uint32_t k = atomicAdd(&s_nstat, 1u);
+            if (k < (uint32_t)stat_cap) gkeys[k] = ((uint64_t)o << 32) | (uint64_t)(o + a.su[p]);
+        });
+        __syncthreads();
+        const uint32_t nstat = s_nstat;
+        const int ndyn = (int)min(s_ndyn, (uint32_t)kDynCap);
+        if (nstat > (uint32_t)stat_cap) {
+            // predecessor set beyond the scratch capacity: report, and still
+            // publish an offset so that no later tensor waits forever
+            if (threadIdx.x == 0) {
+                raise_status(a.status, MP_ENOSPC);
+                agent_store(a.off + qt, 0u);
+            }
+            __syncthreads();
+            continue;
+        }
+        // 2. sorted runs of the placed predecessors: one in LDS when it fits,
+        //    else runs of kRunCap sorted in LDS and kept in global scratch
+        const int nruns = (int)((nstat + kRunCap - 1) / kRunCap);
+        if (nruns == 1) {
+            for (int i = threadIdx.x; i < (int)nstat; i += BLOCK) skeys[i] = gkeys[i];
+            __syncthreads();
+            make_run<BLOCK>(skeys, (int)nstat, scratch);
+        } else {
+            for (int run = 0; run < nruns; ++run) {
+                const int m0 = (int)min((uint32_t)kRunCap, nstat - (uint32_t)run * kRunCap);
+                uint64_t* g = gkeys + (int64_t)run * kRunCap;
+                for (int i = threadIdx.x; i < m0; i += BLOCK) skeys[i] = g[i];
+                __syncthreads();
+                make_run<BLOCK>(skeys, m0, scratch);
+                for (int i = threadIdx.x; i < m0; i += BLOCK) g[i] = skeys[i];
+                __syncthreads();
+            }
+        }
+        // 3. wait for the predecessors that were not placed yet; their ranges
+        //    form one more run
+        for (int d = threadIdx.x; d < ndyn; d += BLOCK) {
+            const uint32_t p = dpos[d];
+            uint32_t o;
+            while ((o = agent_load(a.off + p)) == kUnplacedT) __builtin_amdgcn_s_sleep(1);
+            dkeys[d] = ((uint64_t)o << 32) | (uint64_t)(o + a.su[p]);
+        }
+        __syncthreads();
+        if (ndyn) make_run<BLOCK>(dkeys, ndyn, scratch);
+        // 4. lowest offset clear of every run (one pass)
+        RunRef runs[kScratchRuns + 1];
+        int nr = 0;
+        if (nruns == 1) {
+            runs[nr++] = RunRef{skeys, (int)nstat};
+        } else {
+            for (int run = 0; run < nruns; ++run)
+                runs[nr++] = RunRef{gkeys + (int64_t)run * kRunCap,
+                                    (int)min((uint32_t)kRunCap, nstat - (uint32_t)run * kRunCap)};
+        }
+        if (ndyn) runs[nr++] = RunRef{dkeys, ndyn};
+        const uint32_t x = nr ? fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch) : 0u;
+        if (threadIdx.x == 0) agent_store(a.off + qt, x);
+        __syncthreads();
+    }
+}
+
+__global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restrict__ off,
+                                                       const uint32_t* __restrict__ su,
+                                                       const uint32_t* __restrict__ pid, int64_t n,
+                                                       int64_t* __restrict__ offset_out,
+                                                       TFlags* fl) {
+    __shared__ uint64_t red[256 / kWave];
+    if (fl->abort) return;
+    const uint32_t sh = fl->shift;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    uint64_t pk = 0;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        const uint64_t o = off[q];
+        offset_out[pid[q]] = (int64_t)(o << sh);
+        const uint64_t e = (o + su[q]) << sh;
+        pk = pk > e ? pk : e;
+    }
+    pk = block_reduce<256>(pk, OpMax<uint64_t>(), red);
+    if (threadIdx.x == 0 && pk)
+        atomicMax(reinterpret_cast<unsigned long long*>(&fl->peak), (unsigned long long)pk);
+}
+
+__global__ void t_peak_kernel(const TFlags* fl, int64_t* peak_out) { *peak_out = (int64_t)fl->peak; }
+
+struct TLayout {
+    size_t flags, su, pf, pl, pid, off, reach, keys0, vals0, keys1, vals1, radix, lflag, lpartial,
+        llist, run_keys, total;
+    unsigned grid;
+};
+
+unsigned place_grid() {
+    static unsigned cached = 0;
+    if (cached) return cached;
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, t_place_kernel<kTBlock>, kTBlock, 0) !=
+            hipSuccess ||
+        per < 1)
+        per = 1;
+    cached = (unsigned)(cus * per);
+    return cached;
+}
+
+TLayout t_layout(int64_t n, unsigned grid) {
+    TLayout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += (bytes + 255) & ~(size_t)255;
+        return at;
+    };
+    const int64_t nn = n > 0 ? n : 1;
+    L.flags = take(sizeof(TFlags));
+    L.su = take(nn * 4);
+    L.pf = take(nn * 4);
+    L.pl = take(nn * 4);
+    L.pid = take(nn * 4);
+    L.off = take(nn * 4);
+    L.reach = take(nn * 4);
+    L.keys0 = take(nn * 8);
+    L.vals0 = take(nn * 4);
+    L.keys1 = take(nn * 8);
+    L.vals1 = take(nn * 4);
+    L.radix = take(radix_workspace_bytes(nn));
+    L.lflag = take(nn * 8);
+    L.lpartial = take(scan_workspace_bytes(nn));
+    L.llist = take(nn * 4);
+    L.run_keys = take((size_t)grid * kScratchRuns * kRunCap * 8);
+    L.total = o;
+    L.grid = grid;
+    return L;
+}
+
+unsigned grid_n(int64_t n, int block) {
+    const int64_t g = (n + block - 1) / block;
+    return (unsigned)(g < 1 ? 1 : (g > 4096 ? 4096 : g));
+}
+
+}  // namespace
+
+size_t plan_trace_workspace_bytes(int64_t n) { return t_layout(n, place_grid()).total; }
+
+hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                             int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out,
+                             void* ws, int32_t* status, hipStream_t st) {
+    const TLayout L = t_layout(n, place_grid());
+    char* w = static_cast<char*>(ws);
+    TFlags* fl = reinterpret_cast<TFlags*>(w + L.flags);
+    uint32_t* su = reinterpret_cast<uint32_t*>(w + L.su);
+    int32_t* pf = reinterpret_cast<int32_t*>(w + L.pf);
+    int32_t* pl = reinterpret_cast<int32_t*>(w + L.pl);
+    uint32_t* pid = reinterpret_cast<uint32_t*>(w + L.pid);
+    uint32_t* off = reinterpret_cast<uint32_t*>(w + L.off);
+    int32_t* reach = reinterpret_cast<int32_t*>(w + L.reach);
+    uint64_t* keys0 = reinterpret_cast<uint64_t*>(w + L.keys0);
+    uint32_t* vals0 = reinterpret_cast<uint32_t*>(w + L.vals0);
+    uint64_t* keys1 = reinterpret_cast<uint64_t*>(w + L.keys1);
+    uint32_t* vals1 = reinterpret_cast<uint32_t*>(w + L.vals1);
+    void* rws = w + L.radix;
+    int64_t* lflag = reinterpret_cast<int64_t*>(w + L.lflag);
+    int64_t* lpartial = reinterpret_cast<int64_t*>(w + L.lpartial);
+    int32_t* llist = reinterpret_cast<int32_t*>(w + L.llist);
+
+    hipLaunchKernelGGL(t_init_kernel, dim3(1), dim3(64), 0, st, fl);
+    if (n == 0) {
+        hipLaunchKernelGGL(t_peak_kernel, dim3(1), dim3(1), 0, st, (const TFlags*)fl, peak_out);
+        return hipGetLastError();
+    }
+    const unsigned g = grid_n(n, 256);
+    hipLaunchKernelGGL(t_ingest_kernel, dim3(g), dim3(256), 0, st, size, first, last, n, num_ops,
+                       fl, status);
+    hipLaunchKernelGGL(t_unit_kernel, dim3(1), dim3(1), 0, st, fl, status);
+    // position order (unsorted inputs only)
+    hipLaunchKernelGGL(t_keys_first_kernel, dim3(g), dim3(256), 0, st, first, n, keys0, vals0,
+                       (const TFlags*)fl);
+    bool alt = false;
+    hipError_t e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32, rws, &alt, st,
+                                    &fl->sorted);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(t_positions_kernel, dim3(g), dim3(256), 0, st,
+                       (const uint32_t*)(alt ? vals1 : vals0), size, first, last, n, su, pf, pl,
+                       pid, off, (const TFlags*)fl);
+    hipLaunchKernelGGL(t_reach_kernel, dim3(g), dim3(256), 0, st, first, last, (const int32_t*)pf,
+                       (const int32_t*)pl, (const uint32_t*)pid, n, reach, fl);
+    hipLaunchKernelGGL(t_threshold_kernel, dim3(1), dim3(1), 0, st, fl);
+    hipLaunchKernelGGL(t_long_flags_kernel, dim3(g), dim3(256), 0, st, (const int32_t*)reach, n,
+                       lflag, (const TFlags*)fl);
+    e = device_scan_i64(lflag, n, false, lpartial, nullptr, st, &fl->abort);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(t_long_list_kernel, dim3(g), dim3(256), 0, st, (const int32_t*)reach,
+                       (const int64_t*)lflag, n, llist, fl);
+    // rank order: size descending, stable over positions
+    hipLaunchKernelGGL(t_rank_keys_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)su, n, keys0,
+                       vals0, (const TFlags*)fl);
+    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32, rws, &alt, st, &fl->abort);
+    if (e != hipSuccess) return e;
+    PlaceArgs pa{su,
+                 reach,
+                 alt ? vals1 : vals0,
+                 llist,
+                 off,
+                 reinterpret_cast<uint64_t*>(w + L.run_keys),
+                 n,
+                 fl,
+                 status};
+    void* kargs[] = {&pa};
+    e = hipLaunchCooperativeKernel((const void*)t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock),
+                                   kargs, 0, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(t_output_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)off,
+                       (const uint32_t*)su, (const uint32_t*)pid, n, offset_out, fl);
+    hipLaunchKernelGGL(t_peak_kernel, dim3(1), dim3(1), 0, st, (const TFlags*)fl, peak_out);
+    return hipGetLastError();
+}
+
+}  // namespace mp

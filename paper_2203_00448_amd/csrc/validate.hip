@@ -1,0 +1,385 @@
+// Plan validation: every pair of tensors whose lifetimes intersect and whose
+// byte ranges overlap (the pairwise ordering constraints of Eq. 2.1 state
+// that such a pair may not exist in a valid plan).
+//
+// Works on one trace or on a batch of contiguous traces (segments).  Tensors
+// are taken in position order (segment, first, id); for positions q < j of
+// one segment the lifetimes meet iff first[j] <= last[q], so row q's
+// candidates are the contiguous positions (q, reach[q]).  Short rows are
+// handled by one thread each, long rows by one workgroup each; a count pass,
+// a device-wide scan and a write pass put the pairs in (i, j) order.  When
+// the input is not already sorted by first inside each segment, positions
+// come from a radix sort and the written pairs are radix-sorted at the end.
+#include "internal.hpp"
+#include "mp_device.hpp"
+
+namespace mp {
+
+namespace {
+
+constexpr int kVBlock = 256;
+constexpr int32_t kShortRow = 64;  // longer rows go to the workgroup-per-row kernels
+constexpr unsigned kLongGrid = 1024;
+
+// Workspace words.
+struct VFlags {
+    uint32_t unsorted;  // some segment is not sorted by first
+    uint32_t sorted;    // == !unsorted (lets sort-path kernels skip themselves)
+    uint32_t n_long;    // rows longer than kShortRow
+    uint32_t pad;
+    int64_t begin1[2];  // {0, n} when the caller gives a single trace
+};
+
+struct VArrays {  // position-ordered views (inputs themselves when sorted)
+    const int32_t* first;
+    const int32_t* last;
+    const int64_t* off;
+    const int64_t* size;
+    const uint32_t* id;  // null when sorted: id == position
+};
+
+__device__ __forceinline__ VArrays pick_arrays(const VFlags* fl, const int32_t* first,
+                                               const int32_t* last, const int64_t* off,
+                                               const int64_t* size, const int32_t* pf,
+                                               const int32_t* pl, const int64_t* po,
+                                               const int64_t* ps, const uint32_t* pid) {
+    if (fl->unsorted) return VArrays{pf, pl, po, ps, pid};
+    return VArrays{first, last, off, size, nullptr};
+}
+
+__global__ void v_init_kernel(VFlags* fl, int64_t n) {
+    fl->unsorted = 0;
+    fl->sorted = 1;
+    fl->n_long = 0;
+    fl->begin1[0] = 0;
+    fl->begin1[1] = n;
+}
+
+// Segment end of every tensor, and checks of the segment table.
+__global__ void v_segend_kernel(const int64_t* __restrict__ begin, int64_t n_seg, int64_t n,
+                                int32_t* __restrict__ segend, int32_t* __restrict__ status) {
+    for (int64_t b = blockIdx.x; b < n_seg; b += gridDim.x) {
+        const int64_t lo = begin[b], hi = begin[b + 1];
+        if (lo < 0 || hi < lo || hi > n || (b == 0 && lo != 0) || (b == n_seg - 1 && hi != n)) {
+            if (threadIdx.x == 0) raise_status(status, MP_EINVAL);
+            continue;
+        }
+        for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) segend[i] = (int32_t)hi;
+    }
+}
+
+__global__ __launch_bounds__(kVBlock) void v_check_kernel(
+    const int64_t* __restrict__ size, const int32_t* __restrict__ first,
+    const int32_t* __restrict__ last, const int64_t* __restrict__ off, int64_t n,
+    const int32_t* __restrict__ segend, VFlags* fl, int32_t* __restrict__ status) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    bool bad = false, unsorted = false;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const int64_t s = size[i], o = off[i];
+        const int32_t f = first[i], l = last[i];
+        if (s <= 0 || f < 0 || f > l || o < 0 || o > INT64_MAX - s) bad = true;
+        if (i + 1 < n && i + 1 < segend[i] && first[i + 1] < f) unsorted = true;
+    }
+    if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) raise_status(status, MP_EINVAL);
+    if (__ballot(unsorted) && (threadIdx.x & (kWave - 1)) == 0) {
+        atomicOr(&fl->unsorted, 1u);
+        atomicAnd(&fl->sorted, 0u);
+    }
+}
+
+// Unsorted inputs only: sort keys (segment end, first) with the index.
+__global__ void v_keys_kernel(const int32_t* __restrict__ first, const int32_t* __restrict__ segend,
+                              int64_t n, uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+                              const VFlags* fl) {
+    if (!fl->unsorted) return;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        keys[i] = ((uint64_t)(uint32_t)segend[i] << 32) | (uint32_t)first[i];
+        vals[i] = (uint32_t)i;
+    }
+}
+
+__global__ void v_gather_kernel(const uint32_t* __restrict__ perm, const int64_t* __restrict__ size,
+                                const int32_t* __restrict__ first, const int32_t* __restrict__ last,
+                                const int64_t* __restrict__ off, int64_t n, int32_t* __restrict__ pf,
+                                int32_t* __restrict__ pl, int64_t* __restrict__ po,
+                                int64_t* __restrict__ ps, uint32_t* __restrict__ pid,
+                                const VFlags* fl) {
+    if (!fl->unsorted) return;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        const uint32_t i = perm[q];
+        pf[q] = first[i];
+        pl[q] = last[i];
+        po[q] = off[i];
+        ps[q] = size[i];
+        pid[q] = i;
+    }
+}
+
+// reach[q]: first position of q's segment after q whose first op is > last[q].
+__device__ __forceinline__ int32_t find_reach(const int32_t* f, int32_t q, int32_t end, int32_t l) {
+    int32_t known = q, step = 1, probe = q + 1;
+    while (probe < end && f[probe] <= l) {
+        known = probe;
+        step <<= 1;
+        probe = q + step;
+    }
+    int32_t a = known + 1, z = probe < end ? probe : end;
+    while (a < z) {
+        const int32_t mid = a + ((z - a) >> 1);
+        if (f[mid] <= l) a = mid + 1;
+        else z = mid;
+    }
+    return a;
+}
+
+__device__ __forceinline__ bool bytes_meet(int64_t oa, int64_t sa, int64_t ob, int64_t sb) {
+    return oa < ob + sb && ob < oa + sa;
+}
+
+__device__ __forceinline__ void put_pair(int64_t* pairs, int64_t pos, int64_t cap, const VArrays& a,
+                                         int64_t q, int64_t j) {
+    if (pos >= cap) return;
+    int64_t x = a.id ? (int64_t)a.id[q] : q, y = a.id ? (int64_t)a.id[j] : j;
+    if (x > y) {
+        const int64_t t = x;
+        x = y;
+        y = t;
+    }
+    pairs[2 * pos] = x;
+    pairs[2 * pos + 1] = y;
+}
+
+// Pass over short rows (one thread per row); long rows are queued.
+//   write == 0: cnt[q] = conflicts of row q, reach[q] stored
+//   write == 1: pairs of row q written from cnt[q] (now its start)
+__global__ __launch_bounds__(kVBlock) void v_rows_kernel(
+    const int32_t* first, const int32_t* last, const int64_t* off, const int64_t* size,
+    const int32_t* pf, const int32_t* pl, const int64_t* po, const int64_t* ps,
+    const uint32_t* pid, const int32_t* __restrict__ segend, int64_t n, int32_t* __restrict__ reach,
+    int64_t* __restrict__ cnt, int32_t* __restrict__ long_rows, VFlags* fl, int write,
+    int64_t* __restrict__ pairs, int64_t cap) {
+    const VArrays a = pick_arrays(fl, first, last, off, size, pf, pl, po, ps, pid);
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
+        int32_t r;
+        if (!write) {
+            // clamp the segment end so that a rejected segment table stays in bounds
+            int64_t end = segend[q];
+            end = end > n ? n : (end < q + 1 ? q + 1 : end);
+            r = find_reach(a.first, (int32_t)q, (int32_t)end, a.last[q]);
+            reach[q] = r;
+        } else {
+            r = reach[q];
+        }
+        const int64_t band = (int64_t)r - q - 1;
+        if (band > kShortRow) {
+            if (!write) {
+                cnt[q] = 0;
+                long_rows[atomicAdd(&fl->n_long, 1u)] = (int32_t)q;
+            }
+            continue;
+        }
+        const int64_t oq = a.off[q], sq = a.size[q];
+        int64_t pos = write ? cnt[q] : 0;
+        for (int64_t j = q + 1; j < r; ++j) {
+            if (bytes_meet(oq, sq, a.off[j], a.size[j])) {
+                if (write) put_pair(pairs, pos, cap, a, q, j);
+                ++pos;
+            }
+        }
+        if (!write) cnt[q] = pos;
+    }
+}
+
+// Long rows: one workgroup per row, candidates taken 256 at a time so that
+// the writes keep j order (exclusive scan of the hits of each round).
+__global__ __launch_bounds__(kVBlock) void v_long_kernel(
+    const int32_t* first, const int32_t* last, const int64_t* off, const int64_t* size,
+    const int32_t* pf, const int32_t* pl, const int64_t* po, const int64_t* ps,
+    const uint32_t* pid, const int32_t* __restrict__ reach, int64_t* __restrict__ cnt,
+    const int32_t* __restrict__ long_rows, VFlags* fl, int write, int64_t* __restrict__ pairs,
+    int64_t cap) {
+    __shared__ uint32_t scratch[kVBlock / kWave];
+    const VArrays a = pick_arrays(fl, first, last, off, size, pf, pl, po, ps, pid);
+    const uint32_t n_long = fl->n_long;
+    for (uint32_t k = blockIdx.x; k < n_long; k += gridDim.x) {
+        const int64_t q = long_rows[k];
+        const int64_t r = reach[q];
+        const int64_t oq = a.off[q], sq = a.size[q];
+        int64_t pos = write ? cnt[q] : 0;
+        for (int64_t j0 = q + 1; j0 < r; j0 += kVBlock) {
+            const int64_t j = j0 + threadIdx.x;
+            const bool hit = j < r && bytes_meet(oq, sq, a.off[j], a.size[j]);
+            uint32_t total;
+            const uint32_t before = block_exclusive_sum<kVBlock>(hit ? 1u : 0u, &total, scratch);
+            if (write && hit) put_pair(pairs, pos + before, cap, a, q, j);
+            pos += total;
+        }
+        if (!write && threadIdx.x == 0) cnt[q] = pos;
+    }
+}
+
+__global__ void v_total_kernel(const int64_t* __restrict__ partial, int64_t tiles, int64_t cap,
+                               int64_t* __restrict__ n_out, int32_t* __restrict__ status) {
+    const int64_t total = partial[tiles];
+    *n_out = total;
+    if (total > cap) raise_status(status, MP_ENOSPC);
+}
+
+// Unsorted inputs: pack the written pairs into sort keys (unused slots last).
+__global__ void v_pack_kernel(const int64_t* __restrict__ pairs, const int64_t* __restrict__ n_out,
+                              int64_t cap, uint64_t* __restrict__ keys, const VFlags* fl) {
+    if (!fl->unsorted) return;
+    const int64_t m = *n_out < cap ? *n_out : cap;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < cap; k += stride)
+        keys[k] = k < m ? (((uint64_t)pairs[2 * k] << 32) | (uint64_t)pairs[2 * k + 1]) : ~0ull;
+}
+
+__global__ void v_unpack_kernel(const uint64_t* __restrict__ keys, const int64_t* __restrict__ n_out,
+                                int64_t cap, int64_t* __restrict__ pairs, const VFlags* fl) {
+    if (!fl->unsorted) return;
+    const int64_t m = *n_out < cap ? *n_out : cap;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < m; k += stride) {
+        pairs[2 * k] = (int64_t)(keys[k] >> 32);
+        pairs[2 * k + 1] = (int64_t)(keys[k] & 0xFFFFFFFFu);
+    }
+}
+
+struct VLayout {
+    size_t flags, segend, reach, cnt, long_rows, keys0, vals0, keys1, vals1, pf, pl, po, ps, pid,
+        pk0, pk1, radix, total;
+};
+
+VLayout v_layout(int64_t n, int64_t cap) {
+    VLayout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o += (bytes + 255) & ~(size_t)255;
+        return at;
+    };
+    const int64_t nn = n > 0 ? n : 1;
+    L.flags = take(sizeof(VFlags));
+    L.segend = take(nn * 4);
+    L.reach = take(nn * 4);
+    L.cnt = take((nn + 1) * 8 + scan_workspace_bytes(nn + 1));
+    L.long_rows = take(nn * 4);
+    L.keys0 = take(nn * 8);
+    L.vals0 = take(nn * 4);
+    L.keys1 = take(nn * 8);
+    L.vals1 = take(nn * 4);
+    L.pf = take(nn * 4);
+    L.pl = take(nn * 4);
+    L.po = take(nn * 8);
+    L.ps = take(nn * 8);
+    L.pid = take(nn * 4);
+    const int64_t cc = cap > 0 ? cap : 1;
+    L.pk0 = take(cc * 8);
+    L.pk1 = take(cc * 8);
+    const size_t rad_n = radix_workspace_bytes(nn), rad_c = radix_workspace_bytes(cc);
+    L.radix = take(rad_n > rad_c ? rad_n : rad_c);
+    L.total = o;
+    return L;
+}
+
+unsigned grid_for(int64_t n, int block, unsigned cap) {
+    const int64_t g = (n + block - 1) / block;
+    return (unsigned)(g < 1 ? 1 : (g > cap ? cap : g));
+}
+
+}  // namespace
+
+size_t validate_workspace_bytes(int64_t n, int64_t capacity) { return v_layout(n, capacity).total; }
+
+hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* size,
+                           const int32_t* first, const int32_t* last, const int64_t* off,
+                           int64_t n, int64_t* pairs, int64_t cap, int64_t* n_out, void* ws,
+                           int32_t* status, hipStream_t st) {
+    const VLayout L = v_layout(n, cap);
+    char* w = static_cast<char*>(ws);
+    VFlags* fl = reinterpret_cast<VFlags*>(w + L.flags);
+    int32_t* segend = reinterpret_cast<int32_t*>(w + L.segend);
+    int32_t* reach = reinterpret_cast<int32_t*>(w + L.reach);
+    int64_t* cnt = reinterpret_cast<int64_t*>(w + L.cnt);
+    int64_t* cnt_partial = cnt + (n + 1);
+    int32_t* long_rows = reinterpret_cast<int32_t*>(w + L.long_rows);
+    uint64_t* keys0 = reinterpret_cast<uint64_t*>(w + L.keys0);
+    uint32_t* vals0 = reinterpret_cast<uint32_t*>(w + L.vals0);
+    uint64_t* keys1 = reinterpret_cast<uint64_t*>(w + L.keys1);
+    uint32_t* vals1 = reinterpret_cast<uint32_t*>(w + L.vals1);
+    int32_t* pf = reinterpret_cast<int32_t*>(w + L.pf);
+    int32_t* pl = reinterpret_cast<int32_t*>(w + L.pl);
+    int64_t* po = reinterpret_cast<int64_t*>(w + L.po);
+    int64_t* ps = reinterpret_cast<int64_t*>(w + L.ps);
+    uint32_t* pid = reinterpret_cast<uint32_t*>(w + L.pid);
+    uint64_t* pk0 = reinterpret_cast<uint64_t*>(w + L.pk0);
+    uint64_t* pk1 = reinterpret_cast<uint64_t*>(w + L.pk1);
+    void* rws = w + L.radix;
+
+    hipLaunchKernelGGL(v_init_kernel, dim3(1), dim3(1), 0, st, fl, n);
+    if (n == 0) {
+        hipLaunchKernelGGL(v_total_kernel, dim3(1), dim3(1), 0, st, (const int64_t*)&fl->begin1[0],
+                           (int64_t)0, cap, n_out, status);
+        return hipGetLastError();
+    }
+    const int64_t* seg = begin ? begin : fl->begin1;
+    const int64_t nseg = begin ? n_seg : 1;
+    hipLaunchKernelGGL(v_segend_kernel, dim3(grid_for(nseg, 1, 65535)), dim3(256), 0, st, seg, nseg,
+                       n, segend, status);
+    const unsigned g = grid_for(n, kVBlock, 4096);
+    hipLaunchKernelGGL(v_check_kernel, dim3(g), dim3(kVBlock), 0, st, size, first, last, off, n,
+                       (const int32_t*)segend, fl, status);
+    // position order for unsorted inputs (every kernel below skips itself otherwise)
+    hipLaunchKernelGGL(v_keys_kernel, dim3(g), dim3(kVBlock), 0, st, first, (const int32_t*)segend,
+                       n, keys0, vals0, (const VFlags*)fl);
+    int nbits = 1;
+    while (nbits < 31 && ((int64_t)1 << nbits) <= n) ++nbits;
+    bool alt = false;
+    hipError_t e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32 + nbits, rws, &alt, st,
+                                    &fl->sorted);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(v_gather_kernel, dim3(g), dim3(kVBlock), 0, st,
+                       (const uint32_t*)(alt ? vals1 : vals0), size, first, last, off, n, pf, pl,
+                       po, ps, pid, (const VFlags*)fl);
+    // count, scan, write
+    hipLaunchKernelGGL(v_rows_kernel, dim3(g), dim3(kVBlock), 0, st, first, last, off, size,
+                       (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
+                       (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)segend, n, reach,
+                       cnt, long_rows, fl, 0, pairs, cap);
+    hipLaunchKernelGGL(v_long_kernel, dim3(kLongGrid), dim3(kVBlock), 0, st, first, last, off, size,
+                       (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
+                       (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach, cnt,
+                       (const int32_t*)long_rows, fl, 0, pairs, cap);
+    e = device_scan_i64(cnt, n, false, cnt_partial, nullptr, st);
+    if (e != hipSuccess) return e;
+    const int64_t tiles = (int64_t)(scan_workspace_bytes(n) / sizeof(int64_t)) - 1;
+    hipLaunchKernelGGL(v_total_kernel, dim3(1), dim3(1), 0, st, (const int64_t*)cnt_partial, tiles,
+                       cap, n_out, status);
+    if (cap > 0) {
+        hipLaunchKernelGGL(v_rows_kernel, dim3(g), dim3(kVBlock), 0, st, first, last, off, size,
+                           (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
+                           (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)segend, n,
+                           reach, cnt, long_rows, fl, 1, pairs, cap);
+        hipLaunchKernelGGL(v_long_kernel, dim3(kLongGrid), dim3(kVBlock), 0, st, first, last, off,
+                           size, (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
+                           (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach, cnt,
+                           (const int32_t*)long_rows, fl, 1, pairs, cap);
+        // unsorted inputs: pairs were written in position order; sort them by (i, j)
+        const unsigned gc = grid_for(cap, kVBlock, 4096);
+        hipLaunchKernelGGL(v_pack_kernel, dim3(gc), dim3(kVBlock), 0, st, (const int64_t*)pairs,
+                           (const int64_t*)n_out, cap, pk0, (const VFlags*)fl);
+        bool palt = false;
+        e = radix_sort_pairs(pk0, nullptr, pk1, nullptr, cap, 0, 64, rws, &palt, st, &fl->sorted);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(v_unpack_kernel, dim3(gc), dim3(kVBlock), 0, st,
+                           (const uint64_t*)(palt ? pk1 : pk0), (const int64_t*)n_out, cap, pairs,
+                           (const VFlags*)fl);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mp

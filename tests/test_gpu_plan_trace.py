@@ -1,0 +1,123 @@
+"""Parity of the single-trace HIP planner (mp_plan_trace) with the CPU oracle.
+
+Offsets and the peak must match bit for bit.  The two largest traces use
+reference digests written by tests/golden/make_expected.py (oracle only)."""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import dev, host, need_gpu, torch
+from paper_2203_00448_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def _expected(name):
+    with open(os.path.join(HERE, "golden", "expected.json")) as fh:
+        return json.load(fh)["configs"][name]
+
+
+def _sha(a):
+    return hashlib.sha256(np.ascontiguousarray(a).astype("<i8").tobytes()).hexdigest()
+
+
+def _plan(binding, t, **kw):
+    off, peak = binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                                   dev(t.last, torch.int32), t.num_ops, **kw)
+    return host(off), int(peak.item())
+
+
+def _check(binding, t):
+    off, peak = _plan(binding, t)
+    eo, ep = oracle.plan_trace(t.size, t.first, t.last, t.num_ops)
+    bad = np.nonzero(off != eo)[0]
+    assert bad.size == 0, f"{bad.size} offsets differ, first at {bad[:5]}"
+    assert peak == ep
+
+
+def test_chain256():
+    binding = need_gpu()
+    print("case chain256", flush=True)
+    _check(binding, tg.chain256())
+
+
+def test_random_traces():
+    binding = need_gpu()
+    rng = np.random.default_rng(300)
+    print("case random traces", flush=True)
+    for k in range(24):
+        n = int(rng.choice([1, 2, 3, 40, 700, 5000]))
+        T = int(rng.integers(1, 2000))
+        alphabet = [64, 128, 192, 448, 4096] if k % 3 == 0 else None
+        t = tg.random_trace(rng, n, T, max_len=int(rng.integers(1, T + 1)), sizes=alphabet,
+                            sorted_first=(k % 2 == 0))
+        _check(binding, t)
+
+
+def test_adversarial_shapes():
+    binding = need_gpu()
+    rng = np.random.default_rng(301)
+    print("case full overlap beyond one LDS run", flush=True)
+    n = 9000  # up to 8999 predecessors: more than one sorted run of 8192
+    _check(binding, tg.Trace(64 * rng.integers(1, 200, n), np.zeros(n, np.int32),
+                             np.full(n, 3, np.int32), 4))
+    print("case equal sizes / long-lived / disjoint", flush=True)
+    _check(binding, tg.random_trace(rng, 6000, 3000, max_len=20, sizes=[320]))
+    t = tg.random_trace(rng, 8000, 4000, max_len=4, sorted_first=True)
+    t.last[::50] = 3999  # 160 long-lived tensors
+    _check(binding, t)
+    n = 3000
+    _check(binding, tg.Trace(64 * rng.integers(1, 50, n), np.arange(n, dtype=np.int32),
+                             np.arange(n, dtype=np.int32), n))
+
+
+def test_decode100k():
+    binding = need_gpu()
+    t = tg.decode100k()
+    exp = _expected("decode100k")
+    print("case decode100k", flush=True)
+    off, peak = _plan(binding, t)
+    assert peak == exp["peak"]
+    assert _sha(off) == exp["offsets_sha256"]
+    off2, _ = _plan(binding, t)
+    assert np.array_equal(off, off2)  # repeatable
+
+
+def test_ranking1m():
+    binding = need_gpu()
+    t = tg.ranking1m()
+    exp = _expected("ranking1m")
+    print("case ranking1m", flush=True)
+    off, peak = _plan(binding, t)
+    assert peak == exp["peak"]
+    assert _sha(off) == exp["offsets_sha256"]
+
+
+def test_status_codes_and_empty():
+    binding = need_gpu()
+    off, peak = _plan(binding, tg.Trace(np.zeros(0, np.int64), np.zeros(0, np.int32),
+                                        np.zeros(0, np.int32), 0))
+    assert off.shape == (0,) and peak == 0
+
+    def status(t):
+        st = binding.new_status()
+        binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                           dev(t.last, torch.int32), t.num_ops, check=False, status=st)
+        return int(st.item())
+
+    good = tg.chain256()
+    assert status(good) == binding.MP_OK
+    bad = tg.Trace(good.size.copy(), good.first.copy(), good.last.copy(), good.num_ops)
+    bad.size[9] = -5
+    assert status(bad) == binding.MP_EINVAL
+    big = tg.Trace(np.array([2 ** 62, 2 ** 62], np.int64), np.zeros(2, np.int32),
+                   np.zeros(2, np.int32), 1)
+    assert status(big) == binding.MP_EOVERFLOW
+    wide = tg.Trace(np.array([2 ** 31 + 1, 2 ** 31 + 1], np.int64), np.zeros(2, np.int32),
+                    np.zeros(2, np.int32), 1)
+    assert status(wide) == binding.MP_ENOSPC
