@@ -5,7 +5,8 @@ Workload: the batched ResNeXt-101-like traces -- 1024 independent traces of
 2000 tensors each (2,048,000 tensors), seeds [2, b] -- resident in HBM before
 timing.  One step plans every trace with greedy-by-size (lowest fitting gap),
 computes each trace's live-bytes lower bound, and validates the produced plan
-(every lifetime-intersecting pair checked for address overlap).
+(every lifetime-intersecting pair checked for address overlap; the step
+requires zero conflicts).
 
 Prints one JSON line: tensors planned per second, the roofline of the
 dominant kernel (the batched planner) from HIP events on its stream, and the
@@ -36,7 +37,28 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle (profiling runs)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="after the timed steps, copy 256 MiB device to device three times "
+                         "(a kernel of known traffic for scaling HBM counters)")
     return ap.parse_args()
+
+
+def measured_traffic():
+    """HBM bytes per launch of the planner kernel from the committed counter
+    summary, when it was taken on the current kernel source; else None."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "plan_batch_kernel_resnext_batch_hbm_counters.md")
+    src = os.path.join(ROOT, "paper_2203_00448_amd", "csrc", "plan_batch.hip")
+    try:
+        text = open(path).read()
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    fields = dict(line.split(": ", 1) for line in text.splitlines()
+                  if line.startswith(("traffic_bytes_per_launch:", "plan_batch_source_sha256:")))
+    if fields.get("plan_batch_source_sha256", "").strip() != sha:
+        return None
+    return int(fields["traffic_bytes_per_launch"])
 
 
 def cpu_baseline(batch):
@@ -77,6 +99,11 @@ def main():
     lb = torch.empty(n_traces, dtype=torch.int64, device="cuda")
     status = binding.new_status()
     stream = torch.cuda.current_stream()
+    cap = 1024
+    pairs = torch.empty((cap, 2), dtype=torch.int64, device="cuda")
+    n_conf = torch.empty(1, dtype=torch.int64, device="cuda")
+    vws = torch.empty(binding.workspace_size(binding.OP_VALIDATE, n, 0, cap), dtype=torch.uint8,
+                      device="cuda")
 
     def step(ev=None):
         if ev is not None:
@@ -85,11 +112,16 @@ def main():
                            out=(offset, peak, lb), status=status, stream=stream)
         if ev is not None:
             ev[1].record(stream)
+        binding.validate_batch(begin, size, first, last, offset, capacity=cap, check=False,
+                               status=status, workspace=vws, stream=stream, out=(pairs, n_conf),
+                               assume_sorted=True)
+        if ev is not None:
+            ev[2].record(stream)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    events = [tuple(torch.cuda.Event(enable_timing=True) for _ in range(3))
               for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -100,9 +132,12 @@ def main():
     st = int(status.item())
     if st != binding.MP_OK:
         raise SystemExit(f"device status {st}: {binding.status_string(st)}")
+    if int(n_conf.item()) != 0:
+        raise SystemExit(f"validation found {int(n_conf.item())} conflicting pairs")
 
     ms_per_step = (t1 - t0) * 1e3 / args.steps
-    kern_ms = [a.elapsed_time(b) for a, b in events]
+    kern_ms = [ev[0].elapsed_time(ev[1]) for ev in events]
+    val_ms = [ev[1].elapsed_time(ev[2]) for ev in events]
     kern_avg_ms = float(np.mean(kern_ms))
     algo_bytes = BYTES_PER_TENSOR * n + BYTES_PER_TRACE * n_traces
     achieved = algo_bytes / (kern_avg_ms * 1e-3) / 1e9
@@ -126,12 +161,21 @@ def main():
                                "(seeds [2,b]), greedy-by-size lowest fit",
                    "n_traces": n_traces, "tensors": n, "policy": "lowest_fit"},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(),
                      "kernel": "plan_batch_kernel", "kernel_avg_us": kern_avg_ms * 1e3,
                      "kernel_min_us": float(np.min(kern_ms)) * 1e3,
                      "algorithmic_bytes": algo_bytes},
         "peak_over_lb": {"mean": float(ratio.mean()), "max": float(ratio.max())},
+        "validate_us": float(np.mean(val_ms)) * 1e3,
+        "conflicts": int(n_conf.item()),
     }
+    if args.copy_calibration:
+        src = torch.empty(256 << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = 2 * src.numel()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(batch)
     print(json.dumps(out), flush=True)

@@ -137,13 +137,20 @@ int32_t mp_live_bytes_profile(const int64_t* size, const int32_t* first, const i
  *                      the first `capacity` are written.
  *   n_conflicts_out:   one device int64, always the exact number of pairs;
  *                      MP_ENOSPC on the status word when it exceeds capacity.
+ *   hints:             0 or MP_HINT_SORTED_FIRST (below).
  *   workspace:         mp_workspace_size(MP_OP_VALIDATE, n, 0, capacity) bytes.
  * Data errors (MP_EINVAL): size <= 0, first < 0, first > last, offset < 0,
  * offset + size > INT64_MAX.  Tensors need not be sorted by first. */
 int32_t mp_validate_plan(const int64_t* size, const int32_t* first, const int32_t* last,
                          const int64_t* offset, int64_t n, int64_t* pairs_out, int64_t capacity,
-                         int64_t* n_conflicts_out, void* workspace, size_t workspace_bytes,
-                         int32_t* status_out, void* stream);
+                         int64_t* n_conflicts_out, int32_t hints, void* workspace,
+                         size_t workspace_bytes, int32_t* status_out, void* stream);
+
+/* hints for the validation calls: MP_HINT_SORTED_FIRST promises that first
+ * is non-decreasing within every trace (recorded traces are, since tensors
+ * are numbered in allocation order).  The sorting kernels are then not
+ * enqueued; a broken promise is reported as MP_EINVAL. */
+#define MP_HINT_SORTED_FIRST 1
 
 /* mp_validate_plan over a batch of independent traces (trace b = tensors
  * [begin[b], begin[b+1]) with begin[0] == 0 and begin[n_traces] == n_tensors,
@@ -152,8 +159,8 @@ int32_t mp_validate_plan(const int64_t* size, const int32_t* first, const int32_
 int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t* size,
                           const int32_t* first, const int32_t* last, const int64_t* offset,
                           int64_t n_tensors, int64_t* pairs_out, int64_t capacity,
-                          int64_t* n_conflicts_out, void* workspace, size_t workspace_bytes,
-                          int32_t* status_out, void* stream);
+                          int64_t* n_conflicts_out, int32_t hints, void* workspace,
+                          size_t workspace_bytes, int32_t* status_out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
 OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE = 1, 2, 3
+HINT_SORTED_FIRST = 1
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
 
@@ -49,9 +50,9 @@ def load_library(path: str = LIB_PATH):
     L.mp_workspace_size.restype = sz
     L.mp_live_bytes_profile.argtypes = [p, p, p, i64, i32, p, p, p, sz, p, p]
     L.mp_live_bytes_profile.restype = i32
-    L.mp_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p, p, sz, p, p]
+    L.mp_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p, i32, p, sz, p, p]
     L.mp_validate_plan.restype = i32
-    L.mp_validate_batch.argtypes = [p, i64, p, p, p, p, i64, p, i64, p, p, sz, p, p]
+    L.mp_validate_batch.argtypes = [p, i64, p, p, p, p, i64, p, i64, p, i32, p, sz, p, p]
     L.mp_validate_batch.restype = i32
     L.mp_plan_trace.argtypes = [p, p, p, i64, i32, i32, p, p, p, sz, p, p]
     L.mp_plan_trace.restype = i32
@@ -184,7 +185,7 @@ def live_bytes_profile(size, first, last, num_ops: int, *, check: bool = True, o
 
 
 def _validate(begin, size, first, last, offset, capacity, check, status, workspace, stream,
-              out=None):
+              out=None, assume_sorted=False):
     L = load_library()
     size = _dev(size, torch.int64, "size")
     first = _dev(first, torch.int32, "first")
@@ -202,15 +203,16 @@ def _validate(begin, size, first, last, offset, capacity, check, status, workspa
     ws, need = _workspace(OP_VALIDATE, dev, n, 0, capacity, workspace)
     if status is None:
         status = new_status(dev, stream)
+    hints = HINT_SORTED_FIRST if assume_sorted else 0
     if begin is None:
         rc = L.mp_validate_plan(_p(size), _p(first), _p(last), _p(offset), n, _p(pairs),
-                                int(capacity), _p(count), _p(ws), need, _p(status),
+                                int(capacity), _p(count), hints, _p(ws), need, _p(status),
                                 _stream(stream))
     else:
         begin = _dev(begin, torch.int64, "begin")
         rc = L.mp_validate_batch(_p(begin), begin.numel() - 1, _p(size), _p(first), _p(last),
-                                 _p(offset), n, _p(pairs), int(capacity), _p(count), _p(ws), need,
-                                 _p(status), _stream(stream))
+                                 _p(offset), n, _p(pairs), int(capacity), _p(count), hints,
+                                 _p(ws), need, _p(status), _stream(stream))
     if rc != MP_OK:
         raise PlanError(rc, "validate")
     if check:
@@ -223,19 +225,20 @@ def _validate(begin, size, first, last, offset, capacity, check, status, workspa
 
 
 def validate_plan(size, first, last, offset, *, capacity: int | None = None, check: bool = True,
-                  status=None, workspace=None, stream=None, out=None):
+                  status=None, workspace=None, stream=None, out=None, assume_sorted=False):
     """All lifetime-intersecting pairs whose byte ranges overlap (mp_validate_plan).
     With check=True returns (pairs[k, 2] lexicographic, exact count k, status);
     status is MP_ENOSPC when k exceeds capacity (only capacity pairs returned)."""
     return _validate(None, size, first, last, offset, capacity, check, status, workspace, stream,
-                     out)
+                     out, assume_sorted)
 
 
 def validate_batch(begin, size, first, last, offset, *, capacity: int | None = None,
-                   check: bool = True, status=None, workspace=None, stream=None, out=None):
+                   check: bool = True, status=None, workspace=None, stream=None, out=None,
+                   assume_sorted=False):
     """mp_validate_batch: like validate_plan over the traces begin[b]..begin[b+1]."""
     return _validate(begin, size, first, last, offset, capacity, check, status, workspace, stream,
-                     out)
+                     out, assume_sorted)
 
 
 def plan_trace(size, first, last, num_ops: int, *, policy: int = LOWEST_FIT, check: bool = True,

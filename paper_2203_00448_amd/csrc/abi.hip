@@ -85,38 +85,41 @@ namespace {
 int32_t validate_common(const int64_t* begin, int64_t n_seg, const int64_t* size,
                         const int32_t* first, const int32_t* last, const int64_t* offset,
                         int64_t n, int64_t* pairs_out, int64_t capacity, int64_t* n_conflicts_out,
-                        void* workspace, size_t workspace_bytes, int32_t* status_out,
-                        void* stream) {
+                        int32_t hints, void* workspace, size_t workspace_bytes,
+                        int32_t* status_out, void* stream) {
     if (n < 0 || n > INT32_MAX - 1 || capacity < 0 || !status_out || !n_conflicts_out ||
         !workspace)
         return MP_EINVAL;
     if (n > 0 && (!size || !first || !last || !offset)) return MP_EINVAL;
     if (capacity > 0 && !pairs_out) return MP_EINVAL;
+    if (hints & ~MP_HINT_SORTED_FIRST) return MP_EINVAL;
     if (workspace_bytes < validate_workspace_bytes(n, capacity)) return MP_EINVAL;
     return launched(launch_validate(begin, n_seg, size, first, last, offset, n, pairs_out,
-                                    capacity, n_conflicts_out, workspace, status_out,
-                                    static_cast<hipStream_t>(stream)));
+                                    capacity, n_conflicts_out, (hints & MP_HINT_SORTED_FIRST) != 0,
+                                    workspace, status_out, static_cast<hipStream_t>(stream)));
 }
 
 }  // namespace
 
 extern "C" int32_t mp_validate_plan(const int64_t* size, const int32_t* first, const int32_t* last,
                                     const int64_t* offset, int64_t n, int64_t* pairs_out,
-                                    int64_t capacity, int64_t* n_conflicts_out, void* workspace,
-                                    size_t workspace_bytes, int32_t* status_out, void* stream) {
+                                    int64_t capacity, int64_t* n_conflicts_out, int32_t hints,
+                                    void* workspace, size_t workspace_bytes, int32_t* status_out,
+                                    void* stream) {
     return validate_common(nullptr, 1, size, first, last, offset, n, pairs_out, capacity,
-                           n_conflicts_out, workspace, workspace_bytes, status_out, stream);
+                           n_conflicts_out, hints, workspace, workspace_bytes, status_out, stream);
 }
 
 extern "C" int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t* size,
                                      const int32_t* first, const int32_t* last,
                                      const int64_t* offset, int64_t n_tensors, int64_t* pairs_out,
-                                     int64_t capacity, int64_t* n_conflicts_out, void* workspace,
-                                     size_t workspace_bytes, int32_t* status_out, void* stream) {
+                                     int64_t capacity, int64_t* n_conflicts_out, int32_t hints,
+                                     void* workspace, size_t workspace_bytes, int32_t* status_out,
+                                     void* stream) {
     if (!begin || n_traces < 1 || n_traces > INT32_MAX) return MP_EINVAL;
     return validate_common(begin, n_traces, size, first, last, offset, n_tensors, pairs_out,
-                           capacity, n_conflicts_out, workspace, workspace_bytes, status_out,
-                           stream);
+                           capacity, n_conflicts_out, hints, workspace, workspace_bytes,
+                           status_out, stream);
 }
 
 extern "C" int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,

@@ -71,7 +71,8 @@ __global__ void v_segend_kernel(const int64_t* __restrict__ begin, int64_t n_seg
 __global__ __launch_bounds__(kVBlock) void v_check_kernel(
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, const int64_t* __restrict__ off, int64_t n,
-    const int32_t* __restrict__ segend, VFlags* fl, int32_t* __restrict__ status) {
+    const int32_t* __restrict__ segend, VFlags* fl, int32_t* __restrict__ status,
+    int assume_sorted) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     bool bad = false, unsorted = false;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
@@ -82,8 +83,12 @@ __global__ __launch_bounds__(kVBlock) void v_check_kernel(
     }
     if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) raise_status(status, MP_EINVAL);
     if (__ballot(unsorted) && (threadIdx.x & (kWave - 1)) == 0) {
-        atomicOr(&fl->unsorted, 1u);
-        atomicAnd(&fl->sorted, 0u);
+        if (assume_sorted) {  // broken promise: report, stay on the sorted path
+            raise_status(status, MP_EINVAL);
+        } else {
+            atomicOr(&fl->unsorted, 1u);
+            atomicAnd(&fl->sorted, 0u);
+        }
     }
 }
 
@@ -181,6 +186,7 @@ __global__ __launch_bounds__(kVBlock) void v_rows_kernel(
             }
             continue;
         }
+        if (write && (cnt[q + 1] == cnt[q] || cnt[q] >= cap)) continue;  // nothing to write
         const int64_t oq = a.off[q], sq = a.size[q];
         int64_t pos = write ? cnt[q] : 0;
         for (int64_t j = q + 1; j < r; ++j) {
@@ -222,9 +228,11 @@ __global__ __launch_bounds__(kVBlock) void v_long_kernel(
 }
 
 __global__ void v_total_kernel(const int64_t* __restrict__ partial, int64_t tiles, int64_t cap,
-                               int64_t* __restrict__ n_out, int32_t* __restrict__ status) {
+                               int64_t* __restrict__ n_out, int32_t* __restrict__ status,
+                               int64_t* __restrict__ cnt_end) {
     const int64_t total = partial[tiles];
     *n_out = total;
+    if (cnt_end) *cnt_end = total;  // row starts then bound every row: cnt[q + 1] - cnt[q]
     if (total > cap) raise_status(status, MP_ENOSPC);
 }
 
@@ -297,8 +305,8 @@ size_t validate_workspace_bytes(int64_t n, int64_t capacity) { return v_layout(n
 
 hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* size,
                            const int32_t* first, const int32_t* last, const int64_t* off,
-                           int64_t n, int64_t* pairs, int64_t cap, int64_t* n_out, void* ws,
-                           int32_t* status, hipStream_t st) {
+                           int64_t n, int64_t* pairs, int64_t cap, int64_t* n_out,
+                           bool assume_sorted, void* ws, int32_t* status, hipStream_t st) {
     const VLayout L = v_layout(n, cap);
     char* w = static_cast<char*>(ws);
     VFlags* fl = reinterpret_cast<VFlags*>(w + L.flags);
@@ -323,7 +331,7 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
     hipLaunchKernelGGL(v_init_kernel, dim3(1), dim3(1), 0, st, fl, n);
     if (n == 0) {
         hipLaunchKernelGGL(v_total_kernel, dim3(1), dim3(1), 0, st, (const int64_t*)&fl->begin1[0],
-                           (int64_t)0, cap, n_out, status);
+                           (int64_t)0, cap, n_out, status, (int64_t*)nullptr);
         return hipGetLastError();
     }
     const int64_t* seg = begin ? begin : fl->begin1;
@@ -332,19 +340,21 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
                        n, segend, status);
     const unsigned g = grid_for(n, kVBlock, 4096);
     hipLaunchKernelGGL(v_check_kernel, dim3(g), dim3(kVBlock), 0, st, size, first, last, off, n,
-                       (const int32_t*)segend, fl, status);
+                       (const int32_t*)segend, fl, status, assume_sorted ? 1 : 0);
+    hipError_t e = hipSuccess;
+    if (!assume_sorted) {
     // position order for unsorted inputs (every kernel below skips itself otherwise)
     hipLaunchKernelGGL(v_keys_kernel, dim3(g), dim3(kVBlock), 0, st, first, (const int32_t*)segend,
                        n, keys0, vals0, (const VFlags*)fl);
     int nbits = 1;
     while (nbits < 31 && ((int64_t)1 << nbits) <= n) ++nbits;
     bool alt = false;
-    hipError_t e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32 + nbits, rws, &alt, st,
-                                    &fl->sorted);
+    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32 + nbits, rws, &alt, st, &fl->sorted);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(v_gather_kernel, dim3(g), dim3(kVBlock), 0, st,
                        (const uint32_t*)(alt ? vals1 : vals0), size, first, last, off, n, pf, pl,
                        po, ps, pid, (const VFlags*)fl);
+    }
     // count, scan, write
     hipLaunchKernelGGL(v_rows_kernel, dim3(g), dim3(kVBlock), 0, st, first, last, off, size,
                        (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
@@ -358,7 +368,7 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
     if (e != hipSuccess) return e;
     const int64_t tiles = (int64_t)(scan_workspace_bytes(n) / sizeof(int64_t)) - 1;
     hipLaunchKernelGGL(v_total_kernel, dim3(1), dim3(1), 0, st, (const int64_t*)cnt_partial, tiles,
-                       cap, n_out, status);
+                       cap, n_out, status, cnt + n);
     if (cap > 0) {
         hipLaunchKernelGGL(v_rows_kernel, dim3(g), dim3(kVBlock), 0, st, first, last, off, size,
                            (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
@@ -369,6 +379,7 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
                            (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach, cnt,
                            (const int32_t*)long_rows, fl, 1, pairs, cap);
         // unsorted inputs: pairs were written in position order; sort them by (i, j)
+        if (assume_sorted) return hipGetLastError();
         const unsigned gc = grid_for(cap, kVBlock, 4096);
         hipLaunchKernelGGL(v_pack_kernel, dim3(gc), dim3(kVBlock), 0, st, (const int64_t*)pairs,
                            (const int64_t*)n_out, cap, pk0, (const VFlags*)fl);

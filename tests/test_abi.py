@@ -69,3 +69,26 @@ def test_pair_capacity(lib):
     assert lib.mp_batch_pair_capacity(4097) == -1
     assert lib.mp_batch_pair_capacity(2000) >= 12000   # the 2000-tensor traces need ~11K
     assert lib.mp_batch_pair_capacity(4096) > 0
+
+
+def test_other_host_checks(lib):
+    from paper_2203_00448_amd import binding as b
+    d = ctypes.c_void_p(16)
+    assert lib.mp_status_reset(None, None) == b.MP_EINVAL
+    # plan_trace: too many tensors, bad policy, short workspace
+    assert lib.mp_plan_trace(d, d, d, 1 << 30, 10, 0, d, d, d, 1 << 40, d, None) == b.MP_EINVAL
+    assert lib.mp_plan_trace(d, d, d, 10, 10, 3, d, d, d, 1 << 40, d, None) == b.MP_EINVAL
+    assert lib.mp_plan_trace(d, d, d, 10, 10, 0, d, d, d, 1, d, None) == b.MP_EINVAL
+    # validation: unknown hint bits, negative capacity, short workspace
+    assert lib.mp_validate_plan(d, d, d, d, 10, d, 4, d, 2, d, 1 << 40, d, None) == b.MP_EINVAL
+    assert lib.mp_validate_plan(d, d, d, d, 10, d, -1, d, 0, d, 1 << 40, d, None) == b.MP_EINVAL
+    assert lib.mp_validate_plan(d, d, d, d, 10, d, 4, d, 0, d, 8, d, None) == b.MP_EINVAL
+    assert lib.mp_validate_batch(None, 1, d, d, d, d, 10, d, 4, d, 0, d, 1 << 40, d, None) == b.MP_EINVAL
+    # liveness: short workspace, missing outputs
+    assert lib.mp_live_bytes_profile(d, d, d, 10, 10, d, d, d, 1, d, None) == b.MP_EINVAL
+    assert lib.mp_live_bytes_profile(d, d, d, 10, 10, None, d, d, 1 << 40, d, None) == b.MP_EINVAL
+    # workspace queries
+    assert lib.mp_workspace_size(99, 10, 10, 10) == 0
+    assert lib.mp_workspace_size(b.OP_VALIDATE, -1, 0, 0) == 0
+    assert lib.mp_workspace_size(b.OP_LIVE_BYTES, 0, 100, 0) > 0
+    assert lib.mp_workspace_size(b.OP_VALIDATE, 1000, 0, 100) > 0

@@ -184,3 +184,19 @@ def test_validate_status_codes():
     binding.validate_plan(*_trace_dev(t), dev(off, torch.int64), capacity=8, check=False,
                           status=st)
     assert int(st.item()) == binding.MP_EINVAL
+
+
+def test_validate_sorted_hint():
+    binding = need_gpu()
+    rng = np.random.default_rng(205)
+    t = tg.random_trace(rng, 3000, 500, max_len=10, sorted_first=True)
+    off = 64 * rng.integers(0, 20, t.n)
+    ep, ec = _oracle_pairs(t, off)
+    pairs, cnt, st = binding.validate_plan(*_trace_dev(t), dev(off, torch.int64), capacity=ec,
+                                           assume_sorted=True)
+    assert st == binding.MP_OK and cnt == ec and np.array_equal(host(pairs), ep)
+    u = tg.random_trace(rng, 500, 100, max_len=10, sorted_first=False)
+    st = binding.new_status()
+    binding.validate_plan(*_trace_dev(u), dev(np.zeros(u.n, np.int64), torch.int64),
+                          capacity=1 << 16, assume_sorted=True, check=False, status=st)
+    assert int(st.item()) == binding.MP_EINVAL  # promise broken
