@@ -47,6 +47,9 @@ __device__ unsigned int g_dbg[4096 * 8];
 #define MP_DBG_ADD(slot, v) do { } while (0)
 #endif
 #ifdef MP_PHASE_TIMING
+#define MP_CLK(v) long long v = clock64()
+#define MP_DBG_CLK_ADD(slot, a, b) \
+    do { MP_DBG_ADD(slot, (unsigned)(((b) - (a)) >> 4)); } while (0)
 #define MP_DBG_DECL uint32_t dbg_iters = 0, dbg_chunks = 0, dbg_blocks = 0
 #define MP_DBG_ITER ++dbg_iters
 #define MP_DBG_CHUNK ++dbg_chunks
@@ -59,6 +62,8 @@ __device__ unsigned int g_dbg[4096 * 8];
         MP_DBG_ADD(4, dbg_blocks);    \
     } while (0)
 #else
+#define MP_CLK(v) do { } while (0)
+#define MP_DBG_CLK_ADD(slot, a, b) do { } while (0)
 #define MP_DBG_DECL do { } while (0)
 #define MP_DBG_ITER do { } while (0)
 #define MP_DBG_CHUNK do { } while (0)
@@ -69,9 +74,7 @@ __device__ unsigned int g_dbg[4096 * 8];
 namespace {
 
 constexpr int kBatchBlock = 512;
-constexpr uint32_t kIdleLimit = 1u << 22;  // idle polls without workgroup progress
 constexpr int kChunk = 8;                  // predecessors gathered per round trip
-constexpr uint32_t kMaxBackoff = 8;        // idle rounds sleep up to 8 x 128 cycles
 constexpr int kCoopSlots = 4;              // whole-wave fits take up to 4 x 64 predecessors
 constexpr uint32_t kCoopMax = 64u * kCoopSlots;
 
@@ -195,7 +198,6 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint64_t red[BLOCK / kWave];
-    __shared__ uint32_t progress_count;
 
     // LDS layout (N = cap_n tensor slots, P = cap_pairs list slots):
     //   R0 [8N]     first[N]                     -> placement words ofsz[N]
@@ -324,10 +326,7 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
             cnt[q] = 0;
         }
     }
-    if (tid == 0) {
-        cnt[n] = 0;
-        progress_count = 0;
-    }
+    if (tid == 0) cnt[n] = 0;
     __syncthreads();
     MP_STAMP(2);
 
@@ -443,195 +442,208 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     __syncthreads();
     MP_STAMP(5);
 
-    // ---- placement: dataflow over the predecessor DAG.  Each lane owns the
-    // positions tid + k * BLOCK and works on one of them per round.  A round
-    // gathers the current tensor's predecessor words kChunk at a time (the
-    // loads of a chunk overlap): when one is not placed yet the tensor is
-    // parked on it and, in later rounds, only that word is polled; when all
-    // are placed the lowest fitting gap is found and published.  The polls of
-    // parked tensors are issued at the start of a round and consumed at the
-    // start of the next one, so they overlap the round's gathers.
+    // ---- placement in rounds.  A tensor can be placed once its predecessors
+    // are.  Round: (A) every thread looks at the tensors it owns (positions
+    // tid + k * BLOCK) that are not placed: a tensor whose remembered blocker
+    // is now placed (or that has none) is appended to a ready list -- short
+    // predecessor lists to one list, long ones to another; (B) the short
+    // ready tensors are spread one per thread: gather the predecessor words,
+    // remember the first unplaced one as the new blocker, or fit and publish;
+    // the long ready tensors are taken one per wave and handled by the whole
+    // wave.  Waves without work wait at the barrier instead of spinning.
+    // Every round places at least the lowest-ranked unplaced tensor.
     {
-        uint32_t todo = 0, waitp[ITEMS], cursor[ITEMS], lpb[ITEMS], lpe[ITEMS];
-        uint64_t polled[ITEMS];
+        uint16_t* waitp = reinterpret_cast<uint16_t*>(smem + 8 * N);       // R1
+        uint16_t* rsmall = reinterpret_cast<uint16_t*>(smem + 10 * N);     // R1
+        uint16_t* rbig = reinterpret_cast<uint16_t*>(smem + 12 * N);       // R2
+        uint32_t* cursor = reinterpret_cast<uint32_t*>(smem + 16 * N + 4);  // R3
+        __shared__ uint32_t n_small[2], n_big[2], n_placed;
+        constexpr uint16_t kNone = 0xFFFF;
+        uint32_t todo = 0;
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
-            waitp[k] = kUnplaced;
-            cursor[k] = lpb[k] = lpe[k] = 0;
-            polled[k] = 0;
             if (q < n) {
                 todo |= 1u << k;
-                lpb[k] = cursor[k] = pbeg[q];
-                lpe[k] = pbeg[q + 1];
+                waitp[q] = kNone;
+                cursor[q] = pbeg[q];
             }
         }
-        uint32_t seen = 0, idle = 0, backoff = 0;
-        bool stuck = false;
-        MP_DBG_DECL;
-        // The loop runs until every lane of the wave is done, so that all 64
-        // lanes take part in the whole-wave fits.
-        while (__ballot(todo != 0)) {
-            MP_DBG_ITER;
-            // consume last round's polls, issue this round's
-#pragma unroll
-            for (int k = 0; k < ITEMS; ++k)
-                if (word_off(polled[k]) != kUnplaced) waitp[k] = kUnplaced;
-#pragma unroll
-            for (int k = 0; k < ITEMS; ++k)
-                polled[k] = lds_poll64(ofsz + (waitp[k] != kUnplaced ? waitp[k] : 0u));
-            int cur = -1;
-#pragma unroll
-            for (int k = ITEMS - 1; k >= 0; --k)
-                if ((todo >> k & 1u) && waitp[k] == kUnplaced) cur = k;
-            bool progressed = false;
-            uint32_t c = 0, pb = 0, pe = 0;
+        if (tid == 0) {
+            n_small[0] = n_big[0] = n_small[1] = n_big[1] = 0;
+            n_placed = 0;
+        }
+        __syncthreads();
+        const int lane = tid & (kWave - 1), wid = tid / kWave;
+        constexpr int kWaves = BLOCK / kWave;
+        for (int round = 0;; ++round) {
+            const int par = round & 1;
+            MP_CLK(c0);
+            // (A) submit owned tensors whose blocker is gone
 #pragma unroll
             for (int k = 0; k < ITEMS; ++k) {
-                if (k == cur) {
-                    c = cursor[k];
-                    pb = lpb[k];
-                    pe = lpe[k];
+                if (!(todo >> k & 1u)) continue;
+                const uint32_t q = tid + k * BLOCK;
+                if (word_off(lds_poll64(ofsz + q)) != kUnplaced) {
+                    todo &= ~(1u << k);
+                    continue;
                 }
+                const uint16_t w = waitp[q];
+                if (w != kNone && word_off(lds_poll64(ofsz + w)) == kUnplaced) continue;
+                const uint32_t kp = pbeg[q + 1] - pbeg[q];
+                if (kp > (uint32_t)kChunk && kp <= kCoopMax)
+                    rbig[atomicAdd(&n_big[par], 1u)] = (uint16_t)q;
+                else
+                    rsmall[atomicAdd(&n_small[par], 1u)] = (uint16_t)q;
             }
-            const uint32_t q = cur >= 0 ? tid + cur * BLOCK : 0u;
-            const uint32_t s = (uint32_t)ofsz[q];
-            const bool coop_item = cur >= 0 && pe - pb > (uint32_t)kChunk && pe - pb <= kCoopMax;
-            if (cur >= 0 && !coop_item) {
+            MP_CLK(c1);
+            __syncthreads();
+            MP_CLK(c2);
+            const uint32_t ns = n_small[par], nb = n_big[par];
+            const uint32_t placed_before = n_placed;
+            if (tid == 0) n_small[par ^ 1] = n_big[par ^ 1] = 0;
+            if (tid == 0) {
+                MP_DBG_ADD(1, ns);
+                MP_DBG_ADD(2, nb);
+            }
+            if (placed_before >= (uint32_t)n) {
+                if (tid == 0) MP_DBG_MAX(0, round);
+                break;
+            }
+            if (round > n + 2) {  // cannot happen: every round places a tensor
+                if (tid == 0) raise_status(status, MP_EDEVICE);
+                break;
+            }
+            // (B1) short lists (and very long ones, chunk by chunk), one per thread
+            uint32_t mine = 0;
+            for (uint32_t i = tid; i < ns; i += BLOCK) {
+                const uint32_t q = rsmall[i];
+                const uint32_t pb = pbeg[q], pe = pbeg[q + 1];
+                const uint32_t s = (uint32_t)ofsz[q];
                 uint32_t o[kChunk], e[kChunk];
-                uint32_t blocker = kUnplaced;
-                int blocked = kChunk;
-                do {  // scan: advance over placed predecessors
-                    blocked = gather(preds, c, pe, q, ofsz, o, e);
-                    if (blocked < kChunk) {
-                        blocker = preds[c + blocked];
-                        if (pe - pb > (uint32_t)kChunk) c += blocked;  // short lists restart at pb
+                if (pe - pb <= (uint32_t)kChunk) {
+                    const int bl = gather(preds, pb, pe, q, ofsz, o, e);
+                    if (bl < kChunk) {
+                        // wait on the smallest unplaced predecessor: it ranks
+                        // last among them, so it is likely placed last
+                        int pick = bl;
+                        uint32_t best = e[bl] - o[bl];
+#pragma unroll
+                        for (int j = 0; j < kChunk; ++j) {
+                            const uint32_t sj = e[j] - o[j];
+                            if (pb + j < pe && o[j] == kUnplaced && sj <= best) {
+                                best = sj;
+                                pick = j;
+                            }
+                        }
+                        waitp[q] = preds[pb + pick];
+                        continue;
+                    }
+                    uint32_t x = 0;
+                    while (bump(x, s, o, e)) {
+                    }
+                    lds_publish64(ofsz + q, ((uint64_t)x << 32) | s);
+                    ++mine;
+                    continue;
+                }
+                uint32_t c = cursor[q];  // very long list: resume the scan
+                bool blocked = false;
+                while (c < pe) {
+                    const int bl = gather(preds, c, pe, q, ofsz, o, e);
+                    if (bl < kChunk) {
+                        waitp[q] = preds[c + bl];
+                        cursor[q] = c + bl;
+                        blocked = true;
                         break;
                     }
                     c += kChunk;
-                } while (c < pe);
-                if (blocker == kUnplaced) {
-                    uint32_t x = 0;
-                    if (pe - pb <= (uint32_t)kChunk) {
-                        while (bump(x, s, o, e)) {
-                        }
-                    } else {  // circular sweep over the chunks until a lap is clean
-                        const uint32_t nch = (pe - pb + kChunk - 1) / kChunk;
-                        uint32_t cc = pb, clean = 0;
-                        while (clean < nch) {
-                            gather(preds, cc, pe, q, ofsz, o, e);
-                            bool moved = false;
-                            while (bump(x, s, o, e)) moved = true;
-                            clean = moved ? 1u : clean + 1u;
-                            cc += kChunk;
-                            if (cc >= pe) cc = pb;
-                            MP_DBG_CHUNK;
-                        }
-                    }
-                    lds_publish64(ofsz + q, ((uint64_t)x << 32) | s);
-                    todo &= ~(1u << cur);
-                    progressed = true;
-                } else {
-                    MP_DBG_BLOCK;
-#pragma unroll
-                    for (int k = 0; k < ITEMS; ++k) {
-                        if (k == cur) {
-                            waitp[k] = blocker;
-                            cursor[k] = c;
-                            polled[k] = (uint64_t)kUnplaced << 32;  // the poll in flight is stale
-                        }
-                    }
                 }
+                if (blocked) continue;
+                const uint32_t nch = (pe - pb + kChunk - 1) / kChunk;
+                uint32_t x = 0, cc = pb, clean = 0;
+                while (clean < nch) {  // sweep the chunks until a full lap leaves x alone
+                    gather(preds, cc, pe, q, ofsz, o, e);
+                    bool moved = false;
+                    while (bump(x, s, o, e)) moved = true;
+                    clean = moved ? 1u : clean + 1u;
+                    cc += kChunk;
+                    if (cc >= pe) cc = pb;
+                }
+                lds_publish64(ofsz + q, ((uint64_t)x << 32) | s);
+                ++mine;
             }
-            // whole-wave fits of long predecessor lists, one tensor at a time
-            uint64_t coop = __ballot(coop_item);
-            while (coop) {
-                const int L = __ffsll((long long)coop) - 1;
-                coop &= coop - 1;
-                const uint32_t uq = (uint32_t)__builtin_amdgcn_readlane((int)q, L);
-                const uint32_t upb = (uint32_t)__builtin_amdgcn_readlane((int)pb, L);
-                const uint32_t upe = (uint32_t)__builtin_amdgcn_readlane((int)pe, L);
-                const uint32_t us = (uint32_t)__builtin_amdgcn_readlane((int)s, L);
-                const uint32_t lane = tid & (kWave - 1);
+            MP_CLK(c3);
+            // (B2) long lists: one tensor per wave, one predecessor per lane
+            // taken from the last wave down, since short ones fill the first waves
+            for (uint32_t j = wid; j < nb; j += kWaves) {
+                const uint32_t q = rbig[nb - 1 - j];
+                const uint32_t upb = pbeg[q], upe = pbeg[q + 1];
+                const uint32_t us = (uint32_t)ofsz[q];
+                const int slots = (int)((upe - upb + kWave - 1) / kWave);
                 uint32_t co[kCoopSlots], ce[kCoopSlots];
                 uint64_t w[kCoopSlots];
 #pragma unroll
                 for (int r = 0; r < kCoopSlots; ++r) {
                     const uint32_t pos = upb + r * kWave + lane;
-                    const uint32_t v = preds[pos < upe ? pos : upb];
-                    w[r] = lds_poll64(ofsz + (pos < upe ? v : uq));
+                    if (r < slots) {
+                        const uint32_t v = preds[pos < upe ? pos : upb];
+                        w[r] = lds_poll64(ofsz + (pos < upe ? v : q));
+                    } else {
+                        w[r] = 0;
+                    }
                 }
-                uint32_t blocker = kUnplaced;
+                // the smallest unplaced predecessor, if any, becomes the blocker
+                uint32_t minsz = 0xFFFFFFFFu, minpos = 0xFFFFFFFFu;
 #pragma unroll
-                for (int r = kCoopSlots - 1; r >= 0; --r) {
+                for (int r = 0; r < kCoopSlots; ++r) {
                     const uint32_t pos = upb + r * kWave + lane;
-                    const bool live = pos < upe;
+                    const bool live = r < slots && pos < upe;
                     co[r] = live ? word_off(w[r]) : kUnplaced;
                     ce[r] = live ? word_end(w[r]) : 0u;
-                    const uint64_t unplaced = __ballot(live && co[r] == kUnplaced);
-                    if (unplaced) blocker = upb + r * kWave + (__ffsll((long long)unplaced) - 1);
+                    if (live && co[r] == kUnplaced && (uint32_t)w[r] <= minsz) {
+                        minsz = (uint32_t)w[r];
+                        minpos = pos;
+                    }
                 }
-                if (blocker != kUnplaced) {  // park the owner's tensor on that predecessor
-                    const uint32_t bq = preds[blocker];
-                    if ((int)lane == L) {
+                const uint32_t wmin = ~wave_max_u32(~minsz);
+                if (wmin != 0xFFFFFFFFu) {
+                    const uint64_t holders = __ballot(minsz == wmin);
+                    const uint32_t pos = (uint32_t)__builtin_amdgcn_readlane(
+                        (int)minpos, __ffsll((long long)holders) - 1);
+                    if (lane == 0) waitp[q] = preds[pos];
+                    continue;
+                }
+                uint32_t x = 0;
+                while (true) {  // jump past the highest end overlapping [x, x + s)
+                    bool ov = false;
+                    uint32_t mx = 0;
 #pragma unroll
-                        for (int k = 0; k < ITEMS; ++k) {
-                            if (k == cur) {
-                                waitp[k] = bq;
-                                polled[k] = (uint64_t)kUnplaced << 32;
-                            }
+                    for (int r = 0; r < kCoopSlots; ++r) {
+                        if (co[r] < x + us && x < ce[r]) {
+                            ov = true;
+                            mx = max(mx, ce[r]);
                         }
                     }
-                    MP_DBG_BLOCK;
-                } else {
-                    // move x to the highest end among the ranges overlapping
-                    // [x, x + s) until none overlaps
-                    uint32_t x = 0;
-                    while (true) {
-                        bool ov = false;
-                        uint32_t mx = 0;
-#pragma unroll
-                        for (int r = 0; r < kCoopSlots; ++r) {
-                            if (co[r] < x + us && x < ce[r]) {
-                                ov = true;
-                                mx = max(mx, ce[r]);
-                            }
-                        }
-                        if (!__ballot(ov)) break;
-                        x = wave_max_u32(mx);
-                        MP_DBG_CHUNK;
-                    }
-                    if ((int)lane == L) {
-                        lds_publish64(ofsz + uq, ((uint64_t)x << 32) | us);
-                        todo &= ~(1u << cur);
-                        progressed = true;
-                    }
+                    if (!__ballot(ov)) break;
+                    x = wave_max_u32(mx);
+                }
+                if (lane == 0) {
+                    lds_publish64(ofsz + q, ((uint64_t)x << 32) | us);
+                    ++mine;
                 }
             }
-            const uint64_t any = __ballot(progressed);
-            if (any) {
-                if ((tid & (kWave - 1)) == __ffsll((long long)any) - 1)
-                    atomicAdd(&progress_count, 1u);
-                backoff = 0;
-            } else {
-                const uint32_t now = lds_poll(&progress_count);
-                if (now != seen) {
-                    seen = now;
-                    idle = 0;
-                } else {
-                    ++idle;
-                }
-                if (__ballot(idle > kIdleLimit)) {
-                    stuck = true;  // cannot happen for a valid predecessor DAG
-                    break;
-                }
-                // an idle wave backs off so that busy waves get the SIMD
-                backoff = backoff < kMaxBackoff ? backoff + 1 : kMaxBackoff;
-                for (uint32_t i = 0; i < backoff; ++i) __builtin_amdgcn_s_sleep(2);
+            if (mine) atomicAdd(&n_placed, mine);
+            MP_CLK(c4);
+            __syncthreads();
+            MP_CLK(c5);
+            if (tid == 0) {
+                MP_DBG_CLK_ADD(3, c0, c1);
+                MP_DBG_CLK_ADD(4, c1, c2);
+                MP_DBG_CLK_ADD(5, c2, c3);
+                MP_DBG_CLK_ADD(6, c4, c5);
             }
+            if (tid == 448) MP_DBG_CLK_ADD(7, c3, c4);
         }
-        if (stuck) raise_status(status, MP_EDEVICE);
-        MP_DBG_FLUSH;
     }
     __syncthreads();
     MP_STAMP(6);
