@@ -71,31 +71,32 @@ __device__ __forceinline__ T block_reduce(T v, Op op, T* scratch) {
     return r;
 }
 
-// Inclusive prefix sum across the 64 lanes of a wave.
-__device__ __forceinline__ uint32_t wave_inclusive_sum(uint32_t x) {
+// Inclusive prefix sum across the 64 lanes of a wave (unsigned 32 or 64 bit).
+template <typename T>
+__device__ __forceinline__ T wave_inclusive_sum(T x) {
     const int lane = threadIdx.x & (kWave - 1);
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) {
-        uint32_t y = __shfl_up(x, o, kWave);
+        T y = __shfl_up(x, o, kWave);
         if (lane >= o) x += y;
     }
     return x;
 }
 
 // Exclusive prefix of one value per thread over the workgroup (thread order);
-// returns the prefix, *total gets the sum.  `scratch` holds BLOCK/64 words.
-template <int BLOCK>
-__device__ __forceinline__ uint32_t block_exclusive_sum(uint32_t v, uint32_t* total,
-                                                        uint32_t* scratch) {
+// returns the prefix, *total gets the sum.  `scratch` holds BLOCK/64 values.
+// Contains two barriers.
+template <int BLOCK, typename T>
+__device__ __forceinline__ T block_exclusive_sum(T v, T* total, T* scratch) {
     const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-    uint32_t inc = wave_inclusive_sum(v);
+    T inc = wave_inclusive_sum(v);
     if (lane == kWave - 1) scratch[wid] = inc;
     __syncthreads();
-    uint32_t before = 0, all = 0;
+    T before = 0, all = 0;
 #pragma unroll
     for (int w = 0; w < BLOCK / kWave; ++w) {
-        uint32_t t = scratch[w];
-        before += (w < wid) ? t : 0u;
+        T t = scratch[w];
+        before += (w < wid) ? t : T(0);
         all += t;
     }
     __syncthreads();

@@ -5,20 +5,23 @@
 // avoids the byte ranges of the already placed tensors whose lifetimes meet
 // its own.  Only lifetime-intersecting pairs interact, so the sequential
 // greedy equals evaluating each tensor once all of its "predecessors" --
-// intersecting tensors of lower rank -- are placed.  The kernel builds the
-// predecessor lists in LDS and places tensors in a dataflow schedule whose
-// length is the depth of the predecessor DAG, not the tensor count.
+// intersecting tensors of lower rank -- are placed.  The kernel keeps every
+// intersecting pair once in LDS and places tensors in a dataflow schedule
+// whose length is the depth of the predecessor DAG, not the tensor count.
 //
 // Positions q: the trace's tensors ordered by (first, id).  For q < q' the
 // pair intersects iff first[q'] <= last[q], so tensor q meets exactly the
-// positions (q, reach[q]) ahead of it, reach[q] = upper_bound(first, last[q]).
-// For such a pair q ranks before q' iff size[q] >= size[q'] (equal sizes are
-// ordered by first then id, which is position order).
+// positions (q, reach[q]) to its right, reach[q] = upper_bound(first,
+// last[q]), and the positions to its left whose reach passes q (its "left
+// list").  For an intersecting pair q < q', q ranks first iff size[q] >=
+// size[q'] (equal sizes are ordered by first then id, which is position
+// order).
 //
 // Phases (one workgroup of 512 threads):
-//   ingest + checks -> position order -> reach, band prefix, live-bytes deltas
-//   -> pair count (balanced over pairs) -> list starts -> list fill ->
-//   placement (dataflow: a tensor is fitted once its predecessors are placed)
+//   ingest + checks -> position order -> reach, band lengths, live-bytes
+//   deltas, reach histogram -> one prefix pass (band starts, left-list starts,
+//   live-bytes maximum) -> left-list fill and predecessor counts -> placement
+//   in rounds (a tensor is fitted in the round after its last predecessor)
 //   -> outputs.
 #include "internal.hpp"
 #include "mp_device.hpp"
@@ -40,105 +43,40 @@ __device__ unsigned int g_dbg[4096 * 8];
             g_phase_clock[blockIdx.x * kPhaseSlots + (slot)] = clock64();           \
     } while (0)
 #else
-#define MP_STAMP(slot) \
-    do {               \
-    } while (0)
+#define MP_STAMP(slot) do { } while (0)
 #define MP_DBG_MAX(slot, v) do { } while (0)
 #define MP_DBG_ADD(slot, v) do { } while (0)
-#endif
-#ifdef MP_PHASE_TIMING
-#define MP_CLK(v) long long v = clock64()
-#define MP_DBG_CLK_ADD(slot, a, b) \
-    do { MP_DBG_ADD(slot, (unsigned)(((b) - (a)) >> 4)); } while (0)
-#define MP_DBG_DECL uint32_t dbg_iters = 0, dbg_chunks = 0, dbg_blocks = 0
-#define MP_DBG_ITER ++dbg_iters
-#define MP_DBG_CHUNK ++dbg_chunks
-#define MP_DBG_BLOCK ++dbg_blocks
-#define MP_DBG_FLUSH                  \
-    do {                              \
-        MP_DBG_MAX(0, dbg_iters);     \
-        MP_DBG_ADD(1, dbg_iters);     \
-        MP_DBG_ADD(2, dbg_chunks);    \
-        MP_DBG_ADD(4, dbg_blocks);    \
-    } while (0)
-#else
-#define MP_CLK(v) do { } while (0)
-#define MP_DBG_CLK_ADD(slot, a, b) do { } while (0)
-#define MP_DBG_DECL do { } while (0)
-#define MP_DBG_ITER do { } while (0)
-#define MP_DBG_CHUNK do { } while (0)
-#define MP_DBG_BLOCK do { } while (0)
-#define MP_DBG_FLUSH do { } while (0)
 #endif
 
 namespace {
 
 constexpr int kBatchBlock = 512;
-constexpr int kChunk = 8;                  // predecessors gathered per round trip
-constexpr int kCoopSlots = 4;              // whole-wave fits take up to 4 x 64 predecessors
-constexpr uint32_t kCoopMax = 64u * kCoopSlots;
-
-__device__ __forceinline__ uint64_t lds_poll64(const uint64_t* p) {
-    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
-__device__ __forceinline__ void lds_publish64(uint64_t* p, uint64_t v) {
-    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-}
+constexpr uint32_t kSmallK = 16;           // neighbours of a tensor fitted by a lane quad
+constexpr uint32_t kMidK = 64;             // ... by a 16-lane row; more: by the whole wave
+constexpr int kSlots = 4;                  // neighbours per lane in quads, rows and waves
+constexpr uint32_t kCoopChunk = 64u * kSlots;
+constexpr uint32_t kBigClass = 0x80000000u;  // pending-count flag: more than kSmallK neighbours
+constexpr uint32_t kCountMask = 0x7FFFFFFFu;
 
 // A tensor's LDS word: offset (units) in the high half, size (units) in the
-// low half; the offset half is kUnplaced until the tensor is placed.
+// low half; the offset half is kUnplaced until the tensor is placed.  An
+// unplaced word never overlaps a candidate range: offsets stay below
+// 0xFFFFFFFF because the sizes of a trace sum to at most 0xFFFFFFFE units.
 __device__ __forceinline__ uint32_t word_off(uint64_t w) { return (uint32_t)(w >> 32); }
 __device__ __forceinline__ uint32_t word_end(uint64_t w) {
     return (uint32_t)(w >> 32) + (uint32_t)w;
 }
 
-// Gather up to kChunk predecessor ranges [o, e) starting at list index c.
-// Slots past `end` read the tensor's own word (`self`) and get an empty
-// range that never blocks; the loads are issued unconditionally so that
-// they overlap.  Returns the slot of the first predecessor not placed yet,
-// or kChunk if all are placed.
-__device__ __forceinline__ int gather(const uint16_t* preds, uint32_t c, uint32_t end,
-                                      uint32_t self, const uint64_t* ofsz,
-                                      uint32_t (&o)[kChunk], uint32_t (&e)[kChunk]) {
-    uint32_t idx[kChunk];
-#pragma unroll
-    for (int j = 0; j < kChunk; ++j) {
-        const uint32_t v = preds[c + j];  // in bounds: the list area is padded
-        idx[j] = (c + j < end) ? v : self;
-    }
-    uint64_t w[kChunk];
-#pragma unroll
-    for (int j = 0; j < kChunk; ++j) w[j] = lds_poll64(ofsz + idx[j]);
-    int blocked = kChunk;
-#pragma unroll
-    for (int j = kChunk - 1; j >= 0; --j) {
-        const bool live = c + j < end;
-        o[j] = live ? word_off(w[j]) : kUnplaced;
-        e[j] = live ? word_end(w[j]) : 0u;
-        if (live && o[j] == kUnplaced) blocked = j;
-    }
-    return blocked;
-}
-
-// Move x past every range in the chunk that overlaps [x, x + s); any offset
-// jumped over overlaps that range, so none of them can fit.  Returns true if
-// x moved.
-__device__ __forceinline__ bool bump(uint32_t& x, uint32_t s, const uint32_t (&o)[kChunk],
-                                     const uint32_t (&e)[kChunk]) {
-    bool moved = false;
-#pragma unroll
-    for (int j = 0; j < kChunk; ++j) {
-        if (o[j] < x + s && x < e[j]) {
-            x = e[j];
-            moved = true;
-        }
-    }
-    return moved;
+// Neighbour q' of q ranks after q (a successor) iff it is smaller, or equal
+// in size and later in position order.
+__device__ __forceinline__ bool ranks_after(uint32_t s_other, uint32_t id_other, uint32_t s,
+                                            uint32_t q) {
+    return (s_other < s) | ((s_other == s) & (id_other > q));
 }
 
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
 // row-wise prefix maxima, row broadcasts carry them across rows, lane 63
-// ends up with the total.
+// ends up with the total.  All 64 lanes must be active.
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false));
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false));
@@ -147,6 +85,34 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false));
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false));
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+
+// Maximum over each quad of lanes (4g .. 4g+3), returned to all four:
+// quad permutations swap lanes 1 apart, then 2 apart.
+__device__ __forceinline__ uint32_t quad_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    return v;
+}
+// Maximum over each row of 16 lanes, returned to all of them: rotations by
+// 8, 4, 2 and 1 within the row.
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x122, 0xF, 0xF, false));
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x121, 0xF, 0xF, false));
+    return v;
+}
+// Lane 0 of each quad / of each row, to every lane of it.
+__device__ __forceinline__ uint32_t quad_first(uint32_t v) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x00, 0xF, 0xF, false);
+}
+__device__ __forceinline__ uint32_t row_first(uint32_t v, int lane) {
+    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+    return lane < 32 ? (lane < 16 ? r0 : r1) : (lane < 48 ? r2 : r3);
 }
 
 template <int BLOCK>
@@ -169,24 +135,196 @@ __device__ void bitonic_sort_u64(uint64_t* keys, int m) {
     }
 }
 
-// Exclusive scan of a[0..n) in place (contiguous chunk per thread); a[n] =
-// total.  Returns the total.  Barriers inside.
-template <int BLOCK>
-__device__ uint32_t scan_exclusive_inplace(uint32_t* a, int n, uint32_t* scratch) {
-    const int chunk = (n + BLOCK - 1) / BLOCK;
-    const int a0 = min(n, (int)threadIdx.x * chunk), a1 = min(n, a0 + chunk);
-    uint32_t s = 0;
-    for (int i = a0; i < a1; ++i) s += a[i];
-    uint32_t total;
-    uint32_t run = block_exclusive_sum<BLOCK>(s, &total, scratch);
-    for (int i = a0; i < a1; ++i) {
-        const uint32_t v = a[i];
-        a[i] = run;
-        run += v;
+// Neighbour k of tensor q in its neighbour sequence: the left list first
+// (k < L), then the right band q + 1 .. q + R.  `lv` is the left-list entry
+// lst[lb + k] (ignored for k >= L).  Slots past the end (k >= K) map to q
+// itself, which is unplaced and never a successor of itself.
+__device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
+                                              uint32_t lv) {
+    return k < L ? lv : (k < K ? q + 1 + (k - L) : q);
+}
+
+// Ready lists, one per class (at most kSmallK neighbours, or more).  Each
+// tensor is appended once; the tensors released during a round go after
+// `end` (the end of the round's own range), counted by `cnt`.
+struct ReadyLists {
+    uint16_t* slot[2];
+    uint32_t end[2];
+    uint32_t* cnt[2];
+};
+
+// Exclusive prefix over the wave's lanes of a small count v (< 8), and the
+// wave total: one ballot per bit.  All 64 lanes must be active.
+__device__ __forceinline__ uint32_t wave_prefix_small(uint32_t v, uint32_t& total) {
+    uint32_t pre = 0, tot = 0;
+#pragma unroll
+    for (int bit = 0; bit < 3; ++bit) {
+        const uint64_t m = __ballot((v >> bit) & 1u);
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+        pre += below << bit;
+        tot += (uint32_t)__popcll(m) << bit;
     }
-    if (threadIdx.x == 0) a[n] = total;
-    __syncthreads();
-    return total;
+    total = tot;
+    return pre;
+}
+
+// Decrement the pending counts of the successors among M (<= 7) gathered
+// neighbours (dec[j] is 1 for a successor, else 0: the atomics then issue
+// back to back) and append those that reach zero to their class list, one
+// list reservation per wave.  All 64 lanes must be active.
+template <int M>
+__device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
+                                                   const uint32_t (&ids)[M], uint32_t* rem,
+                                                   const ReadyLists& rl, int lane) {
+    static_assert(M < 8, "counts must fit three bits");
+    uint32_t old[M];
+#pragma unroll
+    for (int j = 0; j < M; ++j) old[j] = atomicSub(rem + ids[j], dec[j]);
+    uint32_t ready[2] = {0, 0};
+#pragma unroll
+    for (int j = 0; j < M; ++j) {
+        const bool r = dec[j] && (old[j] & kCountMask) == 1u;
+        ready[0] |= (r && !(old[j] & kBigClass) ? 1u : 0u) << j;
+        ready[1] |= (r && (old[j] & kBigClass) ? 1u : 0u) << j;
+    }
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+        if (!__ballot(ready[c] != 0)) continue;
+        uint32_t total;
+        const uint32_t pre = wave_prefix_small((uint32_t)__popc(ready[c]), total);
+        uint32_t base = 0;
+        if (lane == 0) base = atomicAdd(rl.cnt[c], total);
+        uint32_t at = rl.end[c] + (uint32_t)__builtin_amdgcn_readlane((int)base, 0) + pre;
+#pragma unroll
+        for (int j = 0; j < M; ++j)
+            if (ready[c] >> j & 1u) rl.slot[c][at++] = (uint16_t)ids[j];
+    }
+}
+
+// Whole-wave placement of tensor q (all 64 lanes active, arguments uniform):
+// the neighbour sequence is swept in chunks of 256, each lane holding up to 4
+// neighbours; within a chunk the candidate offset jumps to the highest end
+// overlapping [x, x + s) until nothing in the chunk overlaps, and chunks are
+// revisited until a full lap leaves x alone.  Then q is published and its
+// successors' pending counts are decremented.
+__device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint32_t K,
+                           uint64_t* ofsz, const uint16_t* lst, uint32_t* rem,
+                           const ReadyLists& rl, int lane) {
+    const uint32_t nch = (K + kCoopChunk - 1) / kCoopChunk;
+    uint32_t id[kSlots], co[kSlots], ce[kSlots], cs[kSlots];
+    auto load = [&](uint32_t kb) {
+        uint32_t lv[kSlots];
+#pragma unroll
+        for (int r = 0; r < kSlots; ++r) {
+            const uint32_t k = kb + r * kWave + lane;
+            lv[r] = lst[k < L ? lb + k : lb];  // in bounds: the list area is padded
+        }
+        uint64_t w[kSlots];
+#pragma unroll
+        for (int r = 0; r < kSlots; ++r) {
+            id[r] = neighbour(kb + r * kWave + lane, L, K, q, lv[r]);
+            w[r] = ofsz[id[r]];
+        }
+#pragma unroll
+        for (int r = 0; r < kSlots; ++r) {
+            co[r] = word_off(w[r]);
+            ce[r] = word_end(w[r]);
+            cs[r] = (uint32_t)w[r];
+        }
+    };
+    uint32_t x = 0, clean = 0, c = 0;
+    while (clean < nch) {
+        load(c * kCoopChunk);
+        bool moved = false;
+        while (true) {  // jump past the highest end overlapping [x, x + s)
+            bool ov = false;
+            uint32_t mx = 0;
+#pragma unroll
+            for (int r = 0; r < kSlots; ++r) {
+                if (co[r] < x + s && x < ce[r]) {
+                    ov = true;
+                    mx = max(mx, ce[r]);
+                }
+            }
+            if (!__ballot(ov)) break;
+            x = wave_max_u32(mx);
+            moved = true;
+        }
+        clean = moved ? 1u : clean + 1u;
+        c = (c + 1 == nch) ? 0u : c + 1;
+    }
+    if (lane == 0) ofsz[q] = ((uint64_t)x << 32) | s;
+    for (uint32_t cc = 0; cc < nch; ++cc) {
+        if (nch > 1) load(cc * kCoopChunk);
+        uint32_t dec[kSlots];
+#pragma unroll
+        for (int r = 0; r < kSlots; ++r) {
+            const uint32_t k = cc * kCoopChunk + r * kWave + lane;
+            dec[r] = ((k < K) & ranks_after(cs[r], id[r], s, q)) ? 1u : 0u;
+        }
+        release_successors(dec, id, rem, rl, lane);
+    }
+}
+
+// A tensor being fitted by a lane group: its id, size, left-list start, left
+// length and neighbour count (all lanes of the group hold the same values).
+struct Item {
+    uint32_t q, s, lb, L, K;
+};
+
+__device__ __forceinline__ Item load_item(uint32_t q, bool has, const uint64_t* ofsz,
+                                          const uint16_t* lbeg, const uint16_t* reach) {
+    Item it{0, 0, 0, 0, 0};
+    if (has) {
+        it.q = q;
+        it.s = (uint32_t)ofsz[q];
+        it.lb = lbeg[q];
+        it.L = (uint32_t)lbeg[q + 1] - it.lb;
+        it.K = it.L + (uint32_t)reach[q] - q - 1;
+    }
+    return it;
+}
+
+// The neighbours k = g + G * r (r < kSlots) of a group's tensor, for the
+// lane at position g of a group of G lanes: ids, ranges [o, e) (o = kUnplaced
+// for an unplaced or missing neighbour, which never overlaps) and sizes.
+// `live` is false for groups without a tensor.
+template <int G>
+__device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t g,
+                                             const uint64_t* ofsz, const uint16_t* lst,
+                                             uint32_t (&id)[kSlots], uint32_t (&o)[kSlots],
+                                             uint32_t (&e)[kSlots], uint32_t (&z)[kSlots]) {
+    uint32_t lv[kSlots];
+#pragma unroll
+    for (int r = 0; r < kSlots; ++r) {
+        const uint32_t k = g + G * r;
+        lv[r] = lst[k < it.L ? it.lb + k : it.lb];  // in bounds: the list area is padded
+    }
+    uint64_t w[kSlots];
+#pragma unroll
+    for (int r = 0; r < kSlots; ++r) {
+        const uint32_t k = g + G * r;
+        id[r] = live ? neighbour(k, it.L, it.K, it.q, lv[r]) : 0u;
+        w[r] = ofsz[id[r]];
+    }
+#pragma unroll
+    for (int r = 0; r < kSlots; ++r) {
+        const bool in = live && (g + G * r) < it.K;
+        o[r] = in ? word_off(w[r]) : kUnplaced;
+        e[r] = word_end(w[r]);
+        z[r] = (uint32_t)w[r];
+    }
+}
+
+// Highest end among the lane's ranges that overlap [x, x + s), 0 if none.
+__device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[kSlots],
+                                                const uint32_t (&e)[kSlots], uint32_t x,
+                                                uint32_t s) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int r = 0; r < kSlots; ++r) m = (o[r] < x + s && x < e[r]) ? max(m, e[r]) : m;
+    return m;
 }
 
 template <int BLOCK, int ITEMS>
@@ -198,29 +336,40 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint64_t red[BLOCK / kWave];
+    __shared__ uint32_t nready[2][3];  // per class: tensors appended in rounds r % 3
 
     // LDS layout (N = cap_n tensor slots, P = cap_pairs list slots):
-    //   R0 [8N]     first[N]                     -> placement words ofsz[N]
-    //   R1 [4N]     size / unit
-    //   R2 [4N+4]   band lengths -> band starts (prefix)
-    //   R3 [4N+4]   live-bytes deltas -> predecessor counts -> fill cursors
-    //   R4 [4N+4]   predecessor list starts
-    //   R5 [2P]     predecessor lists (positions, u16)
-    //   R4+R5 hold the u64 sort keys of an unsorted trace before the lists.
+    //   A [8N]     first[N] (i32)                  -> placement words ofsz[N]
+    //   B [4N+4]   band lengths -> band starts     -> ready queue (u16)
+    //   C [4N+4]   live-bytes deltas -> left-list fill cursors
+    //   D [4N+4]   reach histogram -> pending predecessor counts
+    //   E [2N+2]   left-list starts (u16)
+    //   F [2N]     reach (u16)
+    //   G [2P+32]  left lists (u16 positions; padded for unconditional reads)
+    //   D..G hold the u64 sort keys of an unsorted trace before the reach pass.
     const size_t N = (size_t)cap_n;
     int32_t* fst = reinterpret_cast<int32_t*>(smem);
     uint64_t* ofsz = reinterpret_cast<uint64_t*>(smem);
-    uint32_t* sz = reinterpret_cast<uint32_t*>(smem + 8 * N);
-    uint32_t* bstart = reinterpret_cast<uint32_t*>(smem + 12 * N);
-    uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + 16 * N + 4);
-    uint32_t* pbeg = reinterpret_cast<uint32_t*>(smem + 20 * N + 8);
-    uint16_t* preds = reinterpret_cast<uint16_t*>(smem + 24 * N + 12);
-    uint64_t* keys = reinterpret_cast<uint64_t*>(smem + ((20 * N + 8 + 7) & ~(size_t)7));
+    const uint32_t* szw = reinterpret_cast<const uint32_t*>(smem);  // size half at 2q
+    uint32_t* band = reinterpret_cast<uint32_t*>(smem + 8 * N);
+    uint16_t* readyq = reinterpret_cast<uint16_t*>(smem + 8 * N);
+    uint32_t* live = reinterpret_cast<uint32_t*>(smem + 12 * N + 4);
+    uint32_t* cursor = live;
+    uint32_t* hist = reinterpret_cast<uint32_t*>(smem + 16 * N + 8);
+    uint32_t* rem = hist;
+    uint64_t* keys = reinterpret_cast<uint64_t*>(smem + 16 * N + 8);
+    uint16_t* lbeg = reinterpret_cast<uint16_t*>(smem + 20 * N + 12);
+    uint16_t* reach = reinterpret_cast<uint16_t*>(smem + 22 * N + 14);
+    uint16_t* lst = reinterpret_cast<uint16_t*>(smem + 24 * N + 14);
     uint32_t* scratch = reinterpret_cast<uint32_t*>(red);
 
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
     MP_STAMP(0);
+    if (tid == 0) {
+        nready[0][0] = nready[0][1] = nready[0][2] = 0;
+        nready[1][0] = nready[1][1] = nready[1][2] = 0;
+    }
     const int64_t lo = begin[b], hi = begin[b + 1];
     const int32_t n_ops = num_ops[b];
     if (lo < 0 || hi < lo || hi > n_tensors || n_ops < 0 || hi - lo > cap_n) {
@@ -321,16 +470,17 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         su_r[k] = 0;
         if (q < n) {
             su_r[k] = (uint32_t)((uint64_t)s_r[k] >> sh);
-            sz[q] = su_r[k];
             fst[q] = f_r[k];
-            cnt[q] = 0;
         }
     }
-    if (tid == 0) cnt[n] = 0;
+    for (int i = tid; i <= n; i += BLOCK) {
+        live[i] = 0;
+        hist[i] = 0;
+    }
     __syncthreads();
     MP_STAMP(2);
 
-    // ---- reach (galloping search), band lengths, live-bytes deltas
+    // ---- reach (galloping search), band lengths, live-bytes deltas, reach histogram
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
@@ -348,301 +498,226 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
                 if (fst[mid] <= l) a = mid + 1;
                 else z = mid;
             }
-            bstart[q] = (uint32_t)(a - q - 1);
-            atomicAdd(&cnt[q], su_r[k]);
-            atomicAdd(&cnt[a], 0u - su_r[k]);
+            reach[q] = (uint16_t)a;
+            band[q] = (uint32_t)(a - q - 1);
+            atomicAdd(&live[q], su_r[k]);
+            atomicAdd(&live[a], 0u - su_r[k]);
+            atomicAdd(&hist[a], 1u);
         }
     }
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {  // first[] is no longer needed
+        const int q = tid + k * BLOCK;
+        if (q < n) ofsz[q] = ((uint64_t)kUnplaced << 32) | su_r[k];
+    }
+    MP_STAMP(3);
 
-    // ---- prefix sums: band starts, max live bytes
-    const uint32_t n_band = scan_exclusive_inplace<BLOCK>(bstart, n, scratch);
+    // ---- one prefix pass over positions j (contiguous chunk per thread):
+    //   band start      = sum of band lengths before j        (pair index base)
+    //   left-list start = sum over i < j of #{q : q < i < reach[q]}
+    //                   = j(j-1)/2 - j * H(<j) + sum_{r<j} r * hist[r],
+    //     since position i has i - #{q : reach[q] <= i} left neighbours;
+    //   live bytes      = running sum of the deltas (its maximum is the bound).
+    // The three integer sums share one 64-bit word: band (24 bits, at most
+    // n(n-1)/2), hist count (13 bits, at most n) and r * hist (25 bits).
     uint32_t live_max;
+    uint32_t n_pairs;
     {
         const int chunk = (n + BLOCK - 1) / BLOCK;
         const int a0 = min(n, tid * chunk), a1 = min(n, a0 + chunk);
+        auto pack = [](uint32_t bl, uint32_t h, uint32_t j) {
+            return ((uint64_t)bl << 38) | ((uint64_t)h << 25) | (uint64_t)(h * j);
+        };
+        uint64_t ps = 0;
         uint32_t ds = 0;
-        for (int i = a0; i < a1; ++i) ds += cnt[i];
+        for (int i = a0; i < a1; ++i) {
+            ps += pack(band[i], hist[i], (uint32_t)i);
+            ds += live[i];
+        }
+        uint64_t ptot;
+        uint64_t prun = block_exclusive_sum<BLOCK>(ps, &ptot, red);
         uint32_t dtot;
-        uint32_t run = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
+        uint32_t drun = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
         uint32_t lm = 0;
         for (int i = a0; i < a1; ++i) {
-            run += cnt[i];
-            lm = lm > run ? lm : run;
+            const uint32_t bl = band[i], h = hist[i], dl = live[i];
+            const uint32_t hb = (uint32_t)(prun >> 25) & 0x1FFFu;
+            const uint32_t rh = (uint32_t)prun & 0x1FFFFFFu;
+            const uint32_t ls = (uint32_t)(i * (i - 1) / 2) - (uint32_t)i * hb + rh;
+            band[i] = (uint32_t)(prun >> 38);
+            lbeg[i] = (uint16_t)ls;
+            cursor[i] = ls;
+            rem[i] = 0;
+            drun += dl;
+            lm = lm > drun ? lm : drun;
+            prun += pack(bl, h, (uint32_t)i);
+        }
+        n_pairs = (uint32_t)(ptot >> 38);
+        if (tid == 0) {
+            band[n] = n_pairs;
+            lbeg[n] = (uint16_t)n_pairs;
         }
         live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), scratch);
     }
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        if (q < n) cnt[q] = 0;
-    }
-    __syncthreads();
-    MP_STAMP(3);
-
-    // ---- predecessor counts, balanced over the pairs: pair index p -> (q, j)
-    const uint32_t per = (n_band + BLOCK - 1) / BLOCK;
-    const uint32_t p_lo = min(n_band, (uint32_t)tid * per), p_hi = min(n_band, p_lo + per);
-    int q_lo = 0;  // last position whose band starts at or before p_lo
-    if (p_lo < p_hi) {
-        int a = 0, z = n;
-        while (a < z) {
-            const int mid = (a + z + 1) >> 1;
-            if (bstart[mid] <= p_lo) a = mid;
-            else z = mid - 1;
-        }
-        q_lo = a;
-    }
-    if (p_lo < p_hi) {
-        int q = q_lo;
-        uint32_t nxt = bstart[q + 1];
-        uint32_t sq = sz[q];
-        for (uint32_t p = p_lo; p < p_hi; ++p) {
-            while (nxt <= p) {
-                ++q;
-                nxt = bstart[q + 1];
-                sq = sz[q];
-            }
-            const int j = q + 1 + (int)(p - bstart[q]);
-            const int succ = (sq >= sz[j]) ? j : q;
-            atomicAdd(&cnt[succ], 1u);
-        }
-    }
-    __syncthreads();
-    const uint32_t n_pairs = scan_exclusive_inplace<BLOCK>(cnt, n, scratch);
     if (n_pairs > (uint32_t)cap_pairs) {
         if (tid == 0) raise_status(status, MP_ENOSPC);
         return;
     }
-    for (int i = tid; i <= n; i += BLOCK) pbeg[i] = cnt[i];
-    __syncthreads();
     MP_STAMP(4);
 
-    // ---- predecessor lists
-    if (p_lo < p_hi) {
-        int q = q_lo;
-        uint32_t nxt = bstart[q + 1];
-        uint32_t sq = sz[q];
-        for (uint32_t p = p_lo; p < p_hi; ++p) {
-            while (nxt <= p) {
-                ++q;
-                nxt = bstart[q + 1];
-                sq = sz[q];
+    // ---- left lists and pending predecessor counts, balanced over the pairs:
+    // pair index p -> (q, j), j = q + 1 + (p - band start of q)
+    {
+        const uint32_t per = (n_pairs + BLOCK - 1) / BLOCK;
+        const uint32_t p_lo = min(n_pairs, (uint32_t)tid * per), p_hi = min(n_pairs, p_lo + per);
+        if (p_lo < p_hi) {
+            int a = 0, z = n;  // last position whose band starts at or before p_lo
+            while (a < z) {
+                const int mid = (a + z + 1) >> 1;
+                if (band[mid] <= p_lo) a = mid;
+                else z = mid - 1;
             }
-            const int j = q + 1 + (int)(p - bstart[q]);
-            if (sq >= sz[j]) preds[atomicAdd(&cnt[j], 1u)] = (uint16_t)q;
-            else preds[atomicAdd(&cnt[q], 1u)] = (uint16_t)j;
+            int q = a;
+            uint32_t base = band[q], nxt = band[q + 1];
+            uint32_t sq = szw[2 * q];
+            for (uint32_t p = p_lo; p < p_hi; ++p) {
+                while (nxt <= p) {
+                    ++q;
+                    base = nxt;
+                    nxt = band[q + 1];
+                    sq = szw[2 * q];
+                }
+                const uint32_t j = (uint32_t)q + 1 + (p - base);
+                lst[atomicAdd(&cursor[j], 1u)] = (uint16_t)q;
+                atomicAdd(&rem[sq >= szw[2 * j] ? j : (uint32_t)q], 1u);
+            }
         }
     }
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        if (q < n) ofsz[q] = ((uint64_t)kUnplaced << 32) | su_r[k];
-    }
     __syncthreads();
-    MP_STAMP(5);
 
-    // ---- placement in rounds.  A tensor can be placed once its predecessors
-    // are.  Round: (A) every thread looks at the tensors it owns (positions
-    // tid + k * BLOCK) that are not placed: a tensor whose remembered blocker
-    // is now placed (or that has none) is appended to a ready list -- short
-    // predecessor lists to one list, long ones to another; (B) the short
-    // ready tensors are spread one per thread: gather the predecessor words,
-    // remember the first unplaced one as the new blocker, or fit and publish;
-    // the long ready tensors are taken one per wave and handled by the whole
-    // wave.  Waves without work wait at the barrier instead of spinning.
-    // Every round places at least the lowest-ranked unplaced tensor.
+    // ---- ready lists: tensors with more than kSmallK neighbours form the
+    // big class (flag in the pending count); tensors without predecessors
+    // seed the lists
     {
-        uint16_t* waitp = reinterpret_cast<uint16_t*>(smem + 8 * N);       // R1
-        uint16_t* rsmall = reinterpret_cast<uint16_t*>(smem + 10 * N);     // R1
-        uint16_t* rbig = reinterpret_cast<uint16_t*>(smem + 12 * N);       // R2
-        uint32_t* cursor = reinterpret_cast<uint32_t*>(smem + 16 * N + 4);  // R3
-        __shared__ uint32_t n_small[2], n_big[2], n_placed;
-        constexpr uint16_t kNone = 0xFFFF;
-        uint32_t todo = 0;
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
             if (q < n) {
-                todo |= 1u << k;
-                waitp[q] = kNone;
-                cursor[q] = pbeg[q];
-            }
-        }
-        if (tid == 0) {
-            n_small[0] = n_big[0] = n_small[1] = n_big[1] = 0;
-            n_placed = 0;
-        }
-        __syncthreads();
-        const int lane = tid & (kWave - 1), wid = tid / kWave;
-        constexpr int kWaves = BLOCK / kWave;
-        for (int round = 0;; ++round) {
-            const int par = round & 1;
-            MP_CLK(c0);
-            // (A) submit owned tensors whose blocker is gone
-#pragma unroll
-            for (int k = 0; k < ITEMS; ++k) {
-                if (!(todo >> k & 1u)) continue;
-                const uint32_t q = tid + k * BLOCK;
-                if (word_off(lds_poll64(ofsz + q)) != kUnplaced) {
-                    todo &= ~(1u << k);
-                    continue;
+                const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + (uint32_t)reach[q] - q - 1;
+                const uint32_t r = rem[q] | (K > kSmallK ? kBigClass : 0u);
+                rem[q] = r;
+                if ((r & kCountMask) == 0) {
+                    const int c = (r & kBigClass) ? 1 : 0;
+                    readyq[c * N + atomicAdd(&nready[c][2], 1u)] = (uint16_t)q;
                 }
-                const uint16_t w = waitp[q];
-                if (w != kNone && word_off(lds_poll64(ofsz + w)) == kUnplaced) continue;
-                const uint32_t kp = pbeg[q + 1] - pbeg[q];
-                if (kp > (uint32_t)kChunk && kp <= kCoopMax)
-                    rbig[atomicAdd(&n_big[par], 1u)] = (uint16_t)q;
-                else
-                    rsmall[atomicAdd(&n_small[par], 1u)] = (uint16_t)q;
             }
-            MP_CLK(c1);
-            __syncthreads();
-            MP_CLK(c2);
-            const uint32_t ns = n_small[par], nb = n_big[par];
-            const uint32_t placed_before = n_placed;
-            if (tid == 0) n_small[par ^ 1] = n_big[par ^ 1] = 0;
-            if (tid == 0) {
-                MP_DBG_ADD(1, ns);
-                MP_DBG_ADD(2, nb);
-            }
-            if (placed_before >= (uint32_t)n) {
-                if (tid == 0) MP_DBG_MAX(0, round);
-                break;
-            }
-            if (round > n + 2) {  // cannot happen: every round places a tensor
+        }
+    }
+    __syncthreads();
+    MP_STAMP(5);
+
+    // ---- placement in rounds (Kahn's order over the predecessor DAG): round
+    // r fits every tensor released in round r - 1 -- all of its predecessors
+    // are placed, and no two of them intersect -- with one lane quad per
+    // small-class tensor (four neighbours per lane) and one 16-lane row per
+    // big-class tensor (the whole wave past kMidK neighbours), packed into as
+    // few waves as possible.  A group gathers the neighbours' words (the
+    // placed ones are exactly the predecessors), moves the candidate offset
+    // past the highest overlapping end until nothing overlaps, publishes the
+    // word and decrements the successors' pending counts; those reaching zero
+    // are appended for the next round.  Per-round append counters rotate over
+    // three slots so that one barrier per round suffices.
+    {
+        const int lane = tid & (kWave - 1);
+        const uint32_t g4 = lane & 3, g16 = lane & 15;
+        const uint32_t quad = (uint32_t)tid >> 2, row = (uint32_t)tid >> 4;
+        constexpr uint32_t kQuads = BLOCK / 4, kRows = BLOCK / 16;
+        uint32_t b0 = 0, e0 = nready[0][2], b1 = 0, e1 = nready[1][2];
+        for (int round = 0; b0 < e0 || b1 < e1; ++round) {
+            if (round > n) {  // cannot happen: every round places a tensor
                 if (tid == 0) raise_status(status, MP_EDEVICE);
                 break;
             }
-            // (B1) short lists (and very long ones, chunk by chunk), one per thread
-            uint32_t mine = 0;
-            for (uint32_t i = tid; i < ns; i += BLOCK) {
-                const uint32_t q = rsmall[i];
-                const uint32_t pb = pbeg[q], pe = pbeg[q + 1];
-                const uint32_t s = (uint32_t)ofsz[q];
-                uint32_t o[kChunk], e[kChunk];
-                if (pe - pb <= (uint32_t)kChunk) {
-                    const int bl = gather(preds, pb, pe, q, ofsz, o, e);
-                    if (bl < kChunk) {
-                        // wait on the smallest unplaced predecessor: it ranks
-                        // last among them, so it is likely placed last
-                        int pick = bl;
-                        uint32_t best = e[bl] - o[bl];
-#pragma unroll
-                        for (int j = 0; j < kChunk; ++j) {
-                            const uint32_t sj = e[j] - o[j];
-                            if (pb + j < pe && o[j] == kUnplaced && sj <= best) {
-                                best = sj;
-                                pick = j;
-                            }
-                        }
-                        waitp[q] = preds[pb + pick];
-                        continue;
-                    }
+            const int cur = round % 3, nxt = (round + 1) % 3;
+            if (tid == 0) nready[0][nxt] = nready[1][nxt] = 0;
+            const ReadyLists rl{{readyq, readyq + N}, {e0, e1}, {&nready[0][cur], &nready[1][cur]}};
+#ifdef MP_PHASE_TIMING
+            if (tid == 0) MP_DBG_ADD(0, 1u);
+#endif
+            for (uint32_t it = 0;; ++it) {
+                // small tensors fill quads from the first wave up, big ones
+                // rows from the last wave down
+                const uint32_t i0 = b0 + quad + kQuads * it;
+                const uint32_t i1 = b1 + (kRows - 1 - row) + kRows * it;
+                const bool hs = i0 < e0, hb = i1 < e1;
+                const bool any_s = __ballot(hs) != 0, any_b = __ballot(hb) != 0;
+                if (!any_s && !any_b) break;
+#ifdef MP_PHASE_TIMING
+                if (lane == 0) MP_DBG_ADD(1, 1u);
+#endif
+                if (any_s) {
+                    const Item is = load_item(hs ? readyq[i0] : 0u, hs, ofsz, lbeg, reach);
+                    uint32_t id[kSlots], o[kSlots], e[kSlots], z[kSlots];
+                    gather_group<4>(is, hs, g4, ofsz, lst, id, o, e, z);
                     uint32_t x = 0;
-                    while (bump(x, s, o, e)) {
+                    while (true) {  // jump past the highest overlapping end until none moves
+                        const uint32_t m = quad_max_u32(overlap_end(o, e, x, is.s));
+                        const bool mv = m > x;
+                        x = mv ? m : x;
+#ifdef MP_PHASE_TIMING
+                        if (lane == 0) MP_DBG_ADD(2, 1u);
+#endif
+                        if (!__ballot(mv)) break;
                     }
-                    lds_publish64(ofsz + q, ((uint64_t)x << 32) | s);
-                    ++mine;
-                    continue;
-                }
-                uint32_t c = cursor[q];  // very long list: resume the scan
-                bool blocked = false;
-                while (c < pe) {
-                    const int bl = gather(preds, c, pe, q, ofsz, o, e);
-                    if (bl < kChunk) {
-                        waitp[q] = preds[c + bl];
-                        cursor[q] = c + bl;
-                        blocked = true;
-                        break;
-                    }
-                    c += kChunk;
-                }
-                if (blocked) continue;
-                const uint32_t nch = (pe - pb + kChunk - 1) / kChunk;
-                uint32_t x = 0, cc = pb, clean = 0;
-                while (clean < nch) {  // sweep the chunks until a full lap leaves x alone
-                    gather(preds, cc, pe, q, ofsz, o, e);
-                    bool moved = false;
-                    while (bump(x, s, o, e)) moved = true;
-                    clean = moved ? 1u : clean + 1u;
-                    cc += kChunk;
-                    if (cc >= pe) cc = pb;
-                }
-                lds_publish64(ofsz + q, ((uint64_t)x << 32) | s);
-                ++mine;
-            }
-            MP_CLK(c3);
-            // (B2) long lists: one tensor per wave, one predecessor per lane
-            // taken from the last wave down, since short ones fill the first waves
-            for (uint32_t j = wid; j < nb; j += kWaves) {
-                const uint32_t q = rbig[nb - 1 - j];
-                const uint32_t upb = pbeg[q], upe = pbeg[q + 1];
-                const uint32_t us = (uint32_t)ofsz[q];
-                const int slots = (int)((upe - upb + kWave - 1) / kWave);
-                uint32_t co[kCoopSlots], ce[kCoopSlots];
-                uint64_t w[kCoopSlots];
+                    if (hs && g4 == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
+                    uint32_t dec[kSlots];
 #pragma unroll
-                for (int r = 0; r < kCoopSlots; ++r) {
-                    const uint32_t pos = upb + r * kWave + lane;
-                    if (r < slots) {
-                        const uint32_t v = preds[pos < upe ? pos : upb];
-                        w[r] = lds_poll64(ofsz + (pos < upe ? v : q));
-                    } else {
-                        w[r] = 0;
-                    }
+                    for (int r = 0; r < kSlots; ++r)
+                        dec[r] = (hs & ((g4 + 4 * r) < is.K) & ranks_after(z[r], id[r], is.s, is.q))
+                                     ? 1u : 0u;
+                    release_successors(dec, id, rem, rl, lane);
                 }
-                // the smallest unplaced predecessor, if any, becomes the blocker
-                uint32_t minsz = 0xFFFFFFFFu, minpos = 0xFFFFFFFFu;
+                if (any_b) {
+                    const Item ib = load_item(hb ? readyq[N + i1] : 0u, hb, ofsz, lbeg, reach);
+                    const bool mid = hb && ib.K <= kMidK;
+                    uint32_t id[kSlots], o[kSlots], e[kSlots], z[kSlots];
+                    gather_group<16>(ib, mid, g16, ofsz, lst, id, o, e, z);
+                    uint32_t x = 0;
+                    while (true) {
+                        const uint32_t m = row_max_u32(overlap_end(o, e, x, ib.s));
+                        const bool mv = m > x;
+                        x = mv ? m : x;
+#ifdef MP_PHASE_TIMING
+                        if (lane == 0) MP_DBG_ADD(3, 1u);
+#endif
+                        if (!__ballot(mv)) break;
+                    }
+                    if (mid && g16 == 0) ofsz[ib.q] = ((uint64_t)x << 32) | ib.s;
+                    uint32_t dec[kSlots];
 #pragma unroll
-                for (int r = 0; r < kCoopSlots; ++r) {
-                    const uint32_t pos = upb + r * kWave + lane;
-                    const bool live = r < slots && pos < upe;
-                    co[r] = live ? word_off(w[r]) : kUnplaced;
-                    ce[r] = live ? word_end(w[r]) : 0u;
-                    if (live && co[r] == kUnplaced && (uint32_t)w[r] <= minsz) {
-                        minsz = (uint32_t)w[r];
-                        minpos = pos;
+                    for (int r = 0; r < kSlots; ++r)
+                        dec[r] = (mid & ((g16 + 16 * r) < ib.K) & ranks_after(z[r], id[r], ib.s, ib.q))
+                                     ? 1u : 0u;
+                    release_successors(dec, id, rem, rl, lane);
+                    uint64_t wide = __ballot(hb && !mid && g16 == 0);
+                    while (wide) {
+                        const int src = __ffsll((long long)wide) - 1;
+                        wide &= wide - 1;
+                        place_wave((uint32_t)__builtin_amdgcn_readlane((int)ib.q, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.s, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.lb, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.L, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.K, src), ofsz,
+                                   lst, rem, rl, lane);
                     }
-                }
-                const uint32_t wmin = ~wave_max_u32(~minsz);
-                if (wmin != 0xFFFFFFFFu) {
-                    const uint64_t holders = __ballot(minsz == wmin);
-                    const uint32_t pos = (uint32_t)__builtin_amdgcn_readlane(
-                        (int)minpos, __ffsll((long long)holders) - 1);
-                    if (lane == 0) waitp[q] = preds[pos];
-                    continue;
-                }
-                uint32_t x = 0;
-                while (true) {  // jump past the highest end overlapping [x, x + s)
-                    bool ov = false;
-                    uint32_t mx = 0;
-#pragma unroll
-                    for (int r = 0; r < kCoopSlots; ++r) {
-                        if (co[r] < x + us && x < ce[r]) {
-                            ov = true;
-                            mx = max(mx, ce[r]);
-                        }
-                    }
-                    if (!__ballot(ov)) break;
-                    x = wave_max_u32(mx);
-                }
-                if (lane == 0) {
-                    lds_publish64(ofsz + q, ((uint64_t)x << 32) | us);
-                    ++mine;
                 }
             }
-            if (mine) atomicAdd(&n_placed, mine);
-            MP_CLK(c4);
             __syncthreads();
-            MP_CLK(c5);
-            if (tid == 0) {
-                MP_DBG_CLK_ADD(3, c0, c1);
-                MP_DBG_CLK_ADD(4, c1, c2);
-                MP_DBG_CLK_ADD(5, c2, c3);
-                MP_DBG_CLK_ADD(6, c4, c5);
-            }
-            if (tid == 448) MP_DBG_CLK_ADD(7, c3, c4);
+            b0 = e0;
+            e0 += nready[0][cur];
+            b1 = e1;
+            e1 += nready[1][cur];
         }
     }
     __syncthreads();
@@ -708,24 +783,26 @@ hipError_t launch_reset_status(int32_t* status, hipStream_t st) {
     return hipGetLastError();
 }
 
-// LDS bytes per workgroup: 24 per tensor slot + 16 + 2 per pair slot.  Traces
-// up to about 2000 tensors get a budget that lets two workgroups share a CU's
-// 160 KiB of LDS.  The sort keys (8 bytes per power-of-two slot) must fit in
-// the last two regions.
+// LDS bytes per workgroup: 24 per tensor slot + 16, plus 2 per pair slot + 32.
+// Traces up to about 2000 tensors get a budget that lets two workgroups share
+// a CU's 160 KiB of LDS.  Pair slots stay below 2^16 (left-list starts are
+// u16), which both budgets imply.  The sort keys (8 bytes per power-of-two
+// slot) must fit from region D on.
 BatchShape batch_shape(int64_t max_trace_len) {
     BatchShape s{};
     if (max_trace_len < 0 || max_trace_len > MP_BATCH_MAX_TRACE_LEN) return s;
     const int64_t cap_n = max_trace_len < 1 ? 1 : max_trace_len;
     const int64_t fixed = 24 * cap_n + 16;
     const int64_t budget = (fixed <= 48 * 1024) ? 78 * 1024 : 156 * 1024;
-    int64_t pairs = (budget - fixed - 16) / 2;
+    int64_t pairs = (budget - fixed - 32) / 2;
     pairs &= ~(int64_t)7;
+    if (pairs > 65528) pairs = 65528;
     int64_t m = 1;
     while (m < cap_n) m <<= 1;
-    if (4 * cap_n + 2 * pairs < 8 * m) return s;  // keys would not fit (never for <= 4096)
+    if (8 * cap_n + 2 * pairs + 40 < 8 * m) return s;  // keys would not fit (never for <= 4096)
     s.cap_n = (int32_t)cap_n;
     s.cap_pairs = (int32_t)pairs;
-    s.lds_bytes = (size_t)(fixed + 2 * pairs + 16);  // list reads run up to 8 slots past the end
+    s.lds_bytes = (size_t)(fixed + 2 * pairs + 32);
     int items = 1;
     while (items * kBatchBlock < cap_n) items <<= 1;
     s.items = items;
