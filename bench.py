@@ -102,8 +102,8 @@ def main():
     cap = 1024
     pairs = torch.empty((cap, 2), dtype=torch.int64, device="cuda")
     n_conf = torch.empty(1, dtype=torch.int64, device="cuda")
-    vws = torch.empty(binding.workspace_size(binding.OP_VALIDATE, n, 0, cap), dtype=torch.uint8,
-                      device="cuda")
+    vws = torch.empty(binding.workspace_size(binding.OP_VALIDATE_BATCH, n, n_traces, cap),
+                      dtype=torch.uint8, device="cuda")
 
     def step(ev=None):
         if ev is not None:
@@ -114,7 +114,7 @@ def main():
             ev[1].record(stream)
         binding.validate_batch(begin, size, first, last, offset, capacity=cap, check=False,
                                status=status, workspace=vws, stream=stream, out=(pairs, n_conf),
-                               assume_sorted=True)
+                               assume_sorted=True, max_trace_len=2000)
         if ev is not None:
             ev[2].record(stream)
 

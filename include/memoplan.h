@@ -114,10 +114,13 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
 
 /* Workspace sizes (host query).  op: MP_OP_LIVE_BYTES (uses num_ops),
  * MP_OP_VALIDATE (uses n_tensors and capacity), MP_OP_PLAN_TRACE (uses
- * n_tensors and num_ops).  Returns 0 for an unknown op or negative sizes. */
+ * n_tensors and num_ops), MP_OP_VALIDATE_BATCH (uses n_tensors, capacity and
+ * the number of traces passed as num_ops).  Returns 0 for an unknown op or
+ * negative sizes. */
 #define MP_OP_LIVE_BYTES 1
 #define MP_OP_VALIDATE 2
 #define MP_OP_PLAN_TRACE 3
+#define MP_OP_VALIDATE_BATCH 4
 size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops, int64_t capacity);
 
 /* Per-op live bytes of one trace (the quantity whose maximum lower-bounds
@@ -155,12 +158,22 @@ int32_t mp_validate_plan(const int64_t* size, const int32_t* first, const int32_
 /* mp_validate_plan over a batch of independent traces (trace b = tensors
  * [begin[b], begin[b+1]) with begin[0] == 0 and begin[n_traces] == n_tensors,
  * checked on device).  Pairs use indices into the concatenated arrays; no
- * pair crosses traces.  Workspace as for mp_validate_plan with n_tensors. */
+ * pair crosses traces.
+ *   max_trace_len:  0, or a bound on the tensors of every trace, at most
+ *                   MP_BATCH_MAX_TRACE_LEN.  With MP_HINT_SORTED_FIRST a
+ *                   nonzero bound selects the path that holds each trace in
+ *                   one workgroup's LDS (count per trace, scan, write); a
+ *                   trace above the bound is then MP_EINVAL on device.
+ *                   Otherwise the bound is not used.
+ *   workspace:      mp_workspace_size(MP_OP_VALIDATE_BATCH, n_tensors,
+ *                   n_traces, capacity) bytes; contents need no
+ *                   initialisation. */
 int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t* size,
                           const int32_t* first, const int32_t* last, const int64_t* offset,
-                          int64_t n_tensors, int64_t* pairs_out, int64_t capacity,
-                          int64_t* n_conflicts_out, int32_t hints, void* workspace,
-                          size_t workspace_bytes, int32_t* status_out, void* stream);
+                          int64_t n_tensors, int64_t max_trace_len, int64_t* pairs_out,
+                          int64_t capacity, int64_t* n_conflicts_out, int32_t hints,
+                          void* workspace, size_t workspace_bytes, int32_t* status_out,
+                          void* stream);
 
 #ifdef __cplusplus
 }

@@ -15,7 +15,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
-OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE = 1, 2, 3
+OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH = 1, 2, 3, 4
 HINT_SORTED_FIRST = 1
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
@@ -52,7 +52,7 @@ def load_library(path: str = LIB_PATH):
     L.mp_live_bytes_profile.restype = i32
     L.mp_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p, i32, p, sz, p, p]
     L.mp_validate_plan.restype = i32
-    L.mp_validate_batch.argtypes = [p, i64, p, p, p, p, i64, p, i64, p, i32, p, sz, p, p]
+    L.mp_validate_batch.argtypes = [p, i64, p, p, p, p, i64, i64, p, i64, p, i32, p, sz, p, p]
     L.mp_validate_batch.restype = i32
     L.mp_plan_trace.argtypes = [p, p, p, i64, i32, i32, p, p, p, sz, p, p]
     L.mp_plan_trace.restype = i32
@@ -185,7 +185,7 @@ def live_bytes_profile(size, first, last, num_ops: int, *, check: bool = True, o
 
 
 def _validate(begin, size, first, last, offset, capacity, check, status, workspace, stream,
-              out=None, assume_sorted=False):
+              out=None, assume_sorted=False, max_trace_len=0):
     L = load_library()
     size = _dev(size, torch.int64, "size")
     first = _dev(first, torch.int32, "first")
@@ -200,7 +200,11 @@ def _validate(begin, size, first, last, offset, capacity, check, status, workspa
         count = torch.empty(1, dtype=torch.int64, device=dev)
     else:
         pairs, count = out
-    ws, need = _workspace(OP_VALIDATE, dev, n, 0, capacity, workspace)
+    if begin is None:
+        ws, need = _workspace(OP_VALIDATE, dev, n, 0, capacity, workspace)
+    else:
+        begin = _dev(begin, torch.int64, "begin")
+        ws, need = _workspace(OP_VALIDATE_BATCH, dev, n, begin.numel() - 1, capacity, workspace)
     if status is None:
         status = new_status(dev, stream)
     hints = HINT_SORTED_FIRST if assume_sorted else 0
@@ -209,10 +213,9 @@ def _validate(begin, size, first, last, offset, capacity, check, status, workspa
                                 int(capacity), _p(count), hints, _p(ws), need, _p(status),
                                 _stream(stream))
     else:
-        begin = _dev(begin, torch.int64, "begin")
         rc = L.mp_validate_batch(_p(begin), begin.numel() - 1, _p(size), _p(first), _p(last),
-                                 _p(offset), n, _p(pairs), int(capacity), _p(count), hints,
-                                 _p(ws), need, _p(status), _stream(stream))
+                                 _p(offset), n, int(max_trace_len), _p(pairs), int(capacity),
+                                 _p(count), hints, _p(ws), need, _p(status), _stream(stream))
     if rc != MP_OK:
         raise PlanError(rc, "validate")
     if check:
@@ -235,10 +238,13 @@ def validate_plan(size, first, last, offset, *, capacity: int | None = None, che
 
 def validate_batch(begin, size, first, last, offset, *, capacity: int | None = None,
                    check: bool = True, status=None, workspace=None, stream=None, out=None,
-                   assume_sorted=False):
-    """mp_validate_batch: like validate_plan over the traces begin[b]..begin[b+1]."""
+                   assume_sorted=False, max_trace_len: int = 0):
+    """mp_validate_batch: like validate_plan over the traces begin[b]..begin[b+1].
+    With assume_sorted and a nonzero max_trace_len (a bound on every trace's
+    length, at most BATCH_MAX_TRACE_LEN) each trace is checked in one
+    workgroup."""
     return _validate(begin, size, first, last, offset, capacity, check, status, workspace, stream,
-                     out, assume_sorted)
+                     out, assume_sorted, max_trace_len)
 
 
 def plan_trace(size, first, last, num_ops: int, *, policy: int = LOWEST_FIT, check: bool = True,

@@ -59,7 +59,9 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
         case MP_OP_LIVE_BYTES:
             return num_ops > INT32_MAX ? 0 : live_workspace_bytes((int32_t)num_ops);
         case MP_OP_VALIDATE:
-            return validate_workspace_bytes(n_tensors, capacity);
+            return validate_workspace_bytes(n_tensors, capacity, 1);
+        case MP_OP_VALIDATE_BATCH:
+            return num_ops > INT32_MAX ? 0 : validate_workspace_bytes(n_tensors, capacity, num_ops);
         case MP_OP_PLAN_TRACE:
             return n_tensors >= (int64_t)1 << 30 ? 0 : plan_trace_workspace_bytes(n_tensors);
         default:
@@ -84,19 +86,22 @@ namespace {
 
 int32_t validate_common(const int64_t* begin, int64_t n_seg, const int64_t* size,
                         const int32_t* first, const int32_t* last, const int64_t* offset,
-                        int64_t n, int64_t* pairs_out, int64_t capacity, int64_t* n_conflicts_out,
-                        int32_t hints, void* workspace, size_t workspace_bytes,
-                        int32_t* status_out, void* stream) {
+                        int64_t n, int64_t max_seg, int64_t* pairs_out, int64_t capacity,
+                        int64_t* n_conflicts_out, int32_t hints, void* workspace,
+                        size_t workspace_bytes, int32_t* status_out, void* stream) {
     if (n < 0 || n > INT32_MAX - 1 || capacity < 0 || !status_out || !n_conflicts_out ||
         !workspace)
         return MP_EINVAL;
     if (n > 0 && (!size || !first || !last || !offset)) return MP_EINVAL;
     if (capacity > 0 && !pairs_out) return MP_EINVAL;
     if (hints & ~MP_HINT_SORTED_FIRST) return MP_EINVAL;
-    if (workspace_bytes < validate_workspace_bytes(n, capacity)) return MP_EINVAL;
-    return launched(launch_validate(begin, n_seg, size, first, last, offset, n, pairs_out,
-                                    capacity, n_conflicts_out, (hints & MP_HINT_SORTED_FIRST) != 0,
-                                    workspace, status_out, static_cast<hipStream_t>(stream)));
+    if (max_seg < 0 || max_seg > MP_BATCH_MAX_TRACE_LEN) return MP_EINVAL;
+    if (workspace_bytes < validate_workspace_bytes(n, capacity, begin ? n_seg : 1))
+        return MP_EINVAL;
+    return launched(launch_validate(begin, n_seg, size, first, last, offset, n, max_seg,
+                                    pairs_out, capacity, n_conflicts_out,
+                                    (hints & MP_HINT_SORTED_FIRST) != 0, workspace, status_out,
+                                    static_cast<hipStream_t>(stream)));
 }
 
 }  // namespace
@@ -106,20 +111,20 @@ extern "C" int32_t mp_validate_plan(const int64_t* size, const int32_t* first, c
                                     int64_t capacity, int64_t* n_conflicts_out, int32_t hints,
                                     void* workspace, size_t workspace_bytes, int32_t* status_out,
                                     void* stream) {
-    return validate_common(nullptr, 1, size, first, last, offset, n, pairs_out, capacity,
+    return validate_common(nullptr, 1, size, first, last, offset, n, 0, pairs_out, capacity,
                            n_conflicts_out, hints, workspace, workspace_bytes, status_out, stream);
 }
 
 extern "C" int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t* size,
                                      const int32_t* first, const int32_t* last,
-                                     const int64_t* offset, int64_t n_tensors, int64_t* pairs_out,
-                                     int64_t capacity, int64_t* n_conflicts_out, int32_t hints,
-                                     void* workspace, size_t workspace_bytes, int32_t* status_out,
-                                     void* stream) {
+                                     const int64_t* offset, int64_t n_tensors,
+                                     int64_t max_trace_len, int64_t* pairs_out, int64_t capacity,
+                                     int64_t* n_conflicts_out, int32_t hints, void* workspace,
+                                     size_t workspace_bytes, int32_t* status_out, void* stream) {
     if (!begin || n_traces < 1 || n_traces > INT32_MAX) return MP_EINVAL;
-    return validate_common(begin, n_traces, size, first, last, offset, n_tensors, pairs_out,
-                           capacity, n_conflicts_out, hints, workspace, workspace_bytes,
-                           status_out, stream);
+    return validate_common(begin, n_traces, size, first, last, offset, n_tensors, max_trace_len,
+                           pairs_out, capacity, n_conflicts_out, hints, workspace,
+                           workspace_bytes, status_out, stream);
 }
 
 extern "C" int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,

@@ -60,11 +60,12 @@ hipError_t launch_live_profile(const int64_t* size, const int32_t* first, const 
 
 
 // plan validation (validate.hip); begin == nullptr means one trace of n tensors
-size_t validate_workspace_bytes(int64_t n, int64_t capacity);
+size_t validate_workspace_bytes(int64_t n, int64_t capacity, int64_t n_seg);
 hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* size,
                            const int32_t* first, const int32_t* last, const int64_t* off,
-                           int64_t n, int64_t* pairs, int64_t cap, int64_t* n_out,
-                           bool assume_sorted, void* ws, int32_t* status, hipStream_t st);
+                           int64_t n, int64_t max_seg, int64_t* pairs, int64_t cap,
+                           int64_t* n_out, bool assume_sorted, void* ws, int32_t* status,
+                           hipStream_t st);
 
 
 // single-trace planner (plan_trace.hip)

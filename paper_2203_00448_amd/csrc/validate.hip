@@ -257,12 +257,226 @@ __global__ void v_unpack_kernel(const uint64_t* __restrict__ keys, const int64_t
     }
 }
 
+// ---- batches of short sorted traces: one workgroup per trace, the trace in LDS.
+// Positions are ids (the caller promises first non-decreasing inside every
+// trace); row q's candidates are (q, reach[q]).  The pairs of a trace are
+// split evenly over the threads by pair index (row-major), so the count pass
+// and the write pass enumerate the same pairs in (i, j) order.
+
+constexpr int kVbBlock = 512;
+
+// write == 0: segcnt[b] = conflicts of trace b.
+// write == 1: segcnt holds exclusive starts (segcnt[n_seg] = total); the
+//             pairs of trace b are written from segcnt[b] on, below `cap`.
+template <int BLOCK, int ITEMS>
+__global__ __launch_bounds__(BLOCK) void vb_kernel(
+    const int64_t* __restrict__ begin, int64_t n_seg, const int64_t* __restrict__ size,
+    const int32_t* __restrict__ first, const int32_t* __restrict__ last,
+    const int64_t* __restrict__ off, int64_t n, int32_t cap_n, int64_t* __restrict__ segcnt,
+    int write, int64_t* __restrict__ pairs, int64_t cap, int32_t* __restrict__ status) {
+    extern __shared__ __align__(16) unsigned char smem[];
+    __shared__ uint32_t scratch[BLOCK / kWave];
+    // LDS: off[N] i64, size[N] i64, first[N] i32, band starts[N+1] u32
+    const size_t N = (size_t)cap_n;
+    int64_t* lo64 = reinterpret_cast<int64_t*>(smem);
+    int64_t* ls64 = reinterpret_cast<int64_t*>(smem + 8 * N);
+    int32_t* lf = reinterpret_cast<int32_t*>(smem + 16 * N);
+    uint32_t* band = reinterpret_cast<uint32_t*>(smem + 20 * N);
+    const int tid = threadIdx.x;
+    for (int64_t b = blockIdx.x; b < n_seg; b += gridDim.x) {
+        const int64_t lo = begin[b], hi = begin[b + 1];
+        if (lo < 0 || hi < lo || hi > n || (b == 0 && lo != 0) || (b == n_seg - 1 && hi != n) ||
+            hi - lo > cap_n) {
+            if (tid == 0) {
+                raise_status(status, MP_EINVAL);
+                if (!write) segcnt[b] = 0;
+            }
+            continue;
+        }
+        int64_t base = 0;
+        if (write) {
+            base = segcnt[b];
+            if (segcnt[b + 1] == base || base >= cap) continue;  // nothing to write here
+        }
+        const int m = (int)(hi - lo);
+        int32_t l_r[ITEMS];
+        bool bad = false;
+#pragma unroll
+        for (int k = 0; k < ITEMS; ++k) {
+            const int q = tid + k * BLOCK;
+            l_r[k] = 0;
+            if (q < m) {
+                const int64_t sz = size[lo + q], o = off[lo + q];
+                const int32_t f = first[lo + q], l = last[lo + q];
+                if (sz <= 0 || f < 0 || f > l || o < 0 || o > INT64_MAX - sz) bad = true;
+                lo64[q] = o;
+                ls64[q] = sz;
+                lf[q] = f;
+                l_r[k] = l;
+            }
+        }
+        __syncthreads();
+        // reach (galloping search over first), band lengths; sortedness check
+#pragma unroll
+        for (int k = 0; k < ITEMS; ++k) {
+            const int q = tid + k * BLOCK;
+            if (q < m) {
+                if (q > 0 && lf[q] < lf[q - 1]) bad = true;  // the sorted promise is broken
+                const int32_t l = l_r[k];
+                int known = q, step = 1, probe = q + 1;
+                while (probe < m && lf[probe] <= l) {
+                    known = probe;
+                    step <<= 1;
+                    probe = q + step;
+                }
+                int a = known + 1, z = probe < m ? probe : m;
+                while (a < z) {
+                    const int mid = (a + z) >> 1;
+                    if (lf[mid] <= l) a = mid + 1;
+                    else z = mid;
+                }
+                band[q] = (uint32_t)(a - q - 1);
+            }
+        }
+        if (!write && __ballot(bad) && (tid & (kWave - 1)) == 0) raise_status(status, MP_EINVAL);
+        __syncthreads();
+        // band starts: exclusive scan over contiguous chunks
+        uint32_t n_pairs;
+        {
+            const int chunk = (m + BLOCK - 1) / BLOCK;
+            const int a0 = min(m, tid * chunk), a1 = min(m, a0 + chunk);
+            uint32_t sum = 0;
+            for (int i = a0; i < a1; ++i) sum += band[i];
+            uint32_t tot;
+            uint32_t run = block_exclusive_sum<BLOCK>(sum, &tot, scratch);
+            for (int i = a0; i < a1; ++i) {
+                const uint32_t v = band[i];
+                band[i] = run;
+                run += v;
+            }
+            if (tid == 0) band[m] = tot;
+            n_pairs = tot;
+        }
+        __syncthreads();
+        // pairs p in [p_lo, p_hi) of this thread, row-major
+        const uint32_t per = (n_pairs + BLOCK - 1) / BLOCK;
+        const uint32_t p_lo = min(n_pairs, (uint32_t)tid * per), p_hi = min(n_pairs, p_lo + per);
+        int q0 = 0;
+        if (p_lo < p_hi) {
+            int a = 0, z = m;  // last position whose band starts at or before p_lo
+            while (a < z) {
+                const int mid = (a + z + 1) >> 1;
+                if (band[mid] <= p_lo) a = mid;
+                else z = mid - 1;
+            }
+            q0 = a;
+        }
+        auto sweep = [&](auto&& on_hit) {
+            if (p_lo >= p_hi) return;
+            int q = q0;
+            uint32_t start = band[q], nxt = band[q + 1];
+            int64_t oq = lo64[q], sq = ls64[q];
+            for (uint32_t p = p_lo; p < p_hi; ++p) {
+                while (nxt <= p) {
+                    ++q;
+                    start = nxt;
+                    nxt = band[q + 1];
+                    oq = lo64[q];
+                    sq = ls64[q];
+                }
+                const int j = q + 1 + (int)(p - start);
+                if (bytes_meet(oq, sq, lo64[j], ls64[j])) on_hit(q, j);
+            }
+        };
+        uint32_t hits = 0;
+        sweep([&](int, int) { ++hits; });
+        if (!write) {
+            const uint32_t tot = block_reduce<BLOCK>(hits, OpAdd<uint32_t>(), scratch);
+            if (tid == 0) segcnt[b] = tot;
+        } else {
+            uint32_t tot;
+            const uint32_t before = block_exclusive_sum<BLOCK>(hits, &tot, scratch);
+            int64_t pos = base + before;
+            sweep([&](int q, int j) {
+                if (pos < cap) {
+                    pairs[2 * pos] = lo + q;
+                    pairs[2 * pos + 1] = lo + j;
+                }
+                ++pos;
+            });
+        }
+        __syncthreads();  // LDS is reused by the next trace
+    }
+}
+
+// One workgroup: exclusive scan of the per-trace counts in place,
+// segcnt[n_seg] = total = *n_out; MP_ENOSPC when the total exceeds cap.
+__global__ __launch_bounds__(1024) void vb_scan_kernel(int64_t* __restrict__ segcnt, int64_t n_seg,
+                                                       int64_t cap, int64_t* __restrict__ n_out,
+                                                       int32_t* __restrict__ status) {
+    __shared__ uint64_t scratch[1024 / kWave];
+    constexpr int kItems = 8;
+    uint64_t carry = 0;
+    for (int64_t base = 0; base < n_seg; base += 1024 * kItems) {
+        const int64_t i0 = base + (int64_t)threadIdx.x * kItems;
+        uint64_t v[kItems];
+        uint64_t s = 0;
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            v[k] = (i0 + k < n_seg) ? (uint64_t)segcnt[i0 + k] : 0;
+            s += v[k];
+        }
+        uint64_t total;
+        uint64_t run = carry + block_exclusive_sum<1024>(s, &total, scratch);
+#pragma unroll
+        for (int k = 0; k < kItems; ++k) {
+            if (i0 + k < n_seg) segcnt[i0 + k] = (int64_t)run;
+            run += v[k];
+        }
+        carry += total;
+    }
+    if (threadIdx.x == 0) {
+        segcnt[n_seg] = (int64_t)carry;
+        *n_out = (int64_t)carry;
+        if ((int64_t)carry > cap) raise_status(status, MP_ENOSPC);
+    }
+}
+
+template <int ITEMS>
+hipError_t launch_vb(int write, const int64_t* begin, int64_t n_seg, const int64_t* size,
+                     const int32_t* first, const int32_t* last, const int64_t* off, int64_t n,
+                     int32_t cap_n, int64_t* segcnt, int64_t* pairs, int64_t cap,
+                     int32_t* status, hipStream_t st) {
+    auto kern = vb_kernel<kVbBlock, ITEMS>;
+    const size_t lds = 24 * (size_t)cap_n + 8;
+    hipError_t e = hipFuncSetAttribute((const void*)kern,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    const unsigned grid = (unsigned)(n_seg < 65535 ? n_seg : 65535);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(kVbBlock), lds, st, begin, n_seg, size, first, last,
+                       off, n, cap_n, segcnt, write, pairs, cap, status);
+    return hipGetLastError();
+}
+
+hipError_t launch_vb_any(int write, int items, const int64_t* begin, int64_t n_seg,
+                         const int64_t* size, const int32_t* first, const int32_t* last,
+                         const int64_t* off, int64_t n, int32_t cap_n, int64_t* segcnt,
+                         int64_t* pairs, int64_t cap, int32_t* status, hipStream_t st) {
+    switch (items) {
+        case 1: return launch_vb<1>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
+        case 2: return launch_vb<2>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
+        case 4: return launch_vb<4>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
+        case 8: return launch_vb<8>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
 struct VLayout {
     size_t flags, segend, reach, cnt, long_rows, keys0, vals0, keys1, vals1, pf, pl, po, ps, pid,
         pk0, pk1, radix, total;
 };
 
-VLayout v_layout(int64_t n, int64_t cap) {
+VLayout v_layout(int64_t n, int64_t cap, int64_t n_seg = 1) {
     VLayout L{};
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -274,7 +488,8 @@ VLayout v_layout(int64_t n, int64_t cap) {
     L.flags = take(sizeof(VFlags));
     L.segend = take(nn * 4);
     L.reach = take(nn * 4);
-    L.cnt = take((nn + 1) * 8 + scan_workspace_bytes(nn + 1));
+    const int64_t nc = nn > n_seg ? nn : n_seg;  // also the per-trace counts of a batch
+    L.cnt = take((nc + 1) * 8 + scan_workspace_bytes(nc + 1));
     L.long_rows = take(nn * 4);
     L.keys0 = take(nn * 8);
     L.vals0 = take(nn * 4);
@@ -301,13 +516,32 @@ unsigned grid_for(int64_t n, int block, unsigned cap) {
 
 }  // namespace
 
-size_t validate_workspace_bytes(int64_t n, int64_t capacity) { return v_layout(n, capacity).total; }
+size_t validate_workspace_bytes(int64_t n, int64_t capacity, int64_t n_seg) {
+    return v_layout(n, capacity, n_seg).total;
+}
 
 hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* size,
                            const int32_t* first, const int32_t* last, const int64_t* off,
-                           int64_t n, int64_t* pairs, int64_t cap, int64_t* n_out,
-                           bool assume_sorted, void* ws, int32_t* status, hipStream_t st) {
-    const VLayout L = v_layout(n, cap);
+                           int64_t n, int64_t max_seg, int64_t* pairs, int64_t cap,
+                           int64_t* n_out, bool assume_sorted, void* ws, int32_t* status,
+                           hipStream_t st) {
+    const VLayout L = v_layout(n, cap, begin ? n_seg : 1);
+    if (begin && assume_sorted && max_seg > 0 && max_seg <= MP_BATCH_MAX_TRACE_LEN) {
+        // batch of short sorted traces: count per trace, scan, write
+        int64_t* segcnt = reinterpret_cast<int64_t*>(static_cast<char*>(ws) + L.cnt);
+        int items = 1;
+        while (items * kVbBlock < max_seg) items <<= 1;
+        hipError_t e = launch_vb_any(0, items, begin, n_seg, size, first, last, off, n,
+                                     (int32_t)max_seg, segcnt, pairs, cap, status, st);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(vb_scan_kernel, dim3(1), dim3(1024), 0, st, segcnt, n_seg, cap, n_out,
+                           status);
+        if (cap > 0)
+            e = launch_vb_any(1, items, begin, n_seg, size, first, last, off, n, (int32_t)max_seg,
+                              segcnt, pairs, cap, status, st);
+        if (e != hipSuccess) return e;
+        return hipGetLastError();
+    }
     char* w = static_cast<char*>(ws);
     VFlags* fl = reinterpret_cast<VFlags*>(w + L.flags);
     int32_t* segend = reinterpret_cast<int32_t*>(w + L.segend);

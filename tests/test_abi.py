@@ -83,12 +83,21 @@ def test_other_host_checks(lib):
     assert lib.mp_validate_plan(d, d, d, d, 10, d, 4, d, 2, d, 1 << 40, d, None) == b.MP_EINVAL
     assert lib.mp_validate_plan(d, d, d, d, 10, d, -1, d, 0, d, 1 << 40, d, None) == b.MP_EINVAL
     assert lib.mp_validate_plan(d, d, d, d, 10, d, 4, d, 0, d, 8, d, None) == b.MP_EINVAL
-    assert lib.mp_validate_batch(None, 1, d, d, d, d, 10, d, 4, d, 0, d, 1 << 40, d, None) == b.MP_EINVAL
+    assert lib.mp_validate_batch(None, 1, d, d, d, d, 10, 0, d, 4, d, 0, d, 1 << 40, d, None) == b.MP_EINVAL
+    # batch validation: trace bound beyond the per-workgroup limit, short workspace
+    assert lib.mp_validate_batch(d, 1, d, d, d, d, 10, b.BATCH_MAX_TRACE_LEN + 1, d, 4, d, 1, d,
+                                 1 << 40, d, None) == b.MP_EINVAL
+    assert lib.mp_validate_batch(d, 1, d, d, d, d, 10, -1, d, 4, d, 1, d, 1 << 40, d, None) == b.MP_EINVAL
+    small = lib.mp_workspace_size(b.OP_VALIDATE_BATCH, 10, 1, 4)
+    assert lib.mp_validate_batch(d, 1, d, d, d, d, 10, 16, d, 4, d, 1, d, small - 1, d, None) == b.MP_EINVAL
     # liveness: short workspace, missing outputs
     assert lib.mp_live_bytes_profile(d, d, d, 10, 10, d, d, d, 1, d, None) == b.MP_EINVAL
     assert lib.mp_live_bytes_profile(d, d, d, 10, 10, None, d, d, 1 << 40, d, None) == b.MP_EINVAL
     # workspace queries
     assert lib.mp_workspace_size(99, 10, 10, 10) == 0
     assert lib.mp_workspace_size(b.OP_VALIDATE, -1, 0, 0) == 0
+    # a batch of many empty traces needs room for its per-trace counts
+    assert lib.mp_workspace_size(b.OP_VALIDATE_BATCH, 0, 100000, 0) > lib.mp_workspace_size(
+        b.OP_VALIDATE, 0, 0, 0)
     assert lib.mp_workspace_size(b.OP_LIVE_BYTES, 0, 100, 0) > 0
     assert lib.mp_workspace_size(b.OP_VALIDATE, 1000, 0, 100) > 0

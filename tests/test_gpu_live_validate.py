@@ -175,6 +175,96 @@ def test_validate_batch_matches_per_trace():
     assert np.array_equal(host(pairs), expect)
 
 
+def _batch_expect(traces, batch, off):
+    expect = []
+    for b, t in enumerate(traces):
+        lo = int(batch.begin[b])
+        p, _ = oracle.validate_plan(t.size, t.first, t.last, off[lo:lo + t.n])
+        expect.append(p + lo)
+    return np.concatenate(expect) if expect else np.zeros((0, 2), np.int64)
+
+
+def _batch_dev(batch, off):
+    return (dev(batch.begin, torch.int64), dev(batch.size, torch.int64),
+            dev(batch.first, torch.int32), dev(batch.last, torch.int32), dev(off, torch.int64))
+
+
+@pytest.mark.parametrize("max_len", [700, 2048, 4096])
+def test_validate_batch_per_trace_path(max_len):
+    """Sorted traces with a length bound: one workgroup per trace."""
+    binding = need_gpu()
+    rng = np.random.default_rng(206 + max_len)
+    sizes = [0, 1, 2, 31, 511, 512, 513, 700]
+    traces = [tg.random_trace(rng, int(rng.choice(sizes)), 300, max_len=int(rng.integers(1, 40)),
+                              sorted_first=True) for _ in range(60)]
+    traces.append(tg.random_trace(rng, 700, 50, max_len=50, sorted_first=True))  # dense rows
+    batch = tg.concat(traces)
+    off = 64 * rng.integers(0, 30, batch.size.shape[0])
+    expect = _batch_expect(traces, batch, off)
+    print(f"case per-trace batch validation max_len={max_len} ({expect.shape[0]} conflicts)",
+          flush=True)
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, off), capacity=expect.shape[0],
+                                            assume_sorted=True, max_trace_len=max_len)
+    assert st == binding.MP_OK and cnt == expect.shape[0]
+    assert np.array_equal(host(pairs), expect)
+    # a smaller capacity keeps the first pairs in order and reports ENOSPC
+    k = expect.shape[0] // 3
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, off), capacity=max(k, 1),
+                                            assume_sorted=True, max_trace_len=max_len)
+    assert st == binding.MP_ENOSPC and cnt == expect.shape[0]
+    assert np.array_equal(host(pairs), expect[:max(k, 1)])
+
+
+def test_validate_batch_per_trace_clean_plans():
+    """Oracle plans have no conflicts: the count pass alone decides."""
+    binding = need_gpu()
+    traces = [tg.resnext_trace(b) for b in range(6)] + [tg.chain256()]
+    batch = tg.concat(traces)
+    off, _ = oracle.plan_batch(batch.begin, batch.num_ops, batch.size, batch.first, batch.last)
+    print("case per-trace validation of oracle plans", flush=True)
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, off), capacity=16,
+                                            assume_sorted=True, max_trace_len=2000)
+    assert st == binding.MP_OK and cnt == 0
+    bad, chosen = tg.corrupt_offsets(batch.first, batch.last, off, seed=5, k=40)
+    expect = _batch_expect(traces, batch, bad)
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, bad), capacity=expect.shape[0],
+                                            assume_sorted=True, max_trace_len=2000)
+    assert st == binding.MP_OK and cnt == expect.shape[0]
+    assert np.array_equal(host(pairs), expect)
+
+
+def test_validate_batch_per_trace_errors():
+    binding = need_gpu()
+    rng = np.random.default_rng(209)
+    print("case per-trace validation errors", flush=True)
+    # a trace longer than the promised bound
+    long = tg.concat([tg.random_trace(rng, 300, 100, max_len=5, sorted_first=True)])
+    off = np.zeros(300, np.int64)
+    st = binding.new_status()
+    binding.validate_batch(*_batch_dev(long, off), capacity=4, assume_sorted=True,
+                           max_trace_len=200, check=False, status=st)
+    assert int(st.item()) == binding.MP_EINVAL
+    # a broken sorted promise
+    u = tg.random_trace(rng, 400, 100, max_len=5, sorted_first=False)
+    assert (np.diff(u.first) < 0).any()
+    ub = tg.concat([u])
+    st = binding.new_status()
+    binding.validate_batch(*_batch_dev(ub, np.arange(400, dtype=np.int64) * 64), capacity=1 << 16,
+                           assume_sorted=True, max_trace_len=512, check=False, status=st)
+    assert int(st.item()) == binding.MP_EINVAL
+    # many empty traces (more traces than tensors)
+    traces = [tg.Trace(np.zeros(0, np.int64), np.zeros(0, np.int32), np.zeros(0, np.int32), 0)
+              for _ in range(5000)]
+    traces[17] = tg.random_trace(rng, 40, 10, max_len=5, sorted_first=True)
+    batch = tg.concat(traces)
+    off = 64 * rng.integers(0, 4, 40)
+    expect = _batch_expect(traces, batch, off)
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, off), capacity=max(1, expect.shape[0]),
+                                            assume_sorted=True, max_trace_len=64)
+    assert st == binding.MP_OK and cnt == expect.shape[0]
+    assert np.array_equal(host(pairs), expect)
+
+
 def test_validate_status_codes():
     binding = need_gpu()
     t = tg.chain256()
