@@ -80,11 +80,14 @@ int32_t mp_status_reset(int32_t* status_out, void* stream);
  *   offset_out[n_tensors] int64, peak_out[n_traces] int64 (arena bytes),
  *   lb_out[n_traces]   int64 or NULL: max over ops of the live bytes, a lower
  *                      bound on any valid arena size.
- *   workspace          unused (may be NULL, 0 bytes).
+ *   workspace          device memory of mp_workspace_size(MP_OP_PLAN_BATCH, 0,
+ *                      n_traces, max_trace_len) bytes (each trace's lists of
+ *                      lifetime-intersecting pairs); contents need no
+ *                      initialisation; not used after the call completes.
  * Capacity limits (MP_ENOSPC on device): per trace, sum of sizes divided by
- * 2^ctz(OR of sizes) must be < 2^32, and the number of (earlier-ranked,
- * lifetime-intersecting) tensor pairs must fit the LDS pair list reported by
- * mp_batch_pair_capacity(max_trace_len).  Use mp_plan_trace beyond them. */
+ * 2^ctz(OR of sizes) must be < 2^32, and the number of lifetime-intersecting
+ * tensor pairs must not exceed mp_batch_pair_capacity(max_trace_len).  Use
+ * mp_plan_trace beyond them. */
 int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
                       const int64_t* size, const int32_t* first, const int32_t* last,
                       int64_t n_tensors, int64_t max_trace_len, int32_t policy,
@@ -93,7 +96,8 @@ int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num
                       void* stream);
 
 /* Pair-list capacity per trace of mp_plan_batch for a given max_trace_len
- * (host query, no device work); -1 when max_trace_len is out of range. */
+ * (host query, no device work): every pair of such a trace, at most 64 per
+ * tensor and at most 65520; -1 when max_trace_len is out of range. */
 int64_t mp_batch_pair_capacity(int64_t max_trace_len);
 
 /* Greedy-by-size plan of one trace of any length, using the whole device
@@ -115,12 +119,14 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
 /* Workspace sizes (host query).  op: MP_OP_LIVE_BYTES (uses num_ops),
  * MP_OP_VALIDATE (uses n_tensors and capacity), MP_OP_PLAN_TRACE (uses
  * n_tensors and num_ops), MP_OP_VALIDATE_BATCH (uses n_tensors, capacity and
- * the number of traces passed as num_ops).  Returns 0 for an unknown op or
- * negative sizes. */
+ * the number of traces passed as num_ops), MP_OP_PLAN_BATCH (the number of
+ * traces passed as num_ops, max_trace_len as capacity).  Returns 0 for an
+ * unknown op or out-of-range sizes. */
 #define MP_OP_LIVE_BYTES 1
 #define MP_OP_VALIDATE 2
 #define MP_OP_PLAN_TRACE 3
 #define MP_OP_VALIDATE_BATCH 4
+#define MP_OP_PLAN_BATCH 5
 size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops, int64_t capacity);
 
 /* Per-op live bytes of one trace (the quantity whose maximum lower-bounds

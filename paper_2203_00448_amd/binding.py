@@ -15,7 +15,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
-OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH = 1, 2, 3, 4
+OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH, OP_PLAN_BATCH = 1, 2, 3, 4, 5
 HINT_SORTED_FIRST = 1
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
@@ -109,7 +109,7 @@ def batch_pair_capacity(max_trace_len: int) -> int:
 
 def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None = None,
                policy: int = LOWEST_FIT, with_lb: bool = True, check: bool = True,
-               out=None, status=None, stream=None):
+               out=None, status=None, stream=None, workspace=None):
     """Greedy-by-size plans of many traces (mp_plan_batch).
 
     begin int64[B+1], num_ops int32[B], size int64[N], first/last int32[N], all
@@ -139,9 +139,10 @@ def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None =
         offset, peak, lb = out
     if status is None:
         status = new_status(dev, stream)
+    ws, need = _workspace(OP_PLAN_BATCH, dev, 0, n_traces, max_trace_len, workspace)
     rc = L.mp_plan_batch(_p(begin), n_traces, _p(num_ops), _p(size), _p(first), _p(last), n,
                          int(max_trace_len), int(policy), _p(offset), _p(peak), _p(lb),
-                         None, 0, _p(status), _stream(stream))
+                         _p(ws), need, _p(status), _stream(stream))
     _finish(rc, status, "plan_batch", check)
     return offset, peak, lb
 

@@ -37,18 +37,17 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
                                  int64_t* offset_out, int64_t* peak_out, int64_t* lb_out,
                                  void* workspace, size_t workspace_bytes, int32_t* status_out,
                                  void* stream) {
-    (void)workspace;
-    (void)workspace_bytes;
     if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || !status_out) return MP_EINVAL;
     if (policy != MP_LOWEST_FIT) return MP_EINVAL;
     if (!batch_shape(max_trace_len).ok) return MP_EINVAL;
     if (!begin) return MP_EINVAL;
-    if (n_traces > 0 && (!num_ops || !peak_out)) return MP_EINVAL;
+    if (n_traces > 0 && (!num_ops || !peak_out || !workspace)) return MP_EINVAL;
     if (n_tensors > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
+    if (workspace_bytes < plan_batch_workspace_bytes(n_traces, max_trace_len)) return MP_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (n_traces == 0) return MP_OK;
-    BatchArgs a{begin,      n_traces, num_ops,  size,   first,     last,
-                n_tensors,  max_trace_len, offset_out, peak_out, lb_out, status_out};
+    BatchArgs a{begin,      n_traces,      num_ops,    size,     first,  last,       n_tensors,
+                max_trace_len, offset_out, peak_out, lb_out, status_out, workspace};
     return launched(launch_plan_batch(a, st));
 }
 
@@ -60,6 +59,8 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
             return num_ops > INT32_MAX ? 0 : live_workspace_bytes((int32_t)num_ops);
         case MP_OP_VALIDATE:
             return validate_workspace_bytes(n_tensors, capacity, 1);
+        case MP_OP_PLAN_BATCH:
+            return num_ops > INT32_MAX ? 0 : plan_batch_workspace_bytes(num_ops, capacity);
         case MP_OP_VALIDATE_BATCH:
             return num_ops > INT32_MAX ? 0 : validate_workspace_bytes(n_tensors, capacity, num_ops);
         case MP_OP_PLAN_TRACE:

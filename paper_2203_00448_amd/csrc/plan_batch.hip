@@ -55,8 +55,8 @@ constexpr uint32_t kSmallK = 16;           // neighbours of a tensor fitted by a
 constexpr uint32_t kMidK = 64;             // ... by a 16-lane row; more: by the whole wave
 constexpr int kSlots = 4;                  // neighbours per lane in quads, rows and waves
 constexpr uint32_t kCoopChunk = 64u * kSlots;
-constexpr uint32_t kBigClass = 0x80000000u;  // pending-count flag: more than kSmallK neighbours
-constexpr uint32_t kCountMask = 0x7FFFFFFFu;
+constexpr uint32_t kBigClass = 0x8000u;    // pending-count flag: more than kSmallK neighbours
+constexpr uint32_t kCountMask = 0x7FFFu;
 
 // A tensor's LDS word: offset (units) in the high half, size (units) in the
 // low half; the offset half is kUnplaced until the tensor is placed.  An
@@ -67,11 +67,34 @@ __device__ __forceinline__ uint32_t word_end(uint64_t w) {
     return (uint32_t)(w >> 32) + (uint32_t)w;
 }
 
+// 16-bit counters packed two per 32-bit LDS word (entry i in half i & 1;
+// LDS atomics are 32-bit).  No entry ever leaves [0, 2^16), so a carry or
+// borrow never reaches the neighbouring half.
+__device__ __forceinline__ uint32_t half_shift(uint32_t i) { return (i & 1u) << 4; }
+__device__ __forceinline__ uint32_t packed_get(const uint32_t* w, uint32_t i) {
+    return (w[i >> 1] >> half_shift(i)) & 0xFFFFu;
+}
+__device__ __forceinline__ uint32_t packed_add(uint32_t* w, uint32_t i, uint32_t v) {
+    return (atomicAdd(w + (i >> 1), v << half_shift(i)) >> half_shift(i)) & 0xFFFFu;
+}
+__device__ __forceinline__ uint32_t packed_sub(uint32_t* w, uint32_t i, uint32_t v) {
+    return (atomicSub(w + (i >> 1), v << half_shift(i)) >> half_shift(i)) & 0xFFFFu;
+}
+
 // Neighbour q' of q ranks after q (a successor) iff it is smaller, or equal
 // in size and later in position order.
 __device__ __forceinline__ bool ranks_after(uint32_t s_other, uint32_t id_other, uint32_t s,
                                             uint32_t q) {
     return (s_other < s) | ((s_other == s) & (id_other > q));
+}
+
+// Neighbour k of tensor q in its neighbour sequence: the left list first
+// (k < L), then the right band q + 1 .. q + R.  `lv` is the left-list entry
+// lst[lb + k] (ignored for k >= L).  Slots past the end (k >= K) map to q
+// itself, which is unplaced and never a successor of itself.
+__device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
+                                              uint32_t lv) {
+    return k < L ? lv : (k < K ? q + 1 + (k - L) : q);
 }
 
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
@@ -135,23 +158,23 @@ __device__ void bitonic_sort_u64(uint64_t* keys, int m) {
     }
 }
 
-// Neighbour k of tensor q in its neighbour sequence: the left list first
-// (k < L), then the right band q + 1 .. q + R.  `lv` is the left-list entry
-// lst[lb + k] (ignored for k >= L).  Slots past the end (k >= K) map to q
-// itself, which is unplaced and never a successor of itself.
-__device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
-                                              uint32_t lv) {
-    return k < L ? lv : (k < K ? q + 1 + (k - L) : q);
-}
 
 // Ready lists, one per class (at most kSmallK neighbours, or more).  Each
 // tensor is appended once; the tensors released during a round go after
-// `end` (the end of the round's own range), counted by `cnt`.
+// `end` (the end of the round's own range), counted in one word: small class
+// in the low 16 bits, big class in the high 16 (a round releases fewer than
+// 2^16 tensors of a class, since a trace has at most 4096).
+// Both lists share one array of N slots: the small class fills it from the
+// front, the big class from the back (a tensor is appended once).
 struct ReadyLists {
-    uint16_t* slot[2];
+    uint16_t* slot;
+    uint32_t last;  // N - 1
     uint32_t end[2];
-    uint32_t* cnt[2];
+    uint32_t* cnt;
 };
+__device__ __forceinline__ uint32_t list_index(const ReadyLists& rl, int c, uint32_t k) {
+    return c ? rl.last - k : k;
+}
 
 // Exclusive prefix over the wave's lanes of a small count v (< 8), and the
 // wave total: one ballot per bit.  All 64 lanes must be active.
@@ -178,9 +201,16 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
                                                    const uint32_t (&ids)[M], uint32_t* rem,
                                                    const ReadyLists& rl, int lane) {
     static_assert(M < 8, "counts must fit three bits");
-    uint32_t old[M];
+    uint32_t old[M], any_dec = 0;
 #pragma unroll
-    for (int j = 0; j < M; ++j) old[j] = atomicSub(rem + ids[j], dec[j]);
+    for (int j = 0; j < M; ++j) {
+        old[j] = 0;
+        any_dec |= dec[j];
+    }
+    if (any_dec) {
+#pragma unroll
+        for (int j = 0; j < M; ++j) old[j] = packed_sub(rem, ids[j], dec[j]);
+    }
     uint32_t ready[2] = {0, 0};
 #pragma unroll
     for (int j = 0; j < M; ++j) {
@@ -188,17 +218,20 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
         ready[0] |= (r && !(old[j] & kBigClass) ? 1u : 0u) << j;
         ready[1] |= (r && (old[j] & kBigClass) ? 1u : 0u) << j;
     }
+    const bool any0 = __ballot(ready[0] != 0) != 0, any1 = __ballot(ready[1] != 0) != 0;
+    if (!any0 && !any1) return;
+    uint32_t tot0 = 0, tot1 = 0, pre0 = 0, pre1 = 0;
+    if (any0) pre0 = wave_prefix_small((uint32_t)__popc(ready[0]), tot0);
+    if (any1) pre1 = wave_prefix_small((uint32_t)__popc(ready[1]), tot1);
+    uint32_t base = 0;
+    if (lane == 0) base = atomicAdd(rl.cnt, tot0 | (tot1 << 16));
+    base = (uint32_t)__builtin_amdgcn_readlane((int)base, 0);
+    uint32_t at0 = rl.end[0] + (base & 0xFFFFu) + pre0;
+    uint32_t at1 = rl.end[1] + (base >> 16) + pre1;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-        if (!__ballot(ready[c] != 0)) continue;
-        uint32_t total;
-        const uint32_t pre = wave_prefix_small((uint32_t)__popc(ready[c]), total);
-        uint32_t base = 0;
-        if (lane == 0) base = atomicAdd(rl.cnt[c], total);
-        uint32_t at = rl.end[c] + (uint32_t)__builtin_amdgcn_readlane((int)base, 0) + pre;
-#pragma unroll
-        for (int j = 0; j < M; ++j)
-            if (ready[c] >> j & 1u) rl.slot[c][at++] = (uint16_t)ids[j];
+    for (int j = 0; j < M; ++j) {
+        if (ready[0] >> j & 1u) rl.slot[at0++] = (uint16_t)ids[j];
+        if (ready[1] >> j & 1u) rl.slot[rl.last - at1++] = (uint16_t)ids[j];
     }
 }
 
@@ -218,7 +251,7 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
 #pragma unroll
         for (int r = 0; r < kSlots; ++r) {
             const uint32_t k = kb + r * kWave + lane;
-            lv[r] = lst[k < L ? lb + k : lb];  // in bounds: the list area is padded
+            lv[r] = lst[k < L ? lb + k : lb];  // in bounds: the lists are padded
         }
         uint64_t w[kSlots];
 #pragma unroll
@@ -267,45 +300,45 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
     }
 }
 
-// A tensor being fitted by a lane group: its id, size, left-list start, left
-// length and neighbour count (all lanes of the group hold the same values).
+// A tensor being fitted by a lane group: its position, size, left-list start,
+// left length and neighbour count (all lanes of the group hold the same
+// values).
 struct Item {
     uint32_t q, s, lb, L, K;
 };
 
 __device__ __forceinline__ Item load_item(uint32_t q, bool has, const uint64_t* ofsz,
-                                          const uint16_t* lbeg, const uint16_t* reach) {
+                                          const uint16_t* lbeg, const uint16_t* rlen) {
     Item it{0, 0, 0, 0, 0};
     if (has) {
         it.q = q;
         it.s = (uint32_t)ofsz[q];
         it.lb = lbeg[q];
         it.L = (uint32_t)lbeg[q + 1] - it.lb;
-        it.K = it.L + (uint32_t)reach[q] - q - 1;
+        it.K = it.L + rlen[q];
     }
     return it;
 }
 
 // The neighbours k = g + G * r (r < kSlots) of a group's tensor, for the
-// lane at position g of a group of G lanes: ids, ranges [o, e) (o = kUnplaced
-// for an unplaced or missing neighbour, which never overlaps) and sizes.
-// `live` is false for groups without a tensor.
+// lane at position g of a group of G lanes: positions, ranges [o, e) (o =
+// kUnplaced for an unplaced or missing neighbour, which never overlaps) and
+// successor flags.  `live` is false for groups without a tensor.
 template <int G>
 __device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t g,
                                              const uint64_t* ofsz, const uint16_t* lst,
                                              uint32_t (&id)[kSlots], uint32_t (&o)[kSlots],
-                                             uint32_t (&e)[kSlots], uint32_t (&z)[kSlots]) {
+                                             uint32_t (&e)[kSlots], uint32_t (&sc)[kSlots]) {
     uint32_t lv[kSlots];
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
         const uint32_t k = g + G * r;
-        lv[r] = lst[k < it.L ? it.lb + k : it.lb];  // in bounds: the list area is padded
+        lv[r] = lst[k < it.L ? it.lb + k : it.lb];  // in bounds: the lists are padded
     }
     uint64_t w[kSlots];
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
-        const uint32_t k = g + G * r;
-        id[r] = live ? neighbour(k, it.L, it.K, it.q, lv[r]) : 0u;
+        id[r] = live ? neighbour(g + G * r, it.L, it.K, it.q, lv[r]) : 0u;
         w[r] = ofsz[id[r]];
     }
 #pragma unroll
@@ -313,7 +346,7 @@ __device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t
         const bool in = live && (g + G * r) < it.K;
         o[r] = in ? word_off(w[r]) : kUnplaced;
         e[r] = word_end(w[r]);
-        z[r] = (uint32_t)w[r];
+        sc[r] = (in && ranks_after((uint32_t)w[r], id[r], it.s, it.q)) ? 1u : 0u;
     }
 }
 
@@ -327,48 +360,67 @@ __device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[kSlots],
     return m;
 }
 
+// LDS byte offsets of the regions (N = tensor slots):
+//   A [8N+8]   first[N] (i32) and live-bytes deltas[N+1] (u32, upper half)
+//              -> placement words ofsz[N]
+//   B [2N+4]   band lengths -> band starts (u16)  -> ready lists (u16)
+//   C [2N+4]   left-list fill cursors (packed u16)
+//   D [2N+4]   reach histogram (packed u16)       -> pending predecessor counts
+//   E [2N+4]   left-list starts (u16)
+//   F [2N+4]   band lengths (u16), kept for placement
+// The u64 sort keys of an unsorted trace use the space from 0 before the
+// reach pass.  The left lists themselves live in the global workspace.
+struct BatchLds {
+    size_t a, b, c, d, e, f, total;
+};
+__host__ __device__ inline BatchLds batch_lds(size_t N) {
+    BatchLds L{};
+    const size_t w16 = (2 * N + 4 + 3) & ~(size_t)3;  // N + 1 u16 entries, 4-byte multiple
+    L.a = 0;
+    L.b = 8 * N + 8;
+    L.c = L.b + w16;
+    L.d = L.c + w16;
+    L.e = L.d + w16;
+    L.f = L.e + w16;
+    L.total = L.f + w16;
+    return L;
+}
+
 template <int BLOCK, int ITEMS>
-__global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
+__global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const int64_t* __restrict__ begin, const int32_t* __restrict__ num_ops,
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, int64_t n_tensors, int32_t cap_n, int32_t cap_pairs,
-    int64_t* __restrict__ offset_out, int64_t* __restrict__ peak_out,
-    int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
+    uint16_t* __restrict__ lists, int64_t* __restrict__ offset_out,
+    int64_t* __restrict__ peak_out, int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint64_t red[BLOCK / kWave];
-    __shared__ uint32_t nready[2][3];  // per class: tensors appended in rounds r % 3
+    __shared__ uint32_t nready[3];  // tensors appended in rounds r % 3 (classes packed)
 
-    // LDS layout (N = cap_n tensor slots, P = cap_pairs list slots):
-    //   A [8N]     first[N] (i32)                  -> placement words ofsz[N]
-    //   B [4N+4]   band lengths -> band starts     -> ready queue (u16)
-    //   C [4N+4]   live-bytes deltas -> left-list fill cursors
-    //   D [4N+4]   reach histogram -> pending predecessor counts
-    //   E [2N+2]   left-list starts (u16)
-    //   F [2N]     reach (u16)
-    //   G [2P+32]  left lists (u16 positions; padded for unconditional reads)
-    //   D..G hold the u64 sort keys of an unsorted trace before the reach pass.
     const size_t N = (size_t)cap_n;
-    int32_t* fst = reinterpret_cast<int32_t*>(smem);
-    uint64_t* ofsz = reinterpret_cast<uint64_t*>(smem);
-    const uint32_t* szw = reinterpret_cast<const uint32_t*>(smem);  // size half at 2q
-    uint32_t* band = reinterpret_cast<uint32_t*>(smem + 8 * N);
-    uint16_t* readyq = reinterpret_cast<uint16_t*>(smem + 8 * N);
-    uint32_t* live = reinterpret_cast<uint32_t*>(smem + 12 * N + 4);
-    uint32_t* cursor = live;
-    uint32_t* hist = reinterpret_cast<uint32_t*>(smem + 16 * N + 8);
+    const BatchLds R = batch_lds(N);
+    int32_t* fst = reinterpret_cast<int32_t*>(smem + R.a);
+    uint32_t* live = reinterpret_cast<uint32_t*>(smem + R.a + 4 * N);
+    uint64_t* ofsz = reinterpret_cast<uint64_t*>(smem + R.a);
+    const uint32_t* szw = reinterpret_cast<const uint32_t*>(smem + R.a);  // size half at 2q
+    uint64_t* keys = reinterpret_cast<uint64_t*>(smem);
+    uint16_t* band = reinterpret_cast<uint16_t*>(smem + R.b);
+    uint16_t* readyq = reinterpret_cast<uint16_t*>(smem + R.b);
+    uint32_t* cursor = reinterpret_cast<uint32_t*>(smem + R.c);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(smem + R.d);
     uint32_t* rem = hist;
-    uint64_t* keys = reinterpret_cast<uint64_t*>(smem + 16 * N + 8);
-    uint16_t* lbeg = reinterpret_cast<uint16_t*>(smem + 20 * N + 12);
-    uint16_t* reach = reinterpret_cast<uint16_t*>(smem + 22 * N + 14);
-    uint16_t* lst = reinterpret_cast<uint16_t*>(smem + 24 * N + 14);
+    uint16_t* lbeg = reinterpret_cast<uint16_t*>(smem + R.e);
+    uint16_t* rlen = reinterpret_cast<uint16_t*>(smem + R.f);
     uint32_t* scratch = reinterpret_cast<uint32_t*>(red);
 
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
+    // this trace's workspace: ids by position (unsorted traces), left lists
+    uint16_t* perm = lists + b * ((int64_t)cap_n + (int64_t)cap_pairs + 16);
+    uint16_t* lst = perm + cap_n;
     MP_STAMP(0);
     if (tid == 0) {
-        nready[0][0] = nready[0][1] = nready[0][2] = 0;
-        nready[1][0] = nready[1][1] = nready[1][2] = 0;
+        nready[0] = nready[1] = nready[2] = 0;
     }
     const int64_t lo = begin[b], hi = begin[b + 1];
     const int32_t n_ops = num_ops[b];
@@ -378,24 +430,17 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     }
     const int n = (int)(hi - lo);
 
-    // ---- ingest + checks (ids owned strided: i = tid + k * BLOCK)
-    int64_t s_r[ITEMS];
-    int32_t f_r[ITEMS], l_r[ITEMS], id_r[ITEMS];
+    // ---- ingest + checks (ids owned strided: i = tid + k * BLOCK).  No
+    // per-tensor value stays in registers across phases: each phase reloads
+    // what it needs (from L2 after this first pass).
     uint32_t flags = 0;  // bit 0: invalid tensor, bit 1: first not sorted
     uint64_t orv = 0, sum = 0;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int i = tid + k * BLOCK;
-        s_r[k] = 1;
-        f_r[k] = 0;
-        l_r[k] = 0;
-        id_r[k] = i;
         if (i < n) {
             const int64_t s = size[lo + i];
             const int32_t f = first[lo + i], l = last[lo + i];
-            s_r[k] = s;
-            f_r[k] = f;
-            l_r[k] = l;
             if (s <= 0 || f < 0 || f > l || l >= n_ops) flags |= 1u;
             if (s > 0) {
                 orv |= (uint64_t)s;
@@ -434,49 +479,31 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         if (tid == 0) raise_status(status, MP_ENOSPC);
         return;
     }
+    const bool unsorted = (flags & 2u) != 0;
+    auto id_of = [&](int q) { return unsorted ? (int)perm[q] : q; };  // position -> id
 
     // ---- position order (first, id); recorded traces are normally sorted already
-    int m = 1;
-    while (m < n) m <<= 1;
-    if (flags & 2u) {
-#pragma unroll
-        for (int k = 0; k < ITEMS; ++k) {
-            const int i = tid + k * BLOCK;
-            if (i < m)
-                keys[i] = (i < n) ? (((uint64_t)(uint32_t)f_r[k] << 32) | (uint32_t)i) : ~0ull;
-        }
+    if (unsorted) {
+        int m = 1;
+        while (m < n) m <<= 1;
+        for (int i = tid; i < m; i += BLOCK)
+            keys[i] = (i < n) ? (((uint64_t)(uint32_t)first[lo + i] << 32) | (uint32_t)i) : ~0ull;
         __syncthreads();
         bitonic_sort_u64<BLOCK>(keys, m);
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
-            if (q < n) id_r[k] = (int32_t)(keys[q] & 0xFFFFFFFFu);
+            if (q < n) perm[q] = (uint16_t)(keys[q] & 0xFFFFu);
         }
-        __syncthreads();
+        __syncthreads();  // the keys are dead: first[] goes back in position order
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
-            if (q < n) {
-                s_r[k] = size[lo + id_r[k]];
-                f_r[k] = first[lo + id_r[k]];
-                l_r[k] = last[lo + id_r[k]];
-            }
+            if (q < n) fst[q] = first[lo + perm[q]];
         }
     }
-    uint32_t su_r[ITEMS];
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        su_r[k] = 0;
-        if (q < n) {
-            su_r[k] = (uint32_t)((uint64_t)s_r[k] >> sh);
-            fst[q] = f_r[k];
-        }
-    }
-    for (int i = tid; i <= n; i += BLOCK) {
-        live[i] = 0;
-        hist[i] = 0;
-    }
+    for (int i = tid; i <= n; i += BLOCK) live[i] = 0;
+    for (int i = tid; i <= (n >> 1); i += BLOCK) hist[i] = 0;
     __syncthreads();
     MP_STAMP(2);
 
@@ -485,7 +512,9 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
         if (q < n) {
-            const int32_t l = l_r[k];
+            const int id = id_of(q);
+            const int32_t l = last[lo + id];
+            const uint32_t su = (uint32_t)((uint64_t)size[lo + id] >> sh);
             int known = q, step = 1, probe = q + 1;  // first[known] <= l
             while (probe < n && fst[probe] <= l) {
                 known = probe;
@@ -498,19 +527,14 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
                 if (fst[mid] <= l) a = mid + 1;
                 else z = mid;
             }
-            reach[q] = (uint16_t)a;
-            band[q] = (uint32_t)(a - q - 1);
-            atomicAdd(&live[q], su_r[k]);
-            atomicAdd(&live[a], 0u - su_r[k]);
-            atomicAdd(&hist[a], 1u);
+            band[q] = (uint16_t)(a - q - 1);
+            rlen[q] = (uint16_t)(a - q - 1);
+            atomicAdd(&live[q], su);
+            atomicAdd(&live[a], 0u - su);
+            packed_add(hist, (uint32_t)a, 1u);
         }
     }
     __syncthreads();
-#pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {  // first[] is no longer needed
-        const int q = tid + k * BLOCK;
-        if (q < n) ofsz[q] = ((uint64_t)kUnplaced << 32) | su_r[k];
-    }
     MP_STAMP(3);
 
     // ---- one prefix pass over positions j (contiguous chunk per thread):
@@ -524,7 +548,8 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     uint32_t live_max;
     uint32_t n_pairs;
     {
-        const int chunk = (n + BLOCK - 1) / BLOCK;
+        // even-sized chunks: both halves of a packed word stay with one thread
+        const int chunk = (((n + BLOCK - 1) / BLOCK) + 1) & ~1;
         const int a0 = min(n, tid * chunk), a1 = min(n, a0 + chunk);
         auto pack = [](uint32_t bl, uint32_t h, uint32_t j) {
             return ((uint64_t)bl << 38) | ((uint64_t)h << 25) | (uint64_t)(h * j);
@@ -532,7 +557,7 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         uint64_t ps = 0;
         uint32_t ds = 0;
         for (int i = a0; i < a1; ++i) {
-            ps += pack(band[i], hist[i], (uint32_t)i);
+            ps += pack(band[i], packed_get(hist, (uint32_t)i), (uint32_t)i);
             ds += live[i];
         }
         uint64_t ptot;
@@ -540,30 +565,39 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         uint32_t dtot;
         uint32_t drun = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
         uint32_t lm = 0;
+        uint16_t* cursor16 = reinterpret_cast<uint16_t*>(cursor);
+        uint16_t* rem16 = reinterpret_cast<uint16_t*>(rem);
         for (int i = a0; i < a1; ++i) {
-            const uint32_t bl = band[i], h = hist[i], dl = live[i];
+            const uint32_t bl = band[i], h = packed_get(hist, (uint32_t)i), dl = live[i];
             const uint32_t hb = (uint32_t)(prun >> 25) & 0x1FFFu;
             const uint32_t rh = (uint32_t)prun & 0x1FFFFFFu;
             const uint32_t ls = (uint32_t)(i * (i - 1) / 2) - (uint32_t)i * hb + rh;
-            band[i] = (uint32_t)(prun >> 38);
+            band[i] = (uint16_t)(prun >> 38);
             lbeg[i] = (uint16_t)ls;
-            cursor[i] = ls;
-            rem[i] = 0;
+            cursor16[i] = (uint16_t)ls;
             drun += dl;
             lm = lm > drun ? lm : drun;
             prun += pack(bl, h, (uint32_t)i);
         }
+        for (int i = a0; i < a1; ++i) rem16[i] = 0;  // after this thread's hist reads
         n_pairs = (uint32_t)(ptot >> 38);
         if (tid == 0) {
-            band[n] = n_pairs;
+            band[n] = (uint16_t)n_pairs;
             lbeg[n] = (uint16_t)n_pairs;
         }
         live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), scratch);
     }
-    if (n_pairs > (uint32_t)cap_pairs) {
+    if (n_pairs > (uint32_t)cap_pairs) {  // the u16 starts above are then not used
         if (tid == 0) raise_status(status, MP_ENOSPC);
         return;
     }
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {  // first[] and the deltas are no longer needed
+        const int q = tid + k * BLOCK;
+        if (q < n)
+            ofsz[q] = ((uint64_t)kUnplaced << 32) | (uint32_t)((uint64_t)size[lo + id_of(q)] >> sh);
+    }
+    __syncthreads();
     MP_STAMP(4);
 
     // ---- left lists and pending predecessor counts, balanced over the pairs:
@@ -589,8 +623,8 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
                     sq = szw[2 * q];
                 }
                 const uint32_t j = (uint32_t)q + 1 + (p - base);
-                lst[atomicAdd(&cursor[j], 1u)] = (uint16_t)q;
-                atomicAdd(&rem[sq >= szw[2 * j] ? j : (uint32_t)q], 1u);
+                lst[packed_add(cursor, j, 1u)] = (uint16_t)q;
+                packed_add(rem, sq >= szw[2 * j] ? j : (uint32_t)q, 1u);
             }
         }
     }
@@ -600,16 +634,18 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
     // big class (flag in the pending count); tensors without predecessors
     // seed the lists
     {
+        const ReadyLists rl0{readyq, (uint32_t)N - 1, {0u, 0u}, &nready[2]};
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
             if (q < n) {
-                const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + (uint32_t)reach[q] - q - 1;
-                const uint32_t r = rem[q] | (K > kSmallK ? kBigClass : 0u);
-                rem[q] = r;
-                if ((r & kCountMask) == 0) {
-                    const int c = (r & kBigClass) ? 1 : 0;
-                    readyq[c * N + atomicAdd(&nready[c][2], 1u)] = (uint16_t)q;
+                const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
+                const bool big = K > kSmallK;
+                if (big) atomicOr(rem + (q >> 1), kBigClass << half_shift((uint32_t)q));
+                if ((packed_get(rem, (uint32_t)q) & kCountMask) == 0) {
+                    const int c = big ? 1 : 0;
+                    const uint32_t at = (atomicAdd(&nready[2], c ? 0x10000u : 1u) >> (16 * c)) & 0xFFFFu;
+                    readyq[list_index(rl0, c, at)] = (uint16_t)q;
                 }
             }
         }
@@ -633,33 +669,35 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         const uint32_t g4 = lane & 3, g16 = lane & 15;
         const uint32_t quad = (uint32_t)tid >> 2, row = (uint32_t)tid >> 4;
         constexpr uint32_t kQuads = BLOCK / 4, kRows = BLOCK / 16;
-        uint32_t b0 = 0, e0 = nready[0][2], b1 = 0, e1 = nready[1][2];
+        uint32_t b0 = 0, e0 = nready[2] & 0xFFFFu, b1 = 0, e1 = nready[2] >> 16;
         for (int round = 0; b0 < e0 || b1 < e1; ++round) {
             if (round > n) {  // cannot happen: every round places a tensor
                 if (tid == 0) raise_status(status, MP_EDEVICE);
                 break;
             }
             const int cur = round % 3, nxt = (round + 1) % 3;
-            if (tid == 0) nready[0][nxt] = nready[1][nxt] = 0;
-            const ReadyLists rl{{readyq, readyq + N}, {e0, e1}, {&nready[0][cur], &nready[1][cur]}};
+            if (tid == 0) nready[nxt] = 0;
+            const ReadyLists rl{readyq, (uint32_t)N - 1, {e0, e1}, &nready[cur]};
 #ifdef MP_PHASE_TIMING
             if (tid == 0) MP_DBG_ADD(0, 1u);
 #endif
+            // small tensors fill quads from the first wave up, big ones rows
+            // from the last wave down
             for (uint32_t it = 0;; ++it) {
-                // small tensors fill quads from the first wave up, big ones
-                // rows from the last wave down
                 const uint32_t i0 = b0 + quad + kQuads * it;
                 const uint32_t i1 = b1 + (kRows - 1 - row) + kRows * it;
                 const bool hs = i0 < e0, hb = i1 < e1;
+                const uint32_t qs = hs ? (uint32_t)readyq[i0] : 0u;
+                const uint32_t qb = hb ? (uint32_t)readyq[list_index(rl, 1, i1)] : 0u;
                 const bool any_s = __ballot(hs) != 0, any_b = __ballot(hb) != 0;
                 if (!any_s && !any_b) break;
 #ifdef MP_PHASE_TIMING
                 if (lane == 0) MP_DBG_ADD(1, 1u);
 #endif
                 if (any_s) {
-                    const Item is = load_item(hs ? readyq[i0] : 0u, hs, ofsz, lbeg, reach);
-                    uint32_t id[kSlots], o[kSlots], e[kSlots], z[kSlots];
-                    gather_group<4>(is, hs, g4, ofsz, lst, id, o, e, z);
+                    const Item is = load_item(qs, hs, ofsz, lbeg, rlen);
+                    uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
+                    gather_group<4>(is, hs, g4, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {  // jump past the highest overlapping end until none moves
                         const uint32_t m = quad_max_u32(overlap_end(o, e, x, is.s));
@@ -671,18 +709,13 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
                         if (!__ballot(mv)) break;
                     }
                     if (hs && g4 == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
-                    uint32_t dec[kSlots];
-#pragma unroll
-                    for (int r = 0; r < kSlots; ++r)
-                        dec[r] = (hs & ((g4 + 4 * r) < is.K) & ranks_after(z[r], id[r], is.s, is.q))
-                                     ? 1u : 0u;
-                    release_successors(dec, id, rem, rl, lane);
+                    release_successors(sc, id, rem, rl, lane);
                 }
                 if (any_b) {
-                    const Item ib = load_item(hb ? readyq[N + i1] : 0u, hb, ofsz, lbeg, reach);
+                    const Item ib = load_item(qb, hb, ofsz, lbeg, rlen);
                     const bool mid = hb && ib.K <= kMidK;
-                    uint32_t id[kSlots], o[kSlots], e[kSlots], z[kSlots];
-                    gather_group<16>(ib, mid, g16, ofsz, lst, id, o, e, z);
+                    uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
+                    gather_group<16>(ib, mid, g16, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {
                         const uint32_t m = row_max_u32(overlap_end(o, e, x, ib.s));
@@ -694,12 +727,7 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
                         if (!__ballot(mv)) break;
                     }
                     if (mid && g16 == 0) ofsz[ib.q] = ((uint64_t)x << 32) | ib.s;
-                    uint32_t dec[kSlots];
-#pragma unroll
-                    for (int r = 0; r < kSlots; ++r)
-                        dec[r] = (mid & ((g16 + 16 * r) < ib.K) & ranks_after(z[r], id[r], ib.s, ib.q))
-                                     ? 1u : 0u;
-                    release_successors(dec, id, rem, rl, lane);
+                    release_successors(sc, id, rem, rl, lane);
                     uint64_t wide = __ballot(hb && !mid && g16 == 0);
                     while (wide) {
                         const int src = __ffsll((long long)wide) - 1;
@@ -715,9 +743,10 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
             }
             __syncthreads();
             b0 = e0;
-            e0 += nready[0][cur];
+            const uint32_t added = nready[cur];
+            e0 += added & 0xFFFFu;
             b1 = e1;
-            e1 += nready[1][cur];
+            e1 += added >> 16;
         }
     }
     __syncthreads();
@@ -730,7 +759,7 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
         const int q = tid + k * BLOCK;
         if (q < n) {
             const uint64_t w = ofsz[q];
-            offset_out[lo + id_r[k]] = (int64_t)((uint64_t)word_off(w) << sh);
+            offset_out[lo + id_of(q)] = (int64_t)((uint64_t)word_off(w) << sh);
             const uint32_t e = word_end(w);
             pk = pk > e ? pk : e;
         }
@@ -746,14 +775,16 @@ __global__ __launch_bounds__(BLOCK) void plan_batch_kernel(
 __global__ void reset_status_kernel(int32_t* status) { *status = MP_OK; }
 
 template <int ITEMS>
-hipError_t launch_items(const BatchArgs& a, int cap_n, int cap_pairs, size_t lds, hipStream_t st) {
+hipError_t launch_items(const BatchArgs& a, const BatchShape& s, hipStream_t st) {
     auto kern = plan_batch_kernel<kBatchBlock, ITEMS>;
     hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+                                       hipFuncAttributeMaxDynamicSharedMemorySize,
+                                       (int)s.lds_bytes);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)a.n_traces), dim3(kBatchBlock), lds, st, a.begin,
-                       a.num_ops, a.size, a.first, a.last, a.n_tensors, cap_n, cap_pairs,
-                       a.offset_out, a.peak_out, a.lb_out, a.status);
+    hipLaunchKernelGGL(kern, dim3((unsigned)a.n_traces), dim3(kBatchBlock), s.lds_bytes, st,
+                       a.begin, a.num_ops, a.size, a.first, a.last, a.n_tensors, s.cap_n,
+                       s.cap_pairs, static_cast<uint16_t*>(a.workspace), a.offset_out,
+                       a.peak_out, a.lb_out, a.status);
     return hipGetLastError();
 }
 
@@ -783,26 +814,22 @@ hipError_t launch_reset_status(int32_t* status, hipStream_t st) {
     return hipGetLastError();
 }
 
-// LDS bytes per workgroup: 24 per tensor slot + 16, plus 2 per pair slot + 32.
-// Traces up to about 2000 tensors get a budget that lets two workgroups share
-// a CU's 160 KiB of LDS.  Pair slots stay below 2^16 (left-list starts are
-// u16), which both budgets imply.  The sort keys (8 bytes per power-of-two
-// slot) must fit from region D on.
+// LDS bytes per workgroup: about 18 per tensor slot, so that four
+// workgroups of 2000-tensor traces share a CU's 160 KiB.  Pair capacity per
+// trace: every pair of a trace of max_trace_len tensors, at most 64 per
+// tensor and below 2^16 (list starts are u16).
 BatchShape batch_shape(int64_t max_trace_len) {
     BatchShape s{};
     if (max_trace_len < 0 || max_trace_len > MP_BATCH_MAX_TRACE_LEN) return s;
     const int64_t cap_n = max_trace_len < 1 ? 1 : max_trace_len;
-    const int64_t fixed = 24 * cap_n + 16;
-    const int64_t budget = (fixed <= 48 * 1024) ? 78 * 1024 : 156 * 1024;
-    int64_t pairs = (budget - fixed - 32) / 2;
-    pairs &= ~(int64_t)7;
-    if (pairs > 65528) pairs = 65528;
-    int64_t m = 1;
-    while (m < cap_n) m <<= 1;
-    if (8 * cap_n + 2 * pairs + 40 < 8 * m) return s;  // keys would not fit (never for <= 4096)
+    int64_t pairs = cap_n * (cap_n - 1) / 2;
+    if (pairs > 64 * cap_n) pairs = 64 * cap_n;
+    pairs = (pairs + 7) & ~(int64_t)7;
+    if (pairs < 8) pairs = 8;
+    if (pairs > 65520) pairs = 65520;
     s.cap_n = (int32_t)cap_n;
     s.cap_pairs = (int32_t)pairs;
-    s.lds_bytes = (size_t)(fixed + 2 * pairs + 32);
+    s.lds_bytes = batch_lds((size_t)cap_n).total;
     int items = 1;
     while (items * kBatchBlock < cap_n) items <<= 1;
     s.items = items;
@@ -810,14 +837,20 @@ BatchShape batch_shape(int64_t max_trace_len) {
     return s;
 }
 
+size_t plan_batch_workspace_bytes(int64_t n_traces, int64_t max_trace_len) {
+    const BatchShape s = batch_shape(max_trace_len);
+    if (!s.ok || n_traces < 0) return 0;
+    return (size_t)n_traces * ((size_t)s.cap_n + (size_t)s.cap_pairs + 16) * sizeof(uint16_t);
+}
+
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st) {
     const BatchShape s = batch_shape(a.max_trace_len);
     if (!s.ok) return hipErrorInvalidValue;
     switch (s.items) {
-        case 1: return launch_items<1>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
-        case 2: return launch_items<2>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
-        case 4: return launch_items<4>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
-        case 8: return launch_items<8>(a, s.cap_n, s.cap_pairs, s.lds_bytes, st);
+        case 1: return launch_items<1>(a, s, st);
+        case 2: return launch_items<2>(a, s, st);
+        case 4: return launch_items<4>(a, s, st);
+        case 8: return launch_items<8>(a, s, st);
         default: return hipErrorInvalidValue;
     }
 }

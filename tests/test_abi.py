@@ -62,13 +62,26 @@ def test_plan_batch_host_checks(lib):
                              None, 0, st, None) == b.MP_EINVAL
     assert lib.mp_plan_batch(None, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
                              None, 0, st, None) == b.MP_EINVAL
+    # missing or short workspace (the pair lists of every trace)
+    need = lib.mp_workspace_size(b.OP_PLAN_BATCH, 0, 1, 10)
+    assert need >= 45 * 2
+    assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
+                             None, need, st, None) == b.MP_EINVAL
+    assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
+                             dummy, need - 1, st, None) == b.MP_EINVAL
 
 
 def test_pair_capacity(lib):
+    from paper_2203_00448_amd import binding as b
     assert lib.mp_batch_pair_capacity(-1) == -1
     assert lib.mp_batch_pair_capacity(4097) == -1
     assert lib.mp_batch_pair_capacity(2000) >= 12000   # the 2000-tensor traces need ~11K
     assert lib.mp_batch_pair_capacity(4096) > 0
+    assert lib.mp_batch_pair_capacity(100) >= 100 * 99 // 2   # short traces: every pair
+    # workspace grows with the traces and the capacity
+    assert lib.mp_workspace_size(b.OP_PLAN_BATCH, 0, 1024, 2000) >= (
+        1024 * 2 * lib.mp_batch_pair_capacity(2000))
+    assert lib.mp_workspace_size(b.OP_PLAN_BATCH, 0, 1, 5000) == 0
 
 
 def test_other_host_checks(lib):
