@@ -55,8 +55,9 @@ constexpr uint32_t kSmallK = 16;           // neighbours of a tensor fitted by a
 constexpr uint32_t kMidK = 64;             // ... by a 16-lane row; more: by the whole wave
 constexpr int kSlots = 4;                  // neighbours per lane in quads, rows and waves
 constexpr uint32_t kCoopChunk = 64u * kSlots;
-constexpr uint32_t kBigClass = 0x8000u;    // pending-count flag: more than kSmallK neighbours
-constexpr uint32_t kCountMask = 0x7FFFu;
+constexpr uint32_t kBigClass = 0x80000000u;  // pending-count flag: more than kSmallK neighbours
+constexpr uint32_t kCountMask = 0x7FFFFFFFu;
+constexpr uint32_t kLeftSucc = 0x8000u;      // left-list entry flag: ranks after the list's owner
 
 // A tensor's LDS word: offset (units) in the high half, size (units) in the
 // low half; the offset half is kUnplaced until the tensor is placed.  An
@@ -77,24 +78,19 @@ __device__ __forceinline__ uint32_t packed_get(const uint32_t* w, uint32_t i) {
 __device__ __forceinline__ uint32_t packed_add(uint32_t* w, uint32_t i, uint32_t v) {
     return (atomicAdd(w + (i >> 1), v << half_shift(i)) >> half_shift(i)) & 0xFFFFu;
 }
-__device__ __forceinline__ uint32_t packed_sub(uint32_t* w, uint32_t i, uint32_t v) {
-    return (atomicSub(w + (i >> 1), v << half_shift(i)) >> half_shift(i)) & 0xFFFFu;
-}
-
-// Neighbour q' of q ranks after q (a successor) iff it is smaller, or equal
-// in size and later in position order.
-__device__ __forceinline__ bool ranks_after(uint32_t s_other, uint32_t id_other, uint32_t s,
-                                            uint32_t q) {
-    return (s_other < s) | ((s_other == s) & (id_other > q));
-}
 
 // Neighbour k of tensor q in its neighbour sequence: the left list first
-// (k < L), then the right band q + 1 .. q + R.  `lv` is the left-list entry
-// lst[lb + k] (ignored for k >= L).  Slots past the end (k >= K) map to q
-// itself, which is unplaced and never a successor of itself.
+// (k < L; entry lv = position | kLeftSucc when it ranks after q), then the
+// right band q + 1 .. q + R, whose members rank after q iff their size is
+// at most q's (equal sizes rank by position).  Slots past the end (k >= K)
+// map to q itself, which is unplaced and never a successor.
 __device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
                                               uint32_t lv) {
-    return k < L ? lv : (k < K ? q + 1 + (k - L) : q);
+    return k < L ? (lv & 0x0FFFu) : (k < K ? q + 1 + (k - L) : q);
+}
+__device__ __forceinline__ bool is_successor(uint32_t k, uint32_t L, uint32_t lv,
+                                             uint32_t s_other, uint32_t s) {
+    return k < L ? (lv & kLeftSucc) != 0 : s_other <= s;
 }
 
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
@@ -209,7 +205,7 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
     }
     if (any_dec) {
 #pragma unroll
-        for (int j = 0; j < M; ++j) old[j] = packed_sub(rem, ids[j], dec[j]);
+        for (int j = 0; j < M; ++j) old[j] = atomicSub(rem + ids[j], dec[j]);
     }
     uint32_t ready[2] = {0, 0};
 #pragma unroll
@@ -245,7 +241,7 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
                            uint64_t* ofsz, const uint16_t* lst, uint32_t* rem,
                            const ReadyLists& rl, int lane) {
     const uint32_t nch = (K + kCoopChunk - 1) / kCoopChunk;
-    uint32_t id[kSlots], co[kSlots], ce[kSlots], cs[kSlots];
+    uint32_t id[kSlots], co[kSlots], ce[kSlots], sc[kSlots];
     auto load = [&](uint32_t kb) {
         uint32_t lv[kSlots];
 #pragma unroll
@@ -261,9 +257,10 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
         }
 #pragma unroll
         for (int r = 0; r < kSlots; ++r) {
+            const uint32_t k = kb + r * kWave + lane;
             co[r] = word_off(w[r]);
             ce[r] = word_end(w[r]);
-            cs[r] = (uint32_t)w[r];
+            sc[r] = (k < K && is_successor(k, L, lv[r], (uint32_t)w[r], s)) ? 1u : 0u;
         }
     };
     uint32_t x = 0, clean = 0, c = 0;
@@ -290,13 +287,7 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
     if (lane == 0) ofsz[q] = ((uint64_t)x << 32) | s;
     for (uint32_t cc = 0; cc < nch; ++cc) {
         if (nch > 1) load(cc * kCoopChunk);
-        uint32_t dec[kSlots];
-#pragma unroll
-        for (int r = 0; r < kSlots; ++r) {
-            const uint32_t k = cc * kCoopChunk + r * kWave + lane;
-            dec[r] = ((k < K) & ranks_after(cs[r], id[r], s, q)) ? 1u : 0u;
-        }
-        release_successors(dec, id, rem, rl, lane);
+        release_successors(sc, id, rem, rl, lane);
     }
 }
 
@@ -346,7 +337,7 @@ __device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t
         const bool in = live && (g + G * r) < it.K;
         o[r] = in ? word_off(w[r]) : kUnplaced;
         e[r] = word_end(w[r]);
-        sc[r] = (in && ranks_after((uint32_t)w[r], id[r], it.s, it.q)) ? 1u : 0u;
+        sc[r] = (in && is_successor(g + G * r, it.L, lv[r], (uint32_t)w[r], it.s)) ? 1u : 0u;
     }
 }
 
@@ -365,7 +356,7 @@ __device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[kSlots],
 //              -> placement words ofsz[N]
 //   B [2N+4]   band lengths -> band starts (u16)  -> ready lists (u16)
 //   C [2N+4]   left-list fill cursors (packed u16)
-//   D [2N+4]   reach histogram (packed u16)       -> pending predecessor counts
+//   D [4N+4]   reach histogram (packed u16)       -> pending predecessor counts (u32)
 //   E [2N+4]   left-list starts (u16)
 //   F [2N+4]   band lengths (u16), kept for placement
 // The u64 sort keys of an unsorted trace use the space from 0 before the
@@ -380,7 +371,7 @@ __host__ __device__ inline BatchLds batch_lds(size_t N) {
     L.b = 8 * N + 8;
     L.c = L.b + w16;
     L.d = L.c + w16;
-    L.e = L.d + w16;
+    L.e = L.d + 4 * N + 4;
     L.f = L.e + w16;
     L.total = L.f + w16;
     return L;
@@ -566,7 +557,6 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         uint32_t drun = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
         uint32_t lm = 0;
         uint16_t* cursor16 = reinterpret_cast<uint16_t*>(cursor);
-        uint16_t* rem16 = reinterpret_cast<uint16_t*>(rem);
         for (int i = a0; i < a1; ++i) {
             const uint32_t bl = band[i], h = packed_get(hist, (uint32_t)i), dl = live[i];
             const uint32_t hb = (uint32_t)(prun >> 25) & 0x1FFFu;
@@ -579,7 +569,6 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             lm = lm > drun ? lm : drun;
             prun += pack(bl, h, (uint32_t)i);
         }
-        for (int i = a0; i < a1; ++i) rem16[i] = 0;  // after this thread's hist reads
         n_pairs = (uint32_t)(ptot >> 38);
         if (tid == 0) {
             band[n] = (uint16_t)n_pairs;
@@ -592,10 +581,12 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         return;
     }
 #pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {  // first[] and the deltas are no longer needed
+    for (int k = 0; k < ITEMS; ++k) {  // first[], the deltas and the histogram are dead
         const int q = tid + k * BLOCK;
-        if (q < n)
+        if (q < n) {
             ofsz[q] = ((uint64_t)kUnplaced << 32) | (uint32_t)((uint64_t)size[lo + id_of(q)] >> sh);
+            rem[q] = 0;
+        }
     }
     __syncthreads();
     MP_STAMP(4);
@@ -623,8 +614,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                     sq = szw[2 * q];
                 }
                 const uint32_t j = (uint32_t)q + 1 + (p - base);
-                lst[packed_add(cursor, j, 1u)] = (uint16_t)q;
-                packed_add(rem, sq >= szw[2 * j] ? j : (uint32_t)q, 1u);
+                const bool j_after = sq >= szw[2 * j];  // j ranks after q
+                lst[packed_add(cursor, j, 1u)] = (uint16_t)(q | (j_after ? 0u : kLeftSucc));
+                atomicAdd(&rem[j_after ? j : (uint32_t)q], 1u);
             }
         }
     }
@@ -641,8 +633,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             if (q < n) {
                 const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
                 const bool big = K > kSmallK;
-                if (big) atomicOr(rem + (q >> 1), kBigClass << half_shift((uint32_t)q));
-                if ((packed_get(rem, (uint32_t)q) & kCountMask) == 0) {
+                const uint32_t r = rem[q] | (big ? kBigClass : 0u);
+                rem[q] = r;
+                if ((r & kCountMask) == 0) {
                     const int c = big ? 1 : 0;
                     const uint32_t at = (atomicAdd(&nready[2], c ? 0x10000u : 1u) >> (16 * c)) & 0xFFFFu;
                     readyq[list_index(rl0, c, at)] = (uint16_t)q;
@@ -814,7 +807,7 @@ hipError_t launch_reset_status(int32_t* status, hipStream_t st) {
     return hipGetLastError();
 }
 
-// LDS bytes per workgroup: about 18 per tensor slot, so that four
+// LDS bytes per workgroup: about 20 per tensor slot, so that four
 // workgroups of 2000-tensor traces share a CU's 160 KiB.  Pair capacity per
 // trace: every pair of a trace of max_trace_len tensors, at most 64 per
 // tensor and below 2^16 (list starts are u16).
