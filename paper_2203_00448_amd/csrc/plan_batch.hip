@@ -51,13 +51,19 @@ __device__ unsigned int g_dbg[4096 * 8];
 namespace {
 
 constexpr int kBatchBlock = 512;
-constexpr uint32_t kSmallK = 16;           // neighbours of a tensor fitted by a lane quad
+constexpr uint32_t kPairK = 8;             // neighbours of a tensor fitted by a lane pair
+constexpr uint32_t kQuadK = 16;            // ... by a lane quad
 constexpr uint32_t kMidK = 64;             // ... by a 16-lane row; more: by the whole wave
-constexpr int kSlots = 4;                  // neighbours per lane in quads, rows and waves
+constexpr int kSlots = 4;                  // neighbours per lane in pairs, quads, rows, waves
 constexpr uint32_t kCoopChunk = 64u * kSlots;
-constexpr uint32_t kBigClass = 0x80000000u;  // pending-count flag: more than kSmallK neighbours
-constexpr uint32_t kCountMask = 0x7FFFFFFFu;
-constexpr uint32_t kLeftSucc = 0x8000u;      // left-list entry flag: ranks after the list's owner
+constexpr int kClassShift = 30;            // pending count: ready class in bits 30-31
+constexpr uint32_t kCountMask = (1u << kClassShift) - 1;
+constexpr uint32_t kLeftSucc = 0x8000u;    // left-list entry flag: ranks after the list's owner
+
+// Ready class of a tensor with K neighbours: 0 pair, 1 quad, 2 row or wave.
+__device__ __forceinline__ uint32_t ready_class(uint32_t K) {
+    return K <= kPairK ? 0u : (K <= kQuadK ? 1u : 2u);
+}
 
 // A tensor's LDS word: offset (units) in the high half, size (units) in the
 // low half; the offset half is kUnplaced until the tensor is placed.  An
@@ -122,6 +128,13 @@ __device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x121, 0xF, 0xF, false));
     return v;
 }
+// Maximum over each aligned lane pair, or over each aligned quad where
+// `quad` is set (all lanes of a group agree on it; every lane active).
+__device__ __forceinline__ uint32_t pair_quad_max_u32(uint32_t v, bool quad) {
+    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+    const uint32_t v4 = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    return quad ? v4 : v;
+}
 // Lane 0 of each quad / of each row, to every lane of it.
 __device__ __forceinline__ uint32_t quad_first(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x00, 0xF, 0xF, false);
@@ -155,48 +168,39 @@ __device__ void bitonic_sort_u64(uint64_t* keys, int m) {
 }
 
 
-// Ready lists, one per class (at most kSmallK neighbours, or more).  Each
-// tensor is appended once; the tensors released during a round go after
-// `end` (the end of the round's own range), counted in one word: small class
-// in the low 16 bits, big class in the high 16 (a round releases fewer than
-// 2^16 tensors of a class, since a trace has at most 4096).
-// Both lists share one array of N slots: the small class fills it from the
-// front, the big class from the back (a tensor is appended once).
+// The ready lists of the three classes share one array of N slots: class
+// c owns the region [region[c], region[c] + number of class-c tensors), as
+// each tensor is appended once.  Appends of a round go after `end[c]` (the
+// region position past the round's own range), counted in one 64-bit word
+// with a 16-bit field per class (a trace has at most 4096 tensors).
 struct ReadyLists {
     uint16_t* slot;
-    uint32_t last;  // N - 1
-    uint32_t end[2];
-    uint32_t* cnt;
+    uint32_t end[3];
+    unsigned long long* cnt;
 };
-__device__ __forceinline__ uint32_t list_index(const ReadyLists& rl, int c, uint32_t k) {
-    return c ? rl.last - k : k;
+
+// Inclusive sum over the 64 lanes (DPP row shifts, then row broadcasts).
+// All 64 lanes must be active.
+__device__ __forceinline__ uint32_t wave_inclusive_sum_dpp(uint32_t v) {
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+    return v;
 }
 
-// Exclusive prefix over the wave's lanes of a small count v (< 8), and the
-// wave total: one ballot per bit.  All 64 lanes must be active.
-__device__ __forceinline__ uint32_t wave_prefix_small(uint32_t v, uint32_t& total) {
-    uint32_t pre = 0, tot = 0;
-#pragma unroll
-    for (int bit = 0; bit < 3; ++bit) {
-        const uint64_t m = __ballot((v >> bit) & 1u);
-        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-            (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-        pre += below << bit;
-        tot += (uint32_t)__popcll(m) << bit;
-    }
-    total = tot;
-    return pre;
-}
-
-// Decrement the pending counts of the successors among M (<= 7) gathered
+// Decrement the pending counts of the successors among M (<= 4) gathered
 // neighbours (dec[j] is 1 for a successor, else 0: the atomics then issue
-// back to back) and append those that reach zero to their class list, one
+// back to back) and append those that reach zero to their class list: one
+// wave scan of the per-lane counts (10-bit fields, one per class) and one
 // list reservation per wave.  All 64 lanes must be active.
 template <int M>
 __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
                                                    const uint32_t (&ids)[M], uint32_t* rem,
                                                    const ReadyLists& rl, int lane) {
-    static_assert(M < 8, "counts must fit three bits");
+    static_assert(M <= 4, "a lane releases at most 4 tensors");
     uint32_t old[M], any_dec = 0;
 #pragma unroll
     for (int j = 0; j < M; ++j) {
@@ -207,27 +211,35 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
 #pragma unroll
         for (int j = 0; j < M; ++j) old[j] = atomicSub(rem + ids[j], dec[j]);
     }
-    uint32_t ready[2] = {0, 0};
+    uint32_t packed = 0;  // ready tensors of this lane, 10 bits per class
 #pragma unroll
     for (int j = 0; j < M; ++j) {
         const bool r = dec[j] && (old[j] & kCountMask) == 1u;
-        ready[0] |= (r && !(old[j] & kBigClass) ? 1u : 0u) << j;
-        ready[1] |= (r && (old[j] & kBigClass) ? 1u : 0u) << j;
+        packed += r ? 1u << (10 * (old[j] >> kClassShift)) : 0u;
     }
-    const bool any0 = __ballot(ready[0] != 0) != 0, any1 = __ballot(ready[1] != 0) != 0;
-    if (!any0 && !any1) return;
-    uint32_t tot0 = 0, tot1 = 0, pre0 = 0, pre1 = 0;
-    if (any0) pre0 = wave_prefix_small((uint32_t)__popc(ready[0]), tot0);
-    if (any1) pre1 = wave_prefix_small((uint32_t)__popc(ready[1]), tot1);
-    uint32_t base = 0;
-    if (lane == 0) base = atomicAdd(rl.cnt, tot0 | (tot1 << 16));
-    base = (uint32_t)__builtin_amdgcn_readlane((int)base, 0);
-    uint32_t at0 = rl.end[0] + (base & 0xFFFFu) + pre0;
-    uint32_t at1 = rl.end[1] + (base >> 16) + pre1;
+    if (!__ballot(packed != 0)) return;
+    const uint32_t incl = wave_inclusive_sum_dpp(packed);
+    const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
+    uint32_t pre = incl - packed;
+    unsigned long long base = 0;
+    if (lane == 0) {
+        const unsigned long long add = (unsigned long long)(tot & 0x3FFu) |
+                                       ((unsigned long long)((tot >> 10) & 0x3FFu) << 16) |
+                                       ((unsigned long long)(tot >> 20) << 32);
+        base = atomicAdd(rl.cnt, add);
+    }
+    const uint32_t blo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, 0);
+    const uint32_t bhi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), 0);
+    uint32_t at[3] = {rl.end[0] + (blo & 0xFFFFu) + (pre & 0x3FFu),
+                      rl.end[1] + (blo >> 16) + ((pre >> 10) & 0x3FFu),
+                      rl.end[2] + (bhi & 0xFFFFu) + (pre >> 20)};
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-        if (ready[0] >> j & 1u) rl.slot[at0++] = (uint16_t)ids[j];
-        if (ready[1] >> j & 1u) rl.slot[rl.last - at1++] = (uint16_t)ids[j];
+        if (dec[j] && (old[j] & kCountMask) == 1u) {
+            const uint32_t c = old[j] >> kClassShift;
+            const uint32_t k = c == 0 ? at[0]++ : (c == 1 ? at[1]++ : at[2]++);
+            rl.slot[k] = (uint16_t)ids[j];
+        }
     }
 }
 
@@ -315,8 +327,7 @@ __device__ __forceinline__ Item load_item(uint32_t q, bool has, const uint64_t* 
 // lane at position g of a group of G lanes: positions, ranges [o, e) (o =
 // kUnplaced for an unplaced or missing neighbour, which never overlaps) and
 // successor flags.  `live` is false for groups without a tensor.
-template <int G>
-__device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t g,
+__device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t g, uint32_t G,
                                              const uint64_t* ofsz, const uint16_t* lst,
                                              uint32_t (&id)[kSlots], uint32_t (&o)[kSlots],
                                              uint32_t (&e)[kSlots], uint32_t (&sc)[kSlots]) {
@@ -386,7 +397,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     int64_t* __restrict__ peak_out, int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint64_t red[BLOCK / kWave];
-    __shared__ uint32_t nready[3];  // tensors appended in rounds r % 3 (classes packed)
+    __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class)
+    __shared__ uint32_t ncls[3];              // tensors per ready class
+    __shared__ uint32_t seeds[3];             // tensors per class without predecessors
 
     const size_t N = (size_t)cap_n;
     const BatchLds R = batch_lds(N);
@@ -412,6 +425,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     MP_STAMP(0);
     if (tid == 0) {
         nready[0] = nready[1] = nready[2] = 0;
+        ncls[0] = ncls[1] = ncls[2] = 0;
+        seeds[0] = seeds[1] = seeds[2] = 0;
     }
     const int64_t lo = begin[b], hi = begin[b + 1];
     const int32_t n_ops = num_ops[b];
@@ -622,25 +637,47 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     }
     __syncthreads();
 
-    // ---- ready lists: tensors with more than kSmallK neighbours form the
-    // big class (flag in the pending count); tensors without predecessors
-    // seed the lists
+    // ---- ready classes (in the pending count) and list regions; tensors
+    // without predecessors seed the lists.  Counts and list slots are taken
+    // per wave (ballot, one atomic per class).
+    const int lane_id = tid & (kWave - 1);
+    uint32_t cls_r[ITEMS];
     {
-        const ReadyLists rl0{readyq, (uint32_t)N - 1, {0u, 0u}, &nready[2]};
+        uint32_t cc[3] = {0, 0, 0};
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
+            cls_r[k] = 3;  // no tensor
             if (q < n) {
-                const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
-                const bool big = K > kSmallK;
-                const uint32_t r = rem[q] | (big ? kBigClass : 0u);
-                rem[q] = r;
-                if ((r & kCountMask) == 0) {
-                    const int c = big ? 1 : 0;
-                    const uint32_t at = (atomicAdd(&nready[2], c ? 0x10000u : 1u) >> (16 * c)) & 0xFFFFu;
-                    readyq[list_index(rl0, c, at)] = (uint16_t)q;
-                }
+                const uint32_t c = ready_class((uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q]);
+                rem[q] |= c << kClassShift;
+                cls_r[k] = c;
             }
+#pragma unroll
+            for (int c = 0; c < 3; ++c) cc[c] += (uint32_t)__popcll(__ballot(cls_r[k] == (uint32_t)c));
+        }
+        if (lane_id == 0) {
+#pragma unroll
+            for (int c = 0; c < 3; ++c)
+                if (cc[c]) atomicAdd(&ncls[c], cc[c]);
+        }
+    }
+    __syncthreads();
+    const uint32_t region[3] = {0u, ncls[0], ncls[0] + ncls[1]};
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+        const int q = tid + k * BLOCK;
+        const bool seed = q < n && (rem[q] & kCountMask) == 0;
+#pragma unroll
+        for (int c = 0; c < 3; ++c) {
+            const uint64_t m = __ballot(seed && cls_r[k] == (uint32_t)c);
+            if (!m) continue;
+            uint32_t base = 0;
+            if (lane_id == 0) base = atomicAdd(&seeds[c], (uint32_t)__popcll(m));
+            base = (uint32_t)__builtin_amdgcn_readlane((int)base, 0);
+            const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+            if (seed && cls_r[k] == (uint32_t)c) readyq[region[c] + base + below] = (uint16_t)q;
         }
     }
     __syncthreads();
@@ -648,40 +685,47 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
     // ---- placement in rounds (Kahn's order over the predecessor DAG): round
     // r fits every tensor released in round r - 1 -- all of its predecessors
-    // are placed, and no two of them intersect -- with one lane quad per
-    // small-class tensor (four neighbours per lane) and one 16-lane row per
-    // big-class tensor (the whole wave past kMidK neighbours), packed into as
-    // few waves as possible.  A group gathers the neighbours' words (the
+    // are placed, and no two of them intersect.  Lanes are dealt out over the
+    // workgroup, quads first (tensors of 9..16 neighbours) and then lane
+    // pairs (up to 8), four neighbours per lane, so groups stay aligned; rows
+    // of 16 lanes (up to 64 neighbours; the whole wave beyond) take the rest
+    // from the last wave down.  A group gathers the neighbours' words (the
     // placed ones are exactly the predecessors), moves the candidate offset
     // past the highest overlapping end until nothing overlaps, publishes the
     // word and decrements the successors' pending counts; those reaching zero
     // are appended for the next round.  Per-round append counters rotate over
     // three slots so that one barrier per round suffices.
     {
-        const int lane = tid & (kWave - 1);
-        const uint32_t g4 = lane & 3, g16 = lane & 15;
-        const uint32_t quad = (uint32_t)tid >> 2, row = (uint32_t)tid >> 4;
-        constexpr uint32_t kQuads = BLOCK / 4, kRows = BLOCK / 16;
-        uint32_t b0 = 0, e0 = nready[2] & 0xFFFFu, b1 = 0, e1 = nready[2] >> 16;
-        for (int round = 0; b0 < e0 || b1 < e1; ++round) {
+        const int lane = lane_id;
+        const uint32_t g16 = lane & 15, row = (uint32_t)tid >> 4;
+        constexpr uint32_t kRows = BLOCK / 16;
+        uint32_t bgn[3] = {0, 0, 0}, end[3] = {seeds[0], seeds[1], seeds[2]};
+        for (int round = 0; bgn[0] < end[0] || bgn[1] < end[1] || bgn[2] < end[2]; ++round) {
             if (round > n) {  // cannot happen: every round places a tensor
                 if (tid == 0) raise_status(status, MP_EDEVICE);
                 break;
             }
             const int cur = round % 3, nxt = (round + 1) % 3;
             if (tid == 0) nready[nxt] = 0;
-            const ReadyLists rl{readyq, (uint32_t)N - 1, {e0, e1}, &nready[cur]};
+            const ReadyLists rl{readyq,
+                                {region[0] + end[0], region[1] + end[1], region[2] + end[2]},
+                                &nready[cur]};
 #ifdef MP_PHASE_TIMING
             if (tid == 0) MP_DBG_ADD(0, 1u);
 #endif
-            // small tensors fill quads from the first wave up, big ones rows
-            // from the last wave down
+            const uint32_t nq = end[1] - bgn[1], np = end[0] - bgn[0];
             for (uint32_t it = 0;; ++it) {
-                const uint32_t i0 = b0 + quad + kQuads * it;
-                const uint32_t i1 = b1 + (kRows - 1 - row) + kRows * it;
-                const bool hs = i0 < e0, hb = i1 < e1;
-                const uint32_t qs = hs ? (uint32_t)readyq[i0] : 0u;
-                const uint32_t qb = hb ? (uint32_t)readyq[list_index(rl, 1, i1)] : 0u;
+                const uint32_t gl = it * BLOCK + (uint32_t)tid;  // lane slot over the workgroup
+                const bool quad = gl < 4 * nq;
+                const bool hs = quad || gl < 4 * nq + 2 * np;
+                const uint32_t g = quad ? (gl & 3u) : (gl & 1u);
+                const uint32_t i1 = bgn[2] + (kRows - 1 - row) + kRows * it;
+                const bool hb = i1 < end[2];
+                uint32_t qs = 0;
+                if (hs)
+                    qs = quad ? readyq[region[1] + bgn[1] + (gl >> 2)]
+                              : readyq[region[0] + bgn[0] + ((gl - 4 * nq) >> 1)];
+                const uint32_t qb = hb ? (uint32_t)readyq[region[2] + i1] : 0u;
                 const bool any_s = __ballot(hs) != 0, any_b = __ballot(hb) != 0;
                 if (!any_s && !any_b) break;
 #ifdef MP_PHASE_TIMING
@@ -690,10 +734,10 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 if (any_s) {
                     const Item is = load_item(qs, hs, ofsz, lbeg, rlen);
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group<4>(is, hs, g4, ofsz, lst, id, o, e, sc);
+                    gather_group(is, hs, g, quad ? 4u : 2u, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {  // jump past the highest overlapping end until none moves
-                        const uint32_t m = quad_max_u32(overlap_end(o, e, x, is.s));
+                        const uint32_t m = pair_quad_max_u32(overlap_end(o, e, x, is.s), quad);
                         const bool mv = m > x;
                         x = mv ? m : x;
 #ifdef MP_PHASE_TIMING
@@ -701,14 +745,14 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 #endif
                         if (!__ballot(mv)) break;
                     }
-                    if (hs && g4 == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
+                    if (hs && g == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
                     release_successors(sc, id, rem, rl, lane);
                 }
                 if (any_b) {
                     const Item ib = load_item(qb, hb, ofsz, lbeg, rlen);
                     const bool mid = hb && ib.K <= kMidK;
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group<16>(ib, mid, g16, ofsz, lst, id, o, e, sc);
+                    gather_group(ib, mid, g16, 16u, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {
                         const uint32_t m = row_max_u32(overlap_end(o, e, x, ib.s));
@@ -735,11 +779,12 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 }
             }
             __syncthreads();
-            b0 = e0;
-            const uint32_t added = nready[cur];
-            e0 += added & 0xFFFFu;
-            b1 = e1;
-            e1 += added >> 16;
+            const unsigned long long added = nready[cur];
+#pragma unroll
+            for (int c = 0; c < 3; ++c) {
+                bgn[c] = end[c];
+                end[c] += (uint32_t)(added >> (16 * c)) & 0xFFFFu;
+            }
         }
     }
     __syncthreads();
