@@ -269,19 +269,21 @@ constexpr int kVbBlock = 512;
 // write == 1: segcnt holds exclusive starts (segcnt[n_seg] = total); the
 //             pairs of trace b are written from segcnt[b] on, below `cap`.
 template <int BLOCK, int ITEMS>
-__global__ __launch_bounds__(BLOCK) void vb_kernel(
+__global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
     const int64_t* __restrict__ begin, int64_t n_seg, const int64_t* __restrict__ size,
     const int32_t* __restrict__ first, const int32_t* __restrict__ last,
     const int64_t* __restrict__ off, int64_t n, int32_t cap_n, int64_t* __restrict__ segcnt,
     int write, int64_t* __restrict__ pairs, int64_t cap, int32_t* __restrict__ status) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint32_t scratch[BLOCK / kWave];
-    // LDS: off[N] i64, size[N] i64, first[N] i32, band starts[N+1] u32
+    // LDS: first[N] i32 (reach search) -> then off[N], size[N] i64 over it;
+    // band lengths -> starts [N+1] u32 after them.  20 bytes per tensor, so
+    // four workgroups of 2000-tensor traces share a CU.
     const size_t N = (size_t)cap_n;
+    int32_t* lf = reinterpret_cast<int32_t*>(smem);
     int64_t* lo64 = reinterpret_cast<int64_t*>(smem);
     int64_t* ls64 = reinterpret_cast<int64_t*>(smem + 8 * N);
-    int32_t* lf = reinterpret_cast<int32_t*>(smem + 16 * N);
-    uint32_t* band = reinterpret_cast<uint32_t*>(smem + 20 * N);
+    uint32_t* band = reinterpret_cast<uint32_t*>(smem + 16 * N);
     const int tid = threadIdx.x;
     for (int64_t b = blockIdx.x; b < n_seg; b += gridDim.x) {
         const int64_t lo = begin[b], hi = begin[b + 1];
@@ -306,11 +308,8 @@ __global__ __launch_bounds__(BLOCK) void vb_kernel(
             const int q = tid + k * BLOCK;
             l_r[k] = 0;
             if (q < m) {
-                const int64_t sz = size[lo + q], o = off[lo + q];
                 const int32_t f = first[lo + q], l = last[lo + q];
-                if (sz <= 0 || f < 0 || f > l || o < 0 || o > INT64_MAX - sz) bad = true;
-                lo64[q] = o;
-                ls64[q] = sz;
+                if (f < 0 || f > l) bad = true;
                 lf[q] = f;
                 l_r[k] = l;
             }
@@ -336,6 +335,17 @@ __global__ __launch_bounds__(BLOCK) void vb_kernel(
                     else z = mid;
                 }
                 band[q] = (uint32_t)(a - q - 1);
+            }
+        }
+        __syncthreads();  // first[] is dead: the byte ranges go in its place
+#pragma unroll
+        for (int k = 0; k < ITEMS; ++k) {
+            const int q = tid + k * BLOCK;
+            if (q < m) {
+                const int64_t sz = size[lo + q], o = off[lo + q];
+                if (sz <= 0 || o < 0 || o > INT64_MAX - sz) bad = true;
+                lo64[q] = o;
+                ls64[q] = sz;
             }
         }
         if (!write && __ballot(bad) && (tid & (kWave - 1)) == 0) raise_status(status, MP_EINVAL);
@@ -448,7 +458,7 @@ hipError_t launch_vb(int write, const int64_t* begin, int64_t n_seg, const int64
                      int32_t cap_n, int64_t* segcnt, int64_t* pairs, int64_t cap,
                      int32_t* status, hipStream_t st) {
     auto kern = vb_kernel<kVbBlock, ITEMS>;
-    const size_t lds = 24 * (size_t)cap_n + 8;
+    const size_t lds = 20 * (size_t)cap_n + 8;
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
