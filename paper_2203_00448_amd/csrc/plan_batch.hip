@@ -310,9 +310,12 @@ struct Item {
     uint32_t q, s, lb, L, K;
 };
 
-__device__ __forceinline__ Item load_item(uint32_t q, bool has, const uint64_t* ofsz,
-                                          const uint16_t* lbeg, const uint16_t* rlen) {
-    Item it{0, 0, 0, 0, 0};
+// A lane without a tensor gets the spare word ofsz[N] (never placed, size
+// 0) as its tensor and no neighbours, so every slot reads that word.
+__device__ __forceinline__ Item load_item(uint32_t q, bool has, uint32_t spare,
+                                          const uint64_t* ofsz, const uint16_t* lbeg,
+                                          const uint16_t* rlen) {
+    Item it{spare, 0, 0, 0, 0};
     if (has) {
         it.q = q;
         it.s = (uint32_t)ofsz[q];
@@ -323,32 +326,33 @@ __device__ __forceinline__ Item load_item(uint32_t q, bool has, const uint64_t* 
     return it;
 }
 
-// The neighbours k = g + G * r (r < kSlots) of a group's tensor, for the
-// lane at position g of a group of G lanes: positions, ranges [o, e) (o =
-// kUnplaced for an unplaced or missing neighbour, which never overlaps) and
-// successor flags.  `live` is false for groups without a tensor.
-__device__ __forceinline__ void gather_group(const Item& it, bool live, uint32_t g, uint32_t G,
-                                             const uint64_t* ofsz, const uint16_t* lst,
-                                             uint32_t (&id)[kSlots], uint32_t (&o)[kSlots],
-                                             uint32_t (&e)[kSlots], uint32_t (&sc)[kSlots]) {
+// The neighbours k = 4g + r (r < kSlots) of a group's tensor, for the lane
+// at position g of its group: positions, ranges [o, e) and successor flags.
+// Slots past the neighbour count read the tensor's own word, which is
+// unplaced: an unplaced word never overlaps (its offset half is kUnplaced).
+__device__ __forceinline__ void gather_group(const Item& it, uint32_t g, const uint64_t* ofsz,
+                                             const uint16_t* lst, uint32_t (&id)[kSlots],
+                                             uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
+                                             uint32_t (&sc)[kSlots]) {
+    const uint32_t k0 = g * kSlots;
     uint32_t lv[kSlots];
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
-        const uint32_t k = g + G * r;
+        const uint32_t k = k0 + r;
         lv[r] = lst[k < it.L ? it.lb + k : it.lb];  // in bounds: the lists are padded
     }
     uint64_t w[kSlots];
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
-        id[r] = live ? neighbour(g + G * r, it.L, it.K, it.q, lv[r]) : 0u;
+        id[r] = neighbour(k0 + r, it.L, it.K, it.q, lv[r]);
         w[r] = ofsz[id[r]];
     }
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
-        const bool in = live && (g + G * r) < it.K;
-        o[r] = in ? word_off(w[r]) : kUnplaced;
+        const uint32_t k = k0 + r;
+        o[r] = word_off(w[r]);
         e[r] = word_end(w[r]);
-        sc[r] = (in && is_successor(g + G * r, it.L, lv[r], (uint32_t)w[r], it.s)) ? 1u : 0u;
+        sc[r] = (k < it.K && is_successor(k, it.L, lv[r], (uint32_t)w[r], it.s)) ? 1u : 0u;
     }
 }
 
@@ -595,6 +599,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         if (tid == 0) raise_status(status, MP_ENOSPC);
         return;
     }
+    const uint32_t spare = (uint32_t)N;  // ofsz[N]: never placed, size 0
+    if (tid == 0) ofsz[spare] = (uint64_t)kUnplaced << 32;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {  // first[], the deltas and the histogram are dead
         const int q = tid + k * BLOCK;
@@ -732,9 +738,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 if (lane == 0) MP_DBG_ADD(1, 1u);
 #endif
                 if (any_s) {
-                    const Item is = load_item(qs, hs, ofsz, lbeg, rlen);
+                    const Item is = load_item(qs, hs, spare, ofsz, lbeg, rlen);
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group(is, hs, g, quad ? 4u : 2u, ofsz, lst, id, o, e, sc);
+                    gather_group(is, g, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {  // jump past the highest overlapping end until none moves
                         const uint32_t m = pair_quad_max_u32(overlap_end(o, e, x, is.s), quad);
@@ -749,13 +755,14 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                     release_successors(sc, id, rem, rl, lane);
                 }
                 if (any_b) {
-                    const Item ib = load_item(qb, hb, ofsz, lbeg, rlen);
+                    const Item ib = load_item(qb, hb, spare, ofsz, lbeg, rlen);
                     const bool mid = hb && ib.K <= kMidK;
+                    const Item im = mid ? ib : Item{spare, 0, 0, 0, 0};  // wider: whole wave
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group(ib, mid, g16, 16u, ofsz, lst, id, o, e, sc);
+                    gather_group(im, g16, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {
-                        const uint32_t m = row_max_u32(overlap_end(o, e, x, ib.s));
+                        const uint32_t m = row_max_u32(overlap_end(o, e, x, im.s));
                         const bool mv = m > x;
                         x = mv ? m : x;
 #ifdef MP_PHASE_TIMING
