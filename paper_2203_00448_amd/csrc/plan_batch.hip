@@ -440,34 +440,56 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     }
     const int n = (int)(hi - lo);
 
-    // ---- ingest + checks (ids owned strided: i = tid + k * BLOCK).  No
-    // per-tensor value stays in registers across phases: each phase reloads
-    // what it needs (from L2 after this first pass).
+    // ---- ingest + checks (ids owned strided: i = tid + k * BLOCK).  The
+    // sizes and last ops of a sorted trace stay in registers for the band
+    // pass; later phases reload what they need (from L2).
     uint32_t flags = 0;  // bit 0: invalid tensor, bit 1: first not sorted
     uint64_t orv = 0, sum = 0;
+    int64_t sz_r[ITEMS];
+    int32_t la_r[ITEMS];
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int i = tid + k * BLOCK;
+        sz_r[k] = 0;
+        la_r[k] = 0;
         if (i < n) {
             const int64_t s = size[lo + i];
             const int32_t f = first[lo + i], l = last[lo + i];
+            if (i > 0 && first[lo + i - 1] > f) flags |= 2u;
             if (s <= 0 || f < 0 || f > l || l >= n_ops) flags |= 1u;
             if (s > 0) {
                 orv |= (uint64_t)s;
                 sum = sat_add(sum, (uint64_t)s);
             }
             fst[i] = f;
+            sz_r[k] = s;
+            la_r[k] = l;
         }
     }
-    __syncthreads();
+    // one combined reduction of the flags, the OR and the saturating sum
+    uint64_t or_all, total;
+    {
+        const int lane = tid & (kWave - 1), wid = tid / kWave;
+        flags = wave_reduce(flags, OpOr<uint32_t>());
+        orv = wave_reduce(orv, OpOr<uint64_t>());
+        sum = wave_reduce(sum, OpSatAdd());
+        __shared__ uint64_t red3[3][BLOCK / kWave];
+        if (lane == 0) {
+            red3[0][wid] = flags;
+            red3[1][wid] = orv;
+            red3[2][wid] = sum;
+        }
+        __syncthreads();
+        flags = 0;
+        or_all = 0;
+        total = 0;
 #pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int i = tid + k * BLOCK;
-        if (i > 0 && i < n && fst[i] < fst[i - 1]) flags |= 2u;
+        for (int w = 0; w < BLOCK / kWave; ++w) {
+            flags |= (uint32_t)red3[0][w];
+            or_all |= red3[1][w];
+            total = sat_add(total, red3[2][w]);
+        }
     }
-    flags = block_reduce<BLOCK>(flags, OpOr<uint32_t>(), scratch);
-    const uint64_t or_all = block_reduce<BLOCK>(orv, OpOr<uint64_t>(), red);
-    const uint64_t total = block_reduce<BLOCK>(sum, OpSatAdd(), red);
     {
         int32_t code = (flags & 1u) ? MP_EINVAL : MP_OK;
         if (total > (uint64_t)INT64_MAX) code = MP_EOVERFLOW;
@@ -517,25 +539,46 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     __syncthreads();
     MP_STAMP(2);
 
-    // ---- reach (galloping search), band lengths, live-bytes deltas, reach histogram
+    // ---- reach, band lengths, live-bytes deltas, reach histogram.  The
+    // reach is the first position past q whose first op is after last[q]:
+    // the next four positions are probed at once (short bands, the common
+    // case, end there), longer bands gallop from the fourth.
+    int32_t rch[ITEMS];
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+        const int q = tid + k * BLOCK;
+        rch[k] = q + 1;
+        if (q < n) {
+            const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
+            const int32_t f1 = q + 1 < n ? fst[q + 1] : INT32_MAX;
+            const int32_t f2 = q + 2 < n ? fst[q + 2] : INT32_MAX;
+            const int32_t f3 = q + 3 < n ? fst[q + 3] : INT32_MAX;
+            const int32_t f4 = q + 4 < n ? fst[q + 4] : INT32_MAX;
+            rch[k] = q + 1 + (f1 <= l) + (f2 <= l) + (f3 <= l) + (f4 <= l);
+        }
+    }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
         if (q < n) {
-            const int id = id_of(q);
-            const int32_t l = last[lo + id];
-            const uint32_t su = (uint32_t)((uint64_t)size[lo + id] >> sh);
-            int known = q, step = 1, probe = q + 1;  // first[known] <= l
-            while (probe < n && fst[probe] <= l) {
-                known = probe;
-                step <<= 1;
-                probe = q + step;
-            }
-            int a = known + 1, z = probe < n ? probe : n;
-            while (a < z) {
-                const int mid = (a + z) >> 1;
-                if (fst[mid] <= l) a = mid + 1;
-                else z = mid;
+            const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
+            const int64_t sz = unsorted ? size[lo + perm[q]] : sz_r[k];
+            const uint32_t su = (uint32_t)((uint64_t)sz >> sh);
+            int a = rch[k];
+            if (a == q + 5) {  // first[q + 4] <= l: gallop on
+                int known = q + 4, step = 8, probe = q + 8;  // first[known] <= l
+                while (probe < n && fst[probe] <= l) {
+                    known = probe;
+                    step <<= 1;
+                    probe = q + step;
+                }
+                a = known + 1;
+                int z = probe < n ? probe : n;
+                while (a < z) {
+                    const int mid = (a + z) >> 1;
+                    if (fst[mid] <= l) a = mid + 1;
+                    else z = mid;
+                }
             }
             band[q] = (uint16_t)(a - q - 1);
             rlen[q] = (uint16_t)(a - q - 1);
