@@ -76,7 +76,8 @@ int32_t mp_status_reset(int32_t* status_out, void* stream);
  *   size, first, last  [n_tensors] (int64, int32, int32).
  *   max_trace_len      host bound on begin[b+1] - begin[b], 0..4096; a longer
  *                      trace sets MP_EINVAL.
- *   policy             MP_LOWEST_FIT (MP_BEST_FIT returns MP_EINVAL for now).
+ *   policy             MP_LOWEST_FIT or MP_BEST_FIT (a tensor may then meet at
+ *                      most 256 others in lifetime: MP_ENOSPC on device beyond).
  *   offset_out[n_tensors] int64, peak_out[n_traces] int64 (arena bytes),
  *   lb_out[n_traces]   int64 or NULL: max over ops of the live bytes, a lower
  *                      bound on any valid arena size.
@@ -104,13 +105,13 @@ int64_t mp_batch_pair_capacity(int64_t max_trace_len);
  * (one cooperative persistent launch places the tensors).
  *   size, first, last [n] (int64, int32, int32), 0 <= n < 2^30.
  *   offset_out[n] int64, peak_out: one device int64 (arena bytes).
- *   policy: MP_LOWEST_FIT.
+ *   policy: MP_LOWEST_FIT or MP_BEST_FIT.
  *   workspace: mp_workspace_size(MP_OP_PLAN_TRACE, n, num_ops, 0) bytes; its
  *              contents need no initialisation.
  * Capacity limits (MP_ENOSPC on device): the sum of the sizes divided by
  * 2^ctz(OR of sizes) must be < 2^32, and a tensor may have at most 131072
- * earlier-ranked lifetime-intersecting tensors.  Tensors need not be sorted
- * by first. */
+ * earlier-ranked lifetime-intersecting tensors.
+ * Tensors need not be sorted by first. */
 int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
                       int32_t num_ops, int32_t policy, int64_t* offset_out, int64_t* peak_out,
                       void* workspace, size_t workspace_bytes, int32_t* status_out,

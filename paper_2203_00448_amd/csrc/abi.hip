@@ -38,7 +38,7 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
                                  void* workspace, size_t workspace_bytes, int32_t* status_out,
                                  void* stream) {
     if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || !status_out) return MP_EINVAL;
-    if (policy != MP_LOWEST_FIT) return MP_EINVAL;
+    if (policy != MP_LOWEST_FIT && policy != MP_BEST_FIT) return MP_EINVAL;
     if (!batch_shape(max_trace_len).ok) return MP_EINVAL;
     if (!begin) return MP_EINVAL;
     if (n_traces > 0 && (!num_ops || !peak_out || !workspace)) return MP_EINVAL;
@@ -47,7 +47,7 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (n_traces == 0) return MP_OK;
     BatchArgs a{begin,      n_traces,      num_ops,    size,     first,  last,       n_tensors,
-                max_trace_len, offset_out, peak_out, lb_out, status_out, workspace};
+                max_trace_len, offset_out, peak_out, lb_out, status_out, workspace, policy};
     return launched(launch_plan_batch(a, st));
 }
 
@@ -134,9 +134,9 @@ extern "C" int32_t mp_plan_trace(const int64_t* size, const int32_t* first, cons
                                  int32_t* status_out, void* stream) {
     if (n < 0 || n >= (int64_t)1 << 30 || num_ops < 0 || !status_out || !peak_out || !workspace)
         return MP_EINVAL;
-    if (policy != MP_LOWEST_FIT) return MP_EINVAL;
+    if (policy != MP_LOWEST_FIT && policy != MP_BEST_FIT) return MP_EINVAL;
     if (n > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
     if (workspace_bytes < plan_trace_workspace_bytes(n)) return MP_EINVAL;
-    return launched(launch_plan_trace(size, first, last, n, num_ops, offset_out, peak_out,
+    return launched(launch_plan_trace(size, first, last, n, num_ops, policy, offset_out, peak_out,
                                       workspace, status_out, static_cast<hipStream_t>(stream)));
 }

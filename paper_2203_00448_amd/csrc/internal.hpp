@@ -23,6 +23,7 @@ struct BatchArgs {
     int64_t* lb_out;
     int32_t* status;
     void* workspace;  // left lists: plan_batch_workspace_bytes
+    int32_t policy;   // MP_LOWEST_FIT or MP_BEST_FIT
 };
 
 struct BatchShape {
@@ -73,7 +74,7 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
 // single-trace planner (plan_trace.hip)
 size_t plan_trace_workspace_bytes(int64_t n);
 hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
-                             int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out,
-                             void* ws, int32_t* status, hipStream_t st);
+                             int64_t n, int32_t num_ops, int32_t policy, int64_t* offset_out,
+                             int64_t* peak_out, void* ws, int32_t* status, hipStream_t st);
 
 }  // namespace mp

@@ -243,6 +243,89 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
     }
 }
 
+// BEST_FIT (the tightest-gap reading of Section 2.3's "best fit"): among the
+// free gaps between the placed neighbours' ranges, the smallest one that
+// holds s units, the lowest start among equals; the space above every range
+// only when no finite gap holds s.  A group of LANES lanes holds 4 ranges
+// per lane, element i = 4 l + r at lane l (0 <= l < LANES) and slot r; the
+// group sorts them by offset (bitonic network: slots within a lane, lanes by
+// exchanges with lane l ^ d), takes running maxima of the ends in that order
+// (gap before element i: [max end of elements < i, offset of i)) and a
+// minimum over (gap length, gap start).  Unplaced ranges (offset kUnplaced)
+// sort last and bound no gap.  Every lane of the group gets the result.
+template <int LANES>
+__device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots], uint32_t s,
+                                   uint32_t l) {
+    static_assert(kSlots == 4, "4 ranges per lane");
+    constexpr int kN = 4 * LANES;
+#pragma unroll
+    for (int k = 2; k <= kN; k <<= 1) {
+#pragma unroll
+        for (int j = k >> 1; j >= 1; j >>= 1) {
+            if (j < 4) {
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int r2 = r ^ j;
+                    if (r2 > r) {
+                        const bool up = (((4u * l + (uint32_t)r) & (uint32_t)k) == 0);
+                        const bool sw = up ? (o[r] > o[r2]) : (o[r] < o[r2]);
+                        const uint32_t oa = o[r], ea = e[r];
+                        o[r] = sw ? o[r2] : oa;
+                        e[r] = sw ? e[r2] : ea;
+                        o[r2] = sw ? oa : o[r2];
+                        e[r2] = sw ? ea : e[r2];
+                    }
+                }
+            } else {
+                const int d = j >> 2;  // partner lane l ^ d, same slot
+                const bool lower = (l & (uint32_t)d) == 0;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const uint32_t po = (uint32_t)__shfl_xor((int)o[r], d, LANES);
+                    const uint32_t pe = (uint32_t)__shfl_xor((int)e[r], d, LANES);
+                    const bool up = (((4u * l + (uint32_t)r) & (uint32_t)k) == 0);
+                    const bool take = (lower == up) ? (po < o[r]) : (po > o[r]);
+                    o[r] = take ? po : o[r];
+                    e[r] = take ? pe : e[r];
+                }
+            }
+        }
+    }
+    // running maximum of the placed ends: within the lane, then over the
+    // lanes before it
+    uint32_t incl[4], run = 0;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        run = max(run, o[r] != kUnplaced ? e[r] : 0u);
+        incl[r] = run;
+    }
+    uint32_t scan = run;
+#pragma unroll
+    for (int d = 1; d < LANES; d <<= 1) {
+        const uint32_t y = (uint32_t)__shfl_up((int)scan, d, LANES);
+        if (l >= (uint32_t)d) scan = max(scan, y);
+    }
+    uint32_t before = (uint32_t)__shfl_up((int)scan, 1, LANES);
+    if (l == 0) before = 0;
+    const uint32_t top = (uint32_t)__shfl((int)scan, LANES - 1, LANES);
+    uint64_t best = ~0ull;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const uint32_t pm = r == 0 ? before : max(before, incl[r - 1]);
+        const bool ok = o[r] != kUnplaced && o[r] >= pm && o[r] - pm >= s;
+        const uint64_t key = ((uint64_t)(o[r] - pm) << 32) | pm;
+        best = (ok && key < best) ? key : best;
+    }
+#pragma unroll
+    for (int d = 1; d < LANES; d <<= 1) {
+        const uint32_t blo = (uint32_t)__shfl_xor((int)(uint32_t)best, d, LANES);
+        const uint32_t bhi = (uint32_t)__shfl_xor((int)(uint32_t)(best >> 32), d, LANES);
+        const uint64_t other = ((uint64_t)bhi << 32) | blo;
+        best = other < best ? other : best;
+    }
+    return best != ~0ull ? (uint32_t)best : top;
+}
+
 // Whole-wave placement of tensor q (all 64 lanes active, arguments uniform):
 // the neighbour sequence is swept in chunks of 256, each lane holding up to 4
 // neighbours; within a chunk the candidate offset jumps to the highest end
@@ -251,7 +334,7 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
 // successors' pending counts are decremented.
 __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint32_t K,
                            uint64_t* ofsz, const uint16_t* lst, uint32_t* rem,
-                           const ReadyLists& rl, int lane) {
+                           const ReadyLists& rl, int lane, bool best, int32_t* status) {
     const uint32_t nch = (K + kCoopChunk - 1) / kCoopChunk;
     uint32_t id[kSlots], co[kSlots], ce[kSlots], sc[kSlots];
     auto load = [&](uint32_t kb) {
@@ -275,7 +358,15 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
             sc[r] = (k < K && is_successor(k, L, lv[r], (uint32_t)w[r], s)) ? 1u : 0u;
         }
     };
-    uint32_t x = 0, clean = 0, c = 0;
+    uint32_t x = 0, clean = best ? nch : 0, c = 0;
+    if (best) {  // one chunk of at most 256 neighbours, sorted by the wave
+        if (nch > 1) {
+            if (lane == 0) raise_status(status, MP_ENOSPC);
+        } else {
+            load(0);
+            x = best_fit_group<kWave>(co, ce, s, (uint32_t)lane);
+        }
+    }
     while (clean < nch) {
         load(c * kCoopChunk);
         bool moved = false;
@@ -392,13 +483,14 @@ __host__ __device__ inline BatchLds batch_lds(size_t N) {
     return L;
 }
 
-template <int BLOCK, int ITEMS>
+template <int BLOCK, int ITEMS, bool BEST>
 __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const int64_t* __restrict__ begin, const int32_t* __restrict__ num_ops,
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, int64_t n_tensors, int32_t cap_n, int32_t cap_pairs,
     uint16_t* __restrict__ lists, int64_t* __restrict__ offset_out,
     int64_t* __restrict__ peak_out, int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
+    constexpr bool best = BEST;  // BEST_FIT: every tensor to a 16-lane row or the wave
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint64_t red[BLOCK / kWave];
     __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class)
@@ -698,7 +790,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             const int q = tid + k * BLOCK;
             cls_r[k] = 3;  // no tensor
             if (q < n) {
-                const uint32_t c = ready_class((uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q]);
+                const uint32_t c = best ? 2u : ready_class((uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q]);
                 rem[q] |= c << kClassShift;
                 cls_r[k] = c;
             }
@@ -804,7 +896,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
                     gather_group(im, g16, ofsz, lst, id, o, e, sc);
                     uint32_t x = 0;
-                    while (true) {
+                    if (best) x = best_fit_group<16>(o, e, im.s, g16);
+                    while (!best) {
                         const uint32_t m = row_max_u32(overlap_end(o, e, x, im.s));
                         const bool mv = m > x;
                         x = mv ? m : x;
@@ -824,7 +917,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                                    (uint32_t)__builtin_amdgcn_readlane((int)ib.lb, src),
                                    (uint32_t)__builtin_amdgcn_readlane((int)ib.L, src),
                                    (uint32_t)__builtin_amdgcn_readlane((int)ib.K, src), ofsz,
-                                   lst, rem, rl, lane);
+                                   lst, rem, rl, lane, best, status);
                     }
                 }
             }
@@ -862,9 +955,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
 __global__ void reset_status_kernel(int32_t* status) { *status = MP_OK; }
 
-template <int ITEMS>
+template <int ITEMS, bool BEST>
 hipError_t launch_items(const BatchArgs& a, const BatchShape& s, hipStream_t st) {
-    auto kern = plan_batch_kernel<kBatchBlock, ITEMS>;
+    auto kern = plan_batch_kernel<kBatchBlock, ITEMS, BEST>;
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)s.lds_bytes);
@@ -934,11 +1027,12 @@ size_t plan_batch_workspace_bytes(int64_t n_traces, int64_t max_trace_len) {
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st) {
     const BatchShape s = batch_shape(a.max_trace_len);
     if (!s.ok) return hipErrorInvalidValue;
+    const bool best = a.policy == MP_BEST_FIT;
     switch (s.items) {
-        case 1: return launch_items<1>(a, s, st);
-        case 2: return launch_items<2>(a, s, st);
-        case 4: return launch_items<4>(a, s, st);
-        case 8: return launch_items<8>(a, s, st);
+        case 1: return best ? launch_items<1, true>(a, s, st) : launch_items<1, false>(a, s, st);
+        case 2: return best ? launch_items<2, true>(a, s, st) : launch_items<2, false>(a, s, st);
+        case 4: return best ? launch_items<4, true>(a, s, st) : launch_items<4, false>(a, s, st);
+        case 8: return best ? launch_items<8, true>(a, s, st) : launch_items<8, false>(a, s, st);
         default: return hipErrorInvalidValue;
     }
 }

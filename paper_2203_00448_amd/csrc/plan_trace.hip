@@ -355,6 +355,47 @@ __device__ uint32_t fit_runs(const RunRef (&runs)[MAXR], int nr, uint32_t s, uin
     return block_reduce<BLOCK>(best, OpMin<uint32_t>(), scratch);
 }
 
+// BEST_FIT over the union of the runs (the tightest-gap reading of Section
+// 2.3's "best fit"): the smallest free gap that holds s wins, the lowest
+// start among equals, and the top of the union only when no gap holds s.  A
+// free gap of the union starts at 0 or at the prefix maximum below some key
+// (or at the top) of one run, at a point no other run covers, and reaches the
+// lowest start at or above that point in any run.
+template <int BLOCK, int MAXR>
+__device__ uint32_t best_fit_runs(const RunRef (&runs)[MAXR], int nr, uint32_t s,
+                                  uint64_t* scratch) {
+    uint64_t best = ~0ull;
+    uint32_t top = 0;
+    for (int r = 0; r < nr; ++r) {
+        const uint64_t* k = runs[r].keys;
+        const int m = runs[r].m;
+        if (m == 0) continue;
+        top = max(top, run_pmax(k[m - 1]));
+        for (int i = threadIdx.x; i <= m; i += BLOCK) {
+            const uint32_t c = (i == 0) ? 0u : run_pmax(k[i - 1]);
+            uint64_t end = (i < m) ? (uint64_t)run_start(k[i]) : ~0ull;
+            if (end < (uint64_t)c + s) continue;  // gap of this run too small
+            for (int r2 = 0; r2 < nr && end >= (uint64_t)c + s; ++r2) {
+                if (r2 == r) continue;
+                const uint64_t* k2 = runs[r2].keys;
+                int a = 0, z = runs[r2].m;  // first key with start >= c
+                while (a < z) {
+                    const int mid = (a + z) >> 1;
+                    if (run_start(k2[mid]) < c) a = mid + 1;
+                    else z = mid;
+                }
+                if (a > 0 && run_pmax(k2[a - 1]) > c) end = 0;  // c is covered
+                else if (a < runs[r2].m) end = min(end, (uint64_t)run_start(k2[a]));
+            }
+            if (end == ~0ull || end < (uint64_t)c + s) continue;  // the top, or too small
+            const uint64_t key = ((end - c) << 32) | c;
+            best = key < best ? key : best;
+        }
+    }
+    best = block_reduce<BLOCK>(best, OpMin<uint64_t>(), scratch);
+    return best != ~0ull ? (uint32_t)best : top;
+}
+
 struct PlaceArgs {
     const uint32_t* su;
     const int32_t* reach;
@@ -365,6 +406,7 @@ struct PlaceArgs {
     int64_t n;
     TFlags* fl;
     int32_t* status;
+    int32_t best;  // fit policy: 0 lowest gap, 1 tightest gap
 };
 
 // Visit the positions ranked before t whose lifetimes meet t's: the forward
@@ -396,6 +438,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     __shared__ uint64_t dkeys[kDynCap];  // predecessors placed after t was examined
     __shared__ uint32_t dpos[kDynCap];
     __shared__ uint32_t scratch[BLOCK / kWave];
+    __shared__ uint64_t scratch64[BLOCK / kWave];
     __shared__ uint32_t s_rank, s_nstat, s_ndyn;
     if (a.fl->abort) return;
     const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
@@ -468,7 +511,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         }
         __syncthreads();
         if (ndyn) make_run<BLOCK>(dkeys, ndyn, scratch);
-        // 4. lowest offset clear of every run (one pass)
+        // 4. the fit over every run (one pass)
         RunRef runs[kScratchRuns + 1];
         int nr = 0;
         if (nruns == 1) {
@@ -479,7 +522,9 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                                     (int)min((uint32_t)kRunCap, nstat - (uint32_t)run * kRunCap)};
         }
         if (ndyn) runs[nr++] = RunRef{dkeys, ndyn};
-        const uint32_t x = nr ? fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch) : 0u;
+        uint32_t x;
+        if (a.best) x = best_fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch64);
+        else x = nr ? fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch) : 0u;
         if (threadIdx.x == 0) agent_store(a.off + qt, x);
         __syncthreads();
     }
@@ -569,8 +614,8 @@ unsigned grid_n(int64_t n, int block) {
 size_t plan_trace_workspace_bytes(int64_t n) { return t_layout(n, place_grid()).total; }
 
 hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
-                             int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out,
-                             void* ws, int32_t* status, hipStream_t st) {
+                             int64_t n, int32_t num_ops, int32_t policy, int64_t* offset_out,
+                             int64_t* peak_out, void* ws, int32_t* status, hipStream_t st) {
     const TLayout L = t_layout(n, place_grid());
     char* w = static_cast<char*>(ws);
     TFlags* fl = reinterpret_cast<TFlags*>(w + L.flags);
@@ -630,7 +675,8 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
                  reinterpret_cast<uint64_t*>(w + L.run_keys),
                  n,
                  fl,
-                 status};
+                 status,
+                 policy == MP_BEST_FIT ? 1 : 0};
     void* kargs[] = {&pa};
     e = hipLaunchCooperativeKernel((const void*)t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock),
                                    kargs, 0, st);

@@ -1,0 +1,149 @@
+"""Parity of the BEST_FIT policy on the GPU with the CPU oracle.
+
+BEST_FIT is the tightest-gap reading of the "best fit criterion" of
+Section 2.3: among the free gaps left by the already placed, lifetime-
+intersecting tensors, the smallest one that holds the tensor (lowest start
+among equals), the space above all of them only when no gap holds it.
+Integer work: offsets and peaks must match the oracle bit for bit.  The
+batched planner fits a tensor with at most 256 lifetime-intersecting tensors
+(MP_ENOSPC beyond); the single-trace planner has the same limit for both
+policies (131072 earlier-ranked intersecting tensors)."""
+import hashlib
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from gpu_util import batch_to_device, dev, host, need_gpu, torch
+from paper_2203_00448_amd import tracegen as tg
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+BEST = oracle.BEST_FIT
+
+
+def _sha(a):
+    return hashlib.sha256(np.ascontiguousarray(a).astype("<i8").tobytes()).hexdigest()
+
+
+def _check_batch(binding, batch, **kw):
+    args = batch_to_device(batch)
+    off, peak, lb = binding.plan_batch(*args, policy=binding.BEST_FIT, **kw)
+    off, peak = host(off), host(peak)
+    eo, ep = oracle.plan_batch(batch.begin, batch.num_ops, batch.size, batch.first, batch.last,
+                               BEST)
+    bad = np.nonzero(off != eo)[0]
+    assert bad.size == 0, f"{bad.size} offsets differ, first at {bad[:5]}"
+    assert np.array_equal(peak, ep)
+    return off, peak
+
+
+def _hand_traces():
+    with open(os.path.join(HERE, "golden", "hand_examples.json")) as fh:
+        ex = json.load(fh)["examples"]
+    out = []
+    for e in ex:
+        f = np.asarray(e["first"], np.int32)
+        out.append((e, tg.Trace(np.asarray(e["size"], np.int64), f,
+                                np.asarray(e["last"], np.int32), int(max(e["last"])) + 1)))
+    return out
+
+
+def test_hand_examples_batch_and_trace():
+    binding = need_gpu()
+    print("case hand examples, BEST_FIT", flush=True)
+    hand = _hand_traces()
+    off, _ = _check_batch(binding, tg.concat([t for _, t in hand]), max_trace_len=16)
+    batch = tg.concat([t for _, t in hand])
+    for k, (e, t) in enumerate(hand):
+        lo, hi = int(batch.begin[k]), int(batch.begin[k + 1])
+        assert off[lo:hi].tolist() == e["best_fit"], e["name"]
+        o, p = binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                                  dev(t.last, torch.int32), t.num_ops, policy=binding.BEST_FIT)
+        assert host(o).tolist() == e["best_fit"], e["name"]
+    # the policies differ on E4: id 4 takes the tight gap [256, 320)
+    e4 = [e for e, _ in hand if e["name"] == "E4"][0]
+    assert e4["best_fit"] != e4["lowest_fit"]
+
+
+def test_chain256_against_stored_digest():
+    binding = need_gpu()
+    print("case chain256, BEST_FIT", flush=True)
+    with open(os.path.join(HERE, "golden", "expected.json")) as fh:
+        exp = json.load(fh)["configs"]["chain256_best_fit"]
+    t = tg.chain256()
+    off, peak = _check_batch(binding, tg.concat([t]))
+    assert _sha(off) == exp["offsets_sha256"] and int(peak[0]) == exp["peak"]
+    o, p = binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                              dev(t.last, torch.int32), t.num_ops, policy=binding.BEST_FIT)
+    assert _sha(host(o)) == exp["offsets_sha256"] and int(p.item()) == exp["peak"]
+
+
+def test_random_ragged_batches():
+    binding = need_gpu()
+    rng = np.random.default_rng(400)
+    traces = []
+    for k in range(200):
+        n = int(rng.choice([0, 1, 2, 3, 17, 64, 150, 255, 256, 257, 700, 1500]))
+        if n <= 150:  # dense: up to 149 neighbours per tensor
+            T, span = int(rng.integers(1, 20)), int(rng.integers(1, 20))
+        else:         # about one birth per op, short lifetimes
+            T, span = n * int(rng.integers(1, 3)) + 1, int(rng.integers(1, 12))
+        alphabet = [64, 128, 192, 448, 1024] if k % 3 == 0 else None
+        traces.append(tg.random_trace(rng, n, T, max_len=span, sizes=alphabet,
+                                      sorted_first=(k % 2 == 0)))
+    print("case 200 random ragged traces, BEST_FIT", flush=True)
+    _check_batch(binding, tg.concat(traces), max_trace_len=1500)
+
+
+def test_resnext_batch():
+    binding = need_gpu()
+    print("case resnext batch 1024 x 2000, BEST_FIT", flush=True)
+    _check_batch(binding, tg.resnext_batch(), max_trace_len=2000)
+
+
+def test_batch_neighbour_limit():
+    binding = need_gpu()
+    print("case one tensor meeting 299 others, BEST_FIT", flush=True)
+    n = 300  # tensor 0 lives through every op, tensor i > 0 only at op i: 299 pairs
+    t = tg.Trace(np.full(n, 64, np.int64), np.arange(n, dtype=np.int32),
+                 np.arange(n, dtype=np.int32), n)
+    t.first[0], t.last[0] = 0, n - 1
+    args = batch_to_device(tg.concat([t]))
+    status = binding.new_status()
+    binding.plan_batch(*args, policy=binding.BEST_FIT, check=False, status=status)
+    assert int(status.item()) == binding.MP_ENOSPC
+    # LOWEST_FIT has no such limit
+    off, peak, _ = binding.plan_batch(*args)
+    assert int(peak.item()) == 128
+
+
+@pytest.mark.parametrize("seed", [401, 402])
+def test_single_trace_random(seed):
+    binding = need_gpu()
+    rng = np.random.default_rng(seed)
+    print(f"case single-trace random, BEST_FIT, seed {seed}", flush=True)
+    for k in range(12):
+        n = int(rng.choice([1, 2, 40, 700, 5000]))
+        T = int(rng.integers(1, 2000))
+        alphabet = [64, 128, 192, 448, 4096] if k % 3 == 0 else None
+        t = tg.random_trace(rng, n, T, max_len=int(rng.integers(1, T + 1)), sizes=alphabet,
+                            sorted_first=(k % 2 == 0))
+        o, p = binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                                  dev(t.last, torch.int32), t.num_ops, policy=binding.BEST_FIT)
+        eo, ep = oracle.plan_trace(t.size, t.first, t.last, t.num_ops, BEST)
+        assert np.array_equal(host(o), eo) and int(p.item()) == ep
+
+
+def test_decode100k_single_trace():
+    binding = need_gpu()
+    print("case decode100k, BEST_FIT (oracle about 10 s)", flush=True)
+    t = tg.decode100k()
+    o, p = binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                              dev(t.last, torch.int32), t.num_ops, policy=binding.BEST_FIT)
+    eo, ep = oracle.plan_trace(t.size, t.first, t.last, t.num_ops, BEST)
+    bad = np.nonzero(host(o) != eo)[0]
+    assert bad.size == 0, f"{bad.size} offsets differ, first at {bad[:5]}"
+    assert int(p.item()) == ep
