@@ -10,7 +10,10 @@ requires zero conflicts).
 
 Prints one JSON line: tensors planned per second, the roofline of the
 dominant kernel (the batched planner) from HIP events on its stream, and the
-plain CPU oracle timed on the host as a baseline.
+plain CPU oracle timed on the host as a baseline.  After the timed steps, a
+single-trace leg plans the seq2seq-decode-like trace (100,000 tensors, 4000
+ops, seed 3) with the whole-device planner and reports its tensors per
+second and peak / live-bytes lower bound (outside `value`).
 """
 from __future__ import annotations
 
@@ -37,6 +40,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true",
                     help="skip timing the CPU oracle (profiling runs)")
+    ap.add_argument("--no-single-trace", action="store_true",
+                    help="skip the single-trace leg (profiling runs of the batched step)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, copy 256 MiB device to device three times "
                          "(a kernel of known traffic for scaling HBM counters)")
@@ -59,6 +64,41 @@ def measured_traffic():
     if fields.get("plan_batch_source_sha256", "").strip() != sha:
         return None
     return int(fields["traffic_bytes_per_launch"])
+
+
+def single_trace_leg(binding, tg, np, torch, reps: int = 3):
+    """mp_plan_trace on the decode-like trace, inputs resident in HBM: one
+    warm-up call, then `reps` calls timed with HIP events on the stream."""
+    t = tg.decode100k()
+    d = lambda a, ty: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dtype=ty)
+    size, first, last = d(t.size, torch.int64), d(t.first, torch.int32), d(t.last, torch.int32)
+    n = int(t.size.shape[0])
+    stream = torch.cuda.current_stream()
+    offset = torch.empty(n, dtype=torch.int64, device="cuda")
+    peak = torch.empty(1, dtype=torch.int64, device="cuda")
+    ws = torch.empty(binding.workspace_size(binding.OP_PLAN_TRACE, n, t.num_ops),
+                     dtype=torch.uint8, device="cuda")
+    status = binding.new_status()
+    run = lambda: binding.plan_trace(size, first, last, t.num_ops, check=False, out=(offset, peak),
+                                     status=status, workspace=ws, stream=stream)
+    run()
+    ms = []
+    for _ in range(reps):
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record(stream)
+        run()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        ms.append(ev[0].elapsed_time(ev[1]))
+    st = int(status.item())
+    if st != binding.MP_OK:
+        raise SystemExit(f"single trace: device status {st}: {binding.status_string(st)}")
+    _, max_live = binding.live_bytes_profile(size, first, last, t.num_ops)
+    med = float(np.median(ms))
+    return {"workload": "decode100k: 100,000 tensors, 4000 ops x 25 births, Geometric(0.3) "
+                        "lifetimes, 2% to the end, Pareto(1.5) sizes (seed 3), lowest fit",
+            "tensors_per_s": n / (med * 1e-3), "ms": med, "calls": reps,
+            "peak_over_lb": int(peak.item()) / int(max_live.item())}
 
 
 def cpu_baseline(batch, min_seconds: float = 10.0):
@@ -180,6 +220,8 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = 2 * src.numel()
+    if not args.no_single_trace:
+        out["single_trace"] = single_trace_leg(binding, tg, np, torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(batch)
     print(json.dumps(out), flush=True)

@@ -301,38 +301,54 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
             if (segcnt[b + 1] == base || base >= cap) continue;  // nothing to write here
         }
         const int m = (int)(hi - lo);
+        // all four inputs are requested at once; the byte ranges wait in
+        // registers until the reach pass has released first[]
         int32_t l_r[ITEMS];
+        int64_t s_r[ITEMS], o_r[ITEMS];
         bool bad = false;
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
             l_r[k] = 0;
+            s_r[k] = 1;
+            o_r[k] = 0;
             if (q < m) {
                 const int32_t f = first[lo + q], l = last[lo + q];
+                s_r[k] = size[lo + q];
+                o_r[k] = off[lo + q];
                 if (f < 0 || f > l) bad = true;
                 lf[q] = f;
                 l_r[k] = l;
             }
         }
         __syncthreads();
-        // reach (galloping search over first), band lengths; sortedness check
+        // reach: the next four positions are probed at once (short bands end
+        // there), longer bands gallop on; band lengths; sortedness check
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
             if (q < m) {
                 if (q > 0 && lf[q] < lf[q - 1]) bad = true;  // the sorted promise is broken
                 const int32_t l = l_r[k];
-                int known = q, step = 1, probe = q + 1;
-                while (probe < m && lf[probe] <= l) {
-                    known = probe;
-                    step <<= 1;
-                    probe = q + step;
-                }
-                int a = known + 1, z = probe < m ? probe : m;
-                while (a < z) {
-                    const int mid = (a + z) >> 1;
-                    if (lf[mid] <= l) a = mid + 1;
-                    else z = mid;
+                const int32_t f1 = q + 1 < m ? lf[q + 1] : INT32_MAX;
+                const int32_t f2 = q + 2 < m ? lf[q + 2] : INT32_MAX;
+                const int32_t f3 = q + 3 < m ? lf[q + 3] : INT32_MAX;
+                const int32_t f4 = q + 4 < m ? lf[q + 4] : INT32_MAX;
+                int a = q + 1 + (f1 <= l) + (f2 <= l) + (f3 <= l) + (f4 <= l);
+                if (a == q + 5) {  // first[q + 4] <= l: gallop on
+                    int known = q + 4, step = 8, probe = q + 8;  // first[known] <= l
+                    while (probe < m && lf[probe] <= l) {
+                        known = probe;
+                        step <<= 1;
+                        probe = q + step;
+                    }
+                    a = known + 1;
+                    int z = probe < m ? probe : m;
+                    while (a < z) {
+                        const int mid = (a + z) >> 1;
+                        if (lf[mid] <= l) a = mid + 1;
+                        else z = mid;
+                    }
                 }
                 band[q] = (uint32_t)(a - q - 1);
             }
@@ -342,7 +358,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
             if (q < m) {
-                const int64_t sz = size[lo + q], o = off[lo + q];
+                const int64_t sz = s_r[k], o = o_r[k];
                 if (sz <= 0 || o < 0 || o > INT64_MAX - sz) bad = true;
                 lo64[q] = o;
                 ls64[q] = sz;
