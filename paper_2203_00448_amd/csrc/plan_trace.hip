@@ -439,6 +439,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     __shared__ uint32_t dpos[kDynCap];
     __shared__ uint32_t scratch[BLOCK / kWave];
     __shared__ uint64_t scratch64[BLOCK / kWave];
+    __shared__ uint64_t gbits[kRunCap / 64];  // gaps of the placed run that hold t
     __shared__ uint32_t s_rank, s_nstat, s_ndyn;
     if (a.fl->abort) return;
     const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
@@ -500,6 +501,68 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 for (int i = threadIdx.x; i < m0; i += BLOCK) g[i] = skeys[i];
                 __syncthreads();
             }
+        }
+        // Lowest fit with one run of placed predecessors and at most 64 late
+        // ones: before waiting, mark the run's gaps [prefix maximum below i,
+        // start of i) that hold t.  Then wave 0 alone waits for the late
+        // ones (a lane each, their ranges stay in registers) and walks the
+        // marked gaps in order, then the top: in a gap it moves past the
+        // highest end among the late ranges overlapping [c, c + st) until
+        // none does, and the first gap that still holds t gives the offset.
+        // No workgroup barrier lies between the last wait and the publish.
+        if (!a.best && nruns <= 1 && ndyn <= kWave) {
+            const int m = (int)nstat, words = (m + 63) >> 6;
+            const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+            for (int w = wid; w < words; w += BLOCK / kWave) {
+                const int i = 64 * w + lane;
+                bool ok = false;
+                if (i < m) {
+                    const uint32_t g0 = i ? run_pmax(skeys[i - 1]) : 0u, g1 = run_start(skeys[i]);
+                    ok = g1 > g0 && g1 - g0 >= st;
+                }
+                const uint64_t mk = __ballot(ok);
+                if (lane == 0) gbits[w] = mk;
+            }
+            __syncthreads();
+            if (wid == 0) {
+                uint32_t lo_d = kUnplacedT, hi_d = 0;  // this lane's late range, empty if none
+                if (lane < ndyn) {
+                    const uint32_t p = dpos[lane];
+                    uint32_t o;
+                    while ((o = agent_load(a.off + p)) == kUnplacedT) __builtin_amdgcn_s_sleep(1);
+                    lo_d = o;
+                    hi_d = o + a.su[p];
+                }
+                // lowest c' >= c with [c', c' + st) clear of every late range
+                auto past_late = [&](uint32_t c) {
+                    while (true) {
+                        const bool ov = lo_d < c + st && c < hi_d;
+                        if (!__ballot(ov)) return c;
+                        uint32_t v = ov ? hi_d : 0u;
+#pragma unroll
+                        for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+                        c = v;
+                    }
+                };
+                bool found = false;
+                uint32_t x = 0;
+                for (int w = 0; w < words && !found; ++w) {
+                    for (uint64_t bm = gbits[w]; bm; bm &= bm - 1) {
+                        const int i = 64 * w + __builtin_ctzll(bm);
+                        const uint32_t g0 = i ? run_pmax(skeys[i - 1]) : 0u, g1 = run_start(skeys[i]);
+                        const uint32_t c = past_late(g0);
+                        if ((uint64_t)c + st <= g1) {
+                            x = c;
+                            found = true;
+                            break;
+                        }
+                    }
+                }
+                if (!found) x = past_late(m ? run_pmax(skeys[m - 1]) : 0u);
+                if (lane == 0) agent_store(a.off + qt, x);
+            }
+            __syncthreads();
+            continue;
         }
         // 3. wait for the predecessors that were not placed yet; their ranges
         //    form one more run
