@@ -410,25 +410,74 @@ struct PlaceArgs {
 };
 
 // Visit the positions ranked before t whose lifetimes meet t's: the forward
-// band, the backward window of short bands and the long list.
+// band, the backward window of short bands and the long list; fn(p, o) gets
+// each with its offset as read (kUnplacedT while not placed).  Each thread
+// takes kBatch candidates per turn and issues their loads together (sizes
+// and reaches, then offsets), so the latencies overlap.
+constexpr int kBatch = 4;
+
 template <int BLOCK, typename F>
 __device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, uint32_t st,
                                               uint32_t lthr, uint32_t n_long, F&& fn) {
+    auto finish = [&](const int32_t (&pp)[kBatch], const bool (&ok)[kBatch]) {
+        uint32_t o[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) o[u] = ok[u] ? agent_load(a.off + pp[u]) : 0u;
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            if (ok[u]) fn(pp[u], o[u]);
+    };
     const int32_t rt = a.reach[qt];
     // forward band: meets t; ranked before t iff strictly larger
-    for (int32_t j = qt + 1 + threadIdx.x; j < rt; j += BLOCK)
-        if (a.su[j] > st) fn(j);
+    for (int32_t j0 = qt + 1 + (int32_t)threadIdx.x; j0 < rt; j0 += BLOCK * kBatch) {
+        int32_t pp[kBatch];
+        bool ok[kBatch];
+        uint32_t sz[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            pp[u] = j0 + u * BLOCK;
+            sz[u] = pp[u] < rt ? a.su[pp[u]] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) ok[u] = pp[u] < rt && sz[u] > st;
+        finish(pp, ok);
+    }
     // backward window of short bands: ranked before t iff at least as large
     const int64_t lo = (int64_t)qt - (int64_t)lthr - 1;
-    for (int64_t p = (lo > 0 ? lo : 0) + threadIdx.x; p < qt; p += BLOCK) {
-        const int32_t r = a.reach[p];
-        if ((uint32_t)(r - p - 1) <= lthr && r > qt && a.su[p] >= st) fn((int32_t)p);
+    for (int64_t p0 = (lo > 0 ? lo : 0) + threadIdx.x; p0 < qt; p0 += BLOCK * kBatch) {
+        int32_t pp[kBatch], rr[kBatch];
+        bool ok[kBatch];
+        uint32_t sz[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int64_t p = p0 + (int64_t)u * BLOCK;
+            pp[u] = (int32_t)p;
+            rr[u] = p < qt ? a.reach[p] : 0;
+            sz[u] = p < qt ? a.su[p] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            ok[u] = pp[u] < qt && (uint32_t)(rr[u] - pp[u] - 1) <= lthr && rr[u] > qt && sz[u] >= st;
+        finish(pp, ok);
     }
     // long bands that started before t
-    for (uint32_t k = threadIdx.x; k < n_long; k += BLOCK) {
-        const int32_t p = a.long_list[k];
-        if (p >= qt) continue;
-        if (a.reach[p] > qt && a.su[p] >= st) fn(p);
+    for (uint32_t k0 = threadIdx.x; k0 < n_long; k0 += BLOCK * kBatch) {
+        int32_t pp[kBatch], rr[kBatch];
+        bool ok[kBatch];
+        uint32_t sz[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const uint32_t k = k0 + u * BLOCK;
+            pp[u] = k < n_long ? a.long_list[k] : qt;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            rr[u] = pp[u] < qt ? a.reach[pp[u]] : 0;
+            sz[u] = pp[u] < qt ? a.su[pp[u]] : 0u;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) ok[u] = pp[u] < qt && rr[u] > qt && sz[u] >= st;
+        finish(pp, ok);
     }
 }
 
@@ -458,8 +507,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         const uint32_t st = a.su[qt];
         // 1. collect: placed predecessors as keys, unplaced ones by position
         //    (beyond kDynCap of those, wait for them right here)
-        for_each_pred<BLOCK>(a, qt, st, lthr, n_long, [&](int32_t p) {
-            uint32_t o = agent_load(a.off + p);
+        for_each_pred<BLOCK>(a, qt, st, lthr, n_long, [&](int32_t p, uint32_t o) {
             if (o == kUnplacedT) {
                 const uint32_t d = atomicAdd(&s_ndyn, 1u);
                 if (d < (uint32_t)kDynCap) {
