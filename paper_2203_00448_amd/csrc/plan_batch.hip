@@ -90,13 +90,18 @@ __device__ __forceinline__ uint32_t packed_add(uint32_t* w, uint32_t i, uint32_t
 // right band q + 1 .. q + R, whose members rank after q iff their size is
 // at most q's (equal sizes rank by position).  Slots past the end (k >= K)
 // map to q itself, which is unplaced and never a successor.
+// Both are computed without branches (masks instead of selects that the
+// compiler would turn into divergent blocks around the list load).
 __device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
                                               uint32_t lv) {
-    return k < L ? (lv & 0x0FFFu) : (k < K ? q + 1 + (k - L) : q);
+    const uint32_t in_left = 0u - (uint32_t)(k < L), in_band = 0u - (uint32_t)(k < K);
+    const uint32_t right = q + ((k + 1 - L) & in_band);
+    return ((lv & 0x0FFFu) & in_left) | (right & ~in_left);
 }
 __device__ __forceinline__ bool is_successor(uint32_t k, uint32_t L, uint32_t lv,
                                              uint32_t s_other, uint32_t s) {
-    return k < L ? (lv & kLeftSucc) != 0 : s_other <= s;
+    const uint32_t left_succ = (lv >> 15) & 1u, band_succ = (uint32_t)(s_other <= s);
+    return ((k < L) ? left_succ : band_succ) != 0u;
 }
 
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
