@@ -544,23 +544,35 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     uint64_t orv = 0, sum = 0;
     int64_t sz_r[ITEMS];
     int32_t la_r[ITEMS];
+    // every load is issued before any is used: indices are clamped into
+    // the trace (n >= 1 here), so the loads need no branch around them
+    int32_t fi_r[ITEMS], fp_r[ITEMS];
+    if (n > 0) {
+#pragma unroll
+        for (int k = 0; k < ITEMS; ++k) {
+            const int i = min(tid + k * BLOCK, n - 1);
+            sz_r[k] = size[lo + i];
+            fi_r[k] = first[lo + i];
+            la_r[k] = last[lo + i];
+            fp_r[k] = first[lo + (i > 0 ? i - 1 : 0)];
+        }
+    }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int i = tid + k * BLOCK;
-        sz_r[k] = 0;
-        la_r[k] = 0;
         if (i < n) {
-            const int64_t s = size[lo + i];
-            const int32_t f = first[lo + i], l = last[lo + i];
-            if (i > 0 && first[lo + i - 1] > f) flags |= 2u;
+            const int64_t s = sz_r[k];
+            const int32_t f = fi_r[k], l = la_r[k];
+            if (i > 0 && fp_r[k] > f) flags |= 2u;
             if (s <= 0 || f < 0 || f > l || l >= n_ops) flags |= 1u;
             if (s > 0) {
                 orv |= (uint64_t)s;
                 sum = sat_add(sum, (uint64_t)s);
             }
             fst[i] = f;
-            sz_r[k] = s;
-            la_r[k] = l;
+        } else {
+            sz_r[k] = 0;
+            la_r[k] = 0;
         }
     }
     // one combined reduction of the flags, the OR and the saturating sum
