@@ -301,24 +301,26 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
             if (segcnt[b + 1] == base || base >= cap) continue;  // nothing to write here
         }
         const int m = (int)(hi - lo);
-        // all four inputs are requested at once; the byte ranges wait in
-        // registers until the reach pass has released first[]
+        // first and last of every item are requested before any is used
+        // (indices clamped into the trace: no branch around the loads)
         int32_t l_r[ITEMS];
-        int64_t s_r[ITEMS], o_r[ITEMS];
         bool bad = false;
+        {
+            int32_t f_r[ITEMS];
+            const int mc = m > 0 ? m - 1 : 0;
 #pragma unroll
-        for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
-            l_r[k] = 0;
-            s_r[k] = 1;
-            o_r[k] = 0;
-            if (q < m) {
-                const int32_t f = first[lo + q], l = last[lo + q];
-                s_r[k] = size[lo + q];
-                o_r[k] = off[lo + q];
-                if (f < 0 || f > l) bad = true;
-                lf[q] = f;
-                l_r[k] = l;
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = min(tid + k * BLOCK, mc);
+                f_r[k] = m > 0 ? first[lo + q] : 0;
+                l_r[k] = m > 0 ? last[lo + q] : 0;
+            }
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = tid + k * BLOCK;
+                if (q < m) {
+                    if (f_r[k] < 0 || f_r[k] > l_r[k]) bad = true;
+                    lf[q] = f_r[k];
+                }
             }
         }
         __syncthreads();
@@ -354,14 +356,24 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
             }
         }
         __syncthreads();  // first[] is dead: the byte ranges go in its place
+        {  // the byte ranges, again every load before any use
+            int64_t s_r[ITEMS], o_r[ITEMS];
+            const int mc = m > 0 ? m - 1 : 0;
 #pragma unroll
-        for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
-            if (q < m) {
-                const int64_t sz = s_r[k], o = o_r[k];
-                if (sz <= 0 || o < 0 || o > INT64_MAX - sz) bad = true;
-                lo64[q] = o;
-                ls64[q] = sz;
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = min(tid + k * BLOCK, mc);
+                s_r[k] = m > 0 ? size[lo + q] : 1;
+                o_r[k] = m > 0 ? off[lo + q] : 0;
+            }
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = tid + k * BLOCK;
+                if (q < m) {
+                    const int64_t sz = s_r[k], o = o_r[k];
+                    if (sz <= 0 || o < 0 || o > INT64_MAX - sz) bad = true;
+                    lo64[q] = o;
+                    ls64[q] = sz;
+                }
             }
         }
         if (!write && __ballot(bad) && (tid & (kWave - 1)) == 0) raise_status(status, MP_EINVAL);
