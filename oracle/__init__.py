@@ -60,8 +60,9 @@ def lib():
         L.mpo_plan_trace_w.argtypes = [p, p, p, i64, i32, i32, i32, p, p]
         L.mpo_live_bytes_profile.argtypes = [p, p, p, i64, i32, p, p]
         L.mpo_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p]
+        L.mpo_probe_plan.argtypes = [p, p, p, p, i64, i32, p, p]
         for f in (L.mpo_check_trace, L.mpo_rank_order, L.mpo_plan_trace, L.mpo_plan_trace_w,
-                  L.mpo_live_bytes_profile, L.mpo_validate_plan):
+                  L.mpo_live_bytes_profile, L.mpo_validate_plan, L.mpo_probe_plan):
             f.restype = i32
         _lib = L
     return _lib
@@ -151,3 +152,17 @@ def validate_plan(size, first, last, offset, capacity: int | None = None):
     if st != OK:
         raise OracleError(st, "validate_plan")
     return pairs[: int(cnt.value)], int(cnt.value)
+
+
+def probe_plan(size, first, last, offset, num_ops: int):
+    """Write-pattern aliasing probe of a plan (see mpo_probe_plan).  Returns
+    (clobbered bool[n], count)."""
+    s, f, l = _arr(size, np.int64), _arr(first, np.int32), _arr(last, np.int32)
+    o = _arr(offset, np.int64)
+    out = np.zeros(s.shape[0], np.uint8)
+    cnt = ctypes.c_int64(0)
+    st = lib().mpo_probe_plan(_ptr(s), _ptr(f), _ptr(l), _ptr(o), s.shape[0], int(num_ops),
+                              _ptr(out), ctypes.byref(cnt))
+    if st != OK:
+        raise OracleError(st, "probe_plan")
+    return out.astype(bool), int(cnt.value)

@@ -283,3 +283,85 @@ int32_t mpo_validate_plan(const int64_t* size, const int32_t* first, const int32
     *n_conflicts_out = count;
     return count > capacity ? MPO_ENOSPC : MPO_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Plan application and a write-pattern aliasing probe.  Section 3.3 applies a
+ * plan by allocating one slab of total_size bytes and placing every tensor as
+ * a view at its offset in it (Listing 5).  The probe replays the ops of the
+ * trace in order over such a slab, seen as 32-bit words that are all zero at
+ * the start.  At op t:
+ *   1. every tensor first used at t writes id + 1 into each word of its byte
+ *      range, keeping the larger value where a word already holds one (so
+ *      that writers of the same op resolve the same way in any order);
+ *   2. every tensor last used at t checks each word of its range: a tensor
+ *      that finds any value other than id + 1 is "clobbered";
+ *   3. those tensors clear their words to 0.
+ * With a valid plan no tensor is clobbered; of every pair that breaks the
+ * constraints of Eq. 2.1 at least one tensor is.  Sizes and offsets must be
+ * multiples of 4 bytes. */
+
+int32_t mpo_probe_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                       const int64_t* offset, int64_t n, int32_t num_ops,
+                       uint8_t* clobbered_out, int64_t* n_clobbered_out) {
+    if (!n_clobbered_out || n < 0 || n >= INT32_MAX || num_ops < 0) return MPO_EINVAL;
+    if (n > 0 && (!size || !first || !last || !offset || !clobbered_out)) return MPO_EINVAL;
+    int64_t words = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        if (size[i] <= 0 || size[i] % 4 != 0 || offset[i] < 0 || offset[i] % 4 != 0 ||
+            offset[i] > INT64_MAX - size[i] || first[i] < 0 || first[i] > last[i] ||
+            last[i] >= num_ops)
+            return MPO_EINVAL;
+        const int64_t end = (offset[i] + size[i]) / 4;
+        if (end > words) words = end;
+    }
+    uint32_t* slab = (uint32_t*)calloc((size_t)(words > 0 ? words : 1), sizeof(uint32_t));
+    /* tensors by first op and by last op (counting sort, ids ascending) */
+    int64_t* bstart = (int64_t*)calloc((size_t)num_ops + 1, sizeof(int64_t));
+    int64_t* dstart = (int64_t*)calloc((size_t)num_ops + 1, sizeof(int64_t));
+    int32_t* born = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    int32_t* dies = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    if (!slab || !bstart || !dstart || !born || !dies) {
+        free(slab); free(bstart); free(dstart); free(born); free(dies);
+        return MPO_EINVAL;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        ++bstart[first[i] + 1];
+        ++dstart[last[i] + 1];
+    }
+    for (int32_t t = 0; t < num_ops; ++t) {
+        bstart[t + 1] += bstart[t];
+        dstart[t + 1] += dstart[t];
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        born[bstart[first[i]]++] = (int32_t)i;
+        dies[dstart[last[i]]++] = (int32_t)i;
+    }
+    /* the cursors now hold the ends; the starts are the previous op's ends */
+    int64_t count = 0;
+    for (int32_t t = 0; t < num_ops; ++t) {
+        const int64_t b0 = t ? bstart[t - 1] : 0, b1 = bstart[t];
+        const int64_t d0 = t ? dstart[t - 1] : 0, d1 = dstart[t];
+        for (int64_t k = b0; k < b1; ++k) {
+            const int32_t i = born[k];
+            const uint32_t v = (uint32_t)i + 1u;
+            for (int64_t w = offset[i] / 4; w < (offset[i] + size[i]) / 4; ++w)
+                if (slab[w] < v) slab[w] = v;
+        }
+        for (int64_t k = d0; k < d1; ++k) {
+            const int32_t i = dies[k];
+            const uint32_t v = (uint32_t)i + 1u;
+            uint8_t bad = 0;
+            for (int64_t w = offset[i] / 4; w < (offset[i] + size[i]) / 4; ++w)
+                if (slab[w] != v) bad = 1;
+            clobbered_out[i] = bad;
+            count += bad;
+        }
+        for (int64_t k = d0; k < d1; ++k) {
+            const int32_t i = dies[k];
+            for (int64_t w = offset[i] / 4; w < (offset[i] + size[i]) / 4; ++w) slab[w] = 0;
+        }
+    }
+    free(slab); free(bstart); free(dstart); free(born); free(dies);
+    *n_clobbered_out = count;
+    return MPO_OK;
+}

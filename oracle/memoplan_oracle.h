@@ -71,6 +71,16 @@ int32_t mpo_validate_plan(const int64_t* size, const int32_t* first, const int32
                           const int64_t* offset, int64_t n, int64_t* pairs_out,
                           int64_t capacity, int64_t* n_conflicts_out);
 
+/* Write-pattern aliasing probe of a plan (plan application of Section 3.3,
+ * Listing 5): the ops are replayed in order over a zeroed slab of 32-bit
+ * words; at op t the tensors first used at t write id + 1 into their words
+ * (keeping the larger value), then the tensors last used at t check that
+ * their words hold id + 1 (clobbered_out[i] = 1 otherwise) and clear them.
+ * Sizes and offsets must be multiples of 4.  *n_clobbered_out = the count. */
+int32_t mpo_probe_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                       const int64_t* offset, int64_t n, int32_t num_ops,
+                       uint8_t* clobbered_out, int64_t* n_clobbered_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -305,3 +305,66 @@ def test_generator_statistics_small():
     b = tg.resnext_trace(0)
     assert b.n == 2000 and (b.size % 64 == 0).all()
     assert int(b.size.min()) >= 4096 and int(b.size.max()) <= 1 << 26
+
+
+# ---------------------------------------------------------------- plan application probe
+
+def test_probe_hand_cases():
+    # E1 with every tensor at offset 0: bytes [0, 64) end up holding tensor 2's
+    # pattern (the largest), so tensors 0 and 1 find a foreign word at op 2.
+    clob, cnt = oracle.probe_plan([64, 128, 192], [0, 0, 0], [2, 2, 2], [0, 0, 0], 3)
+    assert clob.tolist() == [True, True, False] and cnt == 2
+    # reuse of the same bytes by tensors with disjoint lifetimes is clean in
+    # either id order (the dying tensor clears its words)
+    for first in ([0, 1], [1, 0]):
+        clob, cnt = oracle.probe_plan([64, 64], first, first, [0, 0], 2)
+        assert cnt == 0 and not clob.any()
+    # a later, smaller id writing into a live larger id's bytes: the larger
+    # value stays, so the later tensor is the one that finds a foreign word
+    clob, _ = oracle.probe_plan([64, 64], [1, 0], [1, 1], [0, 32], 2)
+    assert clob.tolist() == [True, False]
+
+
+def test_probe_valid_plans_are_clean(hand_examples):
+    for ex in hand_examples:
+        for key in ("lowest_fit", "best_fit"):
+            clob, cnt = oracle.probe_plan(ex["size"], ex["first"], ex["last"], ex[key],
+                                          _num_ops(ex))
+            assert cnt == 0, (ex["name"], key)
+    rng = np.random.default_rng(31)
+    for _ in range(30):
+        n = int(rng.integers(1, 200))
+        t = tg.random_trace(rng, n, int(rng.integers(1, 40)), max_len=int(rng.integers(1, 40)))
+        for policy in (LOWEST, BEST):
+            off, _ = oracle.plan_trace(t.size, t.first, t.last, t.num_ops, policy)
+            assert oracle.probe_plan(t.size, t.first, t.last, off, t.num_ops)[1] == 0
+
+
+def test_probe_agrees_with_pair_conflicts():
+    # Eq. 2.1 violations from the all-pairs definition: every clobbered tensor
+    # belongs to a violating pair, and every violating pair has a clobbered
+    # member (the value left in their common bytes is at most one of theirs)
+    rng = np.random.default_rng(32)
+    for _ in range(60):
+        n = int(rng.integers(1, 80))
+        size = 64 * rng.integers(1, 6, n)
+        first = rng.integers(0, 12, n)
+        last = first + rng.integers(0, 6, n)
+        off = 64 * rng.integers(0, 12, n)
+        clob, cnt = oracle.probe_plan(size, first, last, off, int(last.max()) + 1)
+        assert cnt == int(clob.sum())
+        pairs = [(i, j) for i in range(n) for j in range(i + 1, n)
+                 if conflict(first, last, i, j) and off[i] < off[j] + size[j]
+                 and off[j] < off[i] + size[i]]
+        members = {i for p in pairs for i in p}
+        assert set(np.nonzero(clob)[0].tolist()) <= members
+        for i, j in pairs:
+            assert clob[i] or clob[j]
+
+
+def test_probe_invalid_and_empty():
+    assert oracle.probe_plan([], [], [], [], 0)[1] == 0
+    for bad in (dict(size=[62]), dict(off=[2]), dict(size=[0]), dict(first=[2])):
+        kw = dict(size=[64], first=[0], last=[1], off=[0]) | bad
+        with pytest.raises(oracle.OracleError):
+            oracle.probe_plan(kw["size"], kw["first"], kw["last"], kw["off"], 2)
