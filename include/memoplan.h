@@ -128,6 +128,7 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
 #define MP_OP_PLAN_TRACE 3
 #define MP_OP_VALIDATE_BATCH 4
 #define MP_OP_PLAN_BATCH 5
+#define MP_OP_PROBE 6
 size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops, int64_t capacity);
 
 /* Per-op live bytes of one trace (the quantity whose maximum lower-bounds
@@ -181,6 +182,30 @@ int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t*
                           int64_t capacity, int64_t* n_conflicts_out, int32_t hints,
                           void* workspace, size_t workspace_bytes, int32_t* status_out,
                           void* stream);
+
+/* A plan applied and exercised: the slab of Section 3.3 (one allocation of
+ * total_size bytes, every tensor a view at its offset, as in Listing 5),
+ * probed by replaying the ops in order over its 32-bit words, zeroed first.
+ * At op t every tensor first used at t writes id + 1 into each word of its
+ * range, keeping the larger value where a word already holds one; then every
+ * tensor last used at t checks its words -- a tensor that finds another value
+ * is clobbered -- and clears them to 0.  A valid plan clobbers nothing; of
+ * every pair breaking Eq. 2.1 at least one tensor is clobbered (the result
+ * does not depend on the order of the writers of one op).
+ *   size, first, last, offset [n] (int64, int32, int32, int64): sizes and
+ *              offsets multiples of 4 bytes, 0 <= first <= last < num_ops.
+ *   slab:      device memory of slab_bytes >= max(offset + size) bytes (the
+ *              plan's peak), 4-byte aligned; overwritten.
+ *   clobbered_out[n] uint8: 1 for a clobbered tensor, else 0.
+ *   n_clobbered_out: one device int64, the number of clobbered tensors.
+ *   workspace: mp_workspace_size(MP_OP_PROBE, n, num_ops, 0) bytes.
+ * Data errors (MP_EINVAL on the status word): a size <= 0, a size or offset
+ * not a multiple of 4, a negative offset, an invalid lifetime, a slab smaller
+ * than the plan.  One workgroup replays the ops in order. */
+int32_t mp_probe_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                      const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
+                      size_t slab_bytes, uint8_t* clobbered_out, int64_t* n_clobbered_out,
+                      void* workspace, size_t workspace_bytes, int32_t* status_out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -16,6 +16,7 @@ LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
 OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH, OP_PLAN_BATCH = 1, 2, 3, 4, 5
+OP_PROBE = 6
 HINT_SORTED_FIRST = 1
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
@@ -56,6 +57,8 @@ def load_library(path: str = LIB_PATH):
     L.mp_validate_batch.restype = i32
     L.mp_plan_trace.argtypes = [p, p, p, i64, i32, i32, p, p, p, sz, p, p]
     L.mp_plan_trace.restype = i32
+    L.mp_probe_plan.argtypes = [p, p, p, p, i64, i32, p, sz, p, p, p, sz, p, p]
+    L.mp_probe_plan.restype = i32
     _lib = L
     return L
 
@@ -270,3 +273,40 @@ def plan_trace(size, first, last, num_ops: int, *, policy: int = LOWEST_FIT, che
                          _p(peak), _p(ws), need, _p(status), _stream(stream))
     _finish(rc, status, "plan_trace", check)
     return offset, peak
+
+
+def apply_plan(offset, size, peak: int, device="cuda"):
+    """The plan applied as in Section 3.3: one slab of `peak` bytes and every
+    tensor a byte view at its offset (offset, size: host integer sequences).
+    Returns (slab uint8[peak], views); allocation and views are torch's."""
+    slab = torch.empty(max(int(peak), 4), dtype=torch.uint8, device=device)
+    views = [slab.narrow(0, int(o), int(s)) for o, s in zip(offset, size)]
+    return slab, views
+
+
+def probe_plan(size, first, last, offset, num_ops: int, slab: torch.Tensor, *,
+               check: bool = True, out=None, status=None, workspace=None, stream=None):
+    """Write-pattern aliasing probe of a plan over `slab` (mp_probe_plan).
+    Returns (clobbered uint8[n], n_clobbered int64[1]) on the GPU."""
+    L = load_library()
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    offset = _dev(offset, torch.int64, "offset")
+    n = size.numel()
+    dev = size.device
+    if slab.device != dev or not slab.is_contiguous():
+        raise ValueError("slab must be a contiguous tensor on the device of the trace")
+    if out is None:
+        clob = torch.empty(max(n, 1), dtype=torch.uint8, device=dev)[:n]
+        cnt = torch.empty(1, dtype=torch.int64, device=dev)
+    else:
+        clob, cnt = out
+    ws, need = _workspace(OP_PROBE, dev, n, num_ops, 0, workspace)
+    if status is None:
+        status = new_status(dev, stream)
+    rc = L.mp_probe_plan(_p(size), _p(first), _p(last), _p(offset), n, int(num_ops), _p(slab),
+                         slab.numel() * slab.element_size(), _p(clob), _p(cnt), _p(ws), need,
+                         _p(status), _stream(stream))
+    _finish(rc, status, "probe_plan", check)
+    return clob, cnt

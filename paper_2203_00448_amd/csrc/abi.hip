@@ -65,6 +65,8 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
             return num_ops > INT32_MAX ? 0 : validate_workspace_bytes(n_tensors, capacity, num_ops);
         case MP_OP_PLAN_TRACE:
             return n_tensors >= (int64_t)1 << 30 ? 0 : plan_trace_workspace_bytes(n_tensors);
+        case MP_OP_PROBE:
+            return num_ops > INT32_MAX ? 0 : probe_workspace_bytes(n_tensors, (int32_t)num_ops);
         default:
             return 0;
     }
@@ -139,4 +141,20 @@ extern "C" int32_t mp_plan_trace(const int64_t* size, const int32_t* first, cons
     if (workspace_bytes < plan_trace_workspace_bytes(n)) return MP_EINVAL;
     return launched(launch_plan_trace(size, first, last, n, num_ops, policy, offset_out, peak_out,
                                       workspace, status_out, static_cast<hipStream_t>(stream)));
+}
+
+extern "C" int32_t mp_probe_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                                 const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
+                                 size_t slab_bytes, uint8_t* clobbered_out,
+                                 int64_t* n_clobbered_out, void* workspace,
+                                 size_t workspace_bytes, int32_t* status_out, void* stream) {
+    if (n < 0 || n >= INT32_MAX || num_ops < 0 || !status_out || !n_clobbered_out || !workspace)
+        return MP_EINVAL;
+    if (n > 0 && (!size || !first || !last || !offset || !clobbered_out || !slab))
+        return MP_EINVAL;
+    if (slab && (reinterpret_cast<uintptr_t>(slab) & 3)) return MP_EINVAL;
+    if (workspace_bytes < probe_workspace_bytes(n, num_ops)) return MP_EINVAL;
+    return launched(launch_probe(size, first, last, offset, n, num_ops, slab, slab ? slab_bytes : 0,
+                                 clobbered_out, n_clobbered_out, workspace, status_out,
+                                 static_cast<hipStream_t>(stream)));
 }

@@ -39,6 +39,13 @@ size_t plan_batch_workspace_bytes(int64_t n_traces, int64_t max_trace_len);
 hipError_t launch_reset_status(int32_t* status, hipStream_t st);
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st);
 
+// write-pattern aliasing probe of a plan (probe.hip)
+size_t probe_workspace_bytes(int64_t n, int32_t num_ops);
+hipError_t launch_probe(const int64_t* size, const int32_t* first, const int32_t* last,
+                        const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
+                        size_t slab_bytes, uint8_t* clob, int64_t* n_clob, void* ws,
+                        int32_t* status, hipStream_t st);
+
 }  // namespace mp
 
 namespace mp {
