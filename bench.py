@@ -13,7 +13,8 @@ dominant kernel (the batched planner) from HIP events on its stream, and the
 plain CPU oracle timed on the host as a baseline.  After the timed steps, a
 single-trace leg plans the seq2seq-decode-like trace (100,000 tensors, 4000
 ops, seed 3) with the whole-device planner and reports its tensors per
-second and peak / live-bytes lower bound (outside `value`).
+second and peak / live-bytes lower bound, then applies the plan to a slab
+and probes it by replaying the ops (all outside `value`).
 """
 from __future__ import annotations
 
@@ -95,10 +96,35 @@ def single_trace_leg(binding, tg, np, torch, reps: int = 3):
         raise SystemExit(f"single trace: device status {st}: {binding.status_string(st)}")
     _, max_live = binding.live_bytes_profile(size, first, last, t.num_ops)
     med = float(np.median(ms))
+    # the plan applied to a slab of its peak and probed by replaying the ops
+    slab = torch.empty(int(peak.item()), dtype=torch.uint8, device="cuda")
+    pws = torch.empty(binding.workspace_size(binding.OP_PROBE, n, t.num_ops), dtype=torch.uint8,
+                      device="cuda")
+    clob = torch.empty(n, dtype=torch.uint8, device="cuda")
+    n_clob = torch.empty(1, dtype=torch.int64, device="cuda")
+    probe = lambda: binding.probe_plan(size, first, last, offset, t.num_ops, slab, check=False,
+                                       out=(clob, n_clob), status=status, workspace=pws,
+                                       stream=stream)
+    probe()
+    pms = []
+    for _ in range(reps):
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record(stream)
+        probe()
+        ev[1].record(stream)
+        torch.cuda.synchronize()
+        pms.append(ev[0].elapsed_time(ev[1]))
+    if int(status.item()) != binding.MP_OK or int(n_clob.item()) != 0:
+        raise SystemExit("single trace: the probe of the plan found clobbered tensors")
+    pmed = float(np.median(pms))
+    probe_bytes = 3 * int(t.size.sum()) + 25 * n  # write, check, clear; inputs and flags
     return {"workload": "decode100k: 100,000 tensors, 4000 ops x 25 births, Geometric(0.3) "
                         "lifetimes, 2% to the end, Pareto(1.5) sizes (seed 3), lowest fit",
             "tensors_per_s": n / (med * 1e-3), "ms": med, "calls": reps,
-            "peak_over_lb": int(peak.item()) / int(max_live.item())}
+            "peak_over_lb": int(peak.item()) / int(max_live.item()),
+            "probe": {"ms": pmed, "clobbered": 0, "algorithmic_bytes": probe_bytes,
+                      "gb_per_s": probe_bytes / (pmed * 1e-3) / 1e9,
+                      "kernel": "probe_kernel (one workgroup replays the ops)"}}
 
 
 def cpu_baseline(batch, min_seconds: float = 10.0):

@@ -14,10 +14,11 @@
 //
 // One workgroup replays the whole trace: ops are sequential by definition.
 // Tensors are listed by first and by last op with a counting sort in the
-// workspace; within an op, a wave takes a tensor and its lanes stride over
-// the tensor's words.  Ops without a last use cost no barrier.  Writes are
-// device-scope atomic maxima and the checks device-scope loads, so no stale
-// cached line can hide an overwrite.
+// workspace; within an op the words of all its tensors are spread over the
+// workgroup's threads.  Writes are device-scope atomic maxima and the checks
+// device-scope loads, so no stale cached line can hide an overwrite.  All
+// checks of an op come before any of its clears, as in the definition above,
+// also when its tensors are staged in several chunks.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -36,6 +37,17 @@ __device__ __forceinline__ int32_t l2_load(const int32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Barrier between phases that pass data through global memory.  The slab and
+// the counting-sort arrays are written by plain stores and by atomics, both
+// performed in L2, and read by loads that skip the L1; a workgroup barrier
+// alone lets a wave pass while its stores are still on the way to L2, so a
+// late clear could land after the next op's atomic maximum.  Each thread
+// therefore first waits until all of its memory operations are complete.
+__device__ __forceinline__ void l2_barrier() {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+}
+
 __global__ __launch_bounds__(kPBlock) void probe_kernel(
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, const int64_t* __restrict__ offset, int64_t n,
@@ -44,7 +56,7 @@ __global__ __launch_bounds__(kPBlock) void probe_kernel(
     int32_t* __restrict__ status) {
     __shared__ uint64_t red[kPWaves];
     __shared__ int32_t carry;
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    const int tid = threadIdx.x;
 
     // ---- checks, and the highest word the plan touches
     uint64_t bad = 0, top = 0;
@@ -71,7 +83,7 @@ __global__ __launch_bounds__(kPBlock) void probe_kernel(
         bstart[t] = 0;
         dstart[t] = 0;
     }
-    __syncthreads();
+    l2_barrier();
 
     // ---- tensors by first and by last op (counting sort): counts, running
     // sums (bstart[t] = tensors first used before op t), then a scatter that
@@ -80,7 +92,7 @@ __global__ __launch_bounds__(kPBlock) void probe_kernel(
         atomicAdd(&bstart[first[i] + 1], 1);
         atomicAdd(&dstart[last[i] + 1], 1);
     }
-    __syncthreads();
+    l2_barrier();
     for (int h = 0; h < 2; ++h) {
         int32_t* c = h ? dstart : bstart;
         if (tid == 0) carry = 0;
@@ -93,49 +105,115 @@ __global__ __launch_bounds__(kPBlock) void probe_kernel(
             if (t <= num_ops) c[t] = carry + ex + v;
             __syncthreads();
             if (tid == 0) carry += tot;
-            __syncthreads();
+            l2_barrier();
         }
     }
     for (int64_t i = tid; i < n; i += kPBlock) {
         born[atomicAdd(&bstart[first[i]], 1)] = (int32_t)i;
         dies[atomicAdd(&dstart[last[i]], 1)] = (int32_t)i;
     }
-    __syncthreads();
+    l2_barrier();
 
-    // ---- replay
-    int64_t hits = 0;
+    // ---- replay.  An op's births, then its deaths, are staged in LDS (up to
+    // kPBlock at a time) with an exclusive prefix of their word counts; all
+    // threads then walk the concatenated words, word j by thread j % kPBlock,
+    // so neighbouring lanes touch neighbouring words and a large tensor is
+    // spread over the whole workgroup.
+    __shared__ uint64_t s_pre[kPBlock + 1];  // first concatenated word of each entry
+    __shared__ uint64_t s_w0[kPBlock];       // its first slab word
+    __shared__ int32_t s_id[kPBlock];
+    auto stage = [&](const int32_t* list, int32_t e0, int32_t e1) {  // returns the word total
+        const int32_t e = e0 + tid;
+        const bool has = e < e1;
+        const int32_t i = has ? l2_load(&list[e]) : 0;
+        const uint64_t wc = has ? (uint64_t)(size[i] >> 2) : 0;
+        uint64_t tot;
+        const uint64_t ex = block_exclusive_sum<kPBlock>(wc, &tot, red);
+        s_pre[tid] = ex;
+        s_w0[tid] = has ? (uint64_t)(offset[i] >> 2) : 0;
+        s_id[tid] = i;
+        if (tid == 0) s_pre[kPBlock] = ~0ull;
+        __syncthreads();
+        return tot;
+    };
+    // the entry holding concatenated word j (m entries, s_pre ascending)
+    auto entry_of = [&](uint64_t j, int m) {
+        int a = 0, z = m - 1;
+        while (a < z) {
+            const int mid = (a + z + 1) >> 1;
+            if (s_pre[mid] <= j) a = mid;
+            else z = mid - 1;
+        }
+        return a;
+    };
+    // walks over the staged words: atomic maxima, checks, clears
+    auto write = [&](uint64_t tot, int m) {
+        if (tid >= tot) return;
+        int e = entry_of(tid, m);
+        for (uint64_t j = tid; j < tot; j += kPBlock) {
+            while (s_pre[e + 1] <= j) ++e;
+            atomicMax(&slab[s_w0[e] + (j - s_pre[e])], (uint32_t)s_id[e] + 1u);
+        }
+    };
+    auto check = [&](uint64_t tot, int m) {
+        if (tid >= tot) return;
+        int e = entry_of(tid, m);
+        for (uint64_t j = tid; j < tot; j += 4 * kPBlock) {  // four loads in flight
+            int ee[4];
+            uint32_t got[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const uint64_t ju = j + (uint64_t)u * kPBlock;
+                if (ju < tot) {
+                    while (s_pre[e + 1] <= ju) ++e;
+                    ee[u] = e;
+                    got[u] = slab_load(&slab[s_w0[e] + (ju - s_pre[e])]);
+                } else {
+                    ee[u] = -1;
+                    got[u] = 0;
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (ee[u] >= 0 && got[u] != (uint32_t)s_id[ee[u]] + 1u) clob[s_id[ee[u]]] = 1;
+        }
+    };
+    auto clear = [&](uint64_t tot, int m) {
+        if (tid >= tot) return;
+        int e = entry_of(tid, m);
+        for (uint64_t j = tid; j < tot; j += kPBlock) {
+            while (s_pre[e + 1] <= j) ++e;
+            slab[s_w0[e] + (j - s_pre[e])] = 0;
+        }
+    };
     for (int32_t t = 0; t < num_ops; ++t) {
         const int32_t b0 = t ? l2_load(&bstart[t - 1]) : 0, b1 = l2_load(&bstart[t]);
         const int32_t d0 = t ? l2_load(&dstart[t - 1]) : 0, d1 = l2_load(&dstart[t]);
-        for (int32_t k = b0 + wid; k < b1; k += kPWaves) {  // writes: a wave per tensor
-            const int32_t i = l2_load(&born[k]);
-            const uint32_t v = (uint32_t)i + 1u;
-            const int64_t w0 = offset[i] >> 2, w1 = (offset[i] + size[i]) >> 2;
-            for (int64_t w = w0 + lane; w < w1; w += kWave) atomicMax(&slab[w], v);
+        for (int32_t c0 = b0; c0 < b1; c0 += kPBlock) {
+            write(stage(born, c0, b1), min(kPBlock, b1 - c0));
+            l2_barrier();
         }
-        if (d0 == d1) continue;
-        __syncthreads();
-        for (int32_t k = d0 + wid; k < d1; k += kPWaves) {  // checks
-            const int32_t i = l2_load(&dies[k]);
-            const uint32_t v = (uint32_t)i + 1u;
-            const int64_t w0 = offset[i] >> 2, w1 = (offset[i] + size[i]) >> 2;
-            bool foreign = false;
-            for (int64_t w = w0 + lane; w < w1; w += kWave) foreign |= slab_load(&slab[w]) != v;
-            if (__ballot(foreign) && lane == 0) {
-                clob[i] = 1;
-                ++hits;
+        // every check of op t before any of its clears; one chunk is staged
+        // once, several are staged again for the clears
+        const bool one = d1 - d0 <= kPBlock;
+        for (int32_t c0 = d0; c0 < d1; c0 += kPBlock) {
+            const int m = min(kPBlock, d1 - c0);
+            const uint64_t tot = stage(dies, c0, d1);
+            check(tot, m);
+            __syncthreads();
+            if (one) clear(tot, m);
+        }
+        if (!one)
+            for (int32_t c0 = d0; c0 < d1; c0 += kPBlock) {
+                clear(stage(dies, c0, d1), min(kPBlock, d1 - c0));
+                __syncthreads();
             }
-        }
-        __syncthreads();
-        for (int32_t k = d0 + wid; k < d1; k += kPWaves) {  // clears
-            const int32_t i = l2_load(&dies[k]);
-            const int64_t w0 = offset[i] >> 2, w1 = (offset[i] + size[i]) >> 2;
-            for (int64_t w = w0 + lane; w < w1; w += kWave) slab[w] = 0;
-        }
-        __syncthreads();
+        if (d1 > d0) l2_barrier();
     }
-    hits = block_reduce<kPBlock>((uint64_t)hits, OpAdd<uint64_t>(), red);
-    if (tid == 0) *n_clob = hits;
+    uint64_t hits = 0;
+    for (int64_t i = tid; i < n; i += kPBlock) hits += clob[i];
+    hits = block_reduce<kPBlock>(hits, OpAdd<uint64_t>(), red);
+    if (tid == 0) *n_clob = (int64_t)hits;
 }
 
 }  // namespace
