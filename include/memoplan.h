@@ -198,10 +198,19 @@ int32_t mp_validate_batch(const int64_t* begin, int64_t n_traces, const int64_t*
  *              plan's peak), 4-byte aligned; overwritten.
  *   clobbered_out[n] uint8: 1 for a clobbered tensor, else 0.
  *   n_clobbered_out: one device int64, the number of clobbered tensors.
- *   workspace: mp_workspace_size(MP_OP_PROBE, n, num_ops, 0) bytes.
+ *   workspace: mp_workspace_size(MP_OP_PROBE, n, num_ops, capacity) bytes,
+ *              or more; contents need no initialisation.  `capacity` is the
+ *              number of (tensor, 256-byte slab tile) pairs the tiled replay
+ *              holds, 0 for 16 n + 65536; the call takes the largest capacity
+ *              that workspace_bytes holds.
+ * The replay is split by address: one wave per tile of 64 words replays, in
+ * op order, the events of the tensors covering the tile.  A plan with more
+ * pairs than the capacity is replayed op by op by one workgroup instead
+ * (same results, far slower).
  * Data errors (MP_EINVAL on the status word): a size <= 0, a size or offset
  * not a multiple of 4, a negative offset, an invalid lifetime, a slab smaller
- * than the plan.  One workgroup replays the ops in order. */
+ * than the plan.  A workspace too small even for the op-by-op replay is
+ * MP_EINVAL from the call. */
 int32_t mp_probe_plan(const int64_t* size, const int32_t* first, const int32_t* last,
                       const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
                       size_t slab_bytes, uint8_t* clobbered_out, int64_t* n_clobbered_out,

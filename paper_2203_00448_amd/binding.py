@@ -285,9 +285,12 @@ def apply_plan(offset, size, peak: int, device="cuda"):
 
 
 def probe_plan(size, first, last, offset, num_ops: int, slab: torch.Tensor, *,
-               check: bool = True, out=None, status=None, workspace=None, stream=None):
+               check: bool = True, out=None, status=None, workspace=None, stream=None,
+               capacity: int = 0):
     """Write-pattern aliasing probe of a plan over `slab` (mp_probe_plan).
-    Returns (clobbered uint8[n], n_clobbered int64[1]) on the GPU."""
+    `capacity` sizes a new workspace: the (tensor, 256-byte tile) pairs the
+    tiled replay holds (0: the library's default); a plan with more pairs is
+    replayed op by op.  Returns (clobbered uint8[n], n_clobbered int64[1])."""
     L = load_library()
     size = _dev(size, torch.int64, "size")
     first = _dev(first, torch.int32, "first")
@@ -302,11 +305,14 @@ def probe_plan(size, first, last, offset, num_ops: int, slab: torch.Tensor, *,
         cnt = torch.empty(1, dtype=torch.int64, device=dev)
     else:
         clob, cnt = out
-    ws, need = _workspace(OP_PROBE, dev, n, num_ops, 0, workspace)
+    # the library takes the largest capacity the workspace holds (MP_EINVAL
+    # if it is too small even for the op-by-op replay)
+    ws = workspace if workspace is not None else _workspace(OP_PROBE, dev, n, num_ops,
+                                                            capacity)[0]
     if status is None:
         status = new_status(dev, stream)
     rc = L.mp_probe_plan(_p(size), _p(first), _p(last), _p(offset), n, int(num_ops), _p(slab),
-                         slab.numel() * slab.element_size(), _p(clob), _p(cnt), _p(ws), need,
-                         _p(status), _stream(stream))
+                         slab.numel() * slab.element_size(), _p(clob), _p(cnt), _p(ws),
+                         ws.numel() * ws.element_size(), _p(status), _stream(stream))
     _finish(rc, status, "probe_plan", check)
     return clob, cnt

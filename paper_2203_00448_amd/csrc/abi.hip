@@ -66,7 +66,9 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
         case MP_OP_PLAN_TRACE:
             return n_tensors >= (int64_t)1 << 30 ? 0 : plan_trace_workspace_bytes(n_tensors);
         case MP_OP_PROBE:
-            return num_ops > INT32_MAX ? 0 : probe_workspace_bytes(n_tensors, (int32_t)num_ops);
+            return num_ops > INT32_MAX ? 0
+                                       : probe_workspace_bytes(n_tensors, (int32_t)num_ops,
+                                                               capacity);
         default:
             return 0;
     }
@@ -153,8 +155,8 @@ extern "C" int32_t mp_probe_plan(const int64_t* size, const int32_t* first, cons
     if (n > 0 && (!size || !first || !last || !offset || !clobbered_out || !slab))
         return MP_EINVAL;
     if (slab && (reinterpret_cast<uintptr_t>(slab) & 3)) return MP_EINVAL;
-    if (workspace_bytes < probe_workspace_bytes(n, num_ops)) return MP_EINVAL;
+    if (probe_capacity(n, num_ops, workspace_bytes) < 0) return MP_EINVAL;
     return launched(launch_probe(size, first, last, offset, n, num_ops, slab, slab ? slab_bytes : 0,
-                                 clobbered_out, n_clobbered_out, workspace, status_out,
-                                 static_cast<hipStream_t>(stream)));
+                                 clobbered_out, n_clobbered_out, workspace, workspace_bytes,
+                                 status_out, static_cast<hipStream_t>(stream)));
 }

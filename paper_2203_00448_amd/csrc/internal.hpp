@@ -40,11 +40,12 @@ hipError_t launch_reset_status(int32_t* status, hipStream_t st);
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st);
 
 // write-pattern aliasing probe of a plan (probe.hip)
-size_t probe_workspace_bytes(int64_t n, int32_t num_ops);
+size_t probe_workspace_bytes(int64_t n, int32_t num_ops, int64_t capacity);
+int64_t probe_capacity(int64_t n, int32_t num_ops, size_t workspace_bytes);
 hipError_t launch_probe(const int64_t* size, const int32_t* first, const int32_t* last,
                         const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
                         size_t slab_bytes, uint8_t* clob, int64_t* n_clob, void* ws,
-                        int32_t* status, hipStream_t st);
+                        size_t ws_bytes, int32_t* status, hipStream_t st);
 
 }  // namespace mp
 
@@ -60,7 +61,7 @@ hipError_t device_scan_i64(int64_t* data, int64_t n, bool inclusive, int64_t* pa
 size_t radix_workspace_bytes(int64_t n);
 hipError_t radix_sort_pairs(uint64_t* k0, uint32_t* v0, uint64_t* k1, uint32_t* v1, int64_t n,
                             int begin_bit, int end_bit, void* ws, bool* in_alt, hipStream_t st,
-                            const uint32_t* skip = nullptr);
+                            const uint32_t* skip = nullptr, const int64_t* n_live = nullptr);
 
 // liveness profile (live.hip)
 size_t live_workspace_bytes(int32_t num_ops);

@@ -12,13 +12,18 @@
 // plan clobbers nothing; of every pair that breaks the constraints of Eq. 2.1
 // at least one member is clobbered.
 //
-// One workgroup replays the whole trace: ops are sequential by definition.
-// Tensors are listed by first and by last op with a counting sort in the
-// workspace; within an op the words of all its tensors are spread over the
-// workgroup's threads.  Writes are device-scope atomic maxima and the checks
-// device-scope loads, so no stale cached line can hide an overwrite.  All
-// checks of an op come before any of its clears, as in the definition above,
-// also when its tensors are staged in several chunks.
+// What happens to a word depends only on the tensors whose ranges cover it,
+// so the replay splits by address: the slab is cut into tiles of 64 words,
+// one wave replays one tile with one word per lane, and only the events of
+// the tensors covering the tile are visited, in op order (births before
+// deaths).  The per-tile event lists are one radix sort of (tile, 2 op +
+// kind) keys, one key per tensor, tile and kind.  A lane owns its word for
+// the whole replay: it keeps the word's value in a register for the maxima,
+// stores every change to the slab, and checks what it reads back from the
+// slab.  The number of (tensor, tile) pairs is known only on the device;
+// when it exceeds what the workspace holds, the tiled kernels stand down and
+// one workgroup replays the ops one after another instead (same results).
+
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -48,15 +53,34 @@ __device__ __forceinline__ void l2_barrier() {
     __syncthreads();
 }
 
-__global__ __launch_bounds__(kPBlock) void probe_kernel(
+// Device words that choose the path of one call.
+struct ProbeFlags {
+    uint32_t bad;      // an input failed its checks
+    uint32_t skip;     // the tiled kernels do nothing (bad input, or too many pairs)
+    uint32_t run_ops;  // the op-by-op replay runs instead
+    uint32_t pad;
+    unsigned long long top;  // one past the highest word the plan touches
+    int64_t n_tiles;         // tiles of 64 words below top
+};
+static_assert(sizeof(ProbeFlags) <= 256, "the flags fill the first 256 workspace bytes");
+
+// ---------------------------------------------------------------------------
+// Op-by-op replay: one workgroup walks the ops in order.  Tensors are listed
+// by first and by last op with a counting sort in the workspace; within an op
+// the words of all its tensors are spread over the workgroup's threads.
+// Writes are device-scope atomic maxima and the checks device-scope loads, so
+// no stale cached line can hide an overwrite.  All checks of an op come
+// before any of its clears, also when its tensors are staged in chunks.
+__global__ __launch_bounds__(kPBlock) void probe_ops_kernel(
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, const int64_t* __restrict__ offset, int64_t n,
     int32_t num_ops, uint32_t* slab, int64_t slab_words, uint8_t* __restrict__ clob,
     int64_t* __restrict__ n_clob, int32_t* bstart, int32_t* dstart, int32_t* born, int32_t* dies,
-    int32_t* __restrict__ status) {
+    int32_t* __restrict__ status, const ProbeFlags* fl) {
     __shared__ uint64_t red[kPWaves];
     __shared__ int32_t carry;
     const int tid = threadIdx.x;
+    if (!fl->run_ops) return;
 
     // ---- checks, and the highest word the plan touches
     uint64_t bad = 0, top = 0;
@@ -216,24 +240,319 @@ __global__ __launch_bounds__(kPBlock) void probe_kernel(
     if (tid == 0) *n_clob = (int64_t)hits;
 }
 
+// ---------------------------------------------------------------------------
+// Tiled replay.
+
+constexpr int kTileShift = 6;  // 64 words (256 bytes) per tile, one per lane
+constexpr int kTBlock = 256;
+constexpr int kTWaves = kTBlock / kWave;
+
+__global__ void probe_init_kernel(ProbeFlags* fl, int64_t* n_clob) {
+    fl->bad = 0;
+    fl->skip = 1;
+    fl->run_ops = 0;
+    fl->pad = 0;
+    fl->top = 0;
+    fl->n_tiles = 0;
+    *n_clob = 0;
+}
+
+// Checks every tensor, clears its flag and counts its events: a birth and a
+// death in each tile its range meets.
+__global__ __launch_bounds__(kTBlock) void probe_prepare_kernel(
+    const int64_t* __restrict__ size, const int32_t* __restrict__ first,
+    const int32_t* __restrict__ last, const int64_t* __restrict__ offset, int64_t n,
+    int32_t num_ops, uint8_t* __restrict__ clob, int64_t* __restrict__ cnt, ProbeFlags* fl) {
+    const int64_t i = (int64_t)blockIdx.x * kTBlock + threadIdx.x;
+    bool bad = false;
+    uint64_t top = 0;
+    if (i < n) {
+        const int64_t s = size[i], o = offset[i];
+        const int32_t f = first[i], l = last[i];
+        if (s <= 0 || (s & 3) || o < 0 || (o & 3) || o > INT64_MAX - s || f < 0 || f > l ||
+            l >= num_ops) {
+            bad = true;
+            cnt[i] = 0;
+        } else {
+            const uint64_t w0 = (uint64_t)o >> 2, w1 = (uint64_t)(o + s) >> 2;
+            top = w1;
+            cnt[i] = 2 * (int64_t)(((w1 - 1) >> kTileShift) - (w0 >> kTileShift) + 1);
+        }
+        clob[i] = 0;
+    }
+    if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) atomicOr(&fl->bad, 1u);
+    top = wave_reduce(top, OpMax<uint64_t>());
+    if ((threadIdx.x & (kWave - 1)) == 0 && top) atomicMax(&fl->top, (unsigned long long)top);
+}
+
+// Picks the path once the inputs are checked and the events are counted.
+__global__ void probe_decide_kernel(ProbeFlags* fl, const int64_t* total, int64_t capacity,
+                                    int64_t slab_words, int32_t* status) {
+    if (fl->bad || fl->top > (unsigned long long)slab_words) {
+        raise_status(status, MP_EINVAL);
+        return;  // skip stays set, run_ops clear
+    }
+    fl->n_tiles = (int64_t)((fl->top + 63) >> kTileShift);
+    const bool fits = *total <= capacity;
+    fl->skip = fits ? 0u : 1u;
+    fl->run_ops = fits ? 0u : 1u;
+}
+
+// Writes the events of each tensor at its place in the exclusive prefix of
+// the counts: key (tile << op_bits) | (2 first) for the birth and
+// (tile << op_bits) | (2 last + 1) for the death, value the tensor id.
+__global__ __launch_bounds__(kTBlock) void probe_emit_kernel(
+    const int64_t* __restrict__ size, const int32_t* __restrict__ first,
+    const int32_t* __restrict__ last, const int64_t* __restrict__ offset, int64_t n, int op_bits,
+    const int64_t* __restrict__ base, uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+    const ProbeFlags* fl) {
+    if (fl->skip) return;
+    const int64_t i = (int64_t)blockIdx.x * kTBlock + threadIdx.x;
+    if (i >= n) return;
+    const int64_t o = offset[i], s = size[i];
+    const uint64_t kb = 2ull * (uint32_t)first[i], kd = 2ull * (uint32_t)last[i] + 1;
+    const uint64_t t0 = ((uint64_t)o >> 2) >> kTileShift, t1 = (((uint64_t)(o + s) >> 2) - 1) >> kTileShift;
+    int64_t e = base[i];
+    for (uint64_t t = t0; t <= t1; ++t, e += 2) {
+        keys[e] = (t << op_bits) | kb;
+        vals[e] = (uint32_t)i;
+        keys[e + 1] = (t << op_bits) | kd;
+        vals[e + 1] = (uint32_t)i;
+    }
+}
+
+// First index in [0, total) whose tile (key >> op_bits) is >= tile, or > tile
+// when `after`; total if there is none.  The wave samples 64 evenly spaced
+// keys per round, so a million keys take four rounds of one load each.
+__device__ int64_t wave_find(const uint64_t* __restrict__ keys, int64_t total, int op_bits,
+                             uint64_t tile, bool after, int lane) {
+    int64_t lo = 0, hi = total;  // the answer lies in [lo, hi]; hi is total or a hit
+    while (lo < hi) {
+        const int64_t step = (hi - lo + kWave - 1) / kWave;
+        const int64_t idx = lo + (int64_t)(lane + 1) * step - 1;
+        bool hit = true;
+        if (idx < hi) {
+            const uint64_t t = keys[idx] >> op_bits;
+            hit = after ? t > tile : t >= tile;
+        }
+        const uint64_t b = __ballot(hit);
+        if (!b) return hi;
+        const int f = __builtin_ctzll(b);
+        hi = min(hi, lo + (int64_t)(f + 1) * step - 1);
+        lo += (int64_t)f * step;
+    }
+    return lo;
+}
+
+__device__ __forceinline__ uint32_t lane_word_load(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+__device__ __forceinline__ void lane_word_store(uint32_t* p, uint32_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+__device__ __forceinline__ int64_t readlane64(int64_t v, int j) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, j);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), j);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// One wave per tile, word tile * 64 + lane per lane.  The slab accesses are
+// relaxed atomics at wavefront scope only so that every change really goes
+// to memory and every check really reads it back; no other lane ever touches
+// the word.
+__global__ __launch_bounds__(kTBlock) void probe_tiles_kernel(
+    const int64_t* __restrict__ size, const int64_t* __restrict__ offset,
+    const uint64_t* __restrict__ keys, const uint32_t* __restrict__ vals,
+    const int64_t* __restrict__ total_p, int op_bits, uint32_t* slab,
+    uint8_t* __restrict__ clob, const ProbeFlags* fl) {
+    if (fl->skip) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t n_tiles = fl->n_tiles, total = *total_p;
+    const uint64_t top = fl->top;
+    const uint32_t kind_key_mask = op_bits >= 32 ? ~0u : ((1u << op_bits) - 1u);
+    for (int64_t tile = (int64_t)blockIdx.x * kTWaves + threadIdx.x / kWave; tile < n_tiles;
+         tile += (int64_t)gridDim.x * kTWaves) {
+        const int64_t w = (tile << kTileShift) + lane;
+        const bool mine = (uint64_t)w < top;
+        uint32_t* word = slab + (mine ? w : 0);
+        if (mine) lane_word_store(word, 0u);
+        uint32_t v = 0;           // the word's value
+        bool clr = false;         // covered by a death of the pending group
+        uint32_t pend = ~0u;      // key of the pending group of deaths, ~0 for none
+        const int64_t e0 = wave_find(keys, total, op_bits, (uint64_t)tile, false, lane);
+        const int64_t e1 = wave_find(keys, total, op_bits, (uint64_t)tile, true, lane);
+        for (int64_t b = e0; b < e1; b += kWave) {
+            const int64_t k = b + lane;
+            uint32_t key = 0, id = 0;
+            int64_t lo = 0, hi = 0;
+            if (k < e1) {
+                key = (uint32_t)keys[k] & kind_key_mask;
+                id = vals[k];
+                const int64_t o = offset[id];
+                lo = o >> 2;
+                hi = (o + size[id]) >> 2;
+            }
+            const int m = (int)min((int64_t)kWave, e1 - b);
+            for (int j = 0; j < m; ++j) {
+                const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)key, j);
+                const uint32_t idj = (uint32_t)__builtin_amdgcn_readlane((int)id, j);
+                const int64_t loj = readlane64(lo, j), hij = readlane64(hi, j);
+                if (pend != ~0u && kj != pend) {  // the group of deaths is over: clear
+                    if (clr) {
+                        v = 0;
+                        lane_word_store(word, 0u);
+                    }
+                    clr = false;
+                    pend = ~0u;
+                }
+                const bool cov = w >= loj && w < hij;
+                if (!(kj & 1u)) {  // birth
+                    if (cov) {
+                        v = max(v, idj + 1u);
+                        lane_word_store(word, v);
+                    }
+                } else {  // death: check now, clear after the group
+                    pend = kj;
+                    if (cov) {
+                        if (lane_word_load(word) != idj + 1u) clob[idj] = 1;
+                        clr = true;
+                    }
+                }
+            }
+        }
+        if (clr) lane_word_store(word, 0u);
+    }
+}
+
+__global__ __launch_bounds__(kTBlock) void probe_count_kernel(const uint8_t* __restrict__ clob,
+                                                              int64_t n, int64_t* n_clob,
+                                                              const ProbeFlags* fl) {
+    if (fl->skip) return;
+    uint64_t c = 0;
+    for (int64_t i = (int64_t)blockIdx.x * kTBlock + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kTBlock)
+        c += clob[i];
+    c = wave_reduce(c, OpAdd<uint64_t>());
+    if ((threadIdx.x & (kWave - 1)) == 0 && c)
+        atomicAdd(reinterpret_cast<unsigned long long*>(n_clob), (unsigned long long)c);
+}
+
+// Workspace sections.  8-byte arrays come first, then 4-byte ones, with no
+// padding between them, so every extra pair of capacity costs bytes and a
+// workspace of probe_workspace_bytes(n, ops, c) holds capacity c exactly.
+struct ProbeLayout {
+    size_t flags, cnt, partial, keys0, keys1, radix, bstart, dstart, born, dies, vals0, vals1, end;
+};
+
+ProbeLayout probe_layout(int64_t n, int32_t num_ops, int64_t capacity) {
+    const size_t nn = (size_t)(n > 0 ? n : 1), ops = (size_t)num_ops + 1;
+    const size_t ev = (size_t)(capacity > 0 ? 2 * capacity : 1);
+    ProbeLayout L;
+    size_t at = 0;
+    auto take = [&](size_t bytes) {
+        const size_t here = at;
+        at += bytes;
+        return here;
+    };
+    L.flags = take(256);  // ProbeFlags, padded
+    L.cnt = take(nn * 8);
+    L.partial = take(scan_workspace_bytes((int64_t)nn));
+    L.keys0 = take(ev * 8);
+    L.keys1 = take(ev * 8);
+    L.radix = take(radix_workspace_bytes((int64_t)ev));
+    L.bstart = take(ops * 4);
+    L.dstart = take(ops * 4);
+    L.born = take(nn * 4);
+    L.dies = take(nn * 4);
+    L.vals0 = take(ev * 4);
+    L.vals1 = take(ev * 4);
+    L.end = at;
+    return L;
+}
+
+int bit_width(uint64_t x) { return x ? 64 - __builtin_clzll(x) : 0; }
+
 }  // namespace
 
-size_t probe_workspace_bytes(int64_t n, int32_t num_ops) {
-    if (n < 0 || n >= INT32_MAX || num_ops < 0) return 0;
-    return (2 * ((size_t)num_ops + 1) + 2 * (size_t)(n > 0 ? n : 1)) * sizeof(int32_t);
+// capacity: (tensor, tile) pairs the tiled replay can hold; 0 means the
+// default of 16 n + 65536.
+size_t probe_workspace_bytes(int64_t n, int32_t num_ops, int64_t capacity) {
+    if (n < 0 || n >= INT32_MAX || num_ops < 0 || capacity < 0 ||
+        capacity > ((int64_t)1 << 40))
+        return 0;
+    if (capacity == 0) capacity = 16 * n + 65536;
+    return probe_layout(n, num_ops, capacity).end;
+}
+
+// The largest capacity a workspace of `bytes` holds, or -1 if it is too small
+// even for the op-by-op replay.
+int64_t probe_capacity(int64_t n, int32_t num_ops, size_t bytes) {
+    if (n < 0 || n >= INT32_MAX || num_ops < 0) return -1;
+    if (probe_layout(n, num_ops, 0).end > bytes) return -1;
+    int64_t lo = 0, hi = (int64_t)1 << 40;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo + 1) / 2;
+        if (probe_layout(n, num_ops, mid).end <= bytes) lo = mid;
+        else hi = mid - 1;
+    }
+    return lo;
 }
 
 hipError_t launch_probe(const int64_t* size, const int32_t* first, const int32_t* last,
                         const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
                         size_t slab_bytes, uint8_t* clob, int64_t* n_clob, void* ws,
-                        int32_t* status, hipStream_t st) {
-    int32_t* b = static_cast<int32_t*>(ws);
-    int32_t* d = b + (num_ops + 1);
-    int32_t* born = d + (num_ops + 1);
-    int32_t* dies = born + (n > 0 ? n : 1);
-    hipLaunchKernelGGL(probe_kernel, dim3(1), dim3(kPBlock), 0, st, size, first, last, offset, n,
-                       num_ops, static_cast<uint32_t*>(slab), (int64_t)(slab_bytes / 4), clob,
-                       n_clob, b, d, born, dies, status);
+                        size_t ws_bytes, int32_t* status, hipStream_t st) {
+    const int64_t capacity = probe_capacity(n, num_ops, ws_bytes);
+    if (capacity < 0) return hipErrorInvalidValue;
+    const ProbeLayout L = probe_layout(n, num_ops, capacity);
+    char* w = static_cast<char*>(ws);
+    ProbeFlags* fl = reinterpret_cast<ProbeFlags*>(w + L.flags);
+    hipLaunchKernelGGL(probe_init_kernel, dim3(1), dim3(1), 0, st, fl, n_clob);
+    if (n == 0) return hipGetLastError();
+
+    const int64_t slab_words = (int64_t)(slab_bytes / 4);
+    const int64_t max_tiles = (slab_words + 63) >> kTileShift;
+    const int op_bits = num_ops > 0 ? bit_width(2 * (uint64_t)num_ops - 1) : 1;
+    const int tile_bits = bit_width(max_tiles > 1 ? (uint64_t)(max_tiles - 1) : 0);
+    if (op_bits + tile_bits > 64) return hipErrorInvalidValue;
+    int64_t* cnt = reinterpret_cast<int64_t*>(w + L.cnt);
+    int64_t* partial = reinterpret_cast<int64_t*>(w + L.partial);
+    const int64_t* total = partial + (scan_workspace_bytes(n) / sizeof(int64_t) - 1);
+    const unsigned nb = (unsigned)((n + kTBlock - 1) / kTBlock);
+
+    hipLaunchKernelGGL(probe_prepare_kernel, dim3(nb), dim3(kTBlock), 0, st, size, first, last,
+                       offset, n, num_ops, clob, cnt, fl);
+    hipError_t e = device_scan_i64(cnt, n, false, partial, nullptr, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(probe_decide_kernel, dim3(1), dim3(1), 0, st, fl, total, 2 * capacity,
+                       slab_words, status);
+    if (max_tiles > 0 && capacity > 0) {
+        uint64_t* k0 = reinterpret_cast<uint64_t*>(w + L.keys0);
+        uint64_t* k1 = reinterpret_cast<uint64_t*>(w + L.keys1);
+        uint32_t* v0 = reinterpret_cast<uint32_t*>(w + L.vals0);
+        uint32_t* v1 = reinterpret_cast<uint32_t*>(w + L.vals1);
+        hipLaunchKernelGGL(probe_emit_kernel, dim3(nb), dim3(kTBlock), 0, st, size, first, last,
+                           offset, n, op_bits, (const int64_t*)cnt, k0, v0, (const ProbeFlags*)fl);
+        bool alt = false;
+        e = radix_sort_pairs(k0, v0, k1, v1, 2 * capacity, 0, op_bits + tile_bits, w + L.radix,
+                             &alt, st, &fl->skip, total);
+        if (e != hipSuccess) return e;
+        const int64_t blocks = min((max_tiles + kTWaves - 1) / kTWaves, (int64_t)1 << 16);
+        hipLaunchKernelGGL(probe_tiles_kernel, dim3((unsigned)blocks), dim3(kTBlock), 0, st, size,
+                           offset, (const uint64_t*)(alt ? k1 : k0),
+                           (const uint32_t*)(alt ? v1 : v0), total, op_bits,
+                           static_cast<uint32_t*>(slab), clob, (const ProbeFlags*)fl);
+        hipLaunchKernelGGL(probe_count_kernel, dim3((unsigned)min((int64_t)nb, (int64_t)1024)),
+                           dim3(kTBlock), 0, st, (const uint8_t*)clob, n, n_clob,
+                           (const ProbeFlags*)fl);
+    }
+    int32_t* b = reinterpret_cast<int32_t*>(w + L.bstart);
+    int32_t* d = reinterpret_cast<int32_t*>(w + L.dstart);
+    int32_t* born = reinterpret_cast<int32_t*>(w + L.born);
+    int32_t* dies = reinterpret_cast<int32_t*>(w + L.dies);
+    hipLaunchKernelGGL(probe_ops_kernel, dim3(1), dim3(kPBlock), 0, st, size, first, last, offset,
+                       n, num_ops, static_cast<uint32_t*>(slab), slab_words, clob, n_clob, b, d,
+                       born, dies, status, (const ProbeFlags*)fl);
     return hipGetLastError();
 }
 

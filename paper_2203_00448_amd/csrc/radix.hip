@@ -19,12 +19,18 @@ __global__ __launch_bounds__(kRadixBlock) void radix_count_kernel(const uint64_t
                                                                   int64_t n, int shift,
                                                                   int64_t* __restrict__ counts,
                                                                   int64_t n_tiles,
-                                                                  const uint32_t* skip) {
+                                                                  const uint32_t* skip,
+                                                                  const int64_t* n_live) {
     __shared__ uint32_t hist[kDigits];
     if (skip && *skip) return;
+    if (n_live) n = min(n, *n_live);
+    const int64_t base = (int64_t)blockIdx.x * kRadixTile;
+    if (base >= n) {  // a tile past the live elements counts nothing
+        counts[(int64_t)threadIdx.x * n_tiles + blockIdx.x] = 0;
+        return;
+    }
     hist[threadIdx.x] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kRadixTile;
 #pragma unroll
     for (int k = 0; k < kRadixItems; ++k) {
         const int64_t e = base + k * kRadixBlock + threadIdx.x;
@@ -37,9 +43,11 @@ __global__ __launch_bounds__(kRadixBlock) void radix_count_kernel(const uint64_t
 __global__ __launch_bounds__(kRadixBlock) void radix_scatter_kernel(
     const uint64_t* __restrict__ kin, const uint32_t* __restrict__ vin, uint64_t* __restrict__ kout,
     uint32_t* __restrict__ vout, int64_t n, int shift, const int64_t* __restrict__ offs,
-    int64_t n_tiles, const uint32_t* skip) {
+    int64_t n_tiles, const uint32_t* skip, const int64_t* n_live) {
     constexpr int kWaves = kRadixBlock / kWave;
     if (skip && *skip) return;
+    if (n_live) n = min(n, *n_live);
+    if ((int64_t)blockIdx.x * kRadixTile >= n) return;
     __shared__ uint32_t wave_cnt[kWaves][kDigits];
     __shared__ uint32_t running[kDigits];
     __shared__ int64_t gbase[kDigits];
@@ -98,10 +106,12 @@ size_t radix_workspace_bytes(int64_t n) {
 // alternate between (k0, v0) and (k1, v1); *in_alt tells where the result
 // is.  v0/v1 may be null (keys only).  `ws` has radix_workspace_bytes(n).
 // A non-null `skip` word that is nonzero at run time turns every kernel into
-// a no-op (the buffers then stay as they were).
+// a no-op (the buffers then stay as they were).  A non-null `n_live` is a
+// device count read at run time: only the first min(n, *n_live) pairs are
+// sorted (n then only bounds the launch).
 hipError_t radix_sort_pairs(uint64_t* k0, uint32_t* v0, uint64_t* k1, uint32_t* v1, int64_t n,
                             int begin_bit, int end_bit, void* ws, bool* in_alt, hipStream_t st,
-                            const uint32_t* skip) {
+                            const uint32_t* skip, const int64_t* n_live) {
     *in_alt = false;
     if (n <= 1 || end_bit <= begin_bit) return hipSuccess;
     const int64_t tiles = (n + kRadixTile - 1) / kRadixTile;
@@ -115,11 +125,12 @@ hipError_t radix_sort_pairs(uint64_t* k0, uint32_t* v0, uint64_t* k1, uint32_t* 
         uint64_t* ko = alt ? k0 : k1;
         uint32_t* vo = alt ? v0 : v1;
         hipLaunchKernelGGL(radix_count_kernel, dim3((unsigned)tiles), dim3(kRadixBlock), 0, st, ki,
-                           n, shift, counts, tiles, skip);
+                           n, shift, counts, tiles, skip, n_live);
         hipError_t e = device_scan_i64(counts, tiles * kDigits, false, partial, nullptr, st, skip);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(radix_scatter_kernel, dim3((unsigned)tiles), dim3(kRadixBlock), 0, st,
-                           ki, vi, ko, vo, n, shift, (const int64_t*)counts, tiles, skip);
+                           ki, vi, ko, vo, n, shift, (const int64_t*)counts, tiles, skip,
+                           n_live);
         alt = !alt;
     }
     *in_alt = alt;
