@@ -61,6 +61,8 @@ struct ProbeFlags {
     uint32_t pad;
     unsigned long long top;  // one past the highest word the plan touches
     int64_t n_tiles;         // tiles of 64 words below top
+    uint32_t n_big;          // tensors over more than kSmallSpan tiles
+    uint32_t sink;           // written by lanes past the top of the slab, never read
 };
 static_assert(sizeof(ProbeFlags) <= 256, "the flags fill the first 256 workspace bytes");
 
@@ -246,6 +248,9 @@ __global__ __launch_bounds__(kPBlock) void probe_ops_kernel(
 constexpr int kTileShift = 6;  // 64 words (256 bytes) per tile, one per lane
 constexpr int kTBlock = 256;
 constexpr int kTWaves = kTBlock / kWave;
+constexpr int kSmallSpan = 16;  // tensors over more tiles are emitted by whole workgroups
+constexpr int kUnroll = 8;      // events whose checks are in flight together
+constexpr int kPad = 2 * kUnroll;  // event-buffer entries past the capacity (read ahead)
 
 __global__ void probe_init_kernel(ProbeFlags* fl, int64_t* n_clob) {
     fl->bad = 0;
@@ -254,6 +259,7 @@ __global__ void probe_init_kernel(ProbeFlags* fl, int64_t* n_clob) {
     fl->pad = 0;
     fl->top = 0;
     fl->n_tiles = 0;
+    fl->n_big = 0;
     *n_clob = 0;
 }
 
@@ -281,8 +287,9 @@ __global__ __launch_bounds__(kTBlock) void probe_prepare_kernel(
         clob[i] = 0;
     }
     if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) atomicOr(&fl->bad, 1u);
-    top = wave_reduce(top, OpMax<uint64_t>());
-    if ((threadIdx.x & (kWave - 1)) == 0 && top) atomicMax(&fl->top, (unsigned long long)top);
+    __shared__ uint64_t red[kTWaves];
+    top = block_reduce<kTBlock>(top, OpMax<uint64_t>(), red);
+    if (threadIdx.x == 0 && top) atomicMax(&fl->top, (unsigned long long)top);
 }
 
 // Picks the path once the inputs are checked and the events are counted.
@@ -300,24 +307,54 @@ __global__ void probe_decide_kernel(ProbeFlags* fl, const int64_t* total, int64_
 
 // Writes the events of each tensor at its place in the exclusive prefix of
 // the counts: key (tile << op_bits) | (2 first) for the birth and
-// (tile << op_bits) | (2 last + 1) for the death, value the tensor id.
+// (tile << op_bits) | (2 last + 1) for the death, value the tensor id.  A
+// thread writes the events of a tensor over at most kSmallSpan tiles and
+// lists the larger ones for probe_emit_big_kernel.
+__device__ __forceinline__ void emit_pair(uint64_t* keys, uint32_t* vals, int64_t e, uint64_t t,
+                                          int op_bits, uint64_t kb, uint64_t kd, uint32_t i) {
+    keys[e] = (t << op_bits) | kb;
+    vals[e] = i;
+    keys[e + 1] = (t << op_bits) | kd;
+    vals[e + 1] = i;
+}
+
 __global__ __launch_bounds__(kTBlock) void probe_emit_kernel(
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, const int64_t* __restrict__ offset, int64_t n, int op_bits,
     const int64_t* __restrict__ base, uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
-    const ProbeFlags* fl) {
+    int32_t* __restrict__ big, ProbeFlags* fl) {
     if (fl->skip) return;
     const int64_t i = (int64_t)blockIdx.x * kTBlock + threadIdx.x;
     if (i >= n) return;
     const int64_t o = offset[i], s = size[i];
+    const uint64_t t0 = ((uint64_t)o >> 2) >> kTileShift;
+    const uint64_t t1 = (((uint64_t)(o + s) >> 2) - 1) >> kTileShift;
+    if (t1 - t0 >= (uint64_t)kSmallSpan) {
+        big[atomicAdd(&fl->n_big, 1u)] = (int32_t)i;
+        return;
+    }
     const uint64_t kb = 2ull * (uint32_t)first[i], kd = 2ull * (uint32_t)last[i] + 1;
-    const uint64_t t0 = ((uint64_t)o >> 2) >> kTileShift, t1 = (((uint64_t)(o + s) >> 2) - 1) >> kTileShift;
     int64_t e = base[i];
-    for (uint64_t t = t0; t <= t1; ++t, e += 2) {
-        keys[e] = (t << op_bits) | kb;
-        vals[e] = (uint32_t)i;
-        keys[e + 1] = (t << op_bits) | kd;
-        vals[e + 1] = (uint32_t)i;
+    for (uint64_t t = t0; t <= t1; ++t, e += 2) emit_pair(keys, vals, e, t, op_bits, kb, kd, (uint32_t)i);
+}
+
+// One workgroup per listed tensor (grid-stride over the list).
+__global__ __launch_bounds__(kTBlock) void probe_emit_big_kernel(
+    const int64_t* __restrict__ size, const int32_t* __restrict__ first,
+    const int32_t* __restrict__ last, const int64_t* __restrict__ offset, int op_bits,
+    const int64_t* __restrict__ base, uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+    const int32_t* __restrict__ big, const ProbeFlags* fl) {
+    if (fl->skip) return;
+    const uint32_t n_big = fl->n_big;
+    for (uint32_t b = blockIdx.x; b < n_big; b += gridDim.x) {
+        const int32_t i = big[b];
+        const int64_t o = offset[i], s = size[i];
+        const uint64_t t0 = ((uint64_t)o >> 2) >> kTileShift;
+        const uint64_t t1 = (((uint64_t)(o + s) >> 2) - 1) >> kTileShift;
+        const uint64_t kb = 2ull * (uint32_t)first[i], kd = 2ull * (uint32_t)last[i] + 1;
+        const int64_t e0 = base[i];
+        for (uint64_t t = t0 + threadIdx.x; t <= t1; t += kTBlock)
+            emit_pair(keys, vals, e0 + 2 * (int64_t)(t - t0), t, op_bits, kb, kd, (uint32_t)i);
     }
 }
 
@@ -344,83 +381,120 @@ __device__ int64_t wave_find(const uint64_t* __restrict__ keys, int64_t total, i
     return lo;
 }
 
+// Packs each sorted event for the replay, relative to the event's tile:
+// info = first covered lane | count << 8 in the low half for a birth, in the
+// high half for a death (the other half 0), and the tensor id with bit 31 set
+// when the event starts a group -- a run of equal keys, the births or the
+// deaths of one op in one tile.
+__global__ __launch_bounds__(kTBlock) void probe_pack_kernel(
+    const int64_t* __restrict__ size, const int64_t* __restrict__ offset,
+    const uint64_t* __restrict__ keys, const uint32_t* __restrict__ vals,
+    const int64_t* __restrict__ total_p, int op_bits, uint2* __restrict__ packed,
+    const ProbeFlags* fl) {
+    if (fl->skip) return;
+    const int64_t total = *total_p;
+    for (int64_t k = (int64_t)blockIdx.x * kTBlock + threadIdx.x; k < total;
+         k += (int64_t)gridDim.x * kTBlock) {
+        const uint64_t key = keys[k];
+        const uint32_t id = vals[k];
+        const bool start = k == 0 || keys[k - 1] != key;
+        const int64_t tbase = (int64_t)(key >> op_bits) << kTileShift, o = offset[id];
+        const int64_t lo = max((o >> 2) - tbase, (int64_t)0);
+        const int64_t hi = min(((o + size[id]) >> 2) - tbase, (int64_t)kWave);
+        const uint32_t range = (uint32_t)lo | ((uint32_t)(hi - lo) << 8);
+        packed[k] = make_uint2((key & 1u) ? range << 16 : range, id | (start ? 1u << 31 : 0u));
+    }
+}
+
 __device__ __forceinline__ uint32_t lane_word_load(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
 __device__ __forceinline__ void lane_word_store(uint32_t* p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
-__device__ __forceinline__ int64_t readlane64(int64_t v, int j) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, j);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), j);
+
+// A value the whole wave holds, moved to scalar registers.
+__device__ __forceinline__ int64_t uniform64(int64_t x) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)((uint64_t)x >> 32));
     return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// kUnroll packed events read through the scalar cache (the index is the same
+// for the whole wave), so they land in scalar registers.
+struct EventGroup {
+    uint32_t w[2 * kUnroll];
+};
+typedef const __attribute__((address_space(4))) uint32_t* ConstWords;
+__device__ __forceinline__ EventGroup group_at(const uint2* packed, int64_t k) {
+    const ConstWords p = (ConstWords)(packed + k);
+    EventGroup g;
+#pragma unroll
+    for (int i = 0; i < 2 * kUnroll; ++i) g.w[i] = p[i];
+    return g;
 }
 
 // One wave per tile, word tile * 64 + lane per lane.  The slab accesses are
 // relaxed atomics at wavefront scope only so that every change really goes
 // to memory and every check really reads it back; no other lane ever touches
-// the word.
+// the word.  Each event is: clear the word if the event starts a group and
+// the previous group held deaths covering it; store the word (which also
+// lands the previous event's write); read it back; then a birth covering the
+// word takes the maximum, a death covering it keeps the read for its check.
+// Groups of kUnroll events are read one group ahead (the event buffer has
+// kPad entries past its end, so a read never needs a bound) and their checks
+// compared together, so no step waits on the one before.
 __global__ __launch_bounds__(kTBlock) void probe_tiles_kernel(
-    const int64_t* __restrict__ size, const int64_t* __restrict__ offset,
-    const uint64_t* __restrict__ keys, const uint32_t* __restrict__ vals,
+    const uint64_t* __restrict__ keys, const uint2* __restrict__ packed,
     const int64_t* __restrict__ total_p, int op_bits, uint32_t* slab,
-    uint8_t* __restrict__ clob, const ProbeFlags* fl) {
+    uint8_t* __restrict__ clob, ProbeFlags* fl) {
     if (fl->skip) return;
-    const int lane = threadIdx.x & (kWave - 1);
+    const uint32_t lane = threadIdx.x & (kWave - 1);
     const int64_t n_tiles = fl->n_tiles, total = *total_p;
     const uint64_t top = fl->top;
-    const uint32_t kind_key_mask = op_bits >= 32 ? ~0u : ((1u << op_bits) - 1u);
     for (int64_t tile = (int64_t)blockIdx.x * kTWaves + threadIdx.x / kWave; tile < n_tiles;
          tile += (int64_t)gridDim.x * kTWaves) {
         const int64_t w = (tile << kTileShift) + lane;
         const bool mine = (uint64_t)w < top;
-        uint32_t* word = slab + (mine ? w : 0);
-        if (mine) lane_word_store(word, 0u);
-        uint32_t v = 0;           // the word's value
-        bool clr = false;         // covered by a death of the pending group
-        uint32_t pend = ~0u;      // key of the pending group of deaths, ~0 for none
-        const int64_t e0 = wave_find(keys, total, op_bits, (uint64_t)tile, false, lane);
-        const int64_t e1 = wave_find(keys, total, op_bits, (uint64_t)tile, true, lane);
-        for (int64_t b = e0; b < e1; b += kWave) {
-            const int64_t k = b + lane;
-            uint32_t key = 0, id = 0;
-            int64_t lo = 0, hi = 0;
-            if (k < e1) {
-                key = (uint32_t)keys[k] & kind_key_mask;
-                id = vals[k];
-                const int64_t o = offset[id];
-                lo = o >> 2;
-                hi = (o + size[id]) >> 2;
+        uint32_t* word = mine ? slab + w : &fl->sink;
+        uint32_t v = 0;    // the word's value
+        bool clr = false;  // covered by a death of the current group
+        const int64_t e0 = uniform64(wave_find(keys, total, op_bits, (uint64_t)tile, false, lane));
+        const int64_t e1 = uniform64(wave_find(keys, total, op_bits, (uint64_t)tile, true, lane));
+        EventGroup cur = group_at(packed, e0);
+        for (int64_t g = e0; g < e1; g += kUnroll) {
+            const EventGroup nxt = group_at(packed, g + kUnroll);
+            const int rem = (int)min(e1 - g, (int64_t)kUnroll);  // events past e1 cover no lane
+            uint32_t got[kUnroll];
+            uint32_t chk = 0;  // bit u: event g + u is a death covering this word
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const uint32_t f = u < rem ? cur.w[2 * u] : 0u, idw = cur.w[2 * u + 1];
+                const bool start = idw >> 31;
+                const bool covb = lane - (f & 0xFFu) < ((f >> 8) & 0xFFu);
+                const bool covd = lane - ((f >> 16) & 0xFFu) < (f >> 24);
+                v = (start && clr) ? 0u : v;
+                clr = clr && !start;
+                lane_word_store(word, v);
+                got[u] = lane_word_load(word);
+                v = covb ? max(v, (idw & 0x7FFFFFFFu) + 1u) : v;
+                chk |= covd ? 1u << u : 0u;
+                clr = clr || covd;
             }
-            const int m = (int)min((int64_t)kWave, e1 - b);
-            for (int j = 0; j < m; ++j) {
-                const uint32_t kj = (uint32_t)__builtin_amdgcn_readlane((int)key, j);
-                const uint32_t idj = (uint32_t)__builtin_amdgcn_readlane((int)id, j);
-                const int64_t loj = readlane64(lo, j), hij = readlane64(hi, j);
-                if (pend != ~0u && kj != pend) {  // the group of deaths is over: clear
-                    if (clr) {
-                        v = 0;
-                        lane_word_store(word, 0u);
-                    }
-                    clr = false;
-                    pend = ~0u;
-                }
-                const bool cov = w >= loj && w < hij;
-                if (!(kj & 1u)) {  // birth
-                    if (cov) {
-                        v = max(v, idj + 1u);
-                        lane_word_store(word, v);
-                    }
-                } else {  // death: check now, clear after the group
-                    pend = kj;
-                    if (cov) {
-                        if (lane_word_load(word) != idj + 1u) clob[idj] = 1;
-                        clr = true;
-                    }
-                }
+            uint32_t bad = 0;
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                bad |= (((chk >> u) & 1u) && got[u] != (cur.w[2 * u + 1] & 0x7FFFFFFFu) + 1u)
+                           ? 1u << u
+                           : 0u;
+            if (__ballot(bad != 0)) {
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u)
+                    if ((bad >> u) & 1u) clob[cur.w[2 * u + 1] & 0x7FFFFFFFu] = 1;
             }
+            cur = nxt;
         }
-        if (clr) lane_word_store(word, 0u);
+        lane_word_store(word, clr ? 0u : v);
     }
 }
 
@@ -441,12 +515,13 @@ __global__ __launch_bounds__(kTBlock) void probe_count_kernel(const uint8_t* __r
 // padding between them, so every extra pair of capacity costs bytes and a
 // workspace of probe_workspace_bytes(n, ops, c) holds capacity c exactly.
 struct ProbeLayout {
-    size_t flags, cnt, partial, keys0, keys1, radix, bstart, dstart, born, dies, vals0, vals1, end;
+    size_t flags, cnt, partial, keys0, keys1, radix, bstart, dstart, born, dies, big, vals0, vals1,
+        end;
 };
 
 ProbeLayout probe_layout(int64_t n, int32_t num_ops, int64_t capacity) {
     const size_t nn = (size_t)(n > 0 ? n : 1), ops = (size_t)num_ops + 1;
-    const size_t ev = (size_t)(capacity > 0 ? 2 * capacity : 1);
+    const size_t ev = (size_t)(capacity > 0 ? 2 * capacity : 1) + kPad;
     ProbeLayout L;
     size_t at = 0;
     auto take = [&](size_t bytes) {
@@ -464,6 +539,7 @@ ProbeLayout probe_layout(int64_t n, int32_t num_ops, int64_t capacity) {
     L.dstart = take(ops * 4);
     L.born = take(nn * 4);
     L.dies = take(nn * 4);
+    L.big = take(nn * 4);
     L.vals0 = take(ev * 4);
     L.vals1 = take(ev * 4);
     L.end = at;
@@ -531,17 +607,28 @@ hipError_t launch_probe(const int64_t* size, const int32_t* first, const int32_t
         uint64_t* k1 = reinterpret_cast<uint64_t*>(w + L.keys1);
         uint32_t* v0 = reinterpret_cast<uint32_t*>(w + L.vals0);
         uint32_t* v1 = reinterpret_cast<uint32_t*>(w + L.vals1);
+        int32_t* big = reinterpret_cast<int32_t*>(w + L.big);
         hipLaunchKernelGGL(probe_emit_kernel, dim3(nb), dim3(kTBlock), 0, st, size, first, last,
-                           offset, n, op_bits, (const int64_t*)cnt, k0, v0, (const ProbeFlags*)fl);
+                           offset, n, op_bits, (const int64_t*)cnt, k0, v0, big, fl);
+        hipLaunchKernelGGL(probe_emit_big_kernel, dim3((unsigned)min((int64_t)nb, (int64_t)1024)),
+                           dim3(kTBlock), 0, st, size, first, last, offset, op_bits,
+                           (const int64_t*)cnt, k0, v0, (const int32_t*)big,
+                           (const ProbeFlags*)fl);
         bool alt = false;
         e = radix_sort_pairs(k0, v0, k1, v1, 2 * capacity, 0, op_bits + tile_bits, w + L.radix,
                              &alt, st, &fl->skip, total);
         if (e != hipSuccess) return e;
+        const uint64_t* ks = alt ? k1 : k0;
+        const uint32_t* vs = alt ? v1 : v0;
+        uint2* packed = reinterpret_cast<uint2*>(alt ? k0 : k1);  // the other key buffer
+        hipLaunchKernelGGL(probe_pack_kernel, dim3((unsigned)min((2 * capacity + kTBlock - 1) / kTBlock,
+                                                                 (int64_t)4096)),
+                           dim3(kTBlock), 0, st, size, offset, ks, vs, total, op_bits, packed,
+                           (const ProbeFlags*)fl);
         const int64_t blocks = min((max_tiles + kTWaves - 1) / kTWaves, (int64_t)1 << 16);
-        hipLaunchKernelGGL(probe_tiles_kernel, dim3((unsigned)blocks), dim3(kTBlock), 0, st, size,
-                           offset, (const uint64_t*)(alt ? k1 : k0),
-                           (const uint32_t*)(alt ? v1 : v0), total, op_bits,
-                           static_cast<uint32_t*>(slab), clob, (const ProbeFlags*)fl);
+        hipLaunchKernelGGL(probe_tiles_kernel, dim3((unsigned)blocks), dim3(kTBlock), 0, st, ks,
+                           (const uint2*)packed, total, op_bits, static_cast<uint32_t*>(slab), clob,
+                           fl);
         hipLaunchKernelGGL(probe_count_kernel, dim3((unsigned)min((int64_t)nb, (int64_t)1024)),
                            dim3(kTBlock), 0, st, (const uint8_t*)clob, n, n_clob,
                            (const ProbeFlags*)fl);
