@@ -124,7 +124,8 @@ def single_trace_leg(binding, tg, np, torch, reps: int = 3):
             "peak_over_lb": int(peak.item()) / int(max_live.item()),
             "probe": {"ms": pmed, "clobbered": 0, "algorithmic_bytes": probe_bytes,
                       "gb_per_s": probe_bytes / (pmed * 1e-3) / 1e9,
-                      "kernel": "probe_kernel (one workgroup replays the ops)"}}
+                      "kernel": "probe_tiles_kernel (one wave per 256-byte slab tile replays "
+                                "its events in op order, after a radix sort of (tile, op) keys)"}}
 
 
 def cpu_baseline(batch, min_seconds: float = 10.0):
