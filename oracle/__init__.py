@@ -61,6 +61,8 @@ def lib():
         L.mpo_live_bytes_profile.argtypes = [p, p, p, i64, i32, p, p]
         L.mpo_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p]
         L.mpo_probe_plan.argtypes = [p, p, p, p, i64, i32, p, p]
+        L.mpo_bump_plan.argtypes = [p, p, p, i64, i32, p, p]
+        L.mpo_optimal_plan.argtypes = [p, p, p, i64, i32, p, p]
         for f in (L.mpo_check_trace, L.mpo_rank_order, L.mpo_plan_trace, L.mpo_plan_trace_w,
                   L.mpo_live_bytes_profile, L.mpo_validate_plan, L.mpo_probe_plan):
             f.restype = i32
@@ -166,3 +168,27 @@ def probe_plan(size, first, last, offset, num_ops: int):
     if st != OK:
         raise OracleError(st, "probe_plan")
     return out.astype(bool), int(cnt.value)
+
+
+OPT_MAX_N = 12
+
+
+def _offsets_call(fn, what, size, first, last, num_ops):
+    s, f, l = _arr(size, np.int64), _arr(first, np.int32), _arr(last, np.int32)
+    off = np.zeros(s.shape[0], np.int64)
+    peak = ctypes.c_int64(0)
+    st = fn(_ptr(s), _ptr(f), _ptr(l), s.shape[0], int(num_ops), _ptr(off), ctypes.byref(peak))
+    if st != OK:
+        raise OracleError(st, what)
+    return off, int(peak.value)
+
+
+def bump_plan(size, first, last, num_ops: int):
+    """bump_allocation (Section 2.3): (offsets, peak = sum of sizes)."""
+    return _offsets_call(lib().mpo_bump_plan, "bump_plan", size, first, last, num_ops)
+
+
+def optimal_plan(size, first, last, num_ops: int):
+    """The optimum of Eq. 2.1 by exhaustive search over placement orders
+    (n <= OPT_MAX_N): (offsets of one optimal plan, optimal peak)."""
+    return _offsets_call(lib().mpo_optimal_plan, "optimal_plan", size, first, last, num_ops)

@@ -365,3 +365,109 @@ int32_t mpo_probe_plan(const int64_t* size, const int32_t* first, const int32_t*
     *n_clobbered_out = count;
     return MPO_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* bump_allocation: every allocation at the running offset, in the order the
+ * allocations happen (first op, then id). */
+
+int32_t mpo_bump_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                      int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out) {
+    if (!peak_out || (n > 0 && !offset_out)) return MPO_EINVAL;
+    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
+    if (st != MPO_OK) return st;
+    /* the order of allocation: a counting sort by first op, ids ascending */
+    int64_t* at = (int64_t*)calloc((size_t)num_ops + 1, sizeof(int64_t));
+    int64_t* order = (int64_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int64_t));
+    if (!at || !order) {
+        free(at); free(order);
+        return MPO_EINVAL;
+    }
+    for (int64_t i = 0; i < n; ++i) at[first[i] + 1] += 1;
+    for (int32_t t = 0; t < num_ops; ++t) at[t + 1] += at[t];
+    for (int64_t i = 0; i < n; ++i) order[at[first[i]]++] = i;
+    int64_t running = 0;
+    for (int64_t k = 0; k < n; ++k) {
+        offset_out[order[k]] = running;
+        running += size[order[k]];
+    }
+    *peak_out = running;
+    free(at); free(order);
+    return MPO_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* The optimum of Eq. 2.1 by exhaustive search over placement orders.  Why the
+ * least peak over all orders is the optimum: list the tensors of an optimal
+ * plan by offset and place them in that order at the lowest fitting offset;
+ * by induction each lands at or below its optimal offset (the ones placed
+ * before it sit at or below theirs, which end at or below its own optimal
+ * offset whenever their lifetimes meet), so that order reaches the optimum. */
+
+typedef struct {
+    const int64_t* size;
+    const int32_t* first;
+    const int32_t* last;
+    int n;
+    int64_t off[MPO_OPT_MAX_N];
+    int placed[MPO_OPT_MAX_N];  /* placed[i]: tensor i has an offset */
+    int64_t best;
+    int64_t best_off[MPO_OPT_MAX_N];
+} OptSearch;
+
+static int lifetimes_meet(const OptSearch* S, int i, int j) {
+    return S->first[i] <= S->last[j] && S->first[j] <= S->last[i];
+}
+
+/* Lowest offset for tensor c among the placed tensors: 0 or the end of a
+ * placed tensor whose lifetime meets c's, the least such value where c
+ * overlaps none of them. */
+static int64_t opt_lowest_fit(const OptSearch* S, int c) {
+    int64_t best = -1;
+    for (int a = -1; a < S->n; ++a) {
+        if (a >= 0 && !(S->placed[a] && lifetimes_meet(S, a, c))) continue;
+        const int64_t x = a < 0 ? 0 : S->off[a] + S->size[a];
+        int free_here = 1;
+        for (int j = 0; j < S->n && free_here; ++j)
+            if (S->placed[j] && lifetimes_meet(S, j, c) && x < S->off[j] + S->size[j] &&
+                S->off[j] < x + S->size[c])
+                free_here = 0;
+        if (free_here && (best < 0 || x < best)) best = x;
+    }
+    return best;
+}
+
+static void opt_search(OptSearch* S, int depth, int64_t peak) {
+    if (depth == S->n) {
+        if (peak < S->best) {
+            S->best = peak;
+            memcpy(S->best_off, S->off, sizeof(S->off));
+        }
+        return;
+    }
+    for (int c = 0; c < S->n; ++c) {
+        if (S->placed[c]) continue;
+        const int64_t x = opt_lowest_fit(S, c);
+        S->off[c] = x;
+        S->placed[c] = 1;
+        opt_search(S, depth + 1, peak > x + S->size[c] ? peak : x + S->size[c]);
+        S->placed[c] = 0;
+    }
+}
+
+int32_t mpo_optimal_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out) {
+    if (!peak_out || (n > 0 && !offset_out) || n > MPO_OPT_MAX_N) return MPO_EINVAL;
+    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
+    if (st != MPO_OK) return st;
+    OptSearch S;
+    memset(&S, 0, sizeof(S));
+    S.size = size;
+    S.first = first;
+    S.last = last;
+    S.n = (int)n;
+    S.best = INT64_MAX;
+    opt_search(&S, 0, 0);
+    for (int i = 0; i < S.n; ++i) offset_out[i] = S.best_off[i];
+    *peak_out = n > 0 ? S.best : 0;
+    return MPO_OK;
+}

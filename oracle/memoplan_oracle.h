@@ -81,6 +81,22 @@ int32_t mpo_probe_plan(const int64_t* size, const int32_t* first, const int32_t*
                        const int64_t* offset, int64_t n, int32_t num_ops,
                        uint8_t* clobbered_out, int64_t* n_clobbered_out);
 
+/* bump_allocation (Section 2.3, the baseline strategy): allocations are taken
+ * in the order they happen -- by first op, ties by id -- and each goes at a
+ * running offset that then grows by its size; no memory is reused.
+ * *peak_out = the sum of the sizes. */
+int32_t mpo_bump_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                      int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out);
+
+/* The optimum of Eq. 2.1 for tiny traces (n <= MPO_OPT_MAX_N, else -1): the
+ * least peak over all n! placement orders, each tensor placed at the lowest
+ * offset where it overlaps no earlier-placed tensor whose lifetime meets its
+ * own.  offset_out gets the plan of the first optimal order in lexicographic
+ * order of the ids. */
+#define MPO_OPT_MAX_N 12
+int32_t mpo_optimal_plan(const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -368,3 +368,95 @@ def test_probe_invalid_and_empty():
         kw = dict(size=[64], first=[0], last=[1], off=[0]) | bad
         with pytest.raises(oracle.OracleError):
             oracle.probe_plan(kw["size"], kw["first"], kw["last"], kw["off"], 2)
+
+
+# ---------------------------------------------------------------------------
+# bump_allocation and the exact optimum (the strategies Section 2.3 compares
+# greedy_by_size with)
+
+def _random_tiny(rng, n, T=6, span=4, unit=64, kinds=8):
+    size = unit * rng.integers(1, kinds, n)
+    first = rng.integers(0, T, n)
+    last = first + rng.integers(0, span, n)
+    return size, first, last, int(last.max()) + 1
+
+
+def test_bump_plan_hand_case_and_properties():
+    # allocation order (first, id): id 0 and id 2 at op 0, then id 1
+    off, peak = oracle.bump_plan([64, 32, 16], [0, 1, 0], [1, 2, 0], 3)
+    assert off.tolist() == [0, 80, 64] and peak == 112
+    rng = np.random.default_rng(90)
+    for _ in range(30):
+        n = int(rng.integers(1, 200))
+        size, first, last, T = _random_tiny(rng, n, T=50, span=10)
+        off, peak = oracle.bump_plan(size, first, last, T)
+        assert peak == int(size.sum())
+        # nothing is reused: the ranges tile [0, peak) without overlap ...
+        by_off = np.argsort(off, kind="stable")
+        ends = off[by_off] + size[by_off]
+        assert off[by_off][0] == 0 and np.array_equal(off[by_off][1:], ends[:-1])
+        # ... so the plan is valid for any lifetimes, and the offsets rise with
+        # the order of allocation
+        assert oracle.validate_plan(size, first, last, off)[1] == 0
+        alloc = sorted(range(n), key=lambda i: (first[i], i))
+        assert all(off[a] < off[b] for a, b in zip(alloc, alloc[1:]))
+
+
+def test_optimal_plan_golden_and_brute_force(hand_examples):
+    for ex in hand_examples:
+        T = max(ex["last"]) + 1
+        off, peak = oracle.optimal_plan(ex["size"], ex["first"], ex["last"], T)
+        assert peak == ex["opt"], ex["name"]
+        size = np.asarray(ex["size"])
+        assert int((off + size).max()) == peak
+        assert oracle.validate_plan(size, ex["first"], ex["last"], off)[1] == 0
+    rng = np.random.default_rng(91)
+    for _ in range(25):
+        n = int(rng.integers(1, 7))
+        size, first, last, T = _random_tiny(rng, n)
+        off, peak = oracle.optimal_plan(size, first, last, T)
+        assert peak == brute_force_opt(size, first, last, stack=False)
+        assert peak == brute_force_opt(size, first, last, stack=True)
+        assert oracle.validate_plan(size, first, last, off)[1] == 0
+        assert int((off + size).max()) == peak
+
+
+def test_optimal_plan_closed_forms():
+    rng = np.random.default_rng(92)
+    for _ in range(10):
+        n = int(rng.integers(1, 8))
+        size = 16 * rng.integers(1, 20, n)
+        # every pair of lifetimes meets: nothing can share bytes
+        assert oracle.optimal_plan(size, np.zeros(n), np.full(n, 3), 4)[1] == int(size.sum())
+        # no pair meets: everything can start at 0
+        ops = np.arange(n)
+        assert oracle.optimal_plan(size, ops, ops, n)[1] == int(size.max())
+        # equal sizes: an interval graph is perfect, so the optimum is the
+        # size times the most tensors alive at one op
+        first = rng.integers(0, 6, n)
+        last = first + rng.integers(0, 4, n)
+        T = int(last.max()) + 1
+        omega = max(int(((first <= t) & (t <= last)).sum()) for t in range(T))
+        assert oracle.optimal_plan(np.full(n, 48), first, last, T)[1] == 48 * omega
+
+
+def test_strategy_order_of_peaks():
+    """live-bytes lower bound <= optimum <= greedy (either fit) <= bump."""
+    rng = np.random.default_rng(93)
+    for _ in range(40):
+        n = int(rng.integers(1, 9))
+        size, first, last, T = _random_tiny(rng, n)
+        opt = oracle.optimal_plan(size, first, last, T)[1]
+        lb = oracle.live_bytes_profile(size, first, last, T)[1]
+        bump = oracle.bump_plan(size, first, last, T)[1]
+        g_low = oracle.plan_trace(size, first, last, T, oracle.LOWEST_FIT)[1]
+        g_best = oracle.plan_trace(size, first, last, T, oracle.BEST_FIT)[1]
+        assert lb <= opt <= min(g_low, g_best) and max(g_low, g_best) <= bump
+
+
+def test_optimal_plan_limits():
+    with pytest.raises(oracle.OracleError):
+        oracle.optimal_plan(np.full(13, 64), np.zeros(13), np.zeros(13), 1)
+    assert oracle.optimal_plan(np.zeros(0), np.zeros(0), np.zeros(0), 0)[1] == 0
+    with pytest.raises(oracle.OracleError):
+        oracle.bump_plan([64], [1], [0], 2)
