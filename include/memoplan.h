@@ -129,6 +129,7 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
 #define MP_OP_VALIDATE_BATCH 4
 #define MP_OP_PLAN_BATCH 5
 #define MP_OP_PROBE 6
+#define MP_OP_BUMP 7
 size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops, int64_t capacity);
 
 /* Per-op live bytes of one trace (the quantity whose maximum lower-bounds
@@ -215,6 +216,47 @@ int32_t mp_probe_plan(const int64_t* size, const int32_t* first, const int32_t* 
                       const int64_t* offset, int64_t n, int32_t num_ops, void* slab,
                       size_t slab_bytes, uint8_t* clobbered_out, int64_t* n_clobbered_out,
                       void* workspace, size_t workspace_bytes, int32_t* status_out, void* stream);
+
+/* bump_allocation, the baseline strategy of Section 2.3: allocations are
+ * taken in the order they happen -- by first op, ties by id -- and each goes
+ * at a running offset that then grows by its size; nothing is reused, so the
+ * peak is the sum of the sizes.
+ *   begin[n_traces + 1] int64: trace bounds (0 = begin[0] <= ... <=
+ *              begin[n_traces] = n), or NULL for one trace of n tensors.
+ *   size, first, last [n]: as for mp_plan_trace; every last < num_ops (for a
+ *              batch, num_ops bounds every trace's op count).
+ *   offset_out[n] int64, peak_out[n_traces] int64 (one value when begin is
+ *              NULL): the offsets and each trace's sum of sizes.
+ *   workspace: mp_workspace_size(MP_OP_BUMP, n, 0, 0) bytes, contents need no
+ *              initialisation.
+ * Data errors (on the status word): MP_EINVAL for a size <= 0, a lifetime
+ * outside [0, num_ops) or inverted, or bad trace bounds; MP_EOVERFLOW when
+ * the sizes of all traces together exceed INT64_MAX. */
+int32_t mp_bump_plan(const int64_t* begin, int64_t n_traces, const int64_t* size,
+                     const int32_t* first, const int32_t* last, int64_t n, int32_t num_ops,
+                     int64_t* offset_out, int64_t* peak_out, void* workspace,
+                     size_t workspace_bytes, int32_t* status_out, void* stream);
+
+/* The optimum of Eq. 2.1 (the least total_mem under its pairwise
+ * constraints; the thesis's mip strategy) for tiny traces, by exhaustive
+ * search: the least peak over all placement orders with each tensor at the
+ * lowest offset that overlaps no placed tensor whose lifetime meets its own
+ * (an optimal plan listed by offset is such an order).  One workgroup per
+ * trace; subtrees whose partial peak reaches the best found are cut, and a
+ * trace stops once the best equals its live-bytes lower bound.
+ *   begin[n_traces + 1] int64, num_ops[n_traces] int32, size/first/last
+ *              [n_tensors]: as for mp_plan_batch; each trace at most
+ *              MP_OPT_MAX_N tensors.
+ *   offset_out[n_tensors]: one optimal plan (optimal plans are not unique);
+ *   peak_out[n_traces]: the optimum.
+ * Data errors (MP_EINVAL on the status word): a trace over MP_OPT_MAX_N
+ * tensors or with bad bounds, an invalid tensor; MP_EOVERFLOW when a trace's
+ * sizes exceed INT64_MAX.  Time grows like n! in the worst case. */
+#define MP_OPT_MAX_N 12
+int32_t mp_optimal_batch(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                         const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n_tensors, int64_t* offset_out, int64_t* peak_out,
+                         int32_t* status_out, void* stream);
 
 #ifdef __cplusplus
 }

@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
 OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH, OP_PLAN_BATCH = 1, 2, 3, 4, 5
 OP_PROBE = 6
+OP_BUMP = 7
+OPT_MAX_N = 12
 HINT_SORTED_FIRST = 1
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
@@ -59,6 +61,10 @@ def load_library(path: str = LIB_PATH):
     L.mp_plan_trace.restype = i32
     L.mp_probe_plan.argtypes = [p, p, p, p, i64, i32, p, sz, p, p, p, sz, p, p]
     L.mp_probe_plan.restype = i32
+    L.mp_bump_plan.argtypes = [p, i64, p, p, p, i64, i32, p, p, p, sz, p, p]
+    L.mp_bump_plan.restype = i32
+    L.mp_optimal_batch.argtypes = [p, i64, p, p, p, p, i64, p, p, p, p]
+    L.mp_optimal_batch.restype = i32
     _lib = L
     return L
 
@@ -316,3 +322,66 @@ def probe_plan(size, first, last, offset, num_ops: int, slab: torch.Tensor, *,
                          ws.numel() * ws.element_size(), _p(status), _stream(stream))
     _finish(rc, status, "probe_plan", check)
     return clob, cnt
+
+
+def bump_plan(size, first, last, num_ops: int, *, begin=None, check: bool = True, out=None,
+              status=None, workspace=None, stream=None):
+    """bump_allocation (mp_bump_plan): offsets at the running sum of sizes in
+    allocation order (first op, then id).  One trace, or many with `begin`
+    (num_ops then bounds every trace's op count).  Returns (offset int64[n],
+    peak int64[traces])."""
+    L = load_library()
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    n = size.numel()
+    if first.numel() != n or last.numel() != n:
+        raise ValueError("inconsistent array lengths")
+    dev = size.device
+    n_traces = 1
+    if begin is not None:
+        begin = _dev(begin, torch.int64, "begin")
+        n_traces = begin.numel() - 1
+        if n_traces < 0:
+            raise ValueError("begin needs at least one entry")
+    if out is None:
+        offset = torch.empty(max(n, 1), dtype=torch.int64, device=dev)[:n]
+        peak = torch.empty(max(n_traces, 1), dtype=torch.int64, device=dev)[:n_traces]
+    else:
+        offset, peak = out
+    if status is None:
+        status = new_status(dev, stream)
+    ws, need = _workspace(OP_BUMP, dev, n, 0, 0, workspace)
+    rc = L.mp_bump_plan(_p(begin) if begin is not None else None, n_traces, _p(size), _p(first),
+                        _p(last), n, int(num_ops), _p(offset), _p(peak), _p(ws), need,
+                        _p(status), _stream(stream))
+    _finish(rc, status, "bump_plan", check)
+    return offset, peak
+
+
+def optimal_batch(begin, num_ops, size, first, last, *, check: bool = True, out=None,
+                  status=None, stream=None):
+    """The optimum of Eq. 2.1 for tiny traces (at most OPT_MAX_N tensors each)
+    by exhaustive search (mp_optimal_batch).  Returns (offset int64[N] of one
+    optimal plan per trace, peak int64[B] = the optimum)."""
+    L = load_library()
+    begin = _dev(begin, torch.int64, "begin")
+    num_ops = _dev(num_ops, torch.int32, "num_ops")
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    n_traces, n = num_ops.numel(), size.numel()
+    if begin.numel() != n_traces + 1 or first.numel() != n or last.numel() != n:
+        raise ValueError("inconsistent array lengths")
+    dev = size.device
+    if out is None:
+        offset = torch.empty(max(n, 1), dtype=torch.int64, device=dev)[:n]
+        peak = torch.empty(max(n_traces, 1), dtype=torch.int64, device=dev)[:n_traces]
+    else:
+        offset, peak = out
+    if status is None:
+        status = new_status(dev, stream)
+    rc = L.mp_optimal_batch(_p(begin), n_traces, _p(num_ops), _p(size), _p(first), _p(last), n,
+                            _p(offset), _p(peak), _p(status), _stream(stream))
+    _finish(rc, status, "optimal_batch", check)
+    return offset, peak

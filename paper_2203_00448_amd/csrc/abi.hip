@@ -65,6 +65,8 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
             return num_ops > INT32_MAX ? 0 : validate_workspace_bytes(n_tensors, capacity, num_ops);
         case MP_OP_PLAN_TRACE:
             return n_tensors >= (int64_t)1 << 30 ? 0 : plan_trace_workspace_bytes(n_tensors);
+        case MP_OP_BUMP:
+            return bump_workspace_bytes(n_tensors);
         case MP_OP_PROBE:
             return num_ops > INT32_MAX ? 0
                                        : probe_workspace_bytes(n_tensors, (int32_t)num_ops,
@@ -159,4 +161,32 @@ extern "C" int32_t mp_probe_plan(const int64_t* size, const int32_t* first, cons
     return launched(launch_probe(size, first, last, offset, n, num_ops, slab, slab ? slab_bytes : 0,
                                  clobbered_out, n_clobbered_out, workspace, workspace_bytes,
                                  status_out, static_cast<hipStream_t>(stream)));
+}
+
+extern "C" int32_t mp_bump_plan(const int64_t* begin, int64_t n_traces, const int64_t* size,
+                                const int32_t* first, const int32_t* last, int64_t n,
+                                int32_t num_ops, int64_t* offset_out, int64_t* peak_out,
+                                void* workspace, size_t workspace_bytes, int32_t* status_out,
+                                void* stream) {
+    if (n < 0 || n >= INT32_MAX || num_ops < 0 || !status_out || !peak_out || !workspace)
+        return MP_EINVAL;
+    if (begin && (n_traces < 0 || n_traces >= INT32_MAX)) return MP_EINVAL;
+    if (n > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
+    if (workspace_bytes < bump_workspace_bytes(n)) return MP_EINVAL;
+    return launched(launch_bump(begin, begin ? n_traces : 1, size, first, last, n, num_ops,
+                                offset_out, peak_out, workspace, status_out,
+                                static_cast<hipStream_t>(stream)));
+}
+
+extern "C" int32_t mp_optimal_batch(const int64_t* begin, int64_t n_traces,
+                                    const int32_t* num_ops, const int64_t* size,
+                                    const int32_t* first, const int32_t* last,
+                                    int64_t n_tensors, int64_t* offset_out, int64_t* peak_out,
+                                    int32_t* status_out, void* stream) {
+    if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || !status_out) return MP_EINVAL;
+    if (n_traces > 0 && (!begin || !num_ops || !peak_out)) return MP_EINVAL;
+    if (n_tensors > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
+    return launched(launch_optimal(begin, n_traces, num_ops, size, first, last, n_tensors,
+                                   offset_out, peak_out, status_out,
+                                   static_cast<hipStream_t>(stream)));
 }

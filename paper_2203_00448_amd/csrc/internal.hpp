@@ -51,6 +51,17 @@ hipError_t launch_probe(const int64_t* size, const int32_t* first, const int32_t
 
 namespace mp {
 
+// bump_allocation and the exact optimum (strategies.hip)
+size_t bump_workspace_bytes(int64_t n);
+hipError_t launch_bump(const int64_t* begin, int64_t n_seg, const int64_t* size,
+                       const int32_t* first, const int32_t* last, int64_t n, int32_t num_ops,
+                       int64_t* offset_out, int64_t* peak_out, void* ws, int32_t* status,
+                       hipStream_t st);
+hipError_t launch_optimal(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                          const int64_t* size, const int32_t* first, const int32_t* last,
+                          int64_t n_tensors, int64_t* offset_out, int64_t* peak_out,
+                          int32_t* status, hipStream_t st);
+
 // device-wide prefix sums (scan.hip)
 size_t scan_workspace_bytes(int64_t n);
 hipError_t device_scan_i64(int64_t* data, int64_t n, bool inclusive, int64_t* partial,

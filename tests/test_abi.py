@@ -114,3 +114,28 @@ def test_other_host_checks(lib):
         b.OP_VALIDATE, 0, 0, 0)
     assert lib.mp_workspace_size(b.OP_LIVE_BYTES, 0, 100, 0) > 0
     assert lib.mp_workspace_size(b.OP_VALIDATE, 1000, 0, 100) > 0
+
+
+def test_strategy_entry_points_host_checks(lib):
+    from paper_2203_00448_amd import binding as b
+    dummy = ctypes.c_void_p(16)  # never dereferenced: every call below fails a host check
+    need = lib.mp_workspace_size(b.OP_BUMP, 10, 0, 0)
+    assert need > 0
+    # negative n, missing status, short workspace
+    assert lib.mp_bump_plan(None, 1, dummy, dummy, dummy, -1, 4, dummy, dummy, dummy, need,
+                            dummy, None) == b.MP_EINVAL
+    assert lib.mp_bump_plan(None, 1, dummy, dummy, dummy, 10, 4, dummy, dummy, dummy, need,
+                            None, None) == b.MP_EINVAL
+    assert lib.mp_bump_plan(None, 1, dummy, dummy, dummy, 10, 4, dummy, dummy, dummy, need - 1,
+                            dummy, None) == b.MP_EINVAL
+    assert lib.mp_bump_plan(dummy, -3, dummy, dummy, dummy, 10, 4, dummy, dummy, dummy, need,
+                            dummy, None) == b.MP_EINVAL
+    # negative counts, missing arrays
+    assert lib.mp_optimal_batch(dummy, -1, dummy, dummy, dummy, dummy, 4, dummy, dummy, dummy,
+                                None) == b.MP_EINVAL
+    assert lib.mp_optimal_batch(None, 2, dummy, dummy, dummy, dummy, 4, dummy, dummy, dummy,
+                                None) == b.MP_EINVAL
+    assert lib.mp_optimal_batch(dummy, 2, dummy, None, dummy, dummy, 4, dummy, dummy, dummy,
+                                None) == b.MP_EINVAL
+    assert lib.mp_optimal_batch(dummy, 2, dummy, dummy, dummy, dummy, 4, dummy, dummy, None,
+                                None) == b.MP_EINVAL
