@@ -14,7 +14,10 @@ plain CPU oracle timed on the host as a baseline.  After the timed steps, a
 single-trace leg plans the seq2seq-decode-like trace (100,000 tensors, 4000
 ops, seed 3) with the whole-device planner and reports its tensors per
 second and peak / live-bytes lower bound, then applies the plan to a slab
-and probes it by replaying the ops (all outside `value`).
+and probes it by replaying the ops; a strategies leg compares, on 2048 tiny
+ResNeXt-like traces of 10 tensors, the peaks of greedy-by-size (both fits)
+and bump allocation with the exact optimum found on the GPU (all outside
+`value`).
 """
 from __future__ import annotations
 
@@ -43,6 +46,8 @@ def parse():
                     help="skip timing the CPU oracle (profiling runs)")
     ap.add_argument("--no-single-trace", action="store_true",
                     help="skip the single-trace leg (profiling runs of the batched step)")
+    ap.add_argument("--no-strategies", action="store_true",
+                    help="skip the strategy-comparison leg")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="after the timed steps, copy 256 MiB device to device three times "
                          "(a kernel of known traffic for scaling HBM counters)")
@@ -126,6 +131,41 @@ def single_trace_leg(binding, tg, np, torch, reps: int = 3):
                       "gb_per_s": probe_bytes / (pmed * 1e-3) / 1e9,
                       "kernel": "probe_tiles_kernel (one wave per 256-byte slab tile replays "
                                 "its events in op order, after a radix sort of (tile, op) keys)"}}
+
+
+def strategies_leg(binding, tg, np, torch, n_traces: int = 2048, n: int = 10, reps: int = 3):
+    """Peaks of the strategies Section 2.3 compares, on tiny traces where the
+    optimum of Eq. 2.1 is found exactly (mp_optimal_batch)."""
+    batch = tg.tiny_batch(n_traces, n)
+    d = lambda a, t: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dtype=t)
+    args = (d(batch.begin, torch.int64), d(batch.num_ops, torch.int32),
+            d(batch.size, torch.int64), d(batch.first, torch.int32), d(batch.last, torch.int32))
+    _, low, lb = binding.plan_batch(*args, max_trace_len=n)
+    _, best, _ = binding.plan_batch(*args, max_trace_len=n, policy=binding.BEST_FIT)
+    _, bump = binding.bump_plan(args[2], args[3], args[4], n, begin=args[0])
+    binding.optimal_batch(*args)  # warm-up
+    ms = []
+    for _ in range(reps):
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record()
+        off, opt = binding.optimal_batch(*args)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms.append(ev[0].elapsed_time(ev[1]))
+    low, best, bump, opt, lb = (x.cpu().numpy().astype(np.float64)
+                                for x in (low, best, bump, opt, lb))
+
+    def ratio(x):
+        r = x / opt
+        return {"mean": float(r.mean()), "max": float(r.max()),
+                "at_optimum": float((x == opt).mean())}
+    return {"workload": f"tiny_batch: {n_traces} ResNeXt-like traces x {n} tensors "
+                        "(seeds [6,b]), exact optimum by exhaustive search",
+            "optimal_ms": float(np.median(ms)), "calls": reps,
+            "greedy_lowest_over_opt": ratio(low), "greedy_best_over_opt": ratio(best),
+            "bump_over_opt": ratio(bump),
+            "opt_over_lb": {"mean": float((opt / lb).mean()), "max": float((opt / lb).max()),
+                            "at_lb": float((opt == lb).mean())}}
 
 
 def cpu_baseline(batch, min_seconds: float = 10.0):
@@ -249,6 +289,8 @@ def main():
         out["copy_calibration_bytes"] = 2 * src.numel()
     if not args.no_single_trace:
         out["single_trace"] = single_trace_leg(binding, tg, np, torch)
+    if not args.no_strategies:
+        out["strategies"] = strategies_leg(binding, tg, np, torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(batch)
     print(json.dumps(out), flush=True)

@@ -120,6 +120,27 @@ def resnext_batch(n_traces: int = 1024, n: int = 2000) -> Batch:
     return concat(resnext_trace(b, n) for b in range(n_traces))
 
 
+def tiny_trace(b: int, n: int = 10) -> Trace:
+    """A ResNeXt-like trace in miniature (seed [6, b]) for the exact optimum:
+    n tensors over n ops, tensor i born at op i; 20% skip connections living
+    U{2..max(2, n // 2)} ops, the rest U{1..2} ops; sizes as in resnext_trace
+    (log-normal, median 800 KiB, sigma 1.2, clipped to [4 KiB, 64 MiB], r64)."""
+    rng = np.random.default_rng([6, b])
+    i = np.arange(n, dtype=np.int64)
+    skip = rng.random(n) < 0.20
+    ls = rng.integers(2, max(2, n // 2) + 1, n)
+    lc = rng.integers(1, 3, n)
+    last = np.minimum(n - 1, i + np.where(skip, ls, lc))
+    z = rng.standard_normal(n)
+    size = r64(np.clip(np.exp(np.log(819200.0) + 1.2 * z), 4096, 2.0 ** 26))
+    return _pack(size, i, last, n)
+
+
+def tiny_batch(n_traces: int = 2048, n: int = 10) -> Batch:
+    """Traces b = 0..n_traces-1 of tiny_trace, concatenated."""
+    return concat(tiny_trace(b, n) for b in range(n_traces))
+
+
 def decode100k(seed: int = 3) -> Trace:
     """Seq2seq-decode-like trace: 4000 ops each producing 25 tensors
     (first = i // 25); lifetime Geo0(0.3) ops, and with probability 0.02 the

@@ -173,3 +173,14 @@ def test_optimal_status_codes():
                             np.zeros(2, np.int32), 1)])
     binding.optimal_batch(*batch_to_device(b), check=False, status=st)
     assert int(st.item()) == binding.MP_EINVAL
+
+
+def test_optimal_tiny_batch_workload():
+    binding = need_gpu()
+    print("case optimal: first 12 traces of the tiny ResNeXt-like batch (oracle ~1 s each)",
+          flush=True)
+    batch = tg.tiny_batch(12, 10)
+    traces = [batch.trace(k) for k in range(12)]
+    b, o, p = _optimal(binding, traces)
+    expected = [oracle.optimal_plan(t.size, t.first, t.last, t.num_ops)[1] for t in traces]
+    _check_optimal(b, o, p, traces, expected)
