@@ -63,6 +63,8 @@ def lib():
         L.mpo_probe_plan.argtypes = [p, p, p, p, i64, i32, p, p]
         L.mpo_bump_plan.argtypes = [p, p, p, i64, i32, p, p]
         L.mpo_optimal_plan.argtypes = [p, p, p, i64, i32, p, p]
+        L.mpo_breadth_order.argtypes = [p, p, p, i64, i32, p]
+        L.mpo_plan_breadth.argtypes = [p, p, p, i64, i32, i32, p, p]
         for f in (L.mpo_check_trace, L.mpo_rank_order, L.mpo_plan_trace, L.mpo_plan_trace_w,
                   L.mpo_live_bytes_profile, L.mpo_validate_plan, L.mpo_probe_plan):
             f.restype = i32
@@ -192,3 +194,25 @@ def optimal_plan(size, first, last, num_ops: int):
     """The optimum of Eq. 2.1 by exhaustive search over placement orders
     (n <= OPT_MAX_N): (offsets of one optimal plan, optimal peak)."""
     return _offsets_call(lib().mpo_optimal_plan, "optimal_plan", size, first, last, num_ops)
+
+
+def breadth_order(size, first, last, num_ops: int) -> np.ndarray:
+    """Greedy by Breadth placement order (Section 6, Pisarchyk et al.)."""
+    s, f, l = _arr(size, np.int64), _arr(first, np.int32), _arr(last, np.int32)
+    out = np.zeros(s.shape[0], np.int32)
+    st = lib().mpo_breadth_order(_ptr(s), _ptr(f), _ptr(l), s.shape[0], int(num_ops), _ptr(out))
+    if st != OK:
+        raise OracleError(st, "breadth_order")
+    return out
+
+
+def plan_breadth(size, first, last, num_ops: int, policy: int = LOWEST_FIT):
+    """Greedy by Breadth offsets and peak."""
+    s, f, l = _arr(size, np.int64), _arr(first, np.int32), _arr(last, np.int32)
+    off = np.zeros(s.shape[0], np.int64)
+    peak = ctypes.c_int64(0)
+    st = lib().mpo_plan_breadth(_ptr(s), _ptr(f), _ptr(l), s.shape[0], int(num_ops), int(policy),
+                                _ptr(off), ctypes.byref(peak))
+    if st != OK:
+        raise OracleError(st, "plan_breadth")
+    return off, int(peak.value)

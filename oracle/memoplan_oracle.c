@@ -156,27 +156,21 @@ static int push_id(id_list* l, int32_t id) {
     return 1;
 }
 
-int32_t mpo_plan_trace_w(const int64_t* size, const int32_t* first, const int32_t* last,
-                         int64_t n, int32_t num_ops, int32_t policy, int32_t bucket_width,
-                         int64_t* offset_out, int64_t* peak_out) {
-    if (policy != MPO_LOWEST_FIT && policy != MPO_BEST_FIT) return MPO_EINVAL;
-    if (bucket_width < 1 || !peak_out) return MPO_EINVAL;
-    if (n > 0 && !offset_out) return MPO_EINVAL;
-    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
-    if (st != MPO_OK) return st;
+/* Places the tensors in the given order: each at the lowest (LOWEST_FIT) or
+ * the tightest (BEST_FIT) free gap left by the already placed tensors whose
+ * lifetimes intersect its own.  The trace is checked by the caller. */
+static int32_t place_in_order(const int64_t* size, const int32_t* first, const int32_t* last,
+                              int64_t n, int32_t num_ops, int32_t policy, int32_t bucket_width,
+                              const int32_t* order, int64_t* offset_out, int64_t* peak_out) {
     *peak_out = 0;
     if (n == 0) return MPO_OK;
-
-    int32_t* order = (int32_t*)malloc((size_t)n * sizeof(int32_t));
     int64_t nb = ((int64_t)num_ops + bucket_width - 1) / bucket_width;
     id_list* bucket = (id_list*)calloc((size_t)nb, sizeof(id_list));
     range* conf = (range*)malloc((size_t)n * sizeof(range));
-    if (!order || !bucket || !conf) {
-        free(order); free(bucket); free(conf);
+    if (!bucket || !conf) {
+        free(bucket); free(conf);
         return MPO_EINVAL;
     }
-    mpo_rank_order(size, first, n, order);
-
     int32_t status = MPO_OK;
     int64_t peak = 0;
     for (int64_t k = 0; k < n && status == MPO_OK; ++k) {
@@ -203,20 +197,36 @@ int32_t mpo_plan_trace_w(const int64_t* size, const int32_t* first, const int32_
             if (!push_id(&bucket[b], t)) status = MPO_EINVAL;
     }
     *peak_out = peak;
-
     for (int64_t b = 0; b < nb; ++b) free(bucket[b].ids);
     free(bucket);
     free(conf);
-    free(order);
     return status;
 }
 
-int32_t mpo_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
-                       int64_t n, int32_t num_ops, int32_t policy,
-                       int64_t* offset_out, int64_t* peak_out) {
-    /* Bucket width: about one mean lifetime (only speed depends on it). */
+int32_t mpo_plan_trace_w(const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n, int32_t num_ops, int32_t policy, int32_t bucket_width,
+                         int64_t* offset_out, int64_t* peak_out) {
+    if (policy != MPO_LOWEST_FIT && policy != MPO_BEST_FIT) return MPO_EINVAL;
+    if (bucket_width < 1 || !peak_out) return MPO_EINVAL;
+    if (n > 0 && !offset_out) return MPO_EINVAL;
+    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
+    if (st != MPO_OK) return st;
+    *peak_out = 0;
+    if (n == 0) return MPO_OK;
+    int32_t* order = (int32_t*)malloc((size_t)n * sizeof(int32_t));
+    if (!order) return MPO_EINVAL;
+    mpo_rank_order(size, first, n, order);
+    st = place_in_order(size, first, last, n, num_ops, policy, bucket_width, order, offset_out,
+                        peak_out);
+    free(order);
+    return st;
+}
+
+/* About one mean lifetime (only the speed of the conflict index depends on it). */
+static int32_t default_bucket_width(const int32_t* first, const int32_t* last, int64_t n,
+                                    int32_t num_ops) {
     int64_t w = 1;
-    if (n > 0 && size && first && last) {
+    if (n > 0 && first && last) {
         int64_t span = 0;
         for (int64_t i = 0; i < n; ++i)
             if (last[i] >= first[i]) span += (int64_t)last[i] - first[i] + 1;
@@ -225,8 +235,14 @@ int32_t mpo_plan_trace(const int64_t* size, const int32_t* first, const int32_t*
         if (w > num_ops && num_ops > 0) w = num_ops;
         if (w > INT32_MAX) w = INT32_MAX;
     }
-    return mpo_plan_trace_w(size, first, last, n, num_ops, policy, (int32_t)w, offset_out,
-                            peak_out);
+    return (int32_t)w;
+}
+
+int32_t mpo_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last,
+                       int64_t n, int32_t num_ops, int32_t policy,
+                       int64_t* offset_out, int64_t* peak_out) {
+    return mpo_plan_trace_w(size, first, last, n, num_ops, policy,
+                            default_bucket_width(first, last, n, num_ops), offset_out, peak_out);
 }
 
 /* ------------------------------------------------------------------------- */
@@ -470,4 +486,95 @@ int32_t mpo_optimal_plan(const int64_t* size, const int32_t* first, const int32_
     for (int i = 0; i < S.n; ++i) offset_out[i] = S.best_off[i];
     *peak_out = n > 0 ? S.best : 0;
     return MPO_OK;
+}
+
+/* ------------------------------------------------------------------------- */
+/* Greedy by Breadth (Section 6, the strategy of Pisarchyk et al.): operators
+ * in decreasing breadth -- the sum of the sizes of their input and output
+ * tensors -- and, operator by operator, its tensors not yet placed in
+ * decreasing size.  In a trace of lifetimes a tensor is an output of its first
+ * op and an input of its last op (once when the two coincide). */
+
+typedef struct {
+    int64_t key;  /* breadth (sorted descending) or size */
+    int32_t idx;  /* op or tensor id (ascending among equal keys) */
+} keyed;
+
+static int cmp_keyed(const void* pa, const void* pb) {
+    const keyed* a = (const keyed*)pa;
+    const keyed* b = (const keyed*)pb;
+    if (a->key != b->key) return a->key > b->key ? -1 : 1;
+    return (a->idx > b->idx) - (a->idx < b->idx);
+}
+
+int32_t mpo_breadth_order(const int64_t* size, const int32_t* first, const int32_t* last,
+                          int64_t n, int32_t num_ops, int32_t* order_out) {
+    if (n > 0 && !order_out) return MPO_EINVAL;
+    int32_t st = mpo_check_trace(size, first, last, n, num_ops);
+    if (st != MPO_OK) return st;
+    if (n == 0) return MPO_OK;
+    int64_t* breadth = (int64_t*)calloc((size_t)num_ops, sizeof(int64_t));
+    keyed* ops = (keyed*)malloc((size_t)num_ops * sizeof(keyed));
+    keyed* mine = (keyed*)malloc((size_t)n * sizeof(keyed));
+    uint8_t* placed = (uint8_t*)calloc((size_t)n, 1);
+    /* tensors by op: those first or last used there (a counting sort) */
+    int64_t* at = (int64_t*)calloc((size_t)num_ops + 1, sizeof(int64_t));
+    int32_t* by_op = (int32_t*)malloc((size_t)(2 * n) * sizeof(int32_t));
+    if (!breadth || !ops || !mine || !placed || !at || !by_op) {
+        free(breadth); free(ops); free(mine); free(placed); free(at); free(by_op);
+        return MPO_EINVAL;
+    }
+    for (int64_t i = 0; i < n; ++i) {
+        breadth[first[i]] += size[i];
+        at[first[i] + 1] += 1;
+        if (last[i] != first[i]) {
+            breadth[last[i]] += size[i];
+            at[last[i] + 1] += 1;
+        }
+    }
+    for (int32_t t = 0; t < num_ops; ++t) at[t + 1] += at[t];
+    for (int64_t i = 0; i < n; ++i) {
+        by_op[at[first[i]]++] = (int32_t)i;
+        if (last[i] != first[i]) by_op[at[last[i]]++] = (int32_t)i;
+    }
+    /* at[t] is now the end of op t's tensors; op t's start is at[t - 1] */
+    for (int32_t t = 0; t < num_ops; ++t) {
+        ops[t].key = breadth[t];
+        ops[t].idx = t;
+    }
+    qsort(ops, (size_t)num_ops, sizeof(keyed), cmp_keyed);
+    int64_t k = 0;
+    for (int32_t r = 0; r < num_ops; ++r) {
+        const int32_t t = ops[r].idx;
+        const int64_t lo = t ? at[t - 1] : 0, hi = at[t];
+        int64_t m = 0;
+        for (int64_t e = lo; e < hi; ++e) {
+            const int32_t i = by_op[e];
+            if (placed[i]) continue;
+            placed[i] = 1;
+            mine[m].key = size[i];
+            mine[m].idx = i;
+            ++m;
+        }
+        qsort(mine, (size_t)m, sizeof(keyed), cmp_keyed);
+        for (int64_t e = 0; e < m; ++e) order_out[k++] = mine[e].idx;
+    }
+    free(breadth); free(ops); free(mine); free(placed); free(at); free(by_op);
+    return k == n ? MPO_OK : MPO_EINVAL;
+}
+
+int32_t mpo_plan_breadth(const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n, int32_t num_ops, int32_t policy, int64_t* offset_out,
+                         int64_t* peak_out) {
+    if (policy != MPO_LOWEST_FIT && policy != MPO_BEST_FIT) return MPO_EINVAL;
+    if (!peak_out || (n > 0 && !offset_out)) return MPO_EINVAL;
+    int32_t* order = (int32_t*)malloc((size_t)(n > 0 ? n : 1) * sizeof(int32_t));
+    if (!order) return MPO_EINVAL;
+    int32_t st = mpo_breadth_order(size, first, last, n, num_ops, order);
+    if (st == MPO_OK)
+        st = place_in_order(size, first, last, n, num_ops, policy,
+                            default_bucket_width(first, last, n, num_ops), order, offset_out,
+                            peak_out);
+    free(order);
+    return st;
 }

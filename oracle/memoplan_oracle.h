@@ -97,6 +97,20 @@ int32_t mpo_bump_plan(const int64_t* size, const int32_t* first, const int32_t* 
 int32_t mpo_optimal_plan(const int64_t* size, const int32_t* first, const int32_t* last,
                          int64_t n, int32_t num_ops, int64_t* offset_out, int64_t* peak_out);
 
+/* Greedy by Breadth (the strategy of Pisarchyk et al. that Section 6
+ * describes): operators in decreasing breadth, the sum of the sizes of their
+ * input and output tensors (ties: lower op first), and for each operator its
+ * tensors not yet placed in decreasing size (ties: lower id first).  Reading
+ * for a trace of lifetimes: a tensor is an output of its first op and an
+ * input of its last op, counted once when the two coincide.
+ * mpo_breadth_order writes the order; mpo_plan_breadth places the tensors in
+ * it with the fit policy of mpo_plan_trace. */
+int32_t mpo_breadth_order(const int64_t* size, const int32_t* first, const int32_t* last,
+                          int64_t n, int32_t num_ops, int32_t* order_out);
+int32_t mpo_plan_breadth(const int64_t* size, const int32_t* first, const int32_t* last,
+                         int64_t n, int32_t num_ops, int32_t policy, int64_t* offset_out,
+                         int64_t* peak_out);
+
 #ifdef __cplusplus
 }
 #endif

@@ -112,3 +112,31 @@ def intersecting_pairs_band(first, last):
                 break
             pairs.add((min(i, j), max(i, j)))
     return pairs
+
+
+def breadth_order_definitional(size, first, last):
+    """Greedy by Breadth order written out: each op's breadth is the bytes of
+    the tensors it produces (first op) or last reads (last op), once for a
+    tensor that does both; ops by breadth descending then index; within an op
+    its tensors not yet taken by size descending then id."""
+    n = len(size)
+    ops = {}
+    for i in range(n):
+        for t in {int(first[i]), int(last[i])}:
+            ops.setdefault(t, []).append(i)
+    breadth = {t: sum(int(size[i]) for i in ids) for t, ids in ops.items()}
+    taken, order = set(), []
+    for t in sorted(ops, key=lambda t: (-breadth[t], t)):
+        mine = sorted((i for i in ops[t] if i not in taken), key=lambda i: (-int(size[i]), i))
+        taken.update(mine)
+        order += mine
+    return order
+
+
+def place_in_given_order(order, size, first, last, policy):
+    off = [None] * len(size)
+    for k, t in enumerate(order):
+        placed = [(off[p], int(size[p])) for p in order[:k] if conflict(first, last, p, t)]
+        s = int(size[t])
+        off[t] = lowest_fit_candidates(s, placed) if policy == 0 else best_fit_candidates(s, placed)
+    return off, max((off[i] + int(size[i]) for i in range(len(size))), default=0)

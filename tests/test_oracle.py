@@ -460,3 +460,42 @@ def test_optimal_plan_limits():
     assert oracle.optimal_plan(np.zeros(0), np.zeros(0), np.zeros(0), 0)[1] == 0
     with pytest.raises(oracle.OracleError):
         oracle.bump_plan([64], [1], [0], 2)
+
+
+# ---------------------------------------------------------------------------
+# Greedy by Breadth (Section 6, Pisarchyk et al.)
+
+def test_breadth_hand_case():
+    # A 100 B [0,1], B 10 B [1,2], C 50 B [2,3], D 30 B [0,0]: op breadths
+    # 0: A + D = 130, 1: B + A = 110, 2: C + B = 60, 3: C = 50, so the order is
+    # op 0 (A, then D), op 1 (B), op 2 (C)
+    size, first, last = [100, 10, 50, 30], [0, 1, 2, 0], [1, 2, 3, 0]
+    assert oracle.breadth_order(size, first, last, 4).tolist() == [0, 3, 1, 2]
+    off, peak = oracle.plan_breadth(size, first, last, 4)
+    assert off.tolist() == [0, 100, 0, 100] and peak == 130
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_breadth_matches_definitional(policy):
+    from defs import breadth_order_definitional, place_in_given_order
+    rng = np.random.default_rng(120 + policy)
+    for _ in range(40):
+        n = int(rng.integers(1, 120))
+        T = int(rng.integers(1, 40))
+        t = tg.random_trace(rng, n, T, max_len=int(rng.integers(1, 8)),
+                            sizes=[64, 128, 192, 448] if n % 2 else None)
+        order = breadth_order_definitional(t.size, t.first, t.last)
+        assert oracle.breadth_order(t.size, t.first, t.last, t.num_ops).tolist() == order
+        off, peak = oracle.plan_breadth(t.size, t.first, t.last, t.num_ops, policy)
+        doff, dpeak = place_in_given_order(order, t.size, t.first, t.last, policy)
+        assert off.tolist() == doff and peak == dpeak
+        assert oracle.validate_plan(t.size, t.first, t.last, off)[1] == 0
+
+
+def test_breadth_at_least_optimum():
+    rng = np.random.default_rng(122)
+    for _ in range(25):
+        n = int(rng.integers(1, 8))
+        size, first, last, T = _random_tiny(rng, n)
+        opt = oracle.optimal_plan(size, first, last, T)[1]
+        assert oracle.plan_breadth(size, first, last, T)[1] >= opt
