@@ -258,6 +258,27 @@ int32_t mp_optimal_batch(const int64_t* begin, int64_t n_traces, const int32_t* 
                          int64_t n_tensors, int64_t* offset_out, int64_t* peak_out,
                          int32_t* status_out, void* stream);
 
+/* Greedy by Breadth, the strategy of Pisarchyk et al. that Section 6
+ * describes: operators in decreasing breadth (the sum of the sizes of their
+ * input and output tensors; lower op first on ties), and for each operator its
+ * tensors not yet placed in decreasing size (lower id first), each at the
+ * lowest (MP_LOWEST_FIT) or tightest (MP_BEST_FIT) gap left by the placed
+ * tensors whose lifetimes meet its own -- the same fit rules as greedy by
+ * size.  A tensor is an output of its first op and an input of its last op
+ * (once when they coincide): the trace records no other operator membership.
+ *   begin, num_ops, size, first, last, n_tensors: as for mp_plan_batch; each
+ *              trace at most MP_BREADTH_MAX_TRACE_LEN tensors.
+ *   offset_out[n_tensors], peak_out[n_traces]: offsets and peaks.
+ * One workgroup per trace, the trace held in LDS; no workspace.
+ * Data errors (on the status word): MP_EINVAL for an invalid tensor, bad trace
+ * bounds or a trace over MP_BREADTH_MAX_TRACE_LEN tensors; MP_EOVERFLOW when
+ * a trace's sizes exceed INT64_MAX. */
+#define MP_BREADTH_MAX_TRACE_LEN 2048
+int32_t mp_plan_breadth_batch(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                              const int64_t* size, const int32_t* first, const int32_t* last,
+                              int64_t n_tensors, int32_t policy, int64_t* offset_out,
+                              int64_t* peak_out, int32_t* status_out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

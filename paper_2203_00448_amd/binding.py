@@ -19,6 +19,7 @@ OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH, OP_PLAN_BATCH = 1,
 OP_PROBE = 6
 OP_BUMP = 7
 OPT_MAX_N = 12
+BREADTH_MAX_TRACE_LEN = 2048
 HINT_SORTED_FIRST = 1
 LOWEST_FIT, BEST_FIT = 0, 1
 BATCH_MAX_TRACE_LEN = 4096
@@ -65,6 +66,8 @@ def load_library(path: str = LIB_PATH):
     L.mp_bump_plan.restype = i32
     L.mp_optimal_batch.argtypes = [p, i64, p, p, p, p, i64, p, p, p, p]
     L.mp_optimal_batch.restype = i32
+    L.mp_plan_breadth_batch.argtypes = [p, i64, p, p, p, p, i64, i32, p, p, p, p]
+    L.mp_plan_breadth_batch.restype = i32
     _lib = L
     return L
 
@@ -384,4 +387,31 @@ def optimal_batch(begin, num_ops, size, first, last, *, check: bool = True, out=
     rc = L.mp_optimal_batch(_p(begin), n_traces, _p(num_ops), _p(size), _p(first), _p(last), n,
                             _p(offset), _p(peak), _p(status), _stream(stream))
     _finish(rc, status, "optimal_batch", check)
+    return offset, peak
+
+
+def plan_breadth_batch(begin, num_ops, size, first, last, *, policy: int = LOWEST_FIT,
+                       check: bool = True, out=None, status=None, stream=None):
+    """Greedy by Breadth plans of many traces (mp_plan_breadth_batch), each at
+    most BREADTH_MAX_TRACE_LEN tensors.  Returns (offset int64[N], peak int64[B])."""
+    L = load_library()
+    begin = _dev(begin, torch.int64, "begin")
+    num_ops = _dev(num_ops, torch.int32, "num_ops")
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    n_traces, n = num_ops.numel(), size.numel()
+    if begin.numel() != n_traces + 1 or first.numel() != n or last.numel() != n:
+        raise ValueError("inconsistent array lengths")
+    dev = size.device
+    if out is None:
+        offset = torch.empty(max(n, 1), dtype=torch.int64, device=dev)[:n]
+        peak = torch.empty(max(n_traces, 1), dtype=torch.int64, device=dev)[:n_traces]
+    else:
+        offset, peak = out
+    if status is None:
+        status = new_status(dev, stream)
+    rc = L.mp_plan_breadth_batch(_p(begin), n_traces, _p(num_ops), _p(size), _p(first), _p(last),
+                                 n, int(policy), _p(offset), _p(peak), _p(status), _stream(stream))
+    _finish(rc, status, "plan_breadth_batch", check)
     return offset, peak

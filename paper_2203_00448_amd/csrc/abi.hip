@@ -190,3 +190,17 @@ extern "C" int32_t mp_optimal_batch(const int64_t* begin, int64_t n_traces,
                                    offset_out, peak_out, status_out,
                                    static_cast<hipStream_t>(stream)));
 }
+
+extern "C" int32_t mp_plan_breadth_batch(const int64_t* begin, int64_t n_traces,
+                                         const int32_t* num_ops, const int64_t* size,
+                                         const int32_t* first, const int32_t* last,
+                                         int64_t n_tensors, int32_t policy, int64_t* offset_out,
+                                         int64_t* peak_out, int32_t* status_out, void* stream) {
+    if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || !status_out) return MP_EINVAL;
+    if (policy != MP_LOWEST_FIT && policy != MP_BEST_FIT) return MP_EINVAL;
+    if (n_traces > 0 && (!begin || !num_ops || !peak_out)) return MP_EINVAL;
+    if (n_tensors > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
+    return launched(launch_breadth(begin, n_traces, num_ops, size, first, last, n_tensors, policy,
+                                   offset_out, peak_out, status_out,
+                                   static_cast<hipStream_t>(stream)));
+}

@@ -1,0 +1,191 @@
+// Greedy by Breadth, the strategy of Pisarchyk et al. that Section 6 sets
+// beside greedy_by_size: operators in decreasing breadth (the bytes of their
+// input and output tensors, lower op first on ties), and for each operator
+// its tensors not yet placed in decreasing size (lower id first).  In a trace
+// of lifetimes a tensor is an output of its first op and an input of its last
+// op, once when the two coincide.  Each tensor then goes at the lowest (or the
+// tightest) gap left by the placed tensors whose lifetimes meet its own.
+//
+// One workgroup per trace, the trace in LDS.  A tensor is placed with the op
+// that comes first in the op order among its two ops, so the whole order is a
+// sort of the tensors by (breadth of that op desc, op, size desc, id); each
+// tensor finds its rank by counting the tensors before it.  Placement is one
+// tensor after another: the placed tensors whose lifetimes meet it are
+// gathered in LDS, every candidate start (0 or one of their ends) is tested in
+// parallel, and a block minimum picks the answer.
+#include "internal.hpp"
+#include "mp_device.hpp"
+
+namespace mp {
+
+namespace {
+
+constexpr int kBBlock = 512;
+constexpr int kBMax = MP_BREADTH_MAX_TRACE_LEN;
+
+struct BreadthShared {
+    int64_t size[kBMax];
+    int64_t off[kBMax];   // -1 until placed
+    int64_t bkey[kBMax];  // breadth of the op the tensor is placed with
+    int32_t first[kBMax];
+    int32_t last[kBMax];
+    int32_t op[kBMax];
+    uint16_t order[kBMax];
+    uint16_t nb[kBMax];   // placed tensors meeting the current one
+    uint32_t n_nb;
+    int32_t bad;
+};
+
+// Lexicographic (a0, a1) minimum over the workgroup; every thread gets it.
+__device__ void block_min2(uint64_t& a0, uint64_t& a1, uint64_t* scratch) {
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+#pragma unroll
+    for (int o = kWave / 2; o > 0; o >>= 1) {
+        const uint64_t b0 = __shfl_xor(a0, o, kWave), b1 = __shfl_xor(a1, o, kWave);
+        if (b0 < a0 || (b0 == a0 && b1 < a1)) {
+            a0 = b0;
+            a1 = b1;
+        }
+    }
+    if (lane == 0) {
+        scratch[2 * wid] = a0;
+        scratch[2 * wid + 1] = a1;
+    }
+    __syncthreads();
+    a0 = scratch[0];
+    a1 = scratch[1];
+    for (int w = 1; w < kBBlock / kWave; ++w) {
+        const uint64_t b0 = scratch[2 * w], b1 = scratch[2 * w + 1];
+        if (b0 < a0 || (b0 == a0 && b1 < a1)) {
+            a0 = b0;
+            a1 = b1;
+        }
+    }
+    __syncthreads();
+}
+
+__global__ __launch_bounds__(kBBlock) void breadth_kernel(
+    const int64_t* __restrict__ begin, const int32_t* __restrict__ num_ops,
+    const int64_t* __restrict__ size, const int32_t* __restrict__ first,
+    const int32_t* __restrict__ last, int64_t n_tensors, int32_t policy,
+    int64_t* __restrict__ offset_out, int64_t* __restrict__ peak_out,
+    int32_t* __restrict__ status) {
+    __shared__ BreadthShared S;
+    __shared__ uint64_t red[2 * kBBlock / kWave];
+    const int tid = threadIdx.x;
+    const int64_t b0 = begin[blockIdx.x], b1 = begin[blockIdx.x + 1];
+    if (b0 < 0 || b1 > n_tensors || b1 < b0 || b1 - b0 > kBMax) {
+        if (tid == 0) raise_status(status, MP_EINVAL);
+        return;
+    }
+    const int n = (int)(b1 - b0);
+    const int32_t T = num_ops[blockIdx.x];
+    if (tid == 0) S.bad = 0;
+    __syncthreads();
+    uint64_t acc = 0;
+    for (int i = tid; i < n; i += kBBlock) {
+        const int64_t s = size[b0 + i];
+        const int32_t f = first[b0 + i], l = last[b0 + i];
+        if (s <= 0 || f < 0 || f > l || l >= T) atomicOr(&S.bad, 1);
+        else acc = sat_add(acc, (uint64_t)s);
+        S.size[i] = s;
+        S.first[i] = f;
+        S.last[i] = l;
+        S.off[i] = -1;
+    }
+    acc = block_reduce<kBBlock>(acc, OpSatAdd(), red);
+    if (S.bad) {
+        if (tid == 0) raise_status(status, MP_EINVAL);
+        return;
+    }
+    if (acc > (uint64_t)INT64_MAX) {
+        if (tid == 0) raise_status(status, MP_EOVERFLOW);
+        return;
+    }
+    // each tensor's two op breadths, and the op it is placed with
+    for (int i = tid; i < n; i += kBBlock) {
+        const int32_t f = S.first[i], l = S.last[i];
+        int64_t bf = 0, bl = 0;
+        for (int j = 0; j < n; ++j) {
+            const int32_t fj = S.first[j], lj = S.last[j];
+            const int64_t sj = S.size[j];
+            bf += (fj == f || lj == f) ? sj : 0;
+            bl += (fj == l || lj == l) ? sj : 0;
+        }
+        S.bkey[i] = bf >= bl ? bf : bl;
+        S.op[i] = bf >= bl ? f : l;
+    }
+    __syncthreads();
+    // rank: the tensors before i in (breadth desc, op asc, size desc, id asc)
+    for (int i = tid; i < n; i += kBBlock) {
+        const int64_t bi = S.bkey[i], si = S.size[i];
+        const int32_t oi = S.op[i];
+        int r = 0;
+        for (int j = 0; j < n; ++j) {
+            const int64_t bj = S.bkey[j], sj = S.size[j];
+            const int32_t oj = S.op[j];
+            r += (bj > bi || (bj == bi && (oj < oi || (oj == oi && (sj > si || (sj == si && j < i))))))
+                     ? 1
+                     : 0;
+        }
+        S.order[r] = (uint16_t)i;
+    }
+    __syncthreads();
+    int64_t peak = 0;
+    for (int k = 0; k < n; ++k) {
+        const int t = S.order[k];
+        const int32_t ft = S.first[t], lt = S.last[t];
+        const int64_t st = S.size[t];
+        if (tid == 0) S.n_nb = 0;
+        __syncthreads();
+        for (int j = tid; j < n; j += kBBlock)
+            if (S.off[j] >= 0 && S.first[j] <= lt && ft <= S.last[j])
+                S.nb[atomicAdd(&S.n_nb, 1u)] = (uint16_t)j;
+        __syncthreads();
+        const int m = (int)S.n_nb;
+        // candidate starts: 0 (c == m) and each neighbour's end (c < m)
+        uint64_t key0 = ~0ull, key1 = ~0ull;  // lowest: (x, 0); best: (gap, x)
+        for (int c = tid; c <= m; c += kBBlock) {
+            const int64_t x = c < m ? S.off[S.nb[c]] + S.size[S.nb[c]] : 0;
+            bool fits = true;
+            int64_t gap_end = INT64_MAX;  // lowest neighbour start at or above x
+            for (int e = 0; e < m; ++e) {
+                const int j = S.nb[e];
+                const int64_t oj = S.off[j];
+                if (x < oj + S.size[j] && oj < x + st) fits = false;
+                if (oj >= x && oj < gap_end) gap_end = oj;
+            }
+            if (!fits) continue;
+            const uint64_t a0 = policy == MP_BEST_FIT
+                                    ? (gap_end == INT64_MAX ? ~0ull : (uint64_t)(gap_end - x))
+                                    : (uint64_t)x;
+            const uint64_t a1 = policy == MP_BEST_FIT ? (uint64_t)x : 0ull;
+            if (a0 < key0 || (a0 == key0 && a1 < key1)) {
+                key0 = a0;
+                key1 = a1;
+            }
+        }
+        block_min2(key0, key1, red);
+        const int64_t x = policy == MP_BEST_FIT ? (int64_t)key1 : (int64_t)key0;
+        if (tid == 0) S.off[t] = x;
+        peak = max(peak, x + st);
+        __syncthreads();
+    }
+    for (int i = tid; i < n; i += kBBlock) offset_out[b0 + i] = S.off[i];
+    if (tid == 0) peak_out[blockIdx.x] = peak;
+}
+
+}  // namespace
+
+hipError_t launch_breadth(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                          const int64_t* size, const int32_t* first, const int32_t* last,
+                          int64_t n_tensors, int32_t policy, int64_t* offset_out,
+                          int64_t* peak_out, int32_t* status, hipStream_t st) {
+    if (n_traces == 0) return hipSuccess;
+    hipLaunchKernelGGL(breadth_kernel, dim3((unsigned)n_traces), dim3(kBBlock), 0, st, begin,
+                       num_ops, size, first, last, n_tensors, policy, offset_out, peak_out,
+                       status);
+    return hipGetLastError();
+}
+
+}  // namespace mp

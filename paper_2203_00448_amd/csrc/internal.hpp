@@ -62,6 +62,12 @@ hipError_t launch_optimal(const int64_t* begin, int64_t n_traces, const int32_t*
                           int64_t n_tensors, int64_t* offset_out, int64_t* peak_out,
                           int32_t* status, hipStream_t st);
 
+// Greedy by Breadth (breadth.hip)
+hipError_t launch_breadth(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
+                          const int64_t* size, const int32_t* first, const int32_t* last,
+                          int64_t n_tensors, int32_t policy, int64_t* offset_out,
+                          int64_t* peak_out, int32_t* status, hipStream_t st);
+
 // device-wide prefix sums (scan.hip)
 size_t scan_workspace_bytes(int64_t n);
 hipError_t device_scan_i64(int64_t* data, int64_t n, bool inclusive, int64_t* partial,

@@ -184,3 +184,66 @@ def test_optimal_tiny_batch_workload():
     b, o, p = _optimal(binding, traces)
     expected = [oracle.optimal_plan(t.size, t.first, t.last, t.num_ops)[1] for t in traces]
     _check_optimal(b, o, p, traces, expected)
+
+
+# ---------------------------------------------------------------------------
+# Greedy by Breadth: offsets and peaks bit-exact against the oracle
+
+def _check_breadth(binding, traces, policy):
+    b = tg.concat(traces)
+    o, p = binding.plan_breadth_batch(*batch_to_device(b), policy=policy)
+    o, p = host(o), host(p)
+    for k, t in enumerate(traces):
+        lo, hi = int(b.begin[k]), int(b.begin[k + 1])
+        eo, ep = oracle.plan_breadth(t.size, t.first, t.last, t.num_ops, policy)
+        bad = np.nonzero(o[lo:hi] != eo)[0]
+        assert bad.size == 0, f"trace {k}: {bad.size} offsets differ, first at {bad[:5]}"
+        assert int(p[k]) == ep
+
+
+def test_breadth_hand_case():
+    binding = need_gpu()
+    print("case breadth hand case", flush=True)
+    t = tg.Trace(np.array([100, 10, 50, 30], np.int64), np.array([0, 1, 2, 0], np.int32),
+                 np.array([1, 2, 3, 0], np.int32), 4)
+    o, p = binding.plan_breadth_batch(*batch_to_device(tg.concat([t])))
+    assert host(o).tolist() == [0, 100, 0, 100] and int(p.item()) == 130
+
+
+@pytest.mark.parametrize("policy", [0, 1])
+def test_breadth_random_ragged(policy):
+    binding = need_gpu()
+    rng = np.random.default_rng(130 + policy)
+    print(f"case breadth random ragged batch, policy {policy}", flush=True)
+    traces = []
+    for k in range(120):
+        n = int(rng.choice([0, 1, 2, 3, 17, 64, 150, 511, 512, 513, 2047, 2048]))
+        if n <= 150:
+            T, span = int(rng.integers(1, 20)), int(rng.integers(1, 20))
+        else:
+            T, span = n + 1, int(rng.integers(1, 12))
+        alphabet = [64, 128, 192, 448, 1024] if k % 3 == 0 else None
+        traces.append(tg.random_trace(rng, n, T, max_len=span, sizes=alphabet) if n else
+                      tg.Trace(np.zeros(0, np.int64), np.zeros(0, np.int32),
+                               np.zeros(0, np.int32), 1))
+    _check_breadth(binding, traces, policy)
+
+
+def test_breadth_resnext_and_tiny():
+    binding = need_gpu()
+    print("case breadth: 16 ResNeXt-like traces of 2000, 64 tiny traces", flush=True)
+    _check_breadth(binding, [tg.resnext_trace(b) for b in range(16)], 0)
+    tiny = tg.tiny_batch(64, 10)
+    _check_breadth(binding, [tiny.trace(k) for k in range(64)], 1)
+
+
+def test_breadth_status_codes():
+    binding = need_gpu()
+    print("case breadth status codes", flush=True)
+    for t in (tg.Trace(np.full(2049, 64, np.int64), np.zeros(2049, np.int32),
+                       np.zeros(2049, np.int32), 1),
+              tg.Trace(np.array([64, 0], np.int64), np.zeros(2, np.int32),
+                       np.zeros(2, np.int32), 1)):
+        st = binding.new_status()
+        binding.plan_breadth_batch(*batch_to_device(tg.concat([t])), check=False, status=st)
+        assert int(st.item()) == binding.MP_EINVAL
