@@ -15,9 +15,10 @@ single-trace leg plans the seq2seq-decode-like trace (100,000 tensors, 4000
 ops, seed 3) with the whole-device planner and reports its tensors per
 second and peak / live-bytes lower bound, then applies the plan to a slab
 and probes it by replaying the ops; a strategies leg compares, on 2048 tiny
-ResNeXt-like traces of 10 tensors, the peaks of greedy-by-size (both fits)
-and bump allocation with the exact optimum found on the GPU (all outside
-`value`).
+ResNeXt-like traces of 10 tensors, the peaks of greedy-by-size (both fits),
+Greedy by Breadth and bump allocation with the exact optimum found on the
+GPU, and on the benchmark's traces with the live-bytes lower bound (all
+outside `value`).
 """
 from __future__ import annotations
 
@@ -133,9 +134,24 @@ def single_trace_leg(binding, tg, np, torch, reps: int = 3):
                                 "its events in op order, after a radix sort of (tile, op) keys)"}}
 
 
-def strategies_leg(binding, tg, np, torch, n_traces: int = 2048, n: int = 10, reps: int = 3):
-    """Peaks of the strategies Section 2.3 compares, on tiny traces where the
-    optimum of Eq. 2.1 is found exactly (mp_optimal_batch)."""
+def _timed(torch, np, fn, reps):
+    fn()  # warm-up
+    ms, res = [], None
+    for _ in range(reps):
+        ev = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+        ev[0].record()
+        res = fn()
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms.append(ev[0].elapsed_time(ev[1]))
+    return res, float(np.median(ms))
+
+
+def strategies_leg(binding, tg, np, torch, medium, n_traces: int = 2048, n: int = 10,
+                   reps: int = 3):
+    """Peaks of the strategies Sections 2.3 and 6 compare: on tiny traces
+    against the optimum of Eq. 2.1 found exactly (mp_optimal_batch), and on the
+    benchmark's ResNeXt-like traces against the live-bytes lower bound."""
     batch = tg.tiny_batch(n_traces, n)
     d = lambda a, t: torch.from_numpy(np.ascontiguousarray(a)).to("cuda", dtype=t)
     args = (d(batch.begin, torch.int64), d(batch.num_ops, torch.int32),
@@ -143,6 +159,7 @@ def strategies_leg(binding, tg, np, torch, n_traces: int = 2048, n: int = 10, re
     _, low, lb = binding.plan_batch(*args, max_trace_len=n)
     _, best, _ = binding.plan_batch(*args, max_trace_len=n, policy=binding.BEST_FIT)
     _, bump = binding.bump_plan(args[2], args[3], args[4], n, begin=args[0])
+    _, breadth = binding.plan_breadth_batch(*args)
     binding.optimal_batch(*args)  # warm-up
     ms = []
     for _ in range(reps):
@@ -152,8 +169,8 @@ def strategies_leg(binding, tg, np, torch, n_traces: int = 2048, n: int = 10, re
         ev[1].record()
         torch.cuda.synchronize()
         ms.append(ev[0].elapsed_time(ev[1]))
-    low, best, bump, opt, lb = (x.cpu().numpy().astype(np.float64)
-                                for x in (low, best, bump, opt, lb))
+    low, best, bump, breadth, opt, lb = (x.cpu().numpy().astype(np.float64)
+                                         for x in (low, best, bump, breadth, opt, lb))
 
     def ratio(x):
         r = x / opt
@@ -163,9 +180,27 @@ def strategies_leg(binding, tg, np, torch, n_traces: int = 2048, n: int = 10, re
                         "(seeds [6,b]), exact optimum by exhaustive search",
             "optimal_ms": float(np.median(ms)), "calls": reps,
             "greedy_lowest_over_opt": ratio(low), "greedy_best_over_opt": ratio(best),
-            "bump_over_opt": ratio(bump),
+            "breadth_over_opt": ratio(breadth), "bump_over_opt": ratio(bump),
             "opt_over_lb": {"mean": float((opt / lb).mean()), "max": float((opt / lb).max()),
-                            "at_lb": float((opt == lb).mean())}}
+                            "at_lb": float((opt == lb).mean())},
+            "resnext_batch": medium_comparison(binding, np, torch, *medium, reps)}
+
+
+def medium_comparison(binding, np, torch, mbatch, margs, reps):
+    """The benchmark's 1024 ResNeXt-like traces of 2000 tensors: each strategy's
+    peak over the live-bytes lower bound (the optimum is out of reach)."""
+    max_len = int((mbatch.begin[1:] - mbatch.begin[:-1]).max())
+    _, size_peak, lb = binding.plan_batch(*margs, max_trace_len=max_len)
+    (_, breadth), breadth_ms = _timed(torch, np, lambda: binding.plan_breadth_batch(*margs), reps)
+    _, bump = binding.bump_plan(margs[2], margs[3], margs[4], int(mbatch.num_ops.max()),
+                                begin=margs[0])
+    size_peak, breadth, bump, lb = (x.cpu().numpy().astype(np.float64)
+                                    for x in (size_peak, breadth, bump, lb))
+    over = lambda x: {"mean": float((x / lb).mean()), "max": float((x / lb).max()),
+                      "at_lb": float((x == lb).mean())}
+    return {"greedy_size_over_lb": over(size_peak), "greedy_breadth_over_lb": over(breadth),
+            "bump_over_lb": over(bump), "breadth_ms": breadth_ms,
+            "breadth_beats_size": float((breadth < size_peak).mean())}
 
 
 def cpu_baseline(batch, min_seconds: float = 10.0):
@@ -290,7 +325,8 @@ def main():
     if not args.no_single_trace:
         out["single_trace"] = single_trace_leg(binding, tg, np, torch)
     if not args.no_strategies:
-        out["strategies"] = strategies_leg(binding, tg, np, torch)
+        out["strategies"] = strategies_leg(binding, tg, np, torch,
+                                           (batch, (begin, num_ops, size, first, last)))
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(batch)
     print(json.dumps(out), flush=True)
