@@ -192,14 +192,15 @@ def medium_comparison(binding, np, torch, mbatch, margs, reps):
     max_len = int((mbatch.begin[1:] - mbatch.begin[:-1]).max())
     _, size_peak, lb = binding.plan_batch(*margs, max_trace_len=max_len)
     (_, breadth), breadth_ms = _timed(torch, np, lambda: binding.plan_breadth_batch(*margs), reps)
-    _, bump = binding.bump_plan(margs[2], margs[3], margs[4], int(mbatch.num_ops.max()),
-                                begin=margs[0])
+    (_, bump), bump_ms = _timed(
+        torch, np, lambda: binding.bump_plan(margs[2], margs[3], margs[4],
+                                             int(mbatch.num_ops.max()), begin=margs[0]), reps)
     size_peak, breadth, bump, lb = (x.cpu().numpy().astype(np.float64)
                                     for x in (size_peak, breadth, bump, lb))
     over = lambda x: {"mean": float((x / lb).mean()), "max": float((x / lb).max()),
                       "at_lb": float((x == lb).mean())}
     return {"greedy_size_over_lb": over(size_peak), "greedy_breadth_over_lb": over(breadth),
-            "bump_over_lb": over(bump), "breadth_ms": breadth_ms,
+            "bump_over_lb": over(bump), "breadth_ms": breadth_ms, "bump_ms": bump_ms,
             "breadth_beats_size": float((breadth < size_peak).mean())}
 
 

@@ -30,38 +30,43 @@ __global__ void bump_init_kernel(BumpFlags* fl) {
 }
 
 // Checks the tensors (and the trace bounds), and writes each tensor's sort
-// key (trace << op_bits) | first with its id.
+// key (trace << op_bits) | first with its id.  A grid-stride loop over a
+// bounded grid: the blocks add their sums of sizes into one word, and fewer
+// blocks mean fewer of those same-address atomics.
 __global__ __launch_bounds__(kSBlock) void bump_keys_kernel(
     const int64_t* __restrict__ begin, int64_t n_seg, const int64_t* __restrict__ size,
     const int32_t* __restrict__ first, const int32_t* __restrict__ last, int64_t n,
     int32_t num_ops, int op_bits, uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
     BumpFlags* fl, int32_t* status) {
     __shared__ uint64_t red[kSBlock / kWave];
-    const int64_t i = (int64_t)blockIdx.x * kSBlock + threadIdx.x;
+    const int64_t items = max(n, begin ? n_seg + 1 : (int64_t)0);
     uint32_t bad = 0;
     uint64_t acc = 0;
-    if (begin && i <= n_seg) {  // trace bounds: 0 = begin[0] <= ... <= begin[n_seg] = n
-        const int64_t b = begin[i];
-        if ((i == 0 && b != 0) || (i == n_seg && b != n) || (i < n_seg && begin[i + 1] < b))
-            bad = 1;
-    }
-    if (i < n) {
-        const int64_t s = size[i];
-        const int32_t f = first[i], l = last[i];
-        if (s <= 0 || f < 0 || f > l || l >= num_ops) bad = 1;
-        else acc = (uint64_t)s;
-        int64_t seg = 0;  // the last trace whose begin is <= i
-        if (begin) {
-            int64_t lo = 0, hi = n_seg - 1;
-            while (lo < hi) {
-                const int64_t mid = lo + (hi - lo + 1) / 2;
-                if (begin[mid] <= i) lo = mid;
-                else hi = mid - 1;
-            }
-            seg = lo;
+    for (int64_t i = (int64_t)blockIdx.x * kSBlock + threadIdx.x; i < items;
+         i += (int64_t)gridDim.x * kSBlock) {
+        if (begin && i <= n_seg) {  // trace bounds: 0 = begin[0] <= ... <= begin[n_seg] = n
+            const int64_t b = begin[i];
+            if ((i == 0 && b != 0) || (i == n_seg && b != n) || (i < n_seg && begin[i + 1] < b))
+                bad = 1;
         }
-        keys[i] = ((uint64_t)seg << op_bits) | (uint32_t)max(f, 0);
-        vals[i] = (uint32_t)i;
+        if (i < n) {
+            const int64_t s = size[i];
+            const int32_t f = first[i], l = last[i];
+            if (s <= 0 || f < 0 || f > l || l >= num_ops) bad = 1;
+            else acc = sat_add(acc, (uint64_t)s);
+            int64_t seg = 0;  // the last trace whose begin is <= i
+            if (begin) {
+                int64_t lo = 0, hi = n_seg - 1;
+                while (lo < hi) {
+                    const int64_t mid = lo + (hi - lo + 1) / 2;
+                    if (begin[mid] <= i) lo = mid;
+                    else hi = mid - 1;
+                }
+                seg = lo;
+            }
+            keys[i] = ((uint64_t)seg << op_bits) | (uint32_t)max(f, 0);
+            vals[i] = (uint32_t)i;
+        }
     }
     bad = block_reduce<kSBlock>((uint64_t)bad, OpOr<uint64_t>(), red) != 0;
     acc = block_reduce<kSBlock>(acc, OpSatAdd(), red);
@@ -350,7 +355,7 @@ hipError_t launch_bump(const int64_t* begin, int64_t n_seg, const int64_t* size,
     const int64_t items = max(n, begin ? n_seg + 1 : (int64_t)0);
     const unsigned nb = (unsigned)((max(items, (int64_t)1) + kSBlock - 1) / kSBlock);
     hipLaunchKernelGGL(bump_init_kernel, dim3(1), dim3(1), 0, st, fl);
-    hipLaunchKernelGGL(bump_keys_kernel, dim3(nb), dim3(kSBlock), 0, st, begin, n_seg, size,
+    hipLaunchKernelGGL(bump_keys_kernel, dim3(min(nb, 1024u)), dim3(kSBlock), 0, st, begin, n_seg, size,
                        first, last, n, num_ops, op_bits, k0, v0, fl, status);
     bool alt = false;
     hipError_t e = radix_sort_pairs(k0, v0, k1, v1, n, 0, op_bits + seg_bits, w + L.radix, &alt,
