@@ -9,10 +9,12 @@
 // One workgroup per trace, the trace in LDS.  A tensor is placed with the op
 // that comes first in the op order among its two ops, so the whole order is a
 // sort of the tensors by (breadth of that op desc, op, size desc, id); each
-// tensor finds its rank by counting the tensors before it.  Placement is one
-// tensor after another: the placed tensors whose lifetimes meet it are
-// gathered in LDS, every candidate start (0 or one of their ends) is tested in
-// parallel, and a block minimum picks the answer.
+// tensor finds its rank by counting the tensors before it (all waves).
+// Placement is one tensor after another, two barriers a step: all waves find
+// the placed tensors whose lifetimes meet the tensor and compact them into
+// LDS (a ballot prefix within a wave, one LDS atomic per wave); then wave 0
+// tests every candidate start (0 or one of their ends) on its lanes and a
+// shuffle minimum picks the answer.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -25,20 +27,31 @@ constexpr int kBMax = MP_BREADTH_MAX_TRACE_LEN;
 
 struct BreadthShared {
     int64_t size[kBMax];
-    int64_t off[kBMax];   // -1 until placed
-    int64_t bkey[kBMax];  // breadth of the op the tensor is placed with
+    int64_t off[kBMax];  // -1 until placed
     int32_t first[kBMax];
     int32_t last[kBMax];
-    int32_t op[kBMax];
     uint16_t order[kBMax];
-    uint16_t nb[kBMax];   // placed tensors meeting the current one
+    union {  // the ranking's keys, then (while placing) the neighbour list
+        struct {
+            int64_t bkey[kBMax];  // breadth of the op the tensor is placed with
+            int32_t op[kBMax];
+        };
+        uint16_t nb[kBMax];  // placed tensors meeting the current one
+    };
     uint32_t n_nb;
     int32_t bad;
 };
+// two workgroups per CU (160 KB of LDS)
+static_assert(sizeof(BreadthShared) <= 80 * 1024 - 128, "LDS of the breadth planner");
 
-// Lexicographic (a0, a1) minimum over the workgroup; every thread gets it.
-__device__ void block_min2(uint64_t& a0, uint64_t& a1, uint64_t* scratch) {
-    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+__device__ __forceinline__ int64_t readlane64(int64_t v, int q) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, q);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), q);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// Lexicographic (a0, a1) minimum over the wave; every lane gets it.
+__device__ __forceinline__ void wave_min2(uint64_t& a0, uint64_t& a1) {
 #pragma unroll
     for (int o = kWave / 2; o > 0; o >>= 1) {
         const uint64_t b0 = __shfl_xor(a0, o, kWave), b1 = __shfl_xor(a1, o, kWave);
@@ -47,21 +60,6 @@ __device__ void block_min2(uint64_t& a0, uint64_t& a1, uint64_t* scratch) {
             a1 = b1;
         }
     }
-    if (lane == 0) {
-        scratch[2 * wid] = a0;
-        scratch[2 * wid + 1] = a1;
-    }
-    __syncthreads();
-    a0 = scratch[0];
-    a1 = scratch[1];
-    for (int w = 1; w < kBBlock / kWave; ++w) {
-        const uint64_t b0 = scratch[2 * w], b1 = scratch[2 * w + 1];
-        if (b0 < a0 || (b0 == a0 && b1 < a1)) {
-            a0 = b0;
-            a1 = b1;
-        }
-    }
-    __syncthreads();
 }
 
 __global__ __launch_bounds__(kBBlock) void breadth_kernel(
@@ -71,7 +69,7 @@ __global__ __launch_bounds__(kBBlock) void breadth_kernel(
     int64_t* __restrict__ offset_out, int64_t* __restrict__ peak_out,
     int32_t* __restrict__ status) {
     __shared__ BreadthShared S;
-    __shared__ uint64_t red[2 * kBBlock / kWave];
+    __shared__ uint64_t red[kBBlock / kWave];
     const int tid = threadIdx.x;
     const int64_t b0 = begin[blockIdx.x], b1 = begin[blockIdx.x + 1];
     if (b0 < 0 || b1 > n_tensors || b1 < b0 || b1 - b0 > kBMax) {
@@ -131,48 +129,80 @@ __global__ __launch_bounds__(kBBlock) void breadth_kernel(
         S.order[r] = (uint16_t)i;
     }
     __syncthreads();
+    const int lane = tid & (kWave - 1);
+    const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
+    if (tid == 0) S.n_nb = 0;
+    __syncthreads();
     int64_t peak = 0;
     for (int k = 0; k < n; ++k) {
         const int t = S.order[k];
         const int32_t ft = S.first[t], lt = S.last[t];
         const int64_t st = S.size[t];
-        if (tid == 0) S.n_nb = 0;
-        __syncthreads();
-        for (int j = tid; j < n; j += kBBlock)
-            if (S.off[j] >= 0 && S.first[j] <= lt && ft <= S.last[j])
-                S.nb[atomicAdd(&S.n_nb, 1u)] = (uint16_t)j;
-        __syncthreads();
-        const int m = (int)S.n_nb;
-        // candidate starts: 0 (c == m) and each neighbour's end (c < m)
-        uint64_t key0 = ~0ull, key1 = ~0ull;  // lowest: (x, 0); best: (gap, x)
-        for (int c = tid; c <= m; c += kBBlock) {
-            const int64_t x = c < m ? S.off[S.nb[c]] + S.size[S.nb[c]] : 0;
-            bool fits = true;
-            int64_t gap_end = INT64_MAX;  // lowest neighbour start at or above x
-            for (int e = 0; e < m; ++e) {
-                const int j = S.nb[e];
-                const int64_t oj = S.off[j];
-                if (x < oj + S.size[j] && oj < x + st) fits = false;
-                if (oj >= x && oj < gap_end) gap_end = oj;
-            }
-            if (!fits) continue;
-            const uint64_t a0 = policy == MP_BEST_FIT
-                                    ? (gap_end == INT64_MAX ? ~0ull : (uint64_t)(gap_end - x))
-                                    : (uint64_t)x;
-            const uint64_t a1 = policy == MP_BEST_FIT ? (uint64_t)x : 0ull;
-            if (a0 < key0 || (a0 == key0 && a1 < key1)) {
-                key0 = a0;
-                key1 = a1;
+        // placed tensors meeting t, compacted into S.nb (any order)
+        for (int j0 = tid - lane; j0 < n; j0 += kBBlock) {
+            const int j = j0 + lane;
+            const bool hit = j < n && S.off[j] >= 0 && S.first[j] <= lt && ft <= S.last[j];
+            const uint64_t b = __ballot(hit);
+            if (b) {
+                uint32_t base = 0;
+                if (lane == 0) base = atomicAdd(&S.n_nb, (uint32_t)__popcll(b));
+                base = (uint32_t)__shfl(base, 0, kWave);
+                if (hit) S.nb[base + __popcll(b & below)] = (uint16_t)j;
             }
         }
-        block_min2(key0, key1, red);
-        const int64_t x = policy == MP_BEST_FIT ? (int64_t)key1 : (int64_t)key0;
-        if (tid == 0) S.off[t] = x;
-        peak = max(peak, x + st);
+        __syncthreads();
+        if (tid < kWave) {  // wave 0: candidate starts, 0 (c == m) and each neighbour's end
+            const int m = (int)S.n_nb;
+            uint64_t key0 = ~0ull, key1 = ~0ull;  // lowest: (x, 0); best: (gap, x)
+            for (int c0 = 0; c0 <= m; c0 += kWave) {
+                const int c = c0 + lane;
+                int64_t x = 0;
+                if (c < m) {
+                    const int j = S.nb[c];
+                    x = S.off[j] + S.size[j];
+                }
+                bool fits = true;
+                int64_t gap_end = INT64_MAX;  // lowest neighbour start at or above x
+                // neighbours 64 at a time: lane q holds neighbour e0 + q, read
+                // by every lane with readlane
+                for (int e0 = 0; e0 < m; e0 += kWave) {
+                    int64_t oq = 0, eq = 0;
+                    if (e0 + lane < m) {
+                        const int j = S.nb[e0 + lane];
+                        oq = S.off[j];
+                        eq = oq + S.size[j];
+                    }
+                    const int cnt = min(kWave, m - e0);
+                    for (int q = 0; q < cnt; ++q) {
+                        const int64_t o = readlane64(oq, q), e = readlane64(eq, q);
+                        if (x < e && o < x + st) fits = false;
+                        if (o >= x && o < gap_end) gap_end = o;
+                    }
+                }
+                if (c > m || !fits) continue;
+                const uint64_t a0 = policy == MP_BEST_FIT
+                                        ? (gap_end == INT64_MAX ? ~0ull : (uint64_t)(gap_end - x))
+                                        : (uint64_t)x;
+                const uint64_t a1 = policy == MP_BEST_FIT ? (uint64_t)x : 0ull;
+                if (a0 < key0 || (a0 == key0 && a1 < key1)) {
+                    key0 = a0;
+                    key1 = a1;
+                }
+            }
+            wave_min2(key0, key1);
+            const int64_t x = policy == MP_BEST_FIT ? (int64_t)key1 : (int64_t)key0;
+            if (lane == 0) {
+                S.off[t] = x;
+                S.n_nb = 0;
+            }
+            peak = max(peak, x + st);
+        }
         __syncthreads();
     }
-    for (int i = tid; i < n; i += kBBlock) offset_out[b0 + i] = S.off[i];
-    if (tid == 0) peak_out[blockIdx.x] = peak;
+    if (tid < kWave) {
+        for (int i = lane; i < n; i += kWave) offset_out[b0 + i] = S.off[i];
+        if (lane == 0) peak_out[blockIdx.x] = peak;
+    }
 }
 
 }  // namespace
