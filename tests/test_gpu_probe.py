@@ -145,3 +145,34 @@ def test_apply_plan_views_and_errors():
     # empty trace
     assert _probe(binding, np.zeros(0, np.int64), np.zeros(0, np.int32), np.zeros(0, np.int32),
                   np.zeros(0, np.int64), 3)[1] == 0
+
+
+def test_views_replay_chain256():
+    """The slab and its views used as execution would use them: ops in order,
+    each tensor written through its view at its first op and checked at its
+    last -- a valid GPU plan keeps every view intact, a shifted view does not."""
+    binding = need_gpu()
+    print("case views replay, chain256 planned on the GPU", flush=True)
+    t = tg.chain256()
+    o, p = binding.plan_trace(dev(t.size, torch.int64), dev(t.first, torch.int32),
+                              dev(t.last, torch.int32), t.num_ops)
+    off = host(o)
+
+    def replay(offsets):
+        slab, views = binding.apply_plan(offsets, t.size, int((offsets + t.size).max()))
+        slab.zero_()
+        bad = []
+        for op in range(t.num_ops):
+            for i in np.nonzero(t.first == op)[0]:
+                views[i].fill_(int(i) % 251 + 1)
+            for i in np.nonzero(t.last == op)[0]:
+                if not bool((views[i] == int(i) % 251 + 1).all().item()):
+                    bad.append(int(i))
+        return bad
+
+    assert replay(off) == []
+    # tensor 1 moved onto tensor 0's bytes: their lifetimes meet, one is hit
+    moved = off.copy()
+    assert t.first[1] <= t.last[0]
+    moved[1] = off[0]
+    assert replay(moved)
