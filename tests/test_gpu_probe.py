@@ -176,3 +176,17 @@ def test_views_replay_chain256():
     assert t.first[1] <= t.last[0]
     moved[1] = off[0]
     assert replay(moved)
+
+
+def test_sparse_plan_in_a_large_slab():
+    binding = need_gpu()
+    print("case probe: 64 tensors spread over 256 MiB (a million mostly empty tiles)", flush=True)
+    rng = np.random.default_rng(44)
+    n = 64
+    size = 4 * rng.integers(1, 50000, n)
+    first = rng.integers(0, 40, n)
+    last = first + rng.integers(0, 6, n)
+    off = (4 << 20) * rng.integers(0, 64, n) + 4 * rng.integers(0, 1000, n)  # some collide
+    num_ops = int(last.max()) + 1
+    c = _check(binding, size, first, last, off, num_ops, path=TILED)
+    assert _check(binding, size, first, last, off, num_ops, capacity=1, path=OPS) == c
