@@ -24,6 +24,8 @@
 // when it exceeds what the workspace holds, the tiled kernels stand down and
 // one workgroup replays the ops one after another instead (same results).
 
+#include <type_traits>
+
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -381,15 +383,15 @@ __device__ int64_t wave_find(const uint64_t* __restrict__ keys, int64_t total, i
     return lo;
 }
 
-// Packs each sorted event for the replay, relative to the event's tile:
-// info = first covered lane | count << 8 in the low half for a birth, in the
-// high half for a death (the other half 0), and the tensor id with bit 31 set
-// when the event starts a group -- a run of equal keys, the births or the
-// deaths of one op in one tile.
+// Packs each sorted event for the replay as four words, in the form the
+// replay uses them: the mask of the lanes (words) of its tile that the tensor
+// covers (two words); the tensor id + 1, with bit 31 set when the event starts
+// a group -- a run of equal keys, the births or the deaths of one op in one
+// tile; and all ones for a death, 0 for a birth.
 __global__ __launch_bounds__(kTBlock) void probe_pack_kernel(
     const int64_t* __restrict__ size, const int64_t* __restrict__ offset,
     const uint64_t* __restrict__ keys, const uint32_t* __restrict__ vals,
-    const int64_t* __restrict__ total_p, int op_bits, uint2* __restrict__ packed,
+    const int64_t* __restrict__ total_p, int op_bits, uint4* __restrict__ packed,
     const ProbeFlags* fl) {
     if (fl->skip) return;
     const int64_t total = *total_p;
@@ -399,10 +401,11 @@ __global__ __launch_bounds__(kTBlock) void probe_pack_kernel(
         const uint32_t id = vals[k];
         const bool start = k == 0 || keys[k - 1] != key;
         const int64_t tbase = (int64_t)(key >> op_bits) << kTileShift, o = offset[id];
-        const int64_t lo = max((o >> 2) - tbase, (int64_t)0);
-        const int64_t hi = min(((o + size[id]) >> 2) - tbase, (int64_t)kWave);
-        const uint32_t range = (uint32_t)lo | ((uint32_t)(hi - lo) << 8);
-        packed[k] = make_uint2((key & 1u) ? range << 16 : range, id | (start ? 1u << 31 : 0u));
+        const int lo = (int)max((o >> 2) - tbase, (int64_t)0);                  // 0..63
+        const int hi = (int)min(((o + size[id]) >> 2) - tbase, (int64_t)kWave);  // 1..64
+        const uint64_t mask = (hi == kWave ? ~0ull : (1ull << hi) - 1) & ~((1ull << lo) - 1);
+        packed[k] = make_uint4((uint32_t)mask, (uint32_t)(mask >> 32),
+                               (id + 1u) | (start ? 1u << 31 : 0u), (key & 1u) ? ~0u : 0u);
     }
 }
 
@@ -423,15 +426,18 @@ __device__ __forceinline__ int64_t uniform64(int64_t x) {
 // kUnroll packed events read through the scalar cache (the index is the same
 // for the whole wave), so they land in scalar registers.
 struct EventGroup {
-    uint32_t w[2 * kUnroll];
+    uint32_t w[4 * kUnroll];
 };
 typedef const __attribute__((address_space(4))) uint32_t* ConstWords;
-__device__ __forceinline__ EventGroup group_at(const uint2* packed, int64_t k) {
+__device__ __forceinline__ EventGroup group_at(const uint4* packed, int64_t k) {
     const ConstWords p = (ConstWords)(packed + k);
     EventGroup g;
 #pragma unroll
-    for (int i = 0; i < 2 * kUnroll; ++i) g.w[i] = p[i];
+    for (int i = 0; i < 4 * kUnroll; ++i) g.w[i] = p[i];
     return g;
+}
+__device__ __forceinline__ uint64_t pair64(uint32_t lo, uint32_t hi) {
+    return ((uint64_t)hi << 32) | lo;
 }
 
 // One wave per tile, word tile * 64 + lane per lane.  The slab accesses are
@@ -441,11 +447,15 @@ __device__ __forceinline__ EventGroup group_at(const uint2* packed, int64_t k) {
 // the previous group held deaths covering it; store the word (which also
 // lands the previous event's write); read it back; then a birth covering the
 // word takes the maximum, a death covering it keeps the read for its check.
-// Groups of kUnroll events are read one group ahead (the event buffer has
-// kPad entries past its end, so a read never needs a bound) and their checks
-// compared together, so no step waits on the one before.
+// The lane sets (events' lanes, pending clears) are 64-bit masks in scalar
+// registers, combined by scalar ands and ors and used as lane predicates as
+// they are; a lone wave issues each event in about 20 instructions.  Groups
+// of kUnroll events are read one group ahead through the scalar cache (the
+// event buffer has kPad entries past its end, so a read never needs a bound)
+// and their checks compared after the group; only a tile's last group masks
+// out the events past its end.
 __global__ __launch_bounds__(kTBlock) void probe_tiles_kernel(
-    const uint64_t* __restrict__ keys, const uint2* __restrict__ packed,
+    const uint64_t* __restrict__ keys, const uint4* __restrict__ packed,
     const int64_t* __restrict__ total_p, int op_bits, uint32_t* slab,
     uint8_t* __restrict__ clob, ProbeFlags* fl) {
     if (fl->skip) return;
@@ -458,43 +468,47 @@ __global__ __launch_bounds__(kTBlock) void probe_tiles_kernel(
         const bool mine = (uint64_t)w < top;
         uint32_t* word = mine ? slab + w : &fl->sink;
         uint32_t v = 0;    // the word's value
-        bool clr = false;  // covered by a death of the current group
+        uint64_t clr = 0;  // lanes covered by a death of the current group
         const int64_t e0 = uniform64(wave_find(keys, total, op_bits, (uint64_t)tile, false, lane));
         const int64_t e1 = uniform64(wave_find(keys, total, op_bits, (uint64_t)tile, true, lane));
-        EventGroup cur = group_at(packed, e0);
-        for (int64_t g = e0; g < e1; g += kUnroll) {
-            const EventGroup nxt = group_at(packed, g + kUnroll);
-            const int rem = (int)min(e1 - g, (int64_t)kUnroll);  // events past e1 cover no lane
+        auto group = [&](const EventGroup& cur, auto masked, uint32_t live) {
             uint32_t got[kUnroll];
-            uint32_t chk = 0;  // bit u: event g + u is a death covering this word
+            uint64_t dead[kUnroll];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                const uint32_t f = u < rem ? cur.w[2 * u] : 0u, idw = cur.w[2 * u + 1];
-                const bool start = idw >> 31;
-                const bool covb = lane - (f & 0xFFu) < ((f >> 8) & 0xFFu);
-                const bool covd = lane - ((f >> 16) & 0xFFu) < (f >> 24);
-                v = (start && clr) ? 0u : v;
-                clr = clr && !start;
+                const uint32_t* e = cur.w + 4 * u;
+                uint64_t mask = pair64(e[0], e[1]);
+                if constexpr (decltype(masked)::value) mask = ((live >> u) & 1u) ? mask : 0ull;
+                const uint32_t s32 = (uint32_t)((int32_t)e[2] >> 31);  // all ones at a group start
+                const uint64_t starts = pair64(s32, s32), deaths = pair64(e[3], e[3]);
+                v = __builtin_amdgcn_inverse_ballot_w64(clr & starts) ? 0u : v;  // clear
+                clr &= ~starts;
                 lane_word_store(word, v);
                 got[u] = lane_word_load(word);
-                v = covb ? max(v, (idw & 0x7FFFFFFFu) + 1u) : v;
-                chk |= covd ? 1u << u : 0u;
-                clr = clr || covd;
+                v = __builtin_amdgcn_inverse_ballot_w64(mask & ~deaths)
+                        ? max(v, e[2] & 0x7FFFFFFFu)
+                        : v;
+                dead[u] = mask & deaths;
+                clr |= dead[u];
             }
-            uint32_t bad = 0;
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                bad |= (((chk >> u) & 1u) && got[u] != (cur.w[2 * u + 1] & 0x7FFFFFFFu) + 1u)
-                           ? 1u << u
-                           : 0u;
-            if (__ballot(bad != 0)) {
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u)
-                    if ((bad >> u) & 1u) clob[cur.w[2 * u + 1] & 0x7FFFFFFFu] = 1;
+            for (int u = 0; u < kUnroll; ++u) {
+                const uint32_t id1 = cur.w[4 * u + 2] & 0x7FFFFFFFu;
+                if (__ballot(got[u] != id1) & dead[u]) clob[id1 - 1u] = 1;
             }
-            cur = nxt;
+        };
+        if (e1 > e0) {
+            EventGroup cur = group_at(packed, e0);
+            int64_t g = e0;
+            for (; g + kUnroll <= e1; g += kUnroll) {
+                const EventGroup nxt = group_at(packed, g + kUnroll);
+                group(cur, std::false_type{}, 0u);
+                cur = nxt;
+            }
+            if (g < e1) group(cur, std::true_type{}, (1u << (uint32_t)(e1 - g)) - 1u);
         }
-        lane_word_store(word, clr ? 0u : v);
+        v = __builtin_amdgcn_inverse_ballot_w64(clr) ? 0u : v;
+        lane_word_store(word, v);
     }
 }
 
@@ -511,12 +525,12 @@ __global__ __launch_bounds__(kTBlock) void probe_count_kernel(const uint8_t* __r
         atomicAdd(reinterpret_cast<unsigned long long*>(n_clob), (unsigned long long)c);
 }
 
-// Workspace sections.  8-byte arrays come first, then 4-byte ones, with no
-// padding between them, so every extra pair of capacity costs bytes and a
+// Workspace sections.  16- and 8-byte arrays come first, then 4-byte ones,
+// with no padding between them, so every extra pair of capacity costs bytes and a
 // workspace of probe_workspace_bytes(n, ops, c) holds capacity c exactly.
 struct ProbeLayout {
-    size_t flags, cnt, partial, keys0, keys1, radix, bstart, dstart, born, dies, big, vals0, vals1,
-        end;
+    size_t flags, packed, cnt, partial, keys0, keys1, radix, bstart, dstart, born, dies, big, vals0,
+        vals1, end;
 };
 
 ProbeLayout probe_layout(int64_t n, int32_t num_ops, int64_t capacity) {
@@ -530,6 +544,7 @@ ProbeLayout probe_layout(int64_t n, int32_t num_ops, int64_t capacity) {
         return here;
     };
     L.flags = take(256);  // ProbeFlags, padded
+    L.packed = take(ev * 16);  // 16-byte events, 16-byte aligned
     L.cnt = take(nn * 8);
     L.partial = take(scan_workspace_bytes((int64_t)nn));
     L.keys0 = take(ev * 8);
@@ -620,14 +635,14 @@ hipError_t launch_probe(const int64_t* size, const int32_t* first, const int32_t
         if (e != hipSuccess) return e;
         const uint64_t* ks = alt ? k1 : k0;
         const uint32_t* vs = alt ? v1 : v0;
-        uint2* packed = reinterpret_cast<uint2*>(alt ? k0 : k1);  // the other key buffer
+        uint4* packed = reinterpret_cast<uint4*>(w + L.packed);
         hipLaunchKernelGGL(probe_pack_kernel, dim3((unsigned)min((2 * capacity + kTBlock - 1) / kTBlock,
                                                                  (int64_t)4096)),
                            dim3(kTBlock), 0, st, size, offset, ks, vs, total, op_bits, packed,
                            (const ProbeFlags*)fl);
         const int64_t blocks = min((max_tiles + kTWaves - 1) / kTWaves, (int64_t)1 << 16);
         hipLaunchKernelGGL(probe_tiles_kernel, dim3((unsigned)blocks), dim3(kTBlock), 0, st, ks,
-                           (const uint2*)packed, total, op_bits, static_cast<uint32_t*>(slab), clob,
+                           (const uint4*)packed, total, op_bits, static_cast<uint32_t*>(slab), clob,
                            fl);
         hipLaunchKernelGGL(probe_count_kernel, dim3((unsigned)min((int64_t)nb, (int64_t)1024)),
                            dim3(kTBlock), 0, st, (const uint8_t*)clob, n, n_clob,
