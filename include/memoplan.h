@@ -121,7 +121,9 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
  * MP_OP_VALIDATE (uses n_tensors and capacity), MP_OP_PLAN_TRACE (uses
  * n_tensors and num_ops), MP_OP_VALIDATE_BATCH (uses n_tensors, capacity and
  * the number of traces passed as num_ops), MP_OP_PLAN_BATCH (the number of
- * traces passed as num_ops, max_trace_len as capacity).  Returns 0 for an
+ * traces passed as num_ops, max_trace_len as capacity), MP_OP_PROBE (uses
+ * n_tensors, num_ops and capacity, the number of lane events to hold; 0 asks
+ * for 16 n_tensors + 65536), MP_OP_BUMP (uses n_tensors).  Returns 0 for an
  * unknown op or out-of-range sizes. */
 #define MP_OP_LIVE_BYTES 1
 #define MP_OP_VALIDATE 2
