@@ -573,29 +573,69 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
             }
             __syncthreads();
             if (wid == 0) {
+                // The first 64 marked gaps, in address order, one per lane
+                // (a prefix count over the first 64 words of marks); a gap
+                // beyond them is reached by the walk further down.
+                const uint64_t my_bits = lane < words ? gbits[lane] : 0ull;
+                const uint32_t my_cnt = (uint32_t)__popcll(my_bits);
+                const uint32_t incl = wave_inclusive_sum(my_cnt);
+                const uint32_t n_marked = (uint32_t)__shfl(incl, kWave - 1, kWave);
+                const int ncand = (int)min(n_marked, (uint32_t)kWave);
+                uint32_t slot = incl - my_cnt;
+                for (uint64_t bm = my_bits; bm && slot < (uint32_t)kWave; bm &= bm - 1, ++slot)
+                    dpos[kDynCap - kWave + slot] = (uint32_t)(64 * lane + __builtin_ctzll(bm));
+                __builtin_amdgcn_wave_barrier();
+                uint32_t cg0 = 0, cg1 = 0;  // this lane's candidate gap [cg0, cg1)
+                if (lane < ncand) {
+                    const int i = (int)dpos[kDynCap - kWave + lane];
+                    cg0 = i ? run_pmax(skeys[i - 1]) : 0u;
+                    cg1 = run_start(skeys[i]);
+                }
+                // marked gaps past the candidates: the walk resumes after the
+                // last candidate (word 64 on when the first 64 words hold no more)
+                const int resume = n_marked > (uint32_t)kWave || words > kWave
+                                       ? (n_marked >= (uint32_t)kWave
+                                              ? (int)(uint32_t)__builtin_amdgcn_readlane(
+                                                    (int)dpos[kDynCap - 1], 0) + 1
+                                              : 64 * kWave)
+                                       : m;
                 uint32_t lo_d = kUnplacedT, hi_d = 0;  // this lane's late range, empty if none
                 if (lane < ndyn) {
                     const uint32_t p = dpos[lane];
+                    const uint32_t sp = a.su[p];
                     uint32_t o;
                     while ((o = agent_load(a.off + p)) == kUnplacedT) __builtin_amdgcn_s_sleep(1);
                     lo_d = o;
-                    hi_d = o + a.su[p];
+                    hi_d = o + sp;
                 }
-                // lowest c' >= c with [c', c' + st) clear of every late range
+                // lowest c' >= c with [c', c' + st) clear of every late range:
+                // jump to the highest end among the (few) overlapping ones
                 auto past_late = [&](uint32_t c) {
                     while (true) {
-                        const bool ov = lo_d < c + st && c < hi_d;
-                        if (!__ballot(ov)) return c;
-                        uint32_t v = ov ? hi_d : 0u;
-#pragma unroll
-                        for (int o = kWave / 2; o > 0; o >>= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o, kWave));
+                        uint64_t ov = __ballot(lo_d < c + st && c < hi_d);
+                        if (!ov) return c;
+                        uint32_t v = c;
+                        for (; ov; ov &= ov - 1)
+                            v = max(v, (uint32_t)__builtin_amdgcn_readlane((int)hi_d, (int)__builtin_ctzll(ov)));
                         c = v;
                     }
                 };
                 bool found = false;
                 uint32_t x = 0;
-                for (int w = 0; w < words && !found; ++w) {
-                    for (uint64_t bm = gbits[w]; bm; bm &= bm - 1) {
+                for (int k = 0; k < ncand; ++k) {
+                    const uint32_t g0 = (uint32_t)__builtin_amdgcn_readlane((int)cg0, k);
+                    const uint32_t g1 = (uint32_t)__builtin_amdgcn_readlane((int)cg1, k);
+                    const uint32_t c = past_late(g0);
+                    if ((uint64_t)c + st <= g1) {
+                        x = c;
+                        found = true;
+                        break;
+                    }
+                }
+                for (int w = resume >> 6; w < words && !found; ++w) {
+                    uint64_t bm = gbits[w];
+                    if (w == (resume >> 6)) bm &= ~0ull << (resume & 63);
+                    for (; bm; bm &= bm - 1) {
                         const int i = 64 * w + __builtin_ctzll(bm);
                         const uint32_t g0 = i ? run_pmax(skeys[i - 1]) : 0u, g1 = run_start(skeys[i]);
                         const uint32_t c = past_late(g0);
