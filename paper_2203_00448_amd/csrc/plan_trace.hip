@@ -327,6 +327,80 @@ __device__ __forceinline__ bool run_clear(const uint64_t* keys, int m, uint32_t 
     return a == 0 || run_pmax(keys[a - 1]) <= c;
 }
 
+// The placed predecessors as one run of disjoint ranges, when their union is
+// compact: the union drawn as a coverage bitmap over offset units (in the LDS
+// that holds a run), then its maximal covered intervals, in address order,
+// written back over the keys as start << 32 | end (disjoint, so each end is
+// its own prefix maximum) and loaded into `skeys`.  The lowest and the
+// tightest fit depend on the union only.  Returns false, the keys untouched,
+// when the union reaches past kRunCap * 64 units or has more than kRunCap
+// intervals.
+template <int BLOCK>
+__device__ bool union_run(uint64_t* gkeys, uint32_t nstat, uint64_t* skeys, uint32_t* scratch,
+                          uint64_t* scratch64, uint32_t* m_out) {
+    constexpr uint32_t kBits = (uint32_t)kRunCap * 64u;
+    uint32_t top = 0;
+    for (uint32_t i = threadIdx.x; i < nstat; i += BLOCK) top = max(top, (uint32_t)gkeys[i]);
+    top = block_reduce<BLOCK>(top, OpMax<uint32_t>(), scratch);
+    if (top > kBits) return false;
+    uint32_t* bm = reinterpret_cast<uint32_t*>(skeys);
+    const uint32_t nw = (top + 31) >> 5;
+    for (uint32_t j = threadIdx.x; j < nw; j += BLOCK) bm[j] = 0u;
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < nstat; i += BLOCK) {
+        const uint64_t k = gkeys[i];
+        const uint32_t o = (uint32_t)(k >> 32), e = (uint32_t)k;  // e > o
+        const uint32_t w0 = o >> 5, w1 = (e - 1) >> 5;
+        const uint32_t m0 = 0xFFFFFFFFu << (o & 31), m1 = 0xFFFFFFFFu >> (31 - ((e - 1) & 31));
+        if (w0 == w1) {
+            atomicOr(&bm[w0], m0 & m1);
+        } else {
+            atomicOr(&bm[w0], m0);
+            // full words: any interleaving with other writers leaves all ones
+            for (uint32_t j = w0 + 1; j < w1; ++j) bm[j] = 0xFFFFFFFFu;
+            atomicOr(&bm[w1], m1);
+        }
+    }
+    __syncthreads();
+    // interval starts (a covered unit after an uncovered one) and ends (the
+    // reverse), counted per contiguous chunk of words; the k-th start and the
+    // k-th end bound the k-th interval
+    const uint32_t chunk = (nw + BLOCK - 1) / BLOCK;
+    const uint32_t j0 = min(nw, (uint32_t)threadIdx.x * chunk), j1 = min(nw, j0 + chunk);
+    auto edges = [&](uint32_t j, uint32_t& st, uint32_t& en) {
+        const uint32_t w = bm[j];
+        const uint32_t prev = j ? bm[j - 1] >> 31 : 0u;
+        const uint32_t next = j + 1 < nw ? bm[j + 1] & 1u : 0u;
+        st = w & ~((w << 1) | prev);
+        en = w & ~((w >> 1) | (next << 31));
+    };
+    uint32_t cs = 0, ce = 0;
+    for (uint32_t j = j0; j < j1; ++j) {
+        uint32_t st, en;
+        edges(j, st, en);
+        cs += (uint32_t)__popc(st);
+        ce += (uint32_t)__popc(en);
+    }
+    uint64_t total;
+    const uint64_t base =
+        block_exclusive_sum<BLOCK, uint64_t>(((uint64_t)cs << 32) | ce, &total, scratch64);
+    const uint32_t m = (uint32_t)total;
+    if (m > (uint32_t)kRunCap) return false;
+    uint32_t* g32 = reinterpret_cast<uint32_t*>(gkeys);  // key k: [2k] end, [2k + 1] start
+    uint32_t gs = (uint32_t)(base >> 32), ge = (uint32_t)base;
+    for (uint32_t j = j0; j < j1; ++j) {
+        uint32_t st, en;
+        edges(j, st, en);
+        for (; st; st &= st - 1) g32[2 * gs++ + 1] = 32u * j + (uint32_t)__builtin_ctz(st);
+        for (; en; en &= en - 1) g32[2 * ge++] = 32u * j + (uint32_t)__builtin_ctz(en) + 1u;
+    }
+    __syncthreads();
+    for (uint32_t i = threadIdx.x; i < m; i += BLOCK) skeys[i] = gkeys[i];
+    __syncthreads();
+    *m_out = m;
+    return true;
+}
+
 // Lowest offset clear of every run.  It is 0 or the end of some range; an
 // end that is clear of its own run is the prefix maximum just below a gap of
 // at least s in that run (or the run's top), so those gap starts, checked
@@ -520,7 +594,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
             if (k < (uint32_t)stat_cap) gkeys[k] = ((uint64_t)o << 32) | (uint64_t)(o + a.su[p]);
         });
         __syncthreads();
-        const uint32_t nstat = s_nstat;
+        uint32_t nstat = s_nstat;
         const int ndyn = (int)min(s_ndyn, (uint32_t)kDynCap);
         if (nstat > (uint32_t)stat_cap) {
             // predecessor set beyond the scratch capacity: report, and still
@@ -534,11 +608,15 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         }
         // 2. sorted runs of the placed predecessors: one in LDS when it fits,
         //    else runs of kRunCap sorted in LDS and kept in global scratch
-        const int nruns = (int)((nstat + kRunCap - 1) / kRunCap);
+        int nruns = (int)((nstat + kRunCap - 1) / kRunCap);
+        uint32_t m_union = 0;
         if (nruns == 1) {
             for (int i = threadIdx.x; i < (int)nstat; i += BLOCK) skeys[i] = gkeys[i];
             __syncthreads();
             make_run<BLOCK>(skeys, (int)nstat, scratch);
+        } else if (union_run<BLOCK>(gkeys, nstat, skeys, scratch, scratch64, &m_union)) {
+            nstat = m_union;
+            nruns = 1;
         } else {
             for (int run = 0; run < nruns; ++run) {
                 const int m0 = (int)min((uint32_t)kRunCap, nstat - (uint32_t)run * kRunCap);
