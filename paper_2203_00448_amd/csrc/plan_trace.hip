@@ -677,17 +677,15 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                                                     (int)dpos[kDynCap - 1], 0) + 1
                                               : 64 * kWave)
                                        : m;
-                uint32_t lo_d = kUnplacedT, hi_d = 0;  // this lane's late range, empty if none
-                if (lane < ndyn) {
-                    const uint32_t p = dpos[lane];
-                    const uint32_t sp = a.su[p];
-                    uint32_t o;
-                    while ((o = agent_load(a.off + p)) == kUnplacedT) __builtin_amdgcn_s_sleep(1);
-                    lo_d = o;
-                    hi_d = o + sp;
-                }
-                // lowest c' >= c with [c', c' + st) clear of every late range:
-                // jump to the highest end among the (few) overlapping ones
+                // When every marked gap is a candidate and a lane is left, that
+                // lane holds the top of the run (no end): the walk then never
+                // runs past the candidates.
+                const bool closed = resume == m && ncand < kWave;
+                const int nc = ncand + (closed ? 1 : 0), ktop = closed ? ncand : -1;
+                if (closed && lane == ncand) cg0 = m ? run_pmax(skeys[m - 1]) : 0u;
+                uint32_t lo_d = kUnplacedT, hi_d = 0;  // this lane's late range, empty until known
+                // lowest c' >= c with [c', c' + st) clear of every known late
+                // range: jump to the highest end among the (few) overlapping ones
                 auto past_late = [&](uint32_t c) {
                     while (true) {
                         uint64_t ov = __ballot(lo_d < c + st && c < hi_d);
@@ -698,33 +696,69 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                         c = v;
                     }
                 };
-                bool found = false;
+                // lowest fit at or above c in candidates k on: x and its
+                // candidate xk; false when it runs past the candidates
                 uint32_t x = 0;
-                for (int k = 0; k < ncand; ++k) {
-                    const uint32_t g0 = (uint32_t)__builtin_amdgcn_readlane((int)cg0, k);
-                    const uint32_t g1 = (uint32_t)__builtin_amdgcn_readlane((int)cg1, k);
-                    const uint32_t c = past_late(g0);
-                    if ((uint64_t)c + st <= g1) {
-                        x = c;
-                        found = true;
-                        break;
-                    }
-                }
-                for (int w = resume >> 6; w < words && !found; ++w) {
-                    uint64_t bm = gbits[w];
-                    if (w == (resume >> 6)) bm &= ~0ull << (resume & 63);
-                    for (; bm; bm &= bm - 1) {
-                        const int i = 64 * w + __builtin_ctzll(bm);
-                        const uint32_t g0 = i ? run_pmax(skeys[i - 1]) : 0u, g1 = run_start(skeys[i]);
-                        const uint32_t c = past_late(g0);
-                        if ((uint64_t)c + st <= g1) {
+                int xk = 0;
+                auto walk = [&](int k, uint32_t c) {
+                    for (; k < nc; ++k) {
+                        c = past_late(max(c, (uint32_t)__builtin_amdgcn_readlane((int)cg0, k)));
+                        if (k == ktop ||
+                            (uint64_t)c + st <= (uint32_t)__builtin_amdgcn_readlane((int)cg1, k)) {
                             x = c;
-                            found = true;
-                            break;
+                            xk = k;
+                            return true;
                         }
                     }
+                    return false;
+                };
+                // The wait, one late predecessor a lane.  Known ranges only
+                // raise the lowest fit, so the answer is kept up to date as
+                // they arrive: it moves (the walk resumes from it) only when
+                // a range that arrived overlaps it.
+                bool pend = lane < ndyn;
+                uint32_t p = 0, sp = 0;
+                if (pend) {
+                    p = dpos[lane];
+                    sp = a.su[p];
                 }
-                if (!found) x = past_late(m ? run_pmax(skeys[m - 1]) : 0u);
+                bool ok = walk(0, 0u);
+                while (__ballot(pend)) {
+                    bool got = false;
+                    if (pend) {
+                        const uint32_t o = agent_load(a.off + p);
+                        if (o != kUnplacedT) {
+                            lo_d = o;
+                            hi_d = o + sp;
+                            pend = false;
+                            got = true;
+                        }
+                    }
+                    if (!__ballot(got)) {
+                        __builtin_amdgcn_s_sleep(1);
+                        continue;
+                    }
+                    if (ok && __ballot(got && lo_d < x + st && x < hi_d)) ok = walk(xk, x);
+                }
+                // every late range is known
+                if (!ok) {  // past the candidates: the marked gaps after them, then the top
+                    bool found = walk(0, 0u);
+                    for (int w = resume >> 6; w < words && !found; ++w) {
+                        uint64_t bm = gbits[w];
+                        if (w == (resume >> 6)) bm &= ~0ull << (resume & 63);
+                        for (; bm; bm &= bm - 1) {
+                            const int i = 64 * w + __builtin_ctzll(bm);
+                            const uint32_t g0 = i ? run_pmax(skeys[i - 1]) : 0u, g1 = run_start(skeys[i]);
+                            const uint32_t c = past_late(g0);
+                            if ((uint64_t)c + st <= g1) {
+                                x = c;
+                                found = true;
+                                break;
+                            }
+                        }
+                    }
+                    if (!found) x = past_late(m ? run_pmax(skeys[m - 1]) : 0u);
+                }
                 if (lane == 0) agent_store(a.off + qt, x);
             }
             __syncthreads();
