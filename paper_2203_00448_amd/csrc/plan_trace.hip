@@ -33,6 +33,7 @@ namespace {
 constexpr int kTBlock = 512;
 constexpr int kRunCap = 16384;    // ranges sorted at once in LDS
 constexpr int kDynCap = 1024;     // predecessors still unplaced when t is examined
+constexpr uint32_t kUnionMin = 256;  // placed predecessors merged through a bitmap beyond this
 constexpr int64_t kScratchRuns = 8;  // global scratch per workgroup: 8 sorted runs
 constexpr uint32_t kUnplacedT = 0xFFFFFFFFu;
 constexpr int kLongMax = 4096;    // the long list is kept at most this long when possible
@@ -608,15 +609,16 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         }
         // 2. sorted runs of the placed predecessors: one in LDS when it fits,
         //    else runs of kRunCap sorted in LDS and kept in global scratch
+        // beyond a few hundred ranges the union is cheaper than a sort
         int nruns = (int)((nstat + kRunCap - 1) / kRunCap);
         uint32_t m_union = 0;
-        if (nruns == 1) {
+        if (nstat > kUnionMin && union_run<BLOCK>(gkeys, nstat, skeys, scratch, scratch64, &m_union)) {
+            nstat = m_union;
+            nruns = 1;
+        } else if (nruns == 1) {
             for (int i = threadIdx.x; i < (int)nstat; i += BLOCK) skeys[i] = gkeys[i];
             __syncthreads();
             make_run<BLOCK>(skeys, (int)nstat, scratch);
-        } else if (union_run<BLOCK>(gkeys, nstat, skeys, scratch, scratch64, &m_union)) {
-            nstat = m_union;
-            nruns = 1;
         } else {
             for (int run = 0; run < nruns; ++run) {
                 const int m0 = (int)min((uint32_t)kRunCap, nstat - (uint32_t)run * kRunCap);
