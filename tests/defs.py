@@ -140,3 +140,29 @@ def place_in_given_order(order, size, first, last, policy):
         s = int(size[t])
         off[t] = lowest_fit_candidates(s, placed) if policy == 0 else best_fit_candidates(s, placed)
     return off, max((off[i] + int(size[i]) for i in range(len(size))), default=0)
+
+
+def interleaved_trace(k):
+    """(size, first, last, num_ops, offsets, peak) of a trace with a closed-form
+    lowest-fit plan: 2k tensors of 64 B alive at op 0, the odd ids also at op
+    1, then one of 64 B alive at op 1 only.  In rank order (equal sizes: id
+    order) the first 2k pack at 64 j; the last meets only the odd ones, whose
+    ranges are k disjoint intervals, and goes at 0.  Peak 128 k."""
+    n = 2 * k + 1
+    first = np.zeros(n, np.int32)
+    first[-1] = 1
+    last = np.zeros(n, np.int32)
+    last[1:2 * k:2] = 1
+    last[-1] = 1
+    off = np.append(64 * np.arange(2 * k, dtype=np.int64), 0)
+    return np.full(n, 64, np.int64), first, last, 2, off, 128 * k
+
+
+def packed_wide_trace(n):
+    """Closed-form lowest-fit plan of n - 1 tensors of 4 KiB (ids 1..n-1) and
+    one of 64 B (id 0), all alive at ops 0-1: the large ones rank first and
+    pack in id order, the small one goes on top at 4096 (n - 1)."""
+    size = np.full(n, 4096, np.int64)
+    size[0] = 64
+    off = np.append(4096 * (n - 1), 4096 * np.arange(n - 1, dtype=np.int64))
+    return size, np.zeros(n, np.int32), np.ones(n, np.int32), 2, off, 4096 * (n - 1) + 64

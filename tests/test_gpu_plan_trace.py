@@ -10,6 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
+from defs import interleaved_trace, packed_wide_trace
 from gpu_util import dev, host, need_gpu, torch
 from paper_2203_00448_amd import tracegen as tg
 
@@ -62,8 +63,8 @@ def test_random_traces():
 def test_adversarial_shapes():
     binding = need_gpu()
     rng = np.random.default_rng(301)
-    print("case full overlap beyond one LDS run", flush=True)
-    n = 9000  # up to 8999 predecessors: more than one sorted run of 8192
+    print("case full overlap, 9000 tensors", flush=True)
+    n = 9000  # up to 8999 placed predecessors, drawn as one coverage bitmap
     _check(binding, tg.Trace(64 * rng.integers(1, 200, n), np.zeros(n, np.int32),
                              np.full(n, 3, np.int32), 4))
     print("case equal sizes / long-lived / disjoint", flush=True)
@@ -74,6 +75,20 @@ def test_adversarial_shapes():
     n = 3000
     _check(binding, tg.Trace(64 * rng.integers(1, 50, n), np.arange(n, dtype=np.int32),
                              np.arange(n, dtype=np.int32), n))
+
+
+def test_union_fallbacks():
+    """Predecessor sets the coverage bitmap declines take the sorted runs:
+    more than 16,384 disjoint intervals, and a union wider than 2^20 units
+    (with more than 16,384 ranges, so two runs)."""
+    binding = need_gpu()
+    for name, (sz, f, l, T, eo, ep) in [("more intervals than one run", interleaved_trace(16400)),
+                                        ("union wider than the bitmap", packed_wide_trace(16600))]:
+        print("case", name, flush=True)
+        off, peak = _plan(binding, tg.Trace(sz, f, l, T))
+        bad = np.nonzero(off != eo)[0]
+        assert bad.size == 0, f"{name}: {bad.size} offsets differ, first at {bad[:5]}"
+        assert peak == ep
 
 
 def test_decode100k():

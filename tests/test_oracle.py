@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 
 import oracle
-from defs import (best_fit_candidates, brute_force_opt, conflict, greedy_definitional,
+from defs import (interleaved_trace, packed_wide_trace, best_fit_candidates, brute_force_opt, conflict, greedy_definitional,
                   intersecting_pairs_band, live_profile_bruteforce, lowest_fit_candidates,
                   rank_order)
 from paper_2203_00448_amd import tracegen as tg
@@ -74,6 +74,18 @@ def test_full_overlap_prefix_sums():
         expect[order] = np.concatenate([[0], np.cumsum(size[order])[:-1]])
         assert off.tolist() == expect.tolist()
         assert peak == int(size.sum())
+
+
+@pytest.mark.parametrize("make,arg", [(interleaved_trace, 1), (interleaved_trace, 150),
+                                      (packed_wide_trace, 2), (packed_wide_trace, 300)])
+def test_closed_form_plans(make, arg):
+    """Two traces whose lowest-fit plans have closed forms (used at full size
+    by the GPU tests): the oracle and the definitional greedy both give them."""
+    size, first, last, T, off, peak = make(arg)
+    eo, ep = oracle.plan_trace(size, first, last, T)
+    assert np.array_equal(eo, off) and ep == peak
+    if len(size) <= 301:
+        assert np.array_equal(np.asarray(greedy_definitional(size, first, last)[0]), off)
 
 
 def test_disjoint_all_zero():
