@@ -8,13 +8,14 @@
 //
 // One workgroup per trace, the trace in LDS.  A tensor is placed with the op
 // that comes first in the op order among its two ops, so the whole order is a
-// sort of the tensors by (breadth of that op desc, op, size desc, id); each
-// tensor finds its rank by counting the tensors before it (all waves).
+// sort of the tensors by (breadth of that op desc, op, size desc, id): op
+// breadths from a histogram over ops, then a bitonic sort of the indices.
 // Placement is one tensor after another, two barriers a step: all waves find
 // the placed tensors whose lifetimes meet the tensor and compact them into
 // LDS (a ballot prefix within a wave, one LDS atomic per wave); then wave 0
 // tests every candidate start (0 or one of their ends) on its lanes and a
-// shuffle minimum picks the answer.
+// shuffle minimum picks the answer -- or, for the lowest fit with at most 64
+// neighbours, a walk from 0 past the overlapping neighbours.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -100,35 +101,75 @@ __global__ __launch_bounds__(kBBlock) void breadth_kernel(
         if (tid == 0) raise_status(status, MP_EOVERFLOW);
         return;
     }
-    // each tensor's two op breadths, and the op it is placed with
-    for (int i = tid; i < n; i += kBBlock) {
-        const int32_t f = S.first[i], l = S.last[i];
-        int64_t bf = 0, bl = 0;
-        for (int j = 0; j < n; ++j) {
-            const int32_t fj = S.first[j], lj = S.last[j];
-            const int64_t sj = S.size[j];
-            bf += (fj == f || lj == f) ? sj : 0;
-            bl += (fj == l || lj == l) ? sj : 0;
+    // each tensor's two op breadths, and the op it is placed with: a
+    // histogram over ops (a tensor adds its size at its first op and, if
+    // different, at its last), held in the LDS of the offsets while it is
+    // needed; more ops than that: a count over all pairs
+    if (T <= kBMax) {
+        int64_t* hist = S.off;
+        for (int o = tid; o < T; o += kBBlock) hist[o] = 0;
+        __syncthreads();
+        for (int i = tid; i < n; i += kBBlock) {
+            const int32_t f = S.first[i], l = S.last[i];
+            const unsigned long long s = (unsigned long long)S.size[i];
+            atomicAdd(reinterpret_cast<unsigned long long*>(&hist[f]), s);
+            if (l != f) atomicAdd(reinterpret_cast<unsigned long long*>(&hist[l]), s);
         }
-        S.bkey[i] = bf >= bl ? bf : bl;
-        S.op[i] = bf >= bl ? f : l;
+        __syncthreads();
+        for (int i = tid; i < n; i += kBBlock) {
+            const int32_t f = S.first[i], l = S.last[i];
+            const int64_t bf = hist[f], bl = hist[l];
+            S.bkey[i] = bf >= bl ? bf : bl;
+            S.op[i] = bf >= bl ? f : l;
+        }
+        __syncthreads();
+        for (int i = tid; i < n; i += kBBlock) S.off[i] = -1;
+    } else {
+        for (int i = tid; i < n; i += kBBlock) {
+            const int32_t f = S.first[i], l = S.last[i];
+            int64_t bf = 0, bl = 0;
+            for (int j = 0; j < n; ++j) {
+                const int32_t fj = S.first[j], lj = S.last[j];
+                const int64_t sj = S.size[j];
+                bf += (fj == f || lj == f) ? sj : 0;
+                bl += (fj == l || lj == l) ? sj : 0;
+            }
+            S.bkey[i] = bf >= bl ? bf : bl;
+            S.op[i] = bf >= bl ? f : l;
+        }
     }
     __syncthreads();
-    // rank: the tensors before i in (breadth desc, op asc, size desc, id asc)
-    for (int i = tid; i < n; i += kBBlock) {
-        const int64_t bi = S.bkey[i], si = S.size[i];
-        const int32_t oi = S.op[i];
-        int r = 0;
-        for (int j = 0; j < n; ++j) {
-            const int64_t bj = S.bkey[j], sj = S.size[j];
-            const int32_t oj = S.op[j];
-            r += (bj > bi || (bj == bi && (oj < oi || (oj == oi && (sj > si || (sj == si && j < i))))))
-                     ? 1
-                     : 0;
-        }
-        S.order[r] = (uint16_t)i;
-    }
+    // rank order (breadth desc, op asc, size desc, id asc): a bitonic sort of
+    // the indices, padded to a power of two with indices >= n that go last
+    int np2 = 1;
+    while (np2 < n) np2 <<= 1;
+    for (int i = tid; i < np2; i += kBBlock) S.order[i] = (uint16_t)i;
     __syncthreads();
+    auto ranks_before = [&](int a, int b) {
+        if (b >= n) return a < n || a < b;
+        if (a >= n) return false;
+        const int64_t ba = S.bkey[a], bb = S.bkey[b];
+        if (ba != bb) return ba > bb;
+        const int32_t oa = S.op[a], ob = S.op[b];
+        if (oa != ob) return oa < ob;
+        const int64_t sa = S.size[a], sb = S.size[b];
+        if (sa != sb) return sa > sb;
+        return a < b;
+    };
+    for (int k = 2; k <= np2; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < (np2 >> 1); i += kBBlock) {
+                const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo | j;
+                const int a = S.order[lo], b = S.order[hi];
+                const bool up = (lo & k) == 0;
+                if (up ? ranks_before(b, a) : ranks_before(a, b)) {
+                    S.order[lo] = (uint16_t)b;
+                    S.order[hi] = (uint16_t)a;
+                }
+            }
+            __syncthreads();
+        }
+    }
     const int lane = tid & (kWave - 1);
     const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
     if (tid == 0) S.n_nb = 0;
@@ -151,7 +192,31 @@ __global__ __launch_bounds__(kBBlock) void breadth_kernel(
             }
         }
         __syncthreads();
-        if (tid < kWave) {  // wave 0: candidate starts, 0 (c == m) and each neighbour's end
+        if (tid < kWave && policy != MP_BEST_FIT && (int)S.n_nb <= kWave) {
+            // wave 0, lowest fit with at most 64 neighbours (one a lane): from
+            // 0, jump to the highest end among the neighbours overlapping
+            // [x, x + st) until none does; each jump skips only blocked starts
+            const int m = (int)S.n_nb;
+            int64_t oq = 0, eq = INT64_MIN;  // no neighbour: never overlaps
+            if (lane < m) {
+                const int j = S.nb[lane];
+                oq = S.off[j];
+                eq = oq + S.size[j];
+            }
+            int64_t x = 0;
+            while (true) {
+                uint64_t ov = __ballot(oq < x + st && x < eq);
+                if (!ov) break;
+                int64_t v = x;
+                for (; ov; ov &= ov - 1) v = max(v, readlane64(eq, (int)__builtin_ctzll(ov)));
+                x = v;
+            }
+            if (lane == 0) {
+                S.off[t] = x;
+                S.n_nb = 0;
+            }
+            peak = max(peak, x + st);
+        } else if (tid < kWave) {  // wave 0: candidate starts, 0 (c == m) and each neighbour's end
             const int m = (int)S.n_nb;
             uint64_t key0 = ~0ull, key1 = ~0ull;  // lowest: (x, 0); best: (gap, x)
             for (int c0 = 0; c0 <= m; c0 += kWave) {

@@ -226,6 +226,8 @@ def test_breadth_random_ragged(policy):
         traces.append(tg.random_trace(rng, n, T, max_len=span, sizes=alphabet) if n else
                       tg.Trace(np.zeros(0, np.int64), np.zeros(0, np.int32),
                                np.zeros(0, np.int32), 1))
+    # dense traces: hundreds of placed neighbours per tensor (beyond one wave)
+    traces += [tg.random_trace(rng, 600, 20, max_len=20), tg.random_trace(rng, 2000, 40, max_len=40)]
     _check_breadth(binding, traces, policy)
 
 
