@@ -17,11 +17,13 @@
 //   place      persistent kernel: workgroups take ranks from a counter.  For
 //              tensor t the workgroup walks t's candidates (forward band,
 //              backward window, long list), keeps those ranked before t,
-//              sorts the already placed ones by offset (LDS bitonic sort,
-//              prefix maxima of the ends), waits for the rest, and finds the
-//              lowest fitting gap.  A tensor only waits on lower ranks, which
-//              were taken earlier by running workgroups, so the schedule
-//              cannot deadlock.
+//              turns the already placed ones into one run of ranges by
+//              offset (their union through a coverage bitmap, or an LDS
+//              bitonic sort with prefix maxima of the ends), marks the run's
+//              gaps that hold t, then waits for the rest while keeping the
+//              lowest fit up to date as they arrive.  A tensor only waits on
+//              lower ranks, which were taken earlier by running workgroups,
+//              so the schedule cannot deadlock.
 //   output     offsets (scaled back to bytes) and the peak.
 #include "internal.hpp"
 #include "mp_device.hpp"
