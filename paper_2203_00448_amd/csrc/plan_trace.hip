@@ -25,6 +25,8 @@
 //              lower ranks, which were taken earlier by running workgroups,
 //              so the schedule cannot deadlock.
 //   output     offsets (scaled back to bytes) and the peak.
+#include <type_traits>
+
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -35,6 +37,7 @@ namespace {
 constexpr int kTBlock = 512;
 constexpr int kRunCap = 16384;    // ranges sorted at once in LDS
 constexpr int kDynCap = 1024;     // predecessors still unplaced when t is examined
+static_assert(kDynCap <= 16 * kWave, "wave 0 holds every late predecessor, 16 a lane at most");
 constexpr uint32_t kUnionMin = 256;  // placed predecessors merged through a bitmap beyond this
 constexpr int64_t kScratchRuns = 8;  // global scratch per workgroup: 8 sorted runs
 constexpr uint32_t kUnplacedT = 0xFFFFFFFFu;
@@ -566,6 +569,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     __shared__ uint32_t scratch[BLOCK / kWave];
     __shared__ uint64_t scratch64[BLOCK / kWave];
     __shared__ uint64_t gbits[kRunCap / 64];  // gaps of the placed run that hold t
+    __shared__ uint32_t cidx[kWave];           // the first 64 of them
     __shared__ uint32_t s_rank, s_nstat, s_ndyn;
     if (a.fl->abort) return;
     const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
@@ -632,15 +636,15 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 __syncthreads();
             }
         }
-        // Lowest fit with one run of placed predecessors and at most 64 late
-        // ones: before waiting, mark the run's gaps [prefix maximum below i,
-        // start of i) that hold t.  Then wave 0 alone waits for the late
-        // ones (a lane each, their ranges stay in registers) and walks the
+        // Lowest fit with one run of placed predecessors: before waiting,
+        // mark the run's gaps [prefix maximum below i, start of i) that hold
+        // t.  Then wave 0 alone waits for the late ones (all of them: one to
+        // sixteen a lane, their ranges stay in registers) and walks the
         // marked gaps in order, then the top: in a gap it moves past the
         // highest end among the late ranges overlapping [c, c + st) until
         // none does, and the first gap that still holds t gives the offset.
         // No workgroup barrier lies between the last wait and the publish.
-        if (!a.best && nruns <= 1 && ndyn <= kWave) {
+        if (!a.best && nruns <= 1) {
             const int m = (int)nstat, words = (m + 63) >> 6;
             const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
             for (int w = wid; w < words; w += BLOCK / kWave) {
@@ -654,7 +658,10 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 if (lane == 0) gbits[w] = mk;
             }
             __syncthreads();
-            if (wid == 0) {
+            // wave 0; K late predecessors a lane (K = 1, 4 or 16 for up to
+            // 64, 256 or 1024 of them)
+            auto wave0 = [&](auto k_late) {
+                constexpr int K = decltype(k_late)::value;
                 // The first 64 marked gaps, in address order, one per lane
                 // (a prefix count over the first 64 words of marks); a gap
                 // beyond them is reached by the walk further down.
@@ -665,11 +672,11 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 const int ncand = (int)min(n_marked, (uint32_t)kWave);
                 uint32_t slot = incl - my_cnt;
                 for (uint64_t bm = my_bits; bm && slot < (uint32_t)kWave; bm &= bm - 1, ++slot)
-                    dpos[kDynCap - kWave + slot] = (uint32_t)(64 * lane + __builtin_ctzll(bm));
+                    cidx[slot] = (uint32_t)(64 * lane + __builtin_ctzll(bm));
                 __builtin_amdgcn_wave_barrier();
                 uint32_t cg0 = 0, cg1 = 0;  // this lane's candidate gap [cg0, cg1)
                 if (lane < ncand) {
-                    const int i = (int)dpos[kDynCap - kWave + lane];
+                    const int i = (int)cidx[lane];
                     cg0 = i ? run_pmax(skeys[i - 1]) : 0u;
                     cg1 = run_start(skeys[i]);
                 }
@@ -678,7 +685,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 const int resume = n_marked > (uint32_t)kWave || words > kWave
                                        ? (n_marked >= (uint32_t)kWave
                                               ? (int)(uint32_t)__builtin_amdgcn_readlane(
-                                                    (int)dpos[kDynCap - 1], 0) + 1
+                                                    (int)cidx[kWave - 1], 0) + 1
                                               : 64 * kWave)
                                        : m;
                 // When every marked gap is a candidate and a lane is left, that
@@ -687,16 +694,27 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 const bool closed = resume == m && ncand < kWave;
                 const int nc = ncand + (closed ? 1 : 0), ktop = closed ? ncand : -1;
                 if (closed && lane == ncand) cg0 = m ? run_pmax(skeys[m - 1]) : 0u;
-                uint32_t lo_d = kUnplacedT, hi_d = 0;  // this lane's late range, empty until known
+                // this lane's late ranges (late predecessor lane + 64 r in
+                // slot r), empty until known
+                uint32_t lo_d[K], hi_d[K];
+#pragma unroll
+                for (int r = 0; r < K; ++r) {
+                    lo_d[r] = kUnplacedT;
+                    hi_d[r] = 0;
+                }
                 // lowest c' >= c with [c', c' + st) clear of every known late
                 // range: jump to the highest end among the (few) overlapping ones
                 auto past_late = [&](uint32_t c) {
                     while (true) {
-                        uint64_t ov = __ballot(lo_d < c + st && c < hi_d);
+                        uint32_t mx = 0;  // highest overlapping end of this lane (ends are > 0)
+#pragma unroll
+                        for (int r = 0; r < K; ++r)
+                            mx = (lo_d[r] < c + st && c < hi_d[r]) ? max(mx, hi_d[r]) : mx;
+                        uint64_t ov = __ballot(mx != 0);
                         if (!ov) return c;
                         uint32_t v = c;
                         for (; ov; ov &= ov - 1)
-                            v = max(v, (uint32_t)__builtin_amdgcn_readlane((int)hi_d, (int)__builtin_ctzll(ov)));
+                            v = max(v, (uint32_t)__builtin_amdgcn_readlane((int)mx, (int)__builtin_ctzll(ov)));
                         c = v;
                     }
                 };
@@ -720,29 +738,35 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 // raise the lowest fit, so the answer is kept up to date as
                 // they arrive: it moves (the walk resumes from it) only when
                 // a range that arrived overlaps it.
-                bool pend = lane < ndyn;
-                uint32_t p = 0, sp = 0;
-                if (pend) {
-                    p = dpos[lane];
-                    sp = a.su[p];
+                uint32_t pend = 0, p[K], sp[K];  // pend: bit r for slot r
+#pragma unroll
+                for (int r = 0; r < K; ++r) {
+                    const int d = lane + kWave * r;
+                    p[r] = d < ndyn ? dpos[d] : 0u;
+                    sp[r] = d < ndyn ? a.su[p[r]] : 0u;
+                    pend |= d < ndyn ? 1u << r : 0u;
                 }
                 bool ok = walk(0, 0u);
-                while (__ballot(pend)) {
-                    bool got = false;
-                    if (pend) {
-                        const uint32_t o = agent_load(a.off + p);
-                        if (o != kUnplacedT) {
-                            lo_d = o;
-                            hi_d = o + sp;
-                            pend = false;
+                while (__ballot(pend != 0)) {
+                    uint32_t o[K];
+#pragma unroll
+                    for (int r = 0; r < K; ++r) o[r] = (pend >> r) & 1u ? agent_load(a.off + p[r]) : kUnplacedT;
+                    bool got = false, hit = false;
+#pragma unroll
+                    for (int r = 0; r < K; ++r) {
+                        if (o[r] != kUnplacedT) {
+                            lo_d[r] = o[r];
+                            hi_d[r] = o[r] + sp[r];
+                            pend &= ~(1u << r);
                             got = true;
+                            hit = hit || (lo_d[r] < x + st && x < hi_d[r]);
                         }
                     }
                     if (!__ballot(got)) {
                         __builtin_amdgcn_s_sleep(1);
                         continue;
                     }
-                    if (ok && __ballot(got && lo_d < x + st && x < hi_d)) ok = walk(xk, x);
+                    if (ok && __ballot(hit)) ok = walk(xk, x);
                 }
                 // every late range is known
                 if (!ok) {  // past the candidates: the marked gaps after them, then the top
@@ -764,6 +788,11 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                     if (!found) x = past_late(m ? run_pmax(skeys[m - 1]) : 0u);
                 }
                 if (lane == 0) agent_store(a.off + qt, x);
+            };
+            if (wid == 0) {
+                if (ndyn <= kWave) wave0(std::integral_constant<int, 1>{});
+                else if (ndyn <= 4 * kWave) wave0(std::integral_constant<int, 4>{});
+                else wave0(std::integral_constant<int, 16>{});
             }
             __syncthreads();
             continue;
