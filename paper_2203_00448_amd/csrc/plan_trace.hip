@@ -192,15 +192,23 @@ __device__ __forceinline__ int32_t gallop_reach(const int32_t* f, int32_t q, int
 __global__ void t_reach_kernel(const int32_t* first, const int32_t* last, const int32_t* pf,
                                const int32_t* pl, const uint32_t* pid, int64_t n,
                                int32_t* __restrict__ reach, TFlags* fl) {
+    // band-length histogram by bit width: per workgroup in LDS, then one
+    // device atomic per nonzero bin (one per position would serialize on the
+    // few bins most bands fall in)
+    __shared__ uint32_t h[33];
     if (fl->abort) return;
+    if (threadIdx.x < 33) h[threadIdx.x] = 0u;
+    __syncthreads();
     const TView v = view(fl, first, last, pf, pl, pid);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
         const int32_t r = gallop_reach(v.first, (int32_t)q, (int32_t)n, v.last[q]);
         reach[q] = r;
         const uint32_t band = (uint32_t)(r - q - 1);
-        atomicAdd(&fl->hist[band ? 32 - __builtin_clz(band) : 0], 1u);
+        atomicAdd(&h[band ? 32 - __builtin_clz(band) : 0], 1u);
     }
+    __syncthreads();
+    if (threadIdx.x < 33 && h[threadIdx.x]) atomicAdd(&fl->hist[threadIdx.x], h[threadIdx.x]);
 }
 
 // threshold: smallest 2^b with at most kLongMax bands longer than it
