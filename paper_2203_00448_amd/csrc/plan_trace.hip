@@ -36,8 +36,12 @@ namespace {
 
 constexpr int kTBlock = 512;
 constexpr int kRunCap = 16384;    // ranges sorted at once in LDS
-constexpr int kDynCap = 1024;     // predecessors still unplaced when t is examined
-static_assert(kDynCap <= 16 * kWave, "wave 0 holds every late predecessor, 16 a lane at most");
+// Predecessors still unplaced when t is examined.  Each is held by another
+// running workgroup (ranks are taken in order, one at a time per
+// workgroup), so there are fewer than the grid; the host keeps the grid at
+// most kDynCap + 1.
+constexpr int kDynCap = 256;
+static_assert(kDynCap <= 4 * kWave, "wave 0 holds every late predecessor, 4 a lane at most");
 constexpr uint32_t kUnionMin = 256;  // placed predecessors merged through a bitmap beyond this
 constexpr int64_t kScratchRuns = 8;  // global scratch per workgroup: 8 sorted runs
 constexpr uint32_t kUnplacedT = 0xFFFFFFFFu;
@@ -490,7 +494,8 @@ struct PlaceArgs {
     const uint32_t* order;
     const int32_t* long_list;
     uint32_t* off;
-    uint64_t* run_keys;  // per workgroup: kScratchRuns * kRunCap
+    uint64_t* run_keys;  // per workgroup: stat_cap keys
+    int64_t stat_cap;    // min(n, kScratchRuns * kRunCap): a tensor has < n predecessors
     int64_t n;
     TFlags* fl;
     int32_t* status;
@@ -581,8 +586,8 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     __shared__ uint32_t s_rank, s_nstat, s_ndyn;
     if (a.fl->abort) return;
     const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
-    uint64_t* gkeys = a.run_keys + (int64_t)blockIdx.x * kScratchRuns * kRunCap;
-    const int64_t stat_cap = kScratchRuns * (int64_t)kRunCap;
+    uint64_t* gkeys = a.run_keys + (int64_t)blockIdx.x * a.stat_cap;
+    const int64_t stat_cap = a.stat_cap;
     while (true) {
         if (threadIdx.x == 0) {
             s_rank = atomicAdd(&a.fl->ticket, 1u);
@@ -603,6 +608,10 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                     dpos[d] = (uint32_t)p;
                     return;
                 }
+                // more late predecessors than other workgroups: the grid
+                // broke its bound.  Report it; waiting here keeps the result
+                // right and every workgroup finishing.
+                raise_status(a.status, MP_EDEVICE);
                 while ((o = agent_load(a.off + p)) == kUnplacedT) __builtin_amdgcn_s_sleep(2);
             }
             const uint32_t k = atomicAdd(&s_nstat, 1u);
@@ -647,7 +656,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         // Lowest fit with one run of placed predecessors: before waiting,
         // mark the run's gaps [prefix maximum below i, start of i) that hold
         // t.  Then wave 0 alone waits for the late ones (all of them: one to
-        // sixteen a lane, their ranges stay in registers) and walks the
+        // four a lane, their ranges stay in registers) and walks the
         // marked gaps in order, then the top: in a gap it moves past the
         // highest end among the late ranges overlapping [c, c + st) until
         // none does, and the first gap that still holds t gives the offset.
@@ -666,8 +675,8 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 if (lane == 0) gbits[w] = mk;
             }
             __syncthreads();
-            // wave 0; K late predecessors a lane (K = 1, 4 or 16 for up to
-            // 64, 256 or 1024 of them)
+            // wave 0; K late predecessors a lane (K = 1 or 4 for up to 64 or
+            // 256 of them)
             auto wave0 = [&](auto k_late) {
                 constexpr int K = decltype(k_late)::value;
                 // The first 64 marked gaps, in address order, one per lane
@@ -799,8 +808,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
             };
             if (wid == 0) {
                 if (ndyn <= kWave) wave0(std::integral_constant<int, 1>{});
-                else if (ndyn <= 4 * kWave) wave0(std::integral_constant<int, 4>{});
-                else wave0(std::integral_constant<int, 16>{});
+                else wave0(std::integral_constant<int, 4>{});
             }
             __syncthreads();
             continue;
@@ -863,19 +871,28 @@ struct TLayout {
     unsigned grid;
 };
 
+// Workgroups of the placement kernel on the current device: every resident
+// one (more would only wait for a CU), at most kDynCap + 1 so that a tensor
+// never has more late predecessors than wave 0 holds.  The launch needs no
+// co-residency -- a workgroup waits only on ranks taken earlier by running
+// workgroups -- so this is a plain launch sized for throughput.
 unsigned place_grid() {
-    static unsigned cached = 0;
-    if (cached) return cached;
     int dev = 0, cus = 0, per = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
         cus = 256;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, t_place_kernel<kTBlock>, kTBlock, 0) !=
             hipSuccess ||
         per < 1)
         per = 1;
-    cached = (unsigned)(cus * per);
-    return cached;
+    const int64_t g = (int64_t)cus * per;
+    return (unsigned)(g > kDynCap + 1 ? kDynCap + 1 : g);
+}
+
+int64_t stat_cap_of(int64_t n) {
+    const int64_t cap = kScratchRuns * (int64_t)kRunCap;
+    return n < cap ? n : cap;
 }
 
 TLayout t_layout(int64_t n, unsigned grid) {
@@ -902,7 +919,7 @@ TLayout t_layout(int64_t n, unsigned grid) {
     L.lflag = take(nn * 8);
     L.lpartial = take(scan_workspace_bytes(nn));
     L.llist = take(nn * 4);
-    L.run_keys = take((size_t)grid * kScratchRuns * kRunCap * 8);
+    L.run_keys = take((size_t)grid * (size_t)stat_cap_of(nn) * 8);
     L.total = o;
     L.grid = grid;
     return L;
@@ -977,14 +994,12 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
                  llist,
                  off,
                  reinterpret_cast<uint64_t*>(w + L.run_keys),
+                 stat_cap_of(n),
                  n,
                  fl,
                  status,
                  policy == MP_BEST_FIT ? 1 : 0};
-    void* kargs[] = {&pa};
-    e = hipLaunchCooperativeKernel((const void*)t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock),
-                                   kargs, 0, st);
-    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, pa);
     hipLaunchKernelGGL(t_output_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)off,
                        (const uint32_t*)su, (const uint32_t*)pid, n, offset_out, fl);
     hipLaunchKernelGGL(t_peak_kernel, dim3(1), dim3(1), 0, st, (const TFlags*)fl, peak_out);
