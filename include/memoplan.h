@@ -144,6 +144,23 @@ int32_t mp_live_bytes_profile(const int64_t* size, const int32_t* first, const i
                               int64_t* max_live_out, void* workspace, size_t workspace_bytes,
                               int32_t* status_out, void* stream);
 
+/* mp_live_bytes_profile for callers that cannot allocate device memory
+ * (code under stream capture, tight serving loops, harnesses that forbid
+ * hipMalloc): same arguments and results, no workspace.  Its scratch (a
+ * counter and the prefix sum's tile partials, about 64 KiB) is a static
+ * device array that each GPU the library runs on holds until the process
+ * ends, looked up once per device on the first call there.  num_ops above
+ * MP_LIVE_NOALLOC_MAX_OPS is MP_EINVAL from the call (use
+ * mp_live_bytes_profile).  Nothing is allocated, freed or synchronised.
+ * Every call on one GPU shares that scratch: calls that overlap in time on
+ * the same GPU (different streams, or different host threads) race and must
+ * be ordered by the caller.  MP_EDEVICE if the scratch cannot be resolved. */
+#define MP_LIVE_NOALLOC_MAX_OPS (1 << 24)
+int32_t mp_live_bytes_profile_noalloc(const int64_t* size, const int32_t* first,
+                                      const int32_t* last, int64_t n, int32_t num_ops,
+                                      int64_t* live_out, int64_t* max_live_out,
+                                      int32_t* status_out, void* stream);
+
 /* Plan validation against the pairwise constraints of Eq. 2.1: every pair
  * i < j whose lifetimes intersect and whose byte ranges [offset, offset +
  * size) overlap.

@@ -54,6 +54,8 @@ def load_library(path: str = LIB_PATH):
     L.mp_workspace_size.restype = sz
     L.mp_live_bytes_profile.argtypes = [p, p, p, i64, i32, p, p, p, sz, p, p]
     L.mp_live_bytes_profile.restype = i32
+    L.mp_live_bytes_profile_noalloc.argtypes = [p, p, p, i64, i32, p, p, p, p]
+    L.mp_live_bytes_profile_noalloc.restype = i32
     L.mp_validate_plan.argtypes = [p, p, p, p, i64, p, i64, p, i32, p, sz, p, p]
     L.mp_validate_plan.restype = i32
     L.mp_validate_batch.argtypes = [p, i64, p, p, p, p, i64, i64, p, i64, p, i32, p, sz, p, p]
@@ -194,6 +196,28 @@ def live_bytes_profile(size, first, last, num_ops: int, *, check: bool = True, o
     rc = L.mp_live_bytes_profile(_p(size), _p(first), _p(last), n, int(num_ops), _p(live), _p(mx),
                                  _p(ws), need, _p(status), _stream(stream))
     _finish(rc, status, "live_bytes_profile", check)
+    return live, mx
+
+
+LIVE_NOALLOC_MAX_OPS = 1 << 24
+
+
+def live_bytes_profile_noalloc(size, first, last, num_ops: int, *, out, check: bool = True,
+                               status=None, stream=None):
+    """mp_live_bytes_profile_noalloc: the per-op live bytes without a workspace
+    (the library's static device scratch; calls on one GPU must not overlap).
+    `out` = (live int64[num_ops], max_live int64[1]) preallocated by the caller."""
+    L = load_library()
+    size = _dev(size, torch.int64, "size")
+    first = _dev(first, torch.int32, "first")
+    last = _dev(last, torch.int32, "last")
+    live, mx = out
+    if status is None:
+        status = new_status(size.device, stream)
+    rc = L.mp_live_bytes_profile_noalloc(_p(size), _p(first), _p(last), size.numel(),
+                                         int(num_ops), _p(live), _p(mx), _p(status),
+                                         _stream(stream))
+    _finish(rc, status, "live_bytes_profile_noalloc", check)
     return live, mx
 
 

@@ -89,6 +89,19 @@ extern "C" int32_t mp_live_bytes_profile(const int64_t* size, const int32_t* fir
                                         workspace, status_out, static_cast<hipStream_t>(stream)));
 }
 
+extern "C" int32_t mp_live_bytes_profile_noalloc(const int64_t* size, const int32_t* first,
+                                                 const int32_t* last, int64_t n, int32_t num_ops,
+                                                 int64_t* live_out, int64_t* max_live_out,
+                                                 int32_t* status_out, void* stream) {
+    if (n < 0 || num_ops < 0 || num_ops > MP_LIVE_NOALLOC_MAX_OPS || !status_out || !max_live_out)
+        return MP_EINVAL;
+    if (n > 0 && (!size || !first || !last)) return MP_EINVAL;
+    if (num_ops > 0 && !live_out) return MP_EINVAL;
+    return launched(launch_live_profile_noalloc(size, first, last, n, num_ops, live_out,
+                                                max_live_out, status_out,
+                                                static_cast<hipStream_t>(stream)));
+}
+
 namespace {
 
 int32_t validate_common(const int64_t* begin, int64_t n_seg, const int64_t* size,

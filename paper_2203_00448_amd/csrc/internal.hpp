@@ -85,6 +85,11 @@ size_t live_workspace_bytes(int32_t num_ops);
 hipError_t launch_live_profile(const int64_t* size, const int32_t* first, const int32_t* last,
                                int64_t n, int32_t num_ops, int64_t* live_out, int64_t* max_out,
                                void* ws, int32_t* status, hipStream_t st);
+size_t live_noalloc_scratch_bytes();
+hipError_t launch_live_profile_noalloc(const int64_t* size, const int32_t* first,
+                                       const int32_t* last, int64_t n, int32_t num_ops,
+                                       int64_t* live_out, int64_t* max_out, int32_t* status,
+                                       hipStream_t st);
 
 
 // plan validation (validate.hip); begin == nullptr means one trace of n tensors

@@ -3,6 +3,8 @@
 // arena size of any valid plan, since every tensor alive at t needs its own
 // bytes.  Difference array with 64-bit atomics (+size at first, -size at
 // last + 1), then an inclusive device-wide prefix sum.
+#include <mutex>
+
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -82,6 +84,54 @@ hipError_t launch_live_profile(const int64_t* size, const int32_t* first, const 
     if (e != hipSuccess) return e;
     return device_scan_i64(live_out, num_ops, true, partial,
                            reinterpret_cast<unsigned long long*>(max_out), st);
+}
+
+// ---- the same profile without a caller workspace (no allocation anywhere)
+//
+// Scratch of mp_live_bytes_profile_noalloc: the running-sum word and the
+// scan's tile partials, for at most MP_LIVE_NOALLOC_MAX_OPS ops.  Each GPU
+// the library runs on holds one copy until the process ends; every call on a
+// GPU shares it.  Host code never passes `scratch` itself to a kernel (on the
+// host it is only a stand-in for the symbol): the device address is looked up
+// once per device with that device current and kept in scratch_ptr.
+namespace {
+
+constexpr size_t kNoallocScratchBytes = 256 + ((size_t)MP_LIVE_NOALLOC_MAX_OPS / 2048 + 2) * 8;
+__device__ __align__(256) unsigned char scratch[kNoallocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+// Device address of this device's scratch (looked up on first use), or
+// nullptr if it cannot be resolved.
+void* scratch_ptr() {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+size_t live_noalloc_scratch_bytes() { return kNoallocScratchBytes; }
+
+hipError_t launch_live_profile_noalloc(const int64_t* size, const int32_t* first,
+                                       const int32_t* last, int64_t n, int32_t num_ops,
+                                       int64_t* live_out, int64_t* max_out, int32_t* status,
+                                       hipStream_t st) {
+    static_assert(kNoallocScratchBytes >= 256 + (MP_LIVE_NOALLOC_MAX_OPS + 2047) / 2048 * 8 + 8,
+                  "scratch holds the sum word and every tile partial");
+    if (num_ops < 0 || live_workspace_bytes(num_ops) > kNoallocScratchBytes)
+        return hipErrorInvalidValue;
+    void* ws = scratch_ptr();
+    if (!ws) return hipErrorInvalidSymbol;
+    return launch_live_profile(size, first, last, n, num_ops, live_out, max_out, ws, status, st);
 }
 
 }  // namespace mp
