@@ -68,27 +68,31 @@ const char* mp_status_string(int32_t status);
 int32_t mp_status_reset(int32_t* status_out, void* stream);
 
 /* Greedy-by-size plans for many independent traces in one launch (one
- * workgroup per trace, the trace held in LDS).
+ * workgroup per trace).
  *   begin[n_traces + 1] int64: trace b owns tensors [begin[b], begin[b+1]) of
  *                        the concatenated arrays; 0 <= begin[b] <= begin[b+1]
  *                        <= n_tensors (checked on device, MP_EINVAL).
  *   num_ops[n_traces]  int32: op count of each trace (lifetimes < num_ops[b]).
  *   size, first, last  [n_tensors] (int64, int32, int32).
- *   max_trace_len      host bound on begin[b+1] - begin[b], 0..4096; a longer
- *                      trace sets MP_EINVAL.
- *   policy             MP_LOWEST_FIT or MP_BEST_FIT (a tensor may then meet at
- *                      most 256 others in lifetime: MP_ENOSPC on device beyond).
+ *   n_tensors          length of the concatenated arrays (bounds check of begin).
+ *   max_trace_len      host bound on begin[b+1] - begin[b], 0..4096: sizes the
+ *                      per-workgroup LDS without reading begin on the host; a
+ *                      longer trace sets MP_EINVAL (plan it with mp_plan_trace).
+ *   policy             MP_LOWEST_FIT or MP_BEST_FIT.
  *   offset_out[n_tensors] int64, peak_out[n_traces] int64 (arena bytes),
  *   lb_out[n_traces]   int64 or NULL: max over ops of the live bytes, a lower
  *                      bound on any valid arena size.
- *   workspace          device memory of mp_workspace_size(MP_OP_PLAN_BATCH, 0,
- *                      n_traces, max_trace_len) bytes (each trace's lists of
- *                      lifetime-intersecting pairs); contents need no
+ *   workspace          device memory of mp_workspace_bytes(MP_OP_PLAN_BATCH,
+ *                      n_tensors, 0, n_traces) bytes; contents need no
  *                      initialisation; not used after the call completes.
- * Capacity limits (MP_ENOSPC on device): per trace, sum of sizes divided by
- * 2^ctz(OR of sizes) must be < 2^32, and the number of lifetime-intersecting
- * tensor pairs must not exceed mp_batch_pair_capacity(max_trace_len).  Use
- * mp_plan_trace beyond them. */
+ * Every valid trace is planned.  A trace is held in LDS (its intersecting
+ * pairs as one-byte list entries) when its sizes sum to less than 2^31 units
+ * of 2^ctz(OR of sizes), its pairs fit mp_batch_pair_capacity(max_trace_len)
+ * and at most 32 of its tensors meet a tensor born more than 223 positions
+ * later (and, under BEST_FIT, no tensor meets more than 256 others);
+ * otherwise the same workgroup plans it on a general path (64-bit offsets,
+ * working lists in the workspace, O(n^2) work per trace), with the same
+ * results. */
 int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num_ops,
                       const int64_t* size, const int32_t* first, const int32_t* last,
                       int64_t n_tensors, int64_t max_trace_len, int32_t policy,
@@ -96,9 +100,9 @@ int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num
                       void* workspace, size_t workspace_bytes, int32_t* status_out,
                       void* stream);
 
-/* Pair-list capacity per trace of mp_plan_batch for a given max_trace_len
- * (host query, no device work): every pair of such a trace, at most 64 per
- * tensor and at most 65520; -1 when max_trace_len is out of range. */
+/* Intersecting pairs per trace that mp_plan_batch holds in LDS for a given
+ * max_trace_len (host query, no device work); a trace with more takes the
+ * general path.  -1 when max_trace_len is out of range. */
 int64_t mp_batch_pair_capacity(int64_t max_trace_len);
 
 /* Greedy-by-size plan of one trace of any length, using the whole device
@@ -117,14 +121,15 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
                       void* workspace, size_t workspace_bytes, int32_t* status_out,
                       void* stream);
 
-/* Workspace sizes (host query).  op: MP_OP_LIVE_BYTES (uses num_ops),
- * MP_OP_VALIDATE (uses n_tensors and capacity), MP_OP_PLAN_TRACE (uses
- * n_tensors and num_ops), MP_OP_VALIDATE_BATCH (uses n_tensors, capacity and
- * the number of traces passed as num_ops), MP_OP_PLAN_BATCH (the number of
- * traces passed as num_ops, max_trace_len as capacity), MP_OP_PROBE (uses
- * n_tensors, num_ops and capacity, the number of lane events to hold; 0 asks
- * for 16 n_tensors + 65536), MP_OP_BUMP (uses n_tensors).  Returns 0 for an
- * unknown op or out-of-range sizes. */
+/* Workspace bytes of the call selected by `op` (host query, no device
+ * work), from the number of tensors, the largest op count and the number of
+ * traces: MP_OP_PLAN_BATCH (n_tensors, n_traces), MP_OP_PLAN_TRACE
+ * (n_tensors), MP_OP_LIVE_BYTES (max_num_ops), MP_OP_VALIDATE (n_tensors; a
+ * pairs_out capacity of at most n_tensors), MP_OP_VALIDATE_BATCH (n_tensors,
+ * n_traces; capacity at most n_tensors), MP_OP_PROBE (n_tensors,
+ * max_num_ops; the default capacity), MP_OP_BUMP (n_tensors).  The
+ * single-trace planner's size depends on the current device (its CU count).
+ * Returns 0 for an unknown op or out-of-range sizes. */
 #define MP_OP_LIVE_BYTES 1
 #define MP_OP_VALIDATE 2
 #define MP_OP_PLAN_TRACE 3
@@ -132,6 +137,16 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
 #define MP_OP_PLAN_BATCH 5
 #define MP_OP_PROBE 6
 #define MP_OP_BUMP 7
+size_t mp_workspace_bytes(int32_t op, int64_t n_tensors, int64_t max_num_ops, int64_t n_traces);
+
+/* The same sizes with the output capacity explicit: MP_OP_LIVE_BYTES (uses
+ * num_ops), MP_OP_VALIDATE (uses n_tensors and capacity, the pairs_out
+ * capacity), MP_OP_PLAN_TRACE (uses n_tensors), MP_OP_VALIDATE_BATCH (uses
+ * n_tensors, capacity and the number of traces passed as num_ops),
+ * MP_OP_PLAN_BATCH (n_tensors and the number of traces passed as num_ops),
+ * MP_OP_PROBE (uses n_tensors, num_ops and capacity, the number of lane
+ * events to hold; 0 asks for 16 n_tensors + 65536), MP_OP_BUMP (uses
+ * n_tensors).  Returns 0 for an unknown op or out-of-range sizes. */
 size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops, int64_t capacity);
 
 /* Per-op live bytes of one trace (the quantity whose maximum lower-bounds

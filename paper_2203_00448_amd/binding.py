@@ -52,6 +52,8 @@ def load_library(path: str = LIB_PATH):
     L.mp_plan_batch.restype = i32
     L.mp_workspace_size.argtypes = [i32, i64, i64, i64]
     L.mp_workspace_size.restype = sz
+    L.mp_workspace_bytes.argtypes = [i32, i64, i64, i64]
+    L.mp_workspace_bytes.restype = sz
     L.mp_live_bytes_profile.argtypes = [p, p, p, i64, i32, p, p, p, sz, p, p]
     L.mp_live_bytes_profile.restype = i32
     L.mp_live_bytes_profile_noalloc.argtypes = [p, p, p, i64, i32, p, p, p, p]
@@ -153,7 +155,7 @@ def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None =
         offset, peak, lb = out
     if status is None:
         status = new_status(dev, stream)
-    ws, need = _workspace(OP_PLAN_BATCH, dev, 0, n_traces, max_trace_len, workspace)
+    ws, need = _workspace(OP_PLAN_BATCH, dev, n, n_traces, 0, workspace)
     rc = L.mp_plan_batch(_p(begin), n_traces, _p(num_ops), _p(size), _p(first), _p(last), n,
                          int(max_trace_len), int(policy), _p(offset), _p(peak), _p(lb),
                          _p(ws), need, _p(status), _stream(stream))
@@ -162,8 +164,18 @@ def plan_batch(begin, num_ops, size, first, last, *, max_trace_len: int | None =
 
 
 def workspace_size(op: int, n_tensors: int = 0, num_ops: int = 0, capacity: int = 0) -> int:
+    """mp_workspace_size: bytes of workspace for `op`; for MP_OP_PLAN_BATCH
+    num_ops carries the number of traces, for the validation and probe ops
+    capacity the output capacity."""
     return int(load_library().mp_workspace_size(int(op), int(n_tensors), int(num_ops),
                                                  int(capacity)))
+
+
+def workspace_bytes(op: int, n_tensors: int = 0, max_num_ops: int = 0, n_traces: int = 1) -> int:
+    """mp_workspace_bytes: bytes of workspace for `op` from the tensor count,
+    the largest op count and the number of traces."""
+    return int(load_library().mp_workspace_bytes(int(op), int(n_tensors), int(max_num_ops),
+                                                  int(n_traces)))
 
 
 def _workspace(op, dev, n_tensors=0, num_ops=0, capacity=0, workspace=None):

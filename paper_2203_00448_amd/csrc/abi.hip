@@ -43,7 +43,7 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
     if (!begin) return MP_EINVAL;
     if (n_traces > 0 && (!num_ops || !peak_out || !workspace)) return MP_EINVAL;
     if (n_tensors > 0 && (!size || !first || !last || !offset_out)) return MP_EINVAL;
-    if (workspace_bytes < plan_batch_workspace_bytes(n_traces, max_trace_len)) return MP_EINVAL;
+    if (workspace_bytes < plan_batch_workspace_bytes(n_tensors, n_traces)) return MP_EINVAL;
     hipStream_t st = static_cast<hipStream_t>(stream);
     if (n_traces == 0) return MP_OK;
     BatchArgs a{begin,      n_traces,      num_ops,    size,     first,  last,       n_tensors,
@@ -60,7 +60,7 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
         case MP_OP_VALIDATE:
             return validate_workspace_bytes(n_tensors, capacity, 1);
         case MP_OP_PLAN_BATCH:
-            return num_ops > INT32_MAX ? 0 : plan_batch_workspace_bytes(num_ops, capacity);
+            return num_ops > INT32_MAX ? 0 : plan_batch_workspace_bytes(n_tensors, num_ops);
         case MP_OP_VALIDATE_BATCH:
             return num_ops > INT32_MAX ? 0 : validate_workspace_bytes(n_tensors, capacity, num_ops);
         case MP_OP_PLAN_TRACE:
@@ -71,6 +71,31 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
             return num_ops > INT32_MAX ? 0
                                        : probe_workspace_bytes(n_tensors, (int32_t)num_ops,
                                                                capacity);
+        default:
+            return 0;
+    }
+}
+
+extern "C" size_t mp_workspace_bytes(int32_t op, int64_t n_tensors, int64_t max_num_ops,
+                                     int64_t n_traces) {
+    if (n_tensors < 0 || max_num_ops < 0 || max_num_ops > INT32_MAX || n_traces < 0 ||
+        n_traces > INT32_MAX)
+        return 0;
+    switch (op) {
+        case MP_OP_LIVE_BYTES:
+            return live_workspace_bytes((int32_t)max_num_ops);
+        case MP_OP_VALIDATE:
+            return validate_workspace_bytes(n_tensors, n_tensors, 1);
+        case MP_OP_VALIDATE_BATCH:
+            return validate_workspace_bytes(n_tensors, n_tensors, n_traces > 0 ? n_traces : 1);
+        case MP_OP_PLAN_TRACE:
+            return n_tensors >= (int64_t)1 << 30 ? 0 : plan_trace_workspace_bytes(n_tensors);
+        case MP_OP_PLAN_BATCH:
+            return plan_batch_workspace_bytes(n_tensors, n_traces);
+        case MP_OP_BUMP:
+            return bump_workspace_bytes(n_tensors);
+        case MP_OP_PROBE:
+            return probe_workspace_bytes(n_tensors, (int32_t)max_num_ops, 0);
         default:
             return 0;
     }

@@ -22,20 +22,20 @@ struct BatchArgs {
     int64_t* peak_out;
     int64_t* lb_out;
     int32_t* status;
-    void* workspace;  // left lists: plan_batch_workspace_bytes
+    void* workspace;  // plan_batch_workspace_bytes(n_tensors, n_traces)
     int32_t policy;   // MP_LOWEST_FIT or MP_BEST_FIT
 };
 
 struct BatchShape {
     bool ok;
     int32_t cap_n;      // tensor slots per workgroup
-    int32_t cap_pairs;  // left-list slots per trace
+    int32_t cap_pairs;  // left-list entries (one byte each) per trace in LDS
     int32_t items;      // tensor slots per thread
     size_t lds_bytes;   // dynamic LDS per workgroup
 };
 
 BatchShape batch_shape(int64_t max_trace_len);
-size_t plan_batch_workspace_bytes(int64_t n_traces, int64_t max_trace_len);
+size_t plan_batch_workspace_bytes(int64_t n_tensors, int64_t n_traces);
 hipError_t launch_reset_status(int32_t* status, hipStream_t st);
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st);
 

@@ -13,16 +13,24 @@
 // pair intersects iff first[q'] <= last[q], so tensor q meets exactly the
 // positions (q, reach[q]) to its right, reach[q] = upper_bound(first,
 // last[q]), and the positions to its left whose reach passes q (its "left
-// list").  For an intersecting pair q < q', q ranks first iff size[q] >=
-// size[q'] (equal sizes are ordered by first then id, which is position
-// order).
+// list", stored as one byte per entry: the distance back, or the slot of one
+// of a few long-lived tensors).  For an intersecting pair q < q', q ranks
+// first iff size[q] >= size[q'] (equal sizes are ordered by first then id,
+// which is position order).
 //
 // Phases (one workgroup of 512 threads):
 //   ingest + checks -> position order -> reach, band lengths, live-bytes
-//   deltas, reach histogram -> one prefix pass (band starts, left-list starts,
-//   live-bytes maximum) -> left-list fill and predecessor counts -> placement
-//   in rounds (a tensor is fitted in the round after its last predecessor)
-//   -> outputs.
+//   deltas, reach histogram, long tensors -> one prefix pass (band starts,
+//   left-list starts, live-bytes maximum, largest neighbour count) ->
+//   left-list fill and predecessor counts -> placement words -> placement in
+//   rounds (a tensor is fitted in the round after its last predecessor) ->
+//   outputs.
+// A trace the LDS path cannot hold -- sizes summing to 2^31 units or more,
+// more intersecting pairs than the LDS list capacity, more than 32 long
+// tensors, or under BEST_FIT a tensor meeting more than 256 others -- is
+// planned by the same workgroup on the general path (plan_general): the
+// greedy taken literally, one tensor at a time in rank order, 64-bit offsets,
+// its working lists in the workspace.  No valid trace is refused.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -33,8 +41,6 @@ namespace mp {
 constexpr int kPhaseSlots = 8;
 __device__ long long g_phase_clock[4096 * kPhaseSlots];
 __device__ unsigned int g_dbg[4096 * 8];
-#define MP_DBG_MAX(slot, v) \
-    do { if (blockIdx.x < 4096) atomicMax(&g_dbg[blockIdx.x * 8 + (slot)], (unsigned)(v)); } while (0)
 #define MP_DBG_ADD(slot, v) \
     do { if (blockIdx.x < 4096) atomicAdd(&g_dbg[blockIdx.x * 8 + (slot)], (unsigned)(v)); } while (0)
 #define MP_STAMP(slot)                                                              \
@@ -44,7 +50,6 @@ __device__ unsigned int g_dbg[4096 * 8];
     } while (0)
 #else
 #define MP_STAMP(slot) do { } while (0)
-#define MP_DBG_MAX(slot, v) do { } while (0)
 #define MP_DBG_ADD(slot, v) do { } while (0)
 #endif
 
@@ -56,19 +61,30 @@ constexpr uint32_t kQuadK = 16;            // ... by a lane quad
 constexpr uint32_t kMidK = 64;             // ... by a 16-lane row; more: by the whole wave
 constexpr int kSlots = 4;                  // neighbours per lane in pairs, quads, rows, waves
 constexpr uint32_t kCoopChunk = 64u * kSlots;
-constexpr int kClassShift = 30;            // pending count: ready class in bits 30-31
-constexpr uint32_t kCountMask = (1u << kClassShift) - 1;
-constexpr uint32_t kLeftSucc = 0x8000u;    // left-list entry flag: ranks after the list's owner
+constexpr uint32_t kBestMaxK = 4u * kWave; // BEST_FIT on the LDS path: one wave sorts them all
+
+// A tensor's LDS placement word: size (units) in the low half; the high half
+// is the offset (units, below 2^31) once placed, and before that bit 31 set,
+// the ready class in bits 29-30 and the number of unplaced predecessors in
+// bits 0-28.  An unplaced word never overlaps a candidate range: every
+// candidate end stays below 2^31 units because the trace's sizes sum to less.
+constexpr uint32_t kUnplacedBit = 0x80000000u;
+constexpr uint32_t kClassShift = 29;
+constexpr uint32_t kPendMask = (1u << kClassShift) - 1;
+constexpr uint64_t kFastMaxUnits = 0x7FFFFFFFull;
+
+// Left-list entries (one byte): 1 .. kMaxDist is the distance back to the
+// neighbour's position; kLongBase + s names long tensor s (a tensor whose
+// band reaches further than kMaxDist), whose position is in a small table.
+constexpr uint32_t kLongSlots = 32;
+constexpr uint32_t kLongBase = 256 - kLongSlots;
+constexpr uint32_t kMaxDist = kLongBase - 1;
 
 // Ready class of a tensor with K neighbours: 0 pair, 1 quad, 2 row or wave.
 __device__ __forceinline__ uint32_t ready_class(uint32_t K) {
     return K <= kPairK ? 0u : (K <= kQuadK ? 1u : 2u);
 }
 
-// A tensor's LDS word: offset (units) in the high half, size (units) in the
-// low half; the offset half is kUnplaced until the tensor is placed.  An
-// unplaced word never overlaps a candidate range: offsets stay below
-// 0xFFFFFFFF because the sizes of a trace sum to at most 0xFFFFFFFE units.
 __device__ __forceinline__ uint32_t word_off(uint64_t w) { return (uint32_t)(w >> 32); }
 __device__ __forceinline__ uint32_t word_end(uint64_t w) {
     return (uint32_t)(w >> 32) + (uint32_t)w;
@@ -85,23 +101,33 @@ __device__ __forceinline__ uint32_t packed_add(uint32_t* w, uint32_t i, uint32_t
     return (atomicAdd(w + (i >> 1), v << half_shift(i)) >> half_shift(i)) & 0xFFFFu;
 }
 
+// The trace's left lists and long-tensor table, as the placement reads them.
+struct LeftLists {
+    const uint8_t* ent;       // entries, tensor q's at [lbeg[q], lbeg[q + 1])
+    const uint16_t* longtab;  // positions of the long tensors
+};
+
+// Position of the left neighbour named by entry lv of tensor q's list.
+__device__ __forceinline__ uint32_t left_pos(uint32_t q, uint32_t lv, const LeftLists& ll) {
+    return lv >= kLongBase ? (uint32_t)ll.longtab[lv - kLongBase] : q - lv;
+}
+
 // Neighbour k of tensor q in its neighbour sequence: the left list first
-// (k < L; entry lv = position | kLeftSucc when it ranks after q), then the
-// right band q + 1 .. q + R, whose members rank after q iff their size is
-// at most q's (equal sizes rank by position).  Slots past the end (k >= K)
-// map to q itself, which is unplaced and never a successor.
-// Both are computed without branches (masks instead of selects that the
-// compiler would turn into divergent blocks around the list load).
+// (k < L; pl = its position), then the right band q + 1 .. q + R.  Slots
+// past the end (k >= K) map to q itself, which is unplaced and never a
+// successor.  Branch-free (masks instead of selects that the compiler would
+// turn into divergent blocks around the list load).
 __device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
-                                              uint32_t lv) {
+                                              uint32_t pl) {
     const uint32_t in_left = 0u - (uint32_t)(k < L), in_band = 0u - (uint32_t)(k < K);
     const uint32_t right = q + ((k + 1 - L) & in_band);
-    return ((lv & 0x0FFFu) & in_left) | (right & ~in_left);
+    return (pl & in_left) | (right & ~in_left);
 }
-__device__ __forceinline__ bool is_successor(uint32_t k, uint32_t L, uint32_t lv,
-                                             uint32_t s_other, uint32_t s) {
-    const uint32_t left_succ = (lv >> 15) & 1u, band_succ = (uint32_t)(s_other <= s);
-    return ((k < L) ? left_succ : band_succ) != 0u;
+// Does neighbour k rank after q?  A left neighbour (smaller position) does
+// iff it is strictly smaller; a right one iff it is not larger.
+__device__ __forceinline__ bool is_successor(uint32_t k, uint32_t L, uint32_t s_other,
+                                             uint32_t s) {
+    return (k < L) ? (s_other < s) : (s_other <= s);
 }
 
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
@@ -117,13 +143,6 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// Maximum over each quad of lanes (4g .. 4g+3), returned to all four:
-// quad permutations swap lanes 1 apart, then 2 apart.
-__device__ __forceinline__ uint32_t quad_max_u32(uint32_t v) {
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
-    return v;
-}
 // Maximum over each row of 16 lanes, returned to all of them: rotations by
 // 8, 4, 2 and 1 within the row.
 __device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
@@ -139,17 +158,6 @@ __device__ __forceinline__ uint32_t pair_quad_max_u32(uint32_t v, bool quad) {
     v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
     const uint32_t v4 = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
     return quad ? v4 : v;
-}
-// Lane 0 of each quad / of each row, to every lane of it.
-__device__ __forceinline__ uint32_t quad_first(uint32_t v) {
-    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x00, 0xF, 0xF, false);
-}
-__device__ __forceinline__ uint32_t row_first(uint32_t v, int lane) {
-    const uint32_t r0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
-    const uint32_t r1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
-    const uint32_t r2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
-    const uint32_t r3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
-    return lane < 32 ? (lane < 16 ? r0 : r1) : (lane < 48 ? r2 : r3);
 }
 
 template <int BLOCK>
@@ -171,7 +179,6 @@ __device__ void bitonic_sort_u64(uint64_t* keys, int m) {
         }
     }
 }
-
 
 // The ready lists of the three classes share one array of N slots: class
 // c owns the region [region[c], region[c] + number of class-c tensors), as
@@ -198,12 +205,13 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum_dpp(uint32_t v) {
 
 // Decrement the pending counts of the successors among M (<= 4) gathered
 // neighbours (dec[j] is 1 for a successor, else 0: the atomics then issue
-// back to back) and append those that reach zero to their class list: one
-// wave scan of the per-lane counts (10-bit fields, one per class) and one
-// list reservation per wave.  All 64 lanes must be active.
+// back to back; subtracting 0 from a word changes nothing) and append those
+// that reach zero to their class list: one wave scan of the per-lane counts
+// (10-bit fields, one per class) and one list reservation per wave.  All 64
+// lanes must be active.
 template <int M>
 __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
-                                                   const uint32_t (&ids)[M], uint32_t* rem,
+                                                   const uint32_t (&ids)[M], uint64_t* ofsz,
                                                    const ReadyLists& rl, int lane) {
     static_assert(M <= 4, "a lane releases at most 4 tensors");
     uint32_t old[M], any_dec = 0;
@@ -214,13 +222,15 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
     }
     if (any_dec) {
 #pragma unroll
-        for (int j = 0; j < M; ++j) old[j] = atomicSub(rem + ids[j], dec[j]);
+        for (int j = 0; j < M; ++j)
+            old[j] = (uint32_t)(atomicSub(reinterpret_cast<unsigned long long*>(ofsz + ids[j]),
+                                          (unsigned long long)dec[j] << 32) >> 32);
     }
     uint32_t packed = 0;  // ready tensors of this lane, 10 bits per class
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-        const bool r = dec[j] && (old[j] & kCountMask) == 1u;
-        packed += r ? 1u << (10 * (old[j] >> kClassShift)) : 0u;
+        const bool r = dec[j] && (old[j] & kPendMask) == 1u;
+        packed += r ? 1u << (10 * ((old[j] >> kClassShift) & 3u)) : 0u;
     }
     if (!__ballot(packed != 0)) return;
     const uint32_t incl = wave_inclusive_sum_dpp(packed);
@@ -240,8 +250,8 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
                       rl.end[2] + (bhi & 0xFFFFu) + (pre >> 20)};
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-        if (dec[j] && (old[j] & kCountMask) == 1u) {
-            const uint32_t c = old[j] >> kClassShift;
+        if (dec[j] && (old[j] & kPendMask) == 1u) {
+            const uint32_t c = (old[j] >> kClassShift) & 3u;
             const uint32_t k = c == 0 ? at[0]++ : (c == 1 ? at[1]++ : at[2]++);
             rl.slot[k] = (uint16_t)ids[j];
         }
@@ -256,8 +266,9 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
 // group sorts them by offset (bitonic network: slots within a lane, lanes by
 // exchanges with lane l ^ d), takes running maxima of the ends in that order
 // (gap before element i: [max end of elements < i, offset of i)) and a
-// minimum over (gap length, gap start).  Unplaced ranges (offset kUnplaced)
-// sort last and bound no gap.  Every lane of the group gets the result.
+// minimum over (gap length, gap start).  Unplaced ranges (bit 31 of the
+// offset half set) sort last and bound no gap.  Every lane of the group gets
+// the result.
 template <int LANES>
 __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots], uint32_t s,
                                    uint32_t l) {
@@ -301,7 +312,7 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
     uint32_t incl[4], run = 0;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-        run = max(run, o[r] != kUnplaced ? e[r] : 0u);
+        run = max(run, o[r] < kUnplacedBit ? e[r] : 0u);
         incl[r] = run;
     }
     uint32_t scan = run;
@@ -317,7 +328,7 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const uint32_t pm = r == 0 ? before : max(before, incl[r - 1]);
-        const bool ok = o[r] != kUnplaced && o[r] >= pm && o[r] - pm >= s;
+        const bool ok = o[r] < kUnplacedBit && o[r] >= pm && o[r] - pm >= s;
         const uint64_t key = ((uint64_t)(o[r] - pm) << 32) | pm;
         best = (ok && key < best) ? key : best;
     }
@@ -336,23 +347,25 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
 // neighbours; within a chunk the candidate offset jumps to the highest end
 // overlapping [x, x + s) until nothing in the chunk overlaps, and chunks are
 // revisited until a full lap leaves x alone.  Then q is published and its
-// successors' pending counts are decremented.
+// successors' pending counts are decremented.  BEST_FIT tensors reach here
+// with at most 256 neighbours (more go to the general path): one chunk,
+// sorted by the wave.
 __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint32_t K,
-                           uint64_t* ofsz, const uint16_t* lst, uint32_t* rem,
-                           const ReadyLists& rl, int lane, bool best, int32_t* status) {
+                           uint64_t* ofsz, const LeftLists& ll, const ReadyLists& rl, int lane,
+                           bool best) {
     const uint32_t nch = (K + kCoopChunk - 1) / kCoopChunk;
     uint32_t id[kSlots], co[kSlots], ce[kSlots], sc[kSlots];
     auto load = [&](uint32_t kb) {
-        uint32_t lv[kSlots];
+        uint32_t pl[kSlots];
 #pragma unroll
         for (int r = 0; r < kSlots; ++r) {
             const uint32_t k = kb + r * kWave + lane;
-            lv[r] = lst[k < L ? lb + k : lb];  // in bounds: the lists are padded
+            pl[r] = left_pos(q, ll.ent[k < L ? lb + k : lb], ll);  // in bounds: padded
         }
         uint64_t w[kSlots];
 #pragma unroll
         for (int r = 0; r < kSlots; ++r) {
-            id[r] = neighbour(kb + r * kWave + lane, L, K, q, lv[r]);
+            id[r] = neighbour(kb + r * kWave + lane, L, K, q, pl[r]);
             w[r] = ofsz[id[r]];
         }
 #pragma unroll
@@ -360,17 +373,13 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
             const uint32_t k = kb + r * kWave + lane;
             co[r] = word_off(w[r]);
             ce[r] = word_end(w[r]);
-            sc[r] = (k < K && is_successor(k, L, lv[r], (uint32_t)w[r], s)) ? 1u : 0u;
+            sc[r] = (k < K && is_successor(k, L, (uint32_t)w[r], s)) ? 1u : 0u;
         }
     };
     uint32_t x = 0, clean = best ? nch : 0, c = 0;
-    if (best) {  // one chunk of at most 256 neighbours, sorted by the wave
-        if (nch > 1) {
-            if (lane == 0) raise_status(status, MP_ENOSPC);
-        } else {
-            load(0);
-            x = best_fit_group<kWave>(co, ce, s, (uint32_t)lane);
-        }
+    if (best) {
+        load(0);
+        x = best_fit_group<kWave>(co, ce, s, (uint32_t)lane);
     }
     while (clean < nch) {
         load(c * kCoopChunk);
@@ -395,7 +404,7 @@ __device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint
     if (lane == 0) ofsz[q] = ((uint64_t)x << 32) | s;
     for (uint32_t cc = 0; cc < nch; ++cc) {
         if (nch > 1) load(cc * kCoopChunk);
-        release_successors(sc, id, rem, rl, lane);
+        release_successors(sc, id, ofsz, rl, lane);
     }
 }
 
@@ -425,9 +434,9 @@ __device__ __forceinline__ Item load_item(uint32_t q, bool has, uint32_t spare,
 // The neighbours k = 4g + r (r < kSlots) of a group's tensor, for the lane
 // at position g of its group: positions, ranges [o, e) and successor flags.
 // Slots past the neighbour count read the tensor's own word, which is
-// unplaced: an unplaced word never overlaps (its offset half is kUnplaced).
+// unplaced: an unplaced word never overlaps.
 __device__ __forceinline__ void gather_group(const Item& it, uint32_t g, const uint64_t* ofsz,
-                                             const uint16_t* lst, uint32_t (&id)[kSlots],
+                                             const LeftLists& ll, uint32_t (&id)[kSlots],
                                              uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
                                              uint32_t (&sc)[kSlots]) {
     const uint32_t k0 = g * kSlots;
@@ -435,12 +444,12 @@ __device__ __forceinline__ void gather_group(const Item& it, uint32_t g, const u
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
         const uint32_t k = k0 + r;
-        lv[r] = lst[k < it.L ? it.lb + k : it.lb];  // in bounds: the lists are padded
+        lv[r] = ll.ent[k < it.L ? it.lb + k : it.lb];  // in bounds: the lists are padded
     }
     uint64_t w[kSlots];
 #pragma unroll
     for (int r = 0; r < kSlots; ++r) {
-        id[r] = neighbour(k0 + r, it.L, it.K, it.q, lv[r]);
+        id[r] = neighbour(k0 + r, it.L, it.K, it.q, left_pos(it.q, lv[r], ll));
         w[r] = ofsz[id[r]];
     }
 #pragma unroll
@@ -448,7 +457,7 @@ __device__ __forceinline__ void gather_group(const Item& it, uint32_t g, const u
         const uint32_t k = k0 + r;
         o[r] = word_off(w[r]);
         e[r] = word_end(w[r]);
-        sc[r] = (k < it.K && is_successor(k, it.L, lv[r], (uint32_t)w[r], it.s)) ? 1u : 0u;
+        sc[r] = (k < it.K && is_successor(k, it.L, (uint32_t)w[r], it.s)) ? 1u : 0u;
     }
 }
 
@@ -462,29 +471,252 @@ __device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[kSlots],
     return m;
 }
 
-// LDS byte offsets of the regions (N = tensor slots):
-//   A [8N+8]   first[N] (i32) and live-bytes deltas[N+1] (u32, upper half)
-//              -> placement words ofsz[N]
-//   B [2N+4]   band lengths -> band starts (u16)  -> ready lists (u16)
-//   C [2N+4]   left-list fill cursors (packed u16)
-//   D [4N+4]   reach histogram (packed u16)       -> pending predecessor counts (u32)
-//   E [2N+4]   left-list starts (u16)
+// ------------------------------------------------------------ general path
+
+// Loads of data other threads of the workgroup stored to global memory
+// before the last l2_barrier (relaxed agent-scope atomics: served by L2,
+// never by a stale line of the CU's vector cache).
+__device__ __forceinline__ uint64_t l2_load64(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint32_t l2_load32(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Barrier after which every thread's global stores of the workgroup are
+// complete (the workgroup barrier alone does not wait for them).
+__device__ __forceinline__ void l2_barrier() {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+}
+
+// Running maximum over the workgroup in thread order: the maximum of the
+// values of the threads before this one (0 for thread 0); *all gets the
+// maximum over every thread.  Two barriers.
+template <int BLOCK>
+__device__ __forceinline__ uint64_t block_exclusive_max(uint64_t v, uint64_t* all,
+                                                        uint64_t* scratch) {
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    uint64_t inc = v;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+        const uint64_t y = __shfl_up(inc, o, kWave);
+        if (lane >= o) inc = inc > y ? inc : y;
+    }
+    if (lane == kWave - 1) scratch[wid] = inc;
+    __syncthreads();
+    uint64_t before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < BLOCK / kWave; ++w) {
+        const uint64_t t = scratch[w];
+        before = (w < wid && t > before) ? t : before;
+        tot = t > tot ? t : tot;
+    }
+    __syncthreads();
+    uint64_t prev = __shfl_up(inc, 1, kWave);
+    if (lane == 0) prev = 0;
+    *all = tot;
+    return before > prev ? before : prev;
+}
+
+// Per-trace workspace of the general path (bytes from the trace's base, n
+// tensors): two copies of the list of placed tensors sorted by offset --
+// offsets (u64) at 0 and 8n, ids (u32) at 16n and 20n.  The live-bytes
+// difference array (n + 1 u64) uses the first copy before placement.  24n + 8
+// bytes in all; the LDS path keeps its position permutation (u16) at 0.
+constexpr int64_t kWsPerTensor = 24;
+constexpr int64_t kWsPerTrace = 64;
+
+__device__ __forceinline__ unsigned char* trace_ws(unsigned char* ws, int64_t lo, int64_t b) {
+    return ws + kWsPerTensor * lo + kWsPerTrace * b;
+}
+
+// The greedy of Section 2.3 taken literally for one trace of n tensors
+// (1 <= n <= cap_n): tensors in rank order (size desc, first asc, id asc),
+// each at the lowest (or, BEST_FIT, the tightest) gap left by the placed
+// tensors whose lifetimes meet its own, 64-bit offsets in bytes.  The placed
+// tensors are kept sorted by offset; each step filters them by lifetime,
+// takes running maxima of their ends in offset order (the gap before a range
+// runs from the maximum end below it to its start) and inserts the new range
+// while copying the list to its other copy.  O(n^2 / BLOCK) work per trace.
+// The bound is the maximum over positions of the running sum of a
+// difference array (+size at a tensor's position, -size at its reach).
+// LDS: at least 16 n + 8 bytes at smem.
+template <int BLOCK>
+__device__ void plan_general(const int64_t* __restrict__ size, const int32_t* __restrict__ first,
+                             const int32_t* __restrict__ last, int64_t lo, int n, bool best,
+                             unsigned char* smem, unsigned char* tws, uint64_t* red64,
+                             int64_t* __restrict__ offset_out, uint64_t* peak, uint64_t* bound) {
+    const int tid = threadIdx.x;
+    int m = 1;
+    while (m < n) m <<= 1;
+    uint64_t* soff0 = reinterpret_cast<uint64_t*>(tws);
+    uint64_t* soff1 = reinterpret_cast<uint64_t*>(tws + 8 * (size_t)n);
+    uint32_t* sidx0 = reinterpret_cast<uint32_t*>(tws + 16 * (size_t)n);
+    uint32_t* sidx1 = reinterpret_cast<uint32_t*>(tws + 20 * (size_t)n);
+
+    // ---- live-bytes bound: positions by (first, id), difference array
+    {
+        uint64_t* keys = reinterpret_cast<uint64_t*>(smem);
+        unsigned long long* dd = reinterpret_cast<unsigned long long*>(soff0);  // n + 1 entries
+        for (int i = tid; i < m; i += BLOCK)
+            keys[i] = i < n ? ((uint64_t)(uint32_t)first[lo + i] << 32) | (uint32_t)i : ~0ull;
+        for (int i = tid; i <= n; i += BLOCK) dd[i] = 0ull;
+        l2_barrier();
+        bitonic_sort_u64<BLOCK>(keys, m);
+        for (int q = tid; q < n; q += BLOCK) {
+            const uint32_t id = (uint32_t)keys[q];
+            const uint32_t l = (uint32_t)last[lo + id];
+            int a = q + 1, z = n;  // reach: first position born after l
+            while (a < z) {
+                const int mid = (a + z) >> 1;
+                if ((uint32_t)(keys[mid] >> 32) <= l) a = mid + 1;
+                else z = mid;
+            }
+            const unsigned long long s = (unsigned long long)size[lo + id];
+            atomicAdd(dd + q, s);
+            atomicAdd(dd + a, 0ull - s);
+        }
+        l2_barrier();
+        const int chunk = (n + BLOCK - 1) / BLOCK;
+        const int a0 = min(n, tid * chunk), a1 = min(n, a0 + chunk);
+        uint64_t part = 0;
+        for (int i = a0; i < a1; ++i) part += l2_load64(reinterpret_cast<uint64_t*>(dd) + i);
+        uint64_t tot;
+        uint64_t run = block_exclusive_sum<BLOCK, uint64_t>(part, &tot, red64);
+        uint64_t lm = 0;
+        for (int i = a0; i < a1; ++i) {
+            run += l2_load64(reinterpret_cast<uint64_t*>(dd) + i);
+            lm = lm > run ? lm : run;
+        }
+        *bound = block_reduce<BLOCK>(lm, OpMax<uint64_t>(), red64);
+    }
+
+    // ---- rank order: a bitonic sort of the ids with the rank comparison
+    uint64_t* sz = reinterpret_cast<uint64_t*>(smem);                       // 8 n
+    int32_t* fs = reinterpret_cast<int32_t*>(smem + 8 * (size_t)n);        // 4 n
+    uint16_t* ord = reinterpret_cast<uint16_t*>(smem + 12 * (size_t)n);    // m <= 2 n
+    for (int i = tid; i < n; i += BLOCK) {
+        sz[i] = (uint64_t)size[lo + i];
+        fs[i] = first[lo + i];
+    }
+    for (int i = tid; i < m; i += BLOCK) ord[i] = i < n ? (uint16_t)i : (uint16_t)0xFFFFu;
+    __syncthreads();
+    auto before = [&](uint32_t a, uint32_t c) {  // does id a rank before id c? (pads last)
+        if (a == 0xFFFFu) return false;
+        if (c == 0xFFFFu) return true;
+        if (sz[a] != sz[c]) return sz[a] > sz[c];
+        if (fs[a] != fs[c]) return fs[a] < fs[c];
+        return a < c;
+    };
+    for (int k = 2; k <= m; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < (m >> 1); i += BLOCK) {
+                const int a = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+                const int c = a | j;
+                const uint32_t va = ord[a], vc = ord[c];
+                const bool up = (a & k) == 0;
+                if (before(vc, va) == up) {
+                    ord[a] = (uint16_t)vc;
+                    ord[c] = (uint16_t)va;
+                }
+            }
+            __syncthreads();
+        }
+    }
+
+    // ---- placement, one tensor a step
+    uint64_t pk = 0;
+    for (int k = 0; k < n; ++k) {
+        const uint32_t t = ord[k];
+        const uint64_t st = sz[t];
+        const int32_t ft = first[lo + t], lt = last[lo + t];
+        const uint64_t* so = (k & 1) ? soff1 : soff0;
+        const uint32_t* si = (k & 1) ? sidx1 : sidx0;
+        uint64_t* no = (k & 1) ? soff0 : soff1;
+        uint32_t* ni = (k & 1) ? sidx0 : sidx1;
+        const int chunk = (k + BLOCK - 1) / BLOCK;  // k tensors are placed
+        const int e0 = min(k, tid * chunk), e1 = min(k, e0 + chunk);
+        auto meets = [&](uint32_t id) { return first[lo + id] <= lt && ft <= last[lo + id]; };
+        uint64_t hi = 0;  // highest end among this thread's ranges that meet t
+        for (int e = e0; e < e1; ++e) {
+            const uint32_t id = l2_load32(si + e);
+            if (meets(id)) {
+                const uint64_t en = l2_load64(so + e) + sz[id];
+                hi = hi > en ? hi : en;
+            }
+        }
+        uint64_t top;
+        uint64_t run = block_exclusive_max<BLOCK>(hi, &top, red64);
+        uint64_t cand = ~0ull, cgap = ~0ull;  // this thread's choice among its gaps
+        for (int e = e0; e < e1; ++e) {
+            const uint32_t id = l2_load32(si + e);
+            if (!meets(id)) continue;
+            const uint64_t o = l2_load64(so + e);
+            if (o >= run && o - run >= st) {
+                if (!best) {
+                    if (cand == ~0ull) cand = run;
+                } else if (o - run < cgap) {
+                    cgap = o - run;
+                    cand = run;
+                }
+            }
+            const uint64_t en = o + sz[id];
+            run = run > en ? run : en;
+        }
+        uint64_t x;
+        if (!best) {
+            x = block_reduce<BLOCK>(cand, OpMin<uint64_t>(), red64);
+        } else {
+            const uint64_t g = block_reduce<BLOCK>(cgap, OpMin<uint64_t>(), red64);
+            x = block_reduce<BLOCK>(cgap == g ? cand : ~(uint64_t)0, OpMin<uint64_t>(), red64);
+        }
+        if (x == ~0ull) x = top;  // no gap holds t: above every range
+        pk = pk > x + st ? pk : x + st;
+        if (tid == 0) offset_out[lo + t] = (int64_t)x;
+        // the list with t inserted before the first range starting at or above x
+        for (int e = e0; e < e1; ++e) {
+            const uint64_t o = l2_load64(so + e);
+            const uint32_t id = l2_load32(si + e);
+            const int d = e + (o >= x ? 1 : 0);
+            no[d] = o;
+            ni[d] = id;
+            if (o >= x && (e == 0 || l2_load64(so + e - 1) < x)) {
+                no[e] = x;
+                ni[e] = t;
+            }
+        }
+        if (tid == 0 && (k == 0 || l2_load64(so + k - 1) < x)) {
+            no[k] = x;
+            ni[k] = t;
+        }
+        l2_barrier();
+    }
+    *peak = pk;
+}
+
+// LDS byte offsets of the regions of the LDS path (N = tensor slots):
+//   A [8N+8]   first (i32) and live-bytes deltas (u32, from 4N)
+//              -> fill: cursors (u16, at 0), predecessor counts (u16, at
+//                 2N+4), sizes in units (u32, at 4N+8)
+//              -> placement words ofsz[N + 1]
 //   F [2N+4]   band lengths (u16), kept for placement
+//   E [2N+4]   left-list starts (u16, N + 1 of them)
+//   R [2N+4]   reach histogram (packed u16) -> band starts -> ready lists
+//   T [cap+16] left-list entries (u8)
 // The u64 sort keys of an unsorted trace use the space from 0 before the
-// reach pass.  The left lists themselves live in the global workspace.
+// reach pass, and the general path uses all of it (16N + 8 at least).
 struct BatchLds {
-    size_t a, b, c, d, e, f, total;
+    size_t a, f, e, r, t, total;
 };
-__host__ __device__ inline BatchLds batch_lds(size_t N) {
+__host__ __device__ inline BatchLds batch_lds(size_t N, size_t cap) {
     BatchLds L{};
     const size_t w16 = (2 * N + 4 + 3) & ~(size_t)3;  // N + 1 u16 entries, 4-byte multiple
     L.a = 0;
-    L.b = 8 * N + 8;
-    L.c = L.b + w16;
-    L.d = L.c + w16;
-    L.e = L.d + 4 * N + 4;
-    L.f = L.e + w16;
-    L.total = L.f + w16;
+    L.f = 8 * N + 8;
+    L.e = L.f + w16;
+    L.r = L.e + w16;
+    L.t = L.r + w16;
+    L.total = (L.t + cap + 16 + 15) & ~(size_t)15;
     return L;
 }
 
@@ -492,8 +724,8 @@ template <int BLOCK, int ITEMS, bool BEST>
 __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const int64_t* __restrict__ begin, const int32_t* __restrict__ num_ops,
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
-    const int32_t* __restrict__ last, int64_t n_tensors, int32_t cap_n, int32_t cap_pairs,
-    uint16_t* __restrict__ lists, int64_t* __restrict__ offset_out,
+    const int32_t* __restrict__ last, int64_t n_tensors, int32_t cap_n, int32_t cap_lists,
+    unsigned char* __restrict__ ws, int64_t* __restrict__ offset_out,
     int64_t* __restrict__ peak_out, int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
     constexpr bool best = BEST;  // BEST_FIT: every tensor to a 16-lane row or the wave
     extern __shared__ __align__(16) unsigned char smem[];
@@ -501,33 +733,34 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class)
     __shared__ uint32_t ncls[3];              // tensors per ready class
     __shared__ uint32_t seeds[3];             // tensors per class without predecessors
+    __shared__ uint16_t longtab[kLongSlots];  // positions of the long tensors
+    __shared__ uint32_t nlong;
 
     const size_t N = (size_t)cap_n;
-    const BatchLds R = batch_lds(N);
+    const BatchLds R = batch_lds(N, (size_t)cap_lists);
     int32_t* fst = reinterpret_cast<int32_t*>(smem + R.a);
     uint32_t* live = reinterpret_cast<uint32_t*>(smem + R.a + 4 * N);
+    uint32_t* cursor = reinterpret_cast<uint32_t*>(smem + R.a);
+    uint32_t* pend = reinterpret_cast<uint32_t*>(smem + R.a + 2 * N + 4);
+    uint32_t* su = reinterpret_cast<uint32_t*>(smem + R.a + 4 * N + 8);
     uint64_t* ofsz = reinterpret_cast<uint64_t*>(smem + R.a);
-    const uint32_t* szw = reinterpret_cast<const uint32_t*>(smem + R.a);  // size half at 2q
     uint64_t* keys = reinterpret_cast<uint64_t*>(smem);
-    uint16_t* band = reinterpret_cast<uint16_t*>(smem + R.b);
-    uint16_t* readyq = reinterpret_cast<uint16_t*>(smem + R.b);
-    uint32_t* cursor = reinterpret_cast<uint32_t*>(smem + R.c);
-    uint32_t* hist = reinterpret_cast<uint32_t*>(smem + R.d);
-    uint32_t* rem = hist;
-    uint16_t* lbeg = reinterpret_cast<uint16_t*>(smem + R.e);
     uint16_t* rlen = reinterpret_cast<uint16_t*>(smem + R.f);
+    uint16_t* lbeg = reinterpret_cast<uint16_t*>(smem + R.e);
+    uint32_t* hist = reinterpret_cast<uint32_t*>(smem + R.r);
+    uint16_t* bstart = reinterpret_cast<uint16_t*>(smem + R.r);
+    uint16_t* readyq = reinterpret_cast<uint16_t*>(smem + R.r);
+    uint8_t* lents = smem + R.t;
     uint32_t* scratch = reinterpret_cast<uint32_t*>(red);
 
     const int tid = threadIdx.x;
     const int64_t b = blockIdx.x;
-    // this trace's workspace: ids by position (unsorted traces), left lists
-    uint16_t* perm = lists + b * ((int64_t)cap_n + (int64_t)cap_pairs + 16);
-    uint16_t* lst = perm + cap_n;
     MP_STAMP(0);
     if (tid == 0) {
         nready[0] = nready[1] = nready[2] = 0;
         ncls[0] = ncls[1] = ncls[2] = 0;
         seeds[0] = seeds[1] = seeds[2] = 0;
+        nlong = 0;
     }
     const int64_t lo = begin[b], hi = begin[b + 1];
     const int32_t n_ops = num_ops[b];
@@ -536,6 +769,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         return;
     }
     const int n = (int)(hi - lo);
+    unsigned char* tws = trace_ws(ws, lo, b);
+    uint16_t* perm = reinterpret_cast<uint16_t*>(tws);  // ids by position (unsorted traces)
 
     // ---- ingest + checks (ids owned strided: i = tid + k * BLOCK).  The
     // sizes and last ops of a sorted trace stay in registers for the band
@@ -616,153 +851,168 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         return;
     }
     const int sh = __builtin_ctzll(or_all);  // common power-of-two unit of all sizes
-    if ((total >> sh) > 0xFFFFFFFEull) {     // offsets are kept as 32-bit unit counts
-        if (tid == 0) raise_status(status, MP_ENOSPC);
-        return;
-    }
+    bool general = (total >> sh) > kFastMaxUnits;
     const bool unsorted = (flags & 2u) != 0;
     auto id_of = [&](int q) { return unsorted ? (int)perm[q] : q; };  // position -> id
 
-    // ---- position order (first, id); recorded traces are normally sorted already
-    if (unsorted) {
-        int m = 1;
-        while (m < n) m <<= 1;
-        for (int i = tid; i < m; i += BLOCK)
-            keys[i] = (i < n) ? (((uint64_t)(uint32_t)first[lo + i] << 32) | (uint32_t)i) : ~0ull;
+    uint32_t live_max = 0, n_pairs = 0;
+    if (!general) {
+        // ---- position order (first, id); recorded traces are normally sorted already
+        if (unsorted) {
+            int m = 1;
+            while (m < n) m <<= 1;
+            for (int i = tid; i < m; i += BLOCK)
+                keys[i] = (i < n) ? (((uint64_t)(uint32_t)first[lo + i] << 32) | (uint32_t)i) : ~0ull;
+            __syncthreads();
+            bitonic_sort_u64<BLOCK>(keys, m);
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = tid + k * BLOCK;
+                if (q < n) perm[q] = (uint16_t)(keys[q] & 0xFFFFu);
+            }
+            l2_barrier();  // the keys are dead: first[] goes back in position order
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = tid + k * BLOCK;
+                if (q < n) fst[q] = first[lo + perm[q]];
+            }
+        }
+        for (int i = tid; i <= n; i += BLOCK) live[i] = 0;
+        for (int i = tid; i <= (n >> 1); i += BLOCK) hist[i] = 0;
         __syncthreads();
-        bitonic_sort_u64<BLOCK>(keys, m);
-#pragma unroll
-        for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
-            if (q < n) perm[q] = (uint16_t)(keys[q] & 0xFFFFu);
-        }
-        __syncthreads();  // the keys are dead: first[] goes back in position order
-#pragma unroll
-        for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
-            if (q < n) fst[q] = first[lo + perm[q]];
-        }
-    }
-    for (int i = tid; i <= n; i += BLOCK) live[i] = 0;
-    for (int i = tid; i <= (n >> 1); i += BLOCK) hist[i] = 0;
-    __syncthreads();
-    MP_STAMP(2);
+        MP_STAMP(2);
 
-    // ---- reach, band lengths, live-bytes deltas, reach histogram.  The
-    // reach is the first position past q whose first op is after last[q]:
-    // the next four positions are probed at once (short bands, the common
-    // case, end there), longer bands gallop from the fourth.
-    int32_t rch[ITEMS];
+        // ---- reach, band lengths, live-bytes deltas, reach histogram, long
+        // tensors.  The reach is the first position past q whose first op is
+        // after last[q]: the next four positions are probed at once (short
+        // bands, the common case, end there), longer bands gallop from the
+        // fourth.
+        int32_t rch[ITEMS];
 #pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        rch[k] = q + 1;
-        if (q < n) {
-            const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
-            const int32_t f1 = q + 1 < n ? fst[q + 1] : INT32_MAX;
-            const int32_t f2 = q + 2 < n ? fst[q + 2] : INT32_MAX;
-            const int32_t f3 = q + 3 < n ? fst[q + 3] : INT32_MAX;
-            const int32_t f4 = q + 4 < n ? fst[q + 4] : INT32_MAX;
-            rch[k] = q + 1 + (f1 <= l) + (f2 <= l) + (f3 <= l) + (f4 <= l);
+        for (int k = 0; k < ITEMS; ++k) {
+            const int q = tid + k * BLOCK;
+            rch[k] = q + 1;
+            if (q < n) {
+                const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
+                const int32_t f1 = q + 1 < n ? fst[q + 1] : INT32_MAX;
+                const int32_t f2 = q + 2 < n ? fst[q + 2] : INT32_MAX;
+                const int32_t f3 = q + 3 < n ? fst[q + 3] : INT32_MAX;
+                const int32_t f4 = q + 4 < n ? fst[q + 4] : INT32_MAX;
+                rch[k] = q + 1 + (f1 <= l) + (f2 <= l) + (f3 <= l) + (f4 <= l);
+            }
         }
-    }
 #pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        if (q < n) {
-            const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
-            const int64_t sz = unsorted ? size[lo + perm[q]] : sz_r[k];
-            const uint32_t su = (uint32_t)((uint64_t)sz >> sh);
-            int a = rch[k];
-            if (a == q + 5) {  // first[q + 4] <= l: gallop on
-                int known = q + 4, step = 8, probe = q + 8;  // first[known] <= l
-                while (probe < n && fst[probe] <= l) {
-                    known = probe;
-                    step <<= 1;
-                    probe = q + step;
+        for (int k = 0; k < ITEMS; ++k) {
+            const int q = tid + k * BLOCK;
+            if (q < n) {
+                const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
+                const int64_t sz = unsorted ? size[lo + perm[q]] : sz_r[k];
+                const uint32_t sq = (uint32_t)((uint64_t)sz >> sh);
+                int a = rch[k];
+                if (a == q + 5) {  // first[q + 4] <= l: gallop on
+                    int known = q + 4, step = 8, probe = q + 8;  // first[known] <= l
+                    while (probe < n && fst[probe] <= l) {
+                        known = probe;
+                        step <<= 1;
+                        probe = q + step;
+                    }
+                    a = known + 1;
+                    int z = probe < n ? probe : n;
+                    while (a < z) {
+                        const int mid = (a + z) >> 1;
+                        if (fst[mid] <= l) a = mid + 1;
+                        else z = mid;
+                    }
                 }
-                a = known + 1;
-                int z = probe < n ? probe : n;
-                while (a < z) {
-                    const int mid = (a + z) >> 1;
-                    if (fst[mid] <= l) a = mid + 1;
-                    else z = mid;
+                rlen[q] = (uint16_t)(a - q - 1);
+                atomicAdd(&live[q], sq);
+                atomicAdd(&live[a], 0u - sq);
+                packed_add(hist, (uint32_t)a, 1u);
+                if ((uint32_t)(a - q - 1) > kMaxDist) {  // reaches beyond a one-byte distance
+                    const uint32_t slot = atomicAdd(&nlong, 1u);
+                    if (slot < kLongSlots) longtab[slot] = (uint16_t)q;
                 }
             }
-            band[q] = (uint16_t)(a - q - 1);
-            rlen[q] = (uint16_t)(a - q - 1);
-            atomicAdd(&live[q], su);
-            atomicAdd(&live[a], 0u - su);
-            packed_add(hist, (uint32_t)a, 1u);
         }
+        __syncthreads();
+        MP_STAMP(3);
+        general = nlong > kLongSlots;
     }
-    __syncthreads();
-    MP_STAMP(3);
-
-    // ---- one prefix pass over positions j (contiguous chunk per thread):
-    //   band start      = sum of band lengths before j        (pair index base)
-    //   left-list start = sum over i < j of #{q : q < i < reach[q]}
-    //                   = j(j-1)/2 - j * H(<j) + sum_{r<j} r * hist[r],
-    //     since position i has i - #{q : reach[q] <= i} left neighbours;
-    //   live bytes      = running sum of the deltas (its maximum is the bound).
-    // The three integer sums share one 64-bit word: band (24 bits, at most
-    // n(n-1)/2), hist count (13 bits, at most n) and r * hist (25 bits).
-    uint32_t live_max;
-    uint32_t n_pairs;
-    {
-        // even-sized chunks: both halves of a packed word stay with one thread
-        const int chunk = (((n + BLOCK - 1) / BLOCK) + 1) & ~1;
-        const int a0 = min(n, tid * chunk), a1 = min(n, a0 + chunk);
-        auto pack = [](uint32_t bl, uint32_t h, uint32_t j) {
-            return ((uint64_t)bl << 38) | ((uint64_t)h << 25) | (uint64_t)(h * j);
-        };
-        uint64_t ps = 0;
-        uint32_t ds = 0;
-        for (int i = a0; i < a1; ++i) {
-            ps += pack(band[i], packed_get(hist, (uint32_t)i), (uint32_t)i);
-            ds += live[i];
+    if (!general) {
+        // ---- one prefix pass over positions j (contiguous chunk per thread):
+        //   band start      = sum of band lengths before j        (pair index base)
+        //   left-list start = sum over i < j of #{q : q < i < reach[q]}
+        //                   = j(j-1)/2 - j * H(<j) + sum_{r<j} r * hist[r],
+        //     since position i has i - #{q : reach[q] <= i} left neighbours;
+        //   live bytes      = running sum of the deltas (its maximum is the bound).
+        // The three integer sums share one 64-bit word: band (24 bits, at most
+        // n(n-1)/2), hist count (13 bits, at most n) and r * hist (25 bits).
+        uint32_t kmax = 0;
+        {
+            // even-sized chunks: both halves of a packed word stay with one thread
+            const int chunk = (((n + BLOCK - 1) / BLOCK) + 1) & ~1;
+            const int a0 = min(n, tid * chunk), a1 = min(n, a0 + chunk);
+            auto pack = [](uint32_t bl, uint32_t h, uint32_t j) {
+                return ((uint64_t)bl << 38) | ((uint64_t)h << 25) | (uint64_t)(h * j);
+            };
+            uint64_t ps = 0;
+            uint32_t ds = 0;
+            for (int i = a0; i < a1; ++i) {
+                ps += pack(rlen[i], packed_get(hist, (uint32_t)i), (uint32_t)i);
+                ds += live[i];
+            }
+            uint64_t ptot;
+            uint64_t prun = block_exclusive_sum<BLOCK>(ps, &ptot, red);
+            uint32_t dtot;
+            uint32_t drun = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
+            uint32_t lm = 0;
+            uint16_t* cursor16 = reinterpret_cast<uint16_t*>(cursor);
+            for (int i = a0; i < a1; ++i) {
+                const uint32_t bl = rlen[i], h = packed_get(hist, (uint32_t)i), dl = live[i];
+                const uint32_t hb = (uint32_t)(prun >> 25) & 0x1FFFu;
+                const uint32_t rh = (uint32_t)prun & 0x1FFFFFFu;
+                const uint32_t ls = (uint32_t)(i * (i - 1) / 2) - (uint32_t)i * hb + rh;
+                const uint32_t Li = (uint32_t)i - hb - h;  // left neighbours of position i
+                kmax = max(kmax, Li + bl);
+                bstart[i] = (uint16_t)(prun >> 38);  // over hist[i], already read
+                lbeg[i] = (uint16_t)ls;
+                cursor16[i] = (uint16_t)ls;
+                drun += dl;
+                lm = lm > drun ? lm : drun;
+                prun += pack(bl, h, (uint32_t)i);
+            }
+            n_pairs = (uint32_t)(ptot >> 38);
+            if (tid == 0) {
+                bstart[n] = (uint16_t)n_pairs;
+                lbeg[n] = (uint16_t)n_pairs;
+            }
+            live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), scratch);
         }
-        uint64_t ptot;
-        uint64_t prun = block_exclusive_sum<BLOCK>(ps, &ptot, red);
-        uint32_t dtot;
-        uint32_t drun = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
-        uint32_t lm = 0;
-        uint16_t* cursor16 = reinterpret_cast<uint16_t*>(cursor);
-        for (int i = a0; i < a1; ++i) {
-            const uint32_t bl = band[i], h = packed_get(hist, (uint32_t)i), dl = live[i];
-            const uint32_t hb = (uint32_t)(prun >> 25) & 0x1FFFu;
-            const uint32_t rh = (uint32_t)prun & 0x1FFFFFFu;
-            const uint32_t ls = (uint32_t)(i * (i - 1) / 2) - (uint32_t)i * hb + rh;
-            band[i] = (uint16_t)(prun >> 38);
-            lbeg[i] = (uint16_t)ls;
-            cursor16[i] = (uint16_t)ls;
-            drun += dl;
-            lm = lm > drun ? lm : drun;
-            prun += pack(bl, h, (uint32_t)i);
-        }
-        n_pairs = (uint32_t)(ptot >> 38);
+        kmax = block_reduce<BLOCK>(kmax, OpMax<uint32_t>(), scratch);
+        general = n_pairs > (uint32_t)cap_lists || (best && kmax > kBestMaxK);
+    }
+    if (general) {
+        __syncthreads();
+        uint64_t pk = 0, bound = 0;
+        plan_general<BLOCK>(size, first, last, lo, n, best, smem, tws, red, offset_out, &pk,
+                            &bound);
         if (tid == 0) {
-            band[n] = (uint16_t)n_pairs;
-            lbeg[n] = (uint16_t)n_pairs;
+            peak_out[b] = (int64_t)pk;
+            if (lb_out) lb_out[b] = (int64_t)bound;
         }
-        live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), scratch);
-    }
-    if (n_pairs > (uint32_t)cap_pairs) {  // the u16 starts above are then not used
-        if (tid == 0) raise_status(status, MP_ENOSPC);
         return;
     }
-    const uint32_t spare = (uint32_t)N;  // ofsz[N]: never placed, size 0
-    if (tid == 0) ofsz[spare] = (uint64_t)kUnplaced << 32;
+    MP_STAMP(4);
+
+    // ---- sizes in units and zero predecessor counts (over first[] and the
+    // deltas, both dead)
+    for (int i = tid; i <= (n >> 1); i += BLOCK) pend[i] = 0;
 #pragma unroll
-    for (int k = 0; k < ITEMS; ++k) {  // first[], the deltas and the histogram are dead
+    for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
-        if (q < n) {
-            ofsz[q] = ((uint64_t)kUnplaced << 32) | (uint32_t)((uint64_t)size[lo + id_of(q)] >> sh);
-            rem[q] = 0;
-        }
+        if (q < n) su[q] = (uint32_t)((uint64_t)(unsorted ? size[lo + perm[q]] : sz_r[k]) >> sh);
     }
     __syncthreads();
-    MP_STAMP(4);
 
     // ---- left lists and pending predecessor counts, balanced over the pairs:
     // pair index p -> (q, j), j = q + 1 + (p - band start of q)
@@ -773,32 +1023,40 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             int a = 0, z = n;  // last position whose band starts at or before p_lo
             while (a < z) {
                 const int mid = (a + z + 1) >> 1;
-                if (band[mid] <= p_lo) a = mid;
+                if (bstart[mid] <= p_lo) a = mid;
                 else z = mid - 1;
             }
             int q = a;
-            uint32_t base = band[q], nxt = band[q + 1];
-            uint32_t sq = szw[2 * q];
+            uint32_t base = bstart[q], nxt = bstart[q + 1];
+            uint32_t sq = su[q];
             for (uint32_t p = p_lo; p < p_hi; ++p) {
                 while (nxt <= p) {
                     ++q;
                     base = nxt;
-                    nxt = band[q + 1];
-                    sq = szw[2 * q];
+                    nxt = bstart[q + 1];
+                    sq = su[q];
                 }
                 const uint32_t j = (uint32_t)q + 1 + (p - base);
-                const bool j_after = sq >= szw[2 * j];  // j ranks after q
-                lst[packed_add(cursor, j, 1u)] = (uint16_t)(q | (j_after ? 0u : kLeftSucc));
-                atomicAdd(&rem[j_after ? j : (uint32_t)q], 1u);
+                const uint32_t d = j - (uint32_t)q;
+                uint32_t ent = d;
+                if (d > kMaxDist) {  // q is long: its slot in the table
+                    uint32_t s = 0;
+#pragma nounroll
+                    while (s + 1 < kLongSlots && longtab[s] != (uint16_t)q) ++s;
+                    ent = kLongBase + s;
+                }
+                lents[packed_add(cursor, j, 1u)] = (uint8_t)ent;
+                packed_add(pend, sq >= su[j] ? j : (uint32_t)q, 1u);  // j ranks after q?
             }
         }
     }
     __syncthreads();
 
-    // ---- ready classes (in the pending count) and list regions; tensors
-    // without predecessors seed the lists.  Counts and list slots are taken
-    // per wave (ballot, one atomic per class).
+    // ---- placement words (pending count and ready class while unplaced),
+    // class regions, and the tensors without predecessors as seeds.  The
+    // words overwrite the fill's arrays: read everything first.
     const int lane_id = tid & (kWave - 1);
+    uint64_t w_r[ITEMS];
     uint32_t cls_r[ITEMS];
     {
         uint32_t cc[3] = {0, 0, 0};
@@ -806,13 +1064,17 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
             cls_r[k] = 3;  // no tensor
+            w_r[k] = 0;
             if (q < n) {
-                const uint32_t c = best ? 2u : ready_class((uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q]);
-                rem[q] |= c << kClassShift;
-                cls_r[k] = c;
+                const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
+                const uint32_t c = best ? 2u : ready_class(K);
+                const uint32_t pc = packed_get(pend, (uint32_t)q);
+                w_r[k] = ((uint64_t)(kUnplacedBit | (c << kClassShift) | pc) << 32) | su[q];
+                cls_r[k] = pc == 0 ? c + 4 : c;  // +4: a seed
             }
 #pragma unroll
-            for (int c = 0; c < 3; ++c) cc[c] += (uint32_t)__popcll(__ballot(cls_r[k] == (uint32_t)c));
+            for (int c = 0; c < 3; ++c)
+                cc[c] += (uint32_t)__popcll(__ballot((cls_r[k] & 3u) == (uint32_t)c && cls_r[k] != 3u));
         }
         if (lane_id == 0) {
 #pragma unroll
@@ -821,21 +1083,28 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         }
     }
     __syncthreads();
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+        const int q = tid + k * BLOCK;
+        if (q < n) ofsz[q] = w_r[k];
+    }
+    const uint32_t spare = (uint32_t)N;  // ofsz[N]: never placed, size 0
+    if (tid == 0) ofsz[spare] = (uint64_t)kUnplacedBit << 32;
     const uint32_t region[3] = {0u, ncls[0], ncls[0] + ncls[1]};
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
-        const bool seed = q < n && (rem[q] & kCountMask) == 0;
+        const bool seed = q < n && cls_r[k] >= 4u;
 #pragma unroll
         for (int c = 0; c < 3; ++c) {
-            const uint64_t m = __ballot(seed && cls_r[k] == (uint32_t)c);
+            const uint64_t m = __ballot(seed && (cls_r[k] & 3u) == (uint32_t)c);
             if (!m) continue;
             uint32_t base = 0;
             if (lane_id == 0) base = atomicAdd(&seeds[c], (uint32_t)__popcll(m));
             base = (uint32_t)__builtin_amdgcn_readlane((int)base, 0);
             const uint32_t below = __builtin_amdgcn_mbcnt_hi(
                 (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            if (seed && cls_r[k] == (uint32_t)c) readyq[region[c] + base + below] = (uint16_t)q;
+            if (seed && (cls_r[k] & 3u) == (uint32_t)c) readyq[region[c] + base + below] = (uint16_t)q;
         }
     }
     __syncthreads();
@@ -850,10 +1119,11 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     // from the last wave down.  A group gathers the neighbours' words (the
     // placed ones are exactly the predecessors), moves the candidate offset
     // past the highest overlapping end until nothing overlaps, publishes the
-    // word and decrements the successors' pending counts; those reaching zero
+    // word and decrements its successors' pending counts; those reaching zero
     // are appended for the next round.  Per-round append counters rotate over
     // three slots so that one barrier per round suffices.
     {
+        const LeftLists ll{lents, longtab};
         const int lane = lane_id;
         const uint32_t g16 = lane & 15, row = (uint32_t)tid >> 4;
         constexpr uint32_t kRows = BLOCK / 16;
@@ -868,9 +1138,6 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             const ReadyLists rl{readyq,
                                 {region[0] + end[0], region[1] + end[1], region[2] + end[2]},
                                 &nready[cur]};
-#ifdef MP_PHASE_TIMING
-            if (tid == 0) MP_DBG_ADD(0, 1u);
-#endif
             const uint32_t nq = end[1] - bgn[1], np = end[0] - bgn[0];
             for (uint32_t it = 0;; ++it) {
                 const uint32_t gl = it * BLOCK + (uint32_t)tid;  // lane slot over the workgroup
@@ -886,45 +1153,36 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 const uint32_t qb = hb ? (uint32_t)readyq[region[2] + i1] : 0u;
                 const bool any_s = __ballot(hs) != 0, any_b = __ballot(hb) != 0;
                 if (!any_s && !any_b) break;
-#ifdef MP_PHASE_TIMING
-                if (lane == 0) MP_DBG_ADD(1, 1u);
-#endif
                 if (any_s) {
                     const Item is = load_item(qs, hs, spare, ofsz, lbeg, rlen);
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group(is, g, ofsz, lst, id, o, e, sc);
+                    gather_group(is, g, ofsz, ll, id, o, e, sc);
                     uint32_t x = 0;
                     while (true) {  // jump past the highest overlapping end until none moves
-                        const uint32_t m = pair_quad_max_u32(overlap_end(o, e, x, is.s), quad);
-                        const bool mv = m > x;
-                        x = mv ? m : x;
-#ifdef MP_PHASE_TIMING
-                        if (lane == 0) MP_DBG_ADD(2, 1u);
-#endif
+                        const uint32_t mm = pair_quad_max_u32(overlap_end(o, e, x, is.s), quad);
+                        const bool mv = mm > x;
+                        x = mv ? mm : x;
                         if (!__ballot(mv)) break;
                     }
                     if (hs && g == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
-                    release_successors(sc, id, rem, rl, lane);
+                    release_successors(sc, id, ofsz, rl, lane);
                 }
                 if (any_b) {
                     const Item ib = load_item(qb, hb, spare, ofsz, lbeg, rlen);
                     const bool mid = hb && ib.K <= kMidK;
                     const Item im = mid ? ib : Item{spare, 0, 0, 0, 0};  // wider: whole wave
                     uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group(im, g16, ofsz, lst, id, o, e, sc);
+                    gather_group(im, g16, ofsz, ll, id, o, e, sc);
                     uint32_t x = 0;
                     if (best) x = best_fit_group<16>(o, e, im.s, g16);
                     while (!best) {
-                        const uint32_t m = row_max_u32(overlap_end(o, e, x, im.s));
-                        const bool mv = m > x;
-                        x = mv ? m : x;
-#ifdef MP_PHASE_TIMING
-                        if (lane == 0) MP_DBG_ADD(3, 1u);
-#endif
+                        const uint32_t mm = row_max_u32(overlap_end(o, e, x, im.s));
+                        const bool mv = mm > x;
+                        x = mv ? mm : x;
                         if (!__ballot(mv)) break;
                     }
                     if (mid && g16 == 0) ofsz[ib.q] = ((uint64_t)x << 32) | ib.s;
-                    release_successors(sc, id, rem, rl, lane);
+                    release_successors(sc, id, ofsz, rl, lane);
                     uint64_t wide = __ballot(hb && !mid && g16 == 0);
                     while (wide) {
                         const int src = __ffsll((long long)wide) - 1;
@@ -934,7 +1192,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                                    (uint32_t)__builtin_amdgcn_readlane((int)ib.lb, src),
                                    (uint32_t)__builtin_amdgcn_readlane((int)ib.L, src),
                                    (uint32_t)__builtin_amdgcn_readlane((int)ib.K, src), ofsz,
-                                   lst, rem, rl, lane, best, status);
+                                   ll, rl, lane, best);
                     }
                 }
             }
@@ -981,10 +1239,14 @@ hipError_t launch_items(const BatchArgs& a, const BatchShape& s, hipStream_t st)
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)a.n_traces), dim3(kBatchBlock), s.lds_bytes, st,
                        a.begin, a.num_ops, a.size, a.first, a.last, a.n_tensors, s.cap_n,
-                       s.cap_pairs, static_cast<uint16_t*>(a.workspace), a.offset_out,
+                       s.cap_pairs, static_cast<unsigned char*>(a.workspace), a.offset_out,
                        a.peak_out, a.lb_out, a.status);
     return hipGetLastError();
 }
+
+// Static LDS of the kernel, rounded up (the per-workgroup budget minus this
+// is dynamic).
+constexpr size_t kStaticLds = 512;
 
 }  // namespace
 
@@ -1012,33 +1274,45 @@ hipError_t launch_reset_status(int32_t* status, hipStream_t st) {
     return hipGetLastError();
 }
 
-// LDS bytes per workgroup: about 20 per tensor slot, so that four
-// workgroups of 2000-tensor traces share a CU's 160 KiB.  Pair capacity per
-// trace: every pair of a trace of max_trace_len tensors, at most 64 per
-// tensor and below 2^16 (list starts are u16).
+// LDS per workgroup: about 14 bytes per tensor slot plus one byte per list
+// entry, in the smallest budget of {1/4, 1/3, 1/2, all} of a CU's 160 KiB
+// that gives every pair of a trace of max_trace_len tensors a slot, or at
+// least 4 per tensor (and at least 2 per tensor always: the sort keys of an
+// unsorted trace and the general path's 16 bytes per tensor use the same
+// space); the list capacity is whatever that budget leaves.  List starts are
+// u16: at most 65520 entries.  A trace with more pairs than the capacity
+// takes the general path.
 BatchShape batch_shape(int64_t max_trace_len) {
     BatchShape s{};
     if (max_trace_len < 0 || max_trace_len > MP_BATCH_MAX_TRACE_LEN) return s;
-    const int64_t cap_n = max_trace_len < 1 ? 1 : max_trace_len;
-    int64_t pairs = cap_n * (cap_n - 1) / 2;
-    if (pairs > 64 * cap_n) pairs = 64 * cap_n;
-    pairs = (pairs + 7) & ~(int64_t)7;
-    if (pairs < 8) pairs = 8;
-    if (pairs > 65520) pairs = 65520;
-    s.cap_n = (int32_t)cap_n;
-    s.cap_pairs = (int32_t)pairs;
-    s.lds_bytes = batch_lds((size_t)cap_n).total;
+    const int64_t N = max_trace_len < 1 ? 1 : max_trace_len;
+    int64_t want = N * (N - 1) / 2;
+    if (want > 4 * N) want = 4 * N;
+    if (want < 2 * N) want = 2 * N;
+    if (want > 65520) want = 65520;
+    const size_t base = batch_lds((size_t)N, 0).total + kStaticLds;
+    static const size_t tiers[] = {40960, 53248, 81920, 163840};
+    int64_t cap = -1;
+    for (size_t t : tiers) {
+        if (base > t) continue;
+        cap = (int64_t)((t - base) & ~(size_t)15);
+        if (cap >= want) break;
+    }
+    if (cap < 2 * N) return s;
+    if (cap > 65520) cap = 65520;
+    s.cap_n = (int32_t)N;
+    s.cap_pairs = (int32_t)cap;
+    s.lds_bytes = batch_lds((size_t)N, (size_t)cap).total;
     int items = 1;
-    while (items * kBatchBlock < cap_n) items <<= 1;
+    while (items * kBatchBlock < N) items <<= 1;
     s.items = items;
     s.ok = true;
     return s;
 }
 
-size_t plan_batch_workspace_bytes(int64_t n_traces, int64_t max_trace_len) {
-    const BatchShape s = batch_shape(max_trace_len);
-    if (!s.ok || n_traces < 0) return 0;
-    return (size_t)n_traces * ((size_t)s.cap_n + (size_t)s.cap_pairs + 16) * sizeof(uint16_t);
+size_t plan_batch_workspace_bytes(int64_t n_tensors, int64_t n_traces) {
+    if (n_tensors < 0 || n_traces < 0) return 0;
+    return (size_t)(kWsPerTensor * n_tensors + kWsPerTrace * n_traces + 64);
 }
 
 hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st) {

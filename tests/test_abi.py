@@ -62,9 +62,9 @@ def test_plan_batch_host_checks(lib):
                              None, 0, st, None) == b.MP_EINVAL
     assert lib.mp_plan_batch(None, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
                              None, 0, st, None) == b.MP_EINVAL
-    # missing or short workspace (the pair lists of every trace)
-    need = lib.mp_workspace_size(b.OP_PLAN_BATCH, 0, 1, 10)
-    assert need >= 45 * 2
+    # missing or short workspace (24 bytes per tensor and 64 per trace at least)
+    need = lib.mp_workspace_bytes(b.OP_PLAN_BATCH, 4, 0, 1)
+    assert need >= 24 * 4 + 64
     assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
                              None, need, st, None) == b.MP_EINVAL
     assert lib.mp_plan_batch(dummy, 1, dummy, dummy, dummy, dummy, 4, 10, 0, dummy, dummy, None,
@@ -78,10 +78,28 @@ def test_pair_capacity(lib):
     assert lib.mp_batch_pair_capacity(2000) >= 12000   # the 2000-tensor traces need ~11K
     assert lib.mp_batch_pair_capacity(4096) > 0
     assert lib.mp_batch_pair_capacity(100) >= 100 * 99 // 2   # short traces: every pair
-    # workspace grows with the traces and the capacity
-    assert lib.mp_workspace_size(b.OP_PLAN_BATCH, 0, 1024, 2000) >= (
-        1024 * 2 * lib.mp_batch_pair_capacity(2000))
-    assert lib.mp_workspace_size(b.OP_PLAN_BATCH, 0, 1, 5000) == 0
+    # the batched planner's workspace: 24 bytes per tensor (the general path's
+    # two offset-sorted lists, or the position permutation) + 64 per trace
+    assert lib.mp_workspace_size(b.OP_PLAN_BATCH, 2048000, 1024, 0) >= 24 * 2048000 + 64 * 1024
+    assert lib.mp_workspace_bytes(b.OP_PLAN_BATCH, 2048000, 0, 1024) == lib.mp_workspace_size(
+        b.OP_PLAN_BATCH, 2048000, 1024, 0)
+    assert lib.mp_workspace_size(b.OP_PLAN_BATCH, -1, 1, 0) == 0
+
+
+def test_workspace_bytes_query(lib):
+    """mp_workspace_bytes(op, n_tensors, max_num_ops, n_traces) agrees with the
+    capacity-explicit query for every op (validation at capacity n_tensors)."""
+    from paper_2203_00448_amd import binding as b
+    wb, ws = lib.mp_workspace_bytes, lib.mp_workspace_size
+    assert wb(b.OP_LIVE_BYTES, 100, 4000, 1) == ws(b.OP_LIVE_BYTES, 100, 4000, 0) > 0
+    assert wb(b.OP_VALIDATE, 1000, 0, 1) == ws(b.OP_VALIDATE, 1000, 0, 1000) > 0
+    assert wb(b.OP_VALIDATE_BATCH, 1000, 0, 7) == ws(b.OP_VALIDATE_BATCH, 1000, 7, 1000) > 0
+    assert wb(b.OP_PLAN_TRACE, 5000, 100, 1) == ws(b.OP_PLAN_TRACE, 5000, 100, 0) > 0
+    assert wb(b.OP_BUMP, 5000, 0, 1) == ws(b.OP_BUMP, 5000, 0, 0) > 0
+    assert wb(b.OP_PROBE, 5000, 100, 1) == ws(b.OP_PROBE, 5000, 100, 0) > 0
+    for bad in ((99, 10, 10, 1), (b.OP_PLAN_BATCH, -1, 0, 1), (b.OP_PLAN_BATCH, 10, 0, -1),
+                (b.OP_LIVE_BYTES, 10, -5, 1), (b.OP_PLAN_TRACE, 1 << 30, 0, 1)):
+        assert wb(*bad) == 0, bad
 
 
 def test_other_host_checks(lib):

@@ -5,9 +5,8 @@ Section 2.3: among the free gaps left by the already placed, lifetime-
 intersecting tensors, the smallest one that holds the tensor (lowest start
 among equals), the space above all of them only when no gap holds it.
 Integer work: offsets and peaks must match the oracle bit for bit.  The
-batched planner fits a tensor with at most 256 lifetime-intersecting tensors
-(MP_ENOSPC beyond); the single-trace planner has the same limit for both
-policies (131072 earlier-ranked intersecting tensors)."""
+batched planner fits a tensor with up to 256 lifetime-intersecting tensors in
+one wave and plans a trace with a larger one on its general path."""
 import hashlib
 import json
 import os
@@ -111,13 +110,8 @@ def test_batch_neighbour_limit():
     t = tg.Trace(np.full(n, 64, np.int64), np.arange(n, dtype=np.int32),
                  np.arange(n, dtype=np.int32), n)
     t.first[0], t.last[0] = 0, n - 1
-    args = batch_to_device(tg.concat([t]))
-    status = binding.new_status()
-    binding.plan_batch(*args, policy=binding.BEST_FIT, check=False, status=status)
-    assert int(status.item()) == binding.MP_ENOSPC
-    # LOWEST_FIT has no such limit
-    off, peak, _ = binding.plan_batch(*args)
-    assert int(peak.item()) == 128
+    _, peak = _check_batch(binding, tg.concat([t, tg.chain256()]))
+    assert int(peak[0]) == 128
 
 
 @pytest.mark.parametrize("seed", [401, 402])
