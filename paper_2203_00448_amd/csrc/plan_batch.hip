@@ -31,6 +31,8 @@
 // planned by the same workgroup on the general path (plan_general): the
 // greedy taken literally, one tensor at a time in rank order, 64-bit offsets,
 // its working lists in the workspace.  No valid trace is refused.
+#include <type_traits>
+
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -56,12 +58,14 @@ __device__ unsigned int g_dbg[4096 * 8];
 namespace {
 
 constexpr int kBatchBlock = 512;
-constexpr uint32_t kPairK = 8;             // neighbours of a tensor fitted by a lane pair
-constexpr uint32_t kQuadK = 16;            // ... by a lane quad
-constexpr uint32_t kMidK = 64;             // ... by a 16-lane row; more: by the whole wave
-constexpr int kSlots = 4;                  // neighbours per lane in pairs, quads, rows, waves
-constexpr uint32_t kCoopChunk = 64u * kSlots;
-constexpr uint32_t kBestMaxK = 4u * kWave; // BEST_FIT on the LDS path: one wave sorts them all
+constexpr int kSmallSlots = 4;                // neighbours a lane holds in pairs and quads
+constexpr int kSlots = 4;                     // ... in rows and the whole wave
+constexpr uint32_t kPairK = 2u * kSmallSlots; // neighbours of a tensor fitted by a lane pair
+constexpr uint32_t kQuadK = 4u * kSmallSlots; // ... by a lane quad
+constexpr int kRowLanes = 16;                 // lanes of a row
+constexpr uint32_t kRowK = kRowLanes * kSlots; // ... by a row of lanes; more: the whole wave
+constexpr uint32_t kCoopChunk = (uint32_t)kWave * kSlots;
+constexpr uint32_t kBestMaxK = kCoopChunk;    // BEST_FIT on the LDS path: one wave sorts them all
 
 // A tensor's LDS placement word: size (units) in the low half; the high half
 // is the offset (units, below 2^31) once placed, and before that bit 31 set,
@@ -123,12 +127,9 @@ __device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K
     const uint32_t right = q + ((k + 1 - L) & in_band);
     return (pl & in_left) | (right & ~in_left);
 }
-// Does neighbour k rank after q?  A left neighbour (smaller position) does
-// iff it is strictly smaller; a right one iff it is not larger.
-__device__ __forceinline__ bool is_successor(uint32_t k, uint32_t L, uint32_t s_other,
-                                             uint32_t s) {
-    return (k < L) ? (s_other < s) : (s_other <= s);
-}
+// When a tensor is fitted every neighbour ranked before it is placed and none
+// ranked after it is, so its successors are exactly its unplaced neighbours.
+__device__ __forceinline__ uint32_t is_unplaced(uint32_t o) { return o >> 31; }
 
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
 // row-wise prefix maxima, row broadcasts carry them across rows, lane 63
@@ -203,7 +204,7 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum_dpp(uint32_t v) {
     return v;
 }
 
-// Decrement the pending counts of the successors among M (<= 4) gathered
+// Decrement the pending counts of the successors among M (<= 8) gathered
 // neighbours (dec[j] is 1 for a successor, else 0: the atomics then issue
 // back to back; subtracting 0 from a word changes nothing) and append those
 // that reach zero to their class list: one wave scan of the per-lane counts
@@ -213,18 +214,17 @@ template <int M>
 __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
                                                    const uint32_t (&ids)[M], uint64_t* ofsz,
                                                    const ReadyLists& rl, int lane) {
-    static_assert(M <= 4, "a lane releases at most 4 tensors");
+    static_assert(M <= 8, "a lane releases at most 8 tensors (10-bit wave sums)");
     uint32_t old[M], any_dec = 0;
 #pragma unroll
     for (int j = 0; j < M; ++j) {
         old[j] = 0;
         any_dec |= dec[j];
     }
-    if (any_dec) {
+    if (any_dec) {  // 32-bit atomics on the words' high halves (the pending counts)
+        uint32_t* hi = reinterpret_cast<uint32_t*>(ofsz) + 1;
 #pragma unroll
-        for (int j = 0; j < M; ++j)
-            old[j] = (uint32_t)(atomicSub(reinterpret_cast<unsigned long long*>(ofsz + ids[j]),
-                                          (unsigned long long)dec[j] << 32) >> 32);
+        for (int j = 0; j < M; ++j) old[j] = atomicSub(hi + 2 * ids[j], dec[j]);
     }
     uint32_t packed = 0;  // ready tensors of this lane, 10 bits per class
 #pragma unroll
@@ -245,45 +245,48 @@ __device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
     }
     const uint32_t blo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, 0);
     const uint32_t bhi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), 0);
-    uint32_t at[3] = {rl.end[0] + (blo & 0xFFFFu) + (pre & 0x3FFu),
-                      rl.end[1] + (blo >> 16) + ((pre >> 10) & 0x3FFu),
-                      rl.end[2] + (bhi & 0xFFFFu) + (pre >> 20)};
+    // this lane's next slot in each class list, advanced per appended tensor
+    // (selects, no branches around the stores)
+    uint32_t b0 = rl.end[0] + (blo & 0xFFFFu) + (pre & 0x3FFu);
+    uint32_t b1 = rl.end[1] + (blo >> 16) + ((pre >> 10) & 0x3FFu);
+    uint32_t b2 = rl.end[2] + (bhi & 0xFFFFu) + (pre >> 20);
 #pragma unroll
     for (int j = 0; j < M; ++j) {
-        if (dec[j] && (old[j] & kPendMask) == 1u) {
-            const uint32_t c = (old[j] >> kClassShift) & 3u;
-            const uint32_t k = c == 0 ? at[0]++ : (c == 1 ? at[1]++ : at[2]++);
-            rl.slot[k] = (uint16_t)ids[j];
-        }
+        const bool r = dec[j] && (old[j] & kPendMask) == 1u;
+        const uint32_t c = (old[j] >> kClassShift) & 3u;
+        const uint32_t at = c == 0 ? b0 : (c == 1 ? b1 : b2);
+        if (r) rl.slot[at] = (uint16_t)ids[j];
+        b0 += (r && c == 0) ? 1u : 0u;
+        b1 += (r && c == 1) ? 1u : 0u;
+        b2 += (r && c == 2) ? 1u : 0u;
     }
 }
 
 // BEST_FIT (the tightest-gap reading of Section 2.3's "best fit"): among the
 // free gaps between the placed neighbours' ranges, the smallest one that
 // holds s units, the lowest start among equals; the space above every range
-// only when no finite gap holds s.  A group of LANES lanes holds 4 ranges
-// per lane, element i = 4 l + r at lane l (0 <= l < LANES) and slot r; the
-// group sorts them by offset (bitonic network: slots within a lane, lanes by
-// exchanges with lane l ^ d), takes running maxima of the ends in that order
-// (gap before element i: [max end of elements < i, offset of i)) and a
-// minimum over (gap length, gap start).  Unplaced ranges (bit 31 of the
-// offset half set) sort last and bound no gap.  Every lane of the group gets
-// the result.
+// only when no finite gap holds s.  A group of LANES lanes holds kSlots
+// ranges per lane, element i = kSlots l + r at lane l (0 <= l < LANES) and
+// slot r; the group sorts them by offset (bitonic network: slots within a
+// lane, lanes by exchanges with lane l ^ d), takes running maxima of the ends
+// in that order (gap before element i: [max end of elements < i, offset of
+// i)) and a minimum over (gap length, gap start).  Unplaced ranges (bit 31 of
+// the offset half set) sort last and bound no gap.  Every lane of the group
+// gets the result.
 template <int LANES>
 __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots], uint32_t s,
                                    uint32_t l) {
-    static_assert(kSlots == 4, "4 ranges per lane");
-    constexpr int kN = 4 * LANES;
+    constexpr int kN = kSlots * LANES;
 #pragma unroll
     for (int k = 2; k <= kN; k <<= 1) {
 #pragma unroll
         for (int j = k >> 1; j >= 1; j >>= 1) {
-            if (j < 4) {
+            if (j < kSlots) {
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
+                for (int r = 0; r < kSlots; ++r) {
                     const int r2 = r ^ j;
                     if (r2 > r) {
-                        const bool up = (((4u * l + (uint32_t)r) & (uint32_t)k) == 0);
+                        const bool up = ((((uint32_t)kSlots * l + (uint32_t)r) & (uint32_t)k) == 0);
                         const bool sw = up ? (o[r] > o[r2]) : (o[r] < o[r2]);
                         const uint32_t oa = o[r], ea = e[r];
                         o[r] = sw ? o[r2] : oa;
@@ -293,13 +296,13 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
                     }
                 }
             } else {
-                const int d = j >> 2;  // partner lane l ^ d, same slot
+                const int d = j / kSlots;  // partner lane l ^ d, same slot
                 const bool lower = (l & (uint32_t)d) == 0;
 #pragma unroll
-                for (int r = 0; r < 4; ++r) {
+                for (int r = 0; r < kSlots; ++r) {
                     const uint32_t po = (uint32_t)__shfl_xor((int)o[r], d, LANES);
                     const uint32_t pe = (uint32_t)__shfl_xor((int)e[r], d, LANES);
-                    const bool up = (((4u * l + (uint32_t)r) & (uint32_t)k) == 0);
+                    const bool up = ((((uint32_t)kSlots * l + (uint32_t)r) & (uint32_t)k) == 0);
                     const bool take = (lower == up) ? (po < o[r]) : (po > o[r]);
                     o[r] = take ? po : o[r];
                     e[r] = take ? pe : e[r];
@@ -309,9 +312,9 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
     }
     // running maximum of the placed ends: within the lane, then over the
     // lanes before it
-    uint32_t incl[4], run = 0;
+    uint32_t incl[kSlots], run = 0;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < kSlots; ++r) {
         run = max(run, o[r] < kUnplacedBit ? e[r] : 0u);
         incl[r] = run;
     }
@@ -326,7 +329,7 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
     const uint32_t top = (uint32_t)__shfl((int)scan, LANES - 1, LANES);
     uint64_t best = ~0ull;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < kSlots; ++r) {
         const uint32_t pm = r == 0 ? before : max(before, incl[r - 1]);
         const bool ok = o[r] < kUnplacedBit && o[r] >= pm && o[r] - pm >= s;
         const uint64_t key = ((uint64_t)(o[r] - pm) << 32) | pm;
@@ -340,72 +343,6 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
         best = other < best ? other : best;
     }
     return best != ~0ull ? (uint32_t)best : top;
-}
-
-// Whole-wave placement of tensor q (all 64 lanes active, arguments uniform):
-// the neighbour sequence is swept in chunks of 256, each lane holding up to 4
-// neighbours; within a chunk the candidate offset jumps to the highest end
-// overlapping [x, x + s) until nothing in the chunk overlaps, and chunks are
-// revisited until a full lap leaves x alone.  Then q is published and its
-// successors' pending counts are decremented.  BEST_FIT tensors reach here
-// with at most 256 neighbours (more go to the general path): one chunk,
-// sorted by the wave.
-__device__ void place_wave(uint32_t q, uint32_t s, uint32_t lb, uint32_t L, uint32_t K,
-                           uint64_t* ofsz, const LeftLists& ll, const ReadyLists& rl, int lane,
-                           bool best) {
-    const uint32_t nch = (K + kCoopChunk - 1) / kCoopChunk;
-    uint32_t id[kSlots], co[kSlots], ce[kSlots], sc[kSlots];
-    auto load = [&](uint32_t kb) {
-        uint32_t pl[kSlots];
-#pragma unroll
-        for (int r = 0; r < kSlots; ++r) {
-            const uint32_t k = kb + r * kWave + lane;
-            pl[r] = left_pos(q, ll.ent[k < L ? lb + k : lb], ll);  // in bounds: padded
-        }
-        uint64_t w[kSlots];
-#pragma unroll
-        for (int r = 0; r < kSlots; ++r) {
-            id[r] = neighbour(kb + r * kWave + lane, L, K, q, pl[r]);
-            w[r] = ofsz[id[r]];
-        }
-#pragma unroll
-        for (int r = 0; r < kSlots; ++r) {
-            const uint32_t k = kb + r * kWave + lane;
-            co[r] = word_off(w[r]);
-            ce[r] = word_end(w[r]);
-            sc[r] = (k < K && is_successor(k, L, (uint32_t)w[r], s)) ? 1u : 0u;
-        }
-    };
-    uint32_t x = 0, clean = best ? nch : 0, c = 0;
-    if (best) {
-        load(0);
-        x = best_fit_group<kWave>(co, ce, s, (uint32_t)lane);
-    }
-    while (clean < nch) {
-        load(c * kCoopChunk);
-        bool moved = false;
-        while (true) {  // jump past the highest end overlapping [x, x + s)
-            bool ov = false;
-            uint32_t mx = 0;
-#pragma unroll
-            for (int r = 0; r < kSlots; ++r) {
-                if (co[r] < x + s && x < ce[r]) {
-                    ov = true;
-                    mx = max(mx, ce[r]);
-                }
-            }
-            if (!__ballot(ov)) break;
-            x = wave_max_u32(mx);
-            moved = true;
-        }
-        clean = moved ? 1u : clean + 1u;
-        c = (c + 1 == nch) ? 0u : c + 1;
-    }
-    if (lane == 0) ofsz[q] = ((uint64_t)x << 32) | s;
-    for (uint32_t cc = 0; cc < nch; ++cc) {
-        if (nch > 1) load(cc * kCoopChunk);
-        release_successors(sc, id, ofsz, rl, lane);
-    }
 }
 
 // A tensor being fitted by a lane group: its position, size, left-list start,
@@ -431,44 +368,113 @@ __device__ __forceinline__ Item load_item(uint32_t q, bool has, uint32_t spare,
     return it;
 }
 
-// The neighbours k = 4g + r (r < kSlots) of a group's tensor, for the lane
-// at position g of its group: positions, ranges [o, e) and successor flags.
-// Slots past the neighbour count read the tensor's own word, which is
-// unplaced: an unplaced word never overlaps.
-__device__ __forceinline__ void gather_group(const Item& it, uint32_t g, const uint64_t* ofsz,
-                                             const LeftLists& ll, uint32_t (&id)[kSlots],
-                                             uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
-                                             uint32_t (&sc)[kSlots]) {
-    const uint32_t k0 = g * kSlots;
-    uint32_t lv[kSlots];
-#pragma unroll
-    for (int r = 0; r < kSlots; ++r) {
-        const uint32_t k = k0 + r;
-        lv[r] = ll.ent[k < it.L ? it.lb + k : it.lb];  // in bounds: the lists are padded
+// The neighbours k = S g + r (r < S) of a group's tensor, for the lane at
+// position g of its group: o[r] is a placed neighbour's offset, or for an
+// unplaced one kUnplacedBit | its position (never overlapping, and what the
+// release needs); e[r] the placed neighbour's end.  The lane's left-list
+// entries are consecutive bytes, read as aligned words.  Slots past the
+// neighbour count read the tensor's own word, which is unplaced.  LONG: the
+// trace has long tensors (entries at or above kLongBase name one through
+// the table).
+template <int S, bool LONG>
+__device__ __forceinline__ void gather(const Item& it, uint32_t g, const uint64_t* ofsz,
+                                       const LeftLists& ll, uint32_t (&o)[S], uint32_t (&e)[S]) {
+    static_assert(S == 4 || S == 8, "4 or 8 slots a lane");
+    uint32_t id[S];
+    const uint32_t k0 = g * S;
+    const uint32_t s0 = it.lb + min(k0, it.L);  // at most the list capacity: in bounds (padded)
+    const uint32_t* w32 = reinterpret_cast<const uint32_t*>(ll.ent) + (s0 >> 2);
+    uint32_t by[S / 4];
+    {
+        const uint32_t b0 = w32[0], b1 = w32[1];
+        by[0] = __builtin_amdgcn_alignbyte(b1, b0, s0 & 3u);
+        if (S == 8) by[S / 4 - 1] = __builtin_amdgcn_alignbyte(w32[2], b1, s0 & 3u);
     }
-    uint64_t w[kSlots];
+    // slot r holds neighbour k0 + r: left entry r when r < lr, band position
+    // rb + r when lr <= r < kr, the tensor itself beyond
+    const int lr = (int)it.L - (int)k0, kr = (int)it.K - (int)k0;
+    const uint32_t rb = it.q + 1u - (uint32_t)lr;
 #pragma unroll
-    for (int r = 0; r < kSlots; ++r) {
-        id[r] = neighbour(k0 + r, it.L, it.K, it.q, left_pos(it.q, lv[r], ll));
-        w[r] = ofsz[id[r]];
+    for (int r = 0; r < S; ++r) {
+        const uint32_t ent = (by[r >> 2] >> (8 * (r & 3))) & 0xFFu;
+        uint32_t pl = it.q - ent;
+        if (LONG && ent >= kLongBase) pl = ll.longtab[ent - kLongBase];
+        id[r] = r < lr ? pl : (r < kr ? rb + (uint32_t)r : it.q);
     }
+    uint64_t w[S];
 #pragma unroll
-    for (int r = 0; r < kSlots; ++r) {
-        const uint32_t k = k0 + r;
-        o[r] = word_off(w[r]);
+    for (int r = 0; r < S; ++r) w[r] = ofsz[id[r]];
+#pragma unroll
+    for (int r = 0; r < S; ++r) {
+        const uint32_t wo = word_off(w[r]);
+        o[r] = wo < kUnplacedBit ? wo : (kUnplacedBit | id[r]);
         e[r] = word_end(w[r]);
-        sc[r] = (k < it.K && is_successor(k, it.L, (uint32_t)w[r], it.s)) ? 1u : 0u;
+    }
+}
+
+// Successors of a gathered lane: the unplaced neighbours within the count
+// (dec[r] = 1) and the positions to decrement (every slot names a word:
+// subtracting 0 changes nothing).
+template <int S>
+__device__ __forceinline__ void successors(uint32_t k0, uint32_t K, const uint32_t (&o)[S],
+                                           uint32_t (&dec)[S], uint32_t (&ids)[S]) {
+    const int kr = (int)K - (int)k0;
+#pragma unroll
+    for (int r = 0; r < S; ++r) {
+        dec[r] = r < kr ? is_unplaced(o[r]) : 0u;
+        ids[r] = is_unplaced(o[r]) ? (o[r] & 0xFFFFu) : 0u;
     }
 }
 
 // Highest end among the lane's ranges that overlap [x, x + s), 0 if none.
-__device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[kSlots],
-                                                const uint32_t (&e)[kSlots], uint32_t x,
-                                                uint32_t s) {
+template <int S>
+__device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[S], const uint32_t (&e)[S],
+                                                uint32_t x, uint32_t s) {
     uint32_t m = 0;
 #pragma unroll
-    for (int r = 0; r < kSlots; ++r) m = (o[r] < x + s && x < e[r]) ? max(m, e[r]) : m;
+    for (int r = 0; r < S; ++r) m = (o[r] < x + s && x < e[r]) ? max(m, e[r]) : m;
     return m;
+}
+
+// Whole-wave placement of tensor q (all 64 lanes active, arguments uniform):
+// the neighbour sequence is swept in chunks of kCoopChunk, lane l holding
+// neighbours kSlots l .. kSlots l + kSlots - 1 of the chunk; within a chunk
+// the candidate offset jumps to the highest end overlapping [x, x + s) until
+// nothing in the chunk overlaps, and chunks are revisited until a full lap
+// leaves x alone.  Then q is published and its successors' pending counts are
+// decremented.  BEST_FIT tensors reach here with at most kCoopChunk
+// neighbours (more go to the general path): one chunk, sorted by the wave.
+template <bool LONG>
+__device__ void place_wave(const Item& it, uint64_t* ofsz, const LeftLists& ll,
+                           const ReadyLists& rl, int lane, bool best) {
+    const uint32_t nch = (it.K + kCoopChunk - 1) / kCoopChunk;
+    uint32_t co[kSlots], ce[kSlots];
+    const uint32_t g0 = (uint32_t)lane;
+    auto load = [&](uint32_t c) { gather<kSlots, LONG>(it, c * kWave + g0, ofsz, ll, co, ce); };
+    uint32_t x = 0, clean = best ? nch : 0, c = 0;
+    if (best) {
+        load(0);
+        x = best_fit_group<kWave>(co, ce, it.s, (uint32_t)lane);
+    }
+    while (clean < nch) {
+        if (nch > 1 || c == 0) load(c);
+        bool moved = false;
+        while (true) {  // jump past the highest end overlapping [x, x + s)
+            const uint32_t mx = overlap_end(co, ce, x, it.s);
+            if (!__ballot(mx > x)) break;
+            x = wave_max_u32(mx);
+            moved = true;
+        }
+        clean = moved ? 1u : clean + 1u;
+        c = (c + 1 == nch) ? 0u : c + 1;
+    }
+    if (lane == 0) ofsz[it.q] = ((uint64_t)x << 32) | it.s;
+    for (uint32_t cc = 0; cc < nch; ++cc) {
+        if (nch > 1 || best) load(cc);  // (the best-fit sort permuted the slots)
+        uint32_t dec[kSlots], ids[kSlots];
+        successors((cc * kWave + g0) * kSlots, it.K, co, dec, ids);
+        release_successors(dec, ids, ofsz, rl, lane);
+    }
 }
 
 // ------------------------------------------------------------ general path
@@ -1114,19 +1120,20 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     // r fits every tensor released in round r - 1 -- all of its predecessors
     // are placed, and no two of them intersect.  Lanes are dealt out over the
     // workgroup, quads first (tensors of 9..16 neighbours) and then lane
-    // pairs (up to 8), four neighbours per lane, so groups stay aligned; rows
-    // of 16 lanes (up to 64 neighbours; the whole wave beyond) take the rest
-    // from the last wave down.  A group gathers the neighbours' words (the
+    // pairs (up to 8), four neighbours per lane, so groups stay aligned;
+    // rows of 16 lanes (up to 64 neighbours; the whole wave beyond) take the
+    // rest from the last wave down.  A group gathers the neighbours' words (the
     // placed ones are exactly the predecessors), moves the candidate offset
     // past the highest overlapping end until nothing overlaps, publishes the
     // word and decrements its successors' pending counts; those reaching zero
     // are appended for the next round.  Per-round append counters rotate over
     // three slots so that one barrier per round suffices.
-    {
+    auto place_rounds = [&](auto long_tag) {
+        constexpr bool LONG = decltype(long_tag)::value;
         const LeftLists ll{lents, longtab};
         const int lane = lane_id;
         const uint32_t g16 = lane & 15, row = (uint32_t)tid >> 4;
-        constexpr uint32_t kRows = BLOCK / 16;
+        constexpr uint32_t kRows = BLOCK / kRowLanes;
         uint32_t bgn[3] = {0, 0, 0}, end[3] = {seeds[0], seeds[1], seeds[2]};
         for (int round = 0; bgn[0] < end[0] || bgn[1] < end[1] || bgn[2] < end[2]; ++round) {
             if (round > n) {  // cannot happen: every round places a tensor
@@ -1155,8 +1162,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 if (!any_s && !any_b) break;
                 if (any_s) {
                     const Item is = load_item(qs, hs, spare, ofsz, lbeg, rlen);
-                    uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group(is, g, ofsz, ll, id, o, e, sc);
+                    uint32_t o[kSmallSlots], e[kSmallSlots];
+                    gather<kSmallSlots, LONG>(is, g, ofsz, ll, o, e);
                     uint32_t x = 0;
                     while (true) {  // jump past the highest overlapping end until none moves
                         const uint32_t mm = pair_quad_max_u32(overlap_end(o, e, x, is.s), quad);
@@ -1165,16 +1172,21 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                         if (!__ballot(mv)) break;
                     }
                     if (hs && g == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
-                    release_successors(sc, id, ofsz, rl, lane);
+                    uint32_t dec[kSmallSlots], ids[kSmallSlots];
+                    successors(g * kSmallSlots, is.K, o, dec, ids);
+                    release_successors(dec, ids, ofsz, rl, lane);
                 }
                 if (any_b) {
                     const Item ib = load_item(qb, hb, spare, ofsz, lbeg, rlen);
-                    const bool mid = hb && ib.K <= kMidK;
+                    const bool mid = hb && ib.K <= kRowK;
                     const Item im = mid ? ib : Item{spare, 0, 0, 0, 0};  // wider: whole wave
-                    uint32_t id[kSlots], o[kSlots], e[kSlots], sc[kSlots];
-                    gather_group(im, g16, ofsz, ll, id, o, e, sc);
+                    uint32_t o[kSlots], e[kSlots], dec[kSlots], ids[kSlots];
+                    gather<kSlots, LONG>(im, g16, ofsz, ll, o, e);
                     uint32_t x = 0;
-                    if (best) x = best_fit_group<16>(o, e, im.s, g16);
+                    if (best) {  // the sort permutes the slots: successors first
+                        successors(g16 * kSlots, im.K, o, dec, ids);
+                        x = best_fit_group<kRowLanes>(o, e, im.s, g16);
+                    }
                     while (!best) {
                         const uint32_t mm = row_max_u32(overlap_end(o, e, x, im.s));
                         const bool mv = mm > x;
@@ -1182,18 +1194,27 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                         if (!__ballot(mv)) break;
                     }
                     if (mid && g16 == 0) ofsz[ib.q] = ((uint64_t)x << 32) | ib.s;
-                    release_successors(sc, id, ofsz, rl, lane);
-                    uint64_t wide = __ballot(hb && !mid && g16 == 0);
-                    while (wide) {
-                        const int src = __ffsll((long long)wide) - 1;
-                        wide &= wide - 1;
-                        place_wave((uint32_t)__builtin_amdgcn_readlane((int)ib.q, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.s, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.lb, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.L, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)ib.K, src), ofsz,
-                                   ll, rl, lane, best);
-                    }
+                    if (!best) successors(g16 * kSlots, im.K, o, dec, ids);
+                    release_successors(dec, ids, ofsz, rl, lane);
+                }
+            }
+            // class-2 tensors with more than 64 neighbours: the whole wave
+            // each, dealt over the waves
+            for (uint32_t i0 = bgn[2] + (uint32_t)(tid & ~(kWave - 1)); i0 < end[2];
+                 i0 += BLOCK) {
+                const uint32_t i = i0 + (uint32_t)lane;
+                const uint32_t qw = i < end[2] ? (uint32_t)readyq[region[2] + i] : 0u;
+                const Item iw = load_item(qw, i < end[2], spare, ofsz, lbeg, rlen);
+                uint64_t wide = __ballot(i < end[2] && iw.K > kRowK);
+                while (wide) {
+                    const int src = __ffsll((long long)wide) - 1;
+                    wide &= wide - 1;
+                    const Item one{(uint32_t)__builtin_amdgcn_readlane((int)iw.q, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.s, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.lb, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.L, src),
+                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.K, src)};
+                    place_wave<LONG>(one, ofsz, ll, rl, lane, best);
                 }
             }
             __syncthreads();
@@ -1204,7 +1225,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 end[c] += (uint32_t)(added >> (16 * c)) & 0xFFFFu;
             }
         }
-    }
+    };
+    if (nlong) place_rounds(std::true_type{});
+    else place_rounds(std::false_type{});
     __syncthreads();
     MP_STAMP(6);
 
@@ -1230,14 +1253,14 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
 __global__ void reset_status_kernel(int32_t* status) { *status = MP_OK; }
 
-template <int ITEMS, bool BEST>
+template <int BLOCK, int ITEMS, bool BEST>
 hipError_t launch_items(const BatchArgs& a, const BatchShape& s, hipStream_t st) {
-    auto kern = plan_batch_kernel<kBatchBlock, ITEMS, BEST>;
+    auto kern = plan_batch_kernel<BLOCK, ITEMS, BEST>;
     hipError_t e = hipFuncSetAttribute((const void*)kern,
                                        hipFuncAttributeMaxDynamicSharedMemorySize,
                                        (int)s.lds_bytes);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(kern, dim3((unsigned)a.n_traces), dim3(kBatchBlock), s.lds_bytes, st,
+    hipLaunchKernelGGL(kern, dim3((unsigned)a.n_traces), dim3(BLOCK), s.lds_bytes, st,
                        a.begin, a.num_ops, a.size, a.first, a.last, a.n_tensors, s.cap_n,
                        s.cap_pairs, static_cast<unsigned char*>(a.workspace), a.offset_out,
                        a.peak_out, a.lb_out, a.status);
@@ -1303,7 +1326,7 @@ BatchShape batch_shape(int64_t max_trace_len) {
     s.cap_n = (int32_t)N;
     s.cap_pairs = (int32_t)cap;
     s.lds_bytes = batch_lds((size_t)N, (size_t)cap).total;
-    int items = 1;
+    int items = 1;  // tensor slots per thread
     while (items * kBatchBlock < N) items <<= 1;
     s.items = items;
     s.ok = true;
@@ -1319,11 +1342,12 @@ hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st) {
     const BatchShape s = batch_shape(a.max_trace_len);
     if (!s.ok) return hipErrorInvalidValue;
     const bool best = a.policy == MP_BEST_FIT;
+    constexpr int B = kBatchBlock;
     switch (s.items) {
-        case 1: return best ? launch_items<1, true>(a, s, st) : launch_items<1, false>(a, s, st);
-        case 2: return best ? launch_items<2, true>(a, s, st) : launch_items<2, false>(a, s, st);
-        case 4: return best ? launch_items<4, true>(a, s, st) : launch_items<4, false>(a, s, st);
-        case 8: return best ? launch_items<8, true>(a, s, st) : launch_items<8, false>(a, s, st);
+        case 1: return best ? launch_items<B, 1, true>(a, s, st) : launch_items<B, 1, false>(a, s, st);
+        case 2: return best ? launch_items<B, 2, true>(a, s, st) : launch_items<B, 2, false>(a, s, st);
+        case 4: return best ? launch_items<B, 4, true>(a, s, st) : launch_items<B, 4, false>(a, s, st);
+        case 8: return best ? launch_items<B, 8, true>(a, s, st) : launch_items<B, 8, false>(a, s, st);
         default: return hipErrorInvalidValue;
     }
 }
