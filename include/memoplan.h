@@ -106,15 +106,21 @@ int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num
 int64_t mp_batch_pair_capacity(int64_t max_trace_len);
 
 /* Greedy-by-size plan of one trace of any length, using the whole device
- * (one cooperative persistent launch places the tensors).
+ * (a persistent kernel: workgroups take tensors in rank order from a counter
+ * and each fits its tensor once the earlier-ranked tensors that meet it are
+ * placed).
  *   size, first, last [n] (int64, int32, int32), 0 <= n < 2^30.
  *   offset_out[n] int64, peak_out: one device int64 (arena bytes).
  *   policy: MP_LOWEST_FIT or MP_BEST_FIT.
- *   workspace: mp_workspace_size(MP_OP_PLAN_TRACE, n, num_ops, 0) bytes; its
- *              contents need no initialisation.
- * Capacity limits (MP_ENOSPC on device): the sum of the sizes divided by
- * 2^ctz(OR of sizes) must be < 2^32, and a tensor may have at most 131072
- * earlier-ranked lifetime-intersecting tensors.
+ *   workspace: mp_workspace_bytes(MP_OP_PLAN_TRACE, n, num_ops, 1) bytes on
+ *              the current device (it depends on the CU count); its contents
+ *              need no initialisation.
+ * Every valid trace is planned: offsets are kept as 32-bit counts of
+ * 2^ctz(OR of sizes) while the sizes sum to less than 2^32 - 1 such units,
+ * as 64-bit counts beyond (chosen on the device); a tensor with more
+ * earlier-ranked intersecting tensors than its workgroup's buffer holds
+ * (131072, or 32768 with 64-bit counts) waits until all of them are placed,
+ * takes one of two shared buffers of n ranges and is fitted there.
  * Tensors need not be sorted by first. */
 int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
                       int32_t num_ops, int32_t policy, int64_t* offset_out, int64_t* peak_out,

@@ -47,10 +47,15 @@ constexpr int64_t kScratchRuns = 8;  // global scratch per workgroup: 8 sorted r
 constexpr uint32_t kUnplacedT = 0xFFFFFFFFu;
 constexpr int kLongMax = 4096;    // the long list is kept at most this long when possible
 
+constexpr int kPoolSlots = 2;        // shared scratch for predecessor sets beyond a workgroup's own
+constexpr uint64_t kUnplaced64 = ~0ull;
+
 struct TFlags {
-    uint32_t unsorted, sorted, abort, pad0;
+    uint32_t unsorted, sorted, abort, wide;
     uint64_t or_all, sum;
     uint32_t shift, lthr, n_long, ticket;
+    uint32_t skip_narrow, skip_wide;  // nonzero: the 32-bit (64-bit) unit path does not run
+    uint32_t pool[kPoolSlots];        // 1 while a workgroup holds the slot
     uint32_t hist[64];      // band lengths by bit width
     uint64_t peak;
     int64_t long_prefix_tiles;
@@ -67,10 +72,14 @@ struct TView {  // position-ordered arrays
 __global__ void t_init_kernel(TFlags* fl) {
     const int i = threadIdx.x;
     if (i < 64) fl->hist[i] = 0;
+    if (i < kPoolSlots) fl->pool[i] = 0;
     if (i == 0) {
         fl->unsorted = 0;
         fl->sorted = 1;
         fl->abort = 0;
+        fl->wide = 0;
+        fl->skip_narrow = 1;
+        fl->skip_wide = 1;
         fl->or_all = 0;
         fl->sum = 0;
         fl->shift = 0;
@@ -123,16 +132,18 @@ __global__ __launch_bounds__(256) void t_ingest_kernel(const int64_t* __restrict
     }
 }
 
-// unit shift; offsets are kept as 32-bit counts of the unit
-__global__ void t_unit_kernel(TFlags* fl, int32_t* status) {
+// unit shift, and the offset width: 32-bit counts of the unit while the
+// sizes sum to less than 2^32 - 1 units (every offset and end then fits
+// below the unplaced sentinel), 64-bit counts beyond
+__global__ void t_unit_kernel(TFlags* fl) {
     if (fl->abort) return;
     const uint64_t o = fl->or_all;
     const uint32_t sh = o ? (uint32_t)__builtin_ctzll(o) : 0u;
     fl->shift = sh;
-    if ((fl->sum >> sh) > 0xFFFFFFFEull) {
-        raise_status(status, MP_ENOSPC);
-        fl->abort = 1;
-    }
+    const uint32_t wide = (fl->sum >> sh) > 0xFFFFFFFEull ? 1u : 0u;
+    fl->wide = wide;
+    fl->skip_narrow = wide;
+    fl->skip_wide = 1u - wide;
 }
 
 __global__ void t_keys_first_kernel(const int32_t* __restrict__ first, int64_t n,
@@ -153,20 +164,26 @@ __global__ void t_positions_kernel(const uint32_t* __restrict__ perm,
                                    const int32_t* __restrict__ last, int64_t n,
                                    uint32_t* __restrict__ su, int32_t* __restrict__ pf,
                                    int32_t* __restrict__ pl, uint32_t* __restrict__ pid,
-                                   uint32_t* __restrict__ off, const TFlags* fl) {
+                                   uint32_t* __restrict__ off, uint64_t* __restrict__ su64,
+                                   uint64_t* __restrict__ off64, const TFlags* fl) {
     if (fl->abort) return;
-    const bool uns = fl->unsorted != 0;
+    const bool uns = fl->unsorted != 0, wide = fl->wide != 0;
     const uint32_t sh = fl->shift;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
         const uint32_t i = uns ? perm[q] : (uint32_t)q;
-        su[q] = (uint32_t)((uint64_t)size[i] >> sh);
+        if (wide) {
+            su64[q] = (uint64_t)size[i] >> sh;
+            off64[q] = kUnplaced64;
+        } else {
+            su[q] = (uint32_t)((uint64_t)size[i] >> sh);
+            off[q] = kUnplacedT;
+        }
         if (uns) {
             pf[q] = first[i];
             pl[q] = last[i];
         }
         pid[q] = i;
-        off[q] = kUnplacedT;
     }
 }
 
@@ -251,13 +268,16 @@ __global__ void t_long_list_kernel(const int32_t* __restrict__ reach,
     }
 }
 
-__global__ void t_rank_keys_kernel(const uint32_t* __restrict__ su, int64_t n,
+__global__ void t_rank_keys_kernel(const uint32_t* __restrict__ su,
+                                   const uint64_t* __restrict__ su64, int64_t n,
                                    uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
                                    const TFlags* fl) {
     if (fl->abort) return;
+    const bool wide = fl->wide != 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
-        keys[q] = (uint64_t)(0xFFFFFFFFu - su[q]);  // size descending; ties keep position order
+        // size descending; ties keep position order (the sort is stable)
+        keys[q] = wide ? ~su64[q] : (uint64_t)(0xFFFFFFFFu - su[q]);
         vals[q] = (uint32_t)q;
     }
 }
@@ -269,8 +289,23 @@ __global__ void t_rank_keys_kernel(const uint32_t* __restrict__ su, int64_t n,
 __device__ __forceinline__ uint32_t agent_load(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// The publish stays an ordinary (cached) relaxed store: a non-temporal store
+// was never seen by pollers on other XCDs.
 __device__ __forceinline__ void agent_store(uint32_t* p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t agent_load64(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void agent_store64(uint64_t* p, uint64_t v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// Barrier after which every thread's global stores of the workgroup are
+// complete (the workgroup barrier alone does not wait for them); readers then
+// load through L2 (agent_load64).
+__device__ __forceinline__ void l2_barrier() {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
 }
 
 template <int BLOCK>
@@ -495,7 +530,8 @@ struct PlaceArgs {
     const int32_t* long_list;
     uint32_t* off;
     uint64_t* run_keys;  // per workgroup: stat_cap keys
-    int64_t stat_cap;    // min(n, kScratchRuns * kRunCap): a tensor has < n predecessors
+    int64_t stat_cap;    // min(4 n, kScratchRuns * kRunCap)
+    uint64_t* pool;      // kPoolSlots x 4 arrays of n ranges, for larger predecessor sets
     int64_t n;
     TFlags* fl;
     int32_t* status;
@@ -509,27 +545,34 @@ struct PlaceArgs {
 // and reaches, then offsets), so the latencies overlap.
 constexpr int kBatch = 4;
 
-template <int BLOCK, typename F>
-__device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, uint32_t st,
-                                              uint32_t lthr, uint32_t n_long, F&& fn) {
+// The candidate walk over positions, for either width of sizes (SZ) and
+// offsets (OF, kUnplaced of that width while unplaced).
+template <int BLOCK, typename SZ, typename OF, typename F>
+__device__ __forceinline__ void walk_preds(const int32_t* reach, const SZ* su, const OF* off,
+                                           const int32_t* long_list, int32_t qt, SZ st,
+                                           uint32_t lthr, uint32_t n_long, F&& fn) {
+    auto load_off = [&](int32_t p) -> OF {
+        if constexpr (sizeof(OF) == 8) return agent_load64(reinterpret_cast<const uint64_t*>(off) + p);
+        else return agent_load(reinterpret_cast<const uint32_t*>(off) + p);
+    };
     auto finish = [&](const int32_t (&pp)[kBatch], const bool (&ok)[kBatch]) {
-        uint32_t o[kBatch];
+        OF o[kBatch];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) o[u] = ok[u] ? agent_load(a.off + pp[u]) : 0u;
+        for (int u = 0; u < kBatch; ++u) o[u] = ok[u] ? load_off(pp[u]) : OF(0);
 #pragma unroll
         for (int u = 0; u < kBatch; ++u)
             if (ok[u]) fn(pp[u], o[u]);
     };
-    const int32_t rt = a.reach[qt];
+    const int32_t rt = reach[qt];
     // forward band: meets t; ranked before t iff strictly larger
     for (int32_t j0 = qt + 1 + (int32_t)threadIdx.x; j0 < rt; j0 += BLOCK * kBatch) {
         int32_t pp[kBatch];
         bool ok[kBatch];
-        uint32_t sz[kBatch];
+        SZ sz[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             pp[u] = j0 + u * BLOCK;
-            sz[u] = pp[u] < rt ? a.su[pp[u]] : 0u;
+            sz[u] = pp[u] < rt ? su[pp[u]] : SZ(0);
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) ok[u] = pp[u] < rt && sz[u] > st;
@@ -540,13 +583,13 @@ __device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, ui
     for (int64_t p0 = (lo > 0 ? lo : 0) + threadIdx.x; p0 < qt; p0 += BLOCK * kBatch) {
         int32_t pp[kBatch], rr[kBatch];
         bool ok[kBatch];
-        uint32_t sz[kBatch];
+        SZ sz[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int64_t p = p0 + (int64_t)u * BLOCK;
             pp[u] = (int32_t)p;
-            rr[u] = p < qt ? a.reach[p] : 0;
-            sz[u] = p < qt ? a.su[p] : 0u;
+            rr[u] = p < qt ? reach[p] : 0;
+            sz[u] = p < qt ? su[p] : SZ(0);
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u)
@@ -557,20 +600,275 @@ __device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, ui
     for (uint32_t k0 = threadIdx.x; k0 < n_long; k0 += BLOCK * kBatch) {
         int32_t pp[kBatch], rr[kBatch];
         bool ok[kBatch];
-        uint32_t sz[kBatch];
+        SZ sz[kBatch];
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const uint32_t k = k0 + u * BLOCK;
-            pp[u] = k < n_long ? a.long_list[k] : qt;
+            pp[u] = k < n_long ? long_list[k] : qt;
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
-            rr[u] = pp[u] < qt ? a.reach[pp[u]] : 0;
-            sz[u] = pp[u] < qt ? a.su[pp[u]] : 0u;
+            rr[u] = pp[u] < qt ? reach[pp[u]] : 0;
+            sz[u] = pp[u] < qt ? su[pp[u]] : SZ(0);
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) ok[u] = pp[u] < qt && rr[u] > qt && sz[u] >= st;
         finish(pp, ok);
+    }
+}
+
+template <int BLOCK, typename F>
+__device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, uint32_t st,
+                                              uint32_t lthr, uint32_t n_long, F&& fn) {
+    walk_preds<BLOCK, uint32_t, uint32_t>(a.reach, a.su, a.off, a.long_list, qt, st, lthr,
+                                          n_long, fn);
+}
+
+// ------------------------------------------------- general fit (any width)
+//
+// The placed predecessors of a tensor as byte ranges (start, end), 64-bit, in
+// two global arrays (ks, ke) with a second pair (ts, te) of the same length
+// for merging: sorted by start in LDS runs of kGRun, runs merged pairwise
+// (merge path: each thread's share of the output found by a binary search on
+// the two runs), then one pass over the sorted ranges with running maxima of
+// the ends -- the gap before range i runs from the maximum end below it to
+// its start.  Lowest fit: the first gap that holds s, else the top; BEST_FIT:
+// the tightest such gap (lowest start among equals), else the top.  Every
+// thread returns the offset.  Global reads of data other threads wrote go
+// through L2 (agent_load64) after an l2_barrier.
+constexpr int kGRun = 8192;
+
+struct GenRanges {
+    uint64_t* ks;
+    uint64_t* ke;
+    uint64_t* ts;
+    uint64_t* te;
+};
+
+template <int BLOCK>
+__device__ uint64_t fit_general(GenRanges g, uint32_t m, uint64_t s, bool best, uint64_t* lks,
+                                uint64_t* lke, uint64_t* red64) {
+    const int tid = threadIdx.x;
+    l2_barrier();
+    // 1. runs of kGRun sorted by start in LDS
+    for (uint32_t r0 = 0; r0 < m; r0 += kGRun) {
+        const uint32_t len = min((uint32_t)kGRun, m - r0);
+        uint32_t p2 = 1;
+        while (p2 < len) p2 <<= 1;
+        for (uint32_t i = tid; i < p2; i += BLOCK) {
+            lks[i] = i < len ? agent_load64(g.ks + r0 + i) : ~0ull;
+            lke[i] = i < len ? agent_load64(g.ke + r0 + i) : 0ull;
+        }
+        __syncthreads();
+        for (uint32_t k = 2; k <= p2; k <<= 1) {
+            for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+                for (uint32_t i = tid; i < (p2 >> 1); i += BLOCK) {
+                    const uint32_t lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo | j;
+                    const uint64_t a = lks[lo], b = lks[hi];
+                    const bool up = (lo & k) == 0;
+                    if ((a > b) == up) {
+                        lks[lo] = b;
+                        lks[hi] = a;
+                        const uint64_t ea = lke[lo];
+                        lke[lo] = lke[hi];
+                        lke[hi] = ea;
+                    }
+                }
+                __syncthreads();
+            }
+        }
+        for (uint32_t i = tid; i < len; i += BLOCK) {
+            g.ks[r0 + i] = lks[i];
+            g.ke[r0 + i] = lke[i];
+        }
+        __syncthreads();
+    }
+    // 2. pairwise merges of runs of width w, ping-ponging between the arrays
+    for (uint32_t w = kGRun; w < m; w <<= 1) {
+        l2_barrier();
+        const uint32_t chunk = (m + BLOCK - 1) / BLOCK;
+        const uint32_t o0 = min(m, (uint32_t)tid * chunk), o1 = min(m, o0 + chunk);
+        for (uint32_t o = o0; o < o1;) {
+            const uint32_t base = o / (2 * w) * (2 * w);  // this output's pair of runs
+            const uint32_t la = min(w, m - base), lb = min(w, m - base - la);
+            const uint64_t* A = g.ks + base;
+            const uint64_t* B = g.ks + base + la;
+            const uint32_t d = o - base, stop = min(o1, base + la + lb);
+            // co-rank: i outputs of the d come from A
+            uint32_t lo = d > lb ? d - lb : 0u, hi = min(d, la);
+            while (lo < hi) {
+                const uint32_t i = (lo + hi) >> 1;
+                if (agent_load64(B + (d - i - 1)) < agent_load64(A + i)) hi = i;
+                else lo = i + 1;
+            }
+            uint32_t i = lo, j = d - lo;
+            for (; o < stop; ++o) {
+                const bool fromA =
+                    j >= lb || (i < la && agent_load64(A + i) <= agent_load64(B + j));
+                const uint32_t src = fromA ? base + i : base + la + j;
+                g.ts[o] = agent_load64(g.ks + src);
+                g.te[o] = agent_load64(g.ke + src);
+                i += fromA ? 1u : 0u;
+                j += fromA ? 0u : 1u;
+            }
+        }
+        uint64_t* t0 = g.ks;
+        uint64_t* t1 = g.ke;
+        g.ks = g.ts;
+        g.ke = g.te;
+        g.ts = t0;
+        g.te = t1;
+    }
+    l2_barrier();
+    // 3. one pass over the sorted ranges
+    const uint32_t chunk = (m + BLOCK - 1) / BLOCK;
+    const uint32_t e0 = min(m, (uint32_t)tid * chunk), e1 = min(m, e0 + chunk);
+    uint64_t hi_end = 0;
+    for (uint32_t e = e0; e < e1; ++e) hi_end = max(hi_end, agent_load64(g.ke + e));
+    // running maximum of the ends before this thread's chunk, and overall
+    const int lane = tid & (kWave - 1), wid = tid / kWave;
+    uint64_t inc = hi_end;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const uint64_t y = __shfl_up(inc, d, kWave);
+        if (lane >= d) inc = max(inc, y);
+    }
+    if (lane == kWave - 1) red64[wid] = inc;
+    __syncthreads();
+    uint64_t run = 0, top = 0;
+#pragma unroll
+    for (int w = 0; w < BLOCK / kWave; ++w) {
+        const uint64_t t = red64[w];
+        run = w < wid ? max(run, t) : run;
+        top = max(top, t);
+    }
+    __syncthreads();
+    uint64_t prev = __shfl_up(inc, 1, kWave);
+    run = max(run, lane ? prev : 0ull);
+    uint64_t cand = ~0ull, cgap = ~0ull;
+    for (uint32_t e = e0; e < e1; ++e) {
+        const uint64_t st = agent_load64(g.ks + e), en = agent_load64(g.ke + e);
+        if (st >= run && st - run >= s) {
+            if (!best) {
+                if (cand == ~0ull) cand = run;
+            } else if (st - run < cgap) {
+                cgap = st - run;
+                cand = run;
+            }
+        }
+        run = max(run, en);
+    }
+    uint64_t x;
+    if (!best) {
+        x = block_reduce<BLOCK>(cand, OpMin<uint64_t>(), red64);
+    } else {
+        const uint64_t gm = block_reduce<BLOCK>(cgap, OpMin<uint64_t>(), red64);
+        x = block_reduce<BLOCK>(cgap == gm ? cand : ~(uint64_t)0, OpMin<uint64_t>(), red64);
+    }
+    return x == ~0ull ? top : x;
+}
+
+// One of the kPoolSlots shared predecessor buffers (n ranges each), taken
+// only by a workgroup whose tensor has all its predecessors placed, so a
+// holder never waits on anything and every wait for a slot ends.  Thread 0
+// takes it; every thread gets its index.
+__device__ uint32_t pool_acquire(TFlags* fl, uint32_t* s_slot) {
+    if (threadIdx.x == 0) {
+        uint32_t slot = 0;
+        while (true) {
+            for (slot = 0; slot < (uint32_t)kPoolSlots; ++slot)
+                if (atomicCAS(&fl->pool[slot], 0u, 1u) == 0u) break;
+            if (slot < (uint32_t)kPoolSlots) break;
+            __builtin_amdgcn_s_sleep(16);
+        }
+        *s_slot = slot;
+    }
+    __threadfence();
+    __syncthreads();
+    return *s_slot;
+}
+__device__ void pool_release(TFlags* fl, uint32_t slot) {
+    l2_barrier();
+    if (threadIdx.x == 0) {
+        __threadfence();
+        atomicExch(&fl->pool[slot], 0u);
+    }
+}
+__device__ __forceinline__ GenRanges pool_ranges(uint64_t* pool, uint32_t slot, int64_t n) {
+    uint64_t* b = pool + (int64_t)slot * 4 * n;
+    return GenRanges{b, b + n, b + 2 * n, b + 3 * n};
+}
+
+// Placement with 64-bit unit counts (the sizes sum to 2^32 - 1 units or
+// more): the same ticket order, each workgroup waiting for every
+// predecessor of its tensor before the general fit; the ranges go to the
+// workgroup's own buffers (cap each) or, beyond, to a pool slot.
+struct WideArgs {
+    const uint64_t* su;
+    const int32_t* reach;
+    const uint32_t* order;
+    const int32_t* long_list;
+    uint64_t* off;
+    uint64_t* priv;  // per workgroup: 4 arrays of cap ranges
+    int64_t cap;
+    uint64_t* pool;  // kPoolSlots x 4 arrays of n
+    int64_t n;
+    TFlags* fl;
+    int32_t best;
+};
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void t_place_wide_kernel(WideArgs a) {
+    __shared__ uint64_t lks[kGRun];
+    __shared__ uint64_t lke[kGRun];
+    __shared__ uint64_t red64[BLOCK / kWave];
+    __shared__ uint32_t s_rank, s_cnt, s_slot;
+    if (a.fl->abort || !a.fl->wide) return;
+    const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
+    uint64_t* pv = a.priv + (int64_t)blockIdx.x * 4 * a.cap;
+    const GenRanges own{pv, pv + a.cap, pv + 2 * a.cap, pv + 3 * a.cap};
+    while (true) {
+        if (threadIdx.x == 0) {
+            s_rank = atomicAdd(&a.fl->ticket, 1u);
+            s_cnt = 0;
+        }
+        __syncthreads();
+        const uint32_t r = s_rank;
+        if (r >= (uint64_t)a.n) break;
+        const int32_t qt = (int32_t)a.order[r];
+        const uint64_t st = a.su[qt];
+        auto collect = [&](const GenRanges& gr, int64_t cap) {
+            walk_preds<BLOCK, uint64_t, uint64_t>(
+                a.reach, a.su, a.off, a.long_list, qt, st, lthr, n_long, [&](int32_t p, uint64_t o) {
+                    while (o == kUnplaced64) {  // a lower rank, held by a running workgroup
+                        __builtin_amdgcn_s_sleep(2);
+                        o = agent_load64(a.off + p);
+                    }
+                    const uint32_t k = atomicAdd(&s_cnt, 1u);
+                    if (k < cap) {
+                        gr.ks[k] = o;
+                        gr.ke[k] = o + a.su[p];
+                    }
+                });
+            __syncthreads();
+        };
+        collect(own, a.cap);
+        const uint32_t m = s_cnt;
+        uint64_t x;
+        if (m <= a.cap) {
+            x = fit_general<BLOCK>(own, m, st, a.best != 0, lks, lke, red64);
+        } else {  // every predecessor is placed now: a pool slot, the ranges again
+            const uint32_t slot = pool_acquire(a.fl, &s_slot);
+            const GenRanges gr = pool_ranges(a.pool, slot, a.n);
+            __syncthreads();
+            if (threadIdx.x == 0) s_cnt = 0;
+            __syncthreads();
+            collect(gr, a.n);
+            x = fit_general<BLOCK>(gr, s_cnt, st, a.best != 0, lks, lke, red64);
+            pool_release(a.fl, slot);
+        }
+        if (threadIdx.x == 0) agent_store64(a.off + qt, x);
+        __syncthreads();
     }
 }
 
@@ -583,8 +881,8 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     __shared__ uint64_t scratch64[BLOCK / kWave];
     __shared__ uint64_t gbits[kRunCap / 64];  // gaps of the placed run that hold t
     __shared__ uint32_t cidx[kWave];           // the first 64 of them
-    __shared__ uint32_t s_rank, s_nstat, s_ndyn;
-    if (a.fl->abort) return;
+    __shared__ uint32_t s_rank, s_nstat, s_ndyn, s_slot;
+    if (a.fl->abort || a.fl->wide) return;
     const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
     uint64_t* gkeys = a.run_keys + (int64_t)blockIdx.x * a.stat_cap;
     const int64_t stat_cap = a.stat_cap;
@@ -621,12 +919,27 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         uint32_t nstat = s_nstat;
         const int ndyn = (int)min(s_ndyn, (uint32_t)kDynCap);
         if (nstat > (uint32_t)stat_cap) {
-            // predecessor set beyond the scratch capacity: report, and still
-            // publish an offset so that no later tensor waits forever
-            if (threadIdx.x == 0) {
-                raise_status(a.status, MP_ENOSPC);
-                agent_store(a.off + qt, 0u);
-            }
+            // more predecessors than the workgroup's buffer: wait for the late
+            // ones, take a pool slot, collect every predecessor's range there
+            // and fit over all of them (the general fit)
+            for (int d = threadIdx.x; d < ndyn; d += BLOCK)
+                while (agent_load(a.off + dpos[d]) == kUnplacedT) __builtin_amdgcn_s_sleep(1);
+            __syncthreads();
+            const uint32_t slot = pool_acquire(a.fl, &s_slot);
+            const GenRanges gr = pool_ranges(a.pool, slot, a.n);
+            if (threadIdx.x == 0) s_nstat = 0;
+            __syncthreads();
+            for_each_pred<BLOCK>(a, qt, st, lthr, n_long, [&](int32_t p, uint32_t o) {
+                while (o == kUnplacedT) o = agent_load(a.off + p);  // placed: seen above
+                const uint32_t k = atomicAdd(&s_nstat, 1u);
+                gr.ks[k] = o;
+                gr.ke[k] = (uint64_t)o + a.su[p];
+            });
+            __syncthreads();
+            const uint64_t x = fit_general<BLOCK>(gr, s_nstat, st, a.best != 0, skeys,
+                                                  skeys + kGRun, scratch64);
+            pool_release(a.fl, slot);
+            if (threadIdx.x == 0) agent_store(a.off + qt, (uint32_t)x);
             __syncthreads();
             continue;
         }
@@ -844,18 +1157,21 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
 
 __global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restrict__ off,
                                                        const uint32_t* __restrict__ su,
+                                                       const uint64_t* __restrict__ off64,
+                                                       const uint64_t* __restrict__ su64,
                                                        const uint32_t* __restrict__ pid, int64_t n,
                                                        int64_t* __restrict__ offset_out,
                                                        TFlags* fl) {
     __shared__ uint64_t red[256 / kWave];
     if (fl->abort) return;
     const uint32_t sh = fl->shift;
+    const bool wide = fl->wide != 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     uint64_t pk = 0;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
-        const uint64_t o = off[q];
+        const uint64_t o = wide ? off64[q] : (uint64_t)off[q];
         offset_out[pid[q]] = (int64_t)(o << sh);
-        const uint64_t e = (o + su[q]) << sh;
+        const uint64_t e = (o + (wide ? su64[q] : (uint64_t)su[q])) << sh;
         pk = pk > e ? pk : e;
     }
     pk = block_reduce<256>(pk, OpMax<uint64_t>(), red);
@@ -866,8 +1182,8 @@ __global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restric
 __global__ void t_peak_kernel(const TFlags* fl, int64_t* peak_out) { *peak_out = (int64_t)fl->peak; }
 
 struct TLayout {
-    size_t flags, su, pf, pl, pid, off, reach, keys0, vals0, keys1, vals1, radix, lflag, lpartial,
-        llist, run_keys, total;
+    size_t flags, su, pf, pl, pid, off, su64, off64, reach, keys0, vals0, keys1, vals1, radix,
+        lflag, lpartial, llist, run_keys, pool, total;
     unsigned grid;
 };
 
@@ -890,9 +1206,11 @@ unsigned place_grid() {
     return (unsigned)(g > kDynCap + 1 ? kDynCap + 1 : g);
 }
 
+// Keys per workgroup buffer: a tensor has fewer than n predecessors; the
+// 64-bit path uses the same bytes as four arrays of stat_cap / 4 ranges.
 int64_t stat_cap_of(int64_t n) {
     const int64_t cap = kScratchRuns * (int64_t)kRunCap;
-    return n < cap ? n : cap;
+    return 4 * n < cap ? 4 * n : cap;
 }
 
 TLayout t_layout(int64_t n, unsigned grid) {
@@ -910,6 +1228,8 @@ TLayout t_layout(int64_t n, unsigned grid) {
     L.pl = take(nn * 4);
     L.pid = take(nn * 4);
     L.off = take(nn * 4);
+    L.su64 = take(nn * 8);
+    L.off64 = take(nn * 8);
     L.reach = take(nn * 4);
     L.keys0 = take(nn * 8);
     L.vals0 = take(nn * 4);
@@ -920,6 +1240,7 @@ TLayout t_layout(int64_t n, unsigned grid) {
     L.lpartial = take(scan_workspace_bytes(nn));
     L.llist = take(nn * 4);
     L.run_keys = take((size_t)grid * (size_t)stat_cap_of(nn) * 8);
+    L.pool = take((size_t)kPoolSlots * 4 * nn * 8);
     L.total = o;
     L.grid = grid;
     return L;
@@ -945,6 +1266,8 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     int32_t* pl = reinterpret_cast<int32_t*>(w + L.pl);
     uint32_t* pid = reinterpret_cast<uint32_t*>(w + L.pid);
     uint32_t* off = reinterpret_cast<uint32_t*>(w + L.off);
+    uint64_t* su64 = reinterpret_cast<uint64_t*>(w + L.su64);
+    uint64_t* off64 = reinterpret_cast<uint64_t*>(w + L.off64);
     int32_t* reach = reinterpret_cast<int32_t*>(w + L.reach);
     uint64_t* keys0 = reinterpret_cast<uint64_t*>(w + L.keys0);
     uint32_t* vals0 = reinterpret_cast<uint32_t*>(w + L.vals0);
@@ -963,7 +1286,7 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     const unsigned g = grid_n(n, 256);
     hipLaunchKernelGGL(t_ingest_kernel, dim3(g), dim3(256), 0, st, size, first, last, n, num_ops,
                        fl, status);
-    hipLaunchKernelGGL(t_unit_kernel, dim3(1), dim3(1), 0, st, fl, status);
+    hipLaunchKernelGGL(t_unit_kernel, dim3(1), dim3(1), 0, st, fl);
     // position order (unsorted inputs only)
     hipLaunchKernelGGL(t_keys_first_kernel, dim3(g), dim3(256), 0, st, first, n, keys0, vals0,
                        (const TFlags*)fl);
@@ -973,7 +1296,7 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(t_positions_kernel, dim3(g), dim3(256), 0, st,
                        (const uint32_t*)(alt ? vals1 : vals0), size, first, last, n, su, pf, pl,
-                       pid, off, (const TFlags*)fl);
+                       pid, off, su64, off64, (const TFlags*)fl);
     hipLaunchKernelGGL(t_reach_kernel, dim3(g), dim3(256), 0, st, first, last, (const int32_t*)pf,
                        (const int32_t*)pl, (const uint32_t*)pid, n, reach, fl);
     hipLaunchKernelGGL(t_threshold_kernel, dim3(1), dim3(1), 0, st, fl);
@@ -983,11 +1306,18 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(t_long_list_kernel, dim3(g), dim3(256), 0, st, (const int32_t*)reach,
                        (const int64_t*)lflag, n, llist, fl);
-    // rank order: size descending, stable over positions
-    hipLaunchKernelGGL(t_rank_keys_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)su, n, keys0,
-                       vals0, (const TFlags*)fl);
-    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32, rws, &alt, st, &fl->abort);
+    // rank order: size descending, stable over positions -- 32-bit keys, or
+    // 64-bit ones when the unit counts are (the other sort is skipped on the
+    // device; both take an even number of passes, so the result is in keys0)
+    hipLaunchKernelGGL(t_rank_keys_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)su,
+                       (const uint64_t*)su64, n, keys0, vals0, (const TFlags*)fl);
+    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32, rws, &alt, st, &fl->skip_narrow);
     if (e != hipSuccess) return e;
+    bool alt64 = false;
+    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 64, rws, &alt64, st, &fl->skip_wide);
+    if (e != hipSuccess) return e;
+    if (alt != alt64) return hipErrorInvalidValue;  // both sorts end in the same buffer
+    uint64_t* pool = reinterpret_cast<uint64_t*>(w + L.pool);
     PlaceArgs pa{su,
                  reach,
                  alt ? vals1 : vals0,
@@ -995,13 +1325,19 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
                  off,
                  reinterpret_cast<uint64_t*>(w + L.run_keys),
                  stat_cap_of(n),
+                 pool,
                  n,
                  fl,
                  status,
                  policy == MP_BEST_FIT ? 1 : 0};
     hipLaunchKernelGGL(t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, pa);
+    WideArgs wa{su64, reach, alt ? vals1 : vals0, llist, off64,
+                reinterpret_cast<uint64_t*>(w + L.run_keys), stat_cap_of(n) / 4, pool, n, fl,
+                policy == MP_BEST_FIT ? 1 : 0};
+    hipLaunchKernelGGL(t_place_wide_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, wa);
     hipLaunchKernelGGL(t_output_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)off,
-                       (const uint32_t*)su, (const uint32_t*)pid, n, offset_out, fl);
+                       (const uint32_t*)su, (const uint64_t*)off64, (const uint64_t*)su64,
+                       (const uint32_t*)pid, n, offset_out, fl);
     hipLaunchKernelGGL(t_peak_kernel, dim3(1), dim3(1), 0, st, (const TFlags*)fl, peak_out);
     return hipGetLastError();
 }

@@ -133,6 +133,7 @@ def test_status_codes_and_empty():
     big = tg.Trace(np.array([2 ** 62, 2 ** 62], np.int64), np.zeros(2, np.int32),
                    np.zeros(2, np.int32), 1)
     assert status(big) == binding.MP_EOVERFLOW
+    # sizes past 32-bit unit counts are planned (64-bit path), not refused
     wide = tg.Trace(np.array([2 ** 31 + 1, 2 ** 31 + 1], np.int64), np.zeros(2, np.int32),
                     np.zeros(2, np.int32), 1)
-    assert status(wide) == binding.MP_ENOSPC
+    assert status(wide) == binding.MP_OK
