@@ -58,24 +58,32 @@ __device__ unsigned int g_dbg[4096 * 8];
 namespace {
 
 constexpr int kBatchBlock = 512;
-constexpr int kSmallSlots = 4;                // neighbours a lane holds in pairs and quads
-constexpr int kSlots = 4;                     // ... in rows and the whole wave
-constexpr uint32_t kPairK = 2u * kSmallSlots; // neighbours of a tensor fitted by a lane pair
-constexpr uint32_t kQuadK = 4u * kSmallSlots; // ... by a lane quad
-constexpr int kRowLanes = 16;                 // lanes of a row
-constexpr uint32_t kRowK = kRowLanes * kSlots; // ... by a row of lanes; more: the whole wave
-constexpr uint32_t kCoopChunk = (uint32_t)kWave * kSlots;
-constexpr uint32_t kBestMaxK = kCoopChunk;    // BEST_FIT on the LDS path: one wave sorts them all
+constexpr int kLaneSlots = 8;                   // neighbours a lane holds while fitting
+constexpr int kBestSlots = 4;                   // ... in the whole-wave BEST_FIT sort
+constexpr uint32_t kCoopChunk = (uint32_t)kWave * kLaneSlots;
+constexpr uint32_t kBestMaxK = (uint32_t)kWave * kBestSlots;  // BEST_FIT on the LDS path
+
+// Ready classes by neighbour count K: the lanes a tensor is fitted by.
+// 0: K <= 8, one lane; 1: K <= 16, two; 2: K <= 32, four; 3: K <= 64,
+// eight; 4: more, the whole wave (under BEST_FIT every K > 8).
+constexpr int kClasses = 5;
+constexpr int kWideClass = 4;
 
 // A tensor's LDS placement word: size (units) in the low half; the high half
 // is the offset (units, below 2^31) once placed, and before that bit 31 set,
-// the ready class in bits 29-30 and the number of unplaced predecessors in
-// bits 0-28.  An unplaced word never overlaps a candidate range: every
-// candidate end stays below 2^31 units because the trace's sizes sum to less.
+// the tensor's count in its ready class's 4-bit field (1 << (12 + 4 c)) and
+// the number of unplaced predecessors in bits 0-11 (a trace has at most 4096
+// tensors).  An unplaced word never overlaps a candidate range: every
+// candidate end plus the size being fitted stays below 2^31 units, because
+// the trace's sizes sum to less (the greedy's peak never exceeds that sum).
 constexpr uint32_t kUnplacedBit = 0x80000000u;
-constexpr uint32_t kClassShift = 29;
+constexpr uint32_t kClassShift = 12;
 constexpr uint32_t kPendMask = (1u << kClassShift) - 1;
+__device__ __forceinline__ uint32_t class_bits(uint32_t c) { return 1u << (kClassShift + 4u * c); }
 constexpr uint64_t kFastMaxUnits = 0x7FFFFFFFull;
+// A slot past the tensor's neighbour count: sorts after every range, never
+// overlaps one and names no successor.
+constexpr uint32_t kNoSlot = 0xFFFFFFFFu;
 
 // Left-list entries (one byte): 1 .. kMaxDist is the distance back to the
 // neighbour's position; kLongBase + s names long tensor s (a tensor whose
@@ -84,9 +92,10 @@ constexpr uint32_t kLongSlots = 32;
 constexpr uint32_t kLongBase = 256 - kLongSlots;
 constexpr uint32_t kMaxDist = kLongBase - 1;
 
-// Ready class of a tensor with K neighbours: 0 pair, 1 quad, 2 row or wave.
-__device__ __forceinline__ uint32_t ready_class(uint32_t K) {
-    return K <= kPairK ? 0u : (K <= kQuadK ? 1u : 2u);
+__device__ __forceinline__ uint32_t ready_class(uint32_t K, bool best) {
+    if (K <= 8) return 0u;
+    if (best) return (uint32_t)kWideClass;
+    return K <= 16 ? 1u : (K <= 32 ? 2u : (K <= 64 ? 3u : (uint32_t)kWideClass));
 }
 
 __device__ __forceinline__ uint32_t word_off(uint64_t w) { return (uint32_t)(w >> 32); }
@@ -111,26 +120,6 @@ struct LeftLists {
     const uint16_t* longtab;  // positions of the long tensors
 };
 
-// Position of the left neighbour named by entry lv of tensor q's list.
-__device__ __forceinline__ uint32_t left_pos(uint32_t q, uint32_t lv, const LeftLists& ll) {
-    return lv >= kLongBase ? (uint32_t)ll.longtab[lv - kLongBase] : q - lv;
-}
-
-// Neighbour k of tensor q in its neighbour sequence: the left list first
-// (k < L; pl = its position), then the right band q + 1 .. q + R.  Slots
-// past the end (k >= K) map to q itself, which is unplaced and never a
-// successor.  Branch-free (masks instead of selects that the compiler would
-// turn into divergent blocks around the list load).
-__device__ __forceinline__ uint32_t neighbour(uint32_t k, uint32_t L, uint32_t K, uint32_t q,
-                                              uint32_t pl) {
-    const uint32_t in_left = 0u - (uint32_t)(k < L), in_band = 0u - (uint32_t)(k < K);
-    const uint32_t right = q + ((k + 1 - L) & in_band);
-    return (pl & in_left) | (right & ~in_left);
-}
-// When a tensor is fitted every neighbour ranked before it is placed and none
-// ranked after it is, so its successors are exactly its unplaced neighbours.
-__device__ __forceinline__ uint32_t is_unplaced(uint32_t o) { return o >> 31; }
-
 // Maximum over the 64 lanes, returned to every lane: DPP row shifts build
 // row-wise prefix maxima, row broadcasts carry them across rows, lane 63
 // ends up with the total.  All 64 lanes must be active.
@@ -144,21 +133,17 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// Maximum over each row of 16 lanes, returned to all of them: rotations by
-// 8, 4, 2 and 1 within the row.
-__device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x124, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x122, 0xF, 0xF, false));
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x121, 0xF, 0xF, false));
-    return v;
-}
-// Maximum over each aligned lane pair, or over each aligned quad where
-// `quad` is set (all lanes of a group agree on it; every lane active).
-__device__ __forceinline__ uint32_t pair_quad_max_u32(uint32_t v, bool quad) {
-    v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
-    const uint32_t v4 = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
-    return quad ? v4 : v;
+// Maximum over each aligned group of G lanes (G = 1, 2, 4 or 8, per lane;
+// the lanes of a group agree on it), returned to the group: swaps within
+// pairs and quads (quad_perm), then between the two quads of each half row
+// (half-row mirror).  All 64 lanes must be active.
+__device__ __forceinline__ uint32_t group_max_u32(uint32_t v, uint32_t G) {
+    uint32_t t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
+    v = G >= 2 ? t : v;
+    t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
+    v = G >= 4 ? t : v;
+    t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
+    return G >= 8 ? t : v;
 }
 
 template <int BLOCK>
@@ -181,17 +166,6 @@ __device__ void bitonic_sort_u64(uint64_t* keys, int m) {
     }
 }
 
-// The ready lists of the three classes share one array of N slots: class
-// c owns the region [region[c], region[c] + number of class-c tensors), as
-// each tensor is appended once.  Appends of a round go after `end[c]` (the
-// region position past the round's own range), counted in one 64-bit word
-// with a 16-bit field per class (a trace has at most 4096 tensors).
-struct ReadyLists {
-    uint16_t* slot;
-    uint32_t end[3];
-    unsigned long long* cnt;
-};
-
 // Inclusive sum over the 64 lanes (DPP row shifts, then row broadcasts).
 // All 64 lanes must be active.
 __device__ __forceinline__ uint32_t wave_inclusive_sum_dpp(uint32_t v) {
@@ -204,89 +178,161 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum_dpp(uint32_t v) {
     return v;
 }
 
-// Decrement the pending counts of the successors among M (<= 8) gathered
-// neighbours (dec[j] is 1 for a successor, else 0: the atomics then issue
-// back to back; subtracting 0 from a word changes nothing) and append those
-// that reach zero to their class list: one wave scan of the per-lane counts
-// (10-bit fields, one per class) and one list reservation per wave.  All 64
-// lanes must be active.
-template <int M>
-__device__ __forceinline__ void release_successors(const uint32_t (&dec)[M],
-                                                   const uint32_t (&ids)[M], uint64_t* ofsz,
-                                                   const ReadyLists& rl, int lane) {
-    static_assert(M <= 8, "a lane releases at most 8 tensors (10-bit wave sums)");
-    uint32_t old[M], any_dec = 0;
+// The ready lists of the classes share one array of N slots: class c owns
+// the region [region[c], region[c] + number of class-c tensors), as each
+// tensor is appended once.  Appends of a round go after `end[c]` (here the
+// list position past the round's own range, region included), counted in
+// one 64-bit word with a 16-bit field per class 0-3 and a 32-bit word for
+// class 4.
+struct ReadyLists {
+    uint16_t* slot;
+    uint32_t end[kClasses];
+    unsigned long long* cnt;
+    uint32_t* cnt_wide;
+};
+
+// Decrement the pending counts of the successors among a lane's S slots:
+// after a fit, a slot names a successor exactly when it holds an unplaced
+// neighbour (kUnplacedBit | position; every neighbour ranked before the
+// fitted tensor is placed and none ranked after it is); only those issue an
+// atomic (slots masked off issue none, so no lanes pile onto one word), and
+// a slot's tensor is ready exactly when the count it read was 1.  Ready
+// tensors are appended to
+// their class lists: the per-lane counts (a 4-bit field per class, read from
+// the words) are scanned over the wave in 10-bit fields, one reservation per
+// wave, and each lane's list positions are kept as 12-bit fields of one
+// 64-bit word (list positions are below 4096).  All 64 lanes must be active.
+template <int S>
+__device__ __forceinline__ void release(const uint32_t (&o)[S], uint64_t* ofsz,
+                                        const ReadyLists& rl, int lane) {
+    static_assert(S <= 8, "a lane releases at most 8 tensors (4-bit counts)");
+    uint32_t old[S];
+    uint32_t* hi = reinterpret_cast<uint32_t*>(ofsz) + 1;  // the words' high halves
 #pragma unroll
-    for (int j = 0; j < M; ++j) {
-        old[j] = 0;
-        any_dec |= dec[j];
+    for (int r = 0; r < S; ++r) {
+        old[r] = 0;
+        if (o[r] >= kUnplacedBit && o[r] != kNoSlot) old[r] = atomicSub(hi + 2 * (o[r] & 0xFFFFu), 1u);
     }
-    if (any_dec) {  // 32-bit atomics on the words' high halves (the pending counts)
-        uint32_t* hi = reinterpret_cast<uint32_t*>(ofsz) + 1;
+    uint32_t p4 = 0;  // ready tensors of this lane, 4 bits per class
 #pragma unroll
-        for (int j = 0; j < M; ++j) old[j] = atomicSub(hi + 2 * ids[j], dec[j]);
+    for (int r = 0; r < S; ++r) {
+        const bool rd = (old[r] & kPendMask) == 1u;
+        p4 += rd ? __builtin_amdgcn_ubfe(old[r], kClassShift, 17) : 0u;
     }
-    uint32_t packed = 0;  // ready tensors of this lane, 10 bits per class
-#pragma unroll
-    for (int j = 0; j < M; ++j) {
-        const bool r = dec[j] && (old[j] & kPendMask) == 1u;
-        packed += r ? 1u << (10 * ((old[j] >> kClassShift) & 3u)) : 0u;
-    }
-    if (!__ballot(packed != 0)) return;
-    const uint32_t incl = wave_inclusive_sum_dpp(packed);
-    const uint32_t tot = (uint32_t)__builtin_amdgcn_readlane((int)incl, 63);
-    uint32_t pre = incl - packed;
-    unsigned long long base = 0;
+    if (!__ballot(p4 != 0)) return;
+    // classes 0-2 in 10-bit fields of one word, 3-4 of another
+    const uint32_t plo = (p4 & 0xFu) | ((p4 << 6) & (0xFu << 10)) | ((p4 << 12) & (0xFu << 20));
+    const uint32_t phi = ((p4 >> 12) & 0xFu) | ((p4 >> 6) & (0xFu << 10));
+    const uint32_t ilo = wave_inclusive_sum_dpp(plo), ihi = wave_inclusive_sum_dpp(phi);
+    const uint32_t tlo = (uint32_t)__builtin_amdgcn_readlane((int)ilo, 63);
+    const uint32_t thi = (uint32_t)__builtin_amdgcn_readlane((int)ihi, 63);
+    uint32_t b0 = 0, b1 = 0, b4 = 0;
     if (lane == 0) {
-        const unsigned long long add = (unsigned long long)(tot & 0x3FFu) |
-                                       ((unsigned long long)((tot >> 10) & 0x3FFu) << 16) |
-                                       ((unsigned long long)(tot >> 20) << 32);
-        base = atomicAdd(rl.cnt, add);
+        const unsigned long long add = (unsigned long long)(tlo & 0x3FFu) |
+                                       ((unsigned long long)((tlo >> 10) & 0x3FFu) << 16) |
+                                       ((unsigned long long)(tlo >> 20) << 32) |
+                                       ((unsigned long long)(thi & 0x3FFu) << 48);
+        const unsigned long long base = atomicAdd(rl.cnt, add);
+        b0 = (uint32_t)base;
+        b1 = (uint32_t)(base >> 32);
+        if (thi >> 10) b4 = atomicAdd(rl.cnt_wide, thi >> 10);
     }
-    const uint32_t blo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)base, 0);
-    const uint32_t bhi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(base >> 32), 0);
-    // this lane's next slot in each class list, advanced per appended tensor
-    // (selects, no branches around the stores)
-    uint32_t b0 = rl.end[0] + (blo & 0xFFFFu) + (pre & 0x3FFu);
-    uint32_t b1 = rl.end[1] + (blo >> 16) + ((pre >> 10) & 0x3FFu);
-    uint32_t b2 = rl.end[2] + (bhi & 0xFFFFu) + (pre >> 20);
+    b0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b0);
+    b1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b1);
+    b4 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b4);
+    const uint32_t xlo = ilo - plo, xhi = ihi - phi;  // ready tensors of the lanes before
+    uint64_t at = (uint64_t)(rl.end[0] + (b0 & 0xFFFFu) + (xlo & 0x3FFu)) |
+                  ((uint64_t)(rl.end[1] + (b0 >> 16) + ((xlo >> 10) & 0x3FFu)) << 12) |
+                  ((uint64_t)(rl.end[2] + (b1 & 0xFFFFu) + (xlo >> 20)) << 24) |
+                  ((uint64_t)(rl.end[3] + (b1 >> 16) + (xhi & 0x3FFu)) << 36) |
+                  ((uint64_t)(rl.end[4] + b4 + (xhi >> 10)) << 48);
 #pragma unroll
-    for (int j = 0; j < M; ++j) {
-        const bool r = dec[j] && (old[j] & kPendMask) == 1u;
-        const uint32_t c = (old[j] >> kClassShift) & 3u;
-        const uint32_t at = c == 0 ? b0 : (c == 1 ? b1 : b2);
-        if (r) rl.slot[at] = (uint16_t)ids[j];
-        b0 += (r && c == 0) ? 1u : 0u;
-        b1 += (r && c == 1) ? 1u : 0u;
-        b2 += (r && c == 2) ? 1u : 0u;
+    for (int r = 0; r < S; ++r) {
+        if ((old[r] & kPendMask) == 1u) {
+            // class field 4c of the word's count, list field 12c of `at`
+            const uint32_t sh = 3u * (__builtin_ctz(old[r] >> kClassShift));
+            rl.slot[(uint32_t)(at >> sh) & 0xFFFu] = (uint16_t)(o[r] & 0xFFFFu);
+            at += 1ull << sh;
+        }
     }
+}
+
+// Compare-exchange of two (offset, end) slots by offset.
+__device__ __forceinline__ void cex(uint32_t& oa, uint32_t& ea, uint32_t& ob, uint32_t& eb) {
+    const bool sw = oa > ob;
+    const uint32_t to = oa, te = ea;
+    oa = sw ? ob : oa;
+    ea = sw ? eb : ea;
+    ob = sw ? to : ob;
+    eb = sw ? te : eb;
+}
+// The lane's eight slots sorted by offset (a 19-comparator network); unplaced
+// neighbours and empty slots (offsets at or above 2^31) end up last.
+__device__ __forceinline__ void sort8(uint32_t (&o)[8], uint32_t (&e)[8]) {
+#define MP_CEX(a, b) cex(o[a], e[a], o[b], e[b])
+    MP_CEX(0, 2); MP_CEX(1, 3); MP_CEX(4, 6); MP_CEX(5, 7);
+    MP_CEX(0, 4); MP_CEX(1, 5); MP_CEX(2, 6); MP_CEX(3, 7);
+    MP_CEX(0, 1); MP_CEX(2, 3); MP_CEX(4, 5); MP_CEX(6, 7);
+    MP_CEX(2, 4); MP_CEX(3, 5);
+    MP_CEX(1, 4); MP_CEX(3, 6);
+    MP_CEX(1, 2); MP_CEX(3, 4); MP_CEX(5, 6);
+#undef MP_CEX
+}
+
+// Lowest y >= x at which [y, y + s) meets none of the lane's ranges, the
+// ranges sorted by offset: one pass suffices, since a range passed over
+// either ended at or below y or was jumped past, and y only grows.
+__device__ __forceinline__ uint32_t sweep_lowest(const uint32_t (&o)[8], const uint32_t (&e)[8],
+                                                 uint32_t x, uint32_t s) {
+#pragma unroll
+    for (int r = 0; r < 8; ++r) x = (o[r] < x + s && x < e[r]) ? e[r] : x;
+    return x;
+}
+
+// BEST_FIT over the lane's ranges sorted by offset: the free gap before
+// range r runs from the highest end among ranges before it to its offset;
+// the smallest gap that holds s wins (lowest start among equals), else the
+// space above every range.
+__device__ __forceinline__ uint32_t sweep_best(const uint32_t (&o)[8], const uint32_t (&e)[8],
+                                               uint32_t s) {
+    uint32_t m = 0, bg = kNoSlot, bs = 0;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+        const bool placed = o[r] < kUnplacedBit;
+        const bool fits = placed && o[r] >= m && o[r] - m >= s && o[r] - m < bg;
+        bs = fits ? m : bs;
+        bg = fits ? o[r] - m : bg;
+        m = placed ? max(m, e[r]) : m;
+    }
+    return bg != kNoSlot ? bs : m;
 }
 
 // BEST_FIT (the tightest-gap reading of Section 2.3's "best fit"): among the
 // free gaps between the placed neighbours' ranges, the smallest one that
 // holds s units, the lowest start among equals; the space above every range
-// only when no finite gap holds s.  A group of LANES lanes holds kSlots
-// ranges per lane, element i = kSlots l + r at lane l (0 <= l < LANES) and
-// slot r; the group sorts them by offset (bitonic network: slots within a
-// lane, lanes by exchanges with lane l ^ d), takes running maxima of the ends
-// in that order (gap before element i: [max end of elements < i, offset of
-// i)) and a minimum over (gap length, gap start).  Unplaced ranges (bit 31 of
-// the offset half set) sort last and bound no gap.  Every lane of the group
-// gets the result.
+// only when no finite gap holds s.  A group of LANES lanes holds kBestSlots
+// ranges per lane, element i = kBestSlots l + r at lane l (0 <= l < LANES)
+// and slot r; the group sorts them by offset (bitonic network: slots within
+// a lane, lanes by exchanges with lane l ^ d), takes running maxima of the
+// ends in that order (gap before element i: [max end of elements < i,
+// offset of i)) and a minimum over (gap length, gap start).  Unplaced ranges
+// and empty slots (offsets at or above 2^31) sort last and bound no gap.
+// Every lane of the group gets the result.
 template <int LANES>
-__device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots], uint32_t s,
-                                   uint32_t l) {
-    constexpr int kN = kSlots * LANES;
+__device__ uint32_t best_fit_group(uint32_t (&o)[kBestSlots], uint32_t (&e)[kBestSlots],
+                                   uint32_t s, uint32_t l) {
+    constexpr int kS = kBestSlots;
+    constexpr int kN = kS * LANES;
 #pragma unroll
     for (int k = 2; k <= kN; k <<= 1) {
 #pragma unroll
         for (int j = k >> 1; j >= 1; j >>= 1) {
-            if (j < kSlots) {
+            if (j < kS) {
 #pragma unroll
-                for (int r = 0; r < kSlots; ++r) {
+                for (int r = 0; r < kS; ++r) {
                     const int r2 = r ^ j;
                     if (r2 > r) {
-                        const bool up = ((((uint32_t)kSlots * l + (uint32_t)r) & (uint32_t)k) == 0);
+                        const bool up = ((((uint32_t)kS * l + (uint32_t)r) & (uint32_t)k) == 0);
                         const bool sw = up ? (o[r] > o[r2]) : (o[r] < o[r2]);
                         const uint32_t oa = o[r], ea = e[r];
                         o[r] = sw ? o[r2] : oa;
@@ -296,13 +342,13 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
                     }
                 }
             } else {
-                const int d = j / kSlots;  // partner lane l ^ d, same slot
+                const int d = j / kS;  // partner lane l ^ d, same slot
                 const bool lower = (l & (uint32_t)d) == 0;
 #pragma unroll
-                for (int r = 0; r < kSlots; ++r) {
+                for (int r = 0; r < kS; ++r) {
                     const uint32_t po = (uint32_t)__shfl_xor((int)o[r], d, LANES);
                     const uint32_t pe = (uint32_t)__shfl_xor((int)e[r], d, LANES);
-                    const bool up = ((((uint32_t)kSlots * l + (uint32_t)r) & (uint32_t)k) == 0);
+                    const bool up = ((((uint32_t)kS * l + (uint32_t)r) & (uint32_t)k) == 0);
                     const bool take = (lower == up) ? (po < o[r]) : (po > o[r]);
                     o[r] = take ? po : o[r];
                     e[r] = take ? pe : e[r];
@@ -312,9 +358,9 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
     }
     // running maximum of the placed ends: within the lane, then over the
     // lanes before it
-    uint32_t incl[kSlots], run = 0;
+    uint32_t incl[kS], run = 0;
 #pragma unroll
-    for (int r = 0; r < kSlots; ++r) {
+    for (int r = 0; r < kS; ++r) {
         run = max(run, o[r] < kUnplacedBit ? e[r] : 0u);
         incl[r] = run;
     }
@@ -329,7 +375,7 @@ __device__ uint32_t best_fit_group(uint32_t (&o)[kSlots], uint32_t (&e)[kSlots],
     const uint32_t top = (uint32_t)__shfl((int)scan, LANES - 1, LANES);
     uint64_t best = ~0ull;
 #pragma unroll
-    for (int r = 0; r < kSlots; ++r) {
+    for (int r = 0; r < kS; ++r) {
         const uint32_t pm = r == 0 ? before : max(before, incl[r - 1]);
         const bool ok = o[r] < kUnplacedBit && o[r] >= pm && o[r] - pm >= s;
         const uint64_t key = ((uint64_t)(o[r] - pm) << 32) | pm;
@@ -353,7 +399,7 @@ struct Item {
 };
 
 // A lane without a tensor gets the spare word ofsz[N] (never placed, size
-// 0) as its tensor and no neighbours, so every slot reads that word.
+// 0) as its tensor and no neighbours.
 __device__ __forceinline__ Item load_item(uint32_t q, bool has, uint32_t spare,
                                           const uint64_t* ofsz, const uint16_t* lbeg,
                                           const uint16_t* rlen) {
@@ -369,20 +415,21 @@ __device__ __forceinline__ Item load_item(uint32_t q, bool has, uint32_t spare,
 }
 
 // The neighbours k = S g + r (r < S) of a group's tensor, for the lane at
-// position g of its group: o[r] is a placed neighbour's offset, or for an
-// unplaced one kUnplacedBit | its position (never overlapping, and what the
-// release needs); e[r] the placed neighbour's end.  The lane's left-list
-// entries are consecutive bytes, read as aligned words.  Slots past the
-// neighbour count read the tensor's own word, which is unplaced.  LONG: the
-// trace has long tensors (entries at or above kLongBase name one through
-// the table).
+// position g of its group.  The neighbour sequence is the left list, then
+// the right band q + 1 .. q + R.  o[r] is a placed neighbour's offset, or
+// kUnplacedBit | position for an unplaced one (never overlapping, and what
+// the release needs), or kNoSlot past the neighbour count; e[r] the placed
+// neighbour's end.  The lane's left-list entries are consecutive bytes, read
+// as aligned words (the list array is padded for the words past its end).
+// LONG: the trace has long tensors (entries at or above kLongBase name one
+// through the table).
 template <int S, bool LONG>
 __device__ __forceinline__ void gather(const Item& it, uint32_t g, const uint64_t* ofsz,
                                        const LeftLists& ll, uint32_t (&o)[S], uint32_t (&e)[S]) {
     static_assert(S == 4 || S == 8, "4 or 8 slots a lane");
     uint32_t id[S];
     const uint32_t k0 = g * S;
-    const uint32_t s0 = it.lb + min(k0, it.L);  // at most the list capacity: in bounds (padded)
+    const uint32_t s0 = it.lb + min(k0, it.L);
     const uint32_t* w32 = reinterpret_cast<const uint32_t*>(ll.ent) + (s0 >> 2);
     uint32_t by[S / 4];
     {
@@ -391,15 +438,19 @@ __device__ __forceinline__ void gather(const Item& it, uint32_t g, const uint64_
         if (S == 8) by[S / 4 - 1] = __builtin_amdgcn_alignbyte(w32[2], b1, s0 & 3u);
     }
     // slot r holds neighbour k0 + r: left entry r when r < lr, band position
-    // rb + r when lr <= r < kr, the tensor itself beyond
+    // rb + r when lr <= r < kr, nothing beyond (the tensor's own word is read)
     const int lr = (int)it.L - (int)k0, kr = (int)it.K - (int)k0;
     const uint32_t rb = it.q + 1u - (uint32_t)lr;
 #pragma unroll
     for (int r = 0; r < S; ++r) {
-        const uint32_t ent = (by[r >> 2] >> (8 * (r & 3))) & 0xFFu;
+        const uint32_t ent = __builtin_amdgcn_ubfe(by[r >> 2], 8 * (r & 3), 8);
         uint32_t pl = it.q - ent;
-        if (LONG && ent >= kLongBase) pl = ll.longtab[ent - kLongBase];
-        id[r] = r < lr ? pl : (r < kr ? rb + (uint32_t)r : it.q);
+        if (LONG) {  // the table read is unconditional (in bounds), then selected
+            const uint32_t lt = ll.longtab[(ent - kLongBase) & (kLongSlots - 1)];
+            pl = ent >= kLongBase ? lt : pl;
+        }
+        const uint32_t a = r < lr ? pl : rb + (uint32_t)r;
+        id[r] = r < kr ? a : it.q;
     }
     uint64_t w[S];
 #pragma unroll
@@ -407,62 +458,45 @@ __device__ __forceinline__ void gather(const Item& it, uint32_t g, const uint64_
 #pragma unroll
     for (int r = 0; r < S; ++r) {
         const uint32_t wo = word_off(w[r]);
-        o[r] = wo < kUnplacedBit ? wo : (kUnplacedBit | id[r]);
+        o[r] = r >= kr ? kNoSlot : (wo < kUnplacedBit ? wo : (kUnplacedBit | id[r]));
         e[r] = word_end(w[r]);
     }
 }
 
-// Successors of a gathered lane: the unplaced neighbours within the count
-// (dec[r] = 1) and the positions to decrement (every slot names a word:
-// subtracting 0 changes nothing).
-template <int S>
-__device__ __forceinline__ void successors(uint32_t k0, uint32_t K, const uint32_t (&o)[S],
-                                           uint32_t (&dec)[S], uint32_t (&ids)[S]) {
-    const int kr = (int)K - (int)k0;
-#pragma unroll
-    for (int r = 0; r < S; ++r) {
-        dec[r] = r < kr ? is_unplaced(o[r]) : 0u;
-        ids[r] = is_unplaced(o[r]) ? (o[r] & 0xFFFFu) : 0u;
-    }
-}
-
-// Highest end among the lane's ranges that overlap [x, x + s), 0 if none.
-template <int S>
-__device__ __forceinline__ uint32_t overlap_end(const uint32_t (&o)[S], const uint32_t (&e)[S],
-                                                uint32_t x, uint32_t s) {
-    uint32_t m = 0;
-#pragma unroll
-    for (int r = 0; r < S; ++r) m = (o[r] < x + s && x < e[r]) ? max(m, e[r]) : m;
-    return m;
-}
-
 // Whole-wave placement of tensor q (all 64 lanes active, arguments uniform):
-// the neighbour sequence is swept in chunks of kCoopChunk, lane l holding
-// neighbours kSlots l .. kSlots l + kSlots - 1 of the chunk; within a chunk
-// the candidate offset jumps to the highest end overlapping [x, x + s) until
-// nothing in the chunk overlaps, and chunks are revisited until a full lap
-// leaves x alone.  Then q is published and its successors' pending counts are
-// decremented.  BEST_FIT tensors reach here with at most kCoopChunk
-// neighbours (more go to the general path): one chunk, sorted by the wave.
-template <bool LONG>
-__device__ void place_wave(const Item& it, uint64_t* ofsz, const LeftLists& ll,
-                           const ReadyLists& rl, int lane, bool best) {
-    const uint32_t nch = (it.K + kCoopChunk - 1) / kCoopChunk;
-    uint32_t co[kSlots], ce[kSlots];
+// LOWEST_FIT sweeps the neighbour sequence in chunks of kCoopChunk, lane l
+// holding neighbours 8 l .. 8 l + 7 of the chunk, sorted in the lane; within
+// a chunk every lane moves the candidate to the lowest start clear of its
+// own ranges and the wave takes the maximum until no lane moves, and chunks
+// are revisited until a full lap leaves the candidate alone.  BEST_FIT
+// tensors reach here with at most kBestMaxK neighbours (more go to the
+// general path): one chunk of four a lane, sorted by the wave.  Then q is
+// published and its successors' pending counts are decremented.
+template <bool LONG, bool BEST>
+__device__ void place_wave(const Item& it, uint32_t spare, uint64_t* ofsz, const LeftLists& ll,
+                           const ReadyLists& rl, int lane) {
     const uint32_t g0 = (uint32_t)lane;
-    auto load = [&](uint32_t c) { gather<kSlots, LONG>(it, c * kWave + g0, ofsz, ll, co, ce); };
-    uint32_t x = 0, clean = best ? nch : 0, c = 0;
-    if (best) {
-        load(0);
-        x = best_fit_group<kWave>(co, ce, it.s, (uint32_t)lane);
+    if (BEST) {
+        uint32_t o[kBestSlots], e[kBestSlots];
+        gather<kBestSlots, LONG>(it, g0, ofsz, ll, o, e);
+        const uint32_t x = best_fit_group<kWave>(o, e, it.s, (uint32_t)lane);
+        if (lane == 0) ofsz[it.q] = ((uint64_t)x << 32) | it.s;
+        release<kBestSlots>(o, ofsz, rl, lane);
+        return;
     }
+    const uint32_t nch = (it.K + kCoopChunk - 1) / kCoopChunk;
+    uint32_t o[kLaneSlots], e[kLaneSlots];
+    uint32_t x = 0, clean = 0, c = 0;
     while (clean < nch) {
-        if (nch > 1 || c == 0) load(c);
+        if (nch > 1 || c == 0) {
+            gather<kLaneSlots, LONG>(it, c * kWave + g0, ofsz, ll, o, e);
+            sort8(o, e);
+        }
         bool moved = false;
-        while (true) {  // jump past the highest end overlapping [x, x + s)
-            const uint32_t mx = overlap_end(co, ce, x, it.s);
-            if (!__ballot(mx > x)) break;
-            x = wave_max_u32(mx);
+        while (true) {
+            const uint32_t xn = wave_max_u32(sweep_lowest(o, e, x, it.s));
+            if (xn == x) break;
+            x = xn;
             moved = true;
         }
         clean = moved ? 1u : clean + 1u;
@@ -470,10 +504,8 @@ __device__ void place_wave(const Item& it, uint64_t* ofsz, const LeftLists& ll,
     }
     if (lane == 0) ofsz[it.q] = ((uint64_t)x << 32) | it.s;
     for (uint32_t cc = 0; cc < nch; ++cc) {
-        if (nch > 1 || best) load(cc);  // (the best-fit sort permuted the slots)
-        uint32_t dec[kSlots], ids[kSlots];
-        successors((cc * kWave + g0) * kSlots, it.K, co, dec, ids);
-        release_successors(dec, ids, ofsz, rl, lane);
+        if (nch > 1) gather<kLaneSlots, LONG>(it, cc * kWave + g0, ofsz, ll, o, e);
+        release<kLaneSlots>(o, ofsz, rl, lane);
     }
 }
 
@@ -733,12 +765,13 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const int32_t* __restrict__ last, int64_t n_tensors, int32_t cap_n, int32_t cap_lists,
     unsigned char* __restrict__ ws, int64_t* __restrict__ offset_out,
     int64_t* __restrict__ peak_out, int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
-    constexpr bool best = BEST;  // BEST_FIT: every tensor to a 16-lane row or the wave
+    constexpr bool best = BEST;  // BEST_FIT: one lane up to 8 neighbours, else the whole wave
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint64_t red[BLOCK / kWave];
-    __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class)
-    __shared__ uint32_t ncls[3];              // tensors per ready class
-    __shared__ uint32_t seeds[3];             // tensors per class without predecessors
+    __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class 0-3)
+    __shared__ uint32_t nwide[3];             // ... of class 4
+    __shared__ uint32_t ncls[kClasses];       // tensors per ready class
+    __shared__ uint32_t seeds[kClasses];      // tensors per class without predecessors
     __shared__ uint16_t longtab[kLongSlots];  // positions of the long tensors
     __shared__ uint32_t nlong;
 
@@ -764,8 +797,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     MP_STAMP(0);
     if (tid == 0) {
         nready[0] = nready[1] = nready[2] = 0;
-        ncls[0] = ncls[1] = ncls[2] = 0;
-        seeds[0] = seeds[1] = seeds[2] = 0;
+        nwide[0] = nwide[1] = nwide[2] = 0;
+        for (int c = 0; c < kClasses; ++c) ncls[c] = seeds[c] = 0;
         nlong = 0;
     }
     const int64_t lo = begin[b], hi = begin[b + 1];
@@ -1065,26 +1098,26 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     uint64_t w_r[ITEMS];
     uint32_t cls_r[ITEMS];
     {
-        uint32_t cc[3] = {0, 0, 0};
+        uint32_t cc[kClasses] = {0, 0, 0, 0, 0};
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
-            cls_r[k] = 3;  // no tensor
+            cls_r[k] = 7;  // no tensor
             w_r[k] = 0;
             if (q < n) {
                 const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
-                const uint32_t c = best ? 2u : ready_class(K);
+                const uint32_t c = ready_class(K, best);
                 const uint32_t pc = packed_get(pend, (uint32_t)q);
-                w_r[k] = ((uint64_t)(kUnplacedBit | (c << kClassShift) | pc) << 32) | su[q];
-                cls_r[k] = pc == 0 ? c + 4 : c;  // +4: a seed
+                w_r[k] = ((uint64_t)(kUnplacedBit | class_bits(c) | pc) << 32) | su[q];
+                cls_r[k] = pc == 0 ? c + 8 : c;  // +8: a seed
             }
 #pragma unroll
-            for (int c = 0; c < 3; ++c)
-                cc[c] += (uint32_t)__popcll(__ballot((cls_r[k] & 3u) == (uint32_t)c && cls_r[k] != 3u));
+            for (int c = 0; c < kClasses; ++c)
+                cc[c] += (uint32_t)__popcll(__ballot((cls_r[k] & 7u) == (uint32_t)c));
         }
         if (lane_id == 0) {
 #pragma unroll
-            for (int c = 0; c < 3; ++c)
+            for (int c = 0; c < kClasses; ++c)
                 if (cc[c]) atomicAdd(&ncls[c], cc[c]);
         }
     }
@@ -1096,21 +1129,25 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     }
     const uint32_t spare = (uint32_t)N;  // ofsz[N]: never placed, size 0
     if (tid == 0) ofsz[spare] = (uint64_t)kUnplacedBit << 32;
-    const uint32_t region[3] = {0u, ncls[0], ncls[0] + ncls[1]};
+    uint32_t region[kClasses];
+    region[0] = 0;
+#pragma unroll
+    for (int c = 1; c < kClasses; ++c) region[c] = region[c - 1] + ncls[c - 1];
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
-        const bool seed = q < n && cls_r[k] >= 4u;
+        const bool seed = q < n && cls_r[k] >= 8u;
 #pragma unroll
-        for (int c = 0; c < 3; ++c) {
-            const uint64_t m = __ballot(seed && (cls_r[k] & 3u) == (uint32_t)c);
+        for (int c = 0; c < kClasses; ++c) {
+            const uint64_t m = __ballot(seed && (cls_r[k] & 7u) == (uint32_t)c);
             if (!m) continue;
             uint32_t base = 0;
             if (lane_id == 0) base = atomicAdd(&seeds[c], (uint32_t)__popcll(m));
             base = (uint32_t)__builtin_amdgcn_readlane((int)base, 0);
             const uint32_t below = __builtin_amdgcn_mbcnt_hi(
                 (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            if (seed && (cls_r[k] & 3u) == (uint32_t)c) readyq[region[c] + base + below] = (uint16_t)q;
+            if (seed && (cls_r[k] & 7u) == (uint32_t)c)
+                readyq[region[c] + base + below] = (uint16_t)q;
         }
     }
     __syncthreads();
@@ -1118,112 +1155,111 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
     // ---- placement in rounds (Kahn's order over the predecessor DAG): round
     // r fits every tensor released in round r - 1 -- all of its predecessors
-    // are placed, and no two of them intersect.  Lanes are dealt out over the
-    // workgroup, quads first (tensors of 9..16 neighbours) and then lane
-    // pairs (up to 8), four neighbours per lane, so groups stay aligned;
-    // rows of 16 lanes (up to 64 neighbours; the whole wave beyond) take the
-    // rest from the last wave down.  A group gathers the neighbours' words (the
-    // placed ones are exactly the predecessors), moves the candidate offset
-    // past the highest overlapping end until nothing overlaps, publishes the
-    // word and decrements its successors' pending counts; those reaching zero
-    // are appended for the next round.  Per-round append counters rotate over
-    // three slots so that one barrier per round suffices.
+    // are placed, and no two of them intersect.  The round's tensors are
+    // dealt over the workgroup's lanes in one pass, eight-lane groups first
+    // (neighbour counts 33..64), then quads (17..32), pairs (9..16) and single
+    // lanes (up to 8), so every group is aligned; eight neighbours a lane.
+    // A lane sorts its neighbours' ranges by offset and sweeps them once for
+    // the lowest start clear of them; a group takes the maximum over its lanes
+    // until no lane moves.  Then the word is published and the successors'
+    // pending counts decremented; those reaching zero are appended for the
+    // next round.  Tensors with more than 64 neighbours (under BEST_FIT, more
+    // than 8) take a whole wave each, dealt over the waves.  Waves with no
+    // lane in the round go straight to its barrier.  Per-round append
+    // counters rotate over three slots so that one barrier per round
+    // suffices.
     auto place_rounds = [&](auto long_tag) {
         constexpr bool LONG = decltype(long_tag)::value;
         const LeftLists ll{lents, longtab};
         const int lane = lane_id;
-        const uint32_t g16 = lane & 15, row = (uint32_t)tid >> 4;
-        constexpr uint32_t kRows = BLOCK / kRowLanes;
-        uint32_t bgn[3] = {0, 0, 0}, end[3] = {seeds[0], seeds[1], seeds[2]};
-        for (int round = 0; bgn[0] < end[0] || bgn[1] < end[1] || bgn[2] < end[2]; ++round) {
+        const uint32_t wbase = (uint32_t)(tid & ~(kWave - 1));
+        uint32_t bgn[kClasses] = {0, 0, 0, 0, 0};
+        uint32_t end[kClasses];
+#pragma unroll
+        for (int c = 0; c < kClasses; ++c) end[c] = seeds[c];
+        for (int round = 0;; ++round) {
+            const uint32_t n0 = end[0] - bgn[0], n1 = end[1] - bgn[1], n2 = end[2] - bgn[2];
+            const uint32_t n3 = end[3] - bgn[3], n4 = end[4] - bgn[4];
+            if ((n0 | n1 | n2 | n3 | n4) == 0) break;
             if (round > n) {  // cannot happen: every round places a tensor
                 if (tid == 0) raise_status(status, MP_EDEVICE);
                 break;
             }
             const int cur = round % 3, nxt = (round + 1) % 3;
-            if (tid == 0) nready[nxt] = 0;
-            const ReadyLists rl{readyq,
-                                {region[0] + end[0], region[1] + end[1], region[2] + end[2]},
-                                &nready[cur]};
-            const uint32_t nq = end[1] - bgn[1], np = end[0] - bgn[0];
-            for (uint32_t it = 0;; ++it) {
-                const uint32_t gl = it * BLOCK + (uint32_t)tid;  // lane slot over the workgroup
-                const bool quad = gl < 4 * nq;
-                const bool hs = quad || gl < 4 * nq + 2 * np;
-                const uint32_t g = quad ? (gl & 3u) : (gl & 1u);
-                const uint32_t i1 = bgn[2] + (kRows - 1 - row) + kRows * it;
-                const bool hb = i1 < end[2];
-                uint32_t qs = 0;
-                if (hs)
-                    qs = quad ? readyq[region[1] + bgn[1] + (gl >> 2)]
-                              : readyq[region[0] + bgn[0] + ((gl - 4 * nq) >> 1)];
-                const uint32_t qb = hb ? (uint32_t)readyq[region[2] + i1] : 0u;
-                const bool any_s = __ballot(hs) != 0, any_b = __ballot(hb) != 0;
-                if (!any_s && !any_b) break;
-                if (any_s) {
-                    const Item is = load_item(qs, hs, spare, ofsz, lbeg, rlen);
-                    uint32_t o[kSmallSlots], e[kSmallSlots];
-                    gather<kSmallSlots, LONG>(is, g, ofsz, ll, o, e);
-                    uint32_t x = 0;
-                    while (true) {  // jump past the highest overlapping end until none moves
-                        const uint32_t mm = pair_quad_max_u32(overlap_end(o, e, x, is.s), quad);
-                        const bool mv = mm > x;
-                        x = mv ? mm : x;
-                        if (!__ballot(mv)) break;
-                    }
-                    if (hs && g == 0) ofsz[is.q] = ((uint64_t)x << 32) | is.s;
-                    uint32_t dec[kSmallSlots], ids[kSmallSlots];
-                    successors(g * kSmallSlots, is.K, o, dec, ids);
-                    release_successors(dec, ids, ofsz, rl, lane);
-                }
-                if (any_b) {
-                    const Item ib = load_item(qb, hb, spare, ofsz, lbeg, rlen);
-                    const bool mid = hb && ib.K <= kRowK;
-                    const Item im = mid ? ib : Item{spare, 0, 0, 0, 0};  // wider: whole wave
-                    uint32_t o[kSlots], e[kSlots], dec[kSlots], ids[kSlots];
-                    gather<kSlots, LONG>(im, g16, ofsz, ll, o, e);
-                    uint32_t x = 0;
-                    if (best) {  // the sort permutes the slots: successors first
-                        successors(g16 * kSlots, im.K, o, dec, ids);
-                        x = best_fit_group<kRowLanes>(o, e, im.s, g16);
-                    }
-                    while (!best) {
-                        const uint32_t mm = row_max_u32(overlap_end(o, e, x, im.s));
-                        const bool mv = mm > x;
-                        x = mv ? mm : x;
-                        if (!__ballot(mv)) break;
-                    }
-                    if (mid && g16 == 0) ofsz[ib.q] = ((uint64_t)x << 32) | ib.s;
-                    if (!best) successors(g16 * kSlots, im.K, o, dec, ids);
-                    release_successors(dec, ids, ofsz, rl, lane);
-                }
+            if (tid == 0) {
+                nready[nxt] = 0;
+                nwide[nxt] = 0;
             }
-            // class-2 tensors with more than 64 neighbours: the whole wave
-            // each, dealt over the waves
-            for (uint32_t i0 = bgn[2] + (uint32_t)(tid & ~(kWave - 1)); i0 < end[2];
-                 i0 += BLOCK) {
-                const uint32_t i = i0 + (uint32_t)lane;
-                const uint32_t qw = i < end[2] ? (uint32_t)readyq[region[2] + i] : 0u;
-                const Item iw = load_item(qw, i < end[2], spare, ofsz, lbeg, rlen);
-                uint64_t wide = __ballot(i < end[2] && iw.K > kRowK);
-                while (wide) {
-                    const int src = __ffsll((long long)wide) - 1;
-                    wide &= wide - 1;
-                    const Item one{(uint32_t)__builtin_amdgcn_readlane((int)iw.q, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.s, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.lb, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.L, src),
-                                   (uint32_t)__builtin_amdgcn_readlane((int)iw.K, src)};
-                    place_wave<LONG>(one, ofsz, ll, rl, lane, best);
+            const ReadyLists rl{readyq,
+                                {region[0] + end[0], region[1] + end[1], region[2] + end[2],
+                                 region[3] + end[3], region[4] + end[4]},
+                                &nready[cur], &nwide[cur]};
+            // lane space of the round: [0, a3) octs, [a3, a2) quads, [a2, a1)
+            // pairs, [a1, tot) single lanes
+            const uint32_t a3 = 8u * n3, a2 = a3 + 4u * n2, a1 = a2 + 2u * n1, tot = a1 + n0;
+            for (uint32_t pass = 0; pass < tot; pass += BLOCK) {
+                if (pass + wbase >= tot) break;  // wave-uniform: nothing for this wave
+                const uint32_t gl = pass + (uint32_t)tid;
+                uint32_t G, idx, c;
+                if (gl < a3) {
+                    G = 8; c = 3; idx = gl >> 3;
+                } else if (gl < a2) {
+                    G = 4; c = 2; idx = (gl - a3) >> 2;
+                } else if (gl < a1) {
+                    G = 2; c = 1; idx = (gl - a2) >> 1;
+                } else {
+                    G = 1; c = 0; idx = gl - a1;
                 }
+                const bool has = gl < tot;
+                const uint32_t g = gl & (G - 1u);
+                uint32_t q = 0;
+                if (has) {
+                    uint32_t at = region[0] + bgn[0];
+                    at = c == 1 ? region[1] + bgn[1] : at;
+                    at = c == 2 ? region[2] + bgn[2] : at;
+                    at = c == 3 ? region[3] + bgn[3] : at;
+                    q = readyq[at + idx];
+                }
+                const Item it = load_item(q, has, spare, ofsz, lbeg, rlen);
+                uint32_t o[kLaneSlots], e[kLaneSlots];
+                gather<kLaneSlots, LONG>(it, g, ofsz, ll, o, e);
+                sort8(o, e);
+                uint32_t x;
+                if (best) {
+                    x = sweep_best(o, e, it.s);  // class 0 only: K <= 8, one lane
+                } else {
+                    x = group_max_u32(sweep_lowest(o, e, 0u, it.s), G);
+                    if (__ballot(G > 1u)) {
+                        while (true) {
+                            const uint32_t xn = group_max_u32(sweep_lowest(o, e, x, it.s), G);
+                            if (!__ballot(xn != x)) break;
+                            x = xn;
+                        }
+                    }
+                }
+                if (has && g == 0) ofsz[it.q] = ((uint64_t)x << 32) | it.s;
+                release<kLaneSlots>(o, ofsz, rl, lane);
+            }
+            // more neighbours than eight lanes hold: the whole wave each, dealt
+            // over the waves
+            for (uint32_t i0 = bgn[4] + (wbase / kWave); i0 < end[4]; i0 += BLOCK / kWave) {
+                const uint32_t qw = readyq[region[4] + i0];
+                const Item iw = load_item(qw, true, spare, ofsz, lbeg, rlen);
+                const Item one{(uint32_t)__builtin_amdgcn_readfirstlane((int)iw.q),
+                               (uint32_t)__builtin_amdgcn_readfirstlane((int)iw.s),
+                               (uint32_t)__builtin_amdgcn_readfirstlane((int)iw.lb),
+                               (uint32_t)__builtin_amdgcn_readfirstlane((int)iw.L),
+                               (uint32_t)__builtin_amdgcn_readfirstlane((int)iw.K)};
+                place_wave<LONG, best>(one, spare, ofsz, ll, rl, lane);
             }
             __syncthreads();
             const unsigned long long added = nready[cur];
+            const uint32_t added_w = nwide[cur];
 #pragma unroll
-            for (int c = 0; c < 3; ++c) {
-                bgn[c] = end[c];
-                end[c] += (uint32_t)(added >> (16 * c)) & 0xFFFFu;
-            }
+            for (int c = 0; c < kClasses; ++c) bgn[c] = end[c];
+#pragma unroll
+            for (int c = 0; c < 4; ++c) end[c] += (uint32_t)(added >> (16 * c)) & 0xFFFFu;
+            end[4] += added_w;
         }
     };
     if (nlong) place_rounds(std::true_type{});
