@@ -133,17 +133,31 @@ __device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
     return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
 }
 
-// Maximum over each aligned group of G lanes (G = 1, 2, 4 or 8, per lane;
-// the lanes of a group agree on it), returned to the group: swaps within
-// pairs and quads (quad_perm), then between the two quads of each half row
-// (half-row mirror).  All 64 lanes must be active.
+// Maximum over each aligned group of G lanes (G a power of two up to 64,
+// per lane; the lanes of a group agree on it), returned to the group: swaps
+// within pairs and quads (quad_perm), between the quads of each half row
+// (half-row mirror) and the halves of each row (rotation by 8); groups of
+// 32 and 64 lanes combine the row maxima read from the first lane of each
+// row.  All 64 lanes must be active.
 __device__ __forceinline__ uint32_t group_max_u32(uint32_t v, uint32_t G) {
     uint32_t t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, false));
     v = G >= 2 ? t : v;
     t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, false));
     v = G >= 4 ? t : v;
     t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, false));
-    return G >= 8 ? t : v;
+    v = G >= 8 ? t : v;
+    t = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x128, 0xF, 0xF, false));
+    v = G >= 16 ? t : v;
+    if (__ballot(G >= 32u)) {
+        const uint32_t m0 = (uint32_t)__builtin_amdgcn_readlane((int)v, 0);
+        const uint32_t m1 = (uint32_t)__builtin_amdgcn_readlane((int)v, 16);
+        const uint32_t m2 = (uint32_t)__builtin_amdgcn_readlane((int)v, 32);
+        const uint32_t m3 = (uint32_t)__builtin_amdgcn_readlane((int)v, 48);
+        const uint32_t h0 = max(m0, m1), h1 = max(m2, m3);
+        const uint32_t h = (threadIdx.x & 32u) ? h1 : h0;
+        v = G >= 64 ? max(h0, h1) : (G >= 32 ? h : v);
+    }
+    return v;
 }
 
 template <int BLOCK>
@@ -175,6 +189,23 @@ __device__ __forceinline__ uint32_t wave_inclusive_sum_dpp(uint32_t v) {
     v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xF, 0xF, false);
     v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xA, 0xF, false);
     v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xC, 0xF, false);
+    return v;
+}
+
+// Inclusive sum of 64-bit values over the 64 lanes (both halves moved by DPP
+// from the same source lane, added in 64 bits).  All 64 lanes must be active.
+__device__ __forceinline__ uint64_t wave_inclusive_sum64_dpp(uint64_t v) {
+#define MP_STEP64(ctrl, rows)                                                                   \
+    {                                                                                           \
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, ctrl,    \
+                                                                  rows, 0xF, false);           \
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), \
+                                                                  ctrl, rows, 0xF, false);     \
+        v += ((uint64_t)hi << 32) | lo;                                                         \
+    }
+    MP_STEP64(0x111, 0xF) MP_STEP64(0x112, 0xF) MP_STEP64(0x114, 0xF) MP_STEP64(0x118, 0xF)
+    MP_STEP64(0x142, 0xA) MP_STEP64(0x143, 0xC)
+#undef MP_STEP64
     return v;
 }
 
@@ -266,26 +297,35 @@ __device__ __forceinline__ void cex(uint32_t& oa, uint32_t& ea, uint32_t& ob, ui
     ob = sw ? to : ob;
     eb = sw ? te : eb;
 }
-// The lane's eight slots sorted by offset (a 19-comparator network); unplaced
-// neighbours and empty slots (offsets at or above 2^31) end up last.
-__device__ __forceinline__ void sort8(uint32_t (&o)[8], uint32_t (&e)[8]) {
+// The lane's S slots sorted by offset (optimal networks: 1, 5 and 19
+// comparators for 2, 4 and 8 slots); unplaced neighbours and empty slots
+// (offsets at or above 2^31) end up last.
+template <int S>
+__device__ __forceinline__ void sort_slots(uint32_t (&o)[S], uint32_t (&e)[S]) {
 #define MP_CEX(a, b) cex(o[a], e[a], o[b], e[b])
-    MP_CEX(0, 2); MP_CEX(1, 3); MP_CEX(4, 6); MP_CEX(5, 7);
-    MP_CEX(0, 4); MP_CEX(1, 5); MP_CEX(2, 6); MP_CEX(3, 7);
-    MP_CEX(0, 1); MP_CEX(2, 3); MP_CEX(4, 5); MP_CEX(6, 7);
-    MP_CEX(2, 4); MP_CEX(3, 5);
-    MP_CEX(1, 4); MP_CEX(3, 6);
-    MP_CEX(1, 2); MP_CEX(3, 4); MP_CEX(5, 6);
+    if constexpr (S == 2) {
+        MP_CEX(0, 1);
+    } else if constexpr (S == 4) {
+        MP_CEX(0, 1); MP_CEX(2, 3); MP_CEX(0, 2); MP_CEX(1, 3); MP_CEX(1, 2);
+    } else if constexpr (S == 8) {
+        MP_CEX(0, 2); MP_CEX(1, 3); MP_CEX(4, 6); MP_CEX(5, 7);
+        MP_CEX(0, 4); MP_CEX(1, 5); MP_CEX(2, 6); MP_CEX(3, 7);
+        MP_CEX(0, 1); MP_CEX(2, 3); MP_CEX(4, 5); MP_CEX(6, 7);
+        MP_CEX(2, 4); MP_CEX(3, 5);
+        MP_CEX(1, 4); MP_CEX(3, 6);
+        MP_CEX(1, 2); MP_CEX(3, 4); MP_CEX(5, 6);
+    }
 #undef MP_CEX
 }
 
 // Lowest y >= x at which [y, y + s) meets none of the lane's ranges, the
 // ranges sorted by offset: one pass suffices, since a range passed over
 // either ended at or below y or was jumped past, and y only grows.
-__device__ __forceinline__ uint32_t sweep_lowest(const uint32_t (&o)[8], const uint32_t (&e)[8],
+template <int S>
+__device__ __forceinline__ uint32_t sweep_lowest(const uint32_t (&o)[S], const uint32_t (&e)[S],
                                                  uint32_t x, uint32_t s) {
 #pragma unroll
-    for (int r = 0; r < 8; ++r) x = (o[r] < x + s && x < e[r]) ? e[r] : x;
+    for (int r = 0; r < S; ++r) x = (o[r] < x + s && x < e[r]) ? e[r] : x;
     return x;
 }
 
@@ -293,11 +333,12 @@ __device__ __forceinline__ uint32_t sweep_lowest(const uint32_t (&o)[8], const u
 // range r runs from the highest end among ranges before it to its offset;
 // the smallest gap that holds s wins (lowest start among equals), else the
 // space above every range.
-__device__ __forceinline__ uint32_t sweep_best(const uint32_t (&o)[8], const uint32_t (&e)[8],
+template <int S>
+__device__ __forceinline__ uint32_t sweep_best(const uint32_t (&o)[S], const uint32_t (&e)[S],
                                                uint32_t s) {
     uint32_t m = 0, bg = kNoSlot, bs = 0;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) {
+    for (int r = 0; r < S; ++r) {
         const bool placed = o[r] < kUnplacedBit;
         const bool fits = placed && o[r] >= m && o[r] - m >= s && o[r] - m < bg;
         bs = fits ? m : bs;
@@ -426,16 +467,17 @@ __device__ __forceinline__ Item load_item(uint32_t q, bool has, uint32_t spare,
 template <int S, bool LONG>
 __device__ __forceinline__ void gather(const Item& it, uint32_t g, const uint64_t* ofsz,
                                        const LeftLists& ll, uint32_t (&o)[S], uint32_t (&e)[S]) {
-    static_assert(S == 4 || S == 8, "4 or 8 slots a lane");
+    static_assert(S == 1 || S == 2 || S == 4 || S == 8, "1, 2, 4 or 8 slots a lane");
+    constexpr int kW = S == 8 ? 2 : 1;  // 32-bit words of entries a lane needs
     uint32_t id[S];
     const uint32_t k0 = g * S;
     const uint32_t s0 = it.lb + min(k0, it.L);
     const uint32_t* w32 = reinterpret_cast<const uint32_t*>(ll.ent) + (s0 >> 2);
-    uint32_t by[S / 4];
+    uint32_t by[kW];
     {
         const uint32_t b0 = w32[0], b1 = w32[1];
         by[0] = __builtin_amdgcn_alignbyte(b1, b0, s0 & 3u);
-        if (S == 8) by[S / 4 - 1] = __builtin_amdgcn_alignbyte(w32[2], b1, s0 & 3u);
+        if (kW == 2) by[kW - 1] = __builtin_amdgcn_alignbyte(w32[2], b1, s0 & 3u);
     }
     // slot r holds neighbour k0 + r: left entry r when r < lr, band position
     // rb + r when lr <= r < kr, nothing beyond (the tensor's own word is read)
@@ -490,11 +532,11 @@ __device__ void place_wave(const Item& it, uint32_t spare, uint64_t* ofsz, const
     while (clean < nch) {
         if (nch > 1 || c == 0) {
             gather<kLaneSlots, LONG>(it, c * kWave + g0, ofsz, ll, o, e);
-            sort8(o, e);
+            sort_slots<kLaneSlots>(o, e);
         }
         bool moved = false;
         while (true) {
-            const uint32_t xn = wave_max_u32(sweep_lowest(o, e, x, it.s));
+            const uint32_t xn = wave_max_u32(sweep_lowest<kLaneSlots>(o, e, x, it.s));
             if (xn == x) break;
             x = xn;
             moved = true;
@@ -767,11 +809,16 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     int64_t* __restrict__ peak_out, int64_t* __restrict__ lb_out, int32_t* __restrict__ status) {
     constexpr bool best = BEST;  // BEST_FIT: one lane up to 8 neighbours, else the whole wave
     extern __shared__ __align__(16) unsigned char smem[];
+    // static LDS: at most kStaticLds bytes (checked at launch), or four
+    // workgroups of a 2000-tensor trace no longer fit a CU
     __shared__ uint64_t red[BLOCK / kWave];
+    __shared__ uint64_t red3[3][BLOCK / kWave];  // ingest reductions, then the prefix pass's
+    uint32_t(*red32)[BLOCK / kWave] = reinterpret_cast<uint32_t(*)[BLOCK / kWave]>(&red3[0][0]);
     __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class 0-3)
     __shared__ uint32_t nwide[3];             // ... of class 4
-    __shared__ uint32_t ncls[kClasses];       // tensors per ready class
-    __shared__ uint32_t seeds[kClasses];      // tensors per class without predecessors
+    __shared__ unsigned long long ncls64;     // tensors per ready class 0-3 (16-bit fields)
+    __shared__ unsigned long long seeds64;    // ... without predecessors
+    __shared__ uint32_t ncls_w, seeds_w;      // ... of class 4
     __shared__ uint16_t longtab[kLongSlots];  // positions of the long tensors
     __shared__ uint32_t nlong;
 
@@ -798,7 +845,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     if (tid == 0) {
         nready[0] = nready[1] = nready[2] = 0;
         nwide[0] = nwide[1] = nwide[2] = 0;
-        for (int c = 0; c < kClasses; ++c) ncls[c] = seeds[c] = 0;
+        ncls_w = seeds_w = 0;
+        ncls64 = seeds64 = 0;
         nlong = 0;
     }
     const int64_t lo = begin[b], hi = begin[b + 1];
@@ -856,7 +904,6 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         flags = wave_reduce(flags, OpOr<uint32_t>());
         orv = wave_reduce(orv, OpOr<uint64_t>());
         sum = wave_reduce(sum, OpSatAdd());
-        __shared__ uint64_t red3[3][BLOCK / kWave];
         if (lane == 0) {
             red3[0][wid] = flags;
             red3[1][wid] = orv;
@@ -923,9 +970,25 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
         // ---- reach, band lengths, live-bytes deltas, reach histogram, long
         // tensors.  The reach is the first position past q whose first op is
-        // after last[q]: the next four positions are probed at once (short
-        // bands, the common case, end there), longer bands gallop from the
-        // fourth.
+        // after last[q].  When the ops are no more than the tensor slots (one
+        // op per tensor or fewer, as recorded traces are), it is read from a
+        // table over ops, P[op] = number of positions whose first op is at
+        // most op, filled from the first ops in position order (P sits in the
+        // left-list starts' region, unused until the prefix pass).  Otherwise
+        // the next four positions are probed at once (short bands, the common
+        // case, end there) and longer bands gallop from the fourth.
+        const bool by_table = n_ops <= (int32_t)N + 1;
+        uint16_t* ptab = lbeg;
+        if (by_table) {
+            // position i owns the ops [first[i], first[i + 1]) (i = -1: the ops
+            // before the first first op; i = n - 1: up to the last op)
+            for (int i = tid - 1; i < n; i += BLOCK) {
+                const int a = i < 0 ? 0 : fst[i];
+                const int z = i + 1 < n ? fst[i + 1] : n_ops;
+                for (int op = a; op < z; ++op) ptab[op] = (uint16_t)(i + 1);
+            }
+            __syncthreads();
+        }
         int32_t rch[ITEMS];
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
@@ -933,11 +996,15 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             rch[k] = q + 1;
             if (q < n) {
                 const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
-                const int32_t f1 = q + 1 < n ? fst[q + 1] : INT32_MAX;
-                const int32_t f2 = q + 2 < n ? fst[q + 2] : INT32_MAX;
-                const int32_t f3 = q + 3 < n ? fst[q + 3] : INT32_MAX;
-                const int32_t f4 = q + 4 < n ? fst[q + 4] : INT32_MAX;
-                rch[k] = q + 1 + (f1 <= l) + (f2 <= l) + (f3 <= l) + (f4 <= l);
+                if (by_table) {
+                    rch[k] = ptab[l];
+                } else {
+                    const int32_t f1 = q + 1 < n ? fst[q + 1] : INT32_MAX;
+                    const int32_t f2 = q + 2 < n ? fst[q + 2] : INT32_MAX;
+                    const int32_t f3 = q + 3 < n ? fst[q + 3] : INT32_MAX;
+                    const int32_t f4 = q + 4 < n ? fst[q + 4] : INT32_MAX;
+                    rch[k] = q + 1 + (f1 <= l) + (f2 <= l) + (f3 <= l) + (f4 <= l);
+                }
             }
         }
 #pragma unroll
@@ -948,7 +1015,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 const int64_t sz = unsorted ? size[lo + perm[q]] : sz_r[k];
                 const uint32_t sq = (uint32_t)((uint64_t)sz >> sh);
                 int a = rch[k];
-                if (a == q + 5) {  // first[q + 4] <= l: gallop on
+                if (!by_table && a == q + 5) {  // first[q + 4] <= l: gallop on
                     int known = q + 4, step = 8, probe = q + 8;  // first[known] <= l
                     while (probe < n && fst[probe] <= l) {
                         known = probe;
@@ -1000,10 +1067,26 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 ps += pack(rlen[i], packed_get(hist, (uint32_t)i), (uint32_t)i);
                 ds += live[i];
             }
-            uint64_t ptot;
-            uint64_t prun = block_exclusive_sum<BLOCK>(ps, &ptot, red);
-            uint32_t dtot;
-            uint32_t drun = block_exclusive_sum<BLOCK>(ds, &dtot, scratch);
+            // both prefix sums over the workgroup at once (wave scans by DPP,
+            // one barrier), then both maxima (one more)
+            const int lane = tid & (kWave - 1), wid = tid / kWave;
+            const uint64_t pin = wave_inclusive_sum64_dpp(ps);
+            const uint32_t din = wave_inclusive_sum_dpp(ds);
+            if (lane == kWave - 1) {
+                red[wid] = pin;
+                red32[0][wid] = din;
+            }
+            __syncthreads();
+            uint64_t prun = pin - ps, ptot = 0;
+            uint32_t drun = din - ds;
+#pragma unroll
+            for (int w = 0; w < BLOCK / kWave; ++w) {
+                const uint64_t t = red[w];
+                const uint32_t u = red32[0][w];
+                prun += w < wid ? t : 0ull;
+                drun += w < wid ? u : 0u;
+                ptot += t;
+            }
             uint32_t lm = 0;
             uint16_t* cursor16 = reinterpret_cast<uint16_t*>(cursor);
             for (int i = a0; i < a1; ++i) {
@@ -1025,9 +1108,20 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 bstart[n] = (uint16_t)n_pairs;
                 lbeg[n] = (uint16_t)n_pairs;
             }
-            live_max = block_reduce<BLOCK>(lm, OpMax<uint32_t>(), scratch);
+            const uint32_t wl = wave_max_u32(lm), wk = wave_max_u32(kmax);
+            if (lane == 0) {
+                red32[1][wid] = wl;
+                red32[2][wid] = wk;
+            }
+            __syncthreads();
+            live_max = 0;
+            kmax = 0;
+#pragma unroll
+            for (int w = 0; w < BLOCK / kWave; ++w) {
+                live_max = max(live_max, red32[1][w]);
+                kmax = max(kmax, red32[2][w]);
+            }
         }
-        kmax = block_reduce<BLOCK>(kmax, OpMax<uint32_t>(), scratch);
         general = n_pairs > (uint32_t)cap_lists || (best && kmax > kBestMaxK);
     }
     if (general) {
@@ -1093,33 +1187,62 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
     // ---- placement words (pending count and ready class while unplaced),
     // class regions, and the tensors without predecessors as seeds.  The
-    // words overwrite the fill's arrays: read everything first.
+    // words overwrite the fill's arrays: read everything first.  Per lane,
+    // the counts per class of its tensors and of its seeds go in 10-bit
+    // fields (classes 0-2 in one word, 3-4 in another); one wave scan of the
+    // seed counts and one reservation per wave place the seeds.
     const int lane_id = tid & (kWave - 1);
     uint64_t w_r[ITEMS];
     uint32_t cls_r[ITEMS];
+    uint32_t tlo = 0, thi = 0, slo = 0, shi = 0, sb4 = 0;
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) {
+        const int q = tid + k * BLOCK;
+        cls_r[k] = 7;  // no tensor
+        w_r[k] = 0;
+        if (q < n) {
+            const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
+            const uint32_t c = ready_class(K, best);
+            const uint32_t pc = packed_get(pend, (uint32_t)q);
+            w_r[k] = ((uint64_t)(kUnplacedBit | class_bits(c) | pc) << 32) | su[q];
+            cls_r[k] = pc == 0 ? c + 8 : c;  // +8: a seed
+            const uint32_t f = 1u << (10u * (c < 3u ? c : c - 3u));
+            tlo += c < 3u ? f : 0u;
+            thi += c < 3u ? 0u : f;
+            slo += (c < 3u && pc == 0) ? f : 0u;
+            shi += (c >= 3u && pc == 0) ? f : 0u;
+        }
+    }
     {
-        uint32_t cc[kClasses] = {0, 0, 0, 0, 0};
-#pragma unroll
-        for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
-            cls_r[k] = 7;  // no tensor
-            w_r[k] = 0;
-            if (q < n) {
-                const uint32_t K = (uint32_t)lbeg[q + 1] - lbeg[q] + rlen[q];
-                const uint32_t c = ready_class(K, best);
-                const uint32_t pc = packed_get(pend, (uint32_t)q);
-                w_r[k] = ((uint64_t)(kUnplacedBit | class_bits(c) | pc) << 32) | su[q];
-                cls_r[k] = pc == 0 ? c + 8 : c;  // +8: a seed
-            }
-#pragma unroll
-            for (int c = 0; c < kClasses; ++c)
-                cc[c] += (uint32_t)__popcll(__ballot((cls_r[k] & 7u) == (uint32_t)c));
-        }
+        const uint32_t tl = wave_inclusive_sum_dpp(tlo), th = wave_inclusive_sum_dpp(thi);
+        const uint32_t sl = wave_inclusive_sum_dpp(slo), sh2 = wave_inclusive_sum_dpp(shi);
+        const uint32_t Tl = (uint32_t)__builtin_amdgcn_readlane((int)tl, 63);
+        const uint32_t Th = (uint32_t)__builtin_amdgcn_readlane((int)th, 63);
+        const uint32_t Sl = (uint32_t)__builtin_amdgcn_readlane((int)sl, 63);
+        const uint32_t Sh = (uint32_t)__builtin_amdgcn_readlane((int)sh2, 63);
+        auto pack4 = [](uint32_t l, uint32_t h) {  // classes 0-3 as 16-bit fields
+            return (unsigned long long)(l & 0x3FFu) | ((unsigned long long)((l >> 10) & 0x3FFu) << 16) |
+                   ((unsigned long long)(l >> 20) << 32) | ((unsigned long long)(h & 0x3FFu) << 48);
+        };
+        uint32_t b0 = 0, b1 = 0, b4 = 0;
         if (lane_id == 0) {
-#pragma unroll
-            for (int c = 0; c < kClasses; ++c)
-                if (cc[c]) atomicAdd(&ncls[c], cc[c]);
+            atomicAdd(&ncls64, pack4(Tl, Th));
+            if (Th >> 10) atomicAdd(&ncls_w, Th >> 10);
+            const unsigned long long base = atomicAdd(&seeds64, pack4(Sl, Sh));
+            b0 = (uint32_t)base;
+            b1 = (uint32_t)(base >> 32);
+            if (Sh >> 10) b4 = atomicAdd(&seeds_w, Sh >> 10);
         }
+        b0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b0);
+        b1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b1);
+        b4 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b4);
+        const uint32_t xl = sl - slo, xh = sh2 - shi;  // seeds of the lanes before
+        // this lane's next seed position in each class list (region added below)
+        tlo = b0 & 0xFFFFu; tlo += xl & 0x3FFu;
+        thi = (b0 >> 16) + ((xl >> 10) & 0x3FFu);
+        slo = (b1 & 0xFFFFu) + (xl >> 20);
+        shi = (b1 >> 16) + (xh & 0x3FFu);
+        sb4 = b4 + (xh >> 10);
     }
     __syncthreads();
 #pragma unroll
@@ -1130,24 +1253,30 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const uint32_t spare = (uint32_t)N;  // ofsz[N]: never placed, size 0
     if (tid == 0) ofsz[spare] = (uint64_t)kUnplacedBit << 32;
     uint32_t region[kClasses];
-    region[0] = 0;
-#pragma unroll
-    for (int c = 1; c < kClasses; ++c) region[c] = region[c - 1] + ncls[c - 1];
+    {
+        const unsigned long long nc = ncls64;
+        region[0] = 0;
+        region[1] = (uint32_t)nc & 0xFFFFu;
+        region[2] = region[1] + ((uint32_t)(nc >> 16) & 0xFFFFu);
+        region[3] = region[2] + ((uint32_t)(nc >> 32) & 0xFFFFu);
+        region[4] = region[3] + (uint32_t)(nc >> 48);
+    }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
         const int q = tid + k * BLOCK;
-        const bool seed = q < n && cls_r[k] >= 8u;
-#pragma unroll
-        for (int c = 0; c < kClasses; ++c) {
-            const uint64_t m = __ballot(seed && (cls_r[k] & 7u) == (uint32_t)c);
-            if (!m) continue;
-            uint32_t base = 0;
-            if (lane_id == 0) base = atomicAdd(&seeds[c], (uint32_t)__popcll(m));
-            base = (uint32_t)__builtin_amdgcn_readlane((int)base, 0);
-            const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-                (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-            if (seed && (cls_r[k] & 7u) == (uint32_t)c)
-                readyq[region[c] + base + below] = (uint16_t)q;
+        if (q < n && cls_r[k] >= 8u) {
+            const uint32_t c = cls_r[k] & 7u;
+            uint32_t a = tlo;
+            a = c == 1 ? thi : a;
+            a = c == 2 ? slo : a;
+            a = c == 3 ? shi : a;
+            a = c == 4 ? sb4 : a;
+            readyq[region[c] + a] = (uint16_t)q;
+            tlo += c == 0 ? 1u : 0u;
+            thi += c == 1 ? 1u : 0u;
+            slo += c == 2 ? 1u : 0u;
+            shi += c == 3 ? 1u : 0u;
+            sb4 += c == 4 ? 1u : 0u;
         }
     }
     __syncthreads();
@@ -1158,10 +1287,11 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     // are placed, and no two of them intersect.  The round's tensors are
     // dealt over the workgroup's lanes in one pass, eight-lane groups first
     // (neighbour counts 33..64), then quads (17..32), pairs (9..16) and single
-    // lanes (up to 8), so every group is aligned; eight neighbours a lane.
-    // A lane sorts its neighbours' ranges by offset and sweeps them once for
-    // the lowest start clear of them; a group takes the maximum over its lanes
-    // until no lane moves.  Then the word is published and the successors'
+    // lanes (up to 8), so every group is aligned; eight neighbours a lane
+    // (a short round spreads them thinner: four a lane, groups twice as
+    // wide).  A lane sorts its neighbours' ranges by offset and
+    // sweeps them once for the lowest start clear of them; a group takes the
+    // maximum over its lanes until no lane moves.  Then the word is published and the successors'
     // pending counts decremented; those reaching zero are appended for the
     // next round.  Tensors with more than 64 neighbours (under BEST_FIT, more
     // than 8) take a whole wave each, dealt over the waves.  Waves with no
@@ -1175,8 +1305,12 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         const uint32_t wbase = (uint32_t)(tid & ~(kWave - 1));
         uint32_t bgn[kClasses] = {0, 0, 0, 0, 0};
         uint32_t end[kClasses];
+        {
+            const unsigned long long sd = seeds64;
 #pragma unroll
-        for (int c = 0; c < kClasses; ++c) end[c] = seeds[c];
+            for (int c = 0; c < 4; ++c) end[c] = (uint32_t)(sd >> (16 * c)) & 0xFFFFu;
+            end[kWideClass] = seeds_w;
+        }
         for (int round = 0;; ++round) {
             const uint32_t n0 = end[0] - bgn[0], n1 = end[1] - bgn[1], n2 = end[2] - bgn[2];
             const uint32_t n3 = end[3] - bgn[3], n4 = end[4] - bgn[4];
@@ -1194,52 +1328,69 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                                 {region[0] + end[0], region[1] + end[1], region[2] + end[2],
                                  region[3] + end[3], region[4] + end[4]},
                                 &nready[cur], &nwide[cur]};
-            // lane space of the round: [0, a3) octs, [a3, a2) quads, [a2, a1)
-            // pairs, [a1, tot) single lanes
-            const uint32_t a3 = 8u * n3, a2 = a3 + 4u * n2, a1 = a2 + 2u * n1, tot = a1 + n0;
-            for (uint32_t pass = 0; pass < tot; pass += BLOCK) {
-                if (pass + wbase >= tot) break;  // wave-uniform: nothing for this wave
-                const uint32_t gl = pass + (uint32_t)tid;
-                uint32_t G, idx, c;
-                if (gl < a3) {
-                    G = 8; c = 3; idx = gl >> 3;
-                } else if (gl < a2) {
-                    G = 4; c = 2; idx = (gl - a3) >> 2;
-                } else if (gl < a1) {
-                    G = 2; c = 1; idx = (gl - a2) >> 1;
-                } else {
-                    G = 1; c = 0; idx = gl - a1;
-                }
-                const bool has = gl < tot;
-                const uint32_t g = gl & (G - 1u);
-                uint32_t q = 0;
-                if (has) {
-                    uint32_t at = region[0] + bgn[0];
-                    at = c == 1 ? region[1] + bgn[1] : at;
-                    at = c == 2 ? region[2] + bgn[2] : at;
-                    at = c == 3 ? region[3] + bgn[3] : at;
-                    q = readyq[at + idx];
-                }
-                const Item it = load_item(q, has, spare, ofsz, lbeg, rlen);
-                uint32_t o[kLaneSlots], e[kLaneSlots];
-                gather<kLaneSlots, LONG>(it, g, ofsz, ll, o, e);
-                sort8(o, e);
-                uint32_t x;
-                if (best) {
-                    x = sweep_best(o, e, it.s);  // class 0 only: K <= 8, one lane
-                } else {
-                    x = group_max_u32(sweep_lowest(o, e, 0u, it.s), G);
-                    if (__ballot(G > 1u)) {
-                        while (true) {
-                            const uint32_t xn = group_max_u32(sweep_lowest(o, e, x, it.s), G);
-                            if (!__ballot(xn != x)) break;
-                            x = xn;
+            // lane space of the round at S slots a lane: class c takes groups
+            // of (8 / S) << c lanes, [0, a3) class 3, [a3, a2) class 2,
+            // [a2, a1) class 1, [a1, tot) class 0 (aligned: largest first).
+            // A round that fits the workgroup's lanes at four slots a lane is
+            // spread that way (shorter passes where the rounds are short; one
+            // or two a lane measured slower, the group maxima growing);
+            // BEST_FIT keeps eight.
+            auto run = [&](auto slots_tag) {
+                constexpr int S = decltype(slots_tag)::value;
+                constexpr uint32_t M = 8u / S;
+                const uint32_t a3 = 8u * M * n3, a2 = a3 + 4u * M * n2, a1 = a2 + 2u * M * n1;
+                const uint32_t tot = a1 + M * n0;
+                for (uint32_t pass = 0; pass < tot; pass += BLOCK) {
+                    if (pass + wbase >= tot) break;  // wave-uniform: nothing for this wave
+                    const uint32_t gl = pass + (uint32_t)tid;
+                    uint32_t c, lg;  // class, log2 of its group width
+                    if (gl < a3) {
+                        c = 3; lg = 3;
+                    } else if (gl < a2) {
+                        c = 2; lg = 2;
+                    } else if (gl < a1) {
+                        c = 1; lg = 1;
+                    } else {
+                        c = 0; lg = 0;
+                    }
+                    lg += (uint32_t)__builtin_ctz(M);
+                    const uint32_t G = 1u << lg;
+                    const uint32_t start = c == 3 ? 0u : (c == 2 ? a3 : (c == 1 ? a2 : a1));
+                    const uint32_t idx = (gl - start) >> lg;
+                    const bool has = gl < tot;
+                    const uint32_t g = gl & (G - 1u);
+                    uint32_t q = 0;
+                    if (has) {
+                        uint32_t at = region[0] + bgn[0];
+                        at = c == 1 ? region[1] + bgn[1] : at;
+                        at = c == 2 ? region[2] + bgn[2] : at;
+                        at = c == 3 ? region[3] + bgn[3] : at;
+                        q = readyq[at + idx];
+                    }
+                    const Item it = load_item(q, has, spare, ofsz, lbeg, rlen);
+                    uint32_t o[S], e[S];
+                    gather<S, LONG>(it, g, ofsz, ll, o, e);
+                    sort_slots<S>(o, e);
+                    uint32_t x;
+                    if (best) {
+                        x = sweep_best<S>(o, e, it.s);  // class 0 only: K <= 8, one lane
+                    } else {
+                        x = group_max_u32(sweep_lowest<S>(o, e, 0u, it.s), G);
+                        if (M > 1 || __ballot(G > 1u)) {
+                            while (true) {
+                                const uint32_t xn = group_max_u32(sweep_lowest<S>(o, e, x, it.s), G);
+                                if (!__ballot(xn != x)) break;
+                                x = xn;
+                            }
                         }
                     }
+                    if (has && g == 0) ofsz[it.q] = ((uint64_t)x << 32) | it.s;
+                    release<S>(o, ofsz, rl, lane);
                 }
-                if (has && g == 0) ofsz[it.q] = ((uint64_t)x << 32) | it.s;
-                release<kLaneSlots>(o, ofsz, rl, lane);
-            }
+            };
+            const uint32_t t8 = n0 + 2u * n1 + 4u * n2 + 8u * n3;  // lanes at eight slots
+            if (best || 2u * t8 > (uint32_t)BLOCK) run(std::integral_constant<int, 8>{});
+            else run(std::integral_constant<int, 4>{});
             // more neighbours than eight lanes hold: the whole wave each, dealt
             // over the waves
             for (uint32_t i0 = bgn[4] + (wbase / kWave); i0 < end[4]; i0 += BLOCK / kWave) {
@@ -1289,12 +1440,19 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
 
 __global__ void reset_status_kernel(int32_t* status) { *status = MP_OK; }
 
+// Static LDS of the kernel, rounded up (the per-workgroup budget minus this
+// is dynamic).
+constexpr size_t kStaticLds = 512;
+
 template <int BLOCK, int ITEMS, bool BEST>
 hipError_t launch_items(const BatchArgs& a, const BatchShape& s, hipStream_t st) {
     auto kern = plan_batch_kernel<BLOCK, ITEMS, BEST>;
-    hipError_t e = hipFuncSetAttribute((const void*)kern,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize,
-                                       (int)s.lds_bytes);
+    hipFuncAttributes fa{};
+    hipError_t e = hipFuncGetAttributes(&fa, (const void*)kern);
+    if (e != hipSuccess) return e;
+    if (fa.sharedSizeBytes > kStaticLds) return hipErrorInvalidConfiguration;  // LDS budget broken
+    e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)s.lds_bytes);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(kern, dim3((unsigned)a.n_traces), dim3(BLOCK), s.lds_bytes, st,
                        a.begin, a.num_ops, a.size, a.first, a.last, a.n_tensors, s.cap_n,
@@ -1303,9 +1461,6 @@ hipError_t launch_items(const BatchArgs& a, const BatchShape& s, hipStream_t st)
     return hipGetLastError();
 }
 
-// Static LDS of the kernel, rounded up (the per-workgroup budget minus this
-// is dynamic).
-constexpr size_t kStaticLds = 512;
 
 }  // namespace
 
