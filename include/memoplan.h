@@ -22,8 +22,9 @@
  *    int64 bytes, lifetimes int32 op indices, offsets int64 bytes.
  *  - Return value (host, synchronous): MP_OK when the work was enqueued;
  *    MP_EINVAL for bad host arguments (NULL pointer where data is needed,
- *    negative counts, unknown policy, workspace too small), in which case
- *    nothing is launched; MP_EDEVICE when a launch fails.
+ *    negative counts, counts above 2^40, unknown policy, workspace too
+ *    small), in which case nothing is launched; MP_EDEVICE when a launch
+ *    fails.
  *  - Data-dependent errors are found on the device and folded into the
  *    caller's device int32 `*status_out` with an atomic minimum, so the word
  *    is sticky: it holds the most negative code of every call since the last
@@ -52,7 +53,7 @@ extern "C" {
 
 /* Fit policy.  LOWEST_FIT: lowest gap that fits.  BEST_FIT: tightest finite
  * gap that fits (lowest start among equals), the space above every conflicting
- * tensor only when no finite gap fits -- the "best fit criterion" wording of
+ * tensor only when no finite gap fits -- a reading of the best-fit rule of
  * Section 2.3. */
 #define MP_LOWEST_FIT 0
 #define MP_BEST_FIT 1
@@ -135,7 +136,8 @@ int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* 
  * n_traces; capacity at most n_tensors), MP_OP_PROBE (n_tensors,
  * max_num_ops; the default capacity), MP_OP_BUMP (n_tensors).  The
  * single-trace planner's size depends on the current device (its CU count).
- * Returns 0 for an unknown op or out-of-range sizes. */
+ * Returns 0 for an unknown op or out-of-range sizes (negative, or counts above
+ * 2^40). */
 #define MP_OP_LIVE_BYTES 1
 #define MP_OP_VALIDATE 2
 #define MP_OP_PLAN_TRACE 3

@@ -53,7 +53,8 @@ int32_t mpo_check_trace(const int64_t* size, const int32_t* first, const int32_t
 }
 
 /* ------------------------------------------------------------------------- */
-/* Rank order: "sorting all intermediate allocations by size" (Section 2.3). */
+/* Rank order (Section 2.3): size descending, ties by first op ascending,
+ * then by id ascending. */
 
 typedef struct {
     int64_t size;

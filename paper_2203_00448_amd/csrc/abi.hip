@@ -8,6 +8,11 @@ namespace {
 
 int32_t launched(hipError_t e) { return e == hipSuccess ? MP_OK : MP_EDEVICE; }
 
+// Largest element count (tensors, ops, traces, pair capacity) any size
+// computation takes: far beyond any device, small enough that byte counts
+// of a few dozen bytes per element stay within 64 bits.
+constexpr int64_t kMaxElems = (int64_t)1 << 40;
+
 }  // namespace
 
 extern "C" const char* mp_status_string(int32_t status) {
@@ -37,7 +42,9 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
                                  int64_t* offset_out, int64_t* peak_out, int64_t* lb_out,
                                  void* workspace, size_t workspace_bytes, int32_t* status_out,
                                  void* stream) {
-    if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || !status_out) return MP_EINVAL;
+    if (n_traces < 0 || n_traces > INT32_MAX || n_tensors < 0 || n_tensors > kMaxElems ||
+        !status_out)
+        return MP_EINVAL;
     if (policy != MP_LOWEST_FIT && policy != MP_BEST_FIT) return MP_EINVAL;
     if (!batch_shape(max_trace_len).ok) return MP_EINVAL;
     if (!begin) return MP_EINVAL;
@@ -54,6 +61,7 @@ extern "C" int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const i
 extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_ops,
                                     int64_t capacity) {
     if (n_tensors < 0 || num_ops < 0 || capacity < 0) return 0;
+    if (n_tensors > kMaxElems || num_ops > kMaxElems || capacity > kMaxElems) return 0;
     switch (op) {
         case MP_OP_LIVE_BYTES:
             return num_ops > INT32_MAX ? 0 : live_workspace_bytes((int32_t)num_ops);
@@ -78,8 +86,8 @@ extern "C" size_t mp_workspace_size(int32_t op, int64_t n_tensors, int64_t num_o
 
 extern "C" size_t mp_workspace_bytes(int32_t op, int64_t n_tensors, int64_t max_num_ops,
                                      int64_t n_traces) {
-    if (n_tensors < 0 || max_num_ops < 0 || max_num_ops > INT32_MAX || n_traces < 0 ||
-        n_traces > INT32_MAX)
+    if (n_tensors < 0 || n_tensors > kMaxElems || max_num_ops < 0 || max_num_ops > INT32_MAX ||
+        n_traces < 0 || n_traces > INT32_MAX)
         return 0;
     switch (op) {
         case MP_OP_LIVE_BYTES:
@@ -134,8 +142,8 @@ int32_t validate_common(const int64_t* begin, int64_t n_seg, const int64_t* size
                         int64_t n, int64_t max_seg, int64_t* pairs_out, int64_t capacity,
                         int64_t* n_conflicts_out, int32_t hints, void* workspace,
                         size_t workspace_bytes, int32_t* status_out, void* stream) {
-    if (n < 0 || n > INT32_MAX - 1 || capacity < 0 || !status_out || !n_conflicts_out ||
-        !workspace)
+    if (n < 0 || n > INT32_MAX - 1 || capacity < 0 || capacity > kMaxElems || !status_out ||
+        !n_conflicts_out || !workspace)
         return MP_EINVAL;
     if (n > 0 && (!size || !first || !last || !offset)) return MP_EINVAL;
     if (capacity > 0 && !pairs_out) return MP_EINVAL;

@@ -289,8 +289,9 @@ __global__ void t_rank_keys_kernel(const uint32_t* __restrict__ su,
 __device__ __forceinline__ uint32_t agent_load(const uint32_t* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-// The publish stays an ordinary (cached) relaxed store: a non-temporal store
-// was never seen by pollers on other XCDs.
+// The publish must stay an ordinary (cached) relaxed agent-scope store: a
+// non-temporal store was tried and pollers on other XCDs never saw it, so a
+// run waiting on such a publish does not end.
 __device__ __forceinline__ void agent_store(uint32_t* p, uint32_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }

@@ -1,6 +1,6 @@
 """Parity of the BEST_FIT policy on the GPU with the CPU oracle.
 
-BEST_FIT is the tightest-gap reading of the "best fit criterion" of
+BEST_FIT is the tightest-gap reading of the best-fit rule of
 Section 2.3: among the free gaps left by the already placed, lifetime-
 intersecting tensors, the smallest one that holds the tensor (lowest start
 among equals), the space above all of them only when no gap holds it.
