@@ -65,6 +65,7 @@ def lib():
         L.mpo_optimal_plan.argtypes = [p, p, p, i64, i32, p, p]
         L.mpo_breadth_order.argtypes = [p, p, p, i64, i32, p]
         L.mpo_plan_breadth.argtypes = [p, p, p, i64, i32, i32, p, p]
+        L.mpo_dag_depth.argtypes = [p, p, p, i64, i32, p, p]
         for f in (L.mpo_check_trace, L.mpo_rank_order, L.mpo_plan_trace, L.mpo_plan_trace_w,
                   L.mpo_live_bytes_profile, L.mpo_validate_plan, L.mpo_probe_plan):
             f.restype = i32
@@ -109,6 +110,20 @@ def plan_trace(size, first, last, num_ops: int, policy: int = LOWEST_FIT,
     if st != OK:
         raise OracleError(st, "plan_trace")
     return off, int(peak.value)
+
+
+def dag_depth(size, first, last, num_ops: int):
+    """Levels of greedy_by_size's dependency structure (1 + the largest level
+    among the earlier-ranked tensors a tensor meets) and their maximum, the
+    depth.  Returns (level int32[n], depth)."""
+    s, f, l = _arr(size, np.int64), _arr(first, np.int32), _arr(last, np.int32)
+    level = np.zeros(s.shape[0], np.int32)
+    depth = ctypes.c_int32(0)
+    st = lib().mpo_dag_depth(_ptr(s), _ptr(f), _ptr(l), s.shape[0], int(num_ops), _ptr(level),
+                             ctypes.byref(depth))
+    if st != OK:
+        raise OracleError(st, "dag_depth")
+    return level, int(depth.value)
 
 
 def plan_batch(begin, num_ops, size, first, last, policy: int = LOWEST_FIT):

@@ -579,3 +579,109 @@ int32_t mpo_plan_breadth(const int64_t* size, const int32_t* first, const int32_
     free(order);
     return st;
 }
+
+/* ------------------------------------------------------------------------- */
+/* Depth of the greedy's dependency structure: the longest chain t1, t2, ...
+ * in which each tensor ranks after the previous one and their lifetimes meet
+ * (every tensor depends on the earlier-ranked tensors it meets).  Tensors
+ * are taken in rank order; a tensor's level is one more than the largest
+ * level among the earlier tensors alive at some op of its lifetime, read from
+ * a maximum tree over the (compressed) ops that keeps, per op, the largest
+ * level of the tensors alive there.  Workload characterisation only. */
+
+typedef struct {
+    int32_t* mx;   /* largest level in the node's range */
+    int32_t* lazy; /* a level raised over the node's whole range */
+    int64_t m;
+} max_tree;
+
+static int32_t tree_query(const max_tree* T, int64_t node, int64_t lo, int64_t hi, int64_t a,
+                          int64_t b) {
+    if (b < lo || hi < a) return 0;
+    if (a <= lo && hi <= b) return T->mx[node];
+    const int64_t mid = (lo + hi) / 2;
+    const int32_t l = tree_query(T, 2 * node, lo, mid, a, b);
+    const int32_t r = tree_query(T, 2 * node + 1, mid + 1, hi, a, b);
+    int32_t v = l > r ? l : r;
+    return v > T->lazy[node] ? v : T->lazy[node];
+}
+
+static void tree_raise(max_tree* T, int64_t node, int64_t lo, int64_t hi, int64_t a, int64_t b,
+                       int32_t v) {
+    if (b < lo || hi < a) return;
+    if (a <= lo && hi <= b) {
+        if (v > T->mx[node]) T->mx[node] = v;
+        if (v > T->lazy[node]) T->lazy[node] = v;
+        return;
+    }
+    const int64_t mid = (lo + hi) / 2;
+    tree_raise(T, 2 * node, lo, mid, a, b, v);
+    tree_raise(T, 2 * node + 1, mid + 1, hi, a, b, v);
+    int32_t w = T->mx[2 * node] > T->mx[2 * node + 1] ? T->mx[2 * node] : T->mx[2 * node + 1];
+    if (T->lazy[node] > w) w = T->lazy[node];
+    T->mx[node] = w;
+}
+
+static int cmp_i32(const void* pa, const void* pb) {
+    const int32_t a = *(const int32_t*)pa, b = *(const int32_t*)pb;
+    return a < b ? -1 : (a > b ? 1 : 0);
+}
+
+static int64_t coord(const int32_t* c, int64_t m, int32_t v) { /* index of v in sorted c */
+    int64_t lo = 0, hi = m - 1;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) / 2;
+        if (c[mid] < v) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+int32_t mpo_dag_depth(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
+                      int32_t num_ops, int32_t* level_out, int32_t* depth_out) {
+    const int32_t st = check_trace(size, first, last, n, num_ops, 0);
+    if (st != MPO_OK || !depth_out) return st != MPO_OK ? st : MPO_EINVAL;
+    *depth_out = 0;
+    if (n == 0) return MPO_OK;
+    int32_t* order = (int32_t*)malloc((size_t)n * sizeof(int32_t));
+    int32_t* c = (int32_t*)malloc((size_t)(2 * n) * sizeof(int32_t));
+    if (!order || !c) {
+        free(order);
+        free(c);
+        return MPO_EINVAL;
+    }
+    mpo_rank_order(size, first, n, order);
+    for (int64_t i = 0; i < n; ++i) {
+        c[2 * i] = first[i];
+        c[2 * i + 1] = last[i];
+    }
+    qsort(c, (size_t)(2 * n), sizeof(int32_t), cmp_i32);
+    int64_t m = 0;
+    for (int64_t i = 0; i < 2 * n; ++i)
+        if (m == 0 || c[i] != c[m - 1]) c[m++] = c[i];
+    max_tree T = {(int32_t*)calloc((size_t)(4 * m), sizeof(int32_t)),
+                  (int32_t*)calloc((size_t)(4 * m), sizeof(int32_t)), m};
+    if (!T.mx || !T.lazy) {
+        free(order);
+        free(c);
+        free(T.mx);
+        free(T.lazy);
+        return MPO_EINVAL;
+    }
+    int32_t depth = 0;
+    for (int64_t k = 0; k < n; ++k) {
+        const int32_t t = order[k];
+        const int64_t a = coord(c, m, first[t]), b = coord(c, m, last[t]);
+        const int32_t lv = tree_query(&T, 1, 0, m - 1, a, b) + 1;
+        tree_raise(&T, 1, 0, m - 1, a, b, lv);
+        if (level_out) level_out[t] = lv;
+        if (lv > depth) depth = lv;
+    }
+    *depth_out = depth;
+    free(order);
+    free(c);
+    free(T.mx);
+    free(T.lazy);
+    return MPO_OK;
+}
+

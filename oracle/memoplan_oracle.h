@@ -111,6 +111,13 @@ int32_t mpo_plan_breadth(const int64_t* size, const int32_t* first, const int32_
                          int64_t n, int32_t num_ops, int32_t policy, int64_t* offset_out,
                          int64_t* peak_out);
 
+/* Depth of greedy_by_size's dependency structure (workload characterisation,
+ * not a planning result): level[t] = 1 + the largest level among the
+ * earlier-ranked tensors whose lifetimes meet t's (1 when there are none);
+ * *depth_out = the largest level, 0 for n == 0.  level_out may be NULL. */
+int32_t mpo_dag_depth(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
+                      int32_t num_ops, int32_t* level_out, int32_t* depth_out);
+
 #ifdef __cplusplus
 }
 #endif

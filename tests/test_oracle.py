@@ -511,3 +511,34 @@ def test_breadth_at_least_optimum():
         size, first, last, T = _random_tiny(rng, n)
         opt = oracle.optimal_plan(size, first, last, T)[1]
         assert oracle.plan_breadth(size, first, last, T)[1] >= opt
+
+
+def _longest_chain_bruteforce(size, first, last):
+    """Longest path of the dependency DAG built pair by pair: t depends on every
+    earlier-ranked tensor (size desc, first asc, id asc) whose lifetime meets
+    its own; levels by dynamic programming over that order."""
+    n = len(size)
+    order = sorted(range(n), key=lambda i: (-int(size[i]), int(first[i]), i))
+    level = [0] * n
+    for k, t in enumerate(order):
+        level[t] = 1 + max([level[p] for p in order[:k] if conflict(first, last, p, t)],
+                           default=0)
+    return level, max(level, default=0)
+
+
+def test_dag_depth_hand_and_bruteforce():
+    # E5: the chain id2 -> id3 -> id4 -> id1 of its walk-through
+    level, depth = oracle.dag_depth([256, 64, 256, 192, 128], [3, 1, 0, 0, 2], [3, 2, 1, 2, 3], 4)
+    assert level.tolist() == [1, 4, 1, 2, 3] and depth == 4
+    # pairwise-disjoint lifetimes: no dependency; fully overlapping: one chain
+    assert oracle.dag_depth([64] * 5, [0, 1, 2, 3, 4], [0, 1, 2, 3, 4], 5)[1] == 1
+    assert oracle.dag_depth([64, 128, 192, 256], [0] * 4, [3] * 4, 4)[1] == 4
+    rng = np.random.default_rng(130)
+    for _ in range(60):
+        n = int(rng.integers(0, 40))
+        T = int(rng.integers(1, 30))
+        t = tg.random_trace(rng, n, T, max_len=int(rng.integers(1, 10)),
+                            sizes=[64, 128, 192] if n % 3 == 0 else None)
+        level, depth = oracle.dag_depth(t.size, t.first, t.last, t.num_ops)
+        blevel, bdepth = _longest_chain_bruteforce(t.size, t.first, t.last)
+        assert level.tolist() == blevel and depth == bdepth
