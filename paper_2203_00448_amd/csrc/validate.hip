@@ -6,8 +6,13 @@
 // are taken in position order (segment, first, id); for positions q < j of
 // one segment the lifetimes meet iff first[j] <= last[q], so row q's
 // candidates are the contiguous positions (q, reach[q]).  Short rows are
-// handled by one thread each, long rows by one workgroup each; a count pass,
-// a device-wide scan and a write pass put the pairs in (i, j) order.  When
+// handled by one thread each.  Long rows are sorted by band length (one
+// class per power of two, stable, so ascending rows inside a class) and cut
+// into chunks of 64; the count pass tests a chunk
+// against tiles of 1024 candidates staged in registers, so the long bands of a
+// chunk share every load.  A device-wide scan of the row counts then gives
+// each row its start, and the write pass visits only rows that have pairs,
+// one workgroup per row in j order.  When
 // the input is not already sorted by first inside each segment, positions
 // come from a radix sort and the written pairs are radix-sorted at the end.
 #include "internal.hpp"
@@ -18,15 +23,20 @@ namespace mp {
 namespace {
 
 constexpr int kVBlock = 256;
-constexpr int32_t kShortRow = 64;  // longer rows go to the workgroup-per-row kernels
+constexpr int32_t kShortRow = 64;  // longer rows go to the chunked kernels
 constexpr unsigned kLongGrid = 1024;
+constexpr int kChunkRows = 64;                      // long rows per chunk (one per lane)
+constexpr int kTileItems = 4;                       // candidates per thread per tile
+constexpr int64_t kTileJ = kVBlock * kTileItems;    // candidates per tile
+constexpr unsigned kTileGrid = 2048;
+constexpr int kWriteUnroll = 8;                     // candidate loads in flight per lane (write pass)
 
 // Workspace words.
 struct VFlags {
     uint32_t unsorted;  // some segment is not sorted by first
     uint32_t sorted;    // == !unsorted (lets sort-path kernels skip themselves)
     uint32_t n_long;    // rows longer than kShortRow
-    uint32_t pad;
+    uint32_t wide;      // some offset + size is 2^32 or more
     int64_t begin1[2];  // {0, n} when the caller gives a single trace
 };
 
@@ -51,8 +61,28 @@ __global__ void v_init_kernel(VFlags* fl, int64_t n) {
     fl->unsorted = 0;
     fl->sorted = 1;
     fl->n_long = 0;
+    fl->wide = 0;
     fl->begin1[0] = 0;
     fl->begin1[1] = n;
+}
+
+// Single trace: every tensor's segment ends at n.
+__global__ void v_segend_one_kernel(int64_t n, int32_t* __restrict__ segend) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        segend[i] = (int32_t)n;
+}
+
+// Lanes below this one whose bit is set in m.
+__device__ __forceinline__ uint32_t lanes_below(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Sort key of a row: floor(log2(band)) for long rows (band > kShortRow, so
+// at least 6), 0 for short ones.
+__device__ __forceinline__ uint64_t row_class(int64_t band) {
+    return band > kShortRow ? (uint64_t)(63 - __clzll(band)) : 0;
 }
 
 // Segment end of every tensor, and checks of the segment table.
@@ -74,14 +104,16 @@ __global__ __launch_bounds__(kVBlock) void v_check_kernel(
     const int32_t* __restrict__ segend, VFlags* fl, int32_t* __restrict__ status,
     int assume_sorted) {
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    bool bad = false, unsorted = false;
+    bool bad = false, unsorted = false, wide = false;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
         const int64_t s = size[i], o = off[i];
         const int32_t f = first[i], l = last[i];
         if (s <= 0 || f < 0 || f > l || o < 0 || o > INT64_MAX - s) bad = true;
+        else if (o + s > (int64_t)UINT32_MAX) wide = true;
         if (i + 1 < n && i + 1 < segend[i] && first[i + 1] < f) unsorted = true;
     }
     if (__ballot(bad) && (threadIdx.x & (kWave - 1)) == 0) raise_status(status, MP_EINVAL);
+    if (__ballot(wide) && (threadIdx.x & (kWave - 1)) == 0) atomicOr(&fl->wide, 1u);
     if (__ballot(unsorted) && (threadIdx.x & (kWave - 1)) == 0) {
         if (assume_sorted) {  // broken promise: report, stay on the sorted path
             raise_status(status, MP_EINVAL);
@@ -156,15 +188,17 @@ __device__ __forceinline__ void put_pair(int64_t* pairs, int64_t pos, int64_t ca
     pairs[2 * pos + 1] = y;
 }
 
-// Pass over short rows (one thread per row); long rows are queued.
-//   write == 0: cnt[q] = conflicts of row q, reach[q] stored
+// Pass over short rows (one thread per row).
+//   write == 0: cnt[q] = conflicts of row q (0 for long rows), reach[q]
+//               stored, (class, q) written as a sort key and value, long rows
+//               counted
 //   write == 1: pairs of row q written from cnt[q] (now its start)
 __global__ __launch_bounds__(kVBlock) void v_rows_kernel(
     const int32_t* first, const int32_t* last, const int64_t* off, const int64_t* size,
     const int32_t* pf, const int32_t* pl, const int64_t* po, const int64_t* ps,
     const uint32_t* pid, const int32_t* __restrict__ segend, int64_t n, int32_t* __restrict__ reach,
-    int64_t* __restrict__ cnt, int32_t* __restrict__ long_rows, VFlags* fl, int write,
-    int64_t* __restrict__ pairs, int64_t cap) {
+    int64_t* __restrict__ cnt, uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
+    VFlags* fl, int write, int64_t* __restrict__ pairs, int64_t cap) {
     const VArrays a = pick_arrays(fl, first, last, off, size, pf, pl, po, ps, pid);
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
@@ -179,11 +213,16 @@ __global__ __launch_bounds__(kVBlock) void v_rows_kernel(
             r = reach[q];
         }
         const int64_t band = (int64_t)r - q - 1;
-        if (band > kShortRow) {
-            if (!write) {
-                cnt[q] = 0;
-                long_rows[atomicAdd(&fl->n_long, 1u)] = (int32_t)q;
-            }
+        const bool is_long = band > kShortRow;
+        if (!write) {
+            keys[q] = row_class(band);
+            vals[q] = (uint32_t)q;
+            const uint64_t m = __ballot(is_long);
+            if (m && (int)(threadIdx.x & (kWave - 1)) == __ffsll((unsigned long long)__ballot(1)) - 1)
+                atomicAdd(&fl->n_long, (uint32_t)__popcll(m));
+        }
+        if (is_long) {
+            if (!write) cnt[q] = 0;
             continue;
         }
         if (write && (cnt[q + 1] == cnt[q] || cnt[q] >= cap)) continue;  // nothing to write
@@ -199,31 +238,272 @@ __global__ __launch_bounds__(kVBlock) void v_rows_kernel(
     }
 }
 
-// Long rows: one workgroup per row, candidates taken 256 at a time so that
-// the writes keep j order (exclusive scan of the hits of each round).
-__global__ __launch_bounds__(kVBlock) void v_long_kernel(
+// The long rows in class order are the last n_long values of the class sort.
+__device__ __forceinline__ const uint32_t* long_rows_of(const uint32_t* sorted, int64_t n,
+                                                        const VFlags* fl) {
+    return sorted + (n - (int64_t)fl->n_long);
+}
+
+// Candidate range of every chunk of kChunkRows long rows (one wave per
+// chunk): lo = smallest row + 1, tiles = ceil((largest reach - lo) / kTileJ).
+__global__ __launch_bounds__(kVBlock) void v_chunk_kernel(const uint32_t* __restrict__ sorted,
+                                                          int64_t n,
+                                                          const int32_t* __restrict__ reach,
+                                                          const VFlags* fl, int64_t n_chunk_max,
+                                                          int32_t* __restrict__ chunk_lo,
+                                                          int64_t* __restrict__ chunk_tiles) {
+    const int64_t c = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) / kWave;
+    if (c >= n_chunk_max) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t n_long = fl->n_long;
+    const uint32_t* long_rows = long_rows_of(sorted, n, fl);
+    const int64_t k = c * kChunkRows + lane;
+    int32_t q = INT32_MAX, r = 0;
+    if (k < n_long) {
+        q = (int32_t)long_rows[k];
+        r = reach[q];
+    }
+    const int32_t qmin = wave_reduce(q, OpMin<int32_t>());
+    const int32_t rmax = wave_reduce(r, OpMax<int32_t>());
+    if (lane == 0) {
+        const bool any = c * kChunkRows < n_long;
+        chunk_lo[c] = any ? qmin + 1 : 0;
+        chunk_tiles[c] = any ? ((int64_t)rmax - (qmin + 1) + kTileJ - 1) / kTileJ : 0;
+    }
+}
+
+__device__ __forceinline__ int64_t readlane64(int64_t v, int k) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, k);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)((uint64_t)v >> 32), k);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ uint32_t readlane64(uint32_t v, int k) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, k);
+}
+
+// Byte ranges as T: int64_t, or uint32_t when every end is below 2^32.
+template <typename T>
+struct TileRows {
+    int32_t q = INT32_MAX, r = 0;  // this lane's row of the chunk and its reach
+    T o = 0, e = 0;                // and its byte range [o, e)
+};
+
+// One tile for one wave: kTileItems candidates per lane at j0 + i * 256 + tid
+// against the rows of the chunk whose bands meet the tile (a ballot over the
+// lanes that hold the rows; sentinel lanes have r = 0).  Row values are
+// broadcast with readlane.  A row of a valid plan has no hits, so the test
+// only ORs the hit masks; a row with hits is counted again exactly and one
+// lane adds the count to cnt[q].
+template <typename T>
+__device__ __forceinline__ void tile_rows(const TileRows<T>& R, int64_t j0, int64_t n,
+                                          const VArrays& a, int64_t* __restrict__ cnt) {
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    T jo[kTileItems], je[kTileItems];
+    int32_t jj[kTileItems];
+#pragma unroll
+    for (int i = 0; i < kTileItems; ++i) {
+        const int64_t j = j0 + i * kVBlock + tid;
+        jj[i] = j < n ? (int32_t)j : INT32_MAX;  // past n: outside every band
+        jo[i] = 0;
+        je[i] = 0;
+        if (j < n) {
+            const int64_t o = a.off[j];
+            jo[i] = (T)o;
+            je[i] = (T)(o + a.size[j]);
+        }
+    }
+    // tile [jlo, jhi) in int32 (jhi clamped; positions are below 2^31 - 1)
+    const int32_t jlo = (int32_t)j0;
+    const int32_t jhi = (int32_t)(j0 + kTileJ < INT32_MAX ? j0 + kTileJ : INT32_MAX);
+    uint64_t act = __builtin_amdgcn_ballot_w64(R.r > jlo && R.q < jhi - 1);
+    const uint64_t cover = __builtin_amdgcn_ballot_w64(R.q < jlo && R.r >= jhi);
+    while (act) {
+        const int k = (int)__builtin_ctzll(act);
+        act &= act - 1;
+        const T o = readlane64(R.o, k), e = readlane64(R.e, k);
+        uint64_t any = 0;
+        if ((cover >> k) & 1) {  // the band covers the tile (all of it below n)
+#pragma unroll
+            for (int i = 0; i < kTileItems; ++i)
+                any |= __builtin_amdgcn_ballot_w64(o < je[i]) &
+                       __builtin_amdgcn_ballot_w64(jo[i] < e);
+        } else {
+            const int32_t q = __builtin_amdgcn_readlane(R.q, k);
+            const int32_t r = __builtin_amdgcn_readlane(R.r, k);
+#pragma unroll
+            for (int i = 0; i < kTileItems; ++i)
+                any |= __builtin_amdgcn_ballot_w64(jj[i] > q) &
+                       __builtin_amdgcn_ballot_w64(jj[i] < r) &
+                       __builtin_amdgcn_ballot_w64(o < je[i]) &
+                       __builtin_amdgcn_ballot_w64(jo[i] < e);
+        }
+        if (any) {
+            const int32_t q = __builtin_amdgcn_readlane(R.q, k);
+            const int32_t r = __builtin_amdgcn_readlane(R.r, k);
+            uint32_t hits = 0;
+#pragma unroll
+            for (int i = 0; i < kTileItems; ++i)
+                hits += (uint32_t)__popcll(__builtin_amdgcn_ballot_w64(
+                    jj[i] > q && jj[i] < r && o < je[i] && jo[i] < e));
+            if (lane == 0)
+                atomicAdd(reinterpret_cast<unsigned long long*>(&cnt[q]),
+                          (unsigned long long)hits);
+        }
+    }
+}
+
+// Count pass of the long rows.  tile_end is the inclusive prefix of the
+// chunks' tile counts; the tiles are dealt to the workgroups in contiguous
+// ranges.  Every wave works alone: it holds the chunk's rows one per lane
+// and kTileItems candidates per lane of each tile.
+template <typename T>
+__device__ __forceinline__ void tile_pass(const VArrays& a, const int32_t* __restrict__ reach,
+                                          const uint32_t* long_rows, int64_t n_long,
+                                          const int32_t* __restrict__ chunk_lo,
+                                          const int64_t* __restrict__ tile_end, int64_t n,
+                                          int64_t c, int64_t t0, int64_t t1,
+                                          int64_t* __restrict__ cnt) {
+    const int lane = threadIdx.x & (kWave - 1);
+    TileRows<T> R;
+    int64_t loaded = -1;
+    for (int64_t t = t0; t < t1; ++t) {
+        while (tile_end[c] <= t) ++c;
+        if (c != loaded) {
+            R = TileRows<T>{};
+            const int64_t k = c * kChunkRows + lane;
+            if (k < n_long) {
+                R.q = (int32_t)long_rows[k];
+                R.r = reach[R.q];
+                const int64_t o = a.off[R.q];
+                R.o = (T)o;
+                R.e = (T)(o + a.size[R.q]);
+            }
+            loaded = c;
+        }
+        tile_rows<T>(R, chunk_lo[c] + (t - (c ? tile_end[c - 1] : 0)) * kTileJ, n, a, cnt);
+    }
+}
+
+__global__ __launch_bounds__(kVBlock) void v_tile_kernel(
     const int32_t* first, const int32_t* last, const int64_t* off, const int64_t* size,
     const int32_t* pf, const int32_t* pl, const int64_t* po, const int64_t* ps,
-    const uint32_t* pid, const int32_t* __restrict__ reach, int64_t* __restrict__ cnt,
-    const int32_t* __restrict__ long_rows, VFlags* fl, int write, int64_t* __restrict__ pairs,
-    int64_t cap) {
-    __shared__ uint32_t scratch[kVBlock / kWave];
+    const uint32_t* pid, const int32_t* __restrict__ reach, const uint32_t* __restrict__ sorted,
+    const int32_t* __restrict__ chunk_lo, const int64_t* __restrict__ tile_end, int64_t n,
+    const VFlags* fl, int64_t* __restrict__ cnt) {
+    __shared__ int64_t s_chunk;
     const VArrays a = pick_arrays(fl, first, last, off, size, pf, pl, po, ps, pid);
-    const uint32_t n_long = fl->n_long;
-    for (uint32_t k = blockIdx.x; k < n_long; k += gridDim.x) {
-        const int64_t q = long_rows[k];
-        const int64_t r = reach[q];
-        const int64_t oq = a.off[q], sq = a.size[q];
-        int64_t pos = write ? cnt[q] : 0;
-        for (int64_t j0 = q + 1; j0 < r; j0 += kVBlock) {
-            const int64_t j = j0 + threadIdx.x;
-            const bool hit = j < r && bytes_meet(oq, sq, a.off[j], a.size[j]);
-            uint32_t total;
-            const uint32_t before = block_exclusive_sum<kVBlock>(hit ? 1u : 0u, &total, scratch);
-            if (write && hit) put_pair(pairs, pos + before, cap, a, q, j);
-            pos += total;
+    const int64_t n_long = fl->n_long;
+    const uint32_t* long_rows = long_rows_of(sorted, n, fl);
+    const int64_t n_chunks = (n_long + kChunkRows - 1) / kChunkRows;
+    if (n_chunks == 0) return;
+    const int64_t total = tile_end[n_chunks - 1];
+    const int64_t t0 = total * blockIdx.x / gridDim.x, t1 = total * (blockIdx.x + 1) / gridDim.x;
+    if (t0 >= t1) return;
+    const int lane = threadIdx.x & (kWave - 1);
+    if (threadIdx.x < kWave) {
+        // first chunk whose tiles end after t0: 64-way search (tile_end[n_chunks-1] > t0)
+        int64_t lo = 0, hi = n_chunks;
+        while (hi - lo > 1) {
+            const int64_t step = (hi - lo + kWave - 1) / kWave;
+            const int64_t idx = lo + (lane + 1) * step - 1;
+            const bool past = idx >= hi - 1 || tile_end[idx] > t0;
+            const int f = __ffsll((unsigned long long)__ballot(past)) - 1;
+            const int64_t nlo = lo + f * step;
+            hi = nlo + step < hi ? nlo + step : hi;
+            lo = nlo;
         }
-        if (!write && threadIdx.x == 0) cnt[q] = pos;
+        if (lane == 0) s_chunk = lo;
+    }
+    __syncthreads();
+    if (fl->wide)
+        tile_pass<int64_t>(a, reach, long_rows, n_long, chunk_lo, tile_end, n, s_chunk, t0, t1, cnt);
+    else
+        tile_pass<uint32_t>(a, reach, long_rows, n_long, chunk_lo, tile_end, n, s_chunk, t0, t1,
+                            cnt);
+}
+
+// Write pass of the long rows that have pairs.  The workgroup checks 256 of
+// its long rows at once (rows b, b + G, b + 2G, ... for workgroup b of G, so
+// that neighbours in class order, often alike, land in different
+// workgroups) and lists those with pairs; then each listed row is
+// written by the whole workgroup: each wave takes a contiguous quarter of the
+// band, counts its hits, and after an exchange of the four counts writes them
+// in j order.  Rows write disjoint ranges, so the list order is free.
+__global__ __launch_bounds__(kVBlock) void v_long_write_kernel(
+    const int32_t* first, const int32_t* last, const int64_t* off, const int64_t* size,
+    const int32_t* pf, const int32_t* pl, const int64_t* po, const int64_t* ps,
+    const uint32_t* pid, const int32_t* __restrict__ reach, const int64_t* __restrict__ cnt,
+    const uint32_t* __restrict__ sorted, int64_t n, const VFlags* fl,
+    int64_t* __restrict__ pairs, int64_t cap) {
+    constexpr int kWaves = kVBlock / kWave;
+    __shared__ uint32_t wcnt[2][kWaves];
+    __shared__ int32_t list[kVBlock];
+    __shared__ uint32_t n_list;
+    const VArrays a = pick_arrays(fl, first, last, off, size, pf, pl, po, ps, pid);
+    const int64_t n_long = fl->n_long;
+    const uint32_t* long_rows = long_rows_of(sorted, n, fl);
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wid = tid / kWave;
+    int buf = 0;
+    const int64_t G = gridDim.x;
+    for (int64_t base = blockIdx.x; base < n_long; base += G * kVBlock) {
+        if (tid == 0) n_list = 0;
+        __syncthreads();
+        const int64_t k = base + tid * G;
+        if (k < n_long) {
+            const int32_t q = (int32_t)long_rows[k];
+            const int64_t start = cnt[q];
+            if (start != cnt[q + 1] && start < cap) list[atomicAdd(&n_list, 1u)] = q;
+        }
+        __syncthreads();
+        const uint32_t listed = n_list;
+        for (uint32_t li = 0; li < listed; ++li) {
+            const int64_t q = list[li];
+            const int64_t start = cnt[q];
+            const int64_t r = reach[q];
+            const int64_t oq = a.off[q], sq = a.size[q];
+            const int64_t seg = ((r - q - 1 + kWaves * kWave - 1) / (kWaves * kWave)) * kWave;
+            const int64_t s0 = q + 1 + wid * seg;
+            const int64_t s1 = s0 + seg < r ? s0 + seg : r;
+            uint32_t mine = 0;
+            for (int64_t j0 = s0; j0 < s1; j0 += kWave * kWriteUnroll) {
+                int64_t jo[kWriteUnroll], js[kWriteUnroll];  // all loads first, then the tests
+#pragma unroll
+                for (int u = 0; u < kWriteUnroll; ++u) {
+                    const int64_t j = j0 + u * kWave + lane;
+                    jo[u] = j < s1 ? a.off[j] : 0;
+                    js[u] = j < s1 ? a.size[j] : 0;
+                }
+#pragma unroll
+                for (int u = 0; u < kWriteUnroll; ++u) {
+                    const int64_t j = j0 + u * kWave + lane;
+                    mine += (uint32_t)__popcll(__ballot(j < s1 && bytes_meet(oq, sq, jo[u], js[u])));
+                }
+            }
+            if (lane == 0) wcnt[buf][wid] = mine;
+            __syncthreads();
+            int64_t pos = start;
+            for (int w = 0; w < wid; ++w) pos += wcnt[buf][w];
+            buf ^= 1;  // the next row's exchange uses the other buffer
+            for (int64_t j0 = s0; mine > 0 && j0 < s1; j0 += kWave * kWriteUnroll) {
+                int64_t jo[kWriteUnroll], js[kWriteUnroll];
+#pragma unroll
+                for (int u = 0; u < kWriteUnroll; ++u) {
+                    const int64_t j = j0 + u * kWave + lane;
+                    jo[u] = j < s1 ? a.off[j] : 0;
+                    js[u] = j < s1 ? a.size[j] : 0;
+                }
+#pragma unroll
+                for (int u = 0; u < kWriteUnroll; ++u) {
+                    const int64_t j = j0 + u * kWave + lane;
+                    const bool h = j < s1 && bytes_meet(oq, sq, jo[u], js[u]);
+                    const uint64_t m = __ballot(h);
+                    if (h) put_pair(pairs, pos + lanes_below(m), cap, a, q, j);
+                    pos += __popcll(m);
+                    mine -= (uint32_t)__popcll(m);
+                }
+            }
+        }
+        __syncthreads();  // the list and n_list are rewritten for the next rows
     }
 }
 
@@ -236,24 +516,28 @@ __global__ void v_total_kernel(const int64_t* __restrict__ partial, int64_t tile
     if (total > cap) raise_status(status, MP_ENOSPC);
 }
 
-// Unsorted inputs: pack the written pairs into sort keys (unused slots last).
+// Unsorted inputs: pack the written pairs into sort keys (i << nbits | j,
+// ids below 2^nbits; unused slots all ones, so they sort last).
 __global__ void v_pack_kernel(const int64_t* __restrict__ pairs, const int64_t* __restrict__ n_out,
-                              int64_t cap, uint64_t* __restrict__ keys, const VFlags* fl) {
+                              int64_t cap, int nbits, uint64_t* __restrict__ keys,
+                              const VFlags* fl) {
     if (!fl->unsorted) return;
     const int64_t m = *n_out < cap ? *n_out : cap;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < cap; k += stride)
-        keys[k] = k < m ? (((uint64_t)pairs[2 * k] << 32) | (uint64_t)pairs[2 * k + 1]) : ~0ull;
+        keys[k] = k < m ? (((uint64_t)pairs[2 * k] << nbits) | (uint64_t)pairs[2 * k + 1]) : ~0ull;
 }
 
 __global__ void v_unpack_kernel(const uint64_t* __restrict__ keys, const int64_t* __restrict__ n_out,
-                                int64_t cap, int64_t* __restrict__ pairs, const VFlags* fl) {
+                                int64_t cap, int nbits, int64_t* __restrict__ pairs,
+                                const VFlags* fl) {
     if (!fl->unsorted) return;
     const int64_t m = *n_out < cap ? *n_out : cap;
+    const uint64_t low = ((uint64_t)1 << nbits) - 1;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < m; k += stride) {
-        pairs[2 * k] = (int64_t)(keys[k] >> 32);
-        pairs[2 * k + 1] = (int64_t)(keys[k] & 0xFFFFFFFFu);
+        pairs[2 * k] = (int64_t)(keys[k] >> nbits);
+        pairs[2 * k + 1] = (int64_t)(keys[k] & low);
     }
 }
 
@@ -510,7 +794,7 @@ hipError_t launch_vb_any(int write, int items, const int64_t* begin, int64_t n_s
 }
 
 struct VLayout {
-    size_t flags, segend, reach, cnt, long_rows, keys0, vals0, keys1, vals1, pf, pl, po, ps, pid,
+    size_t flags, segend, reach, cnt, chunk_lo, chunk_tiles, keys0, vals0, keys1, vals1, pf, pl, po, ps, pid,
         pk0, pk1, radix, total;
 };
 
@@ -528,7 +812,9 @@ VLayout v_layout(int64_t n, int64_t cap, int64_t n_seg = 1) {
     L.reach = take(nn * 4);
     const int64_t nc = nn > n_seg ? nn : n_seg;  // also the per-trace counts of a batch
     L.cnt = take((nc + 1) * 8 + scan_workspace_bytes(nc + 1));
-    L.long_rows = take(nn * 4);
+    const int64_t ncm = (nn + kChunkRows - 1) / kChunkRows;
+    L.chunk_lo = take(ncm * 4);
+    L.chunk_tiles = take(ncm * 8 + scan_workspace_bytes(ncm));
     L.keys0 = take(nn * 8);
     L.vals0 = take(nn * 4);
     L.keys1 = take(nn * 8);
@@ -586,7 +872,10 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
     int32_t* reach = reinterpret_cast<int32_t*>(w + L.reach);
     int64_t* cnt = reinterpret_cast<int64_t*>(w + L.cnt);
     int64_t* cnt_partial = cnt + (n + 1);
-    int32_t* long_rows = reinterpret_cast<int32_t*>(w + L.long_rows);
+    const int64_t n_chunk_max = (n + kChunkRows - 1) / kChunkRows;
+    int32_t* chunk_lo = reinterpret_cast<int32_t*>(w + L.chunk_lo);
+    int64_t* chunk_tiles = reinterpret_cast<int64_t*>(w + L.chunk_tiles);
+    int64_t* chunk_partial = chunk_tiles + n_chunk_max;
     uint64_t* keys0 = reinterpret_cast<uint64_t*>(w + L.keys0);
     uint32_t* vals0 = reinterpret_cast<uint32_t*>(w + L.vals0);
     uint64_t* keys1 = reinterpret_cast<uint64_t*>(w + L.keys1);
@@ -606,11 +895,16 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
                            (int64_t)0, cap, n_out, status, (int64_t*)nullptr);
         return hipGetLastError();
     }
+    int nbits = 1;  // ids, positions and segment ends are below 2^nbits
+    while (nbits < 31 && ((int64_t)1 << nbits) <= n) ++nbits;
     const int64_t* seg = begin ? begin : fl->begin1;
     const int64_t nseg = begin ? n_seg : 1;
-    hipLaunchKernelGGL(v_segend_kernel, dim3(grid_for(nseg, 1, 65535)), dim3(256), 0, st, seg, nseg,
-                       n, segend, status);
     const unsigned g = grid_for(n, kVBlock, 4096);
+    if (begin)
+        hipLaunchKernelGGL(v_segend_kernel, dim3(grid_for(nseg, 1, 65535)), dim3(256), 0, st, seg,
+                           nseg, n, segend, status);
+    else
+        hipLaunchKernelGGL(v_segend_one_kernel, dim3(g), dim3(kVBlock), 0, st, n, segend);
     hipLaunchKernelGGL(v_check_kernel, dim3(g), dim3(kVBlock), 0, st, size, first, last, off, n,
                        (const int32_t*)segend, fl, status, assume_sorted ? 1 : 0);
     hipError_t e = hipSuccess;
@@ -618,10 +912,10 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
     // position order for unsorted inputs (every kernel below skips itself otherwise)
     hipLaunchKernelGGL(v_keys_kernel, dim3(g), dim3(kVBlock), 0, st, first, (const int32_t*)segend,
                        n, keys0, vals0, (const VFlags*)fl);
-    int nbits = 1;
-    while (nbits < 31 && ((int64_t)1 << nbits) <= n) ++nbits;
+    // a single trace sorts by first alone (bits 0..30); a batch by (segment end, first)
     bool alt = false;
-    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32 + nbits, rws, &alt, st, &fl->sorted);
+    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, begin ? 32 + nbits : 31, rws, &alt, st,
+                         &fl->sorted);
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(v_gather_kernel, dim3(g), dim3(kVBlock), 0, st,
                        (const uint32_t*)(alt ? vals1 : vals0), size, first, last, off, n, pf, pl,
@@ -631,11 +925,22 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
     hipLaunchKernelGGL(v_rows_kernel, dim3(g), dim3(kVBlock), 0, st, first, last, off, size,
                        (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
                        (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)segend, n, reach,
-                       cnt, long_rows, fl, 0, pairs, cap);
-    hipLaunchKernelGGL(v_long_kernel, dim3(kLongGrid), dim3(kVBlock), 0, st, first, last, off, size,
+                       cnt, keys0, vals0, fl, 0, pairs, cap);
+    // long rows in class order: one stable pass over the class byte
+    bool calt = false;
+    e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 8, rws, &calt, st);
+    if (e != hipSuccess) return e;
+    const uint32_t* sorted = calt ? vals1 : vals0;
+    hipLaunchKernelGGL(v_chunk_kernel, dim3(grid_for(n_chunk_max, kVBlock / kWave, INT32_MAX)),
+                       dim3(kVBlock), 0, st, sorted, n, (const int32_t*)reach, (const VFlags*)fl,
+                       n_chunk_max, chunk_lo, chunk_tiles);
+    e = device_scan_i64(chunk_tiles, n_chunk_max, true, chunk_partial, nullptr, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(v_tile_kernel, dim3(kTileGrid), dim3(kVBlock), 0, st, first, last, off, size,
                        (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
-                       (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach, cnt,
-                       (const int32_t*)long_rows, fl, 0, pairs, cap);
+                       (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach, sorted,
+                       (const int32_t*)chunk_lo,
+                       (const int64_t*)chunk_tiles, n, (const VFlags*)fl, cnt);
     e = device_scan_i64(cnt, n, false, cnt_partial, nullptr, st);
     if (e != hipSuccess) return e;
     const int64_t tiles = (int64_t)(scan_workspace_bytes(n) / sizeof(int64_t)) - 1;
@@ -645,22 +950,24 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
         hipLaunchKernelGGL(v_rows_kernel, dim3(g), dim3(kVBlock), 0, st, first, last, off, size,
                            (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
                            (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)segend, n,
-                           reach, cnt, long_rows, fl, 1, pairs, cap);
-        hipLaunchKernelGGL(v_long_kernel, dim3(kLongGrid), dim3(kVBlock), 0, st, first, last, off,
-                           size, (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
-                           (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach, cnt,
-                           (const int32_t*)long_rows, fl, 1, pairs, cap);
+                           reach, cnt, keys0, vals0, fl, 1, pairs, cap);
+        hipLaunchKernelGGL(v_long_write_kernel, dim3(kLongGrid), dim3(kVBlock), 0, st, first,
+                           last, off, size, (const int32_t*)pf, (const int32_t*)pl,
+                           (const int64_t*)po, (const int64_t*)ps, (const uint32_t*)pid,
+                           (const int32_t*)reach, (const int64_t*)cnt, sorted, n,
+                           (const VFlags*)fl, pairs, cap);
         // unsorted inputs: pairs were written in position order; sort them by (i, j)
         if (assume_sorted) return hipGetLastError();
         const unsigned gc = grid_for(cap, kVBlock, 4096);
         hipLaunchKernelGGL(v_pack_kernel, dim3(gc), dim3(kVBlock), 0, st, (const int64_t*)pairs,
-                           (const int64_t*)n_out, cap, pk0, (const VFlags*)fl);
+                           (const int64_t*)n_out, cap, nbits, pk0, (const VFlags*)fl);
         bool palt = false;
-        e = radix_sort_pairs(pk0, nullptr, pk1, nullptr, cap, 0, 64, rws, &palt, st, &fl->sorted);
+        e = radix_sort_pairs(pk0, nullptr, pk1, nullptr, cap, 0, 2 * nbits, rws, &palt, st,
+                             &fl->sorted);
         if (e != hipSuccess) return e;
         hipLaunchKernelGGL(v_unpack_kernel, dim3(gc), dim3(kVBlock), 0, st,
-                           (const uint64_t*)(palt ? pk1 : pk0), (const int64_t*)n_out, cap, pairs,
-                           (const VFlags*)fl);
+                           (const uint64_t*)(palt ? pk1 : pk0), (const int64_t*)n_out, cap, nbits,
+                           pairs, (const VFlags*)fl);
     }
     return hipGetLastError();
 }
