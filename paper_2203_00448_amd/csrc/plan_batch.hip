@@ -800,6 +800,17 @@ __host__ __device__ inline BatchLds batch_lds(size_t N, size_t cap) {
     return L;
 }
 
+// The k-th item of this thread, tid + k * BLOCK, computed where it is used:
+// the thread index goes through an empty asm so that the compiler cannot
+// keep the items of one phase alive into the next (it spilled them to
+// scratch memory rather than recompute them with one addition).
+template <int BLOCK>
+__device__ __forceinline__ int item_index(int k) {
+    int t = (int)threadIdx.x;
+    asm volatile("" : "+v"(t));
+    return t + k * BLOCK;
+}
+
 template <int BLOCK, int ITEMS, bool BEST>
 __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const int64_t* __restrict__ begin, const int32_t* __restrict__ num_ops,
@@ -872,7 +883,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     if (n > 0) {
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
-            const int i = min(tid + k * BLOCK, n - 1);
+            const int i = min(item_index<BLOCK>(k), n - 1);
             sz_r[k] = size[lo + i];
             fi_r[k] = first[lo + i];
             la_r[k] = last[lo + i];
@@ -881,7 +892,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-        const int i = tid + k * BLOCK;
+        const int i = item_index<BLOCK>(k);
         if (i < n) {
             const int64_t s = sz_r[k];
             const int32_t f = fi_r[k], l = la_r[k];
@@ -938,6 +949,10 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     }
     const int sh = __builtin_ctzll(or_all);  // common power-of-two unit of all sizes
     bool general = (total >> sh) > kFastMaxUnits;
+    // sizes in units (below 2^31 unless general), kept instead of the bytes
+    uint32_t su_r[ITEMS];
+#pragma unroll
+    for (int k = 0; k < ITEMS; ++k) su_r[k] = (uint32_t)((uint64_t)sz_r[k] >> sh);
     const bool unsorted = (flags & 2u) != 0;
     auto id_of = [&](int q) { return unsorted ? (int)perm[q] : q; };  // position -> id
 
@@ -953,13 +968,13 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             bitonic_sort_u64<BLOCK>(keys, m);
 #pragma unroll
             for (int k = 0; k < ITEMS; ++k) {
-                const int q = tid + k * BLOCK;
+                const int q = item_index<BLOCK>(k);
                 if (q < n) perm[q] = (uint16_t)(keys[q] & 0xFFFFu);
             }
             l2_barrier();  // the keys are dead: first[] goes back in position order
 #pragma unroll
             for (int k = 0; k < ITEMS; ++k) {
-                const int q = tid + k * BLOCK;
+                const int q = item_index<BLOCK>(k);
                 if (q < n) fst[q] = first[lo + perm[q]];
             }
         }
@@ -992,10 +1007,10 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         int32_t rch[ITEMS];
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
+            const int q = item_index<BLOCK>(k);
             rch[k] = q + 1;
             if (q < n) {
-                const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
+                const int32_t l = last[lo + (unsorted ? (int)perm[q] : q)];
                 if (by_table) {
                     rch[k] = ptab[l];
                 } else {
@@ -1009,11 +1024,11 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
         }
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
-            const int q = tid + k * BLOCK;
+            const int q = item_index<BLOCK>(k);
             if (q < n) {
-                const int32_t l = unsorted ? last[lo + perm[q]] : la_r[k];
-                const int64_t sz = unsorted ? size[lo + perm[q]] : sz_r[k];
-                const uint32_t sq = (uint32_t)((uint64_t)sz >> sh);
+                const int32_t l = last[lo + (unsorted ? (int)perm[q] : q)];
+                const uint32_t sq =
+                    unsorted ? (uint32_t)((uint64_t)size[lo + perm[q]] >> sh) : su_r[k];
                 int a = rch[k];
                 if (!by_table && a == q + 5) {  // first[q + 4] <= l: gallop on
                     int known = q + 4, step = 8, probe = q + 8;  // first[known] <= l
@@ -1142,8 +1157,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     for (int i = tid; i <= (n >> 1); i += BLOCK) pend[i] = 0;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
-        if (q < n) su[q] = (uint32_t)((uint64_t)(unsorted ? size[lo + perm[q]] : sz_r[k]) >> sh);
+        const int q = item_index<BLOCK>(k);
+        if (q < n) su[q] = unsorted ? (uint32_t)((uint64_t)size[lo + perm[q]] >> sh) : su_r[k];
     }
     __syncthreads();
 
@@ -1197,7 +1212,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     uint32_t tlo = 0, thi = 0, slo = 0, shi = 0, sb4 = 0;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
+        const int q = item_index<BLOCK>(k);
         cls_r[k] = 7;  // no tensor
         w_r[k] = 0;
         if (q < n) {
@@ -1247,7 +1262,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     __syncthreads();
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
+        const int q = item_index<BLOCK>(k);
         if (q < n) ofsz[q] = w_r[k];
     }
     const uint32_t spare = (uint32_t)N;  // ofsz[N]: never placed, size 0
@@ -1263,7 +1278,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     }
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
+        const int q = item_index<BLOCK>(k);
         if (q < n && cls_r[k] >= 8u) {
             const uint32_t c = cls_r[k] & 7u;
             uint32_t a = tlo;
@@ -1321,8 +1336,12 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
             }
             const int cur = round % 3, nxt = (round + 1) % 3;
             if (tid == 0) {
-                nready[nxt] = 0;
-                nwide[nxt] = 0;
+                // a zero made here: left to the compiler it was kept in a
+                // register across the loop, spilled, and reloaded every round
+                uint32_t z;
+                asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+                nready[nxt] = ((unsigned long long)z << 32) | z;
+                nwide[nxt] = z;
             }
             const ReadyLists rl{readyq,
                                 {region[0] + end[0], region[1] + end[1], region[2] + end[2],
@@ -1422,7 +1441,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     uint32_t pk = 0;
 #pragma unroll
     for (int k = 0; k < ITEMS; ++k) {
-        const int q = tid + k * BLOCK;
+        const int q = item_index<BLOCK>(k);
         if (q < n) {
             const uint64_t w = ofsz[q];
             offset_out[lo + id_of(q)] = (int64_t)((uint64_t)word_off(w) << sh);
