@@ -31,6 +31,7 @@ struct BatchShape {
     int32_t cap_n;      // tensor slots per workgroup
     int32_t cap_pairs;  // left-list entries (one byte each) per trace in LDS
     int32_t items;      // tensor slots per thread
+    int32_t block;      // threads per workgroup (one trace each)
     size_t lds_bytes;   // dynamic LDS per workgroup
 };
 

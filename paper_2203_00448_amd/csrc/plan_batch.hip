@@ -57,7 +57,12 @@ __device__ unsigned int g_dbg[4096 * 8];
 
 namespace {
 
-constexpr int kBatchBlock = 512;
+// Threads per trace: 256 up to 2048 tensors (four workgroups a CU then have
+// four waves a SIMD, 128 VGPRs each, and measured faster than 512 threads
+// with 64), 512 for longer traces (at most eight tensor slots a thread).
+constexpr int kBatchBlock = 256;
+constexpr int kBatchBlockLong = 512;
+constexpr int kMaxItems = 8;
 constexpr int kLaneSlots = 8;                   // neighbours a lane holds while fitting
 constexpr int kBestSlots = 4;                   // ... in the whole-wave BEST_FIT sort
 constexpr uint32_t kCoopChunk = (uint32_t)kWave * kLaneSlots;
@@ -1536,8 +1541,9 @@ BatchShape batch_shape(int64_t max_trace_len) {
     s.cap_n = (int32_t)N;
     s.cap_pairs = (int32_t)cap;
     s.lds_bytes = batch_lds((size_t)N, (size_t)cap).total;
+    s.block = N <= (int64_t)kBatchBlock * kMaxItems ? kBatchBlock : kBatchBlockLong;
     int items = 1;  // tensor slots per thread
-    while (items * kBatchBlock < N) items <<= 1;
+    while ((int64_t)items * s.block < N) items <<= 1;
     s.items = items;
     s.ok = true;
     return s;
@@ -1552,7 +1558,11 @@ hipError_t launch_plan_batch(const BatchArgs& a, hipStream_t st) {
     const BatchShape s = batch_shape(a.max_trace_len);
     if (!s.ok) return hipErrorInvalidValue;
     const bool best = a.policy == MP_BEST_FIT;
-    constexpr int B = kBatchBlock;
+    constexpr int B = kBatchBlock, BL = kBatchBlockLong;
+    if (s.block == BL) {  // longer traces: eight slots a thread
+        if (s.items != kMaxItems) return hipErrorInvalidValue;
+        return best ? launch_items<BL, 8, true>(a, s, st) : launch_items<BL, 8, false>(a, s, st);
+    }
     switch (s.items) {
         case 1: return best ? launch_items<B, 1, true>(a, s, st) : launch_items<B, 1, false>(a, s, st);
         case 2: return best ? launch_items<B, 2, true>(a, s, st) : launch_items<B, 2, false>(a, s, st);
