@@ -221,12 +221,19 @@ def cfg5_leg(binding, tg, np, torch, t, args, offset, exp, reps=5):
                       device="cuda")
     pairs = torch.empty((cap, 2), dtype=torch.int64, device="cuda")
     cnt = torch.empty(1, dtype=torch.int64, device="cuda")
-    val = lambda off: binding.validate_plan(*args, off, capacity=cap, check=False, status=status,
-                                            workspace=vws, out=(pairs, cnt))
+    val = lambda off, srt=False: binding.validate_plan(*args, off, capacity=cap, check=False,
+                                                       status=status, workspace=vws,
+                                                       out=(pairs, cnt), assume_sorted=srt)
     _, cmed, _ = _timed(torch, np, lambda: val(offset), reps)
     clean = int(cnt.item())
+    # the decode trace is in first order: with the caller's sorted-first hint
+    # the unsorted path's sorts are not enqueued at all
+    _, hmed, _ = _timed(torch, np, lambda: val(offset, True), reps)
+    clean_h = int(cnt.item())
     bad, _ = tg.corrupt_offsets(t.first, t.last, offset.cpu().numpy(), seed=5, k=100)
     bad_d = torch.from_numpy(bad).to("cuda")
+    _, bhmed, _ = _timed(torch, np, lambda: val(bad_d, True), reps)
+    bad_h = (int(cnt.item()), _sha(pairs.cpu().numpy()))
     _, bmed, _ = _timed(torch, np, lambda: val(bad_d), reps)
     if int(status.item()) != binding.MP_OK:
         raise SystemExit("cfg5: device status " + str(int(status.item())))
@@ -241,7 +248,10 @@ def cfg5_leg(binding, tg, np, torch, t, args, offset, exp, reps=5):
             "validate_corrupted": {"us": bmed * 1e3, "tensors_per_s": t.n / (bmed * 1e-3),
                                    "conflicts": int(cnt.item()),
                                    "parity": int(cnt.item()) == cap
-                                   and _sha(pairs.cpu().numpy()) == ev["pairs_sha256"]}}
+                                   and _sha(pairs.cpu().numpy()) == ev["pairs_sha256"]},
+            "validate_sorted_hint": {"clean_us": hmed * 1e3, "corrupted_us": bhmed * 1e3,
+                                     "parity": clean_h == 0 and bad_h[0] == cap
+                                     and bad_h[1] == ev["pairs_sha256"]}}
 
 
 def strategies_leg(binding, tg, np, torch, medium, n_traces: int = 2048, n: int = 10,
