@@ -217,14 +217,13 @@ __device__ __forceinline__ uint64_t wave_inclusive_sum64_dpp(uint64_t v) {
 // The ready lists of the classes share one array of N slots: class c owns
 // the region [region[c], region[c] + number of class-c tensors), as each
 // tensor is appended once.  Appends of a round go after `end[c]` (here the
-// list position past the round's own range, region included), counted in
-// one 64-bit word with a 16-bit field per class 0-3 and a 32-bit word for
-// class 4.
+// list position past the round's own range, region included), counted by
+// one 32-bit LDS counter per class.  The order of a round's appends is
+// free: a tensor's fit depends only on its placed predecessors.
 struct ReadyLists {
     uint16_t* slot;
     uint32_t end[kClasses];
-    unsigned long long* cnt;
-    uint32_t* cnt_wide;
+    uint32_t* cnt;  // kClasses counters of this round's appends
 };
 
 // Decrement the pending counts of the successors among a lane's S slots:
@@ -232,16 +231,12 @@ struct ReadyLists {
 // neighbour (kUnplacedBit | position; every neighbour ranked before the
 // fitted tensor is placed and none ranked after it is); only those issue an
 // atomic (slots masked off issue none, so no lanes pile onto one word), and
-// a slot's tensor is ready exactly when the count it read was 1.  Ready
-// tensors are appended to
-// their class lists: the per-lane counts (a 4-bit field per class, read from
-// the words) are scanned over the wave in 10-bit fields, one reservation per
-// wave, and each lane's list positions are kept as 12-bit fields of one
-// 64-bit word (list positions are below 4096).  All 64 lanes must be active.
+// a slot's tensor is ready exactly when the count it read was 1.  A ready
+// tensor takes its list position from its class's counter (the class is
+// the field of the word's count that is set).
 template <int S>
 __device__ __forceinline__ void release(const uint32_t (&o)[S], uint64_t* ofsz,
                                         const ReadyLists& rl, int lane) {
-    static_assert(S <= 8, "a lane releases at most 8 tensors (4-bit counts)");
     uint32_t old[S];
     uint32_t* hi = reinterpret_cast<uint32_t*>(ofsz) + 1;  // the words' high halves
 #pragma unroll
@@ -249,48 +244,22 @@ __device__ __forceinline__ void release(const uint32_t (&o)[S], uint64_t* ofsz,
         old[r] = 0;
         if (o[r] >= kUnplacedBit && o[r] != kNoSlot) old[r] = atomicSub(hi + 2 * (o[r] & 0xFFFFu), 1u);
     }
-    uint32_t p4 = 0;  // ready tensors of this lane, 4 bits per class
-#pragma unroll
-    for (int r = 0; r < S; ++r) {
-        const bool rd = (old[r] & kPendMask) == 1u;
-        p4 += rd ? __builtin_amdgcn_ubfe(old[r], kClassShift, 17) : 0u;
-    }
-    if (!__ballot(p4 != 0)) return;
-    // classes 0-2 in 10-bit fields of one word, 3-4 of another
-    const uint32_t plo = (p4 & 0xFu) | ((p4 << 6) & (0xFu << 10)) | ((p4 << 12) & (0xFu << 20));
-    const uint32_t phi = ((p4 >> 12) & 0xFu) | ((p4 >> 6) & (0xFu << 10));
-    const uint32_t ilo = wave_inclusive_sum_dpp(plo), ihi = wave_inclusive_sum_dpp(phi);
-    const uint32_t tlo = (uint32_t)__builtin_amdgcn_readlane((int)ilo, 63);
-    const uint32_t thi = (uint32_t)__builtin_amdgcn_readlane((int)ihi, 63);
-    uint32_t b0 = 0, b1 = 0, b4 = 0;
-    if (lane == 0) {
-        const unsigned long long add = (unsigned long long)(tlo & 0x3FFu) |
-                                       ((unsigned long long)((tlo >> 10) & 0x3FFu) << 16) |
-                                       ((unsigned long long)(tlo >> 20) << 32) |
-                                       ((unsigned long long)(thi & 0x3FFu) << 48);
-        const unsigned long long base = atomicAdd(rl.cnt, add);
-        b0 = (uint32_t)base;
-        b1 = (uint32_t)(base >> 32);
-        if (thi >> 10) b4 = atomicAdd(rl.cnt_wide, thi >> 10);
-    }
-    b0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b0);
-    b1 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b1);
-    b4 = (uint32_t)__builtin_amdgcn_readfirstlane((int)b4);
-    const uint32_t xlo = ilo - plo, xhi = ihi - phi;  // ready tensors of the lanes before
-    uint64_t at = (uint64_t)(rl.end[0] + (b0 & 0xFFFFu) + (xlo & 0x3FFu)) |
-                  ((uint64_t)(rl.end[1] + (b0 >> 16) + ((xlo >> 10) & 0x3FFu)) << 12) |
-                  ((uint64_t)(rl.end[2] + (b1 & 0xFFFFu) + (xlo >> 20)) << 24) |
-                  ((uint64_t)(rl.end[3] + (b1 >> 16) + (xhi & 0x3FFu)) << 36) |
-                  ((uint64_t)(rl.end[4] + b4 + (xhi >> 10)) << 48);
+    uint32_t at[S];
 #pragma unroll
     for (int r = 0; r < S; ++r) {
         if ((old[r] & kPendMask) == 1u) {
-            // class field 4c of the word's count, list field 12c of `at`
-            const uint32_t sh = 3u * (__builtin_ctz(old[r] >> kClassShift));
-            rl.slot[(uint32_t)(at >> sh) & 0xFFFu] = (uint16_t)(o[r] & 0xFFFFu);
-            at += 1ull << sh;
+            const uint32_t c = (uint32_t)__builtin_ctz(old[r] >> kClassShift) >> 2;
+            at[r] = rl.end[0];
+            at[r] = c == 1 ? rl.end[1] : at[r];
+            at[r] = c == 2 ? rl.end[2] : at[r];
+            at[r] = c == 3 ? rl.end[3] : at[r];
+            at[r] = c == 4 ? rl.end[4] : at[r];
+            at[r] += atomicAdd(rl.cnt + c, 1u);
         }
     }
+#pragma unroll
+    for (int r = 0; r < S; ++r)
+        if ((old[r] & kPendMask) == 1u) rl.slot[at[r]] = (uint16_t)(o[r] & 0xFFFFu);
 }
 
 // Compare-exchange of two (offset, end) slots by offset.
@@ -817,7 +786,7 @@ __device__ __forceinline__ int item_index(int k) {
 }
 
 template <int BLOCK, int ITEMS, bool BEST>
-__global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
+__global__ __launch_bounds__(BLOCK, BEST ? 4 : (ITEMS <= 4 ? 6 : 4)) void plan_batch_kernel(
     const int64_t* __restrict__ begin, const int32_t* __restrict__ num_ops,
     const int64_t* __restrict__ size, const int32_t* __restrict__ first,
     const int32_t* __restrict__ last, int64_t n_tensors, int32_t cap_n, int32_t cap_lists,
@@ -830,8 +799,7 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     __shared__ uint64_t red[BLOCK / kWave];
     __shared__ uint64_t red3[3][BLOCK / kWave];  // ingest reductions, then the prefix pass's
     uint32_t(*red32)[BLOCK / kWave] = reinterpret_cast<uint32_t(*)[BLOCK / kWave]>(&red3[0][0]);
-    __shared__ unsigned long long nready[3];  // appended in rounds r % 3 (16-bit field per class 0-3)
-    __shared__ uint32_t nwide[3];             // ... of class 4
+    __shared__ uint32_t nready[3][kClasses];  // appended in rounds r % 3, per class
     __shared__ unsigned long long ncls64;     // tensors per ready class 0-3 (16-bit fields)
     __shared__ unsigned long long seeds64;    // ... without predecessors
     __shared__ uint32_t ncls_w, seeds_w;      // ... of class 4
@@ -859,8 +827,8 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
     const int64_t b = blockIdx.x;
     MP_STAMP(0);
     if (tid == 0) {
-        nready[0] = nready[1] = nready[2] = 0;
-        nwide[0] = nwide[1] = nwide[2] = 0;
+        for (int r = 0; r < 3; ++r)
+            for (int c = 0; c < kClasses; ++c) nready[r][c] = 0;
         ncls_w = seeds_w = 0;
         ncls64 = seeds64 = 0;
         nlong = 0;
@@ -1345,13 +1313,13 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 // register across the loop, spilled, and reloaded every round
                 uint32_t z;
                 asm volatile("v_mov_b32 %0, 0" : "=v"(z));
-                nready[nxt] = ((unsigned long long)z << 32) | z;
-                nwide[nxt] = z;
+#pragma unroll
+                for (int c = 0; c < kClasses; ++c) nready[nxt][c] = z;
             }
             const ReadyLists rl{readyq,
                                 {region[0] + end[0], region[1] + end[1], region[2] + end[2],
                                  region[3] + end[3], region[4] + end[4]},
-                                &nready[cur], &nwide[cur]};
+                                nready[cur]};
             // lane space of the round at S slots a lane: class c takes groups
             // of (8 / S) << c lanes, [0, a3) class 3, [a3, a2) class 2,
             // [a2, a1) class 1, [a1, tot) class 0 (aligned: largest first).
@@ -1428,13 +1396,13 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void plan_batch_kernel(
                 place_wave<LONG, best>(one, spare, ofsz, ll, rl, lane);
             }
             __syncthreads();
-            const unsigned long long added = nready[cur];
-            const uint32_t added_w = nwide[cur];
+            uint32_t added[kClasses];
+#pragma unroll
+            for (int c = 0; c < kClasses; ++c) added[c] = nready[cur][c];
 #pragma unroll
             for (int c = 0; c < kClasses; ++c) bgn[c] = end[c];
 #pragma unroll
-            for (int c = 0; c < 4; ++c) end[c] += (uint32_t)(added >> (16 * c)) & 0xFFFFu;
-            end[4] += added_w;
+            for (int c = 0; c < kClasses; ++c) end[c] += added[c];
         }
     };
     if (nlong) place_rounds(std::true_type{});
