@@ -8,13 +8,13 @@
 // candidates are the contiguous positions (q, reach[q]).  Short rows are
 // handled by one thread each.  Long rows are sorted by band length (one
 // class per power of two, stable, so ascending rows inside a class) and cut
-// into chunks of 64; the count pass tests a chunk
-// against tiles of 1024 candidates staged in registers, so the long bands of a
-// chunk share every load.  A device-wide scan of the row counts then gives
-// each row its start, and the write pass visits only rows that have pairs,
-// one workgroup per row in j order.  When
-// the input is not already sorted by first inside each segment, positions
-// come from a radix sort and the written pairs are radix-sorted at the end.
+// into chunks of 64; the count pass tests a chunk against tiles of 1024
+// candidates staged in registers, so the long bands of a chunk share every
+// load.  A device-wide scan of the row counts then gives each row its start,
+// and the write pass visits only rows that have pairs, one workgroup per row
+// in j order.  When the input is not already sorted by first inside each
+// segment, positions come from a radix sort and the written pairs are
+// radix-sorted at the end.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -24,11 +24,11 @@ namespace {
 
 constexpr int kVBlock = 256;
 constexpr int32_t kShortRow = 64;  // longer rows go to the chunked kernels
-constexpr unsigned kLongGrid = 1024;
+constexpr unsigned kLongGrid = 1024;               // workgroups of the long rows' write pass
 constexpr int kChunkRows = 64;                      // long rows per chunk (one per lane)
 constexpr int kTileItems = 4;                       // candidates per thread per tile
 constexpr int64_t kTileJ = kVBlock * kTileItems;    // candidates per tile
-constexpr unsigned kTileGrid = 2048;
+constexpr unsigned kTileGrid = 2048;                // workgroups of the count pass (tile ranges)
 constexpr int kWriteUnroll = 8;                     // candidate loads in flight per lane (write pass)
 
 // Workspace words.
