@@ -117,6 +117,48 @@ __global__ __launch_bounds__(kScanBlock) void rescan_kernel(int64_t* __restrict_
     }
 }
 
+// Short arrays (up to kSmallScan values) in one launch: one workgroup of
+// 1024 threads, 16 contiguous values a thread; partial[tiles] gets the total
+// as after the three-kernel scan.
+constexpr int kSmallBlock = 1024;
+constexpr int kSmallItems = 16;
+constexpr int64_t kSmallScan = (int64_t)kSmallBlock * kSmallItems;
+
+__global__ __launch_bounds__(kSmallBlock) void scan_small_kernel(int64_t* __restrict__ data,
+                                                                  int64_t n, int inclusive,
+                                                                  int64_t* __restrict__ partial,
+                                                                  int64_t tiles,
+                                                                  unsigned long long* max_out,
+                                                                  const uint32_t* skip) {
+    __shared__ int64_t scratch[kSmallBlock / kWave];
+    if (skip && *skip) return;
+    const int64_t base = (int64_t)threadIdx.x * kSmallItems;
+    int64_t v[kSmallItems];
+    int64_t s = 0;
+#pragma unroll
+    for (int k = 0; k < kSmallItems; ++k) {
+        v[k] = (base + k < n) ? data[base + k] : 0;
+        s += v[k];
+    }
+    int64_t total;
+    int64_t run = block_exclusive_sum64<kSmallBlock>(s, &total, scratch);
+    int64_t mx = 0;
+#pragma unroll
+    for (int k = 0; k < kSmallItems; ++k) {
+        if (base + k < n) {
+            const int64_t out = inclusive ? run + v[k] : run;
+            data[base + k] = out;
+            mx = out > mx ? out : mx;
+        }
+        run += v[k];
+    }
+    if (threadIdx.x == 0) partial[tiles] = total;
+    if (max_out) {
+        mx = wave_reduce(mx, OpMax<int64_t>());
+        if ((threadIdx.x & (kWave - 1)) == 0 && mx > 0) atomicMax(max_out, (unsigned long long)mx);
+    }
+}
+
 }  // namespace
 
 size_t scan_workspace_bytes(int64_t n) {
@@ -134,6 +176,11 @@ hipError_t device_scan_i64(int64_t* data, int64_t n, bool inclusive, int64_t* pa
     if (n <= 0) return hipSuccess;
     const int64_t tiles = (n + kScanTile - 1) / kScanTile;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
+    if (n <= kSmallScan) {
+        hipLaunchKernelGGL(scan_small_kernel, dim3(1), dim3(kSmallBlock), 0, st, data, n,
+                           inclusive ? 1 : 0, partial, tiles, max_out, skip);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(tile_sums_kernel, dim3((unsigned)tiles), dim3(kScanBlock), 0, st, data, n,
                        partial, skip);
     hipLaunchKernelGGL(scan_partials_kernel, dim3(1), dim3(1024), 0, st, partial, tiles, skip);
