@@ -126,6 +126,31 @@ def test_validate_long_rows_and_capacity():
     assert gc == ec and gp.shape[0] == 0
 
 
+def test_validate_long_rows_wide_offsets():
+    """Long rows whose byte ranges straddle 2^32 and lie far above it: the
+    count pass compares 64-bit ranges (the 32-bit compares are used only when
+    every offset + size is below 2^32); sorted and unsorted positions."""
+    binding = need_gpu()
+    rng = np.random.default_rng(207)
+    n = 3000
+    t = tg.random_trace(rng, n, 600, max_len=3, sorted_first=True)
+    t.first[::89] = 0
+    t.last[::89] = 599
+    order = np.lexsort((np.arange(n), t.first))
+    t = tg.Trace(t.size[order], t.first[order], t.last[order], t.num_ops)
+    for base in ((1 << 32) - 1000, 1 << 40):
+        off = base + 64 * rng.integers(0, 30, n)
+        ep, ec = _oracle_pairs(t, off)
+        print(f"case wide offsets base {base} ({ec} conflicts)", flush=True)
+        gp, gc, st = _gpu_pairs(binding, t, off, capacity=max(ec, 1))
+        assert st == binding.MP_OK and gc == ec and np.array_equal(gp, ep)
+        perm = rng.permutation(n)
+        tp = tg.Trace(t.size[perm], t.first[perm], t.last[perm], t.num_ops)
+        ep2, ec2 = _oracle_pairs(tp, off[perm])
+        gp2, gc2, st2 = _gpu_pairs(binding, tp, off[perm], capacity=max(ec2, 1))
+        assert st2 == binding.MP_OK and gc2 == ec2 == ec and np.array_equal(gp2, ep2)
+
+
 def test_validate_oracle_plans_are_clean():
     binding = need_gpu()
     rng = np.random.default_rng(203)
