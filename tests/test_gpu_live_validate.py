@@ -200,6 +200,28 @@ def test_validate_batch_matches_per_trace():
     assert np.array_equal(host(pairs), expect)
 
 
+def test_validate_batch_long_rows_across_traces():
+    """Batches whose traces hold long-lived tensors (bands far over 64
+    candidates): the long rows of different traces share chunks of the count
+    pass, and each row stays inside its own trace."""
+    binding = need_gpu()
+    rng = np.random.default_rng(208)
+    traces = []
+    for k in range(12):
+        n = int(rng.choice([1, 200, 900, 1500]))
+        t = tg.random_trace(rng, n, 300, max_len=4, sorted_first=(k % 4 != 0))
+        t.first[::53] = 0
+        t.last[::53] = 299
+        traces.append(t)
+    batch = tg.concat(traces)
+    off = 64 * rng.integers(0, 25, batch.size.shape[0])
+    expect = _batch_expect(traces, batch, off)
+    print(f"case batch long rows ({expect.shape[0]} conflicts)", flush=True)
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, off), capacity=max(1, expect.shape[0]))
+    assert st == binding.MP_OK and cnt == expect.shape[0]
+    assert np.array_equal(host(pairs), expect)
+
+
 def _batch_expect(traces, batch, off):
     expect = []
     for b, t in enumerate(traces):
