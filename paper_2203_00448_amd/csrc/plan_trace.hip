@@ -14,7 +14,9 @@
 //              chosen from a histogram of band lengths, so that the other
 //              tensors meeting t from behind lie in a short window before t
 //   rank       stable radix sort by size descending over positions
-//   place      persistent kernel: workgroups take ranks from a counter.  For
+//   place      persistent kernel: workgroups take ranks in blocks of 32
+//              consecutive ranks claimed per XCD, so that most dependency
+//              links (usually rank r - 1 to rank r) stay inside one L2.  For
 //              tensor t the workgroup walks t's candidates (forward band,
 //              backward window, long list), keeps those ranked before t,
 //              turns the already placed ones into one run of ranges by
@@ -22,8 +24,9 @@
 //              bitonic sort with prefix maxima of the ends), marks the run's
 //              gaps that hold t, then waits for the rest while keeping the
 //              lowest fit up to date as they arrive.  A tensor only waits on
-//              lower ranks, which were taken earlier by running workgroups,
-//              so the schedule cannot deadlock.
+//              lower ranks; each is held by a running workgroup or sits in a
+//              block whose XCD takes it once a running workgroup there
+//              finishes, so the schedule cannot deadlock.
 //   output     offsets (scaled back to bytes) and the peak.
 #include <type_traits>
 
@@ -37,11 +40,19 @@ namespace {
 constexpr int kTBlock = 512;
 constexpr int kRunCap = 16384;    // ranges sorted at once in LDS
 // Predecessors still unplaced when t is examined.  Each is held by another
-// running workgroup (ranks are taken in order, one at a time per
-// workgroup), so there are fewer than the grid; the host keeps the grid at
-// most kDynCap + 1.
-constexpr int kDynCap = 256;
-static_assert(kDynCap <= 4 * kWave, "wave 0 holds every late predecessor, 4 a lane at most");
+// running workgroup (one rank at a time per workgroup) or is still untaken in
+// another XCD's current block (see kTicketBlock), so there are fewer than the
+// grid + kXcdGroups * (kTicketBlock - 1); the host keeps the grid at most
+// kDynCap + 1 - kXcdGroups * (kTicketBlock - 1).
+constexpr int kDynCap = 512;
+static_assert(kDynCap <= 8 * kWave, "wave 0 holds every late predecessor, 8 a lane at most");
+// Ranks are handed out in blocks of kTicketBlock consecutive ranks: a
+// workgroup takes the next slot of its XCD's current block, and the one that
+// opens a block claims the next block of the whole trace.  A rank below t's
+// can then still be untaken, but only in another XCD's current block (at
+// most kTicketBlock - 1 of them per XCD).
+constexpr int kXcdGroups = 8;
+constexpr uint32_t kTicketBlock = 32;
 constexpr uint32_t kUnionMin = 256;  // placed predecessors merged through a bitmap beyond this
 constexpr int64_t kScratchRuns = 8;  // global scratch per workgroup: 8 sorted runs
 constexpr uint32_t kUnplacedT = 0xFFFFFFFFu;
@@ -54,6 +65,8 @@ struct TFlags {
     uint32_t unsorted, sorted, abort, wide;
     uint64_t or_all, sum;
     uint32_t shift, lthr, n_long, ticket;
+    uint32_t xtick[kXcdGroups];  // slots taken per XCD (blocks of kTicketBlock ranks)
+    uint32_t blocks;             // rank blocks claimed
     uint32_t skip_narrow, skip_wide;  // nonzero: the 32-bit (64-bit) unit path does not run
     uint32_t pool[kPoolSlots];        // 1 while a workgroup holds the slot
     uint32_t hist[64];      // band lengths by bit width
@@ -73,6 +86,7 @@ __global__ void t_init_kernel(TFlags* fl) {
     const int i = threadIdx.x;
     if (i < 64) fl->hist[i] = 0;
     if (i < kPoolSlots) fl->pool[i] = 0;
+    if (i < kXcdGroups) fl->xtick[i] = 0;
     if (i == 0) {
         fl->unsorted = 0;
         fl->sorted = 1;
@@ -86,6 +100,7 @@ __global__ void t_init_kernel(TFlags* fl) {
         fl->lthr = 0;
         fl->n_long = 0;
         fl->ticket = 0;
+        fl->blocks = 0;
         fl->peak = 0;
     }
 }
@@ -300,6 +315,30 @@ __device__ __forceinline__ uint64_t agent_load64(const uint64_t* p) {
 }
 __device__ __forceinline__ void agent_store64(uint64_t* p, uint64_t v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+// The next rank for the calling workgroup (thread 0 only): slot c of its
+// XCD's counter lies in that XCD's block c / kTicketBlock; the workgroup
+// taking slot 0 claims the trace's next block and records it (as block + 1)
+// in xbase[x][c / kTicketBlock], where the others of the block read it.
+// Blocks are claimed in increasing order and each XCD fills its own in
+// order, so every rank is taken once, and a rank below one being placed is
+// either held by a running workgroup or waiting in an XCD's current block.
+// Any grouping of workgroups would be correct; the XCD is the fast one.
+__device__ __forceinline__ uint32_t take_rank(TFlags* fl, uint32_t* xbase, int64_t xcap) {
+    uint32_t xcc;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(xcc));
+    const uint32_t x = xcc & (kXcdGroups - 1);
+    const uint32_t c = atomicAdd(&fl->xtick[x], 1u);
+    const uint32_t j = c / kTicketBlock, s = c % kTicketBlock;
+    uint32_t* slot = xbase + (int64_t)x * xcap + j;
+    if (s == 0) {
+        const uint32_t blk = atomicAdd(&fl->blocks, 1u);
+        agent_store(slot, blk + 1u);
+        return blk * kTicketBlock;
+    }
+    uint32_t v;
+    while ((v = agent_load(slot)) == 0u) __builtin_amdgcn_s_sleep(1);
+    return (v - 1u) * kTicketBlock + s;
 }
 // Barrier after which every thread's global stores of the workgroup are
 // complete (the workgroup barrier alone does not wait for them); readers then
@@ -536,7 +575,9 @@ struct PlaceArgs {
     int64_t n;
     TFlags* fl;
     int32_t* status;
-    int32_t best;  // fit policy: 0 lowest gap, 1 tightest gap
+    int32_t best;     // fit policy: 0 lowest gap, 1 tightest gap
+    uint32_t* xbase;  // kXcdGroups x xcap claimed blocks (+1), zero at the launch
+    int64_t xcap;
 };
 
 // Visit the positions ranked before t whose lifetimes meet t's: the forward
@@ -889,7 +930,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     const int64_t stat_cap = a.stat_cap;
     while (true) {
         if (threadIdx.x == 0) {
-            s_rank = atomicAdd(&a.fl->ticket, 1u);
+            s_rank = take_rank(a.fl, a.xbase, a.xcap);
             s_nstat = 0;
             s_ndyn = 0;
         }
@@ -989,8 +1030,8 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 if (lane == 0) gbits[w] = mk;
             }
             __syncthreads();
-            // wave 0; K late predecessors a lane (K = 1 or 4 for up to 64 or
-            // 256 of them)
+            // wave 0; K late predecessors a lane (K = 1, 4 or 8 for up to 64,
+            // 256 or 512 of them)
             auto wave0 = [&](auto k_late) {
                 constexpr int K = decltype(k_late)::value;
                 // The first 64 marked gaps, in address order, one per lane
@@ -1122,7 +1163,8 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
             };
             if (wid == 0) {
                 if (ndyn <= kWave) wave0(std::integral_constant<int, 1>{});
-                else wave0(std::integral_constant<int, 4>{});
+                else if (ndyn <= 4 * kWave) wave0(std::integral_constant<int, 4>{});
+                else wave0(std::integral_constant<int, 8>{});
             }
             __syncthreads();
             continue;
@@ -1182,17 +1224,25 @@ __global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restric
 
 __global__ void t_peak_kernel(const TFlags* fl, int64_t* peak_out) { *peak_out = (int64_t)fl->peak; }
 
+__global__ __launch_bounds__(256) void t_clear_kernel(uint32_t* __restrict__ p, int64_t count) {
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = 0;
+}
+
 struct TLayout {
     size_t flags, su, pf, pl, pid, off, su64, off64, reach, keys0, vals0, keys1, vals1, radix,
-        lflag, lpartial, llist, run_keys, pool, total;
+        lflag, lpartial, llist, run_keys, pool, xbase, total;
+    int64_t xcap;  // rank blocks an XCD can claim
     unsigned grid;
 };
 
 // Workgroups of the placement kernel on the current device: every resident
-// one (more would only wait for a CU), at most kDynCap + 1 so that a tensor
-// never has more late predecessors than wave 0 holds.  The launch needs no
-// co-residency -- a workgroup waits only on ranks taken earlier by running
-// workgroups -- so this is a plain launch sized for throughput.
+// one (more would only wait for a CU), at most 265 so that a tensor never
+// has more late predecessors than wave 0 holds (the other workgroups' ranks
+// and the untaken ranks of the other XCDs' current blocks).  The launch
+// needs no co-residency -- a workgroup waits only on lower ranks, each held
+// by a running workgroup or taken once one on its XCD finishes -- so this
+// is a plain launch sized for throughput.
 unsigned place_grid() {
     int dev = 0, cus = 0, per = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -1204,7 +1254,9 @@ unsigned place_grid() {
         per < 1)
         per = 1;
     const int64_t g = (int64_t)cus * per;
-    return (unsigned)(g > kDynCap + 1 ? kDynCap + 1 : g);
+    constexpr int64_t kMaxGrid = kDynCap + 1 - kXcdGroups * ((int64_t)kTicketBlock - 1);
+    static_assert(kMaxGrid >= 256, "one workgroup per CU of the largest device");
+    return (unsigned)(g > kMaxGrid ? kMaxGrid : g);
 }
 
 // Keys per workgroup buffer: a tensor has fewer than n predecessors; the
@@ -1242,6 +1294,10 @@ TLayout t_layout(int64_t n, unsigned grid) {
     L.llist = take(nn * 4);
     L.run_keys = take((size_t)grid * (size_t)stat_cap_of(nn) * 8);
     L.pool = take((size_t)kPoolSlots * 4 * nn * 8);
+    // an XCD takes at most n ranks and one more per workgroup (the take
+    // that ends it): blocks 0 .. (n + grid) / kTicketBlock
+    L.xcap = (nn + (int64_t)grid) / kTicketBlock + 2;
+    L.xbase = take((size_t)kXcdGroups * (size_t)L.xcap * 4);
     L.total = o;
     L.grid = grid;
     return L;
@@ -1319,6 +1375,9 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     if (e != hipSuccess) return e;
     if (alt != alt64) return hipErrorInvalidValue;  // both sorts end in the same buffer
     uint64_t* pool = reinterpret_cast<uint64_t*>(w + L.pool);
+    uint32_t* xbase = reinterpret_cast<uint32_t*>(w + L.xbase);
+    const int64_t nx = (int64_t)kXcdGroups * L.xcap;
+    hipLaunchKernelGGL(t_clear_kernel, dim3(grid_n(nx, 256)), dim3(256), 0, st, xbase, nx);
     PlaceArgs pa{su,
                  reach,
                  alt ? vals1 : vals0,
@@ -1330,7 +1389,9 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
                  n,
                  fl,
                  status,
-                 policy == MP_BEST_FIT ? 1 : 0};
+                 policy == MP_BEST_FIT ? 1 : 0,
+                 xbase,
+                 L.xcap};
     hipLaunchKernelGGL(t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, pa);
     WideArgs wa{su64, reach, alt ? vals1 : vals0, llist, off64,
                 reinterpret_cast<uint64_t*>(w + L.run_keys), stat_cap_of(n) / 4, pool, n, fl,

@@ -64,7 +64,11 @@ def test_adversarial_shapes():
     binding = need_gpu()
     rng = np.random.default_rng(301)
     print("case full overlap, 9000 tensors", flush=True)
-    n = 9000  # up to 8999 placed predecessors, drawn as one coverage bitmap
+    # up to 8999 placed predecessors, drawn as one coverage bitmap; every
+    # lower rank is a predecessor, so a tensor can find ~500 of them unplaced
+    # (held by other workgroups, or untaken in other XCDs' rank blocks), the
+    # most the wait holds (a broken bound raises the device status)
+    n = 9000
     _check(binding, tg.Trace(64 * rng.integers(1, 200, n), np.zeros(n, np.int32),
                              np.full(n, 3, np.int32), 4))
     print("case equal sizes / long-lived / disjoint", flush=True)
