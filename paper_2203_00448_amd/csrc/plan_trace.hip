@@ -584,28 +584,136 @@ struct PlaceArgs {
 // band, the backward window of short bands and the long list; fn(p, o) gets
 // each with its offset as read (kUnplacedT while not placed).  Each thread
 // takes kBatch candidates per turn and issues their loads together (sizes
-// and reaches, then offsets), so the latencies overlap.
+// and reaches, then offsets), so the latencies overlap.  With 32-bit sizes
+// the forward band and the backward window are read 4 kVec positions a
+// thread per turn, four consecutive ones per 16-byte load.  A forward band
+// longer than one such pass (a long-lived tensor's spans most of the trace,
+// and its walk was a chain of dependent turns) goes in two steps per
+// segment of kBandSeg positions: its sizes, 4 kBandVec positions a thread
+// per turn, filter the candidates into an LDS list (no offset load waits on
+// a size load), then the listed candidates' offsets are loaded kBandLoads a
+// thread at a time.  Decode-like trace: 52.4 -> 49.7 ms.
 constexpr int kBatch = 4;
+constexpr int kVec = 4;
+constexpr int kBandVec = 8;
+constexpr int32_t kBandSeg = 2 * kRunCap;  // list entries (u32) in the run buffer
+constexpr int kBandLoads = 8;
 
 // The candidate walk over positions, for either width of sizes (SZ) and
 // offsets (OF, kUnplaced of that width while unplaced).
+// The 32-bit path passes an LDS list of kBandSeg entries and its counter
+// (every thread of the workgroup calls the walk; it holds barriers then).
 template <int BLOCK, typename SZ, typename OF, typename F>
 __device__ __forceinline__ void walk_preds(const int32_t* reach, const SZ* su, const OF* off,
                                            const int32_t* long_list, int32_t qt, SZ st,
-                                           uint32_t lthr, uint32_t n_long, F&& fn) {
+                                           uint32_t lthr, uint32_t n_long, F&& fn,
+                                           uint32_t* list = nullptr, uint32_t* list_n = nullptr) {
     auto load_off = [&](int32_t p) -> OF {
         if constexpr (sizeof(OF) == 8) return agent_load64(reinterpret_cast<const uint64_t*>(off) + p);
         else return agent_load(reinterpret_cast<const uint32_t*>(off) + p);
     };
-    auto finish = [&](const int32_t (&pp)[kBatch], const bool (&ok)[kBatch]) {
-        OF o[kBatch];
+    auto finish = [&](const auto& pp, const auto& ok) {
+        constexpr int N = sizeof(pp) / sizeof(pp[0]);
+        OF o[N];
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u) o[u] = ok[u] ? load_off(pp[u]) : OF(0);
+        for (int u = 0; u < N; ++u) o[u] = ok[u] ? load_off(pp[u]) : OF(0);
 #pragma unroll
-        for (int u = 0; u < kBatch; ++u)
+        for (int u = 0; u < N; ++u)
             if (ok[u]) fn(pp[u], o[u]);
     };
     const int32_t rt = reach[qt];
+    const int64_t lo = (int64_t)qt - (int64_t)lthr - 1;
+    if constexpr (sizeof(SZ) == 4) {
+        // positions g .. g + 3 (g a multiple of 4) below `end`: one 16-byte
+        // load when all four are, else one load per position below `end`
+        auto load4 = [&](const auto* arr, int32_t g, int32_t end, auto (&v)[4]) {
+            using T = std::remove_cv_t<std::remove_reference_t<decltype(arr[0])>>;
+            if (g + 3 < end) {
+                const uint4 w = *reinterpret_cast<const uint4*>(arr + g);
+                v[0] = (T)w.x; v[1] = (T)w.y; v[2] = (T)w.z; v[3] = (T)w.w;
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) v[e] = g + e < end ? arr[g + e] : T(0);
+            }
+        };
+        constexpr int32_t kStride = 4 * BLOCK;  // positions between a thread's groups
+        // forward band: meets t; ranked before t iff strictly larger
+        if (rt - qt - 1 <= kStride * kVec) {  // one pass
+            for (int32_t g0 = ((qt + 1) & ~3) + 4 * (int32_t)threadIdx.x; g0 < rt;
+                 g0 += kStride * kVec) {
+                uint32_t sz[kVec][4];
+#pragma unroll
+                for (int k = 0; k < kVec; ++k) load4(su, g0 + kStride * k, rt, sz[k]);
+                int32_t pp[4 * kVec];
+                bool ok[4 * kVec];
+#pragma unroll
+                for (int k = 0; k < kVec; ++k)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int32_t p = g0 + kStride * k + e;
+                        pp[4 * k + e] = p;
+                        ok[4 * k + e] = p > qt && p < rt && sz[k][e] > st;
+                    }
+                finish(pp, ok);
+            }
+        } else {
+        for (int32_t s0 = qt + 1; s0 < rt; s0 += kBandSeg) {
+            const int32_t s1 = rt - s0 > kBandSeg ? s0 + kBandSeg : rt;
+            if (threadIdx.x == 0) *list_n = 0;
+            __syncthreads();
+            for (int32_t g0 = (s0 & ~3) + 4 * (int32_t)threadIdx.x; g0 < s1;
+                 g0 += kStride * kBandVec) {
+                uint32_t sz[kBandVec][4];
+#pragma unroll
+                for (int k = 0; k < kBandVec; ++k) load4(su, g0 + kStride * k, s1, sz[k]);
+#pragma unroll
+                for (int k = 0; k < kBandVec; ++k)
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int32_t p = g0 + kStride * k + e;
+                        if (p >= s0 && p < s1 && sz[k][e] > st) list[atomicAdd(list_n, 1u)] = (uint32_t)p;
+                    }
+            }
+            __syncthreads();
+            const uint32_t m = *list_n;
+            for (uint32_t i0 = threadIdx.x; i0 < m; i0 += BLOCK * kBandLoads) {
+                int32_t pp[kBandLoads];
+                bool ok[kBandLoads];
+#pragma unroll
+                for (int u = 0; u < kBandLoads; ++u) {
+                    const uint32_t i = i0 + (uint32_t)(u * BLOCK);
+                    ok[u] = i < m;
+                    pp[u] = ok[u] ? (int32_t)list[i] : 0;
+                }
+                finish(pp, ok);
+            }
+            __syncthreads();  // the list is refilled or handed back
+        }
+        }
+        // backward window of short bands: ranked before t iff at least as large
+        const int32_t w0 = (int32_t)(lo > 0 ? lo : 0);
+        for (int32_t g0 = (w0 & ~3) + 4 * (int32_t)threadIdx.x; g0 < qt; g0 += kStride * kVec) {
+            uint32_t sz[kVec][4];
+            int32_t rr[kVec][4];
+#pragma unroll
+            for (int k = 0; k < kVec; ++k) {
+                load4(su, g0 + kStride * k, qt, sz[k]);
+                load4(reach, g0 + kStride * k, qt, rr[k]);
+            }
+            int32_t pp[4 * kVec];
+            bool ok[4 * kVec];
+#pragma unroll
+            for (int k = 0; k < kVec; ++k)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int32_t p = g0 + kStride * k + e;
+                    pp[4 * k + e] = p;
+                    ok[4 * k + e] = p >= w0 && p < qt && (uint32_t)(rr[k][e] - p - 1) <= lthr &&
+                                    rr[k][e] > qt && sz[k][e] >= st;
+                }
+            finish(pp, ok);
+        }
+    } else {
     // forward band: meets t; ranked before t iff strictly larger
     for (int32_t j0 = qt + 1 + (int32_t)threadIdx.x; j0 < rt; j0 += BLOCK * kBatch) {
         int32_t pp[kBatch];
@@ -621,7 +729,6 @@ __device__ __forceinline__ void walk_preds(const int32_t* reach, const SZ* su, c
         finish(pp, ok);
     }
     // backward window of short bands: ranked before t iff at least as large
-    const int64_t lo = (int64_t)qt - (int64_t)lthr - 1;
     for (int64_t p0 = (lo > 0 ? lo : 0) + threadIdx.x; p0 < qt; p0 += BLOCK * kBatch) {
         int32_t pp[kBatch], rr[kBatch];
         bool ok[kBatch];
@@ -637,6 +744,7 @@ __device__ __forceinline__ void walk_preds(const int32_t* reach, const SZ* su, c
         for (int u = 0; u < kBatch; ++u)
             ok[u] = pp[u] < qt && (uint32_t)(rr[u] - pp[u] - 1) <= lthr && rr[u] > qt && sz[u] >= st;
         finish(pp, ok);
+    }
     }
     // long bands that started before t
     for (uint32_t k0 = threadIdx.x; k0 < n_long; k0 += BLOCK * kBatch) {
@@ -661,9 +769,10 @@ __device__ __forceinline__ void walk_preds(const int32_t* reach, const SZ* su, c
 
 template <int BLOCK, typename F>
 __device__ __forceinline__ void for_each_pred(const PlaceArgs& a, int32_t qt, uint32_t st,
-                                              uint32_t lthr, uint32_t n_long, F&& fn) {
+                                              uint32_t lthr, uint32_t n_long, uint32_t* list,
+                                              uint32_t* list_n, F&& fn) {
     walk_preds<BLOCK, uint32_t, uint32_t>(a.reach, a.su, a.off, a.long_list, qt, st, lthr,
-                                          n_long, fn);
+                                          n_long, fn, list, list_n);
 }
 
 // ------------------------------------------------- general fit (any width)
@@ -923,7 +1032,10 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
     __shared__ uint64_t scratch64[BLOCK / kWave];
     __shared__ uint64_t gbits[kRunCap / 64];  // gaps of the placed run that hold t
     __shared__ uint32_t cidx[kWave];           // the first 64 of them
-    __shared__ uint32_t s_rank, s_nstat, s_ndyn, s_slot;
+    __shared__ uint32_t s_rank, s_nstat, s_ndyn, s_slot, s_lcnt;
+    // the run buffer is free while predecessors are collected: the forward
+    // band's candidate list
+    uint32_t* const band_list = reinterpret_cast<uint32_t*>(skeys);
     if (a.fl->abort || a.fl->wide) return;
     const uint32_t lthr = a.fl->lthr, n_long = a.fl->n_long;
     uint64_t* gkeys = a.run_keys + (int64_t)blockIdx.x * a.stat_cap;
@@ -941,7 +1053,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         const uint32_t st = a.su[qt];
         // 1. collect: placed predecessors as keys, unplaced ones by position
         //    (beyond kDynCap of those, wait for them right here)
-        for_each_pred<BLOCK>(a, qt, st, lthr, n_long, [&](int32_t p, uint32_t o) {
+        for_each_pred<BLOCK>(a, qt, st, lthr, n_long, band_list, &s_lcnt, [&](int32_t p, uint32_t o) {
             if (o == kUnplacedT) {
                 const uint32_t d = atomicAdd(&s_ndyn, 1u);
                 if (d < (uint32_t)kDynCap) {
@@ -971,7 +1083,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
             const GenRanges gr = pool_ranges(a.pool, slot, a.n);
             if (threadIdx.x == 0) s_nstat = 0;
             __syncthreads();
-            for_each_pred<BLOCK>(a, qt, st, lthr, n_long, [&](int32_t p, uint32_t o) {
+            for_each_pred<BLOCK>(a, qt, st, lthr, n_long, band_list, &s_lcnt, [&](int32_t p, uint32_t o) {
                 while (o == kUnplacedT) o = agent_load(a.off + p);  // placed: seen above
                 const uint32_t k = atomicAdd(&s_nstat, 1u);
                 gr.ks[k] = o;
