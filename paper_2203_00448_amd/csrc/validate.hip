@@ -608,12 +608,37 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
             }
         }
         __syncthreads();
-        // reach: the next four positions are probed at once (short bands end
-        // there), longer bands gallop on; band lengths; sortedness check
+        // reach.  When the trace's first ops span at most 3 N values, from a
+        // table over them in the LDS the byte ranges take later: tab[v - f0]
+        // = positions whose first op is at most v, so reach[q] =
+        // tab[last[q] - f0] (every position when last[q] >= the highest
+        // first op), clamped into (q, m] should the sorted promise be broken
+        // (it is reported below).  Otherwise the next four positions are
+        // probed at once (short bands end there) and longer bands gallop on.
+        const int32_t f_lo = m > 0 ? lf[0] : 0, f_hi = m > 0 ? lf[m - 1] : 0;
+        const bool use_tab = m > 0 && f_hi >= f_lo && (int64_t)f_hi - f_lo < 3 * (int64_t)N;
+        uint32_t* tab = reinterpret_cast<uint32_t*>(smem + 4 * N);
+        if (use_tab) {
+#pragma unroll
+            for (int k = 0; k < ITEMS; ++k) {
+                const int q = tid + k * BLOCK;
+                if (q < m) {
+                    const int32_t f = lf[q], f1 = q + 1 < m ? lf[q + 1] : f_hi + 1;
+                    for (int32_t v = max(f, f_lo); v < f1 && v <= f_hi; ++v) tab[v - f_lo] = (uint32_t)(q + 1);
+                }
+            }
+            __syncthreads();
+        }
 #pragma unroll
         for (int k = 0; k < ITEMS; ++k) {
             const int q = tid + k * BLOCK;
-            if (q < m) {
+            if (q < m && use_tab) {
+                if (q > 0 && lf[q] < lf[q - 1]) bad = true;  // the sorted promise is broken
+                const int32_t l = l_r[k];
+                int a = l >= f_hi ? m : (l < f_lo ? q + 1 : (int)tab[l - f_lo]);
+                a = a < q + 1 ? q + 1 : (a > m ? m : a);
+                band[q] = (uint32_t)(a - q - 1);
+            } else if (q < m) {
                 if (q > 0 && lf[q] < lf[q - 1]) bad = true;  // the sorted promise is broken
                 const int32_t l = l_r[k];
                 const int32_t f1 = q + 1 < m ? lf[q + 1] : INT32_MAX;

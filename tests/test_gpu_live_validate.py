@@ -262,6 +262,29 @@ def test_validate_batch_per_trace_path(max_len):
     assert np.array_equal(host(pairs), expect[:max(k, 1)])
 
 
+def test_validate_batch_per_trace_sparse_ops():
+    """Traces whose first ops span more than three times the trace bound
+    find their bands by galloping search, the others from a table over the
+    ops; one batch mixes both."""
+    binding = need_gpu()
+    rng = np.random.default_rng(212)
+    traces = []
+    for k in range(24):
+        n = int(rng.integers(1, 600))
+        T = int(rng.choice([4, 300, 5000, 40000]))  # 5000 and 40000: wider than 3 x 600 slots
+        traces.append(tg.random_trace(rng, n, T, max_len=int(rng.integers(1, max(2, T // 8))),
+                                      sorted_first=True))
+    batch = tg.concat(traces)
+    off = 64 * rng.integers(0, 40, batch.size.shape[0])
+    expect = _batch_expect(traces, batch, off)
+    print(f"case per-trace validation, sparse and dense ops ({expect.shape[0]} conflicts)",
+          flush=True)
+    pairs, cnt, st = binding.validate_batch(*_batch_dev(batch, off), capacity=expect.shape[0],
+                                            assume_sorted=True, max_trace_len=600)
+    assert st == binding.MP_OK and cnt == expect.shape[0]
+    assert np.array_equal(host(pairs), expect)
+
+
 def test_validate_batch_per_trace_clean_plans():
     """Oracle plans have no conflicts: the count pass alone decides."""
     binding = need_gpu()
