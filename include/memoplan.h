@@ -107,9 +107,9 @@ int32_t mp_plan_batch(const int64_t* begin, int64_t n_traces, const int32_t* num
 int64_t mp_batch_pair_capacity(int64_t max_trace_len);
 
 /* Greedy-by-size plan of one trace of any length, using the whole device
- * (a persistent kernel: workgroups take tensors in rank order from a counter
- * and each fits its tensor once the earlier-ranked tensors that meet it are
- * placed).
+ * (a persistent kernel: workgroups take tensors in rank order, in blocks of
+ * 32 consecutive ranks per XCD, and each fits its tensor once the
+ * earlier-ranked tensors that meet it are placed).
  *   size, first, last [n] (int64, int32, int32), 0 <= n < 2^30.
  *   offset_out[n] int64, peak_out: one device int64 (arena bytes).
  *   policy: MP_LOWEST_FIT or MP_BEST_FIT.
@@ -122,7 +122,12 @@ int64_t mp_batch_pair_capacity(int64_t max_trace_len);
  * earlier-ranked intersecting tensors than its workgroup's buffer holds
  * (131072, or 32768 with 64-bit counts) waits until all of them are placed,
  * takes one of two shared buffers of n ranges and is fitted there.
- * Tensors need not be sorted by first. */
+ * Tensors need not be sorted by first.
+ * Debug: the environment variable MEMOPLAN_DEBUG_WAIT, read on each call,
+ * set to "wide" makes every wait for late predecessors take its widest form;
+ * "tight" besides caps the late list at 8, so tensors with more wait during
+ * their collection and the call reports MP_EDEVICE.  Offsets are exact
+ * either way; both only exercise paths the schedule rarely reaches. */
 int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
                       int32_t num_ops, int32_t policy, int64_t* offset_out, int64_t* peak_out,
                       void* workspace, size_t workspace_bytes, int32_t* status_out,

@@ -28,6 +28,9 @@
 //              block whose XCD takes it once a running workgroup there
 //              finishes, so the schedule cannot deadlock.
 //   output     offsets (scaled back to bytes) and the peak.
+#include <stdlib.h>
+#include <string.h>
+
 #include <type_traits>
 
 #include "internal.hpp"
@@ -578,6 +581,11 @@ struct PlaceArgs {
     int32_t best;     // fit policy: 0 lowest gap, 1 tightest gap
     uint32_t* xbase;  // kXcdGroups x xcap claimed blocks (+1), zero at the launch
     int64_t xcap;
+    // debug (MEMOPLAN_DEBUG_WAIT): late predecessors held before the
+    // collection waits itself (kDynCap normally), and the fewest held a lane
+    // in the wait (1 normally; 8 takes the widest form for every tensor)
+    uint32_t dyn_cap;
+    int32_t min_late_k;
 };
 
 // Visit the positions ranked before t whose lifetimes meet t's: the forward
@@ -1056,7 +1064,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         for_each_pred<BLOCK>(a, qt, st, lthr, n_long, band_list, &s_lcnt, [&](int32_t p, uint32_t o) {
             if (o == kUnplacedT) {
                 const uint32_t d = atomicAdd(&s_ndyn, 1u);
-                if (d < (uint32_t)kDynCap) {
+                if (d < a.dyn_cap) {
                     dpos[d] = (uint32_t)p;
                     return;
                 }
@@ -1071,7 +1079,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         });
         __syncthreads();
         uint32_t nstat = s_nstat;
-        const int ndyn = (int)min(s_ndyn, (uint32_t)kDynCap);
+        const int ndyn = (int)min(s_ndyn, a.dyn_cap);
         if (nstat > (uint32_t)stat_cap) {
             // more predecessors than the workgroup's buffer: wait for the late
             // ones, take a pool slot, collect every predecessor's range there
@@ -1274,8 +1282,8 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 if (lane == 0) agent_store(a.off + qt, x);
             };
             if (wid == 0) {
-                if (ndyn <= kWave) wave0(std::integral_constant<int, 1>{});
-                else if (ndyn <= 4 * kWave) wave0(std::integral_constant<int, 4>{});
+                if (ndyn <= kWave && a.min_late_k <= 1) wave0(std::integral_constant<int, 1>{});
+                else if (ndyn <= 4 * kWave && a.min_late_k <= 4) wave0(std::integral_constant<int, 4>{});
                 else wave0(std::integral_constant<int, 8>{});
             }
             __syncthreads();
@@ -1503,7 +1511,17 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
                  status,
                  policy == MP_BEST_FIT ? 1 : 0,
                  xbase,
-                 L.xcap};
+                 L.xcap,
+                 (uint32_t)kDynCap,
+                 1};
+    // MEMOPLAN_DEBUG_WAIT=wide: every wait holds eight late predecessors a
+    // lane; =tight: besides, the late list holds 8, so tensors with more wait
+    // for the rest during the collection (and report MP_EDEVICE, the
+    // condition that path exists for).  Both keep every offset exact.
+    if (const char* dbg = getenv("MEMOPLAN_DEBUG_WAIT")) {
+        if (!strcmp(dbg, "wide") || !strcmp(dbg, "tight")) pa.min_late_k = 8;
+        if (!strcmp(dbg, "tight")) pa.dyn_cap = 8;
+    }
     hipLaunchKernelGGL(t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, pa);
     WideArgs wa{su64, reach, alt ? vals1 : vals0, llist, off64,
                 reinterpret_cast<uint64_t*>(w + L.run_keys), stat_cap_of(n) / 4, pool, n, fl,

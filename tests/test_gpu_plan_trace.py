@@ -117,6 +117,35 @@ def test_ranking1m():
     assert _sha(off) == exp["offsets_sha256"]
 
 
+def test_debug_wait_paths(monkeypatch):
+    """MEMOPLAN_DEBUG_WAIT drives the late-predecessor paths the schedule
+    rarely reaches: "wide" holds eight late predecessors a lane in every
+    wait, "tight" caps the late list at 8 so that tensors with more wait for
+    the rest during their collection (reporting MP_EDEVICE).  Offsets stay
+    exact either way."""
+    binding = need_gpu()
+    t = tg.decode100k()
+    exp = _expected("decode100k")
+    monkeypatch.setenv("MEMOPLAN_DEBUG_WAIT", "wide")
+    print("case decode100k, widest wait", flush=True)
+    off, peak = _plan(binding, t)
+    assert peak == exp["peak"] and _sha(off) == exp["offsets_sha256"]
+    rng = np.random.default_rng(303)
+    n = 3000
+    full = tg.Trace(64 * rng.integers(1, 200, n), np.zeros(n, np.int32), np.full(n, 3, np.int32), 4)
+    print("case full overlap, widest wait", flush=True)
+    _check(binding, full)
+    monkeypatch.setenv("MEMOPLAN_DEBUG_WAIT", "tight")
+    for name, tr in [("full overlap", full),
+                     ("random", tg.random_trace(rng, 5000, 600, max_len=40, sorted_first=True))]:
+        print(f"case {name}, late list of 8", flush=True)
+        st = binding.new_status()
+        off, peak = _plan(binding, tr, check=False, status=st)
+        eo, ep = oracle.plan_trace(tr.size, tr.first, tr.last, tr.num_ops)
+        assert np.array_equal(off, eo) and peak == ep
+        assert int(st.item()) == binding.MP_EDEVICE
+
+
 def test_status_codes_and_empty():
     binding = need_gpu()
     off, peak = _plan(binding, tg.Trace(np.zeros(0, np.int64), np.zeros(0, np.int32),
