@@ -123,11 +123,12 @@ int64_t mp_batch_pair_capacity(int64_t max_trace_len);
  * (131072, or 32768 with 64-bit counts) waits until all of them are placed,
  * takes one of two shared buffers of n ranges and is fitted there.
  * Tensors need not be sorted by first.
- * Debug: the environment variable MEMOPLAN_DEBUG_WAIT, read on each call,
- * set to "wide" makes every wait for late predecessors take its widest form;
- * "tight" besides caps the late list at 8, so tensors with more wait during
- * their collection and the call reports MP_EDEVICE.  Offsets are exact
- * either way; both only exercise paths the schedule rarely reaches. */
+ * Test build: compiled with MP_DEBUG_WAIT (libmemoplan_dbgwait.so), this
+ * call reads the environment variable MEMOPLAN_DEBUG_WAIT on each call; "wide"
+ * makes every wait for late predecessors take its widest form, "tight"
+ * besides caps the late list at 8, so tensors with more wait during their
+ * collection and the call reports MP_EDEVICE.  Offsets are exact either way;
+ * both only exercise paths the schedule rarely reaches. */
 int32_t mp_plan_trace(const int64_t* size, const int32_t* first, const int32_t* last, int64_t n,
                       int32_t num_ops, int32_t policy, int64_t* offset_out, int64_t* peak_out,
                       void* workspace, size_t workspace_bytes, int32_t* status_out,

@@ -13,6 +13,8 @@ import torch
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libmemoplan.so")
+# test build (MP_DEBUG_WAIT): mp_plan_trace honours MEMOPLAN_DEBUG_WAIT
+DBG_WAIT_LIB_PATH = os.path.join(PKG, "libmemoplan_dbgwait.so")
 
 MP_OK, MP_EINVAL, MP_ENOSPC, MP_EOVERFLOW, MP_EDEVICE = 0, -1, -2, -3, -4
 OP_LIVE_BYTES, OP_VALIDATE, OP_PLAN_TRACE, OP_VALIDATE_BATCH, OP_PLAN_BATCH = 1, 2, 3, 4, 5

@@ -1,4 +1,7 @@
-"""Build libmemoplan.so (HIP for gfx950) in-tree with hipcc."""
+"""Build libmemoplan.so (HIP for gfx950) in-tree with hipcc, and beside it
+libmemoplan_dbgwait.so: the same sources with MP_DEBUG_WAIT, a test build
+whose single-trace planner takes its rarely reached late-predecessor paths on
+request (MEMOPLAN_DEBUG_WAIT).  The two compile in parallel."""
 from __future__ import annotations
 
 import glob
@@ -11,6 +14,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libmemoplan.so")
+DBG_WAIT_LIB_PATH = os.path.join(PKG, "libmemoplan_dbgwait.so")
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
@@ -26,12 +30,18 @@ def sources():
 
 def build(verbose: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
-    tmp = LIB_PATH + ".tmp"
-    cmd = [hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-o", tmp, *sources()]
-    if verbose:
-        print(" ".join(cmd), file=sys.stderr)
-    subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB_PATH)
+    jobs = []
+    for out, extra in ((LIB_PATH, []), (DBG_WAIT_LIB_PATH, ["-DMP_DEBUG_WAIT"])):
+        cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, "-o", out + ".tmp",
+               *sources()]
+        if verbose:
+            print(" ".join(cmd), file=sys.stderr)
+        jobs.append((out, subprocess.Popen(cmd)))
+    failed = [out for out, p in jobs if p.wait() != 0]
+    if failed:
+        raise subprocess.CalledProcessError(1, f"hipcc ({', '.join(map(os.path.basename, failed))})")
+    for out, _ in jobs:
+        os.replace(out + ".tmp", out)
     return LIB_PATH
 
 

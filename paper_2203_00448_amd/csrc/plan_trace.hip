@@ -28,10 +28,11 @@
 //              block whose XCD takes it once a running workgroup there
 //              finishes, so the schedule cannot deadlock.
 //   output     offsets (scaled back to bytes) and the peak.
+#include <type_traits>
+#ifdef MP_DEBUG_WAIT
 #include <stdlib.h>
 #include <string.h>
-
-#include <type_traits>
+#endif
 
 #include "internal.hpp"
 #include "mp_device.hpp"
@@ -578,14 +579,11 @@ struct PlaceArgs {
     int64_t n;
     TFlags* fl;
     int32_t* status;
-    int32_t best;     // fit policy: 0 lowest gap, 1 tightest gap
+    // fit policy: 0 lowest gap, 1 tightest gap (a build with MP_DEBUG_WAIT
+    // also reads bits 8 and 9: a late list of 8; the widest wait)
+    int32_t best;
     uint32_t* xbase;  // kXcdGroups x xcap claimed blocks (+1), zero at the launch
     int64_t xcap;
-    // debug (MEMOPLAN_DEBUG_WAIT): late predecessors held before the
-    // collection waits itself (kDynCap normally), and the fewest held a lane
-    // in the wait (1 normally; 8 takes the widest form for every tensor)
-    uint32_t dyn_cap;
-    int32_t min_late_k;
 };
 
 // Visit the positions ranked before t whose lifetimes meet t's: the forward
@@ -1033,6 +1031,17 @@ __global__ __launch_bounds__(BLOCK) void t_place_wide_kernel(WideArgs a) {
 
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
+#ifdef MP_DEBUG_WAIT
+    // test build (MEMOPLAN_DEBUG_WAIT bits of a.best): 0x200 every wait takes
+    // its widest form; 0x100 besides the late list holds 8
+#define T_DYN_CAP ((a.best & 0x100) ? 8u : (uint32_t)kDynCap)
+#define T_BEST (a.best & 1)
+#define T_WIDEST_WAIT ((a.best & 0x200) != 0)
+#else
+#define T_DYN_CAP ((uint32_t)kDynCap)
+#define T_BEST a.best
+#define T_WIDEST_WAIT false
+#endif
     __shared__ uint64_t skeys[kRunCap];  // placed predecessors (one run)
     __shared__ uint64_t dkeys[kDynCap];  // predecessors placed after t was examined
     __shared__ uint32_t dpos[kDynCap];
@@ -1064,7 +1073,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         for_each_pred<BLOCK>(a, qt, st, lthr, n_long, band_list, &s_lcnt, [&](int32_t p, uint32_t o) {
             if (o == kUnplacedT) {
                 const uint32_t d = atomicAdd(&s_ndyn, 1u);
-                if (d < a.dyn_cap) {
+                if (d < T_DYN_CAP) {
                     dpos[d] = (uint32_t)p;
                     return;
                 }
@@ -1079,7 +1088,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         });
         __syncthreads();
         uint32_t nstat = s_nstat;
-        const int ndyn = (int)min(s_ndyn, a.dyn_cap);
+        const int ndyn = (int)min(s_ndyn, T_DYN_CAP);
         if (nstat > (uint32_t)stat_cap) {
             // more predecessors than the workgroup's buffer: wait for the late
             // ones, take a pool slot, collect every predecessor's range there
@@ -1098,7 +1107,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 gr.ke[k] = (uint64_t)o + a.su[p];
             });
             __syncthreads();
-            const uint64_t x = fit_general<BLOCK>(gr, s_nstat, st, a.best != 0, skeys,
+            const uint64_t x = fit_general<BLOCK>(gr, s_nstat, st, T_BEST != 0, skeys,
                                                   skeys + kGRun, scratch64);
             pool_release(a.fl, slot);
             if (threadIdx.x == 0) agent_store(a.off + qt, (uint32_t)x);
@@ -1136,7 +1145,7 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         // highest end among the late ranges overlapping [c, c + st) until
         // none does, and the first gap that still holds t gives the offset.
         // No workgroup barrier lies between the last wait and the publish.
-        if (!a.best && nruns <= 1) {
+        if (!T_BEST && nruns <= 1) {
             const int m = (int)nstat, words = (m + 63) >> 6;
             const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
             for (int w = wid; w < words; w += BLOCK / kWave) {
@@ -1282,8 +1291,9 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                 if (lane == 0) agent_store(a.off + qt, x);
             };
             if (wid == 0) {
-                if (ndyn <= kWave && a.min_late_k <= 1) wave0(std::integral_constant<int, 1>{});
-                else if (ndyn <= 4 * kWave && a.min_late_k <= 4) wave0(std::integral_constant<int, 4>{});
+                if (T_WIDEST_WAIT) wave0(std::integral_constant<int, 8>{});
+                else if (ndyn <= kWave) wave0(std::integral_constant<int, 1>{});
+                else if (ndyn <= 4 * kWave) wave0(std::integral_constant<int, 4>{});
                 else wave0(std::integral_constant<int, 8>{});
             }
             __syncthreads();
@@ -1311,12 +1321,16 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
         }
         if (ndyn) runs[nr++] = RunRef{dkeys, ndyn};
         uint32_t x;
-        if (a.best) x = best_fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch64);
+        if (T_BEST) x = best_fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch64);
         else x = nr ? fit_runs<BLOCK, kScratchRuns + 1>(runs, nr, st, scratch) : 0u;
         if (threadIdx.x == 0) agent_store(a.off + qt, x);
         __syncthreads();
     }
 }
+
+#undef T_DYN_CAP
+#undef T_BEST
+#undef T_WIDEST_WAIT
 
 __global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restrict__ off,
                                                        const uint32_t* __restrict__ su,
@@ -1511,17 +1525,17 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
                  status,
                  policy == MP_BEST_FIT ? 1 : 0,
                  xbase,
-                 L.xcap,
-                 (uint32_t)kDynCap,
-                 1};
-    // MEMOPLAN_DEBUG_WAIT=wide: every wait holds eight late predecessors a
-    // lane; =tight: besides, the late list holds 8, so tensors with more wait
-    // for the rest during the collection (and report MP_EDEVICE, the
-    // condition that path exists for).  Both keep every offset exact.
+                 L.xcap};
+#ifdef MP_DEBUG_WAIT
+    // test build: MEMOPLAN_DEBUG_WAIT=wide makes every wait hold eight late
+    // predecessors a lane; =tight besides caps the late list at 8, so tensors
+    // with more wait for the rest during the collection (and report
+    // MP_EDEVICE, the condition that path exists for).  Offsets stay exact.
     if (const char* dbg = getenv("MEMOPLAN_DEBUG_WAIT")) {
-        if (!strcmp(dbg, "wide") || !strcmp(dbg, "tight")) pa.min_late_k = 8;
-        if (!strcmp(dbg, "tight")) pa.dyn_cap = 8;
+        if (!strcmp(dbg, "wide")) pa.best |= 0x200;
+        if (!strcmp(dbg, "tight")) pa.best |= 0x300;
     }
+#endif
     hipLaunchKernelGGL(t_place_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, pa);
     WideArgs wa{su64, reach, alt ? vals1 : vals0, llist, off64,
                 reinterpret_cast<uint64_t*>(w + L.run_keys), stat_cap_of(n) / 4, pool, n, fl,

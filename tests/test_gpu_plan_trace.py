@@ -118,12 +118,22 @@ def test_ranking1m():
 
 
 def test_debug_wait_paths(monkeypatch):
-    """MEMOPLAN_DEBUG_WAIT drives the late-predecessor paths the schedule
-    rarely reaches: "wide" holds eight late predecessors a lane in every
-    wait, "tight" caps the late list at 8 so that tensors with more wait for
-    the rest during their collection (reporting MP_EDEVICE).  Offsets stay
-    exact either way."""
+    """The test build of the library (MP_DEBUG_WAIT) with MEMOPLAN_DEBUG_WAIT
+    drives the late-predecessor paths the schedule rarely reaches: "wide"
+    holds eight late predecessors a lane in every wait, "tight" caps the late
+    list at 8 so that tensors with more wait for the rest during their
+    collection (reporting MP_EDEVICE).  Offsets stay exact either way."""
     binding = need_gpu()
+    saved = binding._lib
+    binding._lib = None
+    binding.load_library(binding.DBG_WAIT_LIB_PATH)
+    try:
+        _debug_wait_cases(binding, monkeypatch)
+    finally:
+        binding._lib = saved
+
+
+def _debug_wait_cases(binding, monkeypatch):
     t = tg.decode100k()
     exp = _expected("decode100k")
     monkeypatch.setenv("MEMOPLAN_DEBUG_WAIT", "wide")
