@@ -623,8 +623,9 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
             for (int k = 0; k < ITEMS; ++k) {
                 const int q = tid + k * BLOCK;
                 if (q < m) {
-                    const int32_t f = lf[q], f1 = q + 1 < m ? lf[q + 1] : f_hi + 1;
-                    for (int32_t v = max(f, f_lo); v < f1 && v <= f_hi; ++v) tab[v - f_lo] = (uint32_t)(q + 1);
+                    const int64_t f = lf[q], f1 = q + 1 < m ? lf[q + 1] : (int64_t)f_hi + 1;
+                    for (int64_t v = f > f_lo ? f : f_lo; v < f1 && v <= f_hi; ++v)
+                        tab[v - f_lo] = (uint32_t)(q + 1);
                 }
             }
             __syncthreads();
