@@ -663,38 +663,38 @@ __device__ __forceinline__ void walk_preds(const int32_t* reach, const SZ* su, c
                 finish(pp, ok);
             }
         } else {
-        for (int32_t s0 = qt + 1; s0 < rt; s0 += kBandSeg) {
-            const int32_t s1 = rt - s0 > kBandSeg ? s0 + kBandSeg : rt;
-            if (threadIdx.x == 0) *list_n = 0;
-            __syncthreads();
-            for (int32_t g0 = (s0 & ~3) + 4 * (int32_t)threadIdx.x; g0 < s1;
-                 g0 += kStride * kBandVec) {
-                uint32_t sz[kBandVec][4];
-#pragma unroll
-                for (int k = 0; k < kBandVec; ++k) load4(su, g0 + kStride * k, s1, sz[k]);
-#pragma unroll
-                for (int k = 0; k < kBandVec; ++k)
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int32_t p = g0 + kStride * k + e;
-                        if (p >= s0 && p < s1 && sz[k][e] > st) list[atomicAdd(list_n, 1u)] = (uint32_t)p;
-                    }
-            }
-            __syncthreads();
-            const uint32_t m = *list_n;
-            for (uint32_t i0 = threadIdx.x; i0 < m; i0 += BLOCK * kBandLoads) {
-                int32_t pp[kBandLoads];
-                bool ok[kBandLoads];
-#pragma unroll
-                for (int u = 0; u < kBandLoads; ++u) {
-                    const uint32_t i = i0 + (uint32_t)(u * BLOCK);
-                    ok[u] = i < m;
-                    pp[u] = ok[u] ? (int32_t)list[i] : 0;
+            for (int32_t s0 = qt + 1; s0 < rt; s0 += kBandSeg) {
+                const int32_t s1 = rt - s0 > kBandSeg ? s0 + kBandSeg : rt;
+                if (threadIdx.x == 0) *list_n = 0;
+                __syncthreads();
+                for (int32_t g0 = (s0 & ~3) + 4 * (int32_t)threadIdx.x; g0 < s1;
+                     g0 += kStride * kBandVec) {
+                    uint32_t sz[kBandVec][4];
+    #pragma unroll
+                    for (int k = 0; k < kBandVec; ++k) load4(su, g0 + kStride * k, s1, sz[k]);
+    #pragma unroll
+                    for (int k = 0; k < kBandVec; ++k)
+    #pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            const int32_t p = g0 + kStride * k + e;
+                            if (p >= s0 && p < s1 && sz[k][e] > st) list[atomicAdd(list_n, 1u)] = (uint32_t)p;
+                        }
                 }
-                finish(pp, ok);
+                __syncthreads();
+                const uint32_t m = *list_n;
+                for (uint32_t i0 = threadIdx.x; i0 < m; i0 += BLOCK * kBandLoads) {
+                    int32_t pp[kBandLoads];
+                    bool ok[kBandLoads];
+    #pragma unroll
+                    for (int u = 0; u < kBandLoads; ++u) {
+                        const uint32_t i = i0 + (uint32_t)(u * BLOCK);
+                        ok[u] = i < m;
+                        pp[u] = ok[u] ? (int32_t)list[i] : 0;
+                    }
+                    finish(pp, ok);
+                }
+                __syncthreads();  // the list is refilled or handed back
             }
-            __syncthreads();  // the list is refilled or handed back
-        }
         }
         // backward window of short bands: ranked before t iff at least as large
         const int32_t w0 = (int32_t)(lo > 0 ? lo : 0);
