@@ -548,6 +548,7 @@ __global__ void v_unpack_kernel(const uint64_t* __restrict__ keys, const int64_t
 // and the write pass enumerate the same pairs in (i, j) order.
 
 constexpr int kVbBlock = 512;
+constexpr int64_t kVbFuseMax = 4096;  // traces up to which the write pass sums the counts itself
 
 // write == 0: segcnt[b] = conflicts of trace b.
 // write == 1: segcnt holds exclusive starts (segcnt[n_seg] = total); the
@@ -557,9 +558,11 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
     const int64_t* __restrict__ begin, int64_t n_seg, const int64_t* __restrict__ size,
     const int32_t* __restrict__ first, const int32_t* __restrict__ last,
     const int64_t* __restrict__ off, int64_t n, int32_t cap_n, int64_t* __restrict__ segcnt,
-    int write, int64_t* __restrict__ pairs, int64_t cap, int32_t* __restrict__ status) {
+    int write, int64_t* __restrict__ pairs, int64_t cap, int64_t* __restrict__ n_out,
+    int32_t* __restrict__ status) {
     extern __shared__ __align__(16) unsigned char smem[];
     __shared__ uint32_t scratch[BLOCK / kWave];
+    __shared__ uint64_t scratch64[BLOCK / kWave];
     // LDS: first[N] i32 (reach search) -> then off[N], size[N] i64 over it;
     // band lengths -> starts [N+1] u32 after them.  20 bytes per tensor, so
     // four workgroups of 2000-tensor traces share a CU.
@@ -570,6 +573,20 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
     uint32_t* band = reinterpret_cast<uint32_t*>(smem + 16 * N);
     const int tid = threadIdx.x;
     for (int64_t b = blockIdx.x; b < n_seg; b += gridDim.x) {
+        // write 2 (short batches): the counts are as the count pass left
+        // them; this trace's first pair goes after the sum of those before
+        // it, and the last trace's workgroup reports the total
+        int64_t before = 0;
+        if (write == 2) {
+            uint64_t part = 0;
+            for (int64_t i = tid; i < b; i += BLOCK) part += (uint64_t)segcnt[i];
+            before = (int64_t)block_reduce<BLOCK>(part, OpAdd<uint64_t>(), scratch64);
+            if (b == n_seg - 1 && tid == 0) {
+                const int64_t total = before + segcnt[b];
+                *n_out = total;
+                if (total > cap) raise_status(status, MP_ENOSPC);
+            }
+        }
         const int64_t lo = begin[b], hi = begin[b + 1];
         if (lo < 0 || hi < lo || hi > n || (b == 0 && lo != 0) || (b == n_seg - 1 && hi != n) ||
             hi - lo > cap_n) {
@@ -580,9 +597,12 @@ __global__ __launch_bounds__(BLOCK, ITEMS <= 4 ? 8 : 4) void vb_kernel(
             continue;
         }
         int64_t base = 0;
-        if (write) {
+        if (write == 1) {
             base = segcnt[b];
             if (segcnt[b + 1] == base || base >= cap) continue;  // nothing to write here
+        } else if (write == 2) {
+            base = before;
+            if (segcnt[b] == 0 || base >= cap) continue;
         }
         const int m = (int)(hi - lo);
         // first and last of every item are requested before any is used
@@ -794,7 +814,7 @@ template <int ITEMS>
 hipError_t launch_vb(int write, const int64_t* begin, int64_t n_seg, const int64_t* size,
                      const int32_t* first, const int32_t* last, const int64_t* off, int64_t n,
                      int32_t cap_n, int64_t* segcnt, int64_t* pairs, int64_t cap,
-                     int32_t* status, hipStream_t st) {
+                     int64_t* n_out, int32_t* status, hipStream_t st) {
     auto kern = vb_kernel<kVbBlock, ITEMS>;
     const size_t lds = 20 * (size_t)cap_n + 8;
     hipError_t e = hipFuncSetAttribute((const void*)kern,
@@ -802,19 +822,20 @@ hipError_t launch_vb(int write, const int64_t* begin, int64_t n_seg, const int64
     if (e != hipSuccess) return e;
     const unsigned grid = (unsigned)(n_seg < 65535 ? n_seg : 65535);
     hipLaunchKernelGGL(kern, dim3(grid), dim3(kVbBlock), lds, st, begin, n_seg, size, first, last,
-                       off, n, cap_n, segcnt, write, pairs, cap, status);
+                       off, n, cap_n, segcnt, write, pairs, cap, n_out, status);
     return hipGetLastError();
 }
 
 hipError_t launch_vb_any(int write, int items, const int64_t* begin, int64_t n_seg,
                          const int64_t* size, const int32_t* first, const int32_t* last,
                          const int64_t* off, int64_t n, int32_t cap_n, int64_t* segcnt,
-                         int64_t* pairs, int64_t cap, int32_t* status, hipStream_t st) {
+                         int64_t* pairs, int64_t cap, int64_t* n_out, int32_t* status,
+                         hipStream_t st) {
     switch (items) {
-        case 1: return launch_vb<1>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
-        case 2: return launch_vb<2>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
-        case 4: return launch_vb<4>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
-        case 8: return launch_vb<8>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, status, st);
+        case 1: return launch_vb<1>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, n_out, status, st);
+        case 2: return launch_vb<2>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, n_out, status, st);
+        case 4: return launch_vb<4>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, n_out, status, st);
+        case 8: return launch_vb<8>(write, begin, n_seg, size, first, last, off, n, cap_n, segcnt, pairs, cap, n_out, status, st);
         default: return hipErrorInvalidValue;
     }
 }
@@ -882,13 +903,20 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
         int items = 1;
         while (items * kVbBlock < max_seg) items <<= 1;
         hipError_t e = launch_vb_any(0, items, begin, n_seg, size, first, last, off, n,
-                                     (int32_t)max_seg, segcnt, pairs, cap, status, st);
+                                     (int32_t)max_seg, segcnt, pairs, cap, n_out, status, st);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(vb_scan_kernel, dim3(1), dim3(1024), 0, st, segcnt, n_seg, cap, n_out,
-                           status);
-        if (cap > 0)
-            e = launch_vb_any(1, items, begin, n_seg, size, first, last, off, n, (int32_t)max_seg,
-                              segcnt, pairs, cap, status, st);
+        if (n_seg <= kVbFuseMax) {
+            // short batches: each write-pass workgroup sums the counts before
+            // its trace (no scan launch); the last one reports the total
+            e = launch_vb_any(2, items, begin, n_seg, size, first, last, off, n, (int32_t)max_seg,
+                              segcnt, pairs, cap, n_out, status, st);
+        } else {
+            hipLaunchKernelGGL(vb_scan_kernel, dim3(1), dim3(1024), 0, st, segcnt, n_seg, cap,
+                               n_out, status);
+            if (cap > 0)
+                e = launch_vb_any(1, items, begin, n_seg, size, first, last, off, n,
+                                  (int32_t)max_seg, segcnt, pairs, cap, n_out, status, st);
+        }
         if (e != hipSuccess) return e;
         return hipGetLastError();
     }
