@@ -58,6 +58,12 @@ def test_random_traces():
         t = tg.random_trace(rng, n, T, max_len=int(rng.integers(1, T + 1)), sizes=alphabet,
                             sorted_first=(k % 2 == 0))
         _check(binding, t)
+    # ranks are handed out in blocks of 32 per XCD, one rank per workgroup:
+    # traces ending at and around a block, two blocks and the grid
+    print("case rank-block boundaries", flush=True)
+    for n in [31, 32, 33, 63, 64, 65, 255, 256, 257, 1025]:
+        t = tg.random_trace(rng, n, max(2, n // 3), max_len=8, sizes=[64, 192, 448])
+        _check(binding, t)
 
 
 def test_adversarial_shapes():
