@@ -1263,10 +1263,9 @@ __global__ __launch_bounds__(BLOCK) void t_place_kernel(PlaceArgs a) {
                             hit = hit || (lo_d[r] < x + st && x < hi_d[r]);
                         }
                     }
-                    if (!__ballot(got)) {
-                        __builtin_amdgcn_s_sleep(1);
-                        continue;
-                    }
+                    // no sleep between polls: each takes an agent-scope load's
+                    // round trip, and a sleep only delays the detection
+                    if (!__ballot(got)) continue;
                     if (ok && __ballot(hit)) ok = walk(xk, x);
                 }
                 // every late range is known
