@@ -144,3 +144,16 @@ def test_empty_batch_and_empty_traces():
     batch = tg.concat([])
     off, peak, lb = _gpu_batch(binding, batch, max_trace_len=0)
     assert off.shape == (0,) and peak.shape == (0,)
+
+
+@pytest.mark.skip(reason="a trace of this shape, passed by mp_plan_trace to the batched planner as a "
+                         "batch of one (a small-trace route since removed), ended in a GPU memory "
+                         "aperture violation in plan_batch_kernel<256, 1, false>; no cause was found "
+                         "by reading, so the case stays off the GPU until one is")
+def test_one_slot_unsorted_full_bound():
+    """An unsorted 255-tensor trace with 85 ops and lifetimes of up to 8 ops,
+    alone in a batch whose bound is its own length (one slot a thread)."""
+    binding = need_gpu()
+    rng = np.random.default_rng(300)
+    t = tg.random_trace(rng, 255, 85, max_len=8, sizes=[64, 192, 448])
+    _check(binding, tg.concat([t]), max_trace_len=255)
