@@ -71,6 +71,9 @@ struct TFlags {
     uint32_t shift, lthr, n_long, ticket;
     uint32_t xtick[kXcdGroups];  // slots taken per XCD (blocks of kTicketBlock ranks)
     uint32_t blocks;             // rank blocks claimed
+    // workgroups finished in ingest, reach and output (the last one of each
+    // takes the step that needs all of them)
+    uint32_t done_ingest, done_reach, done_output;
     uint32_t skip_narrow, skip_wide;  // nonzero: the 32-bit (64-bit) unit path does not run
     uint32_t pool[kPoolSlots];        // 1 while a workgroup holds the slot
     uint32_t hist[64];      // band lengths by bit width
@@ -105,16 +108,48 @@ __global__ void t_init_kernel(TFlags* fl) {
         fl->n_long = 0;
         fl->ticket = 0;
         fl->blocks = 0;
+        fl->done_ingest = 0;
+        fl->done_reach = 0;
+        fl->done_output = 0;
         fl->peak = 0;
     }
 }
 
+__device__ __forceinline__ uint32_t flag_load(const uint32_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ uint64_t flag_load64(const uint64_t* p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Unit shift, and the offset width: 32-bit counts of the unit while the
+// sizes sum to less than 2^32 - 1 units (every offset and end then fits
+// below the unplaced sentinel), 64-bit counts beyond.  Taken by the last
+// ingest workgroup, once every workgroup's totals are in.
+__device__ void unit_step(TFlags* fl) {
+    if (flag_load(&fl->abort)) return;
+    const uint64_t o = flag_load64(&fl->or_all);
+    const uint32_t sh = o ? (uint32_t)__builtin_ctzll(o) : 0u;
+    fl->shift = sh;
+    const uint32_t wide = (flag_load64(&fl->sum) >> sh) > 0xFFFFFFFEull ? 1u : 0u;
+    fl->wide = wide;
+    fl->skip_narrow = wide;
+    fl->skip_wide = 1u - wide;
+}
+
+// Checks and totals of the input; besides, the (first, id) pairs of the
+// position sort (used only when the input is not sorted by first) and the
+// zeroed rank-block table of the placement.
 __global__ __launch_bounds__(256) void t_ingest_kernel(const int64_t* __restrict__ size,
                                                        const int32_t* __restrict__ first,
                                                        const int32_t* __restrict__ last,
                                                        int64_t n, int32_t num_ops, TFlags* fl,
-                                                       int32_t* __restrict__ status) {
+                                                       int32_t* __restrict__ status,
+                                                       uint64_t* __restrict__ keys,
+                                                       uint32_t* __restrict__ vals,
+                                                       uint32_t* __restrict__ xbase, int64_t nx) {
     __shared__ uint64_t red[256 / kWave];
+    __shared__ uint32_t s_last;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     uint32_t bad = 0, unsorted = 0;
     uint64_t orv = 0, acc = 0;
@@ -127,7 +162,11 @@ __global__ __launch_bounds__(256) void t_ingest_kernel(const int64_t* __restrict
             acc = sat_add(acc, (uint64_t)s);
         }
         if (i + 1 < n && first[i + 1] < f) unsorted = 1;
+        keys[i] = (uint64_t)(uint32_t)f;
+        vals[i] = (uint32_t)i;
     }
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < nx; i += stride)
+        xbase[i] = 0;
     bad = block_reduce<256>(bad, OpOr<uint32_t>(), reinterpret_cast<uint32_t*>(red));
     unsorted = block_reduce<256>(unsorted, OpOr<uint32_t>(), reinterpret_cast<uint32_t*>(red));
     orv = block_reduce<256>(orv, OpOr<uint64_t>(), red);
@@ -148,56 +187,46 @@ __global__ __launch_bounds__(256) void t_ingest_kernel(const int64_t* __restrict
             raise_status(status, MP_EOVERFLOW);
             atomicOr(&fl->abort, 1u);
         }
+        __threadfence();
+        s_last = atomicAdd(&fl->done_ingest, 1u) == gridDim.x - 1 ? 1u : 0u;
+    }
+    __syncthreads();
+    if (s_last && threadIdx.x == 0) {
+        __threadfence();
+        unit_step(fl);
     }
 }
 
-// unit shift, and the offset width: 32-bit counts of the unit while the
-// sizes sum to less than 2^32 - 1 units (every offset and end then fits
-// below the unplaced sentinel), 64-bit counts beyond
-__global__ void t_unit_kernel(TFlags* fl) {
-    if (fl->abort) return;
-    const uint64_t o = fl->or_all;
-    const uint32_t sh = o ? (uint32_t)__builtin_ctzll(o) : 0u;
-    fl->shift = sh;
-    const uint32_t wide = (fl->sum >> sh) > 0xFFFFFFFEull ? 1u : 0u;
-    fl->wide = wide;
-    fl->skip_narrow = wide;
-    fl->skip_wide = 1u - wide;
-}
-
-__global__ void t_keys_first_kernel(const int32_t* __restrict__ first, int64_t n,
-                                    uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                    const TFlags* fl) {
-    if (!fl->unsorted || fl->abort) return;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
-        keys[i] = (uint64_t)(uint32_t)first[i];
-        vals[i] = (uint32_t)i;
-    }
-}
-
-// positions: size in units, first/last in (first, id) order, ids
-__global__ void t_positions_kernel(const uint32_t* __restrict__ perm,
+// positions: size in units, first/last in (first, id) order, ids; and the
+// rank-sort pairs (size descending; ties keep position order, the sort being
+// stable).  perm may be vals (the position sort's result): each thread reads
+// its own entry before writing it.
+__global__ void t_positions_kernel(const uint32_t* perm,
                                    const int64_t* __restrict__ size,
                                    const int32_t* __restrict__ first,
                                    const int32_t* __restrict__ last, int64_t n,
                                    uint32_t* __restrict__ su, int32_t* __restrict__ pf,
                                    int32_t* __restrict__ pl, uint32_t* __restrict__ pid,
                                    uint32_t* __restrict__ off, uint64_t* __restrict__ su64,
-                                   uint64_t* __restrict__ off64, const TFlags* fl) {
+                                   uint64_t* __restrict__ off64, uint64_t* __restrict__ keys,
+                                   uint32_t* vals, const TFlags* fl) {
     if (fl->abort) return;
     const bool uns = fl->unsorted != 0, wide = fl->wide != 0;
     const uint32_t sh = fl->shift;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
         const uint32_t i = uns ? perm[q] : (uint32_t)q;
+        const uint64_t units = (uint64_t)size[i] >> sh;
         if (wide) {
-            su64[q] = (uint64_t)size[i] >> sh;
+            su64[q] = units;
             off64[q] = kUnplaced64;
+            keys[q] = ~units;
         } else {
-            su[q] = (uint32_t)((uint64_t)size[i] >> sh);
+            su[q] = (uint32_t)units;
             off[q] = kUnplacedT;
+            keys[q] = (uint64_t)(0xFFFFFFFFu - (uint32_t)units);
         }
+        vals[q] = (uint32_t)q;
         if (uns) {
             pf[q] = first[i];
             pl[q] = last[i];
@@ -236,6 +265,7 @@ __global__ void t_reach_kernel(const int32_t* first, const int32_t* last, const 
     // device atomic per nonzero bin (one per position would serialize on the
     // few bins most bands fall in)
     __shared__ uint32_t h[33];
+    __shared__ uint32_t s_last;
     if (fl->abort) return;
     if (threadIdx.x < 33) h[threadIdx.x] = 0u;
     __syncthreads();
@@ -249,21 +279,26 @@ __global__ void t_reach_kernel(const int32_t* first, const int32_t* last, const 
     }
     __syncthreads();
     if (threadIdx.x < 33 && h[threadIdx.x]) atomicAdd(&fl->hist[threadIdx.x], h[threadIdx.x]);
-}
-
-// threshold: smallest 2^b with at most kLongMax bands longer than it
-__global__ void t_threshold_kernel(TFlags* fl) {
-    if (fl->abort) return;
-    uint32_t above = 0;
-    int b = 33;
-    // bands of bit width w lie in [2^(w-1), 2^w); count from the top down
-    for (int w = 32; w >= 0; --w) {
-        if (above + fl->hist[w] > (uint32_t)kLongMax) break;
-        above += fl->hist[w];
-        b = w;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = atomicAdd(&fl->done_reach, 1u) == gridDim.x - 1 ? 1u : 0u;
+    __syncthreads();
+    if (s_last && threadIdx.x == 0) {
+        // the last workgroup, all histograms in: the threshold is the
+        // smallest 2^b with at most kLongMax bands longer than it
+        __threadfence();
+        uint32_t above = 0;
+        int b = 33;
+        // bands of bit width w lie in [2^(w-1), 2^w); count from the top down
+        for (int w = 32; w >= 0; --w) {
+            const uint32_t c = flag_load(&fl->hist[w]);
+            if (above + c > (uint32_t)kLongMax) break;
+            above += c;
+            b = w;
+        }
+        // bands with bit width >= b are long: band >= 2^(b-1)
+        fl->lthr = (b >= 33) ? 0xFFFFFFFFu : (b <= 1 ? 0u : (1u << (b - 1)) - 1u);
     }
-    // bands with bit width >= b are long: band >= 2^(b-1)
-    fl->lthr = (b >= 33) ? 0xFFFFFFFFu : (b <= 1 ? 0u : (1u << (b - 1)) - 1u);
 }
 
 __global__ void t_long_flags_kernel(const int32_t* __restrict__ reach, int64_t n,
@@ -284,20 +319,6 @@ __global__ void t_long_list_kernel(const int32_t* __restrict__ reach,
     for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
         if ((uint32_t)(reach[q] - q - 1) > lthr) long_list[pos[q]] = (int32_t)q;
         if (q == n - 1) fl->n_long = (uint32_t)(pos[q] + (((uint32_t)(reach[q] - q - 1) > lthr) ? 1 : 0));
-    }
-}
-
-__global__ void t_rank_keys_kernel(const uint32_t* __restrict__ su,
-                                   const uint64_t* __restrict__ su64, int64_t n,
-                                   uint64_t* __restrict__ keys, uint32_t* __restrict__ vals,
-                                   const TFlags* fl) {
-    if (fl->abort) return;
-    const bool wide = fl->wide != 0;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; q < n; q += stride) {
-        // size descending; ties keep position order (the sort is stable)
-        keys[q] = wide ? ~su64[q] : (uint64_t)(0xFFFFFFFFu - su[q]);
-        vals[q] = (uint32_t)q;
     }
 }
 
@@ -1337,9 +1358,13 @@ __global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restric
                                                        const uint64_t* __restrict__ su64,
                                                        const uint32_t* __restrict__ pid, int64_t n,
                                                        int64_t* __restrict__ offset_out,
-                                                       TFlags* fl) {
+                                                       TFlags* fl, int64_t* __restrict__ peak_out) {
     __shared__ uint64_t red[256 / kWave];
-    if (fl->abort) return;
+    __shared__ uint32_t s_last;
+    if (fl->abort) {
+        if (blockIdx.x == 0 && threadIdx.x == 0) *peak_out = (int64_t)fl->peak;
+        return;
+    }
     const uint32_t sh = fl->shift;
     const bool wide = fl->wide != 0;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
@@ -1351,16 +1376,20 @@ __global__ __launch_bounds__(256) void t_output_kernel(const uint32_t* __restric
         pk = pk > e ? pk : e;
     }
     pk = block_reduce<256>(pk, OpMax<uint64_t>(), red);
-    if (threadIdx.x == 0 && pk)
-        atomicMax(reinterpret_cast<unsigned long long*>(&fl->peak), (unsigned long long)pk);
+    if (threadIdx.x == 0) {
+        if (pk) atomicMax(reinterpret_cast<unsigned long long*>(&fl->peak), (unsigned long long)pk);
+        __threadfence();
+        s_last = atomicAdd(&fl->done_output, 1u) == gridDim.x - 1 ? 1u : 0u;
+    }
+    __syncthreads();
+    if (s_last && threadIdx.x == 0) {  // every workgroup's maximum is in
+        __threadfence();
+        *peak_out = (int64_t)flag_load64(&fl->peak);
+    }
 }
 
 __global__ void t_peak_kernel(const TFlags* fl, int64_t* peak_out) { *peak_out = (int64_t)fl->peak; }
 
-__global__ __launch_bounds__(256) void t_clear_kernel(uint32_t* __restrict__ p, int64_t count) {
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) p[i] = 0;
-}
 
 struct TLayout {
     size_t flags, su, pf, pl, pid, off, su64, off64, reach, keys0, vals0, keys1, vals1, radix,
@@ -1474,22 +1503,21 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
         return hipGetLastError();
     }
     const unsigned g = grid_n(n, 256);
+    uint32_t* xbase = reinterpret_cast<uint32_t*>(w + L.xbase);
+    const int64_t nx = (int64_t)kXcdGroups * L.xcap;
     hipLaunchKernelGGL(t_ingest_kernel, dim3(g), dim3(256), 0, st, size, first, last, n, num_ops,
-                       fl, status);
-    hipLaunchKernelGGL(t_unit_kernel, dim3(1), dim3(1), 0, st, fl);
+                       fl, status, keys0, vals0, xbase, nx);
     // position order (unsorted inputs only)
-    hipLaunchKernelGGL(t_keys_first_kernel, dim3(g), dim3(256), 0, st, first, n, keys0, vals0,
-                       (const TFlags*)fl);
     bool alt = false;
     hipError_t e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32, rws, &alt, st,
                                     &fl->sorted);
     if (e != hipSuccess) return e;
+    // positions, and the rank-sort pairs in (keys0, vals0)
     hipLaunchKernelGGL(t_positions_kernel, dim3(g), dim3(256), 0, st,
                        (const uint32_t*)(alt ? vals1 : vals0), size, first, last, n, su, pf, pl,
-                       pid, off, su64, off64, (const TFlags*)fl);
+                       pid, off, su64, off64, keys0, vals0, (const TFlags*)fl);
     hipLaunchKernelGGL(t_reach_kernel, dim3(g), dim3(256), 0, st, first, last, (const int32_t*)pf,
                        (const int32_t*)pl, (const uint32_t*)pid, n, reach, fl);
-    hipLaunchKernelGGL(t_threshold_kernel, dim3(1), dim3(1), 0, st, fl);
     hipLaunchKernelGGL(t_long_flags_kernel, dim3(g), dim3(256), 0, st, (const int32_t*)reach, n,
                        lflag, (const TFlags*)fl);
     e = device_scan_i64(lflag, n, false, lpartial, nullptr, st, &fl->abort);
@@ -1499,8 +1527,6 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     // rank order: size descending, stable over positions -- 32-bit keys, or
     // 64-bit ones when the unit counts are (the other sort is skipped on the
     // device; both take an even number of passes, so the result is in keys0)
-    hipLaunchKernelGGL(t_rank_keys_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)su,
-                       (const uint64_t*)su64, n, keys0, vals0, (const TFlags*)fl);
     e = radix_sort_pairs(keys0, vals0, keys1, vals1, n, 0, 32, rws, &alt, st, &fl->skip_narrow);
     if (e != hipSuccess) return e;
     bool alt64 = false;
@@ -1508,9 +1534,6 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     if (e != hipSuccess) return e;
     if (alt != alt64) return hipErrorInvalidValue;  // both sorts end in the same buffer
     uint64_t* pool = reinterpret_cast<uint64_t*>(w + L.pool);
-    uint32_t* xbase = reinterpret_cast<uint32_t*>(w + L.xbase);
-    const int64_t nx = (int64_t)kXcdGroups * L.xcap;
-    hipLaunchKernelGGL(t_clear_kernel, dim3(grid_n(nx, 256)), dim3(256), 0, st, xbase, nx);
     PlaceArgs pa{su,
                  reach,
                  alt ? vals1 : vals0,
@@ -1542,8 +1565,7 @@ hipError_t launch_plan_trace(const int64_t* size, const int32_t* first, const in
     hipLaunchKernelGGL(t_place_wide_kernel<kTBlock>, dim3(L.grid), dim3(kTBlock), 0, st, wa);
     hipLaunchKernelGGL(t_output_kernel, dim3(g), dim3(256), 0, st, (const uint32_t*)off,
                        (const uint32_t*)su, (const uint64_t*)off64, (const uint64_t*)su64,
-                       (const uint32_t*)pid, n, offset_out, fl);
-    hipLaunchKernelGGL(t_peak_kernel, dim3(1), dim3(1), 0, st, (const TFlags*)fl, peak_out);
+                       (const uint32_t*)pid, n, offset_out, fl, peak_out);
     return hipGetLastError();
 }
 

@@ -2,7 +2,8 @@
 // per-tile digit counts -> one device-wide exclusive scan in digit-major
 // order -> stable scatter.  Inside a tile, elements are taken in rounds of
 // 256 consecutive elements; a wave ranks equal digits with eight ballots and
-// waves are ordered through per-(wave, digit) counts in LDS.
+// waves are ordered through per-(wave, digit) counts in LDS.  Up to 4,096
+// pairs are sorted by one workgroup in LDS instead, in one launch.
 #include "internal.hpp"
 #include "mp_device.hpp"
 
@@ -94,6 +95,57 @@ __global__ __launch_bounds__(kRadixBlock) void radix_scatter_kernel(
     }
 }
 
+// One workgroup sorts up to kSmallSort pairs in LDS with a bitonic network
+// over (the key's digit bits, input position).  Position breaks every tie, so
+// the permutation is the one the stable digit passes produce; the pairs are
+// written to the buffer those passes would end in (possibly the input: every
+// input is in LDS before anything is written).  Elements [m, P) are padding
+// that sorts last (all-ones key, position >= m).
+constexpr int kSmallSort = 4096;
+constexpr int kSmallSortThreads = 1024;
+
+__global__ __launch_bounds__(kSmallSortThreads) void small_sort_kernel(
+    const uint64_t* kin, const uint32_t* vin, uint64_t* kout, uint32_t* vout, int64_t n,
+    int shift, uint64_t mask, int P, const uint32_t* skip, const int64_t* n_live) {
+    __shared__ uint64_t sk[kSmallSort];  // full keys, moved by the network
+    __shared__ uint16_t si[kSmallSort];  // input positions, moved with them
+    __shared__ uint32_t sv[kSmallSort];  // values, by input position
+    if (skip && *skip) return;
+    int64_t m = n;
+    if (n_live) m = min(m, *n_live);
+    if (m < 0) m = 0;
+    const int T = (int)blockDim.x, tid = (int)threadIdx.x;
+    for (int i = tid; i < P; i += T) {
+        const bool in = i < m;
+        sk[i] = in ? kin[i] : ~0ull;
+        si[i] = (uint16_t)i;
+        if (vin) sv[i] = in ? vin[i] : 0u;
+    }
+    __syncthreads();
+    for (int k = 2; k <= P; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int t = tid; t < P / 2; t += T) {
+                const int a = 2 * t - (t & (j - 1)), b = a + j;  // bit j of a clear
+                const uint64_t ka = sk[a], kb = sk[b];
+                const uint16_t ia = si[a], ib = si[b];
+                const uint64_t da = (ka >> shift) & mask, db = (kb >> shift) & mask;
+                const bool gt = da > db || (da == db && ia > ib);
+                if (gt == ((a & k) == 0)) {  // ascending where bit k of a is clear
+                    sk[a] = kb;
+                    sk[b] = ka;
+                    si[a] = ib;
+                    si[b] = ia;
+                }
+            }
+            __syncthreads();
+        }
+    }
+    for (int r = tid; r < m; r += T) {
+        kout[r] = sk[r];
+        if (vout) vout[r] = sv[si[r]];
+    }
+}
+
 }  // namespace
 
 size_t radix_workspace_bytes(int64_t n) {
@@ -102,9 +154,10 @@ size_t radix_workspace_bytes(int64_t n) {
     return (size_t)counts * sizeof(int64_t) + scan_workspace_bytes(counts);
 }
 
-// Sorts n pairs by bits [begin_bit, end_bit) of the key, stably.  Buffers
-// alternate between (k0, v0) and (k1, v1); *in_alt tells where the result
-// is.  v0/v1 may be null (keys only).  `ws` has radix_workspace_bytes(n).
+// Sorts n pairs by bits [begin_bit, end_bit) of the key (in whole 8-bit
+// digits), stably.  Buffers alternate between (k0, v0) and (k1, v1) once per
+// digit; *in_alt tells where the result is (the single-workgroup sort of up
+// to 4,096 pairs writes it there too).  v0/v1 may be null (keys only).  `ws` has radix_workspace_bytes(n).
 // A non-null `skip` word that is nonzero at run time turns every kernel into
 // a no-op (the buffers then stay as they were).  A non-null `n_live` is a
 // device count read at run time: only the first min(n, *n_live) pairs are
@@ -114,6 +167,19 @@ hipError_t radix_sort_pairs(uint64_t* k0, uint32_t* v0, uint64_t* k1, uint32_t* 
                             const uint32_t* skip, const int64_t* n_live) {
     *in_alt = false;
     if (n <= 1 || end_bit <= begin_bit) return hipSuccess;
+    if (n <= kSmallSort) {
+        const int passes = (end_bit - begin_bit + 7) / 8;
+        const int width = min(8 * passes, 64 - begin_bit);  // the bits the passes order by
+        const uint64_t mask = width >= 64 ? ~0ull : ((1ull << width) - 1ull);
+        int P = 2;
+        while (P < n) P <<= 1;
+        const int threads = max(kWave, min(kSmallSortThreads, P / 2));
+        const bool alt = (passes & 1) != 0;
+        hipLaunchKernelGGL(small_sort_kernel, dim3(1), dim3(threads), 0, st, k0, v0,
+                           alt ? k1 : k0, alt ? v1 : v0, n, begin_bit, mask, P, skip, n_live);
+        *in_alt = alt;
+        return hipGetLastError();
+    }
     const int64_t tiles = (n + kRadixTile - 1) / kRadixTile;
     if (tiles > INT32_MAX) return hipErrorInvalidValue;
     int64_t* counts = static_cast<int64_t*>(ws);

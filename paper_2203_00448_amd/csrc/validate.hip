@@ -507,6 +507,139 @@ __global__ __launch_bounds__(kVBlock) void v_long_write_kernel(
     }
 }
 
+// ---- unsorted inputs with more pairs than the capacity
+// The write pass keeps the first `cap` pairs of position order, which for an
+// input not sorted by first are not the lexicographically first ones.  One
+// workgroup then selects those: pair keys (smaller id << nbits | larger id)
+// are unique, so the cap-th smallest key K* is found digit by digit from the
+// top (12 bits at a time, histograms in LDS over the pairs whose key carries
+// the digits chosen so far), and pairs[0, cap) is rewritten with the keys at
+// or below K*; the pair sort that follows orders them.  Only rows with pairs
+// are walked (row q has cnt[q + 1] - cnt[q], and its walk stops at the last).
+
+constexpr int kSelBlock = 1024;
+constexpr int kSelDigit = 12;
+constexpr int kSelBins = 1 << kSelDigit;
+constexpr int kSelUnroll = 4;
+
+// f(key, x, y) for every pair (x < y ids) of every row with pairs; the
+// workgroup's waves take 64 rows at a time.
+template <class F>
+__device__ __forceinline__ void sel_for_each_pair(const VArrays& a, const int32_t* reach,
+                                                  const int64_t* cnt, int64_t n, int nbits, F f) {
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    constexpr int kWaves = kSelBlock / kWave;
+    for (int64_t r0 = (int64_t)wid * kWave; r0 < n; r0 += (int64_t)kWaves * kWave) {
+        const int64_t rq = r0 + lane;
+        uint64_t rows = __ballot(rq < n && cnt[rq + 1] > cnt[rq]);
+        while (rows) {
+            const int64_t q = r0 + (__ffsll((unsigned long long)rows) - 1);
+            rows &= rows - 1;
+            const int64_t need = cnt[q + 1] - cnt[q];
+            const int64_t r = reach[q];
+            const int64_t oq = a.off[q], sq = a.size[q];
+            const uint64_t xq = a.id ? (uint64_t)a.id[q] : (uint64_t)q;
+            int64_t found = 0;
+            for (int64_t j0 = q + 1; j0 < r && found < need; j0 += kWave * kSelUnroll) {
+                int64_t jo[kSelUnroll], js[kSelUnroll];
+#pragma unroll
+                for (int u = 0; u < kSelUnroll; ++u) {
+                    const int64_t j = j0 + u * kWave + lane;
+                    jo[u] = j < r ? a.off[j] : 0;
+                    js[u] = j < r ? a.size[j] : 0;
+                }
+#pragma unroll
+                for (int u = 0; u < kSelUnroll; ++u) {
+                    const int64_t j = j0 + u * kWave + lane;
+                    const bool h = j < r && bytes_meet(oq, sq, jo[u], js[u]);
+                    if (h) {
+                        uint64_t x = xq, y = a.id ? (uint64_t)a.id[j] : (uint64_t)j;
+                        if (x > y) {
+                            const uint64_t t = x;
+                            x = y;
+                            y = t;
+                        }
+                        f((x << nbits) | y, x, y);
+                    }
+                    found += __popcll(__ballot(h));
+                }
+            }
+        }
+    }
+}
+
+__global__ __launch_bounds__(kSelBlock) void v_select_kernel(
+    const int32_t* first, const int32_t* last, const int64_t* off, const int64_t* size,
+    const int32_t* pf, const int32_t* pl, const int64_t* po, const int64_t* ps,
+    const uint32_t* pid, const int32_t* __restrict__ reach, const int64_t* __restrict__ cnt,
+    int64_t n, const VFlags* fl, const int64_t* __restrict__ n_out, int64_t cap, int nbits,
+    int64_t* __restrict__ pairs) {
+    __shared__ unsigned long long hist[kSelBins];
+    __shared__ unsigned long long part[kSelBlock];
+    __shared__ uint64_t s_prefix;
+    __shared__ int64_t s_rank;
+    __shared__ unsigned long long s_slot;
+    if (!fl->unsorted || cap <= 0 || *n_out <= cap) return;
+    const VArrays a = pick_arrays(fl, first, last, off, size, pf, pl, po, ps, pid);
+    const int tid = threadIdx.x;
+    constexpr int kPer = kSelBins / kSelBlock;
+    uint64_t prefix = 0;  // the digits of K* chosen so far
+    int64_t rank = cap;   // K* is the rank-th smallest key with that prefix (from 1)
+    for (int top = 2 * nbits; top > 0;) {
+        const int D = top < kSelDigit ? top : kSelDigit;
+        const int shift = top - D;
+        const uint64_t dmask = ((uint64_t)1 << D) - 1;
+        for (int i = tid; i < kSelBins; i += kSelBlock) hist[i] = 0;
+        __syncthreads();
+        sel_for_each_pair(a, reach, cnt, n, nbits, [&](uint64_t key, uint64_t, uint64_t) {
+            if ((key >> top) == prefix) atomicAdd(&hist[(key >> shift) & dmask], 1ull);
+        });
+        __syncthreads();
+        // exclusive sums of the per-thread bin groups (Hillis-Steele), then the
+        // thread whose bins hold the rank-th key names the digit
+        unsigned long long mine = 0;
+#pragma unroll
+        for (int k = 0; k < kPer; ++k) mine += hist[tid * kPer + k];
+        part[tid] = mine;
+        __syncthreads();
+        for (int d = 1; d < kSelBlock; d <<= 1) {
+            const unsigned long long add = tid >= d ? part[tid - d] : 0ull;
+            __syncthreads();
+            part[tid] += add;
+            __syncthreads();
+        }
+        int64_t before = (int64_t)(part[tid] - mine);
+        if (before < rank && rank <= before + (int64_t)mine) {
+            for (int k = 0; k < kPer; ++k) {
+                const int64_t c = (int64_t)hist[tid * kPer + k];
+                if (rank <= before + c) {
+                    s_prefix = (prefix << D) | (uint64_t)(tid * kPer + k);
+                    s_rank = rank - before;
+                    break;
+                }
+                before += c;
+            }
+        }
+        __syncthreads();
+        prefix = s_prefix;
+        rank = s_rank;
+        top = shift;
+        __syncthreads();  // s_prefix and s_rank are written again next digit
+    }
+    if (tid == 0) s_slot = 0;
+    __syncthreads();
+    const uint64_t kstar = prefix;
+    sel_for_each_pair(a, reach, cnt, n, nbits, [&](uint64_t key, uint64_t x, uint64_t y) {
+        if (key <= kstar) {
+            const unsigned long long at = atomicAdd(&s_slot, 1ull);
+            if ((int64_t)at < cap) {
+                pairs[2 * at] = (int64_t)x;
+                pairs[2 * at + 1] = (int64_t)y;
+            }
+        }
+    });
+}
+
 __global__ void v_total_kernel(const int64_t* __restrict__ partial, int64_t tiles, int64_t cap,
                                int64_t* __restrict__ n_out, int32_t* __restrict__ status,
                                int64_t* __restrict__ cnt_end) {
@@ -1010,8 +1143,15 @@ hipError_t launch_validate(const int64_t* begin, int64_t n_seg, const int64_t* s
                            (const int64_t*)po, (const int64_t*)ps, (const uint32_t*)pid,
                            (const int32_t*)reach, (const int64_t*)cnt, sorted, n,
                            (const VFlags*)fl, pairs, cap);
-        // unsorted inputs: pairs were written in position order; sort them by (i, j)
+        // unsorted inputs: pairs were written in position order; past the
+        // capacity they are replaced by the lexicographically first ones,
+        // then sorted by (i, j)
         if (assume_sorted) return hipGetLastError();
+        hipLaunchKernelGGL(v_select_kernel, dim3(1), dim3(kSelBlock), 0, st, first, last, off, size,
+                           (const int32_t*)pf, (const int32_t*)pl, (const int64_t*)po,
+                           (const int64_t*)ps, (const uint32_t*)pid, (const int32_t*)reach,
+                           (const int64_t*)cnt, n, (const VFlags*)fl, (const int64_t*)n_out, cap,
+                           nbits, pairs);
         const unsigned gc = grid_for(cap, kVBlock, 4096);
         hipLaunchKernelGGL(v_pack_kernel, dim3(gc), dim3(kVBlock), 0, st, (const int64_t*)pairs,
                            (const int64_t*)n_out, cap, nbits, pk0, (const VFlags*)fl);

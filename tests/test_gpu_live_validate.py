@@ -105,6 +105,23 @@ def test_validate_random_sorted_and_unsorted():
         assert np.array_equal(gp, ep), k
 
 
+def test_validate_sort_path_boundaries():
+    """Unsorted plans on both sides of the 4,096-element single-workgroup sort:
+    the position sort (n tensors) and the pair sort (capacity entries)."""
+    binding = need_gpu()
+    rng = np.random.default_rng(203)
+    for n in [4095, 4096, 4097]:
+        t = tg.random_trace(rng, n, n // 8, max_len=4)
+        for spread in (3000, 500):
+            off = 64 * rng.integers(0, spread, n)
+            ep, ec = _oracle_pairs(t, off)
+            print(f"case unsorted validation, {n} tensors ({ec} conflicts)", flush=True)
+            for cap in sorted({min(ec, 4096), ec, 4097}):
+                gp, gc, st = _gpu_pairs(binding, t, off, capacity=cap)
+                want = binding.MP_OK if cap >= ec else binding.MP_ENOSPC
+                assert st == want and gc == ec and np.array_equal(gp, ep[:cap]), (n, cap)
+
+
 def test_validate_long_rows_and_capacity():
     binding = need_gpu()
     rng = np.random.default_rng(202)

@@ -66,6 +66,23 @@ def test_random_traces():
         _check(binding, t)
 
 
+def test_sort_path_boundaries():
+    """Sorts of up to 4,096 pairs take one workgroup's sort in LDS, longer ones
+    digit passes: unsorted traces on both sides of that size, with few sizes
+    (ties keep position order) and with one-byte units (odd sizes of
+    2^28..2^34 bytes, so the rank keys are 64 bits wide)."""
+    binding = need_gpu()
+    rng = np.random.default_rng(302)
+    for n in [4095, 4096, 4097]:
+        print(f"case unsorted, {n} tensors, three sizes", flush=True)
+        _check(binding, tg.random_trace(rng, n, n // 4, max_len=30, sizes=[64, 192, 448]))
+        print(f"case unsorted, {n} tensors, 64-bit unit counts", flush=True)
+        t = tg.random_trace(rng, n, n // 4, max_len=30)
+        t.size[:] = rng.integers(2 ** 28, 2 ** 34, n) | 1
+        t.size[::3] = 2 ** 33 + 1
+        _check(binding, t)
+
+
 def test_adversarial_shapes():
     binding = need_gpu()
     rng = np.random.default_rng(301)
