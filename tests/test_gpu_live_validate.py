@@ -215,6 +215,16 @@ def test_validate_batch_matches_per_trace():
                                             capacity=max(1, expect.shape[0]))
     assert st == binding.MP_OK and cnt == expect.shape[0]
     assert np.array_equal(host(pairs), expect)
+    # past the capacity: the lexicographically first pairs (some traces are
+    # unsorted, so position order differs from id order)
+    for cap in (expect.shape[0] // 3, 1):
+        pairs, cnt, st = binding.validate_batch(dev(batch.begin, torch.int64),
+                                                dev(batch.size, torch.int64),
+                                                dev(batch.first, torch.int32),
+                                                dev(batch.last, torch.int32),
+                                                dev(off, torch.int64), capacity=cap)
+        assert st == binding.MP_ENOSPC and cnt == expect.shape[0], cap
+        assert np.array_equal(host(pairs), expect[:cap]), cap
 
 
 def test_validate_batch_long_rows_across_traces():
