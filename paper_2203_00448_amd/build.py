@@ -15,6 +15,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG, "libmemoplan.so")
 DBG_WAIT_LIB_PATH = os.path.join(PKG, "libmemoplan_dbgwait.so")
+# profiling build: plan_batch_kernel stamps the clock at each phase of every
+# trace (MP_PHASE_TIMING; read by paper_2203_00448_amd.phase_clock).  Built
+# only on request: python -m paper_2203_00448_amd.build --phase-timing
+PHASE_LIB_PATH = os.path.join(PKG, "libmemoplan_phase.so")
 
 HIPCC_FLAGS = [
     "-O3", "-std=c++17", "--offload-arch=gfx950", "-fPIC", "-shared",
@@ -28,10 +32,13 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, phase_timing: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     jobs = []
-    for out, extra in ((LIB_PATH, []), (DBG_WAIT_LIB_PATH, ["-DMP_DEBUG_WAIT"])):
+    variants = [(LIB_PATH, []), (DBG_WAIT_LIB_PATH, ["-DMP_DEBUG_WAIT"])]
+    if phase_timing:
+        variants = [(PHASE_LIB_PATH, ["-DMP_PHASE_TIMING"])]
+    for out, extra in variants:
         cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", INCLUDE, "-I", CSRC, "-o", out + ".tmp",
                *sources()]
         if verbose:
@@ -42,8 +49,8 @@ def build(verbose: bool = False) -> str:
         raise subprocess.CalledProcessError(1, f"hipcc ({', '.join(map(os.path.basename, failed))})")
     for out, _ in jobs:
         os.replace(out + ".tmp", out)
-    return LIB_PATH
+    return PHASE_LIB_PATH if phase_timing else LIB_PATH
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, phase_timing="--phase-timing" in sys.argv[1:]))
